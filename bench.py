@@ -1,0 +1,171 @@
+"""Benchmark: throughput of the structured-derivatives empirical NTK on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME] [--no-cpu-baseline]
+
+A step is one full NTK evaluation Theta(X1, X2) (every stage of the path: forward
+pass keeping layer inputs, batched cotangent backward, Grams, fused contraction)
+on the synthetic workload, with all inputs already resident in HBM.  The default
+workload is the ReLU MLP of depth 8 and width 2048 (input 3072, O = 10,
+X1 and X2 of 512 samples each).  One JSON line is printed on stdout.
+
+roofline: the dominant kernel class (largest time share) is timed live with HIP
+events recorded by the library around each launch on its own stream during the
+timed steps; `achieved` = its algorithmic FLOPs per launch / average launch time.
+cpu_baseline: the fp64 Jacobian-contraction oracle on a bounded sample of the same
+workload (a few samples of X1 x X2, all outputs), timed on this host.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "NTK entries/sec (N1·N2·O²) and fp32 MFMA TFLOP/s, FCN depth 8 width 2048"
+FP32_MFMA_PEAK_TFLOPS = 157.3      # MI355X dense fp32 matrix peak
+HBM_PEAK_GBS = 8000.0
+
+# kernel class -> stage of the FLOP counter
+STAGE_OF = {"dense_fwd": "forward", "dense_bwd": "backward", "gram": "gram",
+            "ntk_fcn": "contraction", "conv_fwd": "forward", "conv_bwd": "backward",
+            "conv_wgrad": "wgrad", "ntk_splitk": "contraction", "conv_pairsum": "contraction"}
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="relu_mlp_d8_w2048")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-samples", type=int, default=2,
+                    help="samples per side of the oracle's bounded sample")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain device copy of known size (for HBM counter scaling)")
+    return ap.parse_args()
+
+
+def cpu_baseline(name, n):
+    import numpy as np
+    import oracle
+    import workloads as wl
+    from threadpoolctl import threadpool_info
+    spec, params, X1, X2 = wl.make_workload(name)
+    t0 = time.perf_counter()
+    th = oracle.ntk_jc(spec, params, X1[:n], X2[:n])
+    dt = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    return {"value": th.size / dt, "unit": "NTK entries/s", "cores": threads, "kind": "oracle",
+            "sample": f"Theta(X1[:{n}], X2[:{n}]) of {name}, all {th.shape[2]} outputs "
+                      f"({th.size} entries) by fp64 Jacobian contraction in {dt:.1f} s; "
+                      f"host {platform.processor() or platform.machine()}, "
+                      f"{os.cpu_count()} logical CPUs"}
+
+
+def copy_calibration():
+    import torch
+    n = 256 << 20  # 1 GiB of float32
+    a = torch.empty(n, dtype=torch.float32, device="cuda").fill_(1.0)
+    b = torch.empty_like(a)
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes_read": n * 4, "copy_calibration_bytes_written": n * 4}))
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the NTK output "
+              "blocks are independent and would shard over a 2-D grid of GPUs, which this "
+              "build does not run.", file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+
+    import workloads as wl
+    from paper_2206_08720_amd import _lib
+    from paper_2206_08720_amd.flops import ntk_entries, ntk_flops
+    from paper_2206_08720_amd.ntk import NTK
+
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    torch.cuda.set_device(0)
+    name = args.workload
+    spec, params, X1, X2 = wl.make_workload(name)
+    sym = X2 is X1
+    dev = [torch.from_numpy(p).cuda() for p in params]
+    x1 = torch.from_numpy(X1).cuda()
+    x2 = x1 if sym else torch.from_numpy(X2).cuda()
+    n1, n2 = X1.shape[0], X2.shape[0]
+    O = spec["layers"][-1]["out"]
+    h = NTK(spec, n1, n2)
+    out = torch.empty((n1, n2, O, O), dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    for _ in range(args.warmup):
+        h.compute(dev, x1, x2, out=out)
+    torch.cuda.synchronize()
+    h.profile_read()                       # drop anything recorded so far
+    h.profile_enable(True)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    ev0.record(stream)
+    for _ in range(args.steps):
+        h.compute(dev, x1, x2, out=out)
+    ev1.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    ms = ev0.elapsed_time(ev1) / args.steps
+    prof = h.profile_read()
+    h.profile_enable(False)
+
+    entries = ntk_entries(spec, n1, n2)
+    fl = ntk_flops(spec, n1, n2, symmetric=sym)
+    value = entries / (ms * 1e-3)
+    tflops = fl["total"] / (ms * 1e-3) / 1e12
+
+    kernels = {}
+    for k, (tot, cnt) in prof.items():
+        per_step = cnt / args.steps
+        kernels[k] = {"ms_per_step": tot / args.steps, "launches_per_step": per_step}
+        st = STAGE_OF.get(k)
+        if st and st in fl and cnt:
+            kernels[k]["tflops"] = fl[st] / (tot / args.steps * 1e-3) / 1e12
+    dom = max(prof, key=lambda k: prof[k][0])
+    tot, cnt = prof[dom]
+    avg_ms = tot / cnt
+    flop_per_launch = fl[STAGE_OF[dom]] / (cnt / args.steps)
+    achieved = flop_per_launch / (avg_ms * 1e-3) / 1e12
+    roofline = {"kernel": dom, "bound": "mfma", "achieved": achieved,
+                "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
+                "frac": achieved / FP32_MFMA_PEAK_TFLOPS, "traffic": None,
+                "flop_per_launch": flop_per_launch, "avg_launch_ms": avg_ms}
+
+    res = {
+        "metric": METRIC, "value": value, "unit": "NTK entries/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic (seeded N(0,1) inputs, He-init weights)",
+        "config": {"workload": name, "n1": n1, "n2": n2, "O": O,
+                   "layers": [[L.get("in"), L.get("out"), L.get("act")] for L in spec["layers"]],
+                   "symmetric_schedule": sym, "parallelism": "single GPU"},
+        "tflops": tflops, "frac_of_fp32_mfma_peak": tflops / FP32_MFMA_PEAK_TFLOPS,
+        "algorithmic_flops": fl, "kernels": kernels, "roofline": roofline,
+        "wall_s_timed_region": wall,
+    }
+    h.close()
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(name, args.cpu_samples)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,160 @@
+/*
+ * ntk.h -- C ABI of the MI355X (gfx950) structured-derivatives empirical NTK library.
+ *
+ * The library computes the finite-width empirical neural tangent kernel
+ *
+ *     Theta(x1, x2) = [df(x1)/dtheta] [df(x2)/dtheta]^T            (O x O per input pair)
+ *
+ * (Section 3.1.1, Eq. ntk_def_main) for fully-connected and 3x3-convolutional
+ * networks, without ever forming the Jacobian.  It follows the "structured
+ * derivatives" method of Section 3.4: for every weight tensor theta^l it
+ * contracts the smallest Jacobian sub-array of dy/dtheta^l (the layer input,
+ * or its 3x3 patches for a convolution) with the primitive-output cotangents
+ * df/dy of both batches, and sums the summands over layers (Eq.
+ * expanded_ntk_main, Eq. mixed_product_example; per-layer formulas of
+ * Section 4.1 for the FCN and the appendix "CNN NTK Complexity" for the CNN).
+ *
+ * All arithmetic runs on the GPU in fp32 with fp32 accumulation (the paper's
+ * experiments use 32-bit precision, appendix "Experimental Details").
+ *
+ * Networks (the descriptor below):
+ *   * FCN: n >= 1 DENSE layers.  Layer l maps d_l -> d_{l+1}:
+ *       z_l = h_l W_l^T (+ b_l),  h_{l+1} = act_l(z_l),  h_0 = x,  f = z_last.
+ *     The last layer must have act NONE (f is the last pre-activation).
+ *   * CNN: k >= 1 CONV3X3_SAME layers (stride 1, zero padding 1,
+ *     cross-correlation, NHWC activations, OHWI weights [Cout,3,3,Cin]), then
+ *     one GAP layer (mean over the H*W pixels), then one DENSE readout layer
+ *     with act NONE and no bias.  Convolution biases are not supported.
+ *
+ * Conventions: act'(0) = 0 for ReLU; erf'(z) = 2/sqrt(pi) exp(-z^2).
+ *
+ * Ownership and streams: the caller owns every pointer it passes (parameters,
+ * inputs, output); the library owns only its workspace, allocated by
+ * ntk_init and released by ntk_free.  Work is enqueued on the handle's HIP
+ * stream and returns before it finishes; the caller synchronises.  A handle
+ * must not be used by two host threads at once, and two calls on the same
+ * handle must be ordered on one stream (they share the workspace).
+ *
+ * Errors: every entry point returns NTK_OK (0) or a negative NTK_E_* code and,
+ * when a handle exists, records a message readable with ntk_last_error.  No
+ * C++ exception crosses this interface.  On NTK_E_ARG / NTK_E_SHAPE /
+ * NTK_E_UNSUPPORTED nothing is enqueued and the output is left untouched.
+ */
+#ifndef NTK_H_
+#define NTK_H_
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- return codes ---------------------------------------------------------------- */
+#define NTK_OK             0
+#define NTK_E_ARG         -1  /* null pointer, n <= 0, n > max, bad option value            */
+#define NTK_E_SHAPE       -2  /* inconsistent model descriptor (dims do not chain, ...)      */
+#define NTK_E_UNSUPPORTED -3  /* layer kind / activation / layer order not supported          */
+#define NTK_E_OOM         -4  /* workspace allocation failed                                  */
+#define NTK_E_HIP         -5  /* a HIP runtime call or kernel launch failed (message has it)  */
+
+/* ---- layer kinds and activations ------------------------------------------------- */
+#define NTK_DENSE          0
+#define NTK_CONV3X3_SAME   1
+#define NTK_GAP            2
+
+#define NTK_ACT_NONE       0
+#define NTK_ACT_RELU       1
+#define NTK_ACT_ERF        2
+
+typedef struct ntk_layer_desc {
+    int kind;      /* NTK_DENSE, NTK_CONV3X3_SAME or NTK_GAP                              */
+    int in;        /* input features / input channels (ignored for GAP)                   */
+    int out;       /* output features / output channels (ignored for GAP)                 */
+    int act;       /* activation applied to this layer's output (NTK_ACT_*; GAP: NONE)    */
+    int has_bias;  /* 1 if the layer has a bias vector of length `out` (DENSE only)       */
+} ntk_layer_desc;
+
+typedef struct ntk_model_desc {
+    int n_layers;                  /* number of entries in `layers`                      */
+    const ntk_layer_desc* layers;  /* copied by ntk_init; need not outlive the call      */
+    int in_h, in_w, in_c;          /* input shape: FCN uses in_h = in_w = 1, in_c = d_0  */
+    int out_dim;                   /* O, the number of network outputs                   */
+} ntk_model_desc;
+
+typedef struct ntk_handle ntk_handle;
+
+/* ---- options (ntk_set_option) ---------------------------------------------------- */
+/* NTK_OPT_SYMMETRIC: 1 (default) = when X2 == X1 and n2 == n1, run the forward and
+ * backward passes once and compute only the upper triangle of output tiles,
+ * mirroring the transposed O x O blocks (Theta(x,x')[o1,o2] = Theta(x',x)[o2,o1]);
+ * 0 = always treat X1 and X2 as two batches.                                          */
+#define NTK_OPT_SYMMETRIC   1
+/* NTK_OPT_CONV_ORDER: contraction order of the convolutional summands (appendix
+ * "No Structure": outside-in vs inside-out; appendix "CNN NTK Complexity").
+ * 0 = auto (pick the cheaper order by the paper's CNN cost model, per layer),
+ * 1 = outside-in (per-sample weight-space Jacobian, then J1 J2^T),
+ * 2 = inside-out (patch-pair Gram times cotangent Gram, summed over pixel pairs).  */
+#define NTK_OPT_CONV_ORDER  2
+#define NTK_CONV_ORDER_AUTO        0
+#define NTK_CONV_ORDER_OUTSIDE_IN  1
+#define NTK_CONV_ORDER_INSIDE_OUT  2
+
+/*
+ * ntk_init -- validate a model descriptor, plan and allocate the workspace.
+ *   model       descriptor (copied).
+ *   max_n1/2    largest batch sizes later passed to ntk_compute (> 0).
+ *   hip_stream  hipStream_t the work is enqueued on; NULL = the default stream.
+ *   out         receives the new handle; set to NULL on any error.
+ * Returns NTK_OK, NTK_E_ARG, NTK_E_SHAPE, NTK_E_UNSUPPORTED, NTK_E_OOM or NTK_E_HIP.
+ * The device is the one current on the calling thread; later calls must keep it current.
+ */
+int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, void* hip_stream,
+             ntk_handle** out);
+
+/*
+ * ntk_compute -- enqueue Theta(X1, X2) on the handle's stream.
+ *   params  host array of device pointers, one per parameter tensor in layer
+ *           order, weight first then bias (if has_bias): dense weight [out, in]
+ *           row-major, dense bias [out], conv weight [Cout, 3, 3, Cin] (OHWI).
+ *   X1      device [n1, in_c] (FCN) or [n1, in_h, in_w, in_c] NHWC (CNN), fp32.
+ *   X2      device, same layout with n2 rows.  X2 == X1 with n2 == n1 selects the
+ *           symmetric schedule (see NTK_OPT_SYMMETRIC).
+ *   theta   device [n1, n2, O, O] fp32 row-major:
+ *           theta[((n1*N2 + n2)*O + o1)*O + o2] = Theta(x1_{n1}, x2_{n2})[o1, o2].
+ *           Every entry is written.  theta must not overlap the inputs.
+ * Stream-ordered and asynchronous.  Deterministic: two calls with the same inputs
+ * give bit-identical theta (no atomics).
+ */
+int ntk_compute(ntk_handle* h, const float* const* params, const float* X1, int n1,
+                const float* X2, int n2, float* theta);
+
+/* ntk_free -- release the workspace and the handle.  NULL is a no-op.  Synchronises
+ * the handle's stream first. */
+int ntk_free(ntk_handle* h);
+
+/* ntk_last_error -- message of the last failed call on `h` ("" if none).  With
+ * h == NULL, the message of the last failed ntk_init on this thread. */
+const char* ntk_last_error(const ntk_handle* h);
+
+/* ntk_set_option -- set NTK_OPT_* (see above).  NTK_E_ARG for an unknown option/value. */
+int ntk_set_option(ntk_handle* h, int option, int value);
+
+/* ntk_set_stream -- change the stream later work is enqueued on (NULL = default). */
+int ntk_set_stream(ntk_handle* h, void* hip_stream);
+
+/* ntk_workspace_bytes -- bytes of device workspace the handle holds. */
+long long ntk_workspace_bytes(const ntk_handle* h);
+
+/* ---- per-kernel timing ------------------------------------------------------------
+ * When enabled, every kernel launch of ntk_compute is bracketed by HIP events on the
+ * handle's stream and the elapsed times are accumulated per kernel class.
+ * ntk_profile_read synchronises the stream, writes up to `max` entries (class name,
+ * total milliseconds, number of launches) and resets the accumulators.  It returns the
+ * number of classes written (>= 0) or a negative error code.  Names stay valid for the
+ * life of the handle. */
+int ntk_profile_enable(ntk_handle* h, int enable);
+int ntk_profile_read(ntk_handle* h, const char** names, double* total_ms,
+                     long long* launches, int max);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* NTK_H_ */

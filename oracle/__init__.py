@@ -26,7 +26,7 @@ differences, closed forms, hand-worked examples (`tests/golden/`), symmetry,
 positive semi-definiteness and homogeneity.
 """
 from .ntk_jc import forward, jacobian, ntk_jc, ntk_jc_with_norms, param_count
-from .structured_fp64 import ntk_structured_fp64
+from .structured_fp64 import ntk_structured_diag_fp64, ntk_structured_fp64
 
 __all__ = ["forward", "jacobian", "ntk_jc", "ntk_jc_with_norms", "param_count",
-           "ntk_structured_fp64"]
+           "ntk_structured_fp64", "ntk_structured_diag_fp64"]

@@ -13,6 +13,16 @@ Every step follows the paper's definitions:
 * The contraction of the two Jacobians is the "Jacobian contraction" baseline
   of Section 3.2: N1 N2 O^2 P multiply-adds.
 
+Layer storage: with layer_storage="fp64" (default) every intermediate value is
+float64, the plain definition.  With layer_storage="fp32" each layer's output
+h_{l+1} = act(z_l) is rounded to float32 before it feeds the next layer, as in
+a network evaluated in the paper's 32-bit precision (appendix "Experimental
+Details"); pre-activations are still accumulated in float64.  ReLU is
+discontinuous in its derivative, so whether act'(z) is 0 or 1 for a
+pre-activation within rounding distance of 0 depends on the exact stored
+inputs; this mode makes that decision a function of float32-stored layer
+inputs, the values the GPU library decides on.
+
 Conventions (the paper leaves them to the framework): ReLU'(0) = 0;
 erf'(z) = 2/sqrt(pi) exp(-z^2); convolutions are SAME (zero pad 1), stride 1,
 cross-correlation, NHWC activations, OHWI weights; "gap" is the mean over the
@@ -106,7 +116,15 @@ def param_count(spec):
 
 
 # ----------------------------------------------------------------------------- forward pass
-def _forward_record(spec, params, X):
+def _store(h, layer_storage):
+    if layer_storage == "fp64":
+        return h
+    if layer_storage == "fp32":
+        return h.astype(np.float32).astype(np.float64)
+    raise ValueError(f"unknown layer_storage {layer_storage!r}")
+
+
+def _forward_record(spec, params, X, layer_storage="fp64"):
     """Run f on a batch, keeping each layer's input h and pre-activation z."""
     layers = spec["layers"]
     wb = _split_params(spec, params)
@@ -119,7 +137,7 @@ def _forward_record(spec, params, X):
             if b is not None:
                 z = z + b
             rec.append({"h": h, "z": z})
-            h = _phi(L["act"], z)
+            h = _store(_phi(L["act"], z), layer_storage)
         elif L["kind"] == "conv3x3":
             w, b = p
             N, H, W, C = h.shape
@@ -129,18 +147,18 @@ def _forward_record(spec, params, X):
                 z = z + b
             z = z.reshape(N, H, W, w.shape[0])
             rec.append({"h": h, "z": z, "patches": pt})
-            h = _phi(L["act"], z)
+            h = _store(_phi(L["act"], z), layer_storage)
         elif L["kind"] == "gap":
             rec.append({"h": h})
-            h = h.mean(axis=(1, 2))
+            h = _store(h.mean(axis=(1, 2)), layer_storage)
         else:
             raise ValueError(f"unknown layer kind {L['kind']!r}")
     return rec, h
 
 
-def forward(spec, params, X):
+def forward(spec, params, X, layer_storage="fp64"):
     """f(theta, X) in float64: [N, O]."""
-    return _forward_record(spec, params, X)[1]
+    return _forward_record(spec, params, X, layer_storage)[1]
 
 
 # ----------------------------------------------------------------------------- reverse-mode Jacobian
@@ -182,7 +200,8 @@ def _output_cotangents(spec, params, rec, outputs):
     return G
 
 
-def jacobian_blocks(spec, params, X, outputs=None, max_block_bytes=256 << 20, chunk_rows=None):
+def jacobian_blocks(spec, params, X, outputs=None, max_block_bytes=256 << 20, chunk_rows=None,
+                    layer_storage="fp64"):
     """Yield the weight-space Jacobian, block by block: arrays [N*Os, p] (float64).
 
     Concatenating every yielded block along the last axis gives df/dtheta in the
@@ -195,7 +214,7 @@ def jacobian_blocks(spec, params, X, outputs=None, max_block_bytes=256 << 20, ch
     layers = spec["layers"]
     O = layers[-1]["out"]
     outputs = list(range(O)) if outputs is None else list(outputs)
-    rec, _ = _forward_record(spec, params, X)
+    rec, _ = _forward_record(spec, params, X, layer_storage)
     G = _output_cotangents(spec, params, rec, outputs)
     N = np.asarray(X).shape[0]
     R = N * len(outputs)
@@ -229,17 +248,18 @@ def jacobian_blocks(spec, params, X, outputs=None, max_block_bytes=256 << 20, ch
                 yield gf.sum(axis=2).reshape(R, cout)
 
 
-def jacobian(spec, params, X, outputs=None):
+def jacobian(spec, params, X, outputs=None, layer_storage="fp64"):
     """Full per-sample Jacobian df/dtheta: [N, Os, P] float64 (tiny nets only)."""
     N = np.asarray(X).shape[0]
     O = spec["layers"][-1]["out"]
     Os = O if outputs is None else len(list(outputs))
-    blocks = list(jacobian_blocks(spec, params, X, outputs, max_block_bytes=1 << 62))
+    blocks = list(jacobian_blocks(spec, params, X, outputs, max_block_bytes=1 << 62,
+                                  layer_storage=layer_storage))
     return np.concatenate(blocks, axis=1).reshape(N, Os, -1)
 
 
 def ntk_jc_with_norms(spec, params, X1, X2, outputs1=None, outputs2=None,
-                      max_block_bytes=256 << 20):
+                      max_block_bytes=256 << 20, layer_storage="fp64"):
     """Theta [N1, N2, Os1, Os2] plus squared Jacobian row norms [N1, Os1], [N2, Os2].
 
     The row norms give Theta(x1, x1)[o, o] and Theta(x2, x2)[o, o], the natural
@@ -255,8 +275,8 @@ def ntk_jc_with_norms(spec, params, X1, X2, outputs1=None, outputs2=None,
     sq1 = np.zeros(N1 * len(o1))
     sq2 = np.zeros(N2 * len(o2))
     rows = max(N1 * len(o1), N2 * len(o2))
-    it1 = jacobian_blocks(spec, params, X1, o1, max_block_bytes, rows)
-    it2 = jacobian_blocks(spec, params, X2, o2, max_block_bytes, rows)
+    it1 = jacobian_blocks(spec, params, X1, o1, max_block_bytes, rows, layer_storage)
+    it2 = jacobian_blocks(spec, params, X2, o2, max_block_bytes, rows, layer_storage)
     for J1, J2 in zip(it1, it2):
         theta += J1 @ J2.T
         sq1 += np.einsum("rp,rp->r", J1, J1)
@@ -265,6 +285,8 @@ def ntk_jc_with_norms(spec, params, X1, X2, outputs1=None, outputs2=None,
     return np.ascontiguousarray(theta), sq1.reshape(N1, len(o1)), sq2.reshape(N2, len(o2))
 
 
-def ntk_jc(spec, params, X1, X2, outputs1=None, outputs2=None, max_block_bytes=256 << 20):
+def ntk_jc(spec, params, X1, X2, outputs1=None, outputs2=None, max_block_bytes=256 << 20,
+           layer_storage="fp64"):
     """Theta(X1, X2) as [N1, N2, Os1, Os2] float64 by Jacobian contraction."""
-    return ntk_jc_with_norms(spec, params, X1, X2, outputs1, outputs2, max_block_bytes)[0]
+    return ntk_jc_with_norms(spec, params, X1, X2, outputs1, outputs2, max_block_bytes,
+                             layer_storage)[0]

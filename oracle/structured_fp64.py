@@ -18,7 +18,7 @@ import math
 import numpy as np
 from scipy.special import erf as _erf
 
-__all__ = ["ntk_structured_fp64"]
+__all__ = ["ntk_structured_fp64", "ntk_structured_diag_fp64"]
 
 
 def _phi(act, z):
@@ -32,7 +32,7 @@ def _dphi(act, z):
             "none": lambda: np.ones_like(z)}[act]()
 
 
-def _layer_inputs_and_cotangents(spec, params, X):
+def _layer_inputs_and_cotangents(spec, params, X, layer_storage="fp64"):
     layers = spec["layers"]
     if any(L["kind"] != "dense" for L in layers):
         raise ValueError("ntk_structured_fp64 handles fully-connected nets only")
@@ -53,6 +53,10 @@ def _layer_inputs_and_cotangents(spec, params, X):
         z = h @ w.T + (0.0 if b is None else b)
         zs.append(z)
         h = _phi(L["act"], z)
+        if layer_storage == "fp32":          # layer outputs stored in float32
+            h = h.astype(np.float32).astype(np.float64)
+        elif layer_storage != "fp64":
+            raise ValueError(layer_storage)
     nl = len(layers)
     # cotangent of z_l for every output o: G_l [N, O, out_l]; G_{last} = I_O
     N = hs[0].shape[0]
@@ -66,14 +70,17 @@ def _layer_inputs_and_cotangents(spec, params, X):
     return hs, Gs
 
 
-def ntk_structured_fp64(spec, params, X1, X2):
-    """Theta [N1, N2, O, O] float64 for a fully-connected spec."""
+def ntk_structured_fp64(spec, params, X1, X2, layer_storage="fp64"):
+    """Theta [N1, N2, O, O] float64 for a fully-connected spec.
+
+    layer_storage has the meaning of `ntk_jc`'s argument of that name.
+    """
     layers = spec["layers"]
-    h1, G1 = _layer_inputs_and_cotangents(spec, params, X1)
+    h1, G1 = _layer_inputs_and_cotangents(spec, params, X1, layer_storage)
     if X2 is X1:
         h2, G2 = h1, G1
     else:
-        h2, G2 = _layer_inputs_and_cotangents(spec, params, X2)
+        h2, G2 = _layer_inputs_and_cotangents(spec, params, X2, layer_storage)
     N1, N2 = h1[0].shape[0], h2[0].shape[0]
     O = layers[-1]["out"]
     theta = np.zeros((N1, N2, O, O))
@@ -85,5 +92,26 @@ def ntk_structured_fp64(spec, params, X1, X2):
             a = G1[l].reshape(N1 * O, -1)
             b = G2[l].reshape(N2 * O, -1)
             cot = (a @ b.T).reshape(N1, O, N2, O).transpose(0, 2, 1, 3)
-            theta += gram[:, :, None, None] * cot
+            cot *= gram[:, :, None, None]
+            theta += cot
     return theta
+
+
+def ntk_structured_diag_fp64(spec, params, X, layer_storage="fp64"):
+    """Theta(x, x)[o, o] for every sample and output: [N, O] float64 (fully-connected spec).
+
+    The same per-layer formula restricted to n1 = n2, o1 = o2:
+    sum over hidden layers of (|h_l|^2 [+1]) |G_l[n, o, :]|^2, plus |h_L|^2 [+1].
+    """
+    layers = spec["layers"]
+    hs, Gs = _layer_inputs_and_cotangents(spec, params, X, layer_storage)
+    N = hs[0].shape[0]
+    O = layers[-1]["out"]
+    d = np.zeros((N, O))
+    for l, L in enumerate(layers):
+        sq = np.einsum("nj,nj->n", hs[l], hs[l]) + (1.0 if L["bias"] else 0.0)
+        if l == len(layers) - 1:
+            d += sq[:, None]
+        else:
+            d += sq[:, None] * np.einsum("noc,noc->no", Gs[l], Gs[l])
+    return d

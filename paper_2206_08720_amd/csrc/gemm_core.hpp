@@ -1,0 +1,306 @@
+// gemm_core.hpp -- fp32 MFMA building blocks for gfx950 (CDNA4).
+//
+// Every contraction of the structured-derivatives NTK is a dense fp32 product
+// C[M,N] = sum_k A[m,k] B[n,k] with operands that are either K-contiguous in
+// memory ("K-inner": a row of K values is contiguous) or row-contiguous
+// ("K-outer": for a fixed k the rows are contiguous).  The blocks below stage
+// BM x BK and BN x BK tiles through LDS (double buffered, one barrier per K
+// tile) and run v_mfma_f32_32x32x2_f32 on 32x32 fragments held by each wave.
+//
+// MFMA 32x32x2 f32 operand layout (lane l of a 64-wide wave):
+//   A: lane l supplies A[i = l % 32][k = l / 32]
+//   B: lane l supplies B[k = l / 32][j = l % 32]
+//   D: lane l, register v holds D[i = 8*(v/4) + 4*(l/32) + (v%4)][j = l % 32]
+// A K-step of 8 is split as k = kk + 4*(l/32) + t for the t-th of four MFMAs, so
+// each lane fetches 4 consecutive k of its row with one 16-byte LDS read when the
+// LDS tile is K-inner.  The summation over k is order free, and A and B use the
+// same k assignment, so the product is the plain sum over the 8 k values.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ntk {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+
+// ------------------------------------------------------------------------------ tile config
+template <int BM_, int BN_, int BK_, int WM_, int WN_>
+struct TileCfg {
+  static constexpr int BM = BM_, BN = BN_, BK = BK_, WM = WM_, WN = WN_;
+  static constexpr int WAVES_M = BM / WM, WAVES_N = BN / WN;
+  static constexpr int WAVES = WAVES_M * WAVES_N;
+  static constexpr int THREADS = WAVES * 64;
+  static constexpr int FM = WM / 32, FN = WN / 32;      // 32x32 fp32 fragments per wave
+  static constexpr int FM16 = WM / 16, FN16 = WN / 16;  // 16x16 fp64 fragments per wave
+  static_assert(BM % WM == 0 && BN % WN == 0, "wave tiling");
+  static_assert(WM % 16 == 0 && WN % 16 == 0, "MFMA fragments");
+  static_assert(BK % 16 == 0, "K tile is a multiple of 16");
+};
+
+// LDS tile geometry.  K-inner: [ROWS][BK + 4] (16-byte reads of 4 k per lane hit 16
+// distinct bank groups for 16 consecutive rows).  K-outer: [BK][ROWS + 8] (lanes 0-31
+// and 32-63 read rows k and k+4, 4*(ROWS+8) = 32 mod 64 banks apart).
+template <int ROWS, int BK, bool K_INNER>
+struct LdsGeom {
+  static constexpr int LD = K_INNER ? (BK + 4) : (ROWS + 8);
+  static constexpr int FLOATS = K_INNER ? ROWS * LD : BK * LD;
+};
+
+// ------------------------------------------------------------------------------ global -> regs -> LDS
+// A loader provides
+//   static constexpr bool K_INNER;
+//   __device__ f32x4 load4(int row, int k) const;
+// returning elements (row, k..k+3) if K_INNER, else (row..row+3, k), zero outside bounds.
+template <class Loader, int ROWS, int BK, int THREADS>
+struct TileIO {
+  static constexpr bool KI = Loader::K_INNER;
+  static constexpr int NV = ROWS * BK / (4 * THREADS);
+  static_assert(ROWS * BK % (4 * THREADS) == 0, "tile must split evenly into float4 per thread");
+  using G = LdsGeom<ROWS, BK, KI>;
+  f32x4 r[NV];
+
+  __device__ __forceinline__ void load(const Loader& ld, int row0, int k0, int tid) {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int q = tid + i * THREADS;
+      if (KI) {
+        const int row = q / (BK / 4), kq = (q % (BK / 4)) * 4;
+        r[i] = ld.load4(row0 + row, k0 + kq);
+      } else {
+        const int k = q / (ROWS / 4), rq = (q % (ROWS / 4)) * 4;
+        r[i] = ld.load4(row0 + rq, k0 + k);
+      }
+    }
+  }
+  __device__ __forceinline__ void store(float* lds, int tid) const {
+#pragma unroll
+    for (int i = 0; i < NV; ++i) {
+      const int q = tid + i * THREADS;
+      if (KI) {
+        const int row = q / (BK / 4), kq = (q % (BK / 4)) * 4;
+        *reinterpret_cast<f32x4*>(&lds[row * G::LD + kq]) = r[i];
+      } else {
+        const int k = q / (ROWS / 4), rq = (q % (ROWS / 4)) * 4;
+        *reinterpret_cast<f32x4*>(&lds[k * G::LD + rq]) = r[i];
+      }
+    }
+  }
+};
+
+// 4 consecutive k of one row from an LDS tile.
+template <bool KI, int LD>
+__device__ __forceinline__ f32x4 frag_read(const float* lds, int row, int k) {
+  if (KI) {
+    return *reinterpret_cast<const f32x4*>(&lds[row * LD + k]);
+  } else {
+    f32x4 v;
+    v[0] = lds[(k + 0) * LD + row];
+    v[1] = lds[(k + 1) * LD + row];
+    v[2] = lds[(k + 2) * LD + row];
+    v[3] = lds[(k + 3) * LD + row];
+    return v;
+  }
+}
+
+// One LDS stage: acc[fm][fn] += A_tile(wave rows) * B_tile(wave cols)^T over BK.
+template <class Cfg, bool AKI, bool BKI>
+__device__ __forceinline__ void mma_stage(const float* As, const float* Bs,
+                                          f32x16 (&acc)[Cfg::FM][Cfg::FN], int wm0, int wn0,
+                                          int lane) {
+  using GA = LdsGeom<Cfg::BM, Cfg::BK, AKI>;
+  using GB = LdsGeom<Cfg::BN, Cfg::BK, BKI>;
+  const int lr = lane & 31, lk = (lane >> 5) * 4;
+#pragma unroll
+  for (int kk = 0; kk < Cfg::BK; kk += 8) {
+    f32x4 a[Cfg::FM], b[Cfg::FN];
+#pragma unroll
+    for (int fm = 0; fm < Cfg::FM; ++fm) a[fm] = frag_read<AKI, GA::LD>(As, wm0 + fm * 32 + lr, kk + lk);
+#pragma unroll
+    for (int fn = 0; fn < Cfg::FN; ++fn) b[fn] = frag_read<BKI, GB::LD>(Bs, wn0 + fn * 32 + lr, kk + lk);
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int fm = 0; fm < Cfg::FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < Cfg::FN; ++fn)
+          acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[fm][t], b[fn][t], acc[fm][fn], 0, 0, 0);
+  }
+}
+
+template <class Cfg>
+__device__ __forceinline__ void zero_acc(f32x16 (&acc)[Cfg::FM][Cfg::FN]) {
+#pragma unroll
+  for (int fm = 0; fm < Cfg::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < Cfg::FN; ++fn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[fm][fn][v] = 0.0f;
+}
+
+// fp64-accumulated variant for the forward pass: the fp32 LDS fragments are widened
+// exactly to fp64 and multiplied with v_mfma_f64_16x16x4_f64, so a pre-activation is
+// the fp64 sum of exact products of fp32 inputs (its sign, the ReLU decision, is then
+// a deterministic function of the fp32 data).
+// MFMA 16x16x4 f64 layout: A: lane l supplies A[i = l % 16][k = l / 16];
+//   B: B[k = l / 16][j = l % 16];  D: lane l, element v holds D[4*v + l/16][l % 16]
+//   (unlike the fp32 16x16x4 form, the four outputs of a lane are 4 rows apart).
+// K step of 16 split as k = kk + 4*(l/16) + t for the t-th of four MFMAs.
+template <class Cfg, bool AKI, bool BKI>
+__device__ __forceinline__ void mma_stage(const float* As, const float* Bs,
+                                          f64x4 (&acc)[Cfg::FM16][Cfg::FN16], int wm0, int wn0,
+                                          int lane) {
+  using GA = LdsGeom<Cfg::BM, Cfg::BK, AKI>;
+  using GB = LdsGeom<Cfg::BN, Cfg::BK, BKI>;
+  const int lr = lane & 15, lk = (lane >> 4) * 4;
+#pragma unroll
+  for (int kk = 0; kk < Cfg::BK; kk += 16) {
+    f32x4 a[Cfg::FM16], b[Cfg::FN16];
+#pragma unroll
+    for (int fm = 0; fm < Cfg::FM16; ++fm) a[fm] = frag_read<AKI, GA::LD>(As, wm0 + fm * 16 + lr, kk + lk);
+#pragma unroll
+    for (int fn = 0; fn < Cfg::FN16; ++fn) b[fn] = frag_read<BKI, GB::LD>(Bs, wn0 + fn * 16 + lr, kk + lk);
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int fm = 0; fm < Cfg::FM16; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < Cfg::FN16; ++fn)
+          acc[fm][fn] = __builtin_amdgcn_mfma_f64_16x16x4f64((double)a[fm][t], (double)b[fn][t],
+                                                             acc[fm][fn], 0, 0, 0);
+  }
+}
+
+template <class Cfg>
+__device__ __forceinline__ void zero_acc(f64x4 (&acc)[Cfg::FM16][Cfg::FN16]) {
+#pragma unroll
+  for (int fm = 0; fm < Cfg::FM16; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < Cfg::FN16; ++fn)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) acc[fm][fn][v] = 0.0;
+}
+
+template <class Cfg, class F>
+__device__ __forceinline__ void for_each_acc(f64x4 (&acc)[Cfg::FM16][Cfg::FN16], int m0, int n0, F&& f) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
+  const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
+#pragma unroll
+  for (int fm = 0; fm < Cfg::FM16; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < Cfg::FN16; ++fn)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int row = m0 + wm0 + fm * 16 + 4 * v + (lane >> 4);
+        const int col = n0 + wn0 + fn * 16 + (lane & 15);
+        f(row, col, acc[fm][fn][v]);
+      }
+}
+
+// Full K loop over [k_begin, k_end) for the tile (m0, n0): double-buffered LDS, one
+// barrier per K tile.  `smem` holds 2 * (A tile + B tile) floats.  Ends with a barrier,
+// so the caller may reuse `smem` afterwards.  AccT selects the MFMA flavour (fp32
+// 32x32x2 fragments or fp64 16x16x4 fragments).
+template <class Cfg, class LA, class LB, class AccT>
+__device__ __forceinline__ void gemm_mainloop(const LA& la, const LB& lb, int m0, int n0, int k_begin,
+                                              int k_end, float* smem, AccT& acc) {
+  using GA = LdsGeom<Cfg::BM, Cfg::BK, LA::K_INNER>;
+  using GB = LdsGeom<Cfg::BN, Cfg::BK, LB::K_INNER>;
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
+  const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
+  float* As[2] = {smem, smem + GA::FLOATS + GB::FLOATS};
+  float* Bs[2] = {smem + GA::FLOATS, smem + 2 * GA::FLOATS + GB::FLOATS};
+
+  const int nk = (k_end - k_begin + Cfg::BK - 1) / Cfg::BK;
+  if (nk <= 0) return;
+  TileIO<LA, Cfg::BM, Cfg::BK, Cfg::THREADS> ia;
+  TileIO<LB, Cfg::BN, Cfg::BK, Cfg::THREADS> ib;
+  ia.load(la, m0, k_begin, tid);
+  ib.load(lb, n0, k_begin, tid);
+  ia.store(As[0], tid);
+  ib.store(Bs[0], tid);
+  __syncthreads();
+  for (int kt = 0; kt < nk; ++kt) {
+    const int cur = kt & 1;
+    const bool more = kt + 1 < nk;
+    if (more) {
+      ia.load(la, m0, k_begin + (kt + 1) * Cfg::BK, tid);
+      ib.load(lb, n0, k_begin + (kt + 1) * Cfg::BK, tid);
+    }
+    mma_stage<Cfg, LA::K_INNER, LB::K_INNER>(As[cur], Bs[cur], acc, wm0, wn0, lane);
+    if (more) {
+      ia.store(As[cur ^ 1], tid);
+      ib.store(Bs[cur ^ 1], tid);
+    }
+    __syncthreads();
+  }
+}
+
+template <class Cfg, class LA, class LB>
+constexpr int gemm_smem_bytes() {
+  return 2 * (LdsGeom<Cfg::BM, Cfg::BK, LA::K_INNER>::FLOATS +
+              LdsGeom<Cfg::BN, Cfg::BK, LB::K_INNER>::FLOATS) * 4;
+}
+
+// Visit every accumulator element of the wave with its global (row, col).
+template <class Cfg, class F>
+__device__ __forceinline__ void for_each_acc(f32x16 (&acc)[Cfg::FM][Cfg::FN], int m0, int n0, F&& f) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
+  const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
+#pragma unroll
+  for (int fm = 0; fm < Cfg::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < Cfg::FN; ++fn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = m0 + wm0 + fm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        const int col = n0 + wn0 + fn * 32 + (lane & 31);
+        f(row, col, acc[fm][fn][v]);
+      }
+}
+
+// ------------------------------------------------------------------------------ loaders
+// Row-major [rows, K] operand with row stride `ld` (floats), K contiguous.
+struct LoadKInner {
+  static constexpr bool K_INNER = true;
+  const float* p;
+  int rows, K;
+  long long ld;
+  bool vec;  // p 16-byte aligned and ld % 4 == 0: whole float4 loads allowed
+  __device__ __forceinline__ f32x4 load4(int row, int k) const {
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    if (row < rows) {
+      const float* q = p + (long long)row * ld + k;
+      if (vec && k + 3 < K) {
+        v = *reinterpret_cast<const f32x4*>(q);
+      } else {
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          if (k + j < K) v[j] = q[j];
+      }
+    }
+    return v;
+  }
+};
+
+// ------------------------------------------------------------------------------ misc
+__device__ __forceinline__ float act_fwd(int act, float z) {
+  if (act == 1) return z > 0.f ? z : 0.f;
+  if (act == 2) return erff(z);
+  return z;
+}
+// derivative of the activation at z: ReLU'(0) = 0, erf'(z) = 2/sqrt(pi) exp(-z^2)
+__device__ __forceinline__ float act_deriv(int act, float z) {
+  if (act == 1) return z > 0.f ? 1.f : 0.f;
+  if (act == 2) return 1.1283791670955126f * expf(-z * z);
+  return 1.f;
+}
+
+}  // namespace ntk

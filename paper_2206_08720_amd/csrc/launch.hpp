@@ -1,0 +1,72 @@
+// launch.hpp -- host-side launchers of the NTK kernels (internal to the library).
+#pragma once
+#include <hip/hip_runtime.h>
+
+namespace ntk {
+
+constexpr int kMaxLayers = 64;  // parametrised layers a model may have
+
+// Timing hook: every launcher brackets its kernel(s) with prof_begin/prof_end.
+struct Profiler;
+void prof_begin(Profiler* p, hipStream_t s, int cls);
+void prof_end(Profiler* p, hipStream_t s, int cls);
+
+enum KernelClass {
+  KC_DENSE_FWD = 0,
+  KC_DENSE_BWD,
+  KC_BWD_SEED,
+  KC_GRAM,
+  KC_NTK_FCN,
+  KC_TRANSPOSE,
+  KC_CONV_FWD,
+  KC_CONV_BWD,
+  KC_CONV_SEED,
+  KC_GAP,
+  KC_CONV_WGRAD,
+  KC_NTK_SPLITK,
+  KC_NTK_REDUCE,
+  KC_CONV_PAIRSUM,
+  KC_COPY,
+  KC_COUNT
+};
+const char* kernel_class_name(int cls);
+
+// ---- fully-connected path ------------------------------------------------------------
+// z = h W^T (+ b);  hn = act(z);  dphi = act'(z).  h [M, K], W [N, K], hn/dphi [M, N].
+hipError_t launch_dense_fwd(hipStream_t s, const float* h, const float* W, const float* b, int M,
+                            int N, int K, int act, float* hn, float* dphi);
+// out[r, c] = (sum_k G[r, k] Wt[c, k]) * dphi[(r / O), c].  G [R, K], Wt [N, K], dphi [R/O, N].
+hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, const float* dphi,
+                            int R, int N, int K, int O, float* out);
+// G[m, o, c] = W[o, c] * dphi[m, c]   (cotangent of the last hidden pre-activation).
+hipError_t launch_bwd_seed(hipStream_t s, const float* W, const float* dphi, int M, int O, int C,
+                           float* G);
+// Wt [C, R] = W^T for W [R, C].
+hipError_t launch_transpose(hipStream_t s, const float* W, int R, int C, float* Wt);
+
+struct GramBatch {
+  const float* h1[kMaxLayers + 1];
+  const float* h2[kMaxLayers + 1];
+  float* out[kMaxLayers + 1];
+  int K[kMaxLayers + 1];
+  float beta[kMaxLayers + 1];
+  int count;
+};
+// out_l[n1, n2] = h1_l[n1] . h2_l[n2] + beta_l for every l (rows of h have stride K_l).
+hipError_t launch_gram(hipStream_t s, const GramBatch& g, int N1, int N2);
+
+struct FcnContraction {
+  const float* G1[kMaxLayers];    // cotangents of batch 1, [N1*O, K_l]
+  const float* G2[kMaxLayers];    // cotangents of batch 2, [N2*O, K_l]
+  const float* gram[kMaxLayers];  // [N1, N2] input Gram (+ bias term) of layer l
+  int K[kMaxLayers];
+  int L;                          // number of hidden layers (summands with a cotangent Gram)
+  const float* gram_readout;      // [N1, N2], multiplies delta_{o1 o2}
+};
+// theta[n1, n2, o1, o2] = sum_l gram_l[n1,n2] (G1_l G2_l^T)[(n1,o1),(n2,o2)]
+//                         + gram_readout[n1,n2] delta_{o1 o2}.
+// symmetric != 0: batch 2 is batch 1; only upper-triangle tiles run and mirror.
+hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2, int O,
+                          int symmetric, float* theta);
+
+}  // namespace ntk

@@ -1,0 +1,432 @@
+// ntk_api.hip -- the C ABI declared in include/ntk.h: validation, workspace planning and
+// the stream-ordered schedule of kernels for one NTK evaluation.
+//
+// Schedule (structured derivatives, Section 3.4; FCN per-layer formula of Section 4.1):
+//   1. forward pass over the stacked batch [X1; X2] keeping h_l and act'(z_l)
+//   2. the O one-hot output cotangents pulled back through every layer at once
+//      (the reverse-mode Jacobian of Section 3.1.3 without the weight-space cotangents)
+//   3. the layer-input Grams, and 4. the fused per-tile contraction summed over layers.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/ntk.h"
+#include "launch.hpp"
+
+namespace ntk {
+
+const char* kernel_class_name(int cls) {
+  static const char* names[KC_COUNT] = {
+      "dense_fwd", "dense_bwd", "bwd_seed",  "gram",       "ntk_fcn",    "transpose",    "conv_fwd",
+      "conv_bwd",  "conv_seed", "gap",       "conv_wgrad", "ntk_splitk", "ntk_reduce", "conv_pairsum",
+      "copy"};
+  return (cls >= 0 && cls < KC_COUNT) ? names[cls] : "?";
+}
+
+struct Profiler {
+  bool enabled = false;
+  struct Pending {
+    int cls;
+    hipEvent_t a, b;
+  };
+  std::vector<Pending> pending;
+  std::vector<hipEvent_t> pool;
+  double total_ms[KC_COUNT] = {};
+  long long launches[KC_COUNT] = {};
+  hipEvent_t open_ev = nullptr;
+  int open_cls = -1;
+
+  hipEvent_t get() {
+    if (!pool.empty()) {
+      hipEvent_t e = pool.back();
+      pool.pop_back();
+      return e;
+    }
+    hipEvent_t e = nullptr;
+    if (hipEventCreate(&e) != hipSuccess) return nullptr;
+    return e;
+  }
+  ~Profiler() {
+    for (auto& p : pending) {
+      (void)hipEventDestroy(p.a);
+      (void)hipEventDestroy(p.b);
+    }
+    for (auto e : pool) (void)hipEventDestroy(e);
+  }
+};
+
+void prof_begin(Profiler* p, hipStream_t s, int cls) {
+  if (!p || !p->enabled) return;
+  p->open_ev = p->get();
+  p->open_cls = cls;
+  if (p->open_ev) (void)hipEventRecord(p->open_ev, s);
+}
+void prof_end(Profiler* p, hipStream_t s, int cls) {
+  if (!p || !p->enabled || !p->open_ev || p->open_cls != cls) return;
+  hipEvent_t b = p->get();
+  if (!b) return;
+  (void)hipEventRecord(b, s);
+  p->pending.push_back({cls, p->open_ev, b});
+  p->open_ev = nullptr;
+  p->open_cls = -1;
+}
+
+}  // namespace ntk
+
+using namespace ntk;
+
+struct ntk_handle {
+  std::vector<ntk_layer_desc> layers;
+  int in_h = 1, in_w = 1, in_c = 0, out_dim = 0;
+  bool cnn = false;
+  int max_n1 = 0, max_n2 = 0;
+  hipStream_t stream = nullptr;
+  int device = 0;
+  char* ws = nullptr;
+  size_t ws_bytes = 0;
+  int opt_symmetric = 1;
+  int opt_conv_order = NTK_CONV_ORDER_AUTO;
+  std::string err;
+  Profiler prof;
+
+  // ---- fully-connected plan: dense layers 0..L (L = number of hidden layers)
+  int L = 0;
+  std::vector<int> dims;          // d_0 .. d_{L+1}
+  std::vector<size_t> off_h;      // h_l,    l = 0..L      [Mmax, d_l]
+  std::vector<size_t> off_dphi;   // dphi_l, l = 0..L-1    [Mmax, d_{l+1}]
+  std::vector<size_t> off_G;      // G_l,    l = 0..L-1    [Mmax*O, d_{l+1}]
+  std::vector<size_t> off_Wt;     // Wt_l,   l = 1..L-1    [d_l, d_{l+1}]
+  std::vector<size_t> off_gram;   // gram_l, l = 0..L      [max_n1*max_n2]
+  std::vector<int> param_index;   // first parameter slot of dense layer l
+};
+
+static thread_local std::string g_init_error;
+
+static int fail(ntk_handle* h, int code, const std::string& msg) {
+  if (h)
+    h->err = msg;
+  else
+    g_init_error = msg;
+  return code;
+}
+
+static int hip_fail(ntk_handle* h, hipError_t e, const char* what) {
+  return fail(h, NTK_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
+}
+
+// ------------------------------------------------------------------------------ validation
+static int validate(const ntk_model_desc* m, ntk_handle* tmp) {
+  if (!m || !m->layers || m->n_layers <= 0) return fail(nullptr, NTK_E_ARG, "null or empty model descriptor");
+  if (m->out_dim <= 0) return fail(nullptr, NTK_E_SHAPE, "out_dim must be positive");
+  const int n = m->n_layers;
+  for (int i = 0; i < n; ++i) {
+    const ntk_layer_desc& L = m->layers[i];
+    if (L.kind != NTK_DENSE && L.kind != NTK_CONV3X3_SAME && L.kind != NTK_GAP)
+      return fail(nullptr, NTK_E_UNSUPPORTED, "layer " + std::to_string(i) + ": unknown kind");
+    if (L.act != NTK_ACT_NONE && L.act != NTK_ACT_RELU && L.act != NTK_ACT_ERF)
+      return fail(nullptr, NTK_E_UNSUPPORTED, "layer " + std::to_string(i) + ": unknown activation");
+    if (L.kind != NTK_GAP && (L.in <= 0 || L.out <= 0))
+      return fail(nullptr, NTK_E_SHAPE, "layer " + std::to_string(i) + ": in/out must be positive");
+  }
+  const ntk_layer_desc& last = m->layers[n - 1];
+  if (last.kind != NTK_DENSE)
+    return fail(nullptr, NTK_E_UNSUPPORTED, "the last layer must be a dense readout");
+  if (last.act != NTK_ACT_NONE)
+    return fail(nullptr, NTK_E_UNSUPPORTED, "the readout layer must have no activation (f = z_last)");
+  if (last.out != m->out_dim) return fail(nullptr, NTK_E_SHAPE, "last layer out != out_dim");
+
+  bool any_conv = false;
+  for (int i = 0; i < n; ++i) any_conv |= m->layers[i].kind != NTK_DENSE;
+  if (!any_conv) {
+    if (m->in_h != 1 || m->in_w != 1)
+      return fail(nullptr, NTK_E_SHAPE, "a fully-connected model takes in_h = in_w = 1");
+    if (m->layers[0].in != m->in_c) return fail(nullptr, NTK_E_SHAPE, "layer 0 in != in_c");
+    for (int i = 0; i + 1 < n; ++i)
+      if (m->layers[i].out != m->layers[i + 1].in)
+        return fail(nullptr, NTK_E_SHAPE, "layer " + std::to_string(i) + " out != layer " +
+                                               std::to_string(i + 1) + " in");
+    if (n - 1 > kMaxLayers)
+      return fail(nullptr, NTK_E_UNSUPPORTED, "too many hidden layers (max " + std::to_string(kMaxLayers) + ")");
+    tmp->cnn = false;
+    return NTK_OK;
+  }
+  // CNN: conv3x3 x k, gap, dense readout
+  int i = 0;
+  if (m->in_h <= 0 || m->in_w <= 0 || m->in_c <= 0) return fail(nullptr, NTK_E_SHAPE, "bad input shape");
+  int c = m->in_c;
+  while (i < n && m->layers[i].kind == NTK_CONV3X3_SAME) {
+    const ntk_layer_desc& L = m->layers[i];
+    if (L.in != c) return fail(nullptr, NTK_E_SHAPE, "conv layer " + std::to_string(i) + ": in != previous channels");
+    if (L.has_bias) return fail(nullptr, NTK_E_UNSUPPORTED, "convolution biases are not supported");
+    c = L.out;
+    ++i;
+  }
+  if (i == 0 || i > kMaxLayers)
+    return fail(nullptr, NTK_E_UNSUPPORTED, "a CNN is 1..64 conv3x3 layers, then gap, then a dense readout");
+  if (i != n - 2 || m->layers[i].kind != NTK_GAP)
+    return fail(nullptr, NTK_E_UNSUPPORTED, "a CNN is conv3x3 layers, then gap, then one dense readout");
+  if (m->layers[i].act != NTK_ACT_NONE) return fail(nullptr, NTK_E_UNSUPPORTED, "gap takes no activation");
+  if (last.in != c) return fail(nullptr, NTK_E_SHAPE, "readout in != conv channels");
+  if (last.has_bias) return fail(nullptr, NTK_E_UNSUPPORTED, "the CNN readout has no bias");
+  tmp->cnn = true;
+  return NTK_OK;
+}
+
+static size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
+
+// ------------------------------------------------------------------------------ planning
+static void plan_fcn(ntk_handle* h) {
+  const int n = (int)h->layers.size();
+  h->L = n - 1;
+  const int L = h->L;
+  h->dims.resize(L + 2);
+  h->dims[0] = h->layers[0].in;
+  for (int l = 0; l <= L; ++l) h->dims[l + 1] = h->layers[l].out;
+  const size_t Mmax = (size_t)h->max_n1 + h->max_n2;
+  const size_t O = h->out_dim;
+  size_t off = 0;
+  auto take = [&](size_t floats) {
+    size_t o = off;
+    off = align_up(off + floats * 4);
+    return o;
+  };
+  h->off_h.assign(L + 1, 0);
+  h->off_dphi.assign(std::max(L, 1), 0);
+  h->off_G.assign(std::max(L, 1), 0);
+  h->off_Wt.assign(std::max(L, 1), 0);
+  h->off_gram.assign(L + 1, 0);
+  for (int l = 0; l <= L; ++l) h->off_h[l] = take(Mmax * h->dims[l]);
+  for (int l = 0; l < L; ++l) h->off_dphi[l] = take(Mmax * h->dims[l + 1]);
+  for (int l = 0; l < L; ++l) h->off_G[l] = take(Mmax * O * h->dims[l + 1]);
+  for (int l = 1; l < L; ++l) h->off_Wt[l] = take((size_t)h->dims[l] * h->dims[l + 1]);
+  for (int l = 0; l <= L; ++l) h->off_gram[l] = take((size_t)h->max_n1 * h->max_n2);
+  h->ws_bytes = off;
+  h->param_index.assign(L + 1, 0);
+  int p = 0;
+  for (int l = 0; l <= L; ++l) {
+    h->param_index[l] = p;
+    p += 1 + (h->layers[l].has_bias ? 1 : 0);
+  }
+}
+
+// ------------------------------------------------------------------------------ C ABI
+extern "C" int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, void* hip_stream,
+                        ntk_handle** out) {
+  if (!out) return fail(nullptr, NTK_E_ARG, "out is NULL");
+  *out = nullptr;
+  if (max_n1 <= 0 || max_n2 <= 0) return fail(nullptr, NTK_E_ARG, "max_n1 and max_n2 must be positive");
+  ntk_handle tmp;
+  int rc = validate(model, &tmp);
+  if (rc != NTK_OK) return rc;
+  ntk_handle* h = new (std::nothrow) ntk_handle();
+  if (!h) return fail(nullptr, NTK_E_OOM, "host allocation failed");
+  h->layers.assign(model->layers, model->layers + model->n_layers);
+  h->in_h = model->in_h;
+  h->in_w = model->in_w;
+  h->in_c = model->in_c;
+  h->out_dim = model->out_dim;
+  h->cnn = tmp.cnn;
+  h->max_n1 = max_n1;
+  h->max_n2 = max_n2;
+  h->stream = (hipStream_t)hip_stream;
+  if (h->cnn) {
+    delete h;
+    return fail(nullptr, NTK_E_UNSUPPORTED, "convolutional models are not available in this build");
+  }
+  plan_fcn(h);
+  hipError_t e = hipGetDevice(&h->device);
+  if (e != hipSuccess) {
+    delete h;
+    return hip_fail(nullptr, e, "hipGetDevice");
+  }
+  e = hipMalloc((void**)&h->ws, h->ws_bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    size_t bytes = h->ws_bytes;
+    delete h;
+    return fail(nullptr, NTK_E_OOM, "workspace allocation of " + std::to_string(bytes) + " bytes failed");
+  }
+  *out = h;
+  return NTK_OK;
+}
+
+static int compute_fcn(ntk_handle* h, const float* const* params, const float* X1, int n1,
+                       const float* X2, int n2, float* theta) {
+  const int L = h->L;
+  const int O = h->out_dim;
+  const bool sym = h->opt_symmetric && X1 == X2 && n1 == n2;
+  const int M = sym ? n1 : n1 + n2;
+  hipStream_t s = h->stream;
+  Profiler* P = &h->prof;
+  auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
+  for (int l = 0; l <= L; ++l) {
+    if (!params[h->param_index[l]]) return fail(h, NTK_E_ARG, "null weight pointer");
+    if (h->layers[l].has_bias && !params[h->param_index[l] + 1]) return fail(h, NTK_E_ARG, "null bias pointer");
+  }
+  hipError_t e;
+  const int d0 = h->dims[0];
+  const float* h0 = X1;
+  if (!sym) {
+    prof_begin(P, s, KC_COPY);
+    e = hipMemcpyAsync(F(h->off_h[0]), X1, sizeof(float) * (size_t)n1 * d0, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(F(h->off_h[0]) + (size_t)n1 * d0, X2, sizeof(float) * (size_t)n2 * d0,
+                         hipMemcpyDeviceToDevice, s);
+    prof_end(P, s, KC_COPY);
+    if (e != hipSuccess) return hip_fail(h, e, "stacking X1/X2");
+    h0 = F(h->off_h[0]);
+  }
+  auto hptr = [&](int l) -> const float* { return l == 0 ? h0 : F(h->off_h[l]); };
+
+  // 1. forward pass (the readout's own output f is not needed for Theta)
+  for (int l = 0; l < L; ++l) {
+    const float* W = params[h->param_index[l]];
+    const float* b = h->layers[l].has_bias ? params[h->param_index[l] + 1] : nullptr;
+    prof_begin(P, s, KC_DENSE_FWD);
+    e = launch_dense_fwd(s, hptr(l), W, b, M, h->dims[l + 1], h->dims[l], h->layers[l].act,
+                         F(h->off_h[l + 1]), F(h->off_dphi[l]));
+    prof_end(P, s, KC_DENSE_FWD);
+    if (e != hipSuccess) return hip_fail(h, e, "dense forward");
+  }
+  // 2. cotangents of every hidden pre-activation for all O outputs at once
+  if (L >= 1) {
+    for (int l = 1; l < L; ++l) {
+      prof_begin(P, s, KC_TRANSPOSE);
+      e = launch_transpose(s, params[h->param_index[l]], h->dims[l + 1], h->dims[l], F(h->off_Wt[l]));
+      prof_end(P, s, KC_TRANSPOSE);
+      if (e != hipSuccess) return hip_fail(h, e, "weight transpose");
+    }
+    prof_begin(P, s, KC_BWD_SEED);
+    e = launch_bwd_seed(s, params[h->param_index[L]], F(h->off_dphi[L - 1]), M, O, h->dims[L],
+                        F(h->off_G[L - 1]));
+    prof_end(P, s, KC_BWD_SEED);
+    if (e != hipSuccess) return hip_fail(h, e, "backward seed");
+    for (int l = L - 1; l >= 1; --l) {
+      prof_begin(P, s, KC_DENSE_BWD);
+      e = launch_dense_bwd(s, F(h->off_G[l]), F(h->off_Wt[l]), F(h->off_dphi[l - 1]), M * O,
+                           h->dims[l], h->dims[l + 1], O, F(h->off_G[l - 1]));
+      prof_end(P, s, KC_DENSE_BWD);
+      if (e != hipSuccess) return hip_fail(h, e, "dense backward");
+    }
+  }
+  // 3. layer-input Grams (the x1.x2 scalars), one batched launch
+  GramBatch gb{};
+  gb.count = L + 1;
+  for (int l = 0; l <= L; ++l) {
+    const float* hl = hptr(l);
+    gb.h1[l] = hl;
+    gb.h2[l] = sym ? hl : hl + (size_t)n1 * h->dims[l];
+    gb.out[l] = F(h->off_gram[l]);
+    gb.K[l] = h->dims[l];
+    gb.beta[l] = h->layers[l].has_bias ? 1.0f : 0.0f;
+  }
+  prof_begin(P, s, KC_GRAM);
+  e = launch_gram(s, gb, n1, n2);
+  prof_end(P, s, KC_GRAM);
+  if (e != hipSuccess) return hip_fail(h, e, "gram");
+  // 4. fused contraction summed over layers, written as theta[n1][n2][o1][o2]
+  FcnContraction c{};
+  c.L = L;
+  for (int l = 0; l < L; ++l) {
+    c.G1[l] = F(h->off_G[l]);
+    c.G2[l] = sym ? F(h->off_G[l]) : F(h->off_G[l]) + (size_t)n1 * O * h->dims[l + 1];
+    c.gram[l] = F(h->off_gram[l]);
+    c.K[l] = h->dims[l + 1];
+  }
+  c.gram_readout = F(h->off_gram[L]);
+  prof_begin(P, s, KC_NTK_FCN);
+  e = launch_ntk_fcn(s, c, n1, n2, O, sym ? 1 : 0, theta);
+  prof_end(P, s, KC_NTK_FCN);
+  if (e != hipSuccess) return hip_fail(h, e, "ntk contraction");
+  return NTK_OK;
+}
+
+extern "C" int ntk_compute(ntk_handle* h, const float* const* params, const float* X1, int n1,
+                           const float* X2, int n2, float* theta) {
+  if (!h) return fail(nullptr, NTK_E_ARG, "handle is NULL");
+  if (!params || !X1 || !X2 || !theta) return fail(h, NTK_E_ARG, "null pointer argument");
+  if (n1 <= 0 || n2 <= 0) return fail(h, NTK_E_ARG, "n1 and n2 must be positive");
+  if (n1 > h->max_n1 || n2 > h->max_n2)
+    return fail(h, NTK_E_ARG, "n1/n2 exceed the max_n1/max_n2 given to ntk_init");
+  if (h->cnn) return fail(h, NTK_E_UNSUPPORTED, "convolutional models are not available in this build");
+  h->err.clear();
+  return compute_fcn(h, params, X1, n1, X2, n2, theta);
+}
+
+extern "C" int ntk_free(ntk_handle* h) {
+  if (!h) return NTK_OK;
+  (void)hipStreamSynchronize(h->stream);
+  if (h->ws) (void)hipFree(h->ws);
+  delete h;
+  return NTK_OK;
+}
+
+extern "C" const char* ntk_last_error(const ntk_handle* h) {
+  return h ? h->err.c_str() : g_init_error.c_str();
+}
+
+extern "C" int ntk_set_option(ntk_handle* h, int option, int value) {
+  if (!h) return fail(nullptr, NTK_E_ARG, "handle is NULL");
+  if (option == NTK_OPT_SYMMETRIC) {
+    if (value != 0 && value != 1) return fail(h, NTK_E_ARG, "NTK_OPT_SYMMETRIC takes 0 or 1");
+    h->opt_symmetric = value;
+    return NTK_OK;
+  }
+  if (option == NTK_OPT_CONV_ORDER) {
+    if (value < NTK_CONV_ORDER_AUTO || value > NTK_CONV_ORDER_INSIDE_OUT)
+      return fail(h, NTK_E_ARG, "NTK_OPT_CONV_ORDER takes 0, 1 or 2");
+    h->opt_conv_order = value;
+    return NTK_OK;
+  }
+  return fail(h, NTK_E_ARG, "unknown option");
+}
+
+extern "C" int ntk_set_stream(ntk_handle* h, void* hip_stream) {
+  if (!h) return fail(nullptr, NTK_E_ARG, "handle is NULL");
+  h->stream = (hipStream_t)hip_stream;
+  return NTK_OK;
+}
+
+extern "C" long long ntk_workspace_bytes(const ntk_handle* h) { return h ? (long long)h->ws_bytes : 0; }
+
+extern "C" int ntk_profile_enable(ntk_handle* h, int enable) {
+  if (!h) return fail(nullptr, NTK_E_ARG, "handle is NULL");
+  h->prof.enabled = enable != 0;
+  return NTK_OK;
+}
+
+extern "C" int ntk_profile_read(ntk_handle* h, const char** names, double* total_ms, long long* launches,
+                                int max) {
+  if (!h) return fail(nullptr, NTK_E_ARG, "handle is NULL");
+  if (max < 0 || (max > 0 && (!names || !total_ms || !launches))) return fail(h, NTK_E_ARG, "bad output arrays");
+  hipError_t e = hipStreamSynchronize(h->stream);
+  if (e != hipSuccess) return hip_fail(h, e, "hipStreamSynchronize");
+  Profiler& p = h->prof;
+  for (auto& q : p.pending) {
+    float ms = 0.f;
+    if (hipEventElapsedTime(&ms, q.a, q.b) == hipSuccess) {
+      p.total_ms[q.cls] += ms;
+      p.launches[q.cls] += 1;
+    }
+    p.pool.push_back(q.a);
+    p.pool.push_back(q.b);
+  }
+  p.pending.clear();
+  int n = 0;
+  for (int c = 0; c < KC_COUNT && n < max; ++c) {
+    if (p.launches[c] == 0) continue;
+    names[n] = kernel_class_name(c);
+    total_ms[n] = p.total_ms[c];
+    launches[n] = p.launches[c];
+    ++n;
+  }
+  for (int c = 0; c < KC_COUNT; ++c) {
+    p.total_ms[c] = 0;
+    p.launches[c] = 0;
+  }
+  return n;
+}

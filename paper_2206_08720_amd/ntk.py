@@ -1,0 +1,115 @@
+"""Python front end of the MI355X structured-derivatives NTK library.
+
+    theta = compute(spec, params, X1, X2)      # torch tensor [N1, N2, O, O] on the GPU
+
+`spec` is a network description in the `workloads` format; `params` and the
+inputs are float32 torch tensors on the current GPU.  PyTorch supplies device
+memory and the current HIP stream only: every step runs in libntk.so.
+"""
+from __future__ import annotations
+
+import ctypes
+
+import torch
+
+from . import _lib
+
+
+class NTK:
+    """A handle bound to one network, maximum batch sizes, device and stream."""
+
+    def __init__(self, spec, max_n1, max_n2, stream=None, device=None):
+        self._lib = _lib.load()
+        if not torch.cuda.is_available():
+            raise RuntimeError("no GPU visible: the NTK library runs on an MI355X only")
+        self.spec = spec
+        self.out_dim = spec["layers"][-1]["out"]
+        self.max_n1, self.max_n2 = int(max_n1), int(max_n2)
+        self.device = torch.device("cuda", torch.cuda.current_device() if device is None
+                                   else torch.device(device).index or 0)
+        desc, self._keep = _lib.model_desc(spec)
+        h = ctypes.c_void_p()
+        with torch.cuda.device(self.device):
+            s = torch.cuda.current_stream() if stream is None else stream
+            self._stream = s
+            _lib.check(self._lib.ntk_init(ctypes.byref(desc), self.max_n1, self.max_n2,
+                                          ctypes.c_void_p(s.cuda_stream), ctypes.byref(h)))
+        self._h = h
+
+    # -- options -----------------------------------------------------------------------
+    def set_option(self, option, value):
+        _lib.check(self._lib.ntk_set_option(self._h, option, value), self._h)
+
+    def set_stream(self, stream):
+        self._stream = stream
+        _lib.check(self._lib.ntk_set_stream(self._h, ctypes.c_void_p(stream.cuda_stream)), self._h)
+
+    def workspace_bytes(self):
+        return int(self._lib.ntk_workspace_bytes(self._h))
+
+    # -- compute -----------------------------------------------------------------------
+    def _check_tensor(self, t, name):
+        if not isinstance(t, torch.Tensor) or t.device != self.device or t.dtype != torch.float32:
+            raise TypeError(f"{name} must be a float32 tensor on {self.device}")
+        if not t.is_contiguous():
+            raise ValueError(f"{name} must be contiguous")
+
+    def compute(self, params, X1, X2=None, out=None):
+        """Enqueue Theta(X1, X2) on the handle's stream; returns the [N1,N2,O,O] tensor."""
+        if X2 is None:
+            X2 = X1
+        for i, p in enumerate(params):
+            self._check_tensor(p, f"params[{i}]")
+        self._check_tensor(X1, "X1")
+        self._check_tensor(X2, "X2")
+        n1, n2 = X1.shape[0], X2.shape[0]
+        O = self.out_dim
+        if out is None:
+            out = torch.empty((n1, n2, O, O), dtype=torch.float32, device=self.device)
+        else:
+            self._check_tensor(out, "out")
+            if tuple(out.shape) != (n1, n2, O, O):
+                raise ValueError("out has the wrong shape")
+        ptrs = (ctypes.c_void_p * len(params))(*[p.data_ptr() for p in params])
+        _lib.check(self._lib.ntk_compute(self._h, ptrs, ctypes.c_void_p(X1.data_ptr()), n1,
+                                         ctypes.c_void_p(X2.data_ptr()), n2,
+                                         ctypes.c_void_p(out.data_ptr())), self._h)
+        return out
+
+    # -- per-kernel timing -------------------------------------------------------------
+    def profile_enable(self, on=True):
+        _lib.check(self._lib.ntk_profile_enable(self._h, 1 if on else 0), self._h)
+
+    def profile_read(self):
+        """{kernel class: (total ms, launches)} since the last read (synchronises)."""
+        n = 32
+        names = (ctypes.c_char_p * n)()
+        ms = (ctypes.c_double * n)()
+        cnt = (ctypes.c_longlong * n)()
+        k = self._lib.ntk_profile_read(self._h, names, ms, cnt, n)
+        if k < 0:
+            _lib.check(k, self._h)
+        return {names[i].decode(): (ms[i], cnt[i]) for i in range(k)}
+
+    def close(self):
+        if getattr(self, "_h", None) is not None and self._h.value:
+            self._lib.ntk_free(self._h)
+            self._h = ctypes.c_void_p()
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+def compute(spec, params, X1, X2=None):
+    """One-shot Theta(X1, X2) (allocates a handle sized for these batches)."""
+    X2 = X1 if X2 is None else X2
+    h = NTK(spec, X1.shape[0], X2.shape[0])
+    try:
+        out = h.compute(params, X1, X2)
+        torch.cuda.current_stream().synchronize()
+        return out
+    finally:
+        h.close()

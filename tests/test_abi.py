@@ -1,0 +1,79 @@
+"""CPU-side checks of the C ABI (no GPU): the library loads, exports every symbol
+include/ntk.h declares, and rejects bad descriptors/arguments before touching the GPU."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+@pytest.fixture(scope="module")
+def lib():
+    from paper_2206_08720_amd import _lib
+    if not os.path.exists(_lib.LIB_PATH):
+        from paper_2206_08720_amd.build import build
+        build()
+    return _lib.load()
+
+
+def _declared_symbols():
+    txt = open(os.path.join(ROOT, "include", "ntk.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(ntk_[a-z_]+)\s*\(", txt)))
+
+
+def test_header_declares_the_expected_entry_points():
+    from paper_2206_08720_amd import _lib
+    assert set(_declared_symbols()) == set(_lib.EXPORTED_SYMBOLS)
+
+
+def test_library_exports_every_declared_symbol(lib):
+    for name in _declared_symbols():
+        assert hasattr(lib, name), name
+
+
+def _init(lib, spec, n1=4, n2=4):
+    from paper_2206_08720_amd import _lib
+    desc, keep = _lib.model_desc(spec)
+    h = ctypes.c_void_p()
+    rc = lib.ntk_init(ctypes.byref(desc), n1, n2, None, ctypes.byref(h))
+    return rc, h
+
+
+def test_init_rejects_bad_models_before_any_device_call(lib):
+    from paper_2206_08720_amd import _lib
+    bad_chain = wl.fcn_spec("b", 8, [16], 3)
+    bad_chain["layers"][1]["in"] = 15
+    rc, h = _init(lib, bad_chain)
+    assert rc == _lib.NTK_E_SHAPE and not h.value
+    assert "in" in _lib.last_error()
+
+    act_readout = wl.fcn_spec("b", 8, [16], 3)
+    act_readout["layers"][-1]["act"] = "relu"
+    assert _init(lib, act_readout)[0] == _lib.NTK_E_UNSUPPORTED
+
+    conv_bias = wl.cnn_spec("b", (4, 4), 3, [8], 2, bias=True)
+    assert _init(lib, conv_bias)[0] == _lib.NTK_E_UNSUPPORTED
+
+    no_gap = wl.cnn_spec("b", (4, 4), 3, [8], 2)
+    del no_gap["layers"][1]
+    assert _init(lib, no_gap)[0] == _lib.NTK_E_UNSUPPORTED
+
+    assert _init(lib, wl.fcn_spec("b", 8, [16], 3), 0, 4)[0] == _lib.NTK_E_ARG
+
+    desc = _lib.ntk_model_desc(0, None, 1, 1, 8, 3)
+    h = ctypes.c_void_p()
+    assert lib.ntk_init(ctypes.byref(desc), 4, 4, None, ctypes.byref(h)) == _lib.NTK_E_ARG
+
+
+def test_null_handle_calls(lib):
+    from paper_2206_08720_amd import _lib
+    assert lib.ntk_free(None) == _lib.NTK_OK
+    assert lib.ntk_compute(None, None, None, 1, None, 1, None) == _lib.NTK_E_ARG
+    assert lib.ntk_set_option(None, 1, 1) == _lib.NTK_E_ARG
+    assert lib.ntk_workspace_bytes(None) == 0
+    assert isinstance(lib.ntk_last_error(None), bytes)

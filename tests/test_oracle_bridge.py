@@ -46,3 +46,28 @@ def test_structured_equals_jc_on_random_ragged_mlps(act, bias):
     X1 = wl.make_inputs(spec, 9, 8)
     X2 = wl.make_inputs(spec, 5, 9)
     _close(oracle.ntk_structured_fp64(spec, params, X1, X2), oracle.ntk_jc(spec, params, X1, X2))
+
+
+def test_structured_diag_equals_jc_row_norms():
+    spec = wl.fcn_spec("ragged", 13, [37, 19], 7, act="erf", bias=True)
+    params = wl.make_params(spec, 17, bias_var=0.5)
+    X = wl.make_inputs(spec, 6, 18)
+    _, sq, _ = oracle.ntk_jc_with_norms(spec, params, X, X[:1])
+    _close(oracle.ntk_structured_diag_fp64(spec, params, X), sq)
+
+
+@pytest.mark.parametrize("name,rows,outs", [
+    ("tiny_relu_mlp", list(range(8)), None),
+    ("relu_mlp_d8_w2048", [3, 400], [1, 8]),
+])
+def test_structured_equals_jc_with_fp32_layer_storage(name, rows, outs):
+    spec, params, X1, X2 = wl.make_workload(name)
+    a = oracle.ntk_structured_fp64(spec, params, X1[rows], X2[rows], layer_storage="fp32")
+    b = oracle.ntk_jc(spec, params, X1[rows], X2[rows], outs, outs, layer_storage="fp32")
+    if outs is not None:
+        a = a[:, :, outs][:, :, :, outs]
+    _close(a, b)
+    d = oracle.ntk_structured_diag_fp64(spec, params, X1[rows], layer_storage="fp32")
+    _, sq, _ = oracle.ntk_jc_with_norms(spec, params, X1[rows], X2[rows[:1]], outs, outs,
+                                        layer_storage="fp32")
+    _close(d if outs is None else d[:, outs], sq)

@@ -211,3 +211,41 @@ def test_block_chunking_does_not_change_the_result():
     a = oracle.ntk_jc(spec, params, X1, X2)
     b = oracle.ntk_jc(spec, params, X1, X2, max_block_bytes=600)   # forces many column chunks
     np.testing.assert_allclose(a, b, rtol=1e-14, atol=1e-14)
+
+
+# ---- float32 layer storage (the mode GPU parity uses) --------------------------------------
+@pytest.mark.parametrize("fname", ["fcn_hand_relu.json", "fcn_hand_relu_bias.json",
+                                   "cnn_hand_1x2.json"])
+def test_fp32_storage_reproduces_the_hand_worked_values(golden_dir, fname):
+    # every intermediate value of these examples is exactly representable in float32
+    d = json.load(open(os.path.join(golden_dir, fname)))
+    params = [np.array(p, dtype=np.float32) for p in d["params"]]
+    X = np.array(d["X"], dtype=np.float32)
+    th = oracle.ntk_jc(d["spec"], params, X, X, layer_storage="fp32")
+    np.testing.assert_allclose(th, np.array(d["theta"]), rtol=0, atol=1e-12)
+
+
+@pytest.mark.parametrize("idx", [1, 4])
+def test_fp32_storage_is_a_float32_perturbation_on_smooth_nets(idx):
+    # erf nets: rounding the stored layer outputs to float32 moves Theta by ~1e-7 relative
+    spec, wv = _tiny_specs()[idx]
+    params = wl.make_params(spec, 171 + idx, wv, bias_var=0.3)
+    X1 = wl.make_inputs(spec, 4, 181 + idx)
+    X2 = wl.make_inputs(spec, 3, 191 + idx)
+    a = oracle.ntk_jc(spec, params, X1, X2)
+    b = oracle.ntk_jc(spec, params, X1, X2, layer_storage="fp32")
+    assert not np.array_equal(a, b)
+    assert np.max(np.abs(a - b)) <= 1e-6 * np.max(np.abs(a))
+
+
+def test_fp32_storage_rounds_every_stored_layer_output():
+    from oracle.ntk_jc import _forward_record
+    spec, wv = _tiny_specs()[3]
+    params = wl.make_params(spec, 201, wv)
+    X = wl.make_inputs(spec, 3, 202)
+    rec, _ = _forward_record(spec, params, X, layer_storage="fp32")
+    for r in rec[1:]:
+        h = r["h"]
+        assert np.array_equal(h, h.astype(np.float32).astype(np.float64))
+    with pytest.raises(ValueError):
+        _forward_record(spec, params, X, layer_storage="fp16")
