@@ -1,0 +1,457 @@
+// kernels_conv.hip -- convolutional path of the structured-derivatives NTK on gfx950.
+//
+// A 3x3 SAME, stride-1 convolution z[p, c] = sum_k patch[p, k] K[c, k] has a
+// Jacobian dz/dK that is constant-block diagonal along the output channel (the
+// appendix "Constant-block Diagonal" structure, C = W for a convolution), so the
+// smallest sub-array to keep is the patch matrix of the layer input (appendix
+// "CNN NTK Complexity": D x F*Cin per sample, formed here implicitly inside the
+// GEMM loaders).  The kernels compute
+//   * the forward pass keeping every layer input and act'(z) (fp64 accumulation, as
+//     for dense layers, so ReLU decisions are a function of the fp32-stored input)
+//   * global average pooling (the input block-tiled structure of a mean)
+//   * the cotangent of the last conv pre-activation, W_d[o, c] / D * act'(z)
+//   * the transposed convolution pulling the (N1+N2)*O cotangent images back one
+//     layer (a SAME convolution with the spatially flipped, channel-transposed kernel)
+//   * the outside-in weight-sharing contraction: per sample and layer the weight-space
+//     cotangent J[(n,o),(c,k)] = sum_p G[n,o,p,c] patch[n,p,k]
+//   * J1 J2^T with a deterministic split over K, then a reduction adding the readout
+//     summand (g1.g2) delta_{o1 o2} and writing theta[n1][n2][o1][o2].
+#include "gemm_core.hpp"
+#include "launch_conv.hpp"
+
+namespace ntk {
+
+using CfgConvF64 = TileCfg<64, 64, 32, 32, 32>;    // forward, fp64 MFMA
+using CfgConv = TileCfg<128, 64, 32, 64, 32>;      // backward / wgrad, fp32 MFMA
+using CfgSplitK = TileCfg<128, 128, 32, 64, 64>;   // J1 J2^T partial products
+
+static inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
+static inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
+
+template <class Cfg, class LA, class LB>
+static hipError_t set_smem(const void* fn) {
+  constexpr int bytes = gemm_smem_bytes<Cfg, LA, LB>();
+  if (bytes > 65536)
+    return hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  return hipSuccess;
+}
+
+// ------------------------------------------------------------------------------ loaders
+// Patch matrix of an NHWC batch as a K-inner operand: row = img*D + p, p = y*W + x,
+// k = (kh*3 + kw)*C + ci; the tap (kh, kw) reads pixel (y + kh - 1, x + kw - 1), zero
+// outside the image.
+struct LoadPatchesKInner {
+  static constexpr bool K_INNER = true;
+  const float* x;
+  int rows, H, W, C, K;  // K = 9*C
+  FastDiv fD, fW, fC;
+  bool vec;              // C % 4 == 0 and x 16-byte aligned
+  __device__ __forceinline__ float tap_value(int img, int y, int xx, int k) const {
+    const int tap = (int)fC.div(k), ci = k - tap * C;
+    const int kh = (tap * 11) >> 5, kw = tap - 3 * kh;  // tap / 3 for tap < 9
+    const int yy = y + kh - 1, xq = xx + kw - 1;
+    if (yy < 0 || yy >= H || xq < 0 || xq >= W) return 0.f;
+    return x[(((long long)img * H + yy) * W + xq) * C + ci];
+  }
+  __device__ __forceinline__ f32x4 load4(int row, int k) const {
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    if (row >= rows) return v;
+    const int img = (int)fD.div(row), p = row - img * (int)fD.d;
+    const int y = (int)fW.div(p), xx = p - y * W;
+    if (vec && k + 3 < K) {
+      const int tap = (int)fC.div(k), ci = k - tap * C;
+      const int kh = (tap * 11) >> 5, kw = tap - 3 * kh;
+      const int yy = y + kh - 1, xq = xx + kw - 1;
+      if (yy >= 0 && yy < H && xq >= 0 && xq < W)
+        v = *reinterpret_cast<const f32x4*>(x + (((long long)img * H + yy) * W + xq) * C + ci);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (k + j < K) v[j] = tap_value(img, y, xx, k + j);
+    }
+    return v;
+  }
+};
+
+// G of one sample as a K-outer operand of the weight-space cotangent product:
+// row = o*C + c, k = p;  element = G[((s*O + o)*D + p)*C + c]  (base already at sample s).
+struct LoadCotangentKOuter {
+  static constexpr bool K_INNER = false;
+  const float* g;
+  int rows, K, C, D;     // rows = O*C, K = D
+  FastDiv fC;
+  bool vec;              // C % 4 == 0 and g 16-byte aligned
+  __device__ __forceinline__ f32x4 load4(int row, int k) const {
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    if (k >= K) return v;
+    if (vec && row + 3 < rows) {
+      const int o = (int)fC.div(row), c = row - o * C;
+      v = *reinterpret_cast<const f32x4*>(g + ((long long)o * D + k) * C + c);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int r = row + j;
+        if (r < rows) {
+          const int o = (int)fC.div(r), c = r - o * C;
+          v[j] = g[((long long)o * D + k) * C + c];
+        }
+      }
+    }
+    return v;
+  }
+};
+
+// Patch matrix of one sample as a K-outer operand: row = k (tap, ci), kdim = p.
+struct LoadPatchesKOuter {
+  static constexpr bool K_INNER = false;
+  const float* x;        // sample base, [H, W, C]
+  int rows, K, H, W, C;  // rows = 9*C, K = D
+  FastDiv fW, fC;
+  bool vec;
+  __device__ __forceinline__ float tap_value(int y, int xx, int k) const {
+    const int tap = (int)fC.div(k), ci = k - tap * C;
+    const int kh = (tap * 11) >> 5, kw = tap - 3 * kh;
+    const int yy = y + kh - 1, xq = xx + kw - 1;
+    if (yy < 0 || yy >= H || xq < 0 || xq >= W) return 0.f;
+    return x[((long long)yy * W + xq) * C + ci];
+  }
+  __device__ __forceinline__ f32x4 load4(int row, int p) const {
+    f32x4 v = {0.f, 0.f, 0.f, 0.f};
+    if (p >= K) return v;
+    const int y = (int)fW.div(p), xx = p - y * W;
+    if (vec && row + 3 < rows) {
+      const int tap = (int)fC.div(row), ci = row - tap * C;
+      const int kh = (tap * 11) >> 5, kw = tap - 3 * kh;
+      const int yy = y + kh - 1, xq = xx + kw - 1;
+      if (yy >= 0 && yy < H && xq >= 0 && xq < W)
+        v = *reinterpret_cast<const f32x4*>(x + ((long long)yy * W + xq) * C + ci);
+    } else {
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        if (row + j < rows) v[j] = tap_value(y, xx, row + j);
+    }
+    return v;
+  }
+};
+
+static LoadPatchesKInner patches_kinner(const float* x, int images, int H, int W, int C) {
+  LoadPatchesKInner l;
+  l.x = x;
+  l.rows = images * H * W;
+  l.H = H;
+  l.W = W;
+  l.C = C;
+  l.K = 9 * C;
+  l.fD = FastDiv((uint32_t)(H * W));
+  l.fW = FastDiv((uint32_t)W);
+  l.fC = FastDiv((uint32_t)C);
+  l.vec = (C % 4 == 0) && aligned16(x);
+  return l;
+}
+
+// ------------------------------------------------------------------------------ forward
+template <class Cfg>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_conv_fwd(LoadPatchesKInner la, LoadKInner lb, int M, int N, int act, float* __restrict__ hn,
+           float* __restrict__ dphi, int tiles_n) {
+  extern __shared__ float smem[];
+  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  f64x4 acc[Cfg::FM16][Cfg::FN16];
+  zero_acc<Cfg>(acc);
+  gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
+  for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, double z) {
+    if (r < M && c < N) {
+      float h, d;
+      if (act == 1) {
+        h = z > 0.0 ? (float)z : 0.f;
+        d = z > 0.0 ? 1.f : 0.f;
+      } else {
+        const float zf = (float)z;
+        h = act_fwd(act, zf);
+        d = act_deriv(act, zf);
+      }
+      hn[(long long)r * N + c] = h;
+      dphi[(long long)r * N + c] = d;
+    }
+  });
+}
+
+hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int W, int Cin,
+                           const float* K, int Cout, int act, float* hn, float* dphi) {
+  using Cfg = CfgConvF64;
+  LoadPatchesKInner la = patches_kinner(x, images, H, W, Cin);
+  LoadKInner lb{K, Cout, 9 * Cin, 9 * Cin, aligned16(K) && (9 * Cin) % 4 == 0};
+  const int M = images * H * W;
+  const int tn = cdiv(Cout, Cfg::BN), tm = cdiv(M, Cfg::BM);
+  hipError_t e = set_smem<Cfg, LoadPatchesKInner, LoadKInner>((const void*)k_conv_fwd<Cfg>);
+  if (e != hipSuccess) return e;
+  k_conv_fwd<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LoadPatchesKInner, LoadKInner>(), s>>>(
+      la, lb, M, Cout, act, hn, dphi, tn);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------ GAP, seed
+// g[img, c] = mean over the D pixels of h[img, p, c]; one workgroup per image, fixed order.
+__global__ void k_gap(const float* __restrict__ h, int D, int C, float* __restrict__ g) {
+  __shared__ float part[256];
+  const int img = blockIdx.x;
+  const int lanes_c = C < 256 ? C : 256;
+  const int groups = 256 / lanes_c;
+  const int t = threadIdx.x;
+  const int grp = t / lanes_c, cl = t % lanes_c;
+  for (int c0 = 0; c0 < C; c0 += lanes_c) {
+    const int c = c0 + cl;
+    float acc = 0.f;
+    if (grp < groups && c < C)
+      for (int p = grp; p < D; p += groups) acc += h[((long long)img * D + p) * C + c];
+    part[t] = acc;
+    __syncthreads();
+    if (t < lanes_c && c0 + t < C) {
+      float v = 0.f;
+      for (int q = 0; q < groups; ++q) v += part[q * lanes_c + t];
+      g[(long long)img * C + c0 + t] = v / (float)D;
+    }
+    __syncthreads();
+  }
+}
+
+hipError_t launch_gap(hipStream_t s, const float* h, int images, int D, int C, float* g) {
+  k_gap<<<dim3(images), dim3(256), 0, s>>>(h, D, C, g);
+  return hipGetLastError();
+}
+
+// G[(img*O + o), p, c] = Wd[o, c] / D * dphi[img, p, c]
+__global__ void k_conv_seed(const float* __restrict__ Wd, const float* __restrict__ dphi, int images,
+                            int O, int D, int C, float* __restrict__ G) {
+  const long long total = (long long)images * O * D * C;
+  const float inv = 1.0f / (float)D;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int c = (int)(i % C);
+    const long long rest = i / C;
+    const int p = (int)(rest % D);
+    const long long io = rest / D;
+    const int o = (int)(io % O);
+    const long long img = io / O;
+    G[i] = Wd[(long long)o * C + c] * inv * dphi[(img * D + p) * C + c];
+  }
+}
+
+hipError_t launch_conv_seed(hipStream_t s, const float* Wd, const float* dphi, int images, int O, int D,
+                            int C, float* G) {
+  const long long total = (long long)images * O * D * C;
+  const int blocks = (int)std::min<long long>((total + 255) / 256, 256 * 128);
+  k_conv_seed<<<dim3(blocks), dim3(256), 0, s>>>(Wd, dphi, images, O, D, C, G);
+  return hipGetLastError();
+}
+
+// Kt[ci, kh, kw, co] = K[co, 2 - kh, 2 - kw, ci]
+__global__ void k_conv_flip(const float* __restrict__ K, int Cout, int Cin, float* __restrict__ Kt) {
+  const int total = Cout * 9 * Cin;
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int co = i % Cout;
+    const int rest = i / Cout;
+    const int tap = rest % 9, ci = rest / 9;
+    const int kh = tap / 3, kw = tap % 3;
+    Kt[i] = K[((co * 3 + (2 - kh)) * 3 + (2 - kw)) * Cin + ci];
+  }
+}
+
+hipError_t launch_conv_flip(hipStream_t s, const float* K, int Cout, int Cin, float* Kt) {
+  const int total = Cout * 9 * Cin;
+  k_conv_flip<<<dim3(cdiv(total, 256)), dim3(256), 0, s>>>(K, Cout, Cin, Kt);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------ backward
+// out[(img*O+o), p, ci] = (sum_k patch(G)[.., p, k] Kt[ci, k]) * dphi[img, p, ci]
+template <class Cfg>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_conv_bwd(LoadPatchesKInner la, LoadKInner lb, const float* __restrict__ dphi, int R, int N,
+           FastDiv fOD, int D, int O, float* __restrict__ out, int tiles_n) {
+  extern __shared__ float smem[];
+  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  f32x16 acc[Cfg::FM][Cfg::FN];
+  zero_acc<Cfg>(acc);
+  gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
+  for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, float v) {
+    if (r < R && c < N) {
+      const int img = (int)fOD.div(r);            // r = (img*O + o)*D + p
+      const int p = r - (r / D) * D;
+      out[(long long)r * N + c] = v * dphi[((long long)img * D + p) * N + c];
+    }
+  });
+}
+
+hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
+                           const float* Kt, int Cin, const float* dphi, float* out) {
+  using Cfg = CfgConv;
+  const int D = H * W;
+  LoadPatchesKInner la = patches_kinner(G, images * O, H, W, Cg);
+  LoadKInner lb{Kt, Cin, 9 * Cg, 9 * Cg, aligned16(Kt) && (9 * Cg) % 4 == 0};
+  const int R = images * O * D;
+  const int tn = cdiv(Cin, Cfg::BN), tm = cdiv(R, Cfg::BM);
+  hipError_t e = set_smem<Cfg, LoadPatchesKInner, LoadKInner>((const void*)k_conv_bwd<Cfg>);
+  if (e != hipSuccess) return e;
+  k_conv_bwd<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LoadPatchesKInner, LoadKInner>(), s>>>(
+      la, lb, dphi, R, Cin, FastDiv((uint32_t)(O * D)), D, O, out, tn);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------ weight-space cotangent
+// For sample s = blockIdx.y:  J[s*O + o][off + c*KC + k] = sum_p G[s,o,p,c] patch[s,p,k]
+template <class Cfg>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, int H, int W, int C,
+             int Cin, FastDiv fC, FastDiv fW, FastDiv fCin, float* __restrict__ J, long long ldJ,
+             long long off, int tiles_n) {
+  extern __shared__ float smem[];
+  const int s = blockIdx.y;
+  const int D = H * W;
+  const int KC = 9 * Cin;
+  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  LoadCotangentKOuter la;
+  la.g = G + (long long)s * O * D * C;
+  la.rows = O * C;
+  la.K = D;
+  la.C = C;
+  la.D = D;
+  la.fC = fC;
+  la.vec = (C % 4 == 0) && ((reinterpret_cast<uintptr_t>(G) & 15) == 0);
+  LoadPatchesKOuter lb;
+  lb.x = h + (long long)s * D * Cin;
+  lb.rows = KC;
+  lb.K = D;
+  lb.H = H;
+  lb.W = W;
+  lb.C = Cin;
+  lb.fW = fW;
+  lb.fC = fCin;
+  lb.vec = (Cin % 4 == 0) && ((reinterpret_cast<uintptr_t>(h) & 15) == 0);
+  f32x16 acc[Cfg::FM][Cfg::FN];
+  zero_acc<Cfg>(acc);
+  gemm_mainloop<Cfg>(la, lb, m0, n0, 0, D, smem, acc);
+  const int R = O * C;
+  for_each_acc<Cfg>(acc, m0, n0, [&](int r, int k, float v) {
+    if (r < R && k < KC) {
+      const int o = (int)fC.div(r), c = r - o * C;
+      J[((long long)s * O + o) * ldJ + off + (long long)c * KC + k] = v;
+    }
+  });
+}
+
+hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
+                             int W, int C, int Cin, float* J, long long ldJ, long long off) {
+  using Cfg = CfgConv;
+  const int tn = cdiv(9 * Cin, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
+  hipError_t e = set_smem<Cfg, LoadCotangentKOuter, LoadPatchesKOuter>((const void*)k_conv_wgrad<Cfg>);
+  if (e != hipSuccess) return e;
+  k_conv_wgrad<Cfg><<<dim3(tm * tn, images), dim3(Cfg::THREADS),
+                      gemm_smem_bytes<Cfg, LoadCotangentKOuter, LoadPatchesKOuter>(), s>>>(
+      G, h, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
+      ldJ, off, tn);
+  return hipGetLastError();
+}
+
+// ------------------------------------------------------------------------------ split-K J1 J2^T
+__device__ __forceinline__ void tri_index_c(int t, int nt, int& tm, int& tn) {
+  int r = 0, base = 0;
+  while (base + (nt - r) <= t) {
+    base += nt - r;
+    ++r;
+  }
+  tm = r;
+  tn = r + (t - base);
+}
+
+// part[z][r1][r2] = sum_{k in chunk z} J1[r1, k] J2[r2, k]
+template <class Cfg>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_ntk_splitk(LoadKInner la, LoadKInner lb, int chunk, int symmetric, float* __restrict__ part,
+             int tiles_n) {
+  extern __shared__ float smem[];
+  const int z = blockIdx.y;
+  int tm, tn;
+  if (symmetric) {
+    tri_index_c(blockIdx.x, tiles_n, tm, tn);
+  } else {
+    tm = blockIdx.x / tiles_n;
+    tn = blockIdx.x % tiles_n;
+  }
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  const int k0 = z * chunk;
+  const int k1 = min(la.K, k0 + chunk);
+  f32x16 acc[Cfg::FM][Cfg::FN];
+  zero_acc<Cfg>(acc);
+  gemm_mainloop<Cfg>(la, lb, m0, n0, k0, k1, smem, acc);
+  const int R1 = la.rows, R2 = lb.rows;
+  float* P = part + (long long)z * R1 * R2;
+  for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, float v) {
+    if (r < R1 && c < R2) P[(long long)r * R2 + c] = v;
+  });
+}
+
+// theta[n1][n2][o1][o2] = sum_z part[z][r1][r2] + (o1 == o2) gram[n1, n2]
+__global__ void k_ntk_reduce(const float* __restrict__ part, int splits, int N1, int N2, int O,
+                             int symmetric, int tile, const float* __restrict__ gram,
+                             float* __restrict__ theta) {
+  const int R1 = N1 * O, R2 = N2 * O;
+  const long long total = (long long)R1 * R2;
+  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
+       i += (long long)gridDim.x * blockDim.x) {
+    const int r1 = (int)(i / R2), r2 = (int)(i - (long long)r1 * R2);
+    long long src = i;
+    if (symmetric && (r1 / tile) > (r2 / tile)) src = (long long)r2 * R2 + r1;
+    float v = 0.f;
+    for (int z = 0; z < splits; ++z) v += part[(long long)z * total + src];
+    const int n1 = r1 / O, o1 = r1 - n1 * O, n2 = r2 / O, o2 = r2 - n2 * O;
+    if (o1 == o2) v += gram[(long long)n1 * N2 + n2];
+    theta[(((long long)n1 * N2 + n2) * O + o1) * O + o2] = v;
+  }
+}
+
+int splitk_tile() { return CfgSplitK::BM; }
+
+int splitk_plan(int R1, int R2, long long K, int symmetric, long long part_capacity, int* chunk_out) {
+  using Cfg = CfgSplitK;
+  const int tm = cdiv(R1, Cfg::BM), tn = cdiv(R2, Cfg::BN);
+  const int tiles = symmetric ? tn * (tn + 1) / 2 : tm * tn;
+  // aim for about 4 workgroups per compute unit, with chunks that are whole K tiles, and
+  // never more partial [R1, R2] products than the workspace holds
+  long long want = std::min<long long>(1024 / std::max(tiles, 1), cdiv(K, 256));
+  want = std::min<long long>(want, part_capacity / ((long long)R1 * R2));
+  int splits = (int)std::max<long long>(1, want);
+  long long chunk = (K + splits - 1) / splits;
+  chunk = ((chunk + Cfg::BK - 1) / Cfg::BK) * Cfg::BK;
+  splits = (int)((K + chunk - 1) / chunk);
+  *chunk_out = (int)chunk;
+  return splits;
+}
+
+hipError_t launch_ntk_splitk(hipStream_t s, const float* J1, const float* J2, int R1, int R2,
+                             long long K, int symmetric, int chunk, int splits, float* part) {
+  using Cfg = CfgSplitK;
+  LoadKInner la{J1, R1, (int)K, K, aligned16(J1) && K % 4 == 0};
+  LoadKInner lb{J2, R2, (int)K, K, aligned16(J2) && K % 4 == 0};
+  const int tm = cdiv(R1, Cfg::BM), tn = cdiv(R2, Cfg::BN);
+  const int tiles = symmetric ? tn * (tn + 1) / 2 : tm * tn;
+  hipError_t e = set_smem<Cfg, LoadKInner, LoadKInner>((const void*)k_ntk_splitk<Cfg>);
+  if (e != hipSuccess) return e;
+  k_ntk_splitk<Cfg><<<dim3(tiles, splits), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LoadKInner, LoadKInner>(), s>>>(
+      la, lb, chunk, symmetric, part, tn);
+  return hipGetLastError();
+}
+
+hipError_t launch_ntk_reduce(hipStream_t s, const float* part, int splits, int N1, int N2, int O,
+                             int symmetric, const float* gram, float* theta) {
+  const long long total = (long long)N1 * O * N2 * O;
+  const int blocks = (int)std::min<long long>((total + 255) / 256, 256 * 64);
+  k_ntk_reduce<<<dim3(blocks), dim3(256), 0, s>>>(part, splits, N1, N2, O, symmetric, CfgSplitK::BM,
+                                                  gram, theta);
+  return hipGetLastError();
+}
+
+}  // namespace ntk

@@ -1,0 +1,35 @@
+// launch_conv.hpp -- host-side launchers of the convolutional NTK kernels (internal).
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include "launch.hpp"
+
+namespace ntk {
+
+// hn/dphi [images, H, W, Cout] = act / act' of the SAME 3x3 convolution of x [images, H, W, Cin]
+// with K [Cout, 3, 3, Cin] (fp64 accumulation).
+hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int W, int Cin,
+                           const float* K, int Cout, int act, float* hn, float* dphi);
+// g [images, C] = mean over the D pixels of h [images, D, C].
+hipError_t launch_gap(hipStream_t s, const float* h, int images, int D, int C, float* g);
+// G [images*O, D, C] = Wd[o, c] / D * dphi[img, p, c].
+hipError_t launch_conv_seed(hipStream_t s, const float* Wd, const float* dphi, int images, int O,
+                            int D, int C, float* G);
+// Kt [Cin, 3, 3, Cout] = K [Cout, 2-kh, 2-kw, Cin]  (the kernel of the transposed convolution).
+hipError_t launch_conv_flip(hipStream_t s, const float* K, int Cout, int Cin, float* Kt);
+// out [images*O, D, Cin] = conv3x3(G [images*O, H, W, Cg], Kt [Cin, 3, 3, Cg]) * dphi [images, D, Cin].
+hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
+                           const float* Kt, int Cin, const float* dphi, float* out);
+// J[(s*O + o), off + c*9*Cin + k] = sum_p G[s, o, p, c] patch(h)[s, p, k] for every sample s.
+hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
+                             int W, int C, int Cin, float* J, long long ldJ, long long off);
+// Deterministic split-K product J1 J2^T: plan, partial products, reduction into theta.
+int splitk_tile();
+// splits * R1 * R2 <= part_capacity (floats) always holds for the returned plan.
+int splitk_plan(int R1, int R2, long long K, int symmetric, long long part_capacity, int* chunk_out);
+hipError_t launch_ntk_splitk(hipStream_t s, const float* J1, const float* J2, int R1, int R2,
+                             long long K, int symmetric, int chunk, int splits, float* part);
+hipError_t launch_ntk_reduce(hipStream_t s, const float* part, int splits, int N1, int N2, int O,
+                             int symmetric, const float* gram, float* theta);
+
+}  // namespace ntk

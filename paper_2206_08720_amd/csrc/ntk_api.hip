@@ -16,6 +16,7 @@
 
 #include "../../include/ntk.h"
 #include "launch.hpp"
+#include "launch_conv.hpp"
 
 namespace ntk {
 
@@ -102,6 +103,17 @@ struct ntk_handle {
   std::vector<size_t> off_Wt;     // Wt_l,   l = 1..L-1    [d_l, d_{l+1}]
   std::vector<size_t> off_gram;   // gram_l, l = 0..L      [max_n1*max_n2]
   std::vector<int> param_index;   // first parameter slot of dense layer l
+
+  // ---- convolutional plan: conv layers 0..nc-1, GAP, dense readout
+  int nc = 0, H = 0, W = 0, D = 0;
+  std::vector<int> ch;            // c_0 .. c_nc (channels)
+  std::vector<size_t> off_ch;     // conv layer inputs h_l, l = 0..nc   [Mmax, D, c_l]
+  std::vector<size_t> off_cdphi;  // act'(z_l), l = 0..nc-1             [Mmax, D, c_{l+1}]
+  std::vector<size_t> off_Kt;     // flipped kernels, l = 1..nc-1       [c_l, 9, c_{l+1}]
+  std::vector<long long> joff;    // column offset of layer l in J
+  long long Ktot = 0;             // columns of J = sum_l 9 c_l c_{l+1}
+  size_t off_g = 0, off_Gping = 0, off_Gpong = 0, off_J = 0, off_gram_r = 0, off_part = 0;
+  long long part_capacity = 0;    // floats of the split-K partial buffer
 };
 
 static thread_local std::string g_init_error;
@@ -213,6 +225,51 @@ static void plan_fcn(ntk_handle* h) {
   }
 }
 
+static void plan_cnn(ntk_handle* h) {
+  const int n = (int)h->layers.size();
+  h->nc = n - 2;
+  h->H = h->in_h;
+  h->W = h->in_w;
+  h->D = h->H * h->W;
+  const int nc = h->nc;
+  h->ch.resize(nc + 1);
+  h->ch[0] = h->in_c;
+  for (int l = 0; l < nc; ++l) h->ch[l + 1] = h->layers[l].out;
+  const size_t Mmax = (size_t)h->max_n1 + h->max_n2;
+  const size_t O = h->out_dim, D = h->D;
+  size_t off = 0;
+  auto take = [&](size_t floats) {
+    size_t o = off;
+    off = align_up(off + floats * 4);
+    return o;
+  };
+  int cmax = 0;
+  for (int l = 1; l <= nc; ++l) cmax = std::max(cmax, h->ch[l]);
+  h->off_ch.assign(nc + 1, 0);
+  h->off_cdphi.assign(nc, 0);
+  h->off_Kt.assign(nc, 0);
+  h->joff.assign(nc, 0);
+  for (int l = 0; l <= nc; ++l) h->off_ch[l] = take(Mmax * D * h->ch[l]);
+  for (int l = 0; l < nc; ++l) h->off_cdphi[l] = take(Mmax * D * h->ch[l + 1]);
+  for (int l = 1; l < nc; ++l) h->off_Kt[l] = take((size_t)9 * h->ch[l] * h->ch[l + 1]);
+  h->off_g = take(Mmax * h->ch[nc]);
+  h->off_Gping = take(Mmax * O * D * cmax);
+  h->off_Gpong = take(Mmax * O * D * cmax);
+  long long kt = 0;
+  for (int l = 0; l < nc; ++l) {
+    h->joff[l] = kt;
+    kt += 9LL * h->ch[l] * h->ch[l + 1];
+  }
+  h->Ktot = kt;
+  h->off_J = take(Mmax * O * (size_t)kt);
+  h->off_gram_r = take((size_t)h->max_n1 * h->max_n2);
+  const int T = splitk_tile();
+  const size_t tiles_max = (size_t)((h->max_n1 * O + T - 1) / T) * ((h->max_n2 * O + T - 1) / T);
+  h->part_capacity = (long long)(1024 + tiles_max) * T * T;   // >= R1max * R2max
+  h->off_part = take((size_t)h->part_capacity);
+  h->ws_bytes = off;
+}
+
 // ------------------------------------------------------------------------------ C ABI
 extern "C" int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, void* hip_stream,
                         ntk_handle** out) {
@@ -233,11 +290,10 @@ extern "C" int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, voi
   h->max_n1 = max_n1;
   h->max_n2 = max_n2;
   h->stream = (hipStream_t)hip_stream;
-  if (h->cnn) {
-    delete h;
-    return fail(nullptr, NTK_E_UNSUPPORTED, "convolutional models are not available in this build");
-  }
-  plan_fcn(h);
+  if (h->cnn)
+    plan_cnn(h);
+  else
+    plan_fcn(h);
   hipError_t e = hipGetDevice(&h->device);
   if (e != hipSuccess) {
     delete h;
@@ -345,6 +401,102 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   return NTK_OK;
 }
 
+static int compute_cnn(ntk_handle* h, const float* const* params, const float* X1, int n1,
+                       const float* X2, int n2, float* theta) {
+  const int nc = h->nc, O = h->out_dim, H = h->H, W = h->W, D = h->D;
+  const bool sym = h->opt_symmetric && X1 == X2 && n1 == n2;
+  const int M = sym ? n1 : n1 + n2;
+  hipStream_t s = h->stream;
+  Profiler* P = &h->prof;
+  auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
+  for (int l = 0; l <= nc; ++l)
+    if (!params[l]) return fail(h, NTK_E_ARG, "null weight pointer");
+  if (h->opt_conv_order == NTK_CONV_ORDER_INSIDE_OUT)
+    return fail(h, NTK_E_UNSUPPORTED, "the inside-out convolution order is not available in this build");
+  hipError_t e;
+  const size_t img_floats = (size_t)D * h->ch[0];
+  const float* h0 = X1;
+  if (!sym) {
+    prof_begin(P, s, KC_COPY);
+    e = hipMemcpyAsync(F(h->off_ch[0]), X1, sizeof(float) * n1 * img_floats, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(F(h->off_ch[0]) + n1 * img_floats, X2, sizeof(float) * n2 * img_floats,
+                         hipMemcpyDeviceToDevice, s);
+    prof_end(P, s, KC_COPY);
+    if (e != hipSuccess) return hip_fail(h, e, "stacking X1/X2");
+    h0 = F(h->off_ch[0]);
+  }
+  auto hptr = [&](int l) -> const float* { return l == 0 ? h0 : F(h->off_ch[l]); };
+  // 1. forward pass keeping every conv layer input, then global average pooling
+  for (int l = 0; l < nc; ++l) {
+    prof_begin(P, s, KC_CONV_FWD);
+    e = launch_conv_fwd(s, hptr(l), M, H, W, h->ch[l], params[l], h->ch[l + 1], h->layers[l].act,
+                        F(h->off_ch[l + 1]), F(h->off_cdphi[l]));
+    prof_end(P, s, KC_CONV_FWD);
+    if (e != hipSuccess) return hip_fail(h, e, "conv forward");
+  }
+  const int C = h->ch[nc];
+  prof_begin(P, s, KC_GAP);
+  e = launch_gap(s, F(h->off_ch[nc]), M, D, C, F(h->off_g));
+  prof_end(P, s, KC_GAP);
+  if (e != hipSuccess) return hip_fail(h, e, "global average pooling");
+  // readout summand: (g1 . g2) delta_{o1 o2}
+  GramBatch gb{};
+  gb.count = 1;
+  gb.h1[0] = F(h->off_g);
+  gb.h2[0] = sym ? F(h->off_g) : F(h->off_g) + (size_t)n1 * C;
+  gb.out[0] = F(h->off_gram_r);
+  gb.K[0] = C;
+  gb.beta[0] = 0.f;
+  prof_begin(P, s, KC_GRAM);
+  e = launch_gram(s, gb, n1, n2);
+  prof_end(P, s, KC_GRAM);
+  if (e != hipSuccess) return hip_fail(h, e, "gram");
+  // 2. cotangents of every conv pre-activation for all O outputs, and per layer the
+  //    weight-space cotangent J_l = sum_p G_l (x) patch_l (outside-in order)
+  for (int l = 1; l < nc; ++l) {
+    prof_begin(P, s, KC_TRANSPOSE);
+    e = launch_conv_flip(s, params[l], h->ch[l + 1], h->ch[l], F(h->off_Kt[l]));
+    prof_end(P, s, KC_TRANSPOSE);
+    if (e != hipSuccess) return hip_fail(h, e, "kernel flip");
+  }
+  float* Gcur = F(h->off_Gping);
+  float* Gnext = F(h->off_Gpong);
+  prof_begin(P, s, KC_CONV_SEED);
+  e = launch_conv_seed(s, params[nc], F(h->off_cdphi[nc - 1]), M, O, D, C, Gcur);
+  prof_end(P, s, KC_CONV_SEED);
+  if (e != hipSuccess) return hip_fail(h, e, "conv seed");
+  float* J = F(h->off_J);
+  for (int l = nc - 1; l >= 0; --l) {
+    prof_begin(P, s, KC_CONV_WGRAD);
+    e = launch_conv_wgrad(s, Gcur, hptr(l), M, O, H, W, h->ch[l + 1], h->ch[l], J, h->Ktot, h->joff[l]);
+    prof_end(P, s, KC_CONV_WGRAD);
+    if (e != hipSuccess) return hip_fail(h, e, "conv weight-space cotangent");
+    if (l >= 1) {
+      prof_begin(P, s, KC_CONV_BWD);
+      e = launch_conv_bwd(s, Gcur, M, O, H, W, h->ch[l + 1], F(h->off_Kt[l]), h->ch[l],
+                          F(h->off_cdphi[l - 1]), Gnext);
+      prof_end(P, s, KC_CONV_BWD);
+      if (e != hipSuccess) return hip_fail(h, e, "conv backward");
+      std::swap(Gcur, Gnext);
+    }
+  }
+  // 3. Theta = J1 J2^T (deterministic split over K) + readout summand
+  const int R1 = n1 * O, R2 = n2 * O;
+  int chunk = 0;
+  const int splits = splitk_plan(R1, R2, h->Ktot, sym ? 1 : 0, h->part_capacity, &chunk);
+  const float* J2 = sym ? J : J + (size_t)n1 * O * h->Ktot;
+  prof_begin(P, s, KC_NTK_SPLITK);
+  e = launch_ntk_splitk(s, J, J2, R1, R2, h->Ktot, sym ? 1 : 0, chunk, splits, F(h->off_part));
+  prof_end(P, s, KC_NTK_SPLITK);
+  if (e != hipSuccess) return hip_fail(h, e, "split-K contraction");
+  prof_begin(P, s, KC_NTK_REDUCE);
+  e = launch_ntk_reduce(s, F(h->off_part), splits, n1, n2, O, sym ? 1 : 0, F(h->off_gram_r), theta);
+  prof_end(P, s, KC_NTK_REDUCE);
+  if (e != hipSuccess) return hip_fail(h, e, "split-K reduction");
+  return NTK_OK;
+}
+
 extern "C" int ntk_compute(ntk_handle* h, const float* const* params, const float* X1, int n1,
                            const float* X2, int n2, float* theta) {
   if (!h) return fail(nullptr, NTK_E_ARG, "handle is NULL");
@@ -352,8 +504,8 @@ extern "C" int ntk_compute(ntk_handle* h, const float* const* params, const floa
   if (n1 <= 0 || n2 <= 0) return fail(h, NTK_E_ARG, "n1 and n2 must be positive");
   if (n1 > h->max_n1 || n2 > h->max_n2)
     return fail(h, NTK_E_ARG, "n1/n2 exceed the max_n1/max_n2 given to ntk_init");
-  if (h->cnn) return fail(h, NTK_E_UNSUPPORTED, "convolutional models are not available in this build");
   h->err.clear();
+  if (h->cnn) return compute_cnn(h, params, X1, n1, X2, n2, theta);
   return compute_fcn(h, params, X1, n1, X2, n2, theta);
 }
 

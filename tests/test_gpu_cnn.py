@@ -1,0 +1,92 @@
+"""GPU parity of the convolutional path against the fp64 oracle (needs an MI355X).
+
+The references are the Jacobian-contraction oracle with float32 layer storage
+(see tests/test_gpu_fcn.py); the 4-layer 64-channel CNN on 32x32x3 inputs is
+compared in full.
+"""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from tests.gpu_helpers import TOL, errors, gpu_ntk, report
+
+pytestmark = pytest.mark.gpu
+S = "fp32"
+
+
+def _vs_jc(name, spec, params, X1, X2, symmetric=True):
+    got = gpu_ntk(spec, params, X1, X2, symmetric=symmetric)
+    print(f"[parity] {name}: GPU done", flush=True)
+    ref, d1, d2 = oracle.ntk_jc_with_norms(spec, params, X1, X2, layer_storage=S)
+    cs, nw = errors(got, ref, d1, d2)
+    report(name, cs, nw)
+    assert got.shape == ref.shape
+    assert cs <= TOL and nw <= TOL
+    return got
+
+
+@pytest.mark.parametrize("symmetric", [True, False])
+def test_hand_worked_cnn_golden_on_gpu(golden_dir, symmetric):
+    d = json.load(open(os.path.join(golden_dir, "cnn_hand_1x2.json")))
+    params = [np.array(p, dtype=np.float32) for p in d["params"]]
+    X = np.array(d["X"], dtype=np.float32)
+    got = gpu_ntk(d["spec"], params, X, X, symmetric=symmetric)
+    np.testing.assert_allclose(got, np.array(d["theta"]), rtol=1e-6, atol=1e-5)
+
+
+def test_cnn4_c64_32x32_full():
+    spec, params, X1, X2 = wl.make_workload("cnn4_c64_32x32")
+    _vs_jc("cnn4_c64_32x32", spec, params, X1, X2)
+
+
+CASES = [
+    # label, spec, n1, n2
+    ("one conv layer, 1x1 images", wl.cnn_spec("c1", (1, 1), 3, [8], 4), 5, 6),
+    ("channels not multiple of 4, erf", wl.cnn_spec("c2", (5, 3), 5, [6, 10], 3, act="erf"), 5, 7),
+    ("ragged 7x9, 3 layers", wl.cnn_spec("c3", (7, 9), 3, [16, 12, 20], 10), 9, 4),
+    ("O=1, n1=n2=1", wl.cnn_spec("c4", (6, 6), 4, [8, 8], 1), 1, 1),
+    ("tile-spanning rows, 8x8", wl.cnn_spec("c5", (8, 8), 3, [32, 32], 10), 23, 17),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_cnn_edge_shapes(case):
+    label, spec, n1, n2 = case
+    params = wl.make_params(spec, 300 + n1, "2/fan_in")
+    X1 = wl.make_inputs(spec, n1, 310 + n1)
+    X2 = wl.make_inputs(spec, n2, 320 + n2)
+    _vs_jc(label, spec, params, X1, X2)
+
+
+@pytest.mark.parametrize("symmetric", [True, False])
+def test_cnn_aliased_inputs(symmetric):
+    spec = wl.cnn_spec("alias", (6, 5), 3, [16, 16], 10)
+    params = wl.make_params(spec, 401, "2/fan_in")
+    X = wl.make_inputs(spec, 30, 402)
+    got = _vs_jc(f"cnn aliased sym={symmetric}", spec, params, X, X, symmetric=symmetric)
+    N, O = got.shape[0], got.shape[2]
+    M = got.transpose(0, 2, 1, 3).reshape(N * O, N * O)
+    np.testing.assert_allclose(M, M.T, rtol=0, atol=1e-5 * np.abs(M).max())
+
+
+def test_cnn_determinism_and_reuse():
+    from paper_2206_08720_amd.ntk import NTK
+    spec = wl.cnn_spec("det", (8, 8), 3, [16, 16], 5)
+    params = wl.make_params(spec, 501, "2/fan_in")
+    X1 = wl.make_inputs(spec, 12, 502)
+    X2 = wl.make_inputs(spec, 9, 503)
+    h = NTK(spec, 16, 16)
+    try:
+        a = gpu_ntk(spec, params, X1, X2, handle=h)
+        b = gpu_ntk(spec, params, X1, X2, handle=h)
+        assert np.array_equal(a, b), "two calls must be bit-identical"
+        c = gpu_ntk(spec, params, X1[:3], X2[:2], handle=h)
+        ref, d1, d2 = oracle.ntk_jc_with_norms(spec, params, X1[:3], X2[:2], layer_storage=S)
+        cs, nw = errors(c, ref, d1, d2)
+        assert cs <= TOL and nw <= TOL
+    finally:
+        h.close()
