@@ -50,6 +50,30 @@ def parse():
     return ap.parse_args()
 
 
+def sources_sha16():
+    import glob
+    import hashlib
+    csrc = os.path.join(ROOT, "paper_2206_08720_amd", "csrc")
+    files = sorted(glob.glob(os.path.join(csrc, "*.hip"))) + sorted(glob.glob(os.path.join(csrc, "*.hpp")))
+    h = hashlib.sha256()
+    for f in files:
+        h.update(open(f, "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(name, kernel):
+    """HBM bytes per launch from the committed FETCH_SIZE/WRITE_SIZE record, or None when the
+    record is for another kernel/workload or the kernel sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"{name}_traffic.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    if rec.get("kernel") != kernel or rec.get("sources_sha256_16") != sources_sha16():
+        return None
+    return (rec["fetch_size_kib_per_launch"] * rec["fetch_scale"]
+            + rec["write_size_kib_per_launch"] * rec["write_scale"]) * 1024.0
+
+
 def cpu_baseline(name, n):
     import numpy as np
     import oracle
@@ -146,7 +170,7 @@ def main():
     achieved = flop_per_launch / (avg_ms * 1e-3) / 1e12
     roofline = {"kernel": dom, "bound": "mfma", "achieved": achieved,
                 "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": achieved / FP32_MFMA_PEAK_TFLOPS, "traffic": None,
+                "frac": achieved / FP32_MFMA_PEAK_TFLOPS, "traffic": measured_traffic(name, dom),
                 "flop_per_launch": flop_per_launch, "avg_launch_ms": avg_ms}
 
     res = {

@@ -1,0 +1,49 @@
+"""The analytic operation counter against the paper's cost formulas (CPU only).
+
+The paper counts a (M,K)x(K,P) product as M*K*P multiply-adds (appendix
+"Experimental Details"); the counter reports 2*M*K*P flops.  The FCN terms are
+those of Section 4.1 ("FCN SD cost": N O L W^2 + N^2 O^2 L W + N^2 O^3) and the CNN
+terms those of the appendix "CNN NTK Complexity" / table "complexities_cnn".
+"""
+import pytest
+
+import workloads as wl
+from paper_2206_08720_amd.flops import cnn_flops, fcn_flops, ntk_entries
+
+
+def test_fcn_terms_match_section_4_1():
+    N, O, L, W = 16, 7, 5, 96
+    spec = wl.fcn_spec("f", W, [W] * L, O)            # input size W as in Section 4.1
+    f = fcn_flops(spec, N, N)
+    # contraction: the N^2 O^2 L W term (one O x O product per layer and pair)
+    assert f["contraction"] == 2 * N * N * O * O * L * W
+    # backward: the (N1 + N2) O (L - 1) W^2 cotangent products (the N O L W^2 term)
+    assert f["backward"] == 2 * (2 * N) * O * (L - 1) * W * W
+    # forward: (N1 + N2) L W^2 (no readout: f itself is not needed)
+    assert f["forward"] == 2 * (2 * N) * L * W * W
+    assert f["gram"] == 2 * N * N * (L + 1) * W
+    sym = fcn_flops(spec, N, N, symmetric=True)
+    assert sym["forward"] == f["forward"] / 2 and sym["backward"] == f["backward"] / 2
+
+
+def test_workload_totals():
+    spec, _, X1, X2 = wl.make_workload("relu_mlp_d8_w2048")
+    f = fcn_flops(spec, 512, 512)
+    assert f["total"] == pytest.approx(1.5435e12, rel=1e-4)
+    assert f["contraction"] == pytest.approx(8.59e11, rel=1e-3)
+    assert ntk_entries(spec, 512, 512) == 512 * 512 * 100
+    spec, _, _, _ = wl.make_workload("cnn4_c64_32x32")
+    c = cnn_flops(spec, 64, 64)
+    assert c["total"] == pytest.approx(7.06e11, rel=1e-3)
+
+
+def test_cnn_terms_match_complexities_cnn():
+    N, O, D, W, Fs = 4, 5, 36, 8, 9
+    spec = wl.cnn_spec("c", (6, 6), W, [W, W], O)
+    oi = cnn_flops(spec, N, N, order="outside_in")
+    io = cnn_flops(spec, N, N, order="inside_out")
+    # outside-in: N^2 O^2 F W^2 per layer for J1 J2^T, plus N O D F W^2 to form J
+    assert oi["contraction"] == 2 * (N * O) * (N * O) * 2 * Fs * W * W
+    assert oi["wgrad"] == 2 * (2 * N) * O * W * Fs * W * D * 2
+    # inside-out: N^2 (D^2 F W + O D^2 W + O^2 D W) per layer
+    assert io["contraction"] == 2 * 2 * N * N * (D * D * Fs * W + O * D * D * W + O * O * D * W)
