@@ -394,9 +394,10 @@ k_ntk_splitk(LoadKInner la, LoadKInner lb, int chunk, int symmetric, float* __re
   });
 }
 
-// theta[n1][n2][o1][o2] = sum_z part[z][r1][r2] + (o1 == o2) gram[n1, n2]
+// theta[n1][n2][o1][o2] = sum_z part[z][r1][r2] + (o1 == o2) gram[n1, n2], or, with
+// accumulate, theta += sum_z part[z][r1][r2] (the readout summand is then already in theta).
 __global__ void k_ntk_reduce(const float* __restrict__ part, int splits, int N1, int N2, int O,
-                             int symmetric, int tile, const float* __restrict__ gram,
+                             int symmetric, int tile, const float* __restrict__ gram, int accumulate,
                              float* __restrict__ theta) {
   const int R1 = N1 * O, R2 = N2 * O;
   const long long total = (long long)R1 * R2;
@@ -408,8 +409,12 @@ __global__ void k_ntk_reduce(const float* __restrict__ part, int splits, int N1,
     float v = 0.f;
     for (int z = 0; z < splits; ++z) v += part[(long long)z * total + src];
     const int n1 = r1 / O, o1 = r1 - n1 * O, n2 = r2 / O, o2 = r2 - n2 * O;
-    if (o1 == o2) v += gram[(long long)n1 * N2 + n2];
-    theta[(((long long)n1 * N2 + n2) * O + o1) * O + o2] = v;
+    float* dst = theta + (((long long)n1 * N2 + n2) * O + o1) * O + o2;
+    if (accumulate)
+      v += *dst;
+    else if (o1 == o2)
+      v += gram[(long long)n1 * N2 + n2];
+    *dst = v;
   }
 }
 
@@ -432,10 +437,11 @@ int splitk_plan(int R1, int R2, long long K, int symmetric, long long part_capac
 }
 
 hipError_t launch_ntk_splitk(hipStream_t s, const float* J1, const float* J2, int R1, int R2,
-                             long long K, int symmetric, int chunk, int splits, float* part) {
+                             long long K, long long ld, int symmetric, int chunk, int splits,
+                             float* part) {
   using Cfg = CfgSplitK;
-  LoadKInner la{J1, R1, (int)K, K, aligned16(J1) && K % 4 == 0};
-  LoadKInner lb{J2, R2, (int)K, K, aligned16(J2) && K % 4 == 0};
+  LoadKInner la{J1, R1, (int)K, ld, aligned16(J1) && ld % 4 == 0};
+  LoadKInner lb{J2, R2, (int)K, ld, aligned16(J2) && ld % 4 == 0};
   const int tm = cdiv(R1, Cfg::BM), tn = cdiv(R2, Cfg::BN);
   const int tiles = symmetric ? tn * (tn + 1) / 2 : tm * tn;
   hipError_t e = set_smem<Cfg, LoadKInner, LoadKInner>((const void*)k_ntk_splitk<Cfg>);
@@ -446,11 +452,152 @@ hipError_t launch_ntk_splitk(hipStream_t s, const float* J1, const float* J2, in
 }
 
 hipError_t launch_ntk_reduce(hipStream_t s, const float* part, int splits, int N1, int N2, int O,
-                             int symmetric, const float* gram, float* theta) {
+                             int symmetric, const float* gram, int accumulate, float* theta) {
   const long long total = (long long)N1 * O * N2 * O;
   const int blocks = (int)std::min<long long>((total + 255) / 256, 256 * 64);
   k_ntk_reduce<<<dim3(blocks), dim3(256), 0, s>>>(part, splits, N1, N2, O, symmetric, CfgSplitK::BM,
-                                                  gram, theta);
+                                                  gram, accumulate, theta);
+  return hipGetLastError();
+}
+
+}  // namespace ntk
+
+namespace ntk {
+
+// ------------------------------------------------------------------------------ inside-out order
+// For one input pair (n1, n2) = blockIdx.x and every conv layer marked inside-out:
+//   PK[p1, p2] = patch1[p1] . patch2[p2]   (the inner Jacobian product; built from the pixel
+//                Gram H[q1, q2] = h1[q1] . h2[q2] summed over the 9 taps shifted together)
+//   T[c, p2]   = sum_p1 G1[o1, p1, c] PK[p1, p2]                      (one o1 at a time)
+//   theta[o1, o2] += sum_{p2, c} T[c, p2] G2[o2, p2, c]
+// which is the inside-out contraction order of the constant-block-diagonal MJJMP with
+// cost N^2 (D^2 F W + O D^2 W + O^2 D W).  Then the readout summand (g1.g2) delta is added
+// (unless an outside-in pass already wrote theta, in which case theta is accumulated into).
+// Fixed summation order: deterministic.  Limits: D <= 64, O <= 64 (LDS), C chunked by 64.
+constexpr int kPairDMax = 64, kPairOMax = 64, kPairCC = 64, kPairOB = 16;
+
+struct PairLayer {
+  const float* h;    // layer input of the stacked batch, [M, D, Cin]
+  const float* G;    // cotangent of the layer output, [M*O, D, C]
+  int Cin, C;
+};
+struct PairArgs {
+  PairLayer layer[kMaxLayers];
+  int count;
+};
+
+__global__ void __launch_bounds__(256)
+k_conv_pairsum(PairArgs a, int n1, int n2, int n2_offset, int O, int H, int W,
+               const float* __restrict__ gram, int accumulate, float* __restrict__ theta) {
+  extern __shared__ float sm[];
+  const int D = H * W;
+  float* Hs = sm;                           // [D][D]; later the reduction scratch [256][OB]
+  float* PK = Hs + 256 * kPairOB;           // [D][D]
+  float* Ts = PK + kPairDMax * kPairDMax;   // [CC][D]
+  float* Th = Ts + kPairCC * kPairDMax;     // [O][O]
+  const int t = threadIdx.x;
+  const int i1 = blockIdx.x / n2, i2 = blockIdx.x % n2;   // sample indices within batch 1 / 2
+  const int s1 = i1, s2 = n2_offset + i2;                  // rows of the stacked batch
+  for (int q = t; q < O * O; q += 256) Th[q] = 0.f;
+  for (int li = 0; li < a.count; ++li) {
+    const PairLayer L = a.layer[li];
+    const float* h1 = L.h + (long long)s1 * D * L.Cin;
+    const float* h2 = L.h + (long long)s2 * D * L.Cin;
+    // pixel Gram
+    for (int q = t; q < D * D; q += 256) {
+      const int q1 = q / D, q2 = q - q1 * D;
+      float acc = 0.f;
+      for (int ci = 0; ci < L.Cin; ++ci) acc += h1[q1 * L.Cin + ci] * h2[q2 * L.Cin + ci];
+      Hs[q] = acc;
+    }
+    __syncthreads();
+    // patch-pair Gram: both patches use the same tap, so the shifted pixel pairs are summed
+    for (int q = t; q < D * D; q += 256) {
+      const int p1 = q / D, p2 = q - p1 * D;
+      const int y1 = p1 / W, x1 = p1 - y1 * W, y2 = p2 / W, x2 = p2 - y2 * W;
+      float acc = 0.f;
+      for (int kh = 0; kh < 3; ++kh)
+        for (int kw = 0; kw < 3; ++kw) {
+          const int a1 = y1 + kh - 1, b1 = x1 + kw - 1, a2 = y2 + kh - 1, b2 = x2 + kw - 1;
+          if (a1 >= 0 && a1 < H && b1 >= 0 && b1 < W && a2 >= 0 && a2 < H && b2 >= 0 && b2 < W)
+            acc += Hs[(a1 * W + b1) * D + (a2 * W + b2)];
+        }
+      PK[q] = acc;
+    }
+    __syncthreads();
+    const float* G1 = L.G + (long long)s1 * O * D * L.C;
+    const float* G2 = L.G + (long long)s2 * O * D * L.C;
+    for (int c0 = 0; c0 < L.C; c0 += kPairCC) {
+      const int cc = min(kPairCC, L.C - c0);
+      for (int o1 = 0; o1 < O; ++o1) {
+        // T[c, p2] = sum_p1 G1[o1, p1, c0 + c] PK[p1, p2]
+        for (int q = t; q < cc * D; q += 256) {
+          const int p2 = q / cc, c = q - p2 * cc;
+          float acc = 0.f;
+          for (int p1 = 0; p1 < D; ++p1)
+            acc += G1[((long long)o1 * D + p1) * L.C + c0 + c] * PK[p1 * D + p2];
+          Ts[c * D + p2] = acc;
+        }
+        __syncthreads();
+        // theta[o1, o2] += sum_{p2, c} T[c, p2] G2[o2, p2, c0 + c], OB outputs at a time
+        for (int ob = 0; ob < O; ob += kPairOB) {
+          float part[kPairOB];
+#pragma unroll
+          for (int j = 0; j < kPairOB; ++j) part[j] = 0.f;
+          for (int q = t; q < cc * D; q += 256) {
+            const int p2 = q / cc, c = q - p2 * cc;
+            const float tv = Ts[c * D + p2];
+#pragma unroll
+            for (int j = 0; j < kPairOB; ++j)
+              if (ob + j < O) part[j] += tv * G2[((long long)(ob + j) * D + p2) * L.C + c0 + c];
+          }
+#pragma unroll
+          for (int j = 0; j < kPairOB; ++j) Hs[j * 256 + t] = part[j];
+          __syncthreads();
+          if (t < kPairOB && ob + t < O) {
+            float v = 0.f;
+            for (int q = 0; q < 256; ++q) v += Hs[t * 256 + q];
+            Th[o1 * O + ob + t] += v;
+          }
+          __syncthreads();
+        }
+      }
+    }
+  }
+  __syncthreads();
+  const float gr = gram[(long long)i1 * n2 + i2];
+  for (int q = t; q < O * O; q += 256) {
+    const int o1 = q / O, o2 = q - o1 * O;
+    float* dst = theta + (((long long)i1 * n2 + i2) * O) * O + q;
+    float v = Th[q];
+    if (accumulate)
+      v += *dst;
+    else if (o1 == o2)
+      v += gr;
+    *dst = v;
+  }
+}
+
+int pairsum_supported(int D, int O) { return D <= kPairDMax && O <= kPairOMax; }
+
+hipError_t launch_conv_pairsum(hipStream_t s, const PairLayerList& layers, int n1, int n2,
+                               int n2_offset, int O, int H, int W, const float* gram, int accumulate,
+                               float* theta) {
+  PairArgs a{};
+  a.count = layers.count;
+  for (int i = 0; i < layers.count; ++i) {
+    a.layer[i].h = layers.h[i];
+    a.layer[i].G = layers.G[i];
+    a.layer[i].Cin = layers.Cin[i];
+    a.layer[i].C = layers.C[i];
+  }
+  const int bytes = (256 * kPairOB + 2 * kPairDMax * kPairDMax + kPairCC * kPairDMax +
+                     kPairOMax * kPairOMax) * 4;
+  hipError_t e = hipFuncSetAttribute((const void*)k_conv_pairsum,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e != hipSuccess) return e;
+  k_conv_pairsum<<<dim3(n1 * n2), dim3(256), bytes, s>>>(a, n1, n2, n2_offset, O, H, W, gram,
+                                                         accumulate, theta);
   return hipGetLastError();
 }
 

@@ -28,8 +28,24 @@ int splitk_tile();
 // splits * R1 * R2 <= part_capacity (floats) always holds for the returned plan.
 int splitk_plan(int R1, int R2, long long K, int symmetric, long long part_capacity, int* chunk_out);
 hipError_t launch_ntk_splitk(hipStream_t s, const float* J1, const float* J2, int R1, int R2,
-                             long long K, int symmetric, int chunk, int splits, float* part);
+                             long long K, long long ld, int symmetric, int chunk, int splits,
+                             float* part);
+// accumulate = 0: theta = partial sum + readout summand; 1: theta += partial sum.
 hipError_t launch_ntk_reduce(hipStream_t s, const float* part, int splits, int N1, int N2, int O,
-                             int symmetric, const float* gram, float* theta);
+                             int symmetric, const float* gram, int accumulate, float* theta);
+
+// Inside-out order for the conv layers listed (see k_conv_pairsum).  The G pointers must stay
+// valid until the kernel runs, so every listed layer's cotangent must still be resident.
+struct PairLayerList {
+  const float* h[kMaxLayers];
+  const float* G[kMaxLayers];
+  int Cin[kMaxLayers];
+  int C[kMaxLayers];
+  int count;
+};
+int pairsum_supported(int D, int O);
+hipError_t launch_conv_pairsum(hipStream_t s, const PairLayerList& layers, int n1, int n2,
+                               int n2_offset, int O, int H, int W, const float* gram, int accumulate,
+                               float* theta);
 
 }  // namespace ntk

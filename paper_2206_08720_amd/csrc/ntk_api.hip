@@ -411,8 +411,27 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
   for (int l = 0; l <= nc; ++l)
     if (!params[l]) return fail(h, NTK_E_ARG, "null weight pointer");
-  if (h->opt_conv_order == NTK_CONV_ORDER_INSIDE_OUT)
-    return fail(h, NTK_E_UNSUPPORTED, "the inside-out convolution order is not available in this build");
+  // contraction order per layer: the cost model of the appendix "CNN NTK Complexity"
+  // (outside-in N1 N2 O^2 F Cin Cout plus forming J, N O D F Cin Cout per sample, against
+  // inside-out N1 N2 (D^2 F Cin + O D^2 Cout + O^2 D Cout)), or the forced option
+  std::vector<char> inside(nc, 0);
+  const bool io_ok = pairsum_supported(D, O) != 0;
+  for (int l = 0; l < nc; ++l) {
+    const double Cin = h->ch[l], Co = h->ch[l + 1];
+    const double oi = (double)n1 * n2 * O * O * 9 * Cin * Co + (double)M * O * D * 9 * Cin * Co;
+    const double io = (double)n1 * n2 * ((double)D * D * 9 * Cin + (double)O * D * D * Co + (double)O * O * D * Co);
+    if (h->opt_conv_order == NTK_CONV_ORDER_INSIDE_OUT) inside[l] = 1;
+    else if (h->opt_conv_order == NTK_CONV_ORDER_AUTO) inside[l] = (io_ok && io < oi) ? 1 : 0;
+  }
+  long long Kcall = 0;
+  std::vector<long long> jo(nc, 0);
+  for (int l = 0; l < nc; ++l) {
+    if (inside[l]) continue;
+    jo[l] = Kcall;
+    Kcall += 9LL * h->ch[l] * h->ch[l + 1];
+  }
+  if (Kcall < h->Ktot && !io_ok)
+    return fail(h, NTK_E_UNSUPPORTED, "the inside-out order needs D <= 64 pixels and O <= 64");
   hipError_t e;
   const size_t img_floats = (size_t)D * h->ch[0];
   const float* h0 = X1;
@@ -467,11 +486,27 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   prof_end(P, s, KC_CONV_SEED);
   if (e != hipSuccess) return hip_fail(h, e, "conv seed");
   float* J = F(h->off_J);
+  bool theta_written = false;
+  const int n2_off = sym ? 0 : n1;
   for (int l = nc - 1; l >= 0; --l) {
-    prof_begin(P, s, KC_CONV_WGRAD);
-    e = launch_conv_wgrad(s, Gcur, hptr(l), M, O, H, W, h->ch[l + 1], h->ch[l], J, h->Ktot, h->joff[l]);
-    prof_end(P, s, KC_CONV_WGRAD);
-    if (e != hipSuccess) return hip_fail(h, e, "conv weight-space cotangent");
+    if (inside[l]) {
+      PairLayerList pl{};
+      pl.count = 1;
+      pl.h[0] = hptr(l);
+      pl.G[0] = Gcur;
+      pl.Cin[0] = h->ch[l];
+      pl.C[0] = h->ch[l + 1];
+      prof_begin(P, s, KC_CONV_PAIRSUM);
+      e = launch_conv_pairsum(s, pl, n1, n2, n2_off, O, H, W, F(h->off_gram_r), theta_written ? 1 : 0, theta);
+      prof_end(P, s, KC_CONV_PAIRSUM);
+      if (e != hipSuccess) return hip_fail(h, e, "conv inside-out pair sum");
+      theta_written = true;
+    } else {
+      prof_begin(P, s, KC_CONV_WGRAD);
+      e = launch_conv_wgrad(s, Gcur, hptr(l), M, O, H, W, h->ch[l + 1], h->ch[l], J, Kcall, jo[l]);
+      prof_end(P, s, KC_CONV_WGRAD);
+      if (e != hipSuccess) return hip_fail(h, e, "conv weight-space cotangent");
+    }
     if (l >= 1) {
       prof_begin(P, s, KC_CONV_BWD);
       e = launch_conv_bwd(s, Gcur, M, O, H, W, h->ch[l + 1], F(h->off_Kt[l]), h->ch[l],
@@ -481,19 +516,22 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
       std::swap(Gcur, Gnext);
     }
   }
-  // 3. Theta = J1 J2^T (deterministic split over K) + readout summand
-  const int R1 = n1 * O, R2 = n2 * O;
-  int chunk = 0;
-  const int splits = splitk_plan(R1, R2, h->Ktot, sym ? 1 : 0, h->part_capacity, &chunk);
-  const float* J2 = sym ? J : J + (size_t)n1 * O * h->Ktot;
-  prof_begin(P, s, KC_NTK_SPLITK);
-  e = launch_ntk_splitk(s, J, J2, R1, R2, h->Ktot, sym ? 1 : 0, chunk, splits, F(h->off_part));
-  prof_end(P, s, KC_NTK_SPLITK);
-  if (e != hipSuccess) return hip_fail(h, e, "split-K contraction");
-  prof_begin(P, s, KC_NTK_REDUCE);
-  e = launch_ntk_reduce(s, F(h->off_part), splits, n1, n2, O, sym ? 1 : 0, F(h->off_gram_r), theta);
-  prof_end(P, s, KC_NTK_REDUCE);
-  if (e != hipSuccess) return hip_fail(h, e, "split-K reduction");
+  // 3. Theta += J1 J2^T over the outside-in layers (deterministic split over K)
+  if (Kcall > 0) {
+    const int R1 = n1 * O, R2 = n2 * O;
+    int chunk = 0;
+    const int splits = splitk_plan(R1, R2, Kcall, sym ? 1 : 0, h->part_capacity, &chunk);
+    const float* J2 = sym ? J : J + (size_t)n1 * O * Kcall;
+    prof_begin(P, s, KC_NTK_SPLITK);
+    e = launch_ntk_splitk(s, J, J2, R1, R2, Kcall, Kcall, sym ? 1 : 0, chunk, splits, F(h->off_part));
+    prof_end(P, s, KC_NTK_SPLITK);
+    if (e != hipSuccess) return hip_fail(h, e, "split-K contraction");
+    prof_begin(P, s, KC_NTK_REDUCE);
+    e = launch_ntk_reduce(s, F(h->off_part), splits, n1, n2, O, sym ? 1 : 0, F(h->off_gram_r),
+                          theta_written ? 1 : 0, theta);
+    prof_end(P, s, KC_NTK_REDUCE);
+    if (e != hipSuccess) return hip_fail(h, e, "split-K reduction");
+  }
   return NTK_OK;
 }
 

@@ -21,7 +21,10 @@ def to_dev(arrs):
     return [torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)).cuda() for a in arrs]
 
 
-def gpu_ntk(spec, params, X1, X2, symmetric=True, handle=None, max_n=None):
+def gpu_ntk(spec, params, X1, X2, symmetric=True, handle=None, max_n=None, options=None,
+            profile=None):
+    """Theta from the HIP library.  options: {NTK_OPT_*: value}; profile: a dict that
+    receives the per-kernel-class timing of this call."""
     import torch
     from paper_2206_08720_amd import _lib
     from paper_2206_08720_amd.ntk import NTK
@@ -30,8 +33,16 @@ def gpu_ntk(spec, params, X1, X2, symmetric=True, handle=None, max_n=None):
     x2 = x1 if X2 is X1 else to_dev([X2])[0]
     h = handle or NTK(spec, max_n or X1.shape[0], max_n or X2.shape[0])
     h.set_option(_lib.NTK_OPT_SYMMETRIC, 1 if symmetric else 0)
+    for k, v in (options or {}).items():
+        h.set_option(k, v)
+    if profile is not None:
+        h.profile_read()
+        h.profile_enable(True)
     out = h.compute(ps, x1, x2)
     torch.cuda.synchronize()
+    if profile is not None:
+        profile.update(h.profile_read())
+        h.profile_enable(False)
     res = out.cpu().numpy()
     if handle is None:
         h.close()

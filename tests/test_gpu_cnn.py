@@ -90,3 +90,70 @@ def test_cnn_determinism_and_reuse():
         assert cs <= TOL and nw <= TOL
     finally:
         h.close()
+
+
+# ---- contraction order: outside-in vs inside-out (appendix "CNN NTK Complexity") ----------
+ORDER_CASES = [
+    ("D=1", wl.cnn_spec("o1", (1, 1), 3, [16, 16], 10), 6, 5),
+    ("D=4", wl.cnn_spec("o4", (2, 2), 3, [16, 16], 10), 6, 5),
+    ("D=16", wl.cnn_spec("o16", (4, 4), 3, [64, 64, 64], 10), 8, 7),
+    ("D=16 erf, C=20, O=7", wl.cnn_spec("o16e", (4, 4), 5, [20, 20], 7, act="erf"), 5, 9),
+]
+
+
+@pytest.mark.parametrize("order", ["outside_in", "inside_out", "auto"])
+@pytest.mark.parametrize("case", ORDER_CASES, ids=[c[0] for c in ORDER_CASES])
+def test_conv_contraction_orders(case, order):
+    from paper_2206_08720_amd import _lib
+    label, spec, n1, n2 = case
+    code = {"outside_in": _lib.NTK_CONV_ORDER_OUTSIDE_IN, "inside_out": _lib.NTK_CONV_ORDER_INSIDE_OUT,
+            "auto": _lib.NTK_CONV_ORDER_AUTO}[order]
+    params = wl.make_params(spec, 700 + n1, "2/fan_in")
+    X1 = wl.make_inputs(spec, n1, 710 + n1)
+    X2 = wl.make_inputs(spec, n2, 720 + n2)
+    prof = {}
+    got = gpu_ntk(spec, params, X1, X2, options={_lib.NTK_OPT_CONV_ORDER: code}, profile=prof)
+    ref, d1, d2 = oracle.ntk_jc_with_norms(spec, params, X1, X2, layer_storage=S)
+    cs, nw = errors(got, ref, d1, d2)
+    report(f"{label} order={order} kernels={sorted(prof)}", cs, nw)
+    assert cs <= TOL and nw <= TOL
+    if order == "inside_out":
+        assert "conv_pairsum" in prof and "ntk_splitk" not in prof
+    if order == "outside_in":
+        assert "conv_pairsum" not in prof and "ntk_splitk" in prof
+    if order == "auto" and label == "D=16":
+        # the first layer (Cin = 3) is cheaper outside-in, the 64-channel layers inside-out
+        assert "conv_pairsum" in prof and "ntk_splitk" in prof
+
+
+def test_inside_out_symmetric():
+    from paper_2206_08720_amd import _lib
+    spec = wl.cnn_spec("ios", (3, 3), 4, [12, 12], 6)
+    params = wl.make_params(spec, 801, "2/fan_in")
+    X = wl.make_inputs(spec, 11, 802)
+    got = gpu_ntk(spec, params, X, X, options={_lib.NTK_OPT_CONV_ORDER: _lib.NTK_CONV_ORDER_INSIDE_OUT})
+    ref, d1, d2 = oracle.ntk_jc_with_norms(spec, params, X, X, layer_storage=S)
+    cs, nw = errors(got, ref, d1, d2)
+    report("inside-out symmetric", cs, nw)
+    assert cs <= TOL and nw <= TOL
+
+
+def test_inside_out_rejects_large_images_without_enqueuing():
+    import torch
+    from paper_2206_08720_amd import _lib
+    from paper_2206_08720_amd.ntk import NTK
+    from tests.gpu_helpers import to_dev
+    spec = wl.cnn_spec("big", (9, 9), 3, [8], 2)         # D = 81 > 64
+    params = to_dev(wl.make_params(spec, 1, "2/fan_in"))
+    X = to_dev([wl.make_inputs(spec, 2, 2)])[0]
+    h = NTK(spec, 2, 2)
+    try:
+        h.set_option(_lib.NTK_OPT_CONV_ORDER, _lib.NTK_CONV_ORDER_INSIDE_OUT)
+        out = torch.full((2, 2, 2, 2), 3.0, device="cuda")
+        with pytest.raises(_lib.NTKError) as ei:
+            h.compute(params, X, X, out=out)
+        assert ei.value.code == _lib.NTK_E_UNSUPPORTED
+        torch.cuda.synchronize()
+        assert bool((out == 3.0).all())
+    finally:
+        h.close()
