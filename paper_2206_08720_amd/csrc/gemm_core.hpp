@@ -51,8 +51,11 @@ struct LdsGeom {
 // ------------------------------------------------------------------------------ global -> regs -> LDS
 // A loader provides
 //   static constexpr bool K_INNER;
-//   __device__ f32x4 load4(int row, int k) const;
-// returning elements (row, k..k+3) if K_INNER, else (row..row+3, k), zero outside bounds.
+//   __device__ f32x4 load4(int row, int k, uint32_t& valid) const;
+// returning the raw elements (row, k..k+3) if K_INNER, else (row..row+3, k), read from
+// clamped in-range addresses, with bit j of `valid` set when element j is inside the
+// operand.  The zero fill of invalid elements happens at the LDS store, so the selects do
+// not wait on the global loads and the prefetch stays in flight across the MFMA stage.
 template <class Loader, int ROWS, int BK, int THREADS>
 struct TileIO {
   static constexpr bool KI = Loader::K_INNER;
@@ -60,6 +63,7 @@ struct TileIO {
   static_assert(ROWS * BK % (4 * THREADS) == 0, "tile must split evenly into float4 per thread");
   using G = LdsGeom<ROWS, BK, KI>;
   f32x4 r[NV];
+  uint32_t m[NV];
 
   __device__ __forceinline__ void load(const Loader& ld, int row0, int k0, int tid) {
 #pragma unroll
@@ -67,10 +71,10 @@ struct TileIO {
       const int q = tid + i * THREADS;
       if (KI) {
         const int row = q / (BK / 4), kq = (q % (BK / 4)) * 4;
-        r[i] = ld.load4(row0 + row, k0 + kq);
+        r[i] = ld.load4(row0 + row, k0 + kq, m[i]);
       } else {
         const int k = q / (ROWS / 4), rq = (q % (ROWS / 4)) * 4;
-        r[i] = ld.load4(row0 + rq, k0 + k);
+        r[i] = ld.load4(row0 + rq, k0 + k, m[i]);
       }
     }
   }
@@ -78,12 +82,17 @@ struct TileIO {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int q = tid + i * THREADS;
+      f32x4 v = r[i];
+      v[0] = (m[i] & 1u) ? v[0] : 0.f;
+      v[1] = (m[i] & 2u) ? v[1] : 0.f;
+      v[2] = (m[i] & 4u) ? v[2] : 0.f;
+      v[3] = (m[i] & 8u) ? v[3] : 0.f;
       if (KI) {
         const int row = q / (BK / 4), kq = (q % (BK / 4)) * 4;
-        *reinterpret_cast<f32x4*>(&lds[row * G::LD + kq]) = r[i];
+        *reinterpret_cast<f32x4*>(&lds[row * G::LD + kq]) = v;
       } else {
         const int k = q / (ROWS / 4), rq = (q % (ROWS / 4)) * 4;
-        *reinterpret_cast<f32x4*>(&lds[k * G::LD + rq]) = r[i];
+        *reinterpret_cast<f32x4*>(&lds[k * G::LD + rq]) = v;
       }
     }
   }
@@ -104,7 +113,10 @@ __device__ __forceinline__ f32x4 frag_read(const float* lds, int row, int k) {
   }
 }
 
-// One LDS stage: acc[fm][fn] += A_tile(wave rows) * B_tile(wave cols)^T over BK.
+// One LDS stage: acc[fm][fn] += A_tile(wave rows) * B_tile(wave cols)^T over BK.  The
+// fragments of K step kk+8 are read while the MFMAs of step kk issue (two fragment
+// buffers), and a scheduling fence per step keeps the compiler from hoisting every
+// fragment read of the stage (which would cost 4x the fragment registers).
 template <class Cfg, bool AKI, bool BKI>
 __device__ __forceinline__ void mma_stage(const float* As, const float* Bs,
                                           f32x16 (&acc)[Cfg::FM][Cfg::FN], int wm0, int wn0,
@@ -112,20 +124,30 @@ __device__ __forceinline__ void mma_stage(const float* As, const float* Bs,
   using GA = LdsGeom<Cfg::BM, Cfg::BK, AKI>;
   using GB = LdsGeom<Cfg::BN, Cfg::BK, BKI>;
   const int lr = lane & 31, lk = (lane >> 5) * 4;
+  f32x4 a[2][Cfg::FM], b[2][Cfg::FN];
+#pragma unroll
+  for (int fm = 0; fm < Cfg::FM; ++fm) a[0][fm] = frag_read<AKI, GA::LD>(As, wm0 + fm * 32 + lr, lk);
+#pragma unroll
+  for (int fn = 0; fn < Cfg::FN; ++fn) b[0][fn] = frag_read<BKI, GB::LD>(Bs, wn0 + fn * 32 + lr, lk);
 #pragma unroll
   for (int kk = 0; kk < Cfg::BK; kk += 8) {
-    f32x4 a[Cfg::FM], b[Cfg::FN];
+    const int cur = (kk / 8) & 1;
+    if (kk + 8 < Cfg::BK) {
 #pragma unroll
-    for (int fm = 0; fm < Cfg::FM; ++fm) a[fm] = frag_read<AKI, GA::LD>(As, wm0 + fm * 32 + lr, kk + lk);
+      for (int fm = 0; fm < Cfg::FM; ++fm)
+        a[cur ^ 1][fm] = frag_read<AKI, GA::LD>(As, wm0 + fm * 32 + lr, kk + 8 + lk);
 #pragma unroll
-    for (int fn = 0; fn < Cfg::FN; ++fn) b[fn] = frag_read<BKI, GB::LD>(Bs, wn0 + fn * 32 + lr, kk + lk);
+      for (int fn = 0; fn < Cfg::FN; ++fn)
+        b[cur ^ 1][fn] = frag_read<BKI, GB::LD>(Bs, wn0 + fn * 32 + lr, kk + 8 + lk);
+    }
 #pragma unroll
     for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int fm = 0; fm < Cfg::FM; ++fm)
 #pragma unroll
         for (int fn = 0; fn < Cfg::FN; ++fn)
-          acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[fm][t], b[fn][t], acc[fm][fn], 0, 0, 0);
+          acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[cur][fm][t], b[cur][fn][t], acc[fm][fn], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
   }
 }
 
@@ -213,8 +235,9 @@ __device__ __forceinline__ void gemm_mainloop(const LA& la, const LB& lb, int m0
   const int lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
   const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
-  float* As[2] = {smem, smem + GA::FLOATS + GB::FLOATS};
-  float* Bs[2] = {smem + GA::FLOATS, smem + 2 * GA::FLOATS + GB::FLOATS};
+  // stage s of the double buffer: A at smem + s * STAGE, B right after it.  Offsets (not an
+  // array of pointers) keep every access in the LDS address space (ds_read / ds_write).
+  constexpr int STAGE = GA::FLOATS + GB::FLOATS;
 
   const int nk = (k_end - k_begin + Cfg::BK - 1) / Cfg::BK;
   if (nk <= 0) return;
@@ -222,20 +245,20 @@ __device__ __forceinline__ void gemm_mainloop(const LA& la, const LB& lb, int m0
   TileIO<LB, Cfg::BN, Cfg::BK, Cfg::THREADS> ib;
   ia.load(la, m0, k_begin, tid);
   ib.load(lb, n0, k_begin, tid);
-  ia.store(As[0], tid);
-  ib.store(Bs[0], tid);
+  ia.store(smem, tid);
+  ib.store(smem + GA::FLOATS, tid);
   __syncthreads();
   for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
+    const int cur = (kt & 1) * STAGE, nxt = STAGE - cur;
     const bool more = kt + 1 < nk;
     if (more) {
       ia.load(la, m0, k_begin + (kt + 1) * Cfg::BK, tid);
       ib.load(lb, n0, k_begin + (kt + 1) * Cfg::BK, tid);
     }
-    mma_stage<Cfg, LA::K_INNER, LB::K_INNER>(As[cur], Bs[cur], acc, wm0, wn0, lane);
+    mma_stage<Cfg, LA::K_INNER, LB::K_INNER>(smem + cur, smem + cur + GA::FLOATS, acc, wm0, wn0, lane);
     if (more) {
-      ia.store(As[cur ^ 1], tid);
-      ib.store(Bs[cur ^ 1], tid);
+      ia.store(smem + nxt, tid);
+      ib.store(smem + nxt + GA::FLOATS, tid);
     }
     __syncthreads();
   }
@@ -266,29 +289,84 @@ __device__ __forceinline__ void for_each_acc(f32x16 (&acc)[Cfg::FM][Cfg::FN], in
       }
 }
 
+// Two-phase epilogues: first gather one auxiliary value per accumulator element (all loads
+// issued before any is used), then combine and store.
+template <class Cfg, class L>
+__device__ __forceinline__ void gather_acc(float (&g)[Cfg::FM][Cfg::FN][16], int m0, int n0, L&& load) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
+  const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
+#pragma unroll
+  for (int fm = 0; fm < Cfg::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < Cfg::FN; ++fn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = m0 + wm0 + fm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        const int col = n0 + wn0 + fn * 32 + (lane & 31);
+        g[fm][fn][v] = load(row, col);
+      }
+}
+
+template <class Cfg, class F>
+__device__ __forceinline__ void for_each_acc_aux(f32x16 (&acc)[Cfg::FM][Cfg::FN],
+                                                 const float (&g)[Cfg::FM][Cfg::FN][16], int m0, int n0,
+                                                 F&& f) {
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
+  const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
+#pragma unroll
+  for (int fm = 0; fm < Cfg::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < Cfg::FN; ++fn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int row = m0 + wm0 + fm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+        const int col = n0 + wn0 + fn * 32 + (lane & 31);
+        f(row, col, acc[fm][fn][v], g[fm][fn][v]);
+      }
+}
+
 // ------------------------------------------------------------------------------ loaders
-// Row-major [rows, K] operand with row stride `ld` (floats), K contiguous.
-struct LoadKInner {
+// Loaders never branch: an out-of-range element is read from a clamped (valid) address and
+// replaced by 0 with a select, so the main loop has no divergent control flow.
+//
+// Row-major [rows, K] operand with row stride `ld` (floats), K contiguous.  VEC = whole
+// float4 loads: requires p 16-byte aligned, ld % 4 == 0 and K % 4 == 0.
+template <bool VEC>
+struct LoadKInnerT {
   static constexpr bool K_INNER = true;
   const float* p;
   int rows, K;
   long long ld;
-  bool vec;  // p 16-byte aligned and ld % 4 == 0: whole float4 loads allowed
-  __device__ __forceinline__ f32x4 load4(int row, int k) const {
-    f32x4 v = {0.f, 0.f, 0.f, 0.f};
-    if (row < rows) {
-      const float* q = p + (long long)row * ld + k;
-      if (vec && k + 3 < K) {
-        v = *reinterpret_cast<const f32x4*>(q);
-      } else {
+  __device__ __forceinline__ f32x4 load4(int row, int k, uint32_t& valid) const {
+    const int rc = min(row, rows - 1);
+    if (VEC) {
+      const int kc = min(k, K - 4);
+      valid = (row < rows && k < K) ? 0xFu : 0u;
+      return *reinterpret_cast<const f32x4*>(p + (long long)rc * ld + kc);
+    } else {
+      f32x4 v;
+      valid = 0;
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
-          if (k + j < K) v[j] = q[j];
+      for (int j = 0; j < 4; ++j) {
+        const int kc = min(k + j, K - 1);
+        v[j] = p[(long long)rc * ld + kc];
+        valid |= (row < rows && k + j < K) ? (1u << j) : 0u;
       }
+      return v;
     }
-    return v;
   }
 };
+using LoadKInner = LoadKInnerT<true>;
+
+// The VEC form is usable when every pointer is 16-byte aligned and the strides and K are
+// multiples of 4 floats.
+__host__ inline bool vec_ok(const void* p, long long ld, long long K) {
+  return (reinterpret_cast<uintptr_t>(p) & 15) == 0 && ld % 4 == 0 && K % 4 == 0;
+}
 
 // ------------------------------------------------------------------------------ misc
 __device__ __forceinline__ float act_fwd(int act, float z) {

@@ -37,105 +37,127 @@ static hipError_t set_smem(const void* fn) {
 }
 
 // ------------------------------------------------------------------------------ loaders
+// All loaders read from clamped in-range addresses and report per-element validity (bit j
+// of `valid`); the zero fill happens at the LDS store (see TileIO).
+//
 // Patch matrix of an NHWC batch as a K-inner operand: row = img*D + p, p = y*W + x,
 // k = (kh*3 + kw)*C + ci; the tap (kh, kw) reads pixel (y + kh - 1, x + kw - 1), zero
-// outside the image.
-struct LoadPatchesKInner {
+// outside the image.  VEC: C % 4 == 0 and x 16-byte aligned (4 k share one tap).
+template <bool VEC>
+struct LoadPatchesKInnerT {
   static constexpr bool K_INNER = true;
   const float* x;
   int rows, H, W, C, K;  // K = 9*C
   FastDiv fD, fW, fC;
-  bool vec;              // C % 4 == 0 and x 16-byte aligned
-  __device__ __forceinline__ float tap_value(int img, int y, int xx, int k) const {
-    const int tap = (int)fC.div(k), ci = k - tap * C;
-    const int kh = (tap * 11) >> 5, kw = tap - 3 * kh;  // tap / 3 for tap < 9
+  __device__ __forceinline__ float tap(int img, int y, int xx, int k, bool& ok) const {
+    const int kc = min(k, K - 1);
+    const int t = (int)fC.div(kc), ci = kc - t * C;
+    const int kh = (t * 11) >> 5, kw = t - 3 * kh;  // t / 3 for t < 9
     const int yy = y + kh - 1, xq = xx + kw - 1;
-    if (yy < 0 || yy >= H || xq < 0 || xq >= W) return 0.f;
-    return x[(((long long)img * H + yy) * W + xq) * C + ci];
+    ok = k < K && yy >= 0 && yy < H && xq >= 0 && xq < W;
+    const int yc = min(max(yy, 0), H - 1), xc = min(max(xq, 0), W - 1);
+    return x[(((long long)img * H + yc) * W + xc) * C + ci];
   }
-  __device__ __forceinline__ f32x4 load4(int row, int k) const {
-    f32x4 v = {0.f, 0.f, 0.f, 0.f};
-    if (row >= rows) return v;
-    const int img = (int)fD.div(row), p = row - img * (int)fD.d;
+  __device__ __forceinline__ f32x4 load4(int row, int k, uint32_t& valid) const {
+    const int rc = min(row, rows - 1);
+    const int img = (int)fD.div(rc), p = rc - img * (int)fD.d;
     const int y = (int)fW.div(p), xx = p - y * W;
-    if (vec && k + 3 < K) {
-      const int tap = (int)fC.div(k), ci = k - tap * C;
-      const int kh = (tap * 11) >> 5, kw = tap - 3 * kh;
+    if (VEC) {
+      const int kc = min(k, K - 4);
+      const int t = (int)fC.div(kc), ci = kc - t * C;
+      const int kh = (t * 11) >> 5, kw = t - 3 * kh;
       const int yy = y + kh - 1, xq = xx + kw - 1;
-      if (yy >= 0 && yy < H && xq >= 0 && xq < W)
-        v = *reinterpret_cast<const f32x4*>(x + (((long long)img * H + yy) * W + xq) * C + ci);
+      const bool ok = row < rows && k < K && yy >= 0 && yy < H && xq >= 0 && xq < W;
+      const int yc = min(max(yy, 0), H - 1), xc = min(max(xq, 0), W - 1);
+      valid = ok ? 0xFu : 0u;
+      return *reinterpret_cast<const f32x4*>(x + (((long long)img * H + yc) * W + xc) * C + ci);
     } else {
+      f32x4 v;
+      valid = 0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (k + j < K) v[j] = tap_value(img, y, xx, k + j);
+      for (int j = 0; j < 4; ++j) {
+        bool ok;
+        v[j] = tap(img, y, xx, k + j, ok);
+        valid |= (ok && row < rows) ? (1u << j) : 0u;
+      }
+      return v;
     }
-    return v;
   }
 };
 
 // G of one sample as a K-outer operand of the weight-space cotangent product:
 // row = o*C + c, k = p;  element = G[((s*O + o)*D + p)*C + c]  (base already at sample s).
-struct LoadCotangentKOuter {
+// VEC: C % 4 == 0 and g 16-byte aligned.
+template <bool VEC>
+struct LoadCotangentKOuterT {
   static constexpr bool K_INNER = false;
   const float* g;
   int rows, K, C, D;     // rows = O*C, K = D
   FastDiv fC;
-  bool vec;              // C % 4 == 0 and g 16-byte aligned
-  __device__ __forceinline__ f32x4 load4(int row, int k) const {
-    f32x4 v = {0.f, 0.f, 0.f, 0.f};
-    if (k >= K) return v;
-    if (vec && row + 3 < rows) {
-      const int o = (int)fC.div(row), c = row - o * C;
-      v = *reinterpret_cast<const f32x4*>(g + ((long long)o * D + k) * C + c);
+  __device__ __forceinline__ f32x4 load4(int row, int k, uint32_t& valid) const {
+    const int kc = min(k, K - 1);
+    if (VEC) {
+      const int rc = min(row, rows - 4);
+      const int o = (int)fC.div(rc), c = rc - o * C;
+      valid = (row < rows && k < K) ? 0xFu : 0u;
+      return *reinterpret_cast<const f32x4*>(g + ((long long)o * D + kc) * C + c);
     } else {
+      f32x4 v;
+      valid = 0;
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        const int r = row + j;
-        if (r < rows) {
-          const int o = (int)fC.div(r), c = r - o * C;
-          v[j] = g[((long long)o * D + k) * C + c];
-        }
+        const int rc = min(row + j, rows - 1);
+        const int o = (int)fC.div(rc), c = rc - o * C;
+        v[j] = g[((long long)o * D + kc) * C + c];
+        valid |= (row + j < rows && k < K) ? (1u << j) : 0u;
       }
+      return v;
     }
-    return v;
   }
 };
 
 // Patch matrix of one sample as a K-outer operand: row = k (tap, ci), kdim = p.
-struct LoadPatchesKOuter {
+// VEC: C % 4 == 0 and x 16-byte aligned.
+template <bool VEC>
+struct LoadPatchesKOuterT {
   static constexpr bool K_INNER = false;
   const float* x;        // sample base, [H, W, C]
   int rows, K, H, W, C;  // rows = 9*C, K = D
   FastDiv fW, fC;
-  bool vec;
-  __device__ __forceinline__ float tap_value(int y, int xx, int k) const {
-    const int tap = (int)fC.div(k), ci = k - tap * C;
-    const int kh = (tap * 11) >> 5, kw = tap - 3 * kh;
-    const int yy = y + kh - 1, xq = xx + kw - 1;
-    if (yy < 0 || yy >= H || xq < 0 || xq >= W) return 0.f;
-    return x[((long long)yy * W + xq) * C + ci];
-  }
-  __device__ __forceinline__ f32x4 load4(int row, int p) const {
-    f32x4 v = {0.f, 0.f, 0.f, 0.f};
-    if (p >= K) return v;
-    const int y = (int)fW.div(p), xx = p - y * W;
-    if (vec && row + 3 < rows) {
-      const int tap = (int)fC.div(row), ci = row - tap * C;
-      const int kh = (tap * 11) >> 5, kw = tap - 3 * kh;
+  __device__ __forceinline__ f32x4 load4(int row, int p, uint32_t& valid) const {
+    const int pc = min(p, K - 1);
+    const int y = (int)fW.div(pc), xx = pc - y * W;
+    if (VEC) {
+      const int rc = min(row, rows - 4);
+      const int t = (int)fC.div(rc), ci = rc - t * C;
+      const int kh = (t * 11) >> 5, kw = t - 3 * kh;
       const int yy = y + kh - 1, xq = xx + kw - 1;
-      if (yy >= 0 && yy < H && xq >= 0 && xq < W)
-        v = *reinterpret_cast<const f32x4*>(x + ((long long)yy * W + xq) * C + ci);
+      const bool ok = row < rows && p < K && yy >= 0 && yy < H && xq >= 0 && xq < W;
+      const int yc = min(max(yy, 0), H - 1), xc = min(max(xq, 0), W - 1);
+      valid = ok ? 0xFu : 0u;
+      return *reinterpret_cast<const f32x4*>(x + ((long long)yc * W + xc) * C + ci);
     } else {
+      f32x4 v;
+      valid = 0;
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        if (row + j < rows) v[j] = tap_value(y, xx, row + j);
+      for (int j = 0; j < 4; ++j) {
+        const int rc = min(row + j, rows - 1);
+        const int t = (int)fC.div(rc), ci = rc - t * C;
+        const int kh = (t * 11) >> 5, kw = t - 3 * kh;
+        const int yy = y + kh - 1, xq = xx + kw - 1;
+        const bool ok = row + j < rows && p < K && yy >= 0 && yy < H && xq >= 0 && xq < W;
+        const int yc = min(max(yy, 0), H - 1), xc = min(max(xq, 0), W - 1);
+        v[j] = x[((long long)yc * W + xc) * C + ci];
+        valid |= ok ? (1u << j) : 0u;
+      }
+      return v;
     }
-    return v;
   }
 };
 
-static LoadPatchesKInner patches_kinner(const float* x, int images, int H, int W, int C) {
-  LoadPatchesKInner l;
+template <bool VEC>
+static LoadPatchesKInnerT<VEC> patches_kinner(const float* x, int images, int H, int W, int C) {
+  LoadPatchesKInnerT<VEC> l;
   l.x = x;
   l.rows = images * H * W;
   l.H = H;
@@ -145,15 +167,14 @@ static LoadPatchesKInner patches_kinner(const float* x, int images, int H, int W
   l.fD = FastDiv((uint32_t)(H * W));
   l.fW = FastDiv((uint32_t)W);
   l.fC = FastDiv((uint32_t)C);
-  l.vec = (C % 4 == 0) && aligned16(x);
   return l;
 }
 
 // ------------------------------------------------------------------------------ forward
-template <class Cfg>
+template <class Cfg, bool VEC>
 __global__ void __launch_bounds__(Cfg::THREADS)
-k_conv_fwd(LoadPatchesKInner la, LoadKInner lb, int M, int N, int act, float* __restrict__ hn,
-           float* __restrict__ dphi, int tiles_n) {
+k_conv_fwd(LoadPatchesKInnerT<VEC> la, LoadKInnerT<VEC> lb, int M, int N, int act,
+           float* __restrict__ hn, float* __restrict__ dphi, int tiles_n) {
   extern __shared__ float smem[];
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
@@ -161,34 +182,44 @@ k_conv_fwd(LoadPatchesKInner la, LoadKInner lb, int M, int N, int act, float* __
   zero_acc<Cfg>(acc);
   gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
   for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, double z) {
+    float h, d;
+    if (act == 1) {
+      h = z > 0.0 ? (float)z : 0.f;
+      d = z > 0.0 ? 1.f : 0.f;
+    } else {
+      const float zf = (float)z;
+      h = act_fwd(act, zf);
+      d = act_deriv(act, zf);
+    }
     if (r < M && c < N) {
-      float h, d;
-      if (act == 1) {
-        h = z > 0.0 ? (float)z : 0.f;
-        d = z > 0.0 ? 1.f : 0.f;
-      } else {
-        const float zf = (float)z;
-        h = act_fwd(act, zf);
-        d = act_deriv(act, zf);
-      }
       hn[(long long)r * N + c] = h;
       dphi[(long long)r * N + c] = d;
     }
   });
 }
 
-hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int W, int Cin,
-                           const float* K, int Cout, int act, float* hn, float* dphi) {
+template <bool VEC>
+static hipError_t conv_fwd_vec(hipStream_t s, const float* x, int images, int H, int W, int Cin,
+                               const float* K, int Cout, int act, float* hn, float* dphi) {
   using Cfg = CfgConvF64;
-  LoadPatchesKInner la = patches_kinner(x, images, H, W, Cin);
-  LoadKInner lb{K, Cout, 9 * Cin, 9 * Cin, aligned16(K) && (9 * Cin) % 4 == 0};
+  using LA = LoadPatchesKInnerT<VEC>;
+  using LB = LoadKInnerT<VEC>;
+  LA la = patches_kinner<VEC>(x, images, H, W, Cin);
+  LB lb{K, Cout, 9 * Cin, 9 * Cin};
   const int M = images * H * W;
   const int tn = cdiv(Cout, Cfg::BN), tm = cdiv(M, Cfg::BM);
-  hipError_t e = set_smem<Cfg, LoadPatchesKInner, LoadKInner>((const void*)k_conv_fwd<Cfg>);
+  hipError_t e = set_smem<Cfg, LA, LB>((const void*)k_conv_fwd<Cfg, VEC>);
   if (e != hipSuccess) return e;
-  k_conv_fwd<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LoadPatchesKInner, LoadKInner>(), s>>>(
+  k_conv_fwd<Cfg, VEC><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LA, LB>(), s>>>(
       la, lb, M, Cout, act, hn, dphi, tn);
   return hipGetLastError();
+}
+
+hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int W, int Cin,
+                           const float* K, int Cout, int act, float* hn, float* dphi) {
+  if (Cin % 4 == 0 && aligned16(x) && vec_ok(K, 9 * Cin, 9 * Cin))
+    return conv_fwd_vec<true>(s, x, images, H, W, Cin, K, Cout, act, hn, dphi);
+  return conv_fwd_vec<false>(s, x, images, H, W, Cin, K, Cout, act, hn, dphi);
 }
 
 // ------------------------------------------------------------------------------ GAP, seed
@@ -266,43 +297,56 @@ hipError_t launch_conv_flip(hipStream_t s, const float* K, int Cout, int Cin, fl
 
 // ------------------------------------------------------------------------------ backward
 // out[(img*O+o), p, ci] = (sum_k patch(G)[.., p, k] Kt[ci, k]) * dphi[img, p, ci]
-template <class Cfg>
+template <class Cfg, bool VEC>
 __global__ void __launch_bounds__(Cfg::THREADS)
-k_conv_bwd(LoadPatchesKInner la, LoadKInner lb, const float* __restrict__ dphi, int R, int N,
-           FastDiv fOD, int D, int O, float* __restrict__ out, int tiles_n) {
+k_conv_bwd(LoadPatchesKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restrict__ dphi, int R,
+           int N, FastDiv fOD, FastDiv fD, float* __restrict__ out, int tiles_n) {
   extern __shared__ float smem[];
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
   gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
-  for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, float v) {
-    if (r < R && c < N) {
-      const int img = (int)fOD.div(r);            // r = (img*O + o)*D + p
-      const int p = r - (r / D) * D;
-      out[(long long)r * N + c] = v * dphi[((long long)img * D + p) * N + c];
-    }
+  float g[Cfg::FM][Cfg::FN][16];
+  gather_acc<Cfg>(g, m0, n0, [&](int r, int c) {
+    const int rc = min(r, R - 1), cc = min(c, N - 1);
+    const int img = (int)fOD.div(rc);              // r = (img*O + o)*D + p
+    const int p = rc - (int)fD.div(rc) * (int)fD.d;
+    return dphi[((long long)img * fD.d + p) * N + cc];
   });
+  for_each_acc_aux<Cfg>(acc, g, m0, n0, [&](int r, int c, float v, float d) {
+    if (r < R && c < N) out[(long long)r * N + c] = v * d;
+  });
+}
+
+template <bool VEC>
+static hipError_t conv_bwd_vec(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
+                               const float* Kt, int Cin, const float* dphi, float* out) {
+  using Cfg = CfgConv;
+  using LA = LoadPatchesKInnerT<VEC>;
+  using LB = LoadKInnerT<VEC>;
+  const int D = H * W;
+  LA la = patches_kinner<VEC>(G, images * O, H, W, Cg);
+  LB lb{Kt, Cin, 9 * Cg, 9 * Cg};
+  const int R = images * O * D;
+  const int tn = cdiv(Cin, Cfg::BN), tm = cdiv(R, Cfg::BM);
+  hipError_t e = set_smem<Cfg, LA, LB>((const void*)k_conv_bwd<Cfg, VEC>);
+  if (e != hipSuccess) return e;
+  k_conv_bwd<Cfg, VEC><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LA, LB>(), s>>>(
+      la, lb, dphi, R, Cin, FastDiv((uint32_t)(O * D)), FastDiv((uint32_t)D), out, tn);
+  return hipGetLastError();
 }
 
 hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
                            const float* Kt, int Cin, const float* dphi, float* out) {
-  using Cfg = CfgConv;
-  const int D = H * W;
-  LoadPatchesKInner la = patches_kinner(G, images * O, H, W, Cg);
-  LoadKInner lb{Kt, Cin, 9 * Cg, 9 * Cg, aligned16(Kt) && (9 * Cg) % 4 == 0};
-  const int R = images * O * D;
-  const int tn = cdiv(Cin, Cfg::BN), tm = cdiv(R, Cfg::BM);
-  hipError_t e = set_smem<Cfg, LoadPatchesKInner, LoadKInner>((const void*)k_conv_bwd<Cfg>);
-  if (e != hipSuccess) return e;
-  k_conv_bwd<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LoadPatchesKInner, LoadKInner>(), s>>>(
-      la, lb, dphi, R, Cin, FastDiv((uint32_t)(O * D)), D, O, out, tn);
-  return hipGetLastError();
+  if (Cg % 4 == 0 && aligned16(G) && vec_ok(Kt, 9 * Cg, 9 * Cg))
+    return conv_bwd_vec<true>(s, G, images, O, H, W, Cg, Kt, Cin, dphi, out);
+  return conv_bwd_vec<false>(s, G, images, O, H, W, Cg, Kt, Cin, dphi, out);
 }
 
 // ------------------------------------------------------------------------------ weight-space cotangent
 // For sample s = blockIdx.y:  J[s*O + o][off + c*KC + k] = sum_p G[s,o,p,c] patch[s,p,k]
-template <class Cfg>
+template <class Cfg, bool VEC>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, int H, int W, int C,
              int Cin, FastDiv fC, FastDiv fW, FastDiv fCin, float* __restrict__ J, long long ldJ,
@@ -313,15 +357,14 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
   const int KC = 9 * Cin;
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
-  LoadCotangentKOuter la;
+  LoadCotangentKOuterT<VEC> la;
   la.g = G + (long long)s * O * D * C;
   la.rows = O * C;
   la.K = D;
   la.C = C;
   la.D = D;
   la.fC = fC;
-  la.vec = (C % 4 == 0) && ((reinterpret_cast<uintptr_t>(G) & 15) == 0);
-  LoadPatchesKOuter lb;
+  LoadPatchesKOuterT<VEC> lb;
   lb.x = h + (long long)s * D * Cin;
   lb.rows = KC;
   lb.K = D;
@@ -330,7 +373,6 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
   lb.C = Cin;
   lb.fW = fW;
   lb.fC = fCin;
-  lb.vec = (Cin % 4 == 0) && ((reinterpret_cast<uintptr_t>(h) & 15) == 0);
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
   gemm_mainloop<Cfg>(la, lb, m0, n0, 0, D, smem, acc);
@@ -343,17 +385,26 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
   });
 }
 
-hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
-                             int W, int C, int Cin, float* J, long long ldJ, long long off) {
+template <bool VEC>
+static hipError_t conv_wgrad_vec(hipStream_t s, const float* G, const float* h, int images, int O,
+                                 int H, int W, int C, int Cin, float* J, long long ldJ, long long off) {
   using Cfg = CfgConv;
+  using LA = LoadCotangentKOuterT<VEC>;
+  using LB = LoadPatchesKOuterT<VEC>;
   const int tn = cdiv(9 * Cin, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
-  hipError_t e = set_smem<Cfg, LoadCotangentKOuter, LoadPatchesKOuter>((const void*)k_conv_wgrad<Cfg>);
+  hipError_t e = set_smem<Cfg, LA, LB>((const void*)k_conv_wgrad<Cfg, VEC>);
   if (e != hipSuccess) return e;
-  k_conv_wgrad<Cfg><<<dim3(tm * tn, images), dim3(Cfg::THREADS),
-                      gemm_smem_bytes<Cfg, LoadCotangentKOuter, LoadPatchesKOuter>(), s>>>(
+  k_conv_wgrad<Cfg, VEC><<<dim3(tm * tn, images), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LA, LB>(), s>>>(
       G, h, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
       ldJ, off, tn);
   return hipGetLastError();
+}
+
+hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
+                             int W, int C, int Cin, float* J, long long ldJ, long long off) {
+  if (C % 4 == 0 && Cin % 4 == 0 && aligned16(G) && aligned16(h))
+    return conv_wgrad_vec<true>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
+  return conv_wgrad_vec<false>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
 }
 
 // ------------------------------------------------------------------------------ split-K J1 J2^T
@@ -368,9 +419,9 @@ __device__ __forceinline__ void tri_index_c(int t, int nt, int& tm, int& tn) {
 }
 
 // part[z][r1][r2] = sum_{k in chunk z} J1[r1, k] J2[r2, k]
-template <class Cfg>
+template <class Cfg, bool VEC>
 __global__ void __launch_bounds__(Cfg::THREADS)
-k_ntk_splitk(LoadKInner la, LoadKInner lb, int chunk, int symmetric, float* __restrict__ part,
+k_ntk_splitk(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, int chunk, int symmetric, float* __restrict__ part,
              int tiles_n) {
   extern __shared__ float smem[];
   const int z = blockIdx.y;
@@ -436,19 +487,29 @@ int splitk_plan(int R1, int R2, long long K, int symmetric, long long part_capac
   return splits;
 }
 
-hipError_t launch_ntk_splitk(hipStream_t s, const float* J1, const float* J2, int R1, int R2,
+template <bool VEC>
+static hipError_t splitk_vec(hipStream_t s, const float* J1, const float* J2, int R1, int R2,
                              long long K, long long ld, int symmetric, int chunk, int splits,
                              float* part) {
   using Cfg = CfgSplitK;
-  LoadKInner la{J1, R1, (int)K, ld, aligned16(J1) && ld % 4 == 0};
-  LoadKInner lb{J2, R2, (int)K, ld, aligned16(J2) && ld % 4 == 0};
+  using L = LoadKInnerT<VEC>;
+  L la{J1, R1, (int)K, ld};
+  L lb{J2, R2, (int)K, ld};
   const int tm = cdiv(R1, Cfg::BM), tn = cdiv(R2, Cfg::BN);
   const int tiles = symmetric ? tn * (tn + 1) / 2 : tm * tn;
-  hipError_t e = set_smem<Cfg, LoadKInner, LoadKInner>((const void*)k_ntk_splitk<Cfg>);
+  hipError_t e = set_smem<Cfg, L, L>((const void*)k_ntk_splitk<Cfg, VEC>);
   if (e != hipSuccess) return e;
-  k_ntk_splitk<Cfg><<<dim3(tiles, splits), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LoadKInner, LoadKInner>(), s>>>(
+  k_ntk_splitk<Cfg, VEC><<<dim3(tiles, splits), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, L, L>(), s>>>(
       la, lb, chunk, symmetric, part, tn);
   return hipGetLastError();
+}
+
+hipError_t launch_ntk_splitk(hipStream_t s, const float* J1, const float* J2, int R1, int R2,
+                             long long K, long long ld, int symmetric, int chunk, int splits,
+                             float* part) {
+  if (vec_ok(J1, ld, K) && vec_ok(J2, ld, K))
+    return splitk_vec<true>(s, J1, J2, R1, R2, K, ld, symmetric, chunk, splits, part);
+  return splitk_vec<false>(s, J1, J2, R1, R2, K, ld, symmetric, chunk, splits, part);
 }
 
 hipError_t launch_ntk_reduce(hipStream_t s, const float* part, int splits, int N1, int N2, int O,

@@ -11,6 +11,8 @@
 //   * the fused contraction: per output tile, sum over layers of
 //     gram_l[n1,n2] * (G1_l G2_l^T)[(n1,o1),(n2,o2)] in registers, plus the readout
 //     summand gram_L[n1,n2] delta_{o1 o2}, written as theta[n1][n2][o1][o2]  (k_ntk_fcn)
+#include <type_traits>
+
 #include "gemm_core.hpp"
 #include "launch.hpp"
 
@@ -18,6 +20,8 @@ namespace ntk {
 
 using CfgBig = TileCfg<128, 128, 32, 64, 64>;   // 4 waves, 64x64 per wave
 using CfgSmall = TileCfg<64, 64, 32, 32, 32>;   // 4 waves, 32x32 per wave
+using TrueT = std::true_type;
+using FalseT = std::false_type;
 
 static inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 
@@ -29,15 +33,13 @@ static hipError_t set_smem(const void* fn) {
   return hipSuccess;
 }
 
-static inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
-
 // ------------------------------------------------------------------------------ forward
 // The pre-activation is accumulated in fp64 from the fp32 layer input and weights, then
 // the activation's decision (ReLU sign) is taken on that value and h_{l+1} is stored in fp32.
-template <class Cfg>
+template <class Cfg, bool VEC>
 __global__ void __launch_bounds__(Cfg::THREADS)
-k_dense_fwd(LoadKInner la, LoadKInner lb, const float* __restrict__ bias, int M, int N, int act,
-            float* __restrict__ hn, float* __restrict__ dphi, int tiles_n) {
+k_dense_fwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restrict__ bias, int M, int N,
+            int act, float* __restrict__ hn, float* __restrict__ dphi, int tiles_n) {
   extern __shared__ float smem[];
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
@@ -45,73 +47,89 @@ k_dense_fwd(LoadKInner la, LoadKInner lb, const float* __restrict__ bias, int M,
   zero_acc<Cfg>(acc);
   gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
   for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, double v) {
+    const double b = bias ? (double)bias[min(c, N - 1)] : 0.0;
+    const double z = v + b;
+    float h, d;
+    if (act == 1) {
+      h = z > 0.0 ? (float)z : 0.f;
+      d = z > 0.0 ? 1.f : 0.f;
+    } else {
+      const float zf = (float)z;
+      h = act_fwd(act, zf);
+      d = act_deriv(act, zf);
+    }
     if (r < M && c < N) {
-      const double z = v + (bias ? (double)bias[c] : 0.0);
-      float h, d;
-      if (act == 1) {
-        h = z > 0.0 ? (float)z : 0.f;
-        d = z > 0.0 ? 1.f : 0.f;
-      } else {
-        const float zf = (float)z;
-        h = act_fwd(act, zf);
-        d = act_deriv(act, zf);
-      }
       hn[(long long)r * N + c] = h;
       dphi[(long long)r * N + c] = d;
     }
   });
 }
 
-template <class Cfg>
+template <class Cfg, bool VEC>
 static hipError_t dense_fwd_cfg(hipStream_t s, const float* h, const float* W, const float* b, int M,
                                 int N, int K, int act, float* hn, float* dphi) {
-  LoadKInner la{h, M, K, K, aligned16(h) && K % 4 == 0};
-  LoadKInner lb{W, N, K, K, aligned16(W) && K % 4 == 0};
+  using L = LoadKInnerT<VEC>;
+  L la{h, M, K, K};
+  L lb{W, N, K, K};
   const int tn = cdiv(N, Cfg::BN), tm = cdiv(M, Cfg::BM);
-  hipError_t e = set_smem<Cfg, LoadKInner, LoadKInner>((const void*)k_dense_fwd<Cfg>);
+  hipError_t e = set_smem<Cfg, L, L>((const void*)k_dense_fwd<Cfg, VEC>);
   if (e != hipSuccess) return e;
-  k_dense_fwd<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LoadKInner, LoadKInner>(), s>>>(la, lb, b, M, N, act, hn, dphi, tn);
+  k_dense_fwd<Cfg, VEC><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, L, L>(), s>>>(
+      la, lb, b, M, N, act, hn, dphi, tn);
   return hipGetLastError();
 }
 
 hipError_t launch_dense_fwd(hipStream_t s, const float* h, const float* W, const float* b, int M,
                             int N, int K, int act, float* hn, float* dphi) {
-  return dense_fwd_cfg<CfgSmall>(s, h, W, b, M, N, K, act, hn, dphi);
+  if (vec_ok(h, K, K) && vec_ok(W, K, K))
+    return dense_fwd_cfg<CfgSmall, true>(s, h, W, b, M, N, K, act, hn, dphi);
+  return dense_fwd_cfg<CfgSmall, false>(s, h, W, b, M, N, K, act, hn, dphi);
 }
 
 // ------------------------------------------------------------------------------ backward
-template <class Cfg>
+template <class Cfg, bool VEC>
 __global__ void __launch_bounds__(Cfg::THREADS)
-k_dense_bwd(LoadKInner la, LoadKInner lb, const float* __restrict__ dphi, int R, int N, int O,
-            float* __restrict__ out, int tiles_n) {
+k_dense_bwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restrict__ dphi, int R, int N,
+            FastDiv fO, float* __restrict__ out, int tiles_n) {
   extern __shared__ float smem[];
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
   gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
-  for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, float v) {
-    if (r < R && c < N) out[(long long)r * N + c] = v * dphi[(long long)(r / O) * N + c];
+  float g[Cfg::FM][Cfg::FN][16];
+  gather_acc<Cfg>(g, m0, n0, [&](int r, int c) {
+    const int rc = min(r, R - 1), cc = min(c, N - 1);
+    return dphi[(long long)fO.div(rc) * N + cc];
+  });
+  for_each_acc_aux<Cfg>(acc, g, m0, n0, [&](int r, int c, float v, float d) {
+    if (r < R && c < N) out[(long long)r * N + c] = v * d;
   });
 }
 
-template <class Cfg>
+template <class Cfg, bool VEC>
 static hipError_t dense_bwd_cfg(hipStream_t s, const float* G, const float* Wt, const float* dphi,
                                 int R, int N, int K, int O, float* out) {
-  LoadKInner la{G, R, K, K, aligned16(G) && K % 4 == 0};
-  LoadKInner lb{Wt, N, K, K, aligned16(Wt) && K % 4 == 0};
+  using L = LoadKInnerT<VEC>;
+  L la{G, R, K, K};
+  L lb{Wt, N, K, K};
   const int tn = cdiv(N, Cfg::BN), tm = cdiv(R, Cfg::BM);
-  hipError_t e = set_smem<Cfg, LoadKInner, LoadKInner>((const void*)k_dense_bwd<Cfg>);
+  hipError_t e = set_smem<Cfg, L, L>((const void*)k_dense_bwd<Cfg, VEC>);
   if (e != hipSuccess) return e;
-  k_dense_bwd<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LoadKInner, LoadKInner>(), s>>>(la, lb, dphi, R, N, O, out, tn);
+  k_dense_bwd<Cfg, VEC><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, L, L>(), s>>>(
+      la, lb, dphi, R, N, FastDiv((uint32_t)O), out, tn);
   return hipGetLastError();
 }
 
 hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, const float* dphi,
                             int R, int N, int K, int O, float* out) {
   const long long big_tiles = (long long)cdiv(R, 128) * cdiv(N, 128);
-  if (big_tiles >= 512) return dense_bwd_cfg<CfgBig>(s, G, Wt, dphi, R, N, K, O, out);
-  return dense_bwd_cfg<CfgSmall>(s, G, Wt, dphi, R, N, K, O, out);
+  const bool v = vec_ok(G, K, K) && vec_ok(Wt, K, K);
+  if (big_tiles >= 512)
+    return v ? dense_bwd_cfg<CfgBig, true>(s, G, Wt, dphi, R, N, K, O, out)
+             : dense_bwd_cfg<CfgBig, false>(s, G, Wt, dphi, R, N, K, O, out);
+  return v ? dense_bwd_cfg<CfgSmall, true>(s, G, Wt, dphi, R, N, K, O, out)
+           : dense_bwd_cfg<CfgSmall, false>(s, G, Wt, dphi, R, N, K, O, out);
 }
 
 // ------------------------------------------------------------------------------ seed, transpose
@@ -157,7 +175,7 @@ hipError_t launch_transpose(hipStream_t s, const float* W, int R, int C, float* 
 }
 
 // ------------------------------------------------------------------------------ Grams
-template <class Cfg>
+template <class Cfg, bool VEC>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_gram(GramBatch g, int N1, int N2, int tiles_n) {
   extern __shared__ float smem[];
@@ -165,10 +183,8 @@ k_gram(GramBatch g, int N1, int N2, int tiles_n) {
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   const int K = g.K[z];
-  const bool vec = (K % 4 == 0) && ((reinterpret_cast<uintptr_t>(g.h1[z]) & 15) == 0) &&
-                   ((reinterpret_cast<uintptr_t>(g.h2[z]) & 15) == 0);
-  LoadKInner la{g.h1[z], N1, K, K, vec};
-  LoadKInner lb{g.h2[z], N2, K, K, vec};
+  LoadKInnerT<VEC> la{g.h1[z], N1, K, K};
+  LoadKInnerT<VEC> lb{g.h2[z], N2, K, K};
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
   gemm_mainloop<Cfg>(la, lb, m0, n0, 0, K, smem, acc);
@@ -179,13 +195,23 @@ k_gram(GramBatch g, int N1, int N2, int tiles_n) {
   });
 }
 
-hipError_t launch_gram(hipStream_t s, const GramBatch& g, int N1, int N2) {
+template <bool VEC>
+static hipError_t gram_vec(hipStream_t s, const GramBatch& g, int N1, int N2) {
   using Cfg = CfgSmall;
+  using L = LoadKInnerT<VEC>;
   const int tn = cdiv(N2, Cfg::BN), tm = cdiv(N1, Cfg::BM);
-  hipError_t e = set_smem<Cfg, LoadKInner, LoadKInner>((const void*)k_gram<Cfg>);
+  hipError_t e = set_smem<Cfg, L, L>((const void*)k_gram<Cfg, VEC>);
   if (e != hipSuccess) return e;
-  k_gram<Cfg><<<dim3(tm * tn, g.count), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LoadKInner, LoadKInner>(), s>>>(g, N1, N2, tn);
+  k_gram<Cfg, VEC><<<dim3(tm * tn, g.count), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, L, L>(), s>>>(
+      g, N1, N2, tn);
   return hipGetLastError();
+}
+
+hipError_t launch_gram(hipStream_t s, const GramBatch& g, int N1, int N2) {
+  bool v = true;
+  for (int z = 0; z < g.count; ++z)
+    v = v && vec_ok(g.h1[z], g.K[z], g.K[z]) && vec_ok(g.h2[z], g.K[z], g.K[z]);
+  return v ? gram_vec<true>(s, g, N1, N2) : gram_vec<false>(s, g, N1, N2);
 }
 
 // ------------------------------------------------------------------------------ fused contraction
@@ -200,9 +226,28 @@ __device__ __forceinline__ void tri_index(int t, int nt, int& tm, int& tn) {
   tn = r + (t - base);
 }
 
+// Stage the block of a Gram matrix that a tile touches (rows r cover samples r / O) into
+// LDS: sg[a * S2 + b] = gram[n1lo + a][n2lo + b].  Ends with a barrier.
 template <class Cfg>
+__device__ __forceinline__ void stage_gram(const float* __restrict__ gram, int N2, int R1, int R2,
+                                           FastDiv fO, int m0, int n0, float* sg, int& n1lo,
+                                           int& n2lo, int& S2) {
+  n1lo = (int)fO.div(m0);
+  n2lo = (int)fO.div(n0);
+  const int n1hi = (int)fO.div(min(m0 + Cfg::BM, R1) - 1);
+  const int n2hi = (int)fO.div(min(n0 + Cfg::BN, R2) - 1);
+  const int S1 = n1hi - n1lo + 1;
+  S2 = n2hi - n2lo + 1;
+  for (int q = threadIdx.x; q < S1 * S2; q += Cfg::THREADS) {
+    const int a = q / S2, b = q - a * S2;
+    sg[q] = gram[(long long)(n1lo + a) * N2 + n2lo + b];
+  }
+  __syncthreads();
+}
+
+template <class Cfg, bool VEC>
 __global__ void __launch_bounds__(Cfg::THREADS)
-k_ntk_fcn(FcnContraction c, int N1, int N2, int O, int symmetric, float* __restrict__ theta,
+k_ntk_fcn(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __restrict__ theta,
           int tiles_m, int tiles_n) {
   extern __shared__ float smem[];
   int tm, tn;
@@ -212,66 +257,86 @@ k_ntk_fcn(FcnContraction c, int N1, int N2, int O, int symmetric, float* __restr
     tm = blockIdx.x / tiles_n;
     tn = blockIdx.x % tiles_n;
   }
+  const int O = (int)fO.d;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   const int R1 = N1 * O, R2 = N2 * O;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM, wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
 
   f32x16 tot[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(tot);
   for (int l = 0; l < c.L; ++l) {
     const int K = c.K[l];
-    const bool vec = (K % 4 == 0) && ((reinterpret_cast<uintptr_t>(c.G1[l]) & 15) == 0) &&
-                     ((reinterpret_cast<uintptr_t>(c.G2[l]) & 15) == 0);
-    LoadKInner la{c.G1[l], R1, K, K, vec};
-    LoadKInner lb{c.G2[l], R2, K, K, vec};
+    LoadKInnerT<VEC> la{c.G1[l], R1, K, K};
+    LoadKInnerT<VEC> lb{c.G2[l], R2, K, K};
     f32x16 acc[Cfg::FM][Cfg::FN];
     zero_acc<Cfg>(acc);
     gemm_mainloop<Cfg>(la, lb, m0, n0, 0, K, smem, acc);
-    const float* gram = c.gram[l];
-    // tot += gram_l[n1, n2] * acc   (the scalar x1.x2 of Eq. mixed_product_example)
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM, wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
+    // tot += gram_l[n1, n2] * acc  (the scalar x1.x2 of Eq. mixed_product_example); the
+    // tile's Gram block is staged in the LDS tile area, free after the main loop
+    int n1lo, n2lo, S2;
+    stage_gram<Cfg>(c.gram[l], N2, R1, R2, fO, m0, n0, smem, n1lo, n2lo, S2);
 #pragma unroll
     for (int fn = 0; fn < Cfg::FN; ++fn) {
-      const int s = n0 + wn0 + fn * 32 + (lane & 31);
-      const int n2 = s < R2 ? s / O : 0;
+      const int s = min(n0 + wn0 + fn * 32 + (lane & 31), R2 - 1);
+      const int b = (int)fO.div(s) - n2lo;
 #pragma unroll
-      for (int fm = 0; fm < Cfg::FM; ++fm)
+      for (int fm = 0; fm < Cfg::FM; ++fm) {
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int r = m0 + wm0 + fm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
-          const int n1 = r < R1 ? r / O : 0;
-          tot[fm][fn][v] += gram[(long long)n1 * N2 + n2] * acc[fm][fn][v];
+          const int r = min(m0 + wm0 + fm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3), R1 - 1);
+          const int a = (int)fO.div(r) - n1lo;
+          tot[fm][fn][v] += smem[a * S2 + b] * acc[fm][fn][v];
         }
+        // keep one fragment's Gram values live at a time (register pressure)
+        __builtin_amdgcn_sched_barrier(0);
+      }
     }
+    __syncthreads();
   }
-  const float* gro = c.gram_readout;
+  int n1lo, n2lo, S2;
+  stage_gram<Cfg>(c.gram_readout, N2, R1, R2, fO, m0, n0, smem, n1lo, n2lo, S2);
   const bool mirror = symmetric && tm != tn;
   for_each_acc<Cfg>(tot, m0, n0, [&](int r, int s, float v) {
     if (r < R1 && s < R2) {
-      const int n1 = r / O, o1 = r - n1 * O;
-      const int n2 = s / O, o2 = s - n2 * O;
-      if (o1 == o2) v += gro[(long long)n1 * N2 + n2];
+      const int n1 = (int)fO.div(r), o1 = r - n1 * O;
+      const int n2 = (int)fO.div(s), o2 = s - n2 * O;
+      if (o1 == o2) v += smem[(n1 - n1lo) * S2 + (n2 - n2lo)];
       theta[(((long long)n1 * N2 + n2) * O + o1) * O + o2] = v;
       if (mirror) theta[(((long long)n2 * N1 + n1) * O + o2) * O + o1] = v;
     }
   });
 }
 
+// The staged Gram block is at most (BM/O + 2) x (BN/O + 2) floats, and BM x BN for O = 1;
+// it must fit the LDS tile area.
+template <class Cfg, class L>
+constexpr bool gram_block_fits() {
+  return (Cfg::BM + 1) * (Cfg::BN + 1) <= gemm_smem_bytes<Cfg, L, L>() / 4;
+}
+
 hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2, int O,
                           int symmetric, float* theta) {
   const int R1 = N1 * O, R2 = N2 * O;
-  auto go = [&](auto cfg_tag) -> hipError_t {
+  bool v = true;
+  for (int l = 0; l < c.L; ++l)
+    v = v && vec_ok(c.G1[l], c.K[l], c.K[l]) && vec_ok(c.G2[l], c.K[l], c.K[l]);
+  auto go = [&](auto cfg_tag, auto vec_tag) -> hipError_t {
     using Cfg = decltype(cfg_tag);
+    constexpr bool VEC = decltype(vec_tag)::value;
+    using L = LoadKInnerT<VEC>;
+    static_assert(gram_block_fits<Cfg, L>(), "Gram block must fit the LDS tile area");
     const int tm = cdiv(R1, Cfg::BM), tn = cdiv(R2, Cfg::BN);
     const int tiles = symmetric ? tn * (tn + 1) / 2 : tm * tn;
-    hipError_t e = set_smem<Cfg, LoadKInner, LoadKInner>((const void*)k_ntk_fcn<Cfg>);
+    hipError_t e = set_smem<Cfg, L, L>((const void*)k_ntk_fcn<Cfg, VEC>);
     if (e != hipSuccess) return e;
-    k_ntk_fcn<Cfg><<<dim3(tiles), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LoadKInner, LoadKInner>(), s>>>(c, N1, N2, O, symmetric, theta, tm, tn);
+    k_ntk_fcn<Cfg, VEC><<<dim3(tiles), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, L, L>(), s>>>(
+        c, N1, N2, FastDiv((uint32_t)O), symmetric, theta, tm, tn);
     return hipGetLastError();
   };
   const long long big_tiles = (long long)cdiv(R1, 128) * cdiv(R2, 128);
-  if (big_tiles >= 512) return go(CfgBig{});
-  return go(CfgSmall{});
+  if (big_tiles >= 512) return v ? go(CfgBig{}, TrueT{}) : go(CfgBig{}, FalseT{});
+  return v ? go(CfgSmall{}, TrueT{}) : go(CfgSmall{}, FalseT{});
 }
 
 }  // namespace ntk
