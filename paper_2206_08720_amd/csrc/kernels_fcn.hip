@@ -19,6 +19,7 @@
 namespace ntk {
 
 using CfgBig = TileCfg<128, 128, 32, 64, 64>;   // 4 waves, 64x64 per wave
+using CfgBig8 = TileCfg<128, 128, 32, 32, 64>;  // 8 waves, 32x64 per wave
 using CfgSmall = TileCfg<64, 64, 32, 32, 32>;   // 4 waves, 32x32 per wave
 using TrueT = std::true_type;
 using FalseT = std::false_type;
@@ -126,8 +127,8 @@ hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, cons
   const long long big_tiles = (long long)cdiv(R, 128) * cdiv(N, 128);
   const bool v = vec_ok(G, K, K) && vec_ok(Wt, K, K);
   if (big_tiles >= 512)
-    return v ? dense_bwd_cfg<CfgBig, true>(s, G, Wt, dphi, R, N, K, O, out)
-             : dense_bwd_cfg<CfgBig, false>(s, G, Wt, dphi, R, N, K, O, out);
+    return v ? dense_bwd_cfg<CfgBig8, true>(s, G, Wt, dphi, R, N, K, O, out)
+             : dense_bwd_cfg<CfgBig8, false>(s, G, Wt, dphi, R, N, K, O, out);
   return v ? dense_bwd_cfg<CfgSmall, true>(s, G, Wt, dphi, R, N, K, O, out)
            : dense_bwd_cfg<CfgSmall, false>(s, G, Wt, dphi, R, N, K, O, out);
 }
@@ -335,7 +336,7 @@ hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2
     return hipGetLastError();
   };
   const long long big_tiles = (long long)cdiv(R1, 128) * cdiv(R2, 128);
-  if (big_tiles >= 512) return v ? go(CfgBig{}, TrueT{}) : go(CfgBig{}, FalseT{});
+  if (big_tiles >= 512) return v ? go(CfgBig8{}, TrueT{}) : go(CfgBig8{}, FalseT{});
   return v ? go(CfgSmall{}, TrueT{}) : go(CfgSmall{}, FalseT{});
 }
 
