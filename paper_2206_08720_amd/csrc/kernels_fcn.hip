@@ -309,6 +309,151 @@ k_ntk_fcn(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __
   });
 }
 
+// ------------------------------------------------------------------------------ stream-K contraction
+// The contraction's work is T tiles x L layers.  With whole tiles per workgroup, T / #CU is
+// rarely an integer (1600 / 256 = 6.25 for the depth-8 width-2048 FCN) and the last round
+// leaves most compute units idle.  Here P persistent workgroups (one per compute unit) take
+// equal contiguous ranges of the T*L (tile, layer) units.  A workgroup that covers all
+// layers of a tile writes theta directly; a tile split between workgroups has its per-range
+// partial sums stored in `part` (slot 0: the first tile of a range, slot 1: its last tile),
+// and k_ntk_fcn_fixup adds them in range order.  No workgroup waits for another.
+__device__ __forceinline__ long long sk_start(int lam, long long U, int P) {
+  return (long long)lam * U / P;
+}
+
+template <class Cfg>
+__device__ __forceinline__ void tile_coords(int t, int symmetric, int tiles_n, int& tm, int& tn) {
+  if (symmetric) {
+    tri_index(t, tiles_n, tm, tn);
+  } else {
+    tm = t / tiles_n;
+    tn = t - tm * tiles_n;
+  }
+}
+
+// Final epilogue of a tile: add the readout summand, write theta (and its mirror).
+template <class Cfg>
+__device__ __forceinline__ void fcn_tile_out(f32x16 (&tot)[Cfg::FM][Cfg::FN], const float* gram_readout,
+                                             int N1, int N2, FastDiv fO, int R1, int R2, int m0, int n0,
+                                             bool mirror, float* smem, float* __restrict__ theta) {
+  const int O = (int)fO.d;
+  int n1lo, n2lo, S2;
+  stage_gram<Cfg>(gram_readout, N2, R1, R2, fO, m0, n0, smem, n1lo, n2lo, S2);
+  for_each_acc<Cfg>(tot, m0, n0, [&](int r, int s, float v) {
+    if (r < R1 && s < R2) {
+      const int n1 = (int)fO.div(r), o1 = r - n1 * O;
+      const int n2 = (int)fO.div(s), o2 = s - n2 * O;
+      if (o1 == o2) v += smem[(n1 - n1lo) * S2 + (n2 - n2lo)];
+      theta[(((long long)n1 * N2 + n2) * O + o1) * O + o2] = v;
+      if (mirror) theta[(((long long)n2 * N1 + n1) * O + o2) * O + o1] = v;
+    }
+  });
+  __syncthreads();
+}
+
+template <class Cfg, bool VEC>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_ntk_fcn_sk(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __restrict__ theta,
+             int tiles_n, int T, int P, float* __restrict__ part) {
+  extern __shared__ float smem[];
+  // XCD-aware order: consecutive workgroup ids go to different XCDs (round robin), so range
+  // lam = (bid % 8) * (P / 8) + bid / 8 gives each XCD a contiguous band of tiles (shared
+  // operand panels stay in that XCD's L2).  P is a multiple of 8.
+  const int bid = blockIdx.x;
+  const int lam = (bid & 7) * (P >> 3) + (bid >> 3);
+  const int L = c.L;
+  const long long U = (long long)T * L;
+  const long long beg = sk_start(lam, U, P), end = sk_start(lam + 1, U, P);
+  const int O = (int)fO.d;
+  const int R1 = N1 * O, R2 = N2 * O;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM, wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
+  const int first_tile = (int)(beg / L);
+  for (long long u = beg; u < end;) {
+    const int t = (int)(u / L);
+    const int l0 = (int)(u - (long long)t * L);
+    const int l1 = (int)min((long long)L, l0 + (end - u));
+    int tm, tn;
+    tile_coords<Cfg>(t, symmetric, tiles_n, tm, tn);
+    const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+    f32x16 tot[Cfg::FM][Cfg::FN];
+    zero_acc<Cfg>(tot);
+    for (int l = l0; l < l1; ++l) {
+      const int K = c.K[l];
+      LoadKInnerT<VEC> la{c.G1[l], R1, K, K};
+      LoadKInnerT<VEC> lb{c.G2[l], R2, K, K};
+      f32x16 acc[Cfg::FM][Cfg::FN];
+      zero_acc<Cfg>(acc);
+      gemm_mainloop<Cfg>(la, lb, m0, n0, 0, K, smem, acc);
+      int n1lo, n2lo, S2;
+      stage_gram<Cfg>(c.gram[l], N2, R1, R2, fO, m0, n0, smem, n1lo, n2lo, S2);
+#pragma unroll
+      for (int fn = 0; fn < Cfg::FN; ++fn) {
+        const int sc = min(n0 + wn0 + fn * 32 + (lane & 31), R2 - 1);
+        const int b = (int)fO.div(sc) - n2lo;
+#pragma unroll
+        for (int fm = 0; fm < Cfg::FM; ++fm) {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int r = min(m0 + wm0 + fm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3), R1 - 1);
+            const int a = (int)fO.div(r) - n1lo;
+            tot[fm][fn][v] += smem[a * S2 + b] * acc[fm][fn][v];
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        }
+      }
+      __syncthreads();
+    }
+    if (l0 == 0 && l1 == L) {
+      fcn_tile_out<Cfg>(tot, c.gram_readout, N1, N2, fO, R1, R2, m0, n0, symmetric && tm != tn, smem,
+                        theta);
+    } else {
+      float* dst = part + ((long long)lam * 2 + (t == first_tile ? 0 : 1)) * (Cfg::BM * Cfg::BN);
+      for_each_acc<Cfg>(tot, 0, 0, [&](int i, int j, float v) { dst[i * Cfg::BN + j] = v; });
+    }
+    u += l1 - l0;
+  }
+}
+
+// One workgroup per range boundary lam = 1..P-1: if the boundary falls inside a tile and is
+// the first boundary inside it, sum that tile's partials (ranges in order) and write it.
+template <class Cfg>
+__global__ void __launch_bounds__(256)
+k_ntk_fcn_fixup(int L, const float* __restrict__ gram_readout, int N1, int N2, FastDiv fO,
+                int symmetric, float* __restrict__ theta, int tiles_n, int T, int P,
+                const float* __restrict__ part) {
+  const int lam = blockIdx.x + 1;
+  const long long U = (long long)T * L;
+  const long long b = sk_start(lam, U, P);
+  if (b >= U || b % L == 0) return;
+  const int t = (int)(b / L);
+  if (sk_start(lam - 1, U, P) > (long long)t * L) return;   // an earlier boundary owns tile t
+  int tm, tn;
+  tile_coords<Cfg>(t, symmetric, tiles_n, tm, tn);
+  const int O = (int)fO.d;
+  const int R1 = N1 * O, R2 = N2 * O;
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  const bool mirror = symmetric && tm != tn;
+  const long long tile_end = (long long)(t + 1) * L;
+  for (int e = threadIdx.x; e < Cfg::BM * Cfg::BN; e += 256) {
+    const int i = e / Cfg::BN, j = e - i * Cfg::BN;
+    const int r = m0 + i, s = n0 + j;
+    float v = 0.f;
+    for (int q = lam - 1; q < P && sk_start(q, U, P) < tile_end; ++q) {
+      if (sk_start(q + 1, U, P) <= sk_start(q, U, P)) continue;   // empty range: wrote nothing
+      const int slot = (sk_start(q, U, P) / L == t) ? 0 : 1;
+      v += part[((long long)q * 2 + slot) * (Cfg::BM * Cfg::BN) + e];
+    }
+    if (r < R1 && s < R2) {
+      const int n1 = (int)fO.div(r), o1 = r - n1 * O;
+      const int n2 = (int)fO.div(s), o2 = s - n2 * O;
+      if (o1 == o2) v += gram_readout[(long long)n1 * N2 + n2];
+      theta[(((long long)n1 * N2 + n2) * O + o1) * O + o2] = v;
+      if (mirror) theta[(((long long)n2 * N1 + n1) * O + o2) * O + o1] = v;
+    }
+  }
+}
+
 // The staged Gram block is at most (BM/O + 2) x (BN/O + 2) floats, and BM x BN for O = 1;
 // it must fit the LDS tile area.
 template <class Cfg, class L>
@@ -316,8 +461,12 @@ constexpr bool gram_block_fits() {
   return (Cfg::BM + 1) * (Cfg::BN + 1) <= gemm_smem_bytes<Cfg, L, L>() / 4;
 }
 
+long long ntk_fcn_part_floats(int num_cu) {
+  return (long long)num_cu * 2 * CfgBig8::BM * CfgBig8::BN;
+}
+
 hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2, int O,
-                          int symmetric, float* theta) {
+                          int symmetric, float* theta, int num_cu, float* part) {
   const int R1 = N1 * O, R2 = N2 * O;
   bool v = true;
   for (int l = 0; l < c.L; ++l)
@@ -335,7 +484,29 @@ hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2
         c, N1, N2, FastDiv((uint32_t)O), symmetric, theta, tm, tn);
     return hipGetLastError();
   };
+  auto go_sk = [&](auto vec_tag) -> hipError_t {
+    using Cfg = CfgBig8;
+    constexpr bool VEC = decltype(vec_tag)::value;
+    using L = LoadKInnerT<VEC>;
+    const int tm = cdiv(R1, Cfg::BM), tn = cdiv(R2, Cfg::BN);
+    const int T = symmetric ? tn * (tn + 1) / 2 : tm * tn;
+    const int P = num_cu;
+    hipError_t e = set_smem<Cfg, L, L>((const void*)k_ntk_fcn_sk<Cfg, VEC>);
+    if (e != hipSuccess) return e;
+    const FastDiv fO((uint32_t)O);
+    k_ntk_fcn_sk<Cfg, VEC><<<dim3(P), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, L, L>(), s>>>(
+        c, N1, N2, fO, symmetric, theta, tn, T, P, part);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    k_ntk_fcn_fixup<Cfg><<<dim3(P - 1), dim3(256), 0, s>>>(c.L, c.gram_readout, N1, N2, fO, symmetric,
+                                                           theta, tn, T, P, part);
+    return hipGetLastError();
+  };
   const long long big_tiles = (long long)cdiv(R1, 128) * cdiv(R2, 128);
+  // stream-K when there are at least as many whole tiles as compute units (P must be a
+  // multiple of 8 for the XCD-aware range order)
+  if (c.L >= 1 && part && num_cu >= 8 && num_cu % 8 == 0 && big_tiles >= num_cu)
+    return v ? go_sk(TrueT{}) : go_sk(FalseT{});
   if (big_tiles >= 512) return v ? go(CfgBig8{}, TrueT{}) : go(CfgBig8{}, FalseT{});
   return v ? go(CfgSmall{}, TrueT{}) : go(CfgSmall{}, FalseT{});
 }

@@ -66,7 +66,10 @@ struct FcnContraction {
 // theta[n1, n2, o1, o2] = sum_l gram_l[n1,n2] (G1_l G2_l^T)[(n1,o1),(n2,o2)]
 //                         + gram_readout[n1,n2] delta_{o1 o2}.
 // symmetric != 0: batch 2 is batch 1; only upper-triangle tiles run and mirror.
+// Large problems use a stream-K schedule over num_cu persistent workgroups with a partial
+// buffer `part` of ntk_fcn_part_floats(num_cu) floats (part may be null: no stream-K).
+long long ntk_fcn_part_floats(int num_cu);
 hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2, int O,
-                          int symmetric, float* theta);
+                          int symmetric, float* theta, int num_cu, float* part);
 
 }  // namespace ntk

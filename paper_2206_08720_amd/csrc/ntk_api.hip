@@ -103,6 +103,8 @@ struct ntk_handle {
   std::vector<size_t> off_Wt;     // Wt_l,   l = 1..L-1    [d_l, d_{l+1}]
   std::vector<size_t> off_gram;   // gram_l, l = 0..L      [max_n1*max_n2]
   std::vector<int> param_index;   // first parameter slot of dense layer l
+  int num_cu = 0;                 // compute units of the device (stream-K workgroup count)
+  size_t off_skpart = 0;          // stream-K partial tiles of the contraction
 
   // ---- convolutional plan: conv layers 0..nc-1, GAP, dense readout
   int nc = 0, H = 0, W = 0, D = 0;
@@ -216,6 +218,7 @@ static void plan_fcn(ntk_handle* h) {
   for (int l = 0; l < L; ++l) h->off_G[l] = take(Mmax * O * h->dims[l + 1]);
   for (int l = 1; l < L; ++l) h->off_Wt[l] = take((size_t)h->dims[l] * h->dims[l + 1]);
   for (int l = 0; l <= L; ++l) h->off_gram[l] = take((size_t)h->max_n1 * h->max_n2);
+  h->off_skpart = take((size_t)ntk_fcn_part_floats(h->num_cu));
   h->ws_bytes = off;
   h->param_index.assign(L + 1, 0);
   int p = 0;
@@ -290,15 +293,20 @@ extern "C" int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, voi
   h->max_n1 = max_n1;
   h->max_n2 = max_n2;
   h->stream = (hipStream_t)hip_stream;
-  if (h->cnn)
-    plan_cnn(h);
-  else
-    plan_fcn(h);
   hipError_t e = hipGetDevice(&h->device);
   if (e != hipSuccess) {
     delete h;
     return hip_fail(nullptr, e, "hipGetDevice");
   }
+  e = hipDeviceGetAttribute(&h->num_cu, hipDeviceAttributeMultiprocessorCount, h->device);
+  if (e != hipSuccess) {
+    delete h;
+    return hip_fail(nullptr, e, "hipDeviceGetAttribute");
+  }
+  if (h->cnn)
+    plan_cnn(h);
+  else
+    plan_fcn(h);
   e = hipMalloc((void**)&h->ws, h->ws_bytes);
   if (e != hipSuccess) {
     (void)hipGetLastError();
@@ -395,7 +403,7 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   }
   c.gram_readout = F(h->off_gram[L]);
   prof_begin(P, s, KC_NTK_FCN);
-  e = launch_ntk_fcn(s, c, n1, n2, O, sym ? 1 : 0, theta);
+  e = launch_ntk_fcn(s, c, n1, n2, O, sym ? 1 : 0, theta, h->num_cu, F(h->off_skpart));
   prof_end(P, s, KC_NTK_FCN);
   if (e != hipSuccess) return hip_fail(h, e, "ntk contraction");
   return NTK_OK;

@@ -162,3 +162,34 @@ def test_argument_errors_leave_output_untouched():
         assert bool((out == 7.0).all())
     finally:
         h.close()
+
+
+# ---- stream-K schedule of the contraction (used once the output has >= one tile per CU) ----
+SK_CASES = [
+    # label, spec, n1, n2, X2 is X1
+    # symmetric: 17 x 17 tiles -> 153 triangle tiles x 8 layers over 256 ranges, so a tile
+    # spans 2-3 ranges
+    ("tiles over 3 ranges, 8 hidden layers, symmetric", wl.fcn_spec("sk1", 24, [64] * 8, 10), 205, 205, True),
+    ("split tiles, 2 hidden layers, symmetric", wl.fcn_spec("sk1b", 24, [64, 64], 10), 256, 256, True),
+    # one hidden layer: a unit is a whole tile (no splits); 153 units over 256 ranges leaves
+    # empty ranges
+    ("one hidden layer, symmetric, empty ranges", wl.fcn_spec("sk2", 16, [24], 10, bias=True),
+     205, 205, True),
+    ("ragged R1 != R2, 3 layers", wl.fcn_spec("sk3", 20, [48, 40], 8, act="erf", bias=True), 300, 250, False),
+    ("8 hidden layers, R1 != R2", wl.fcn_spec("sk4", 12, [32] * 8, 9), 240, 231, False),
+]
+
+
+@pytest.mark.parametrize("case", SK_CASES, ids=[c[0] for c in SK_CASES])
+def test_stream_k_contraction(case):
+    label, spec, n1, n2, alias = case
+    params = wl.make_params(spec, 900 + n1, bias_var=0.2)
+    X1 = wl.make_inputs(spec, n1, 910 + n1)
+    X2 = X1 if alias else wl.make_inputs(spec, n2, 920 + n2)
+    O = spec["layers"][-1]["out"]
+    assert (n1 * O // 128) * (n2 * O // 128) >= 256, "case must take the stream-K path"
+    got = _vs_jc(f"stream-K {label}", spec, params, X1, X2)
+    if alias:
+        N = got.shape[0]
+        M = got.transpose(0, 2, 1, 3).reshape(N * O, N * O)
+        np.testing.assert_allclose(M, M.T, rtol=0, atol=1e-5 * np.abs(M).max())
