@@ -20,7 +20,9 @@ namespace ntk {
 
 using CfgBig = TileCfg<128, 128, 32, 64, 64>;   // 4 waves, 64x64 per wave
 using CfgBig8 = TileCfg<128, 128, 32, 32, 64>;  // 8 waves, 32x64 per wave
+using CfgSK = CfgBig8;                          // stream-K contraction
 using CfgSmall = TileCfg<64, 64, 32, 32, 32>;   // 4 waves, 32x32 per wave
+using CfgFwd64 = TileCfg<64, 64, 32, 32, 16>;   // fp64 forward: 8 waves, 32x16 per wave
 using TrueT = std::true_type;
 using FalseT = std::false_type;
 
@@ -83,29 +85,43 @@ static hipError_t dense_fwd_cfg(hipStream_t s, const float* h, const float* W, c
 hipError_t launch_dense_fwd(hipStream_t s, const float* h, const float* W, const float* b, int M,
                             int N, int K, int act, float* hn, float* dphi) {
   if (vec_ok(h, K, K) && vec_ok(W, K, K))
-    return dense_fwd_cfg<CfgSmall, true>(s, h, W, b, M, N, K, act, hn, dphi);
-  return dense_fwd_cfg<CfgSmall, false>(s, h, W, b, M, N, K, act, hn, dphi);
+    return dense_fwd_cfg<CfgFwd64, true>(s, h, W, b, M, N, K, act, hn, dphi);
+  return dense_fwd_cfg<CfgFwd64, false>(s, h, W, b, M, N, K, act, hn, dphi);
 }
 
 // ------------------------------------------------------------------------------ backward
+// out[r, c] = acc[r, c] * dphi[r / O, c]
+struct EpiBwd {
+  const float* dphi;
+  float* out;
+  int R, N;
+  FastDiv fO;
+  template <class Cfg>
+  __device__ __forceinline__ void tile(f32x16 (&acc)[Cfg::FM][Cfg::FN], int m0, int n0) const {
+    float g[Cfg::FM][Cfg::FN][16];
+    gather_acc<Cfg>(g, m0, n0, [&](int r, int c) {
+      const int rc = min(r, R - 1), cc = min(c, N - 1);
+      return dphi[(long long)fO.div(rc) * N + cc];
+    });
+    for_each_acc_aux<Cfg>(acc, g, m0, n0, [&](int r, int c, float v, float d) {
+      if (r < R && c < N) out[(long long)r * N + c] = v * d;
+    });
+  }
+  __device__ __forceinline__ void elem(int r, int c, float v) const {
+    if (r < R && c < N) out[(long long)r * N + c] = v * dphi[(long long)fO.div(r) * N + c];
+  }
+};
+
 template <class Cfg, bool VEC>
 __global__ void __launch_bounds__(Cfg::THREADS)
-k_dense_bwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restrict__ dphi, int R, int N,
-            FastDiv fO, float* __restrict__ out, int tiles_n) {
+k_dense_bwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, EpiBwd epi, int tiles_n) {
   extern __shared__ float smem[];
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
   gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
-  float g[Cfg::FM][Cfg::FN][16];
-  gather_acc<Cfg>(g, m0, n0, [&](int r, int c) {
-    const int rc = min(r, R - 1), cc = min(c, N - 1);
-    return dphi[(long long)fO.div(rc) * N + cc];
-  });
-  for_each_acc_aux<Cfg>(acc, g, m0, n0, [&](int r, int c, float v, float d) {
-    if (r < R && c < N) out[(long long)r * N + c] = v * d;
-  });
+  epi.template tile<Cfg>(acc, m0, n0);
 }
 
 template <class Cfg, bool VEC>
@@ -114,14 +130,19 @@ static hipError_t dense_bwd_cfg(hipStream_t s, const float* G, const float* Wt, 
   using L = LoadKInnerT<VEC>;
   L la{G, R, K, K};
   L lb{Wt, N, K, K};
+  EpiBwd epi{dphi, out, R, N, FastDiv((uint32_t)O)};
   const int tn = cdiv(N, Cfg::BN), tm = cdiv(R, Cfg::BM);
   hipError_t e = set_smem<Cfg, L, L>((const void*)k_dense_bwd<Cfg, VEC>);
   if (e != hipSuccess) return e;
   k_dense_bwd<Cfg, VEC><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, L, L>(), s>>>(
-      la, lb, dphi, R, N, FastDiv((uint32_t)O), out, tn);
+      la, lb, epi, tn);
   return hipGetLastError();
 }
 
+// Two 8-wave workgroups share a compute unit (4 waves per SIMD).  A stream-K schedule with one
+// workgroup per compute unit removes the partial last round (1280 tiles over 512 slots at the
+// depth-8 width-2048 shape) but measured slower (113 vs 122 TFLOP/s): the extra waves per SIMD
+// are worth more than the tail here.
 hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, const float* dphi,
                             int R, int N, int K, int O, float* out) {
   const long long big_tiles = (long long)cdiv(R, 128) * cdiv(N, 128);
@@ -462,7 +483,7 @@ constexpr bool gram_block_fits() {
 }
 
 long long ntk_fcn_part_floats(int num_cu) {
-  return (long long)num_cu * 2 * CfgBig8::BM * CfgBig8::BN;
+  return (long long)num_cu * 2 * CfgSK::BM * CfgSK::BN;
 }
 
 hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2, int O,
@@ -485,7 +506,7 @@ hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2
     return hipGetLastError();
   };
   auto go_sk = [&](auto vec_tag) -> hipError_t {
-    using Cfg = CfgBig8;
+    using Cfg = CfgSK;
     constexpr bool VEC = decltype(vec_tag)::value;
     using L = LoadKInnerT<VEC>;
     const int tm = cdiv(R1, Cfg::BM), tn = cdiv(R2, Cfg::BN);
