@@ -22,7 +22,7 @@
 namespace ntk {
 
 using CfgConvF64 = TileCfg<64, 64, 32, 32, 32>;    // forward, fp64 MFMA
-using CfgConv = TileCfg<128, 64, 32, 64, 32>;      // backward / wgrad, fp32 MFMA
+using CfgConv = TileCfg<128, 64, 32, 32, 32>;      // backward / wgrad, fp32 MFMA: 8 waves
 using CfgSplitK = TileCfg<128, 128, 32, 64, 64>;   // J1 J2^T partial products
 
 static inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
