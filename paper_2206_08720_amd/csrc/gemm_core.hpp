@@ -406,3 +406,141 @@ struct FastDiv {
 };
 
 }  // namespace ntk
+
+namespace ntk {
+
+// ------------------------------------------------------------------------------ direct-to-LDS main loop
+// gfx950 loads global memory straight into LDS (global_load_lds_dwordx4): lane l of a wave
+// writes its 16 bytes at M0 + 16 l, so one instruction fills 1 KB of LDS with no register
+// staging and no ds_write.  Tiles are stored unpadded, [rows][BK] with BK = 32 (8 chunks of
+// 16 bytes per row), and the chunk c of row r sits at position c ^ ((r >> 1) & 7): the 16
+// rows read by a ds_read_b128 then hit 16 distinct 16-byte bank groups.  Three LDS stages:
+// tile kt + 2 is in flight while tile kt is multiplied, one barrier per K tile.
+//
+// Requirements (checked by the host): both operands K-contiguous with 16-byte aligned rows
+// (LoadKInnerT<true> conditions) and K % 32 == 0.  Rows past the operand are read from the
+// last row (clamped): they only feed output rows/columns that are discarded.
+constexpr int kDmaStages = 3;
+
+template <int ROWS>
+struct DmaTile {
+  static constexpr int BK = 32;
+  static constexpr int FLOATS = ROWS * BK;
+  __device__ static __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
+  // Issue this wave's share of the tile (rows split over the workgroup's waves, 8 rows per
+  // instruction).
+  template <int WAVES>
+  __device__ static __forceinline__ void issue(const float* __restrict__ p, long long ld, int rows,
+                                               int row0, int k0, float* lds, int wave, int lane) {
+    static_assert(ROWS % (8 * WAVES) == 0, "tile rows must split over the waves");
+#pragma unroll
+    for (int i = 0; i < ROWS / (8 * WAVES); ++i) {
+      const int r0 = (i * WAVES + wave) * 8;                 // first tile row of this instruction
+      const int r = r0 + (lane >> 3);
+      const int pos = lane & 7;
+      const int c = swz(r, pos);                              // global chunk stored at `pos`
+      const int gr = min(row0 + r, rows - 1);
+      const float* src = p + (long long)gr * ld + k0 + 4 * c;
+      float* dst = lds + __builtin_amdgcn_readfirstlane(r0 * BK);
+      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+    }
+  }
+  __device__ static __forceinline__ f32x4 frag(const float* lds, int row, int k) {
+    return *reinterpret_cast<const f32x4*>(&lds[row * BK + (swz(row, k >> 2) << 2)]);
+  }
+};
+
+template <class Cfg>
+__device__ __forceinline__ void mma_stage_dma(const float* As, const float* Bs,
+                                              f32x16 (&acc)[Cfg::FM][Cfg::FN], int wm0, int wn0,
+                                              int lane) {
+  using TA = DmaTile<Cfg::BM>;
+  using TB = DmaTile<Cfg::BN>;
+  const int lr = lane & 31, lk = (lane >> 5) * 4;
+  f32x4 a[2][Cfg::FM], b[2][Cfg::FN];
+#pragma unroll
+  for (int fm = 0; fm < Cfg::FM; ++fm) a[0][fm] = TA::frag(As, wm0 + fm * 32 + lr, lk);
+#pragma unroll
+  for (int fn = 0; fn < Cfg::FN; ++fn) b[0][fn] = TB::frag(Bs, wn0 + fn * 32 + lr, lk);
+#pragma unroll
+  for (int kk = 0; kk < 32; kk += 8) {
+    const int cur = (kk / 8) & 1;
+    if (kk + 8 < 32) {
+#pragma unroll
+      for (int fm = 0; fm < Cfg::FM; ++fm) a[cur ^ 1][fm] = TA::frag(As, wm0 + fm * 32 + lr, kk + 8 + lk);
+#pragma unroll
+      for (int fn = 0; fn < Cfg::FN; ++fn) b[cur ^ 1][fn] = TB::frag(Bs, wn0 + fn * 32 + lr, kk + 8 + lk);
+    }
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int fm = 0; fm < Cfg::FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < Cfg::FN; ++fn)
+          acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[cur][fm][t], b[cur][fn][t], acc[fm][fn], 0, 0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+  }
+}
+
+// s_waitcnt immediate (gfx9 encoding) that waits until at most n vector-memory operations of
+// this wave are outstanding and does not wait on the other counters.
+__device__ __forceinline__ void wait_vmcnt_dyn(int n) {
+  // the count must be an immediate: the few cases the pipeline needs
+  if (n <= 0) __builtin_amdgcn_s_waitcnt(0x0F70);
+  else if (n == 2) __builtin_amdgcn_s_waitcnt(0x0F72);
+  else if (n == 4) __builtin_amdgcn_s_waitcnt(0x0F74);
+  else if (n == 8) __builtin_amdgcn_s_waitcnt(0x0F78);
+  else __builtin_amdgcn_s_waitcnt(0x0F70);
+}
+
+template <class Cfg, int NSTAGE = kDmaStages>
+constexpr int gemm_dma_smem_bytes() {
+  return NSTAGE * (DmaTile<Cfg::BM>::FLOATS + DmaTile<Cfg::BN>::FLOATS) * 4;
+}
+
+// K loop over [k_begin, k_end) (both multiples of 32) for the tile (m0, n0), with NSTAGE LDS
+// stages (2: tile kt+1 in flight during tile kt; 3: tiles kt+1 and kt+2).  Ends with a
+// barrier, so the caller may reuse `smem` afterwards.
+template <class Cfg, int NSTAGE = kDmaStages>
+__device__ __forceinline__ void gemm_mainloop_dma(const float* __restrict__ A, long long lda, int rowsA,
+                                                  const float* __restrict__ B, long long ldb, int rowsB,
+                                                  int m0, int n0, int k_begin, int k_end, float* smem,
+                                                  f32x16 (&acc)[Cfg::FM][Cfg::FN]) {
+  static_assert(Cfg::BK == 32, "direct-to-LDS main loop uses BK = 32");
+  using TA = DmaTile<Cfg::BM>;
+  using TB = DmaTile<Cfg::BN>;
+  constexpr int STAGE = TA::FLOATS + TB::FLOATS;
+  constexpr int PER_TILE = Cfg::BM / (8 * Cfg::WAVES) + Cfg::BN / (8 * Cfg::WAVES);  // DMA ops per wave
+  const int tid = threadIdx.x;
+  const int lane = tid & 63, wave = tid >> 6;
+  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
+  const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
+  const int nk = (k_end - k_begin) / 32;
+  if (nk <= 0) return;
+  static_assert(NSTAGE == 2 || NSTAGE == 3, "two or three LDS stages");
+  auto issue = [&](int kt) {
+    float* st = smem + (kt % NSTAGE) * STAGE;
+    TA::template issue<Cfg::WAVES>(A, lda, rowsA, m0, k_begin + kt * 32, st, wave, lane);
+    TB::template issue<Cfg::WAVES>(B, ldb, rowsB, n0, k_begin + kt * 32, st + TA::FLOATS, wave, lane);
+  };
+  issue(0);
+  if (NSTAGE == 3 && nk > 1) issue(1);
+  for (int kt = 0; kt < nk; ++kt) {
+    // wait for this wave's loads of tile kt (with three stages tile kt+1's may stay in
+    // flight); a bare s_barrier (no fence, which would drain every outstanding load) then
+    // makes tile kt visible to every wave and guarantees all waves are done reading the stage
+    // that the next issue overwrites
+    if (NSTAGE == 3)
+      wait_vmcnt_dyn(kt + 1 < nk ? PER_TILE : 0);
+    else
+      wait_vmcnt_dyn(0);
+    __builtin_amdgcn_s_barrier();
+    __builtin_amdgcn_sched_barrier(0);
+    if (kt + NSTAGE - 1 < nk) issue(kt + NSTAGE - 1);
+    const float* st = smem + (kt % NSTAGE) * STAGE;
+    mma_stage_dma<Cfg>(st, st + TA::FLOATS, acc, wm0, wn0, lane);
+  }
+  __syncthreads();
+}
+
+}  // namespace ntk

@@ -112,7 +112,7 @@ struct EpiBwd {
   }
 };
 
-template <class Cfg, bool VEC>
+template <class Cfg, bool VEC, bool DMA>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_dense_bwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, EpiBwd epi, int tiles_n) {
   extern __shared__ float smem[];
@@ -120,11 +120,14 @@ k_dense_bwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, EpiBwd epi, int tiles_n) {
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
-  gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
+  if (DMA)
+    gemm_mainloop_dma<Cfg, 2>(la.p, la.ld, la.rows, lb.p, lb.ld, lb.rows, m0, n0, 0, la.K, smem, acc);
+  else
+    gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
   epi.template tile<Cfg>(acc, m0, n0);
 }
 
-template <class Cfg, bool VEC>
+template <class Cfg, bool VEC, bool DMA = false>
 static hipError_t dense_bwd_cfg(hipStream_t s, const float* G, const float* Wt, const float* dphi,
                                 int R, int N, int K, int O, float* out) {
   using L = LoadKInnerT<VEC>;
@@ -132,10 +135,11 @@ static hipError_t dense_bwd_cfg(hipStream_t s, const float* G, const float* Wt, 
   L lb{Wt, N, K, K};
   EpiBwd epi{dphi, out, R, N, FastDiv((uint32_t)O)};
   const int tn = cdiv(N, Cfg::BN), tm = cdiv(R, Cfg::BM);
-  hipError_t e = set_smem<Cfg, L, L>((const void*)k_dense_bwd<Cfg, VEC>);
+  constexpr int bytes = DMA ? gemm_dma_smem_bytes<Cfg, 2>() : gemm_smem_bytes<Cfg, L, L>();
+  hipError_t e = hipFuncSetAttribute((const void*)k_dense_bwd<Cfg, VEC, DMA>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   if (e != hipSuccess) return e;
-  k_dense_bwd<Cfg, VEC><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, L, L>(), s>>>(
-      la, lb, epi, tn);
+  k_dense_bwd<Cfg, VEC, DMA><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(la, lb, epi, tn);
   return hipGetLastError();
 }
 
@@ -147,9 +151,11 @@ hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, cons
                             int R, int N, int K, int O, float* out) {
   const long long big_tiles = (long long)cdiv(R, 128) * cdiv(N, 128);
   const bool v = vec_ok(G, K, K) && vec_ok(Wt, K, K);
-  if (big_tiles >= 512)
+  if (big_tiles >= 512) {
+    if (v && K % 32 == 0) return dense_bwd_cfg<CfgBig8, true, true>(s, G, Wt, dphi, R, N, K, O, out);
     return v ? dense_bwd_cfg<CfgBig8, true>(s, G, Wt, dphi, R, N, K, O, out)
              : dense_bwd_cfg<CfgBig8, false>(s, G, Wt, dphi, R, N, K, O, out);
+  }
   return v ? dense_bwd_cfg<CfgSmall, true>(s, G, Wt, dphi, R, N, K, O, out)
            : dense_bwd_cfg<CfgSmall, false>(s, G, Wt, dphi, R, N, K, O, out);
 }
@@ -331,25 +337,46 @@ k_ntk_fcn(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __
 }
 
 // ------------------------------------------------------------------------------ stream-K contraction
-// The contraction's work is T tiles x L layers.  With whole tiles per workgroup, T / #CU is
-// rarely an integer (1600 / 256 = 6.25 for the depth-8 width-2048 FCN) and the last round
-// leaves most compute units idle.  Here P persistent workgroups (one per compute unit) take
-// equal contiguous ranges of the T*L (tile, layer) units.  A workgroup that covers all
-// layers of a tile writes theta directly; a tile split between workgroups has its per-range
-// partial sums stored in `part` (slot 0: the first tile of a range, slot 1: its last tile),
-// and k_ntk_fcn_fixup adds them in range order.  No workgroup waits for another.
+// The contraction's work is T tiles x L layers over P persistent workgroups (one per compute
+// unit; P = 8 * P8, P8 per XCD).  Workgroup ids are dispatched round robin over the 8 XCDs,
+// each with its own L2, so the schedule is built per XCD:
+//   * tile order: the tile grid is cut into 8 bands of columns and ordered band by band,
+//     row by row inside a band; XCD x takes the x-th contiguous eighth of that order, so its
+//     workgroups share the B panels of a few columns for the whole launch;
+//   * data-parallel rounds: the XCD's P8 workgroups take whole tiles, P8 per round (the
+//     tiles of one round are neighbours and progress through the layers together);
+//   * stream-K tail: the XCD's last (T_x mod P8) tiles are cut into (tile, layer) units and
+//     split into P8 equal contiguous ranges.  A range covering all layers of a tile writes
+//     theta; a split tile's partial sums go to `part` (slot 0: the first tile of a range,
+//     slot 1: its last) and k_ntk_fcn_fixup adds them in range order.
+// No workgroup waits for another; the summation order is fixed for a given device.
 __device__ __forceinline__ long long sk_start(int lam, long long U, int P) {
   return (long long)lam * U / P;
 }
 
-template <class Cfg>
-__device__ __forceinline__ void tile_coords(int t, int symmetric, int tiles_n, int& tm, int& tn) {
+// Tile at position `ord` of the column-banded order (non-symmetric), or of the triangle order.
+__device__ __forceinline__ void tile_coords(int ord, int symmetric, int tiles_m, int tiles_n, int& tm,
+                                            int& tn) {
   if (symmetric) {
-    tri_index(t, tiles_n, tm, tn);
-  } else {
-    tm = t / tiles_n;
-    tn = t - tm * tiles_n;
+    tri_index(ord, tiles_n, tm, tn);
+    return;
   }
+  const int cb = (tiles_n + 7) / 8;               // band width (columns)
+  const int full = tiles_m * cb;                   // tiles in a full band
+  const int band = ord / full;
+  const int rem = ord - band * full;
+  const int w = min(cb, tiles_n - band * cb);     // width of this band (last may be narrower)
+  tm = rem / w;
+  tn = band * cb + (rem - tm * w);
+}
+
+// Per-XCD share of the tiles and of the workgroups.
+struct XcdShare {
+  int base, count;   // tile ordinals [base, base + count)
+};
+__device__ __forceinline__ XcdShare xcd_share(int x, int T) {
+  const int b0 = (int)((long long)x * T / 8), b1 = (int)((long long)(x + 1) * T / 8);
+  return {b0, b1 - b0};
 }
 
 // Final epilogue of a tile: add the readout summand, write theta (and its mirror).
@@ -372,98 +399,129 @@ __device__ __forceinline__ void fcn_tile_out(f32x16 (&tot)[Cfg::FM][Cfg::FN], co
   __syncthreads();
 }
 
-template <class Cfg, bool VEC>
-__global__ void __launch_bounds__(Cfg::THREADS)
-k_ntk_fcn_sk(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __restrict__ theta,
-             int tiles_n, int T, int P, float* __restrict__ part) {
-  extern __shared__ float smem[];
-  // XCD-aware order: consecutive workgroup ids go to different XCDs (round robin), so range
-  // lam = (bid % 8) * (P / 8) + bid / 8 gives each XCD a contiguous band of tiles (shared
-  // operand panels stay in that XCD's L2).  P is a multiple of 8.
-  const int bid = blockIdx.x;
-  const int lam = (bid & 7) * (P >> 3) + (bid >> 3);
-  const int L = c.L;
-  const long long U = (long long)T * L;
-  const long long beg = sk_start(lam, U, P), end = sk_start(lam + 1, U, P);
-  const int O = (int)fO.d;
-  const int R1 = N1 * O, R2 = N2 * O;
+// tot += sum over layers [l0, l1) of gram_l (.) (G1_l G2_l^T) for the tile at (m0, n0).
+// DMA: direct-to-LDS main loop (every K % 32 == 0, VEC operands).
+template <class Cfg, bool VEC, bool DMA>
+__device__ __forceinline__ void fcn_tile_layers(const FcnContraction& c, int l0, int l1, int N2,
+                                                FastDiv fO, int R1, int R2, int m0, int n0,
+                                                float* smem, f32x16 (&tot)[Cfg::FM][Cfg::FN]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM, wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
-  const int first_tile = (int)(beg / L);
-  for (long long u = beg; u < end;) {
-    const int t = (int)(u / L);
-    const int l0 = (int)(u - (long long)t * L);
-    const int l1 = (int)min((long long)L, l0 + (end - u));
+  for (int l = l0; l < l1; ++l) {
+    const int K = c.K[l];
+    f32x16 acc[Cfg::FM][Cfg::FN];
+    zero_acc<Cfg>(acc);
+    if (DMA) {
+      gemm_mainloop_dma<Cfg>(c.G1[l], K, R1, c.G2[l], K, R2, m0, n0, 0, K, smem, acc);
+    } else {
+      LoadKInnerT<VEC> la{c.G1[l], R1, K, K};
+      LoadKInnerT<VEC> lb{c.G2[l], R2, K, K};
+      gemm_mainloop<Cfg>(la, lb, m0, n0, 0, K, smem, acc);
+    }
+    int n1lo, n2lo, S2;
+    stage_gram<Cfg>(c.gram[l], N2, R1, R2, fO, m0, n0, smem, n1lo, n2lo, S2);
+#pragma unroll
+    for (int fn = 0; fn < Cfg::FN; ++fn) {
+      const int sc = min(n0 + wn0 + fn * 32 + (lane & 31), R2 - 1);
+      const int b = (int)fO.div(sc) - n2lo;
+#pragma unroll
+      for (int fm = 0; fm < Cfg::FM; ++fm) {
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = min(m0 + wm0 + fm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3), R1 - 1);
+          const int a = (int)fO.div(r) - n1lo;
+          tot[fm][fn][v] += smem[a * S2 + b] * acc[fm][fn][v];
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    __syncthreads();
+  }
+}
+
+template <class Cfg, bool VEC, bool DMA>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_ntk_fcn_sk(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __restrict__ theta,
+             int tiles_m, int tiles_n, int T, int P, float* __restrict__ part) {
+  extern __shared__ float smem[];
+  const int bid = blockIdx.x;
+  const int P8 = P >> 3;
+  const int x = bid & 7, j = bid >> 3;        // XCD and workgroup index inside it
+  const int lam = x * P8 + j;                 // partial-buffer owner id
+  const XcdShare sh = xcd_share(x, T);
+  const int L = c.L;
+  const int O = (int)fO.d;
+  const int R1 = N1 * O, R2 = N2 * O;
+  // data-parallel rounds over the XCD's tiles
+  const int rounds = sh.count / P8;
+  for (int i = 0; i < rounds; ++i) {
     int tm, tn;
-    tile_coords<Cfg>(t, symmetric, tiles_n, tm, tn);
+    tile_coords(sh.base + i * P8 + j, symmetric, tiles_m, tiles_n, tm, tn);
     const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
     f32x16 tot[Cfg::FM][Cfg::FN];
     zero_acc<Cfg>(tot);
-    for (int l = l0; l < l1; ++l) {
-      const int K = c.K[l];
-      LoadKInnerT<VEC> la{c.G1[l], R1, K, K};
-      LoadKInnerT<VEC> lb{c.G2[l], R2, K, K};
-      f32x16 acc[Cfg::FM][Cfg::FN];
-      zero_acc<Cfg>(acc);
-      gemm_mainloop<Cfg>(la, lb, m0, n0, 0, K, smem, acc);
-      int n1lo, n2lo, S2;
-      stage_gram<Cfg>(c.gram[l], N2, R1, R2, fO, m0, n0, smem, n1lo, n2lo, S2);
-#pragma unroll
-      for (int fn = 0; fn < Cfg::FN; ++fn) {
-        const int sc = min(n0 + wn0 + fn * 32 + (lane & 31), R2 - 1);
-        const int b = (int)fO.div(sc) - n2lo;
-#pragma unroll
-        for (int fm = 0; fm < Cfg::FM; ++fm) {
-#pragma unroll
-          for (int v = 0; v < 16; ++v) {
-            const int r = min(m0 + wm0 + fm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3), R1 - 1);
-            const int a = (int)fO.div(r) - n1lo;
-            tot[fm][fn][v] += smem[a * S2 + b] * acc[fm][fn][v];
-          }
-          __builtin_amdgcn_sched_barrier(0);
-        }
-      }
-      __syncthreads();
-    }
+    fcn_tile_layers<Cfg, VEC, DMA>(c, 0, L, N2, fO, R1, R2, m0, n0, smem, tot);
+    fcn_tile_out<Cfg>(tot, c.gram_readout, N1, N2, fO, R1, R2, m0, n0, symmetric && tm != tn, smem, theta);
+  }
+  // stream-K over the XCD's remaining tiles
+  const int first_sk = sh.base + rounds * P8;
+  const long long U = (long long)(sh.count - rounds * P8) * L;
+  const long long beg = sk_start(j, U, P8), end = sk_start(j + 1, U, P8);
+  const int first_tile = (int)(beg / L);
+  for (long long u = beg; u < end;) {
+    const int ts = (int)(u / L);
+    const int l0 = (int)(u - (long long)ts * L);
+    const int l1 = (int)min((long long)L, l0 + (end - u));
+    int tm, tn;
+    tile_coords(first_sk + ts, symmetric, tiles_m, tiles_n, tm, tn);
+    const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+    f32x16 tot[Cfg::FM][Cfg::FN];
+    zero_acc<Cfg>(tot);
+    fcn_tile_layers<Cfg, VEC, DMA>(c, l0, l1, N2, fO, R1, R2, m0, n0, smem, tot);
     if (l0 == 0 && l1 == L) {
       fcn_tile_out<Cfg>(tot, c.gram_readout, N1, N2, fO, R1, R2, m0, n0, symmetric && tm != tn, smem,
                         theta);
     } else {
-      float* dst = part + ((long long)lam * 2 + (t == first_tile ? 0 : 1)) * (Cfg::BM * Cfg::BN);
-      for_each_acc<Cfg>(tot, 0, 0, [&](int i, int j, float v) { dst[i * Cfg::BN + j] = v; });
+      float* dst = part + ((long long)lam * 2 + (ts == first_tile ? 0 : 1)) * (Cfg::BM * Cfg::BN);
+      for_each_acc<Cfg>(tot, 0, 0, [&](int ii, int jj, float v) { dst[ii * Cfg::BN + jj] = v; });
     }
     u += l1 - l0;
   }
 }
 
-// One workgroup per range boundary lam = 1..P-1: if the boundary falls inside a tile and is
-// the first boundary inside it, sum that tile's partials (ranges in order) and write it.
+// One workgroup per (XCD x, range boundary j = 1..P8-1) of the stream-K tails: if the boundary
+// falls inside a tile and is the first boundary inside it, sum that tile's partials (ranges in
+// order) and write it.
 template <class Cfg>
 __global__ void __launch_bounds__(256)
 k_ntk_fcn_fixup(int L, const float* __restrict__ gram_readout, int N1, int N2, FastDiv fO,
-                int symmetric, float* __restrict__ theta, int tiles_n, int T, int P,
+                int symmetric, float* __restrict__ theta, int tiles_m, int tiles_n, int T, int P,
                 const float* __restrict__ part) {
-  const int lam = blockIdx.x + 1;
-  const long long U = (long long)T * L;
-  const long long b = sk_start(lam, U, P);
+  const int P8 = P >> 3;
+  const int x = blockIdx.x / (P8 - 1), j = blockIdx.x % (P8 - 1) + 1;
+  const XcdShare sh = xcd_share(x, T);
+  const int rounds = sh.count / P8;
+  const int first_sk = sh.base + rounds * P8;
+  const long long U = (long long)(sh.count - rounds * P8) * L;
+  const long long b = sk_start(j, U, P8);
   if (b >= U || b % L == 0) return;
-  const int t = (int)(b / L);
-  if (sk_start(lam - 1, U, P) > (long long)t * L) return;   // an earlier boundary owns tile t
+  const int ts = (int)(b / L);
+  if (sk_start(j - 1, U, P8) > (long long)ts * L) return;   // an earlier boundary owns the tile
   int tm, tn;
-  tile_coords<Cfg>(t, symmetric, tiles_n, tm, tn);
+  tile_coords(first_sk + ts, symmetric, tiles_m, tiles_n, tm, tn);
   const int O = (int)fO.d;
   const int R1 = N1 * O, R2 = N2 * O;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   const bool mirror = symmetric && tm != tn;
-  const long long tile_end = (long long)(t + 1) * L;
+  const long long tile_end = (long long)(ts + 1) * L;
   for (int e = threadIdx.x; e < Cfg::BM * Cfg::BN; e += 256) {
-    const int i = e / Cfg::BN, j = e - i * Cfg::BN;
-    const int r = m0 + i, s = n0 + j;
+    const int i = e / Cfg::BN, jj = e - i * Cfg::BN;
+    const int r = m0 + i, s = n0 + jj;
     float v = 0.f;
-    for (int q = lam - 1; q < P && sk_start(q, U, P) < tile_end; ++q) {
-      if (sk_start(q + 1, U, P) <= sk_start(q, U, P)) continue;   // empty range: wrote nothing
-      const int slot = (sk_start(q, U, P) / L == t) ? 0 : 1;
-      v += part[((long long)q * 2 + slot) * (Cfg::BM * Cfg::BN) + e];
+    for (int q = j - 1; q < P8 && sk_start(q, U, P8) < tile_end; ++q) {
+      if (sk_start(q + 1, U, P8) <= sk_start(q, U, P8)) continue;   // empty range: wrote nothing
+      const int slot = (sk_start(q, U, P8) / L == ts) ? 0 : 1;
+      v += part[((long long)(x * P8 + q) * 2 + slot) * (Cfg::BM * Cfg::BN) + e];
     }
     if (r < R1 && s < R2) {
       const int n1 = (int)fO.div(r), o1 = r - n1 * O;
@@ -505,29 +563,35 @@ hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2
         c, N1, N2, FastDiv((uint32_t)O), symmetric, theta, tm, tn);
     return hipGetLastError();
   };
-  auto go_sk = [&](auto vec_tag) -> hipError_t {
+  bool dma = v;
+  for (int l = 0; l < c.L; ++l) dma = dma && c.K[l] % 32 == 0;
+  auto go_sk = [&](auto vec_tag, auto dma_tag) -> hipError_t {
     using Cfg = CfgSK;
     constexpr bool VEC = decltype(vec_tag)::value;
+    constexpr bool DMA = decltype(dma_tag)::value;
     using L = LoadKInnerT<VEC>;
     const int tm = cdiv(R1, Cfg::BM), tn = cdiv(R2, Cfg::BN);
     const int T = symmetric ? tn * (tn + 1) / 2 : tm * tn;
     const int P = num_cu;
-    hipError_t e = set_smem<Cfg, L, L>((const void*)k_ntk_fcn_sk<Cfg, VEC>);
+    constexpr int bytes = DMA ? gemm_dma_smem_bytes<Cfg>() : gemm_smem_bytes<Cfg, L, L>();
+    static_assert((Cfg::BM + 1) * (Cfg::BN + 1) * 4 <= bytes, "Gram block must fit the LDS area");
+    hipError_t e = hipFuncSetAttribute((const void*)k_ntk_fcn_sk<Cfg, VEC, DMA>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (e != hipSuccess) return e;
     const FastDiv fO((uint32_t)O);
-    k_ntk_fcn_sk<Cfg, VEC><<<dim3(P), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, L, L>(), s>>>(
-        c, N1, N2, fO, symmetric, theta, tn, T, P, part);
+    k_ntk_fcn_sk<Cfg, VEC, DMA><<<dim3(P), dim3(Cfg::THREADS), bytes, s>>>(
+        c, N1, N2, fO, symmetric, theta, tm, tn, T, P, part);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    k_ntk_fcn_fixup<Cfg><<<dim3(P - 1), dim3(256), 0, s>>>(c.L, c.gram_readout, N1, N2, fO, symmetric,
-                                                           theta, tn, T, P, part);
+    k_ntk_fcn_fixup<Cfg><<<dim3(8 * (P / 8 - 1)), dim3(256), 0, s>>>(
+        c.L, c.gram_readout, N1, N2, fO, symmetric, theta, tm, tn, T, P, part);
     return hipGetLastError();
   };
   const long long big_tiles = (long long)cdiv(R1, 128) * cdiv(R2, 128);
   // stream-K when there are at least as many whole tiles as compute units (P must be a
   // multiple of 8 for the XCD-aware range order)
-  if (c.L >= 1 && part && num_cu >= 8 && num_cu % 8 == 0 && big_tiles >= num_cu)
-    return v ? go_sk(TrueT{}) : go_sk(FalseT{});
+  if (c.L >= 1 && part && num_cu >= 16 && num_cu % 8 == 0 && big_tiles >= num_cu)
+    return dma ? go_sk(TrueT{}, TrueT{}) : (v ? go_sk(TrueT{}, FalseT{}) : go_sk(FalseT{}, FalseT{}));
   if (big_tiles >= 512) return v ? go(CfgBig8{}, TrueT{}) : go(CfgBig8{}, FalseT{});
   return v ? go(CfgSmall{}, TrueT{}) : go(CfgSmall{}, FalseT{});
 }
