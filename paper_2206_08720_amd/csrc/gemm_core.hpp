@@ -482,6 +482,32 @@ __device__ __forceinline__ void mma_stage_dma(const float* As, const float* Bs,
   }
 }
 
+// fp64 16x16x4 flavour of the stage (pre-activations of the forward pass), same tiles.
+template <class Cfg>
+__device__ __forceinline__ void mma_stage_dma(const float* As, const float* Bs,
+                                              f64x4 (&acc)[Cfg::FM16][Cfg::FN16], int wm0, int wn0,
+                                              int lane) {
+  using TA = DmaTile<Cfg::BM>;
+  using TB = DmaTile<Cfg::BN>;
+  const int lr = lane & 15, lk = (lane >> 4) * 4;
+#pragma unroll
+  for (int kk = 0; kk < 32; kk += 16) {
+    f32x4 a[Cfg::FM16], b[Cfg::FN16];
+#pragma unroll
+    for (int fm = 0; fm < Cfg::FM16; ++fm) a[fm] = TA::frag(As, wm0 + fm * 16 + lr, kk + lk);
+#pragma unroll
+    for (int fn = 0; fn < Cfg::FN16; ++fn) b[fn] = TB::frag(Bs, wn0 + fn * 16 + lr, kk + lk);
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int fm = 0; fm < Cfg::FM16; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < Cfg::FN16; ++fn)
+          acc[fm][fn] = __builtin_amdgcn_mfma_f64_16x16x4f64((double)a[fm][t], (double)b[fn][t],
+                                                             acc[fm][fn], 0, 0, 0);
+  }
+}
+
 // s_waitcnt immediate (gfx9 encoding) that waits until at most n vector-memory operations of
 // this wave are outstanding and does not wait on the other counters.
 __device__ __forceinline__ void wait_vmcnt_dyn(int n) {
@@ -501,11 +527,11 @@ constexpr int gemm_dma_smem_bytes() {
 // K loop over [k_begin, k_end) (both multiples of 32) for the tile (m0, n0), with NSTAGE LDS
 // stages (2: tile kt+1 in flight during tile kt; 3: tiles kt+1 and kt+2).  Ends with a
 // barrier, so the caller may reuse `smem` afterwards.
-template <class Cfg, int NSTAGE = kDmaStages>
+template <class Cfg, int NSTAGE = kDmaStages, class AccT>
 __device__ __forceinline__ void gemm_mainloop_dma(const float* __restrict__ A, long long lda, int rowsA,
                                                   const float* __restrict__ B, long long ldb, int rowsB,
                                                   int m0, int n0, int k_begin, int k_end, float* smem,
-                                                  f32x16 (&acc)[Cfg::FM][Cfg::FN]) {
+                                                  AccT& acc) {
   static_assert(Cfg::BK == 32, "direct-to-LDS main loop uses BK = 32");
   using TA = DmaTile<Cfg::BM>;
   using TB = DmaTile<Cfg::BN>;

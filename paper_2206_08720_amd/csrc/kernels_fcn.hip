@@ -39,7 +39,7 @@ static hipError_t set_smem(const void* fn) {
 // ------------------------------------------------------------------------------ forward
 // The pre-activation is accumulated in fp64 from the fp32 layer input and weights, then
 // the activation's decision (ReLU sign) is taken on that value and h_{l+1} is stored in fp32.
-template <class Cfg, bool VEC>
+template <class Cfg, bool VEC, bool DMA>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_dense_fwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restrict__ bias, int M, int N,
             int act, float* __restrict__ hn, float* __restrict__ dphi, int tiles_n) {
@@ -48,7 +48,10 @@ k_dense_fwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restrict__ 
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   f64x4 acc[Cfg::FM16][Cfg::FN16];
   zero_acc<Cfg>(acc);
-  gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
+  if (DMA)
+    gemm_mainloop_dma<Cfg, 3>(la.p, la.ld, la.rows, lb.p, lb.ld, lb.rows, m0, n0, 0, la.K, smem, acc);
+  else
+    gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
   for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, double v) {
     const double b = bias ? (double)bias[min(c, N - 1)] : 0.0;
     const double z = v + b;
@@ -68,24 +71,27 @@ k_dense_fwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restrict__ 
   });
 }
 
-template <class Cfg, bool VEC>
+template <class Cfg, bool VEC, bool DMA = false>
 static hipError_t dense_fwd_cfg(hipStream_t s, const float* h, const float* W, const float* b, int M,
                                 int N, int K, int act, float* hn, float* dphi) {
   using L = LoadKInnerT<VEC>;
   L la{h, M, K, K};
   L lb{W, N, K, K};
   const int tn = cdiv(N, Cfg::BN), tm = cdiv(M, Cfg::BM);
-  hipError_t e = set_smem<Cfg, L, L>((const void*)k_dense_fwd<Cfg, VEC>);
+  constexpr int bytes = DMA ? gemm_dma_smem_bytes<Cfg, 3>() : gemm_smem_bytes<Cfg, L, L>();
+  hipError_t e = hipFuncSetAttribute((const void*)k_dense_fwd<Cfg, VEC, DMA>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   if (e != hipSuccess) return e;
-  k_dense_fwd<Cfg, VEC><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, L, L>(), s>>>(
-      la, lb, b, M, N, act, hn, dphi, tn);
+  k_dense_fwd<Cfg, VEC, DMA><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(la, lb, b, M, N, act, hn,
+                                                                               dphi, tn);
   return hipGetLastError();
 }
 
 hipError_t launch_dense_fwd(hipStream_t s, const float* h, const float* W, const float* b, int M,
                             int N, int K, int act, float* hn, float* dphi) {
-  if (vec_ok(h, K, K) && vec_ok(W, K, K))
-    return dense_fwd_cfg<CfgFwd64, true>(s, h, W, b, M, N, K, act, hn, dphi);
+  const bool v = vec_ok(h, K, K) && vec_ok(W, K, K);
+  if (v && K % 32 == 0) return dense_fwd_cfg<CfgFwd64, true, true>(s, h, W, b, M, N, K, act, hn, dphi);
+  if (v) return dense_fwd_cfg<CfgFwd64, true>(s, h, W, b, M, N, K, act, hn, dphi);
   return dense_fwd_cfg<CfgFwd64, false>(s, h, W, b, M, N, K, act, hn, dphi);
 }
 
