@@ -19,6 +19,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "index_math.hpp"
+
 namespace ntk {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
@@ -385,25 +387,6 @@ __device__ __forceinline__ float act_deriv(int act, float z) {
 
 namespace ntk {
 
-// Division of non-negative int32 values by a runtime divisor via a multiply-high:
-// with s = ceil(log2 d) and m = floor(2^32 (2^s - d) / d) + 1,  n / d = (umulhi(n, m) + n) >> s
-// for 0 <= n < 2^31 (the round-up reciprocal method of Granlund and Montgomery, 1994).
-struct FastDiv {
-  uint32_t d = 1, m = 1, s = 0;
-  FastDiv() = default;
-  __host__ explicit FastDiv(uint32_t div) : d(div) {
-    s = 0;
-    while ((1ull << s) < d) ++s;
-    m = (uint32_t)((((1ull << s) - d) << 32) / d + 1);
-  }
-  __host__ __device__ __forceinline__ uint32_t div(uint32_t n) const {
-#if defined(__HIP_DEVICE_COMPILE__)
-    return (__umulhi(n, m) + n) >> s;
-#else
-    return (uint32_t)((((uint64_t)n * m) >> 32) + n) >> s;
-#endif
-  }
-};
 
 }  // namespace ntk
 

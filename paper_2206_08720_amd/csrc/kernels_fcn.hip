@@ -249,17 +249,6 @@ hipError_t launch_gram(hipStream_t s, const GramBatch& g, int N1, int N2) {
 }
 
 // ------------------------------------------------------------------------------ fused contraction
-// Tile index -> (tm, tn).  Symmetric: enumerate the upper triangle tm <= tn row by row.
-__device__ __forceinline__ void tri_index(int t, int nt, int& tm, int& tn) {
-  int r = 0, base = 0;
-  while (base + (nt - r) <= t) {
-    base += nt - r;
-    ++r;
-  }
-  tm = r;
-  tn = r + (t - base);
-}
-
 // Stage the block of a Gram matrix that a tile touches (rows r cover samples r / O) into
 // LDS: sg[a * S2 + b] = gram[n1lo + a][n2lo + b].  Ends with a barrier.
 template <class Cfg>
@@ -356,35 +345,6 @@ k_ntk_fcn(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __
 //     theta; a split tile's partial sums go to `part` (slot 0: the first tile of a range,
 //     slot 1: its last) and k_ntk_fcn_fixup adds them in range order.
 // No workgroup waits for another; the summation order is fixed for a given device.
-__device__ __forceinline__ long long sk_start(int lam, long long U, int P) {
-  return (long long)lam * U / P;
-}
-
-// Tile at position `ord` of the column-banded order (non-symmetric), or of the triangle order.
-__device__ __forceinline__ void tile_coords(int ord, int symmetric, int tiles_m, int tiles_n, int& tm,
-                                            int& tn) {
-  if (symmetric) {
-    tri_index(ord, tiles_n, tm, tn);
-    return;
-  }
-  const int cb = (tiles_n + 7) / 8;               // band width (columns)
-  const int full = tiles_m * cb;                   // tiles in a full band
-  const int band = ord / full;
-  const int rem = ord - band * full;
-  const int w = min(cb, tiles_n - band * cb);     // width of this band (last may be narrower)
-  tm = rem / w;
-  tn = band * cb + (rem - tm * w);
-}
-
-// Per-XCD share of the tiles and of the workgroups.
-struct XcdShare {
-  int base, count;   // tile ordinals [base, base + count)
-};
-__device__ __forceinline__ XcdShare xcd_share(int x, int T) {
-  const int b0 = (int)((long long)x * T / 8), b1 = (int)((long long)(x + 1) * T / 8);
-  return {b0, b1 - b0};
-}
-
 // Final epilogue of a tile: add the readout summand, write theta (and its mirror).
 template <class Cfg>
 __device__ __forceinline__ void fcn_tile_out(f32x16 (&tot)[Cfg::FM][Cfg::FN], const float* gram_readout,
@@ -454,13 +414,12 @@ k_ntk_fcn_sk(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float*
   const int P8 = P >> 3;
   const int x = bid & 7, j = bid >> 3;        // XCD and workgroup index inside it
   const int lam = x * P8 + j;                 // partial-buffer owner id
-  const XcdShare sh = xcd_share(x, T);
   const int L = c.L;
+  const SkShare sh = sk_share(x, T, P8, L);
   const int O = (int)fO.d;
   const int R1 = N1 * O, R2 = N2 * O;
   // data-parallel rounds over the XCD's tiles
-  const int rounds = sh.count / P8;
-  for (int i = 0; i < rounds; ++i) {
+  for (int i = 0; i < sh.rounds; ++i) {
     int tm, tn;
     tile_coords(sh.base + i * P8 + j, symmetric, tiles_m, tiles_n, tm, tn);
     const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
@@ -470,16 +429,13 @@ k_ntk_fcn_sk(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float*
     fcn_tile_out<Cfg>(tot, c.gram_readout, N1, N2, fO, R1, R2, m0, n0, symmetric && tm != tn, smem, theta);
   }
   // stream-K over the XCD's remaining tiles
-  const int first_sk = sh.base + rounds * P8;
-  const long long U = (long long)(sh.count - rounds * P8) * L;
-  const long long beg = sk_start(j, U, P8), end = sk_start(j + 1, U, P8);
-  const int first_tile = (int)(beg / L);
+  const long long beg = sk_start(j, sh.U, P8), end = sk_start(j + 1, sh.U, P8);
   for (long long u = beg; u < end;) {
     const int ts = (int)(u / L);
     const int l0 = (int)(u - (long long)ts * L);
     const int l1 = (int)min((long long)L, l0 + (end - u));
     int tm, tn;
-    tile_coords(first_sk + ts, symmetric, tiles_m, tiles_n, tm, tn);
+    tile_coords(sh.first_sk + ts, symmetric, tiles_m, tiles_n, tm, tn);
     const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
     f32x16 tot[Cfg::FM][Cfg::FN];
     zero_acc<Cfg>(tot);
@@ -488,7 +444,7 @@ k_ntk_fcn_sk(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float*
       fcn_tile_out<Cfg>(tot, c.gram_readout, N1, N2, fO, R1, R2, m0, n0, symmetric && tm != tn, smem,
                         theta);
     } else {
-      float* dst = part + ((long long)lam * 2 + (ts == first_tile ? 0 : 1)) * (Cfg::BM * Cfg::BN);
+      float* dst = part + ((long long)lam * 2 + sk_slot(beg, L, ts)) * (Cfg::BM * Cfg::BN);
       for_each_acc<Cfg>(tot, 0, 0, [&](int ii, int jj, float v) { dst[ii * Cfg::BN + jj] = v; });
     }
     u += l1 - l0;
@@ -505,16 +461,11 @@ k_ntk_fcn_fixup(int L, const float* __restrict__ gram_readout, int N1, int N2, F
                 const float* __restrict__ part) {
   const int P8 = P >> 3;
   const int x = blockIdx.x / (P8 - 1), j = blockIdx.x % (P8 - 1) + 1;
-  const XcdShare sh = xcd_share(x, T);
-  const int rounds = sh.count / P8;
-  const int first_sk = sh.base + rounds * P8;
-  const long long U = (long long)(sh.count - rounds * P8) * L;
-  const long long b = sk_start(j, U, P8);
-  if (b >= U || b % L == 0) return;
-  const int ts = (int)(b / L);
-  if (sk_start(j - 1, U, P8) > (long long)ts * L) return;   // an earlier boundary owns the tile
+  const SkShare sh = sk_share(x, T, P8, L);
+  const int ts = sk_fixup_tile(sh, j, P8, L);
+  if (ts < 0) return;
   int tm, tn;
-  tile_coords(first_sk + ts, symmetric, tiles_m, tiles_n, tm, tn);
+  tile_coords(sh.first_sk + ts, symmetric, tiles_m, tiles_n, tm, tn);
   const int O = (int)fO.d;
   const int R1 = N1 * O, R2 = N2 * O;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
@@ -524,10 +475,10 @@ k_ntk_fcn_fixup(int L, const float* __restrict__ gram_readout, int N1, int N2, F
     const int i = e / Cfg::BN, jj = e - i * Cfg::BN;
     const int r = m0 + i, s = n0 + jj;
     float v = 0.f;
-    for (int q = j - 1; q < P8 && sk_start(q, U, P8) < tile_end; ++q) {
-      if (sk_start(q + 1, U, P8) <= sk_start(q, U, P8)) continue;   // empty range: wrote nothing
-      const int slot = (sk_start(q, U, P8) / L == ts) ? 0 : 1;
-      v += part[((long long)(x * P8 + q) * 2 + slot) * (Cfg::BM * Cfg::BN) + e];
+    for (int q = j - 1; q < P8 && sk_start(q, sh.U, P8) < tile_end; ++q) {
+      const long long qb = sk_start(q, sh.U, P8);
+      if (sk_start(q + 1, sh.U, P8) <= qb) continue;   // empty range: wrote nothing
+      v += part[((long long)(x * P8 + q) * 2 + sk_slot(qb, L, ts)) * (Cfg::BM * Cfg::BN) + e];
     }
     if (r < R1 && s < R2) {
       const int n1 = (int)fO.div(r), o1 = r - n1 * O;
