@@ -43,7 +43,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="relu_mlp_d8_w2048")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-samples", type=int, default=2,
+    ap.add_argument("--cpu-samples", type=int, default=6,
                     help="samples per side of the oracle's bounded sample")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (for HBM counter scaling)")
@@ -74,21 +74,40 @@ def measured_traffic(name, kernel):
             + rec["write_size_kib_per_launch"] * rec["write_scale"]) * 1024.0
 
 
-def cpu_baseline(name, n):
+def cpu_baseline(name, n, n1_full, n2_full):
+    """Time the fp64 Jacobian-contraction oracle on Theta(X1[:n], X2[:n]) (after an untimed
+    one-sample call), and extrapolate to the full Theta: the per-sample part (forward, O
+    backward passes, Jacobian rows) linear in the samples, the contraction 2 N1 N2 O^2 P
+    FLOPs at the host's fp64 GEMM rate measured here."""
     import numpy as np
     import oracle
     import workloads as wl
     from threadpoolctl import threadpool_info
     spec, params, X1, X2 = wl.make_workload(name)
+    oracle.ntk_jc(spec, params, X1[:1], X2[:1])          # warm-up (page faults, BLAS threads)
     t0 = time.perf_counter()
     th = oracle.ntk_jc(spec, params, X1[:n], X2[:n])
     dt = time.perf_counter() - t0
+    A = np.random.default_rng(0).standard_normal((2048, 2048))
+    gemm_s = []
+    for _ in range(3):
+        t1 = time.perf_counter()
+        A @ A
+        gemm_s.append(time.perf_counter() - t1)
+    rate = 2 * 2048 ** 3 / min(gemm_s)
+    O, P = th.shape[2], oracle.param_count(spec)
+    per_pair = 2.0 * O * O * P / rate                    # contraction seconds per sample pair
+    per_sample = max(0.0, (dt - per_pair * n * n) / (2 * n))
+    full_s = per_sample * (n1_full + n2_full) + per_pair * n1_full * n2_full
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     return {"value": th.size / dt, "unit": "NTK entries/s", "cores": threads, "kind": "oracle",
-            "sample": f"Theta(X1[:{n}], X2[:{n}]) of {name}, all {th.shape[2]} outputs "
-                      f"({th.size} entries) by fp64 Jacobian contraction in {dt:.1f} s; "
-                      f"host {platform.processor() or platform.machine()}, "
-                      f"{os.cpu_count()} logical CPUs"}
+            "extrapolated_full_theta_s": full_s,
+            "sample": f"Theta(X1[:{n}], X2[:{n}]) of {name}, all {O} outputs ({th.size} entries) "
+                      f"by fp64 Jacobian contraction in {dt:.1f} s; host "
+                      f"{platform.processor() or platform.machine()}, {os.cpu_count()} logical "
+                      f"CPUs. extrapolated_full_theta_s (extrapolated, not measured): per-sample "
+                      f"part {per_sample:.3g} s x (N1 + N2) + contraction 2 N1 N2 O^2 P FLOPs "
+                      f"(P = {P}) at the measured fp64 GEMM rate {rate / 1e9:.0f} GFLOP/s"}
 
 
 def copy_calibration():
@@ -139,15 +158,18 @@ def main():
     h.profile_read()                       # drop anything recorded so far
     h.profile_enable(True)
     torch.cuda.synchronize()
-    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
     t0 = time.perf_counter()
-    ev0.record(stream)
-    for _ in range(args.steps):
+    evs[0].record(stream)
+    for i in range(args.steps):
         h.compute(dev, x1, x2, out=out)
-    ev1.record(stream)
+        evs[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ms = ev0.elapsed_time(ev1) / args.steps
+    ms = evs[0].elapsed_time(evs[-1]) / args.steps
+    step_ms = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+    ms_median = step_ms[len(step_ms) // 2] if len(step_ms) % 2 else \
+        0.5 * (step_ms[len(step_ms) // 2 - 1] + step_ms[len(step_ms) // 2])
     prof = h.profile_read()
     h.profile_enable(False)
 
@@ -173,9 +195,17 @@ def main():
                 "frac": achieved / FP32_MFMA_PEAK_TFLOPS, "traffic": measured_traffic(name, dom),
                 "flop_per_launch": flop_per_launch, "avg_launch_ms": avg_ms}
 
+    h.close()
+    num_cu, clock_khz = _lib.device_info()
+    ceiling = {"fp32_tflops": _lib.mfma_peak("fp32"), "fp64_tflops": _lib.mfma_peak("fp64"),
+               "kernel": "independent MFMA chains, 4 waves per SIMD"}
+    roofline["measured_ceiling"] = ceiling["fp32_tflops"]
+    roofline["frac_of_measured_ceiling"] = achieved / ceiling["fp32_tflops"]
+
     res = {
         "metric": METRIC, "value": value, "unit": "NTK entries/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
+        "ms_per_step_median": ms_median, "ms_per_step_min": step_ms[0],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded N(0,1) inputs, He-init weights)",
         "config": {"workload": name, "n1": n1, "n2": n2, "O": O,
@@ -183,11 +213,13 @@ def main():
                    "symmetric_schedule": sym, "parallelism": "single GPU"},
         "tflops": tflops, "frac_of_fp32_mfma_peak": tflops / FP32_MFMA_PEAK_TFLOPS,
         "algorithmic_flops": fl, "kernels": kernels, "roofline": roofline,
+        "mfma_ceiling_measured": ceiling,
+        "device": {"name": torch.cuda.get_device_name(0), "compute_units": num_cu,
+                   "peak_clock_mhz": clock_khz / 1000.0},
         "wall_s_timed_region": wall,
     }
-    h.close()
     if not args.no_cpu_baseline:
-        res["cpu_baseline"] = cpu_baseline(name, args.cpu_samples)
+        res["cpu_baseline"] = cpu_baseline(name, min(args.cpu_samples, n1, n2), n1, n2)
     print(json.dumps(res), flush=True)
 
 

@@ -14,8 +14,11 @@
  * expanded_ntk_main, Eq. mixed_product_example; per-layer formulas of
  * Section 4.1 for the FCN and the appendix "CNN NTK Complexity" for the CNN).
  *
- * All arithmetic runs on the GPU in fp32 with fp32 accumulation (the paper's
- * experiments use 32-bit precision, appendix "Experimental Details").
+ * The contractions run on the GPU in fp32 with fp32 accumulation (the paper's
+ * experiments use 32-bit precision, appendix "Experimental Details").  The forward
+ * pre-activations are accumulated in fp64 from the fp32 layer inputs and weights, so that
+ * the activation's decisions (the ReLU sign) are those of the exact pre-activation; every
+ * stored array (layer inputs, derivatives, cotangents, Theta) is fp32.
  *
  * Networks (the descriptor below):
  *   * FCN: n >= 1 DENSE layers.  Layer l maps d_l -> d_{l+1}:
@@ -153,6 +156,18 @@ long long ntk_workspace_bytes(const ntk_handle* h);
 int ntk_profile_enable(ntk_handle* h, int enable);
 int ntk_profile_read(ntk_handle* h, const char** names, double* total_ms,
                      long long* launches, int max);
+
+/* ---- device diagnostics ----------------------------------------------------------
+ * ntk_device_info -- number of compute units and peak engine clock (kHz) of the device
+ * current on the calling thread.  NTK_E_ARG for a null pointer, NTK_E_HIP on a HIP error.
+ *
+ * ntk_mfma_peak -- measured matrix-core ceiling of the current device in TFLOP/s:
+ * which = 0 for v_mfma_f32_32x32x2_f32 (fp32), 1 for v_mfma_f64_16x16x4_f64 (fp64).  A
+ * kernel of independent MFMA chains (four 4-wave workgroups per compute unit) is timed
+ * with HIP events on a private stream; the call is synchronous and allocates (then frees)
+ * a small output buffer.  Returns NTK_OK, NTK_E_ARG, NTK_E_OOM or NTK_E_HIP. */
+int ntk_device_info(int* num_cu, int* clock_khz);
+int ntk_mfma_peak(int which, double* tflops);
 
 #ifdef __cplusplus
 }

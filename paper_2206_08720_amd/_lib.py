@@ -29,7 +29,7 @@ NTK_CONV_ORDER_AUTO, NTK_CONV_ORDER_OUTSIDE_IN, NTK_CONV_ORDER_INSIDE_OUT = 0, 1
 
 EXPORTED_SYMBOLS = ("ntk_init", "ntk_compute", "ntk_free", "ntk_last_error", "ntk_set_option",
                     "ntk_set_stream", "ntk_workspace_bytes", "ntk_profile_enable",
-                    "ntk_profile_read")
+                    "ntk_profile_read", "ntk_device_info", "ntk_mfma_peak")
 
 
 class ntk_layer_desc(ctypes.Structure):
@@ -83,8 +83,26 @@ def load():
                                      ctypes.POINTER(ctypes.c_double),
                                      ctypes.POINTER(ctypes.c_longlong), ctypes.c_int]
     lib.ntk_profile_read.restype = ctypes.c_int
+    lib.ntk_device_info.argtypes = [ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int)]
+    lib.ntk_device_info.restype = ctypes.c_int
+    lib.ntk_mfma_peak.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double)]
+    lib.ntk_mfma_peak.restype = ctypes.c_int
     _lib = lib
     return lib
+
+
+def device_info():
+    """(compute units, peak engine clock in kHz) of the current HIP device."""
+    cu, clk = ctypes.c_int(0), ctypes.c_int(0)
+    check(load().ntk_device_info(ctypes.byref(cu), ctypes.byref(clk)))
+    return cu.value, clk.value
+
+
+def mfma_peak(which="fp32"):
+    """Measured matrix-core ceiling (TFLOP/s) of the current device: "fp32" or "fp64"."""
+    out = ctypes.c_double(0.0)
+    check(load().ntk_mfma_peak({"fp32": 0, "fp64": 1}[which], ctypes.byref(out)))
+    return out.value
 
 
 def last_error(handle=None):

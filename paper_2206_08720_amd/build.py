@@ -25,6 +25,9 @@ ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wno-unused-result", "-I", os.path.join(PKG, "..", "include")]
+# Per-file extras.  diag.hip: keep MFMA accumulators in the VGPR form, so that the fp64
+# chains are not copied between accumulation and architectural registers every iteration.
+PER_FILE = {"diag.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _run(cmd):
@@ -44,7 +47,8 @@ def build(verbose=False, extra_flags=()):
 
     def compile_one(src):
         obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-        out = _run([HIPCC, *COMMON, *extra_flags, "-c", src, "-o", obj])
+        per = PER_FILE.get(os.path.basename(src), [])
+        out = _run([HIPCC, *COMMON, *per, *extra_flags, "-c", src, "-o", obj])
         if verbose and out.strip():
             print(out)
         return obj

@@ -451,41 +451,58 @@ k_ntk_fcn_sk(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float*
   }
 }
 
-// One workgroup per (XCD x, range boundary j = 1..P8-1) of the stream-K tails: if the boundary
-// falls inside a tile and is the first boundary inside it, sum that tile's partials (ranges in
-// order) and write it.
+// Fixup of the stream-K tails.  Boundary j = 1..P8-1 of XCD x owns a tile when it falls inside
+// it and is the first boundary inside it (sk_fixup_tile); kFixupSplit workgroups share that
+// tile, each thread adds the partial sums of one float4 of it (ranges in order), adds the
+// readout summand and writes theta.
+constexpr int kFixupSplit = 16;
 template <class Cfg>
 __global__ void __launch_bounds__(256)
 k_ntk_fcn_fixup(int L, const float* __restrict__ gram_readout, int N1, int N2, FastDiv fO,
                 int symmetric, float* __restrict__ theta, int tiles_m, int tiles_n, int T, int P,
                 const float* __restrict__ part) {
+  static_assert(Cfg::BM * Cfg::BN == kFixupSplit * 256 * 4, "one float4 per thread");
   const int P8 = P >> 3;
-  const int x = blockIdx.x / (P8 - 1), j = blockIdx.x % (P8 - 1) + 1;
+  const int blk = blockIdx.x / kFixupSplit, sub = blockIdx.x % kFixupSplit;
+  const int x = blk / (P8 - 1), j = blk % (P8 - 1) + 1;
   const SkShare sh = sk_share(x, T, P8, L);
   const int ts = sk_fixup_tile(sh, j, P8, L);
   if (ts < 0) return;
   int tm, tn;
   tile_coords(sh.first_sk + ts, symmetric, tiles_m, tiles_n, tm, tn);
+  const int e0 = (sub * 256 + threadIdx.x) * 4;
+  const long long tile_end = (long long)(ts + 1) * L;
+  float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+  long long qb = sk_start(j - 1, sh.U, P8);
+  for (int q = j - 1; q < P8 && qb < tile_end; ++q) {
+    const long long qe = sk_start(q + 1, sh.U, P8);
+    if (qe > qb) {   // an empty range wrote nothing
+      const float4 p = *reinterpret_cast<const float4*>(
+          part + ((long long)(x * P8 + q) * 2 + sk_slot(qb, L, ts)) * (Cfg::BM * Cfg::BN) + e0);
+      v.x += p.x;
+      v.y += p.y;
+      v.z += p.z;
+      v.w += p.w;
+    }
+    qb = qe;
+  }
   const int O = (int)fO.d;
   const int R1 = N1 * O, R2 = N2 * O;
-  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   const bool mirror = symmetric && tm != tn;
-  const long long tile_end = (long long)(ts + 1) * L;
-  for (int e = threadIdx.x; e < Cfg::BM * Cfg::BN; e += 256) {
-    const int i = e / Cfg::BN, jj = e - i * Cfg::BN;
-    const int r = m0 + i, s = n0 + jj;
-    float v = 0.f;
-    for (int q = j - 1; q < P8 && sk_start(q, sh.U, P8) < tile_end; ++q) {
-      const long long qb = sk_start(q, sh.U, P8);
-      if (sk_start(q + 1, sh.U, P8) <= qb) continue;   // empty range: wrote nothing
-      v += part[((long long)(x * P8 + q) * 2 + sk_slot(qb, L, ts)) * (Cfg::BM * Cfg::BN) + e];
-    }
-    if (r < R1 && s < R2) {
-      const int n1 = (int)fO.div(r), o1 = r - n1 * O;
+  const int i = e0 / Cfg::BN, jj = e0 - i * Cfg::BN;
+  const int r = tm * Cfg::BM + i;
+  if (r >= R1) return;
+  const int n1 = (int)fO.div(r), o1 = r - n1 * O;
+  const float vals[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int s = tn * Cfg::BN + jj + k;
+    if (s < R2) {
       const int n2 = (int)fO.div(s), o2 = s - n2 * O;
-      if (o1 == o2) v += gram_readout[(long long)n1 * N2 + n2];
-      theta[(((long long)n1 * N2 + n2) * O + o1) * O + o2] = v;
-      if (mirror) theta[(((long long)n2 * N1 + n1) * O + o2) * O + o1] = v;
+      float w = vals[k];
+      if (o1 == o2) w += gram_readout[(long long)n1 * N2 + n2];
+      theta[(((long long)n1 * N2 + n2) * O + o1) * O + o2] = w;
+      if (mirror) theta[(((long long)n2 * N1 + n1) * O + o2) * O + o1] = w;
     }
   }
 }
@@ -540,7 +557,7 @@ hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2
         c, N1, N2, fO, symmetric, theta, tm, tn, T, P, part);
     e = hipGetLastError();
     if (e != hipSuccess) return e;
-    k_ntk_fcn_fixup<Cfg><<<dim3(8 * (P / 8 - 1)), dim3(256), 0, s>>>(
+    k_ntk_fcn_fixup<Cfg><<<dim3(8 * (P / 8 - 1) * kFixupSplit), dim3(256), 0, s>>>(
         c.L, c.gram_readout, N1, N2, fO, symmetric, theta, tm, tn, T, P, part);
     return hipGetLastError();
   };

@@ -77,3 +77,12 @@ def test_null_handle_calls(lib):
     assert lib.ntk_set_option(None, 1, 1) == _lib.NTK_E_ARG
     assert lib.ntk_workspace_bytes(None) == 0
     assert isinstance(lib.ntk_last_error(None), bytes)
+
+
+def test_diagnostics_reject_bad_arguments_before_any_device_call(lib):
+    from paper_2206_08720_amd import _lib
+    out = ctypes.c_double(0.0)
+    assert lib.ntk_mfma_peak(2, ctypes.byref(out)) == _lib.NTK_E_ARG
+    assert lib.ntk_mfma_peak(0, None) == _lib.NTK_E_ARG
+    cu = ctypes.c_int(0)
+    assert lib.ntk_device_info(ctypes.byref(cu), None) == _lib.NTK_E_ARG
