@@ -99,6 +99,28 @@ typedef struct ntk_handle ntk_handle;
 #define NTK_CONV_ORDER_AUTO        0
 #define NTK_CONV_ORDER_OUTSIDE_IN  1
 #define NTK_CONV_ORDER_INSIDE_OUT  2
+/* NTK_OPT_OUTPUT: which part of the O x O block of every input pair is computed (the
+ * pseudo-NTK of the appendix "Pseudo-NTK"; compute-wise these have O = 1):
+ *   NTK_OUTPUT_FULL  (default) the whole block Theta(x1, x2)[o1, o2];
+ *   NTK_OUTPUT_TRACE its trace sum_o Theta(x1, x2)[o, o] (divide by O for the mean of the
+ *                    O diagonal blocks);
+ *   NTK_OUTPUT_LOGIT Theta(x1, x2)[o*, o*] for the logit o* set by NTK_OPT_LOGIT (the NTK of
+ *                    that one output; the backward pass runs for it alone).
+ * NTK_OPT_LOGIT: o*, 0 <= o* < O (default 0).
+ * NTK_OPT_BATCH: which input pairs are computed:
+ *   NTK_BATCH_FULL     (default) every pair (n1, n2);
+ *   NTK_BATCH_DIAGONAL only the pairs (n, n), Theta(x1_n, x2_n); needs n1 == n2.
+ * The layout of theta follows (row-major, fp32):
+ *   FULL  x FULL      [n1, n2, O, O]      FULL  x DIAGONAL  [n, O, O]
+ *   TRACE/LOGIT x FULL [n1, n2]           TRACE/LOGIT x DIAGONAL [n]                      */
+#define NTK_OPT_OUTPUT      3
+#define NTK_OUTPUT_FULL     0
+#define NTK_OUTPUT_TRACE    1
+#define NTK_OUTPUT_LOGIT    2
+#define NTK_OPT_LOGIT       4
+#define NTK_OPT_BATCH       5
+#define NTK_BATCH_FULL      0
+#define NTK_BATCH_DIAGONAL  1
 
 /*
  * ntk_init -- validate a model descriptor, plan and allocate the workspace.
@@ -121,8 +143,10 @@ int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, void* hip_stre
  *   X2      device, same layout with n2 rows.  X2 == X1 with n2 == n1 selects the
  *           symmetric schedule (see NTK_OPT_SYMMETRIC).
  *   theta   device [n1, n2, O, O] fp32 row-major:
- *           theta[((n1*N2 + n2)*O + o1)*O + o2] = Theta(x1_{n1}, x2_{n2})[o1, o2].
+ *           theta[((n1*N2 + n2)*O + o1)*O + o2] = Theta(x1_{n1}, x2_{n2})[o1, o2],
+ *           or the smaller array that NTK_OPT_OUTPUT / NTK_OPT_BATCH select (see there).
  *           Every entry is written.  theta must not overlap the inputs.
+ * NTK_E_ARG also when NTK_OPT_LOGIT is not below O, or NTK_BATCH_DIAGONAL with n1 != n2.
  * Stream-ordered and asynchronous.  Deterministic: two calls with the same inputs
  * give bit-identical theta (no atomics).
  */

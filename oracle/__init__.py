@@ -14,6 +14,9 @@ Contents
   rows of I_O, Section 3.1.3), contracted block by block in float64.
 * `jacobian` -- the full per-sample Jacobian [N, O, P] for tiny nets.
 * `forward` -- the network function f(theta, x) itself.
+* `ntk_jc_variant` -- the output-trace, single-logit and batch-diagonal parts of
+  Theta, contracted directly from the Jacobian rows they need (appendix
+  "Pseudo-NTK").
 * `ntk_structured_fp64` -- a secondary fp64 reference for fully-connected nets
   that evaluates the per-layer formula of Section 4.1 (input Gram times
   cotangent Gram, summed over layers).  It is not the definition: the tests pin
@@ -27,6 +30,7 @@ positive semi-definiteness and homogeneity.
 """
 from .ntk_jc import forward, jacobian, ntk_jc, ntk_jc_with_norms, param_count
 from .structured_fp64 import ntk_structured_diag_fp64, ntk_structured_fp64
+from .variants import ntk_jc_variant
 
 __all__ = ["forward", "jacobian", "ntk_jc", "ntk_jc_with_norms", "param_count",
-           "ntk_structured_fp64", "ntk_structured_diag_fp64"]
+           "ntk_structured_fp64", "ntk_structured_diag_fp64", "ntk_jc_variant"]

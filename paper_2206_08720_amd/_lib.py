@@ -26,6 +26,9 @@ NTK_DENSE, NTK_CONV3X3_SAME, NTK_GAP = 0, 1, 2
 NTK_ACT_NONE, NTK_ACT_RELU, NTK_ACT_ERF = 0, 1, 2
 NTK_OPT_SYMMETRIC, NTK_OPT_CONV_ORDER = 1, 2
 NTK_CONV_ORDER_AUTO, NTK_CONV_ORDER_OUTSIDE_IN, NTK_CONV_ORDER_INSIDE_OUT = 0, 1, 2
+NTK_OPT_OUTPUT, NTK_OPT_LOGIT, NTK_OPT_BATCH = 3, 4, 5
+NTK_OUTPUT_FULL, NTK_OUTPUT_TRACE, NTK_OUTPUT_LOGIT = 0, 1, 2
+NTK_BATCH_FULL, NTK_BATCH_DIAGONAL = 0, 1
 
 EXPORTED_SYMBOLS = ("ntk_init", "ntk_compute", "ntk_free", "ntk_last_error", "ntk_set_option",
                     "ntk_set_stream", "ntk_workspace_bytes", "ntk_profile_enable",

@@ -445,10 +445,12 @@ k_ntk_splitk(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, int chunk, int symmetric,
   });
 }
 
-// theta[n1][n2][o1][o2] = sum_z part[z][r1][r2] + (o1 == o2) gram[n1, n2], or, with
-// accumulate, theta += sum_z part[z][r1][r2] (the readout summand is then already in theta).
+// theta[n1][n2][o1][o2] = w[n1, n2] sum_z part[z][r1][r2] + (o1 == o2) rscale gram[n1, n2], or,
+// with accumulate, theta += w[n1, n2] sum_z part[z][r1][r2] (the readout summand is then
+// already in theta).  w = null means 1; gram = null means no readout summand.
 __global__ void k_ntk_reduce(const float* __restrict__ part, int splits, int N1, int N2, int O,
-                             int symmetric, int tile, const float* __restrict__ gram, int accumulate,
+                             int symmetric, int tile, const float* __restrict__ w,
+                             const float* __restrict__ gram, float rscale, int accumulate,
                              float* __restrict__ theta) {
   const int R1 = N1 * O, R2 = N2 * O;
   const long long total = (long long)R1 * R2;
@@ -460,11 +462,12 @@ __global__ void k_ntk_reduce(const float* __restrict__ part, int splits, int N1,
     float v = 0.f;
     for (int z = 0; z < splits; ++z) v += part[(long long)z * total + src];
     const int n1 = r1 / O, o1 = r1 - n1 * O, n2 = r2 / O, o2 = r2 - n2 * O;
+    if (w) v *= w[(long long)n1 * N2 + n2];
     float* dst = theta + (((long long)n1 * N2 + n2) * O + o1) * O + o2;
     if (accumulate)
       v += *dst;
-    else if (o1 == o2)
-      v += gram[(long long)n1 * N2 + n2];
+    else if (o1 == o2 && gram)
+      v += rscale * gram[(long long)n1 * N2 + n2];
     *dst = v;
   }
 }
@@ -513,11 +516,12 @@ hipError_t launch_ntk_splitk(hipStream_t s, const float* J1, const float* J2, in
 }
 
 hipError_t launch_ntk_reduce(hipStream_t s, const float* part, int splits, int N1, int N2, int O,
-                             int symmetric, const float* gram, int accumulate, float* theta) {
+                             int symmetric, const float* w, const float* gram, float rscale,
+                             int accumulate, float* theta) {
   const long long total = (long long)N1 * O * N2 * O;
   const int blocks = (int)std::min<long long>((total + 255) / 256, 256 * 64);
   k_ntk_reduce<<<dim3(blocks), dim3(256), 0, s>>>(part, splits, N1, N2, O, symmetric, CfgSplitK::BM,
-                                                  gram, accumulate, theta);
+                                                  w, gram, rscale, accumulate, theta);
   return hipGetLastError();
 }
 
@@ -549,7 +553,8 @@ struct PairArgs {
 
 __global__ void __launch_bounds__(256)
 k_conv_pairsum(PairArgs a, int n1, int n2, int n2_offset, int O, int H, int W,
-               const float* __restrict__ gram, int accumulate, float* __restrict__ theta) {
+               const float* __restrict__ gram, int accumulate, int trace, int diag,
+               float* __restrict__ theta) {
   extern __shared__ float sm[];
   const int D = H * W;
   float* Hs = sm;                           // [D][D]; later the reduction scratch [256][OB]
@@ -557,9 +562,11 @@ k_conv_pairsum(PairArgs a, int n1, int n2, int n2_offset, int O, int H, int W,
   float* Ts = PK + kPairDMax * kPairDMax;   // [CC][D]
   float* Th = Ts + kPairCC * kPairDMax;     // [O][O]
   const int t = threadIdx.x;
-  const int i1 = blockIdx.x / n2, i2 = blockIdx.x % n2;   // sample indices within batch 1 / 2
+  // sample indices within batch 1 / 2 (batch diagonal: the pair (n, n))
+  const int i1 = diag ? blockIdx.x : blockIdx.x / n2, i2 = diag ? blockIdx.x : blockIdx.x % n2;
   const int s1 = i1, s2 = n2_offset + i2;                  // rows of the stacked batch
-  for (int q = t; q < O * O; q += 256) Th[q] = 0.f;
+  const int n_out = trace ? 1 : O * O;                     // outputs per pair
+  for (int q = t; q < n_out; q += 256) Th[q] = 0.f;
   for (int li = 0; li < a.count; ++li) {
     const PairLayer L = a.layer[li];
     const float* h1 = L.h + (long long)s1 * D * L.Cin;
@@ -601,7 +608,10 @@ k_conv_pairsum(PairArgs a, int n1, int n2, int n2_offset, int O, int H, int W,
         }
         __syncthreads();
         // theta[o1, o2] += sum_{p2, c} T[c, p2] G2[o2, p2, c0 + c], OB outputs at a time
-        for (int ob = 0; ob < O; ob += kPairOB) {
+        // (traced: only o2 = o1, summed into one value)
+        const int ob_begin = trace ? o1 : 0, ob_end = trace ? o1 + 1 : O;
+        for (int ob = ob_begin; ob < ob_end; ob += kPairOB) {
+          const int nb = min(kPairOB, ob_end - ob);
           float part[kPairOB];
 #pragma unroll
           for (int j = 0; j < kPairOB; ++j) part[j] = 0.f;
@@ -610,15 +620,15 @@ k_conv_pairsum(PairArgs a, int n1, int n2, int n2_offset, int O, int H, int W,
             const float tv = Ts[c * D + p2];
 #pragma unroll
             for (int j = 0; j < kPairOB; ++j)
-              if (ob + j < O) part[j] += tv * G2[((long long)(ob + j) * D + p2) * L.C + c0 + c];
+              if (j < nb) part[j] += tv * G2[((long long)(ob + j) * D + p2) * L.C + c0 + c];
           }
 #pragma unroll
           for (int j = 0; j < kPairOB; ++j) Hs[j * 256 + t] = part[j];
           __syncthreads();
-          if (t < kPairOB && ob + t < O) {
+          if (t < nb) {
             float v = 0.f;
             for (int q = 0; q < 256; ++q) v += Hs[t * 256 + q];
-            Th[o1 * O + ob + t] += v;
+            Th[trace ? 0 : o1 * O + ob + t] += v;
           }
           __syncthreads();
         }
@@ -626,13 +636,18 @@ k_conv_pairsum(PairArgs a, int n1, int n2, int n2_offset, int O, int H, int W,
     }
   }
   __syncthreads();
-  const float gr = gram[(long long)i1 * n2 + i2];
-  for (int q = t; q < O * O; q += 256) {
+  // readout summand (g1 . g2) delta_{o1 o2}; traced: O (g1 . g2).  gram is [n1, n2], or the
+  // per-sample [n] vector on the batch diagonal.
+  const float gr = diag ? gram[i1] : gram[(long long)i1 * n2 + i2];
+  const long long pair = diag ? i1 : (long long)i1 * n2 + i2;
+  for (int q = t; q < n_out; q += 256) {
     const int o1 = q / O, o2 = q - o1 * O;
-    float* dst = theta + (((long long)i1 * n2 + i2) * O) * O + q;
+    float* dst = theta + pair * n_out + q;
     float v = Th[q];
     if (accumulate)
       v += *dst;
+    else if (trace)
+      v += (float)O * gr;
     else if (o1 == o2)
       v += gr;
     *dst = v;
@@ -643,7 +658,7 @@ int pairsum_supported(int D, int O) { return D <= kPairDMax && O <= kPairOMax; }
 
 hipError_t launch_conv_pairsum(hipStream_t s, const PairLayerList& layers, int n1, int n2,
                                int n2_offset, int O, int H, int W, const float* gram, int accumulate,
-                               float* theta) {
+                               int trace, int diag, float* theta) {
   PairArgs a{};
   a.count = layers.count;
   for (int i = 0; i < layers.count; ++i) {
@@ -657,8 +672,9 @@ hipError_t launch_conv_pairsum(hipStream_t s, const PairLayerList& layers, int n
   hipError_t e = hipFuncSetAttribute((const void*)k_conv_pairsum,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   if (e != hipSuccess) return e;
-  k_conv_pairsum<<<dim3(n1 * n2), dim3(256), bytes, s>>>(a, n1, n2, n2_offset, O, H, W, gram,
-                                                         accumulate, theta);
+  k_conv_pairsum<<<dim3(diag ? n1 : n1 * n2), dim3(256), bytes, s>>>(a, n1, n2, n2_offset, O, H, W,
+                                                                     gram, accumulate, trace, diag,
+                                                                     theta);
   return hipGetLastError();
 }
 

@@ -324,7 +324,7 @@ k_ntk_fcn(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __
     if (r < R1 && s < R2) {
       const int n1 = (int)fO.div(r), o1 = r - n1 * O;
       const int n2 = (int)fO.div(s), o2 = s - n2 * O;
-      if (o1 == o2) v += smem[(n1 - n1lo) * S2 + (n2 - n2lo)];
+      if (o1 == o2) v += c.readout_scale * smem[(n1 - n1lo) * S2 + (n2 - n2lo)];
       theta[(((long long)n1 * N2 + n2) * O + o1) * O + o2] = v;
       if (mirror) theta[(((long long)n2 * N1 + n1) * O + o2) * O + o1] = v;
     }
@@ -348,8 +348,9 @@ k_ntk_fcn(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __
 // Final epilogue of a tile: add the readout summand, write theta (and its mirror).
 template <class Cfg>
 __device__ __forceinline__ void fcn_tile_out(f32x16 (&tot)[Cfg::FM][Cfg::FN], const float* gram_readout,
-                                             int N1, int N2, FastDiv fO, int R1, int R2, int m0, int n0,
-                                             bool mirror, float* smem, float* __restrict__ theta) {
+                                             float rscale, int N1, int N2, FastDiv fO, int R1, int R2,
+                                             int m0, int n0, bool mirror, float* smem,
+                                             float* __restrict__ theta) {
   const int O = (int)fO.d;
   int n1lo, n2lo, S2;
   stage_gram<Cfg>(gram_readout, N2, R1, R2, fO, m0, n0, smem, n1lo, n2lo, S2);
@@ -357,7 +358,7 @@ __device__ __forceinline__ void fcn_tile_out(f32x16 (&tot)[Cfg::FM][Cfg::FN], co
     if (r < R1 && s < R2) {
       const int n1 = (int)fO.div(r), o1 = r - n1 * O;
       const int n2 = (int)fO.div(s), o2 = s - n2 * O;
-      if (o1 == o2) v += smem[(n1 - n1lo) * S2 + (n2 - n2lo)];
+      if (o1 == o2) v += rscale * smem[(n1 - n1lo) * S2 + (n2 - n2lo)];
       theta[(((long long)n1 * N2 + n2) * O + o1) * O + o2] = v;
       if (mirror) theta[(((long long)n2 * N1 + n1) * O + o2) * O + o1] = v;
     }
@@ -426,7 +427,7 @@ k_ntk_fcn_sk(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float*
     f32x16 tot[Cfg::FM][Cfg::FN];
     zero_acc<Cfg>(tot);
     fcn_tile_layers<Cfg, VEC, DMA>(c, 0, L, N2, fO, R1, R2, m0, n0, smem, tot);
-    fcn_tile_out<Cfg>(tot, c.gram_readout, N1, N2, fO, R1, R2, m0, n0, symmetric && tm != tn, smem, theta);
+    fcn_tile_out<Cfg>(tot, c.gram_readout, c.readout_scale, N1, N2, fO, R1, R2, m0, n0, symmetric && tm != tn, smem, theta);
   }
   // stream-K over the XCD's remaining tiles
   const long long beg = sk_start(j, sh.U, P8), end = sk_start(j + 1, sh.U, P8);
@@ -441,7 +442,7 @@ k_ntk_fcn_sk(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float*
     zero_acc<Cfg>(tot);
     fcn_tile_layers<Cfg, VEC, DMA>(c, l0, l1, N2, fO, R1, R2, m0, n0, smem, tot);
     if (l0 == 0 && l1 == L) {
-      fcn_tile_out<Cfg>(tot, c.gram_readout, N1, N2, fO, R1, R2, m0, n0, symmetric && tm != tn, smem,
+      fcn_tile_out<Cfg>(tot, c.gram_readout, c.readout_scale, N1, N2, fO, R1, R2, m0, n0, symmetric && tm != tn, smem,
                         theta);
     } else {
       float* dst = part + ((long long)lam * 2 + sk_slot(beg, L, ts)) * (Cfg::BM * Cfg::BN);
@@ -458,7 +459,7 @@ k_ntk_fcn_sk(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float*
 constexpr int kFixupSplit = 16;
 template <class Cfg>
 __global__ void __launch_bounds__(256)
-k_ntk_fcn_fixup(int L, const float* __restrict__ gram_readout, int N1, int N2, FastDiv fO,
+k_ntk_fcn_fixup(int L, const float* __restrict__ gram_readout, float rscale, int N1, int N2, FastDiv fO,
                 int symmetric, float* __restrict__ theta, int tiles_m, int tiles_n, int T, int P,
                 const float* __restrict__ part) {
   static_assert(Cfg::BM * Cfg::BN == kFixupSplit * 256 * 4, "one float4 per thread");
@@ -500,7 +501,7 @@ k_ntk_fcn_fixup(int L, const float* __restrict__ gram_readout, int N1, int N2, F
     if (s < R2) {
       const int n2 = (int)fO.div(s), o2 = s - n2 * O;
       float w = vals[k];
-      if (o1 == o2) w += gram_readout[(long long)n1 * N2 + n2];
+      if (o1 == o2) w += rscale * gram_readout[(long long)n1 * N2 + n2];
       theta[(((long long)n1 * N2 + n2) * O + o1) * O + o2] = w;
       if (mirror) theta[(((long long)n2 * N1 + n1) * O + o2) * O + o1] = w;
     }
@@ -558,7 +559,7 @@ hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2
     e = hipGetLastError();
     if (e != hipSuccess) return e;
     k_ntk_fcn_fixup<Cfg><<<dim3(8 * (P / 8 - 1) * kFixupSplit), dim3(256), 0, s>>>(
-        c.L, c.gram_readout, N1, N2, fO, symmetric, theta, tm, tn, T, P, part);
+        c.L, c.gram_readout, c.readout_scale, N1, N2, fO, symmetric, theta, tm, tn, T, P, part);
     return hipGetLastError();
   };
   const long long big_tiles = (long long)cdiv(R1, 128) * cdiv(R2, 128);

@@ -27,6 +27,7 @@ enum KernelClass {
   KC_NTK_REDUCE,
   KC_CONV_PAIRSUM,
   KC_COPY,
+  KC_NTK_DIAG,
   KC_COUNT
 };
 const char* kernel_class_name(int cls);
@@ -62,14 +63,41 @@ struct FcnContraction {
   int K[kMaxLayers];
   int L;                          // number of hidden layers (summands with a cotangent Gram)
   const float* gram_readout;      // [N1, N2], multiplies delta_{o1 o2}
+  float readout_scale;            // factor of the readout summand (O for the output trace)
 };
 // theta[n1, n2, o1, o2] = sum_l gram_l[n1,n2] (G1_l G2_l^T)[(n1,o1),(n2,o2)]
-//                         + gram_readout[n1,n2] delta_{o1 o2}.
+//                         + readout_scale gram_readout[n1,n2] delta_{o1 o2}.
 // symmetric != 0: batch 2 is batch 1; only upper-triangle tiles run and mirror.
 // Large problems use a stream-K schedule over num_cu persistent workgroups with a partial
 // buffer `part` of ntk_fcn_part_floats(num_cu) floats (part may be null: no stream-K).
 long long ntk_fcn_part_floats(int num_cu);
 hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2, int O,
                           int symmetric, float* theta, int num_cu, float* part);
+
+// ---- output- and batch-axis variants ---------------------------------------------------
+struct RowdotBatch {
+  const float* a[kMaxLayers + 1];
+  const float* b[kMaxLayers + 1];
+  float* out[kMaxLayers + 1];
+  long long K[kMaxLayers + 1];    // row length = row stride
+  float beta[kMaxLayers + 1];
+  int count;
+};
+// out_j[n] = a_j[n] . b_j[n] + beta_j for n < N and every job j.
+hipError_t launch_rowdot(hipStream_t s, const RowdotBatch& r, int N);
+
+struct DiagTerms {
+  const float* A[kMaxLayers];     // per sample n: the O x K_l block at A_l + n O K_l (traced: 1 x K_l)
+  const float* B[kMaxLayers];
+  const float* w[kMaxLayers];     // per-sample weight w_l[n]; null = 1
+  long long K[kMaxLayers];
+  int count;
+  const float* readout;           // per-sample readout scalar; null = none
+  float readout_scale;
+};
+// O > 0: theta[n, o1, o2] (+)= sum_l w_l[n] (A_l[n] B_l[n]^T)[o1, o2] + readout_scale readout[n] delta.
+// O = 0 (traced): theta[n] (+)= sum_l w_l[n] (A_l[n] . B_l[n]) + readout_scale readout[n].
+// accumulate != 0 adds to theta.
+hipError_t launch_ntk_diag(hipStream_t s, const DiagTerms& t, int N, int O, int accumulate, float* theta);
 
 }  // namespace ntk

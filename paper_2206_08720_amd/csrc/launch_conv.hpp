@@ -30,9 +30,11 @@ int splitk_plan(int R1, int R2, long long K, int symmetric, long long part_capac
 hipError_t launch_ntk_splitk(hipStream_t s, const float* J1, const float* J2, int R1, int R2,
                              long long K, long long ld, int symmetric, int chunk, int splits,
                              float* part);
-// accumulate = 0: theta = partial sum + readout summand; 1: theta += partial sum.
+// accumulate = 0: theta = w (.) partial sum + rscale * readout summand; 1: theta += w (.) partial
+// sum.  w [N1, N2] may be null (= 1); gram [N1, N2] may be null (no readout summand).
 hipError_t launch_ntk_reduce(hipStream_t s, const float* part, int splits, int N1, int N2, int O,
-                             int symmetric, const float* gram, int accumulate, float* theta);
+                             int symmetric, const float* w, const float* gram, float rscale,
+                             int accumulate, float* theta);
 
 // Inside-out order for the conv layers listed (see k_conv_pairsum).  The G pointers must stay
 // valid until the kernel runs, so every listed layer's cotangent must still be resident.
@@ -44,8 +46,11 @@ struct PairLayerList {
   int count;
 };
 int pairsum_supported(int D, int O);
+// trace != 0: one value per pair, sum_o Theta[o, o] (readout summand O (g1 . g2)).
+// diag != 0: only the pairs (n, n), n < n1; gram is then the per-sample vector g1[n] . g2[n]
+// and theta is [n1, ...].
 hipError_t launch_conv_pairsum(hipStream_t s, const PairLayerList& layers, int n1, int n2,
                                int n2_offset, int O, int H, int W, const float* gram, int accumulate,
-                               float* theta);
+                               int trace, int diag, float* theta);
 
 }  // namespace ntk

@@ -24,7 +24,7 @@ const char* kernel_class_name(int cls) {
   static const char* names[KC_COUNT] = {
       "dense_fwd", "dense_bwd", "bwd_seed",  "gram",       "ntk_fcn",    "transpose",    "conv_fwd",
       "conv_bwd",  "conv_seed", "gap",       "conv_wgrad", "ntk_splitk", "ntk_reduce", "conv_pairsum",
-      "copy"};
+      "copy",      "ntk_diag"};
   return (cls >= 0 && cls < KC_COUNT) ? names[cls] : "?";
 }
 
@@ -91,6 +91,9 @@ struct ntk_handle {
   size_t ws_bytes = 0;
   int opt_symmetric = 1;
   int opt_conv_order = NTK_CONV_ORDER_AUTO;
+  int opt_output = NTK_OUTPUT_FULL;
+  int opt_logit = 0;
+  int opt_batch = NTK_BATCH_FULL;
   std::string err;
   Profiler prof;
 
@@ -105,6 +108,8 @@ struct ntk_handle {
   std::vector<int> param_index;   // first parameter slot of dense layer l
   int num_cu = 0;                 // compute units of the device (stream-K workgroup count)
   size_t off_skpart = 0;          // stream-K partial tiles of the contraction
+  size_t off_vpart = 0;           // split-K partials of the one-output variants (trace, logit)
+  long long vpart_capacity = 0;
 
   // ---- convolutional plan: conv layers 0..nc-1, GAP, dense readout
   int nc = 0, H = 0, W = 0, D = 0;
@@ -219,6 +224,12 @@ static void plan_fcn(ntk_handle* h) {
   for (int l = 1; l < L; ++l) h->off_Wt[l] = take((size_t)h->dims[l] * h->dims[l + 1]);
   for (int l = 0; l <= L; ++l) h->off_gram[l] = take((size_t)h->max_n1 * h->max_n2);
   h->off_skpart = take((size_t)ntk_fcn_part_floats(h->num_cu));
+  {
+    const int T = splitk_tile();
+    const size_t tiles_max = (size_t)((h->max_n1 + T - 1) / T) * ((h->max_n2 + T - 1) / T);
+    h->vpart_capacity = (long long)(1024 + tiles_max) * T * T;   // >= max_n1 * max_n2
+    h->off_vpart = take((size_t)h->vpart_capacity);
+  }
   h->ws_bytes = off;
   h->param_index.assign(L + 1, 0);
   int p = 0;
@@ -356,7 +367,12 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     prof_end(P, s, KC_DENSE_FWD);
     if (e != hipSuccess) return hip_fail(h, e, "dense forward");
   }
-  // 2. cotangents of every hidden pre-activation for all O outputs at once
+  // 2. cotangents of every hidden pre-activation for all O outputs at once (for the one
+  //    logit o* alone in NTK_OUTPUT_LOGIT: the cotangent rows are then (n) instead of (n, o))
+  const bool logit = h->opt_output == NTK_OUTPUT_LOGIT;
+  const bool trace = h->opt_output == NTK_OUTPUT_TRACE;
+  const bool diag = h->opt_batch == NTK_BATCH_DIAGONAL;
+  const int Oe = logit ? 1 : O;
   if (L >= 1) {
     for (int l = 1; l < L; ++l) {
       prof_begin(P, s, KC_TRANSPOSE);
@@ -364,26 +380,64 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
       prof_end(P, s, KC_TRANSPOSE);
       if (e != hipSuccess) return hip_fail(h, e, "weight transpose");
     }
+    const float* WL = params[h->param_index[L]] + (logit ? (size_t)h->opt_logit * h->dims[L] : 0);
     prof_begin(P, s, KC_BWD_SEED);
-    e = launch_bwd_seed(s, params[h->param_index[L]], F(h->off_dphi[L - 1]), M, O, h->dims[L],
-                        F(h->off_G[L - 1]));
+    e = launch_bwd_seed(s, WL, F(h->off_dphi[L - 1]), M, Oe, h->dims[L], F(h->off_G[L - 1]));
     prof_end(P, s, KC_BWD_SEED);
     if (e != hipSuccess) return hip_fail(h, e, "backward seed");
     for (int l = L - 1; l >= 1; --l) {
       prof_begin(P, s, KC_DENSE_BWD);
-      e = launch_dense_bwd(s, F(h->off_G[l]), F(h->off_Wt[l]), F(h->off_dphi[l - 1]), M * O,
-                           h->dims[l], h->dims[l + 1], O, F(h->off_G[l - 1]));
+      e = launch_dense_bwd(s, F(h->off_G[l]), F(h->off_Wt[l]), F(h->off_dphi[l - 1]), M * Oe,
+                           h->dims[l], h->dims[l + 1], Oe, F(h->off_G[l - 1]));
       prof_end(P, s, KC_DENSE_BWD);
       if (e != hipSuccess) return hip_fail(h, e, "dense backward");
     }
+  }
+  auto G1 = [&](int l) -> const float* { return F(h->off_G[l]); };
+  auto G2 = [&](int l) -> const float* {
+    return sym ? F(h->off_G[l]) : F(h->off_G[l]) + (size_t)n1 * Oe * h->dims[l + 1];
+  };
+  auto H2 = [&](int l) -> const float* { return sym ? hptr(l) : hptr(l) + (size_t)n1 * h->dims[l]; };
+  const float rscale = trace ? (float)O : 1.f;   // sum over o of delta_{oo} for the trace
+  if (diag) {
+    // 3'. batch diagonal: per-sample layer-input scalars d_l[n] = h1_l[n] . h2_l[n] (+1), then
+    //     theta[n] = sum_l d_l[n] G1_l[n] G2_l[n]^T + d_L[n] I (traced: a dot of O*K_l columns)
+    RowdotBatch rb{};
+    rb.count = L + 1;
+    for (int l = 0; l <= L; ++l) {
+      rb.a[l] = hptr(l);
+      rb.b[l] = H2(l);
+      rb.out[l] = F(h->off_gram[l]);
+      rb.K[l] = h->dims[l];
+      rb.beta[l] = h->layers[l].has_bias ? 1.0f : 0.0f;
+    }
+    prof_begin(P, s, KC_GRAM);
+    e = launch_rowdot(s, rb, n1);
+    prof_end(P, s, KC_GRAM);
+    if (e != hipSuccess) return hip_fail(h, e, "diagonal layer-input scalars");
+    DiagTerms t{};
+    t.count = L;
+    const bool flat = trace || logit;
+    for (int l = 0; l < L; ++l) {
+      t.A[l] = G1(l);
+      t.B[l] = G2(l);
+      t.w[l] = F(h->off_gram[l]);
+      t.K[l] = (long long)(flat ? Oe : 1) * h->dims[l + 1];
+    }
+    t.readout = F(h->off_gram[L]);
+    t.readout_scale = rscale;
+    prof_begin(P, s, KC_NTK_DIAG);
+    e = launch_ntk_diag(s, t, n1, flat ? 0 : O, 0, theta);
+    prof_end(P, s, KC_NTK_DIAG);
+    if (e != hipSuccess) return hip_fail(h, e, "diagonal contraction");
+    return NTK_OK;
   }
   // 3. layer-input Grams (the x1.x2 scalars), one batched launch
   GramBatch gb{};
   gb.count = L + 1;
   for (int l = 0; l <= L; ++l) {
-    const float* hl = hptr(l);
-    gb.h1[l] = hl;
-    gb.h2[l] = sym ? hl : hl + (size_t)n1 * h->dims[l];
+    gb.h1[l] = hptr(l);
+    gb.h2[l] = H2(l);
     gb.out[l] = F(h->off_gram[l]);
     gb.K[l] = h->dims[l];
     gb.beta[l] = h->layers[l].has_bias ? 1.0f : 0.0f;
@@ -392,16 +446,43 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   e = launch_gram(s, gb, n1, n2);
   prof_end(P, s, KC_GRAM);
   if (e != hipSuccess) return hip_fail(h, e, "gram");
+  if (trace || logit) {
+    // 4'. one output: per layer a split-K product of the cotangent rows (n) of Oe*K_l columns,
+    //     weighted by gram_l and accumulated into theta [n1, n2] layer by layer
+    if (L == 0) {
+      prof_begin(P, s, KC_NTK_REDUCE);
+      e = launch_ntk_reduce(s, F(h->off_vpart), 0, n1, n2, 1, 0, nullptr, F(h->off_gram[L]), rscale, 0,
+                            theta);
+      prof_end(P, s, KC_NTK_REDUCE);
+      if (e != hipSuccess) return hip_fail(h, e, "readout summand");
+    }
+    for (int l = 0; l < L; ++l) {
+      const long long K = (long long)Oe * h->dims[l + 1];
+      int chunk = 0;
+      const int splits = splitk_plan(n1, n2, K, sym ? 1 : 0, h->vpart_capacity, &chunk);
+      prof_begin(P, s, KC_NTK_SPLITK);
+      e = launch_ntk_splitk(s, G1(l), G2(l), n1, n2, K, K, sym ? 1 : 0, chunk, splits, F(h->off_vpart));
+      prof_end(P, s, KC_NTK_SPLITK);
+      if (e != hipSuccess) return hip_fail(h, e, "split-K contraction");
+      prof_begin(P, s, KC_NTK_REDUCE);
+      e = launch_ntk_reduce(s, F(h->off_vpart), splits, n1, n2, 1, sym ? 1 : 0, F(h->off_gram[l]),
+                            F(h->off_gram[L]), rscale, l > 0 ? 1 : 0, theta);
+      prof_end(P, s, KC_NTK_REDUCE);
+      if (e != hipSuccess) return hip_fail(h, e, "split-K reduction");
+    }
+    return NTK_OK;
+  }
   // 4. fused contraction summed over layers, written as theta[n1][n2][o1][o2]
   FcnContraction c{};
   c.L = L;
   for (int l = 0; l < L; ++l) {
-    c.G1[l] = F(h->off_G[l]);
-    c.G2[l] = sym ? F(h->off_G[l]) : F(h->off_G[l]) + (size_t)n1 * O * h->dims[l + 1];
+    c.G1[l] = G1(l);
+    c.G2[l] = G2(l);
     c.gram[l] = F(h->off_gram[l]);
     c.K[l] = h->dims[l + 1];
   }
   c.gram_readout = F(h->off_gram[L]);
+  c.readout_scale = 1.f;
   prof_begin(P, s, KC_NTK_FCN);
   e = launch_ntk_fcn(s, c, n1, n2, O, sym ? 1 : 0, theta, h->num_cu, F(h->off_skpart));
   prof_end(P, s, KC_NTK_FCN);
@@ -419,15 +500,23 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
   for (int l = 0; l <= nc; ++l)
     if (!params[l]) return fail(h, NTK_E_ARG, "null weight pointer");
+  // variants: one logit (the cotangent rows are then (n) instead of (n, o)), the trace over
+  // outputs, the batch diagonal (pairs (n, n) only)
+  const bool logit = h->opt_output == NTK_OUTPUT_LOGIT;
+  const bool trace = h->opt_output == NTK_OUTPUT_TRACE;
+  const bool diag = h->opt_batch == NTK_BATCH_DIAGONAL;
+  const int Oe = logit ? 1 : O;
+  const double pairs = diag ? (double)n1 : (double)n1 * n2;
+  const double Oc = trace ? (double)O : (double)Oe * Oe;   // output pairs per input pair
   // contraction order per layer: the cost model of the appendix "CNN NTK Complexity"
   // (outside-in N1 N2 O^2 F Cin Cout plus forming J, N O D F Cin Cout per sample, against
   // inside-out N1 N2 (D^2 F Cin + O D^2 Cout + O^2 D Cout)), or the forced option
   std::vector<char> inside(nc, 0);
-  const bool io_ok = pairsum_supported(D, O) != 0;
+  const bool io_ok = pairsum_supported(D, Oe) != 0;
   for (int l = 0; l < nc; ++l) {
     const double Cin = h->ch[l], Co = h->ch[l + 1];
-    const double oi = (double)n1 * n2 * O * O * 9 * Cin * Co + (double)M * O * D * 9 * Cin * Co;
-    const double io = (double)n1 * n2 * ((double)D * D * 9 * Cin + (double)O * D * D * Co + (double)O * O * D * Co);
+    const double oi = pairs * Oc * 9 * Cin * Co + (double)M * Oe * D * 9 * Cin * Co;
+    const double io = pairs * ((double)D * D * 9 * Cin + (double)Oe * D * D * Co + Oc * D * Co);
     if (h->opt_conv_order == NTK_CONV_ORDER_INSIDE_OUT) inside[l] = 1;
     else if (h->opt_conv_order == NTK_CONV_ORDER_AUTO) inside[l] = (io_ok && io < oi) ? 1 : 0;
   }
@@ -467,17 +556,31 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   e = launch_gap(s, F(h->off_ch[nc]), M, D, C, F(h->off_g));
   prof_end(P, s, KC_GAP);
   if (e != hipSuccess) return hip_fail(h, e, "global average pooling");
-  // readout summand: (g1 . g2) delta_{o1 o2}
-  GramBatch gb{};
-  gb.count = 1;
-  gb.h1[0] = F(h->off_g);
-  gb.h2[0] = sym ? F(h->off_g) : F(h->off_g) + (size_t)n1 * C;
-  gb.out[0] = F(h->off_gram_r);
-  gb.K[0] = C;
-  gb.beta[0] = 0.f;
-  prof_begin(P, s, KC_GRAM);
-  e = launch_gram(s, gb, n1, n2);
-  prof_end(P, s, KC_GRAM);
+  // readout summand: (g1 . g2) delta_{o1 o2} ([n1, n2], or [n] on the batch diagonal)
+  const float* g2p = sym ? F(h->off_g) : F(h->off_g) + (size_t)n1 * C;
+  if (diag) {
+    RowdotBatch rb{};
+    rb.count = 1;
+    rb.a[0] = F(h->off_g);
+    rb.b[0] = g2p;
+    rb.out[0] = F(h->off_gram_r);
+    rb.K[0] = C;
+    rb.beta[0] = 0.f;
+    prof_begin(P, s, KC_GRAM);
+    e = launch_rowdot(s, rb, n1);
+    prof_end(P, s, KC_GRAM);
+  } else {
+    GramBatch gb{};
+    gb.count = 1;
+    gb.h1[0] = F(h->off_g);
+    gb.h2[0] = g2p;
+    gb.out[0] = F(h->off_gram_r);
+    gb.K[0] = C;
+    gb.beta[0] = 0.f;
+    prof_begin(P, s, KC_GRAM);
+    e = launch_gram(s, gb, n1, n2);
+    prof_end(P, s, KC_GRAM);
+  }
   if (e != hipSuccess) return hip_fail(h, e, "gram");
   // 2. cotangents of every conv pre-activation for all O outputs, and per layer the
   //    weight-space cotangent J_l = sum_p G_l (x) patch_l (outside-in order)
@@ -490,7 +593,8 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   float* Gcur = F(h->off_Gping);
   float* Gnext = F(h->off_Gpong);
   prof_begin(P, s, KC_CONV_SEED);
-  e = launch_conv_seed(s, params[nc], F(h->off_cdphi[nc - 1]), M, O, D, C, Gcur);
+  const float* Wd = params[nc] + (logit ? (size_t)h->opt_logit * C : 0);
+  e = launch_conv_seed(s, Wd, F(h->off_cdphi[nc - 1]), M, Oe, D, C, Gcur);
   prof_end(P, s, KC_CONV_SEED);
   if (e != hipSuccess) return hip_fail(h, e, "conv seed");
   float* J = F(h->off_J);
@@ -505,38 +609,60 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
       pl.Cin[0] = h->ch[l];
       pl.C[0] = h->ch[l + 1];
       prof_begin(P, s, KC_CONV_PAIRSUM);
-      e = launch_conv_pairsum(s, pl, n1, n2, n2_off, O, H, W, F(h->off_gram_r), theta_written ? 1 : 0, theta);
+      e = launch_conv_pairsum(s, pl, n1, n2, n2_off, Oe, H, W, F(h->off_gram_r), theta_written ? 1 : 0,
+                              trace ? 1 : 0, diag ? 1 : 0, theta);
       prof_end(P, s, KC_CONV_PAIRSUM);
       if (e != hipSuccess) return hip_fail(h, e, "conv inside-out pair sum");
       theta_written = true;
     } else {
       prof_begin(P, s, KC_CONV_WGRAD);
-      e = launch_conv_wgrad(s, Gcur, hptr(l), M, O, H, W, h->ch[l + 1], h->ch[l], J, Kcall, jo[l]);
+      e = launch_conv_wgrad(s, Gcur, hptr(l), M, Oe, H, W, h->ch[l + 1], h->ch[l], J, Kcall, jo[l]);
       prof_end(P, s, KC_CONV_WGRAD);
       if (e != hipSuccess) return hip_fail(h, e, "conv weight-space cotangent");
     }
     if (l >= 1) {
       prof_begin(P, s, KC_CONV_BWD);
-      e = launch_conv_bwd(s, Gcur, M, O, H, W, h->ch[l + 1], F(h->off_Kt[l]), h->ch[l],
+      e = launch_conv_bwd(s, Gcur, M, Oe, H, W, h->ch[l + 1], F(h->off_Kt[l]), h->ch[l],
                           F(h->off_cdphi[l - 1]), Gnext);
       prof_end(P, s, KC_CONV_BWD);
       if (e != hipSuccess) return hip_fail(h, e, "conv backward");
       std::swap(Gcur, Gnext);
     }
   }
-  // 3. Theta += J1 J2^T over the outside-in layers (deterministic split over K)
+  // 3. Theta += J1 J2^T over the outside-in layers (deterministic split over K).  The J rows
+  //    of one sample are contiguous, so the traced variant contracts rows (n) of Oe*Kcall
+  //    columns; the batch diagonal contracts each sample's rows with its own.
   if (Kcall > 0) {
-    const int R1 = n1 * O, R2 = n2 * O;
+    const float* J2 = sym ? J : J + (size_t)n1 * Oe * Kcall;
+    const float rscale = trace ? (float)O : 1.f;
+    if (diag) {
+      DiagTerms t{};
+      t.count = 1;
+      t.A[0] = J;
+      t.B[0] = J2;
+      t.w[0] = nullptr;
+      const bool flat = trace || logit;
+      t.K[0] = (flat ? Oe : 1) * Kcall;
+      t.readout = F(h->off_gram_r);
+      t.readout_scale = rscale;
+      prof_begin(P, s, KC_NTK_DIAG);
+      e = launch_ntk_diag(s, t, n1, flat ? 0 : O, theta_written ? 1 : 0, theta);
+      prof_end(P, s, KC_NTK_DIAG);
+      if (e != hipSuccess) return hip_fail(h, e, "diagonal contraction");
+      return NTK_OK;
+    }
+    const int Or = trace ? 1 : Oe;                 // rows per sample of the contraction
+    const long long Kc = trace ? (long long)O * Kcall : Kcall;
+    const int R1 = n1 * Or, R2 = n2 * Or;
     int chunk = 0;
-    const int splits = splitk_plan(R1, R2, Kcall, sym ? 1 : 0, h->part_capacity, &chunk);
-    const float* J2 = sym ? J : J + (size_t)n1 * O * Kcall;
+    const int splits = splitk_plan(R1, R2, Kc, sym ? 1 : 0, h->part_capacity, &chunk);
     prof_begin(P, s, KC_NTK_SPLITK);
-    e = launch_ntk_splitk(s, J, J2, R1, R2, Kcall, Kcall, sym ? 1 : 0, chunk, splits, F(h->off_part));
+    e = launch_ntk_splitk(s, J, J2, R1, R2, Kc, Kc, sym ? 1 : 0, chunk, splits, F(h->off_part));
     prof_end(P, s, KC_NTK_SPLITK);
     if (e != hipSuccess) return hip_fail(h, e, "split-K contraction");
     prof_begin(P, s, KC_NTK_REDUCE);
-    e = launch_ntk_reduce(s, F(h->off_part), splits, n1, n2, O, sym ? 1 : 0, F(h->off_gram_r),
-                          theta_written ? 1 : 0, theta);
+    e = launch_ntk_reduce(s, F(h->off_part), splits, n1, n2, Or, sym ? 1 : 0, nullptr, F(h->off_gram_r),
+                          rscale, theta_written ? 1 : 0, theta);
     prof_end(P, s, KC_NTK_REDUCE);
     if (e != hipSuccess) return hip_fail(h, e, "split-K reduction");
   }
@@ -550,6 +676,10 @@ extern "C" int ntk_compute(ntk_handle* h, const float* const* params, const floa
   if (n1 <= 0 || n2 <= 0) return fail(h, NTK_E_ARG, "n1 and n2 must be positive");
   if (n1 > h->max_n1 || n2 > h->max_n2)
     return fail(h, NTK_E_ARG, "n1/n2 exceed the max_n1/max_n2 given to ntk_init");
+  if (h->opt_output == NTK_OUTPUT_LOGIT && h->opt_logit >= h->out_dim)
+    return fail(h, NTK_E_ARG, "NTK_OPT_LOGIT must be below the number of outputs");
+  if (h->opt_batch == NTK_BATCH_DIAGONAL && n1 != n2)
+    return fail(h, NTK_E_ARG, "NTK_BATCH_DIAGONAL needs n1 == n2");
   h->err.clear();
   if (h->cnn) return compute_cnn(h, params, X1, n1, X2, n2, theta);
   return compute_fcn(h, params, X1, n1, X2, n2, theta);
@@ -578,6 +708,23 @@ extern "C" int ntk_set_option(ntk_handle* h, int option, int value) {
     if (value < NTK_CONV_ORDER_AUTO || value > NTK_CONV_ORDER_INSIDE_OUT)
       return fail(h, NTK_E_ARG, "NTK_OPT_CONV_ORDER takes 0, 1 or 2");
     h->opt_conv_order = value;
+    return NTK_OK;
+  }
+  if (option == NTK_OPT_OUTPUT) {
+    if (value != NTK_OUTPUT_FULL && value != NTK_OUTPUT_TRACE && value != NTK_OUTPUT_LOGIT)
+      return fail(h, NTK_E_ARG, "NTK_OPT_OUTPUT takes NTK_OUTPUT_FULL, _TRACE or _LOGIT");
+    h->opt_output = value;
+    return NTK_OK;
+  }
+  if (option == NTK_OPT_LOGIT) {
+    if (value < 0 || value >= h->out_dim) return fail(h, NTK_E_ARG, "NTK_OPT_LOGIT must be in [0, O)");
+    h->opt_logit = value;
+    return NTK_OK;
+  }
+  if (option == NTK_OPT_BATCH) {
+    if (value != NTK_BATCH_FULL && value != NTK_BATCH_DIAGONAL)
+      return fail(h, NTK_E_ARG, "NTK_OPT_BATCH takes NTK_BATCH_FULL or NTK_BATCH_DIAGONAL");
+    h->opt_batch = value;
     return NTK_OK;
   }
   return fail(h, NTK_E_ARG, "unknown option");

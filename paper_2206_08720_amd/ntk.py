@@ -35,10 +35,31 @@ class NTK:
             _lib.check(self._lib.ntk_init(ctypes.byref(desc), self.max_n1, self.max_n2,
                                           ctypes.c_void_p(s.cuda_stream), ctypes.byref(h)))
         self._h = h
+        self._output = _lib.NTK_OUTPUT_FULL
+        self._batch = _lib.NTK_BATCH_FULL
 
     # -- options -----------------------------------------------------------------------
     def set_option(self, option, value):
         _lib.check(self._lib.ntk_set_option(self._h, option, value), self._h)
+        if option == _lib.NTK_OPT_OUTPUT:
+            self._output = value
+        elif option == _lib.NTK_OPT_BATCH:
+            self._batch = value
+
+    def set_variant(self, output="full", batch="full", logit=0):
+        """output: "full" | "trace" | "logit" (with `logit` = o*); batch: "full" | "diagonal"."""
+        self.set_option(_lib.NTK_OPT_OUTPUT, {"full": _lib.NTK_OUTPUT_FULL, "trace": _lib.NTK_OUTPUT_TRACE,
+                                              "logit": _lib.NTK_OUTPUT_LOGIT}[output])
+        self.set_option(_lib.NTK_OPT_LOGIT, int(logit))
+        self.set_option(_lib.NTK_OPT_BATCH, {"full": _lib.NTK_BATCH_FULL,
+                                             "diagonal": _lib.NTK_BATCH_DIAGONAL}[batch])
+
+    def out_shape(self, n1, n2):
+        """Shape of theta for batches of n1 and n2 under the current variant options."""
+        O = self.out_dim
+        inner = (O, O) if self._output == _lib.NTK_OUTPUT_FULL else ()
+        outer = (n1,) if self._batch == _lib.NTK_BATCH_DIAGONAL else (n1, n2)
+        return outer + inner
 
     def set_stream(self, stream):
         self._stream = stream
@@ -55,7 +76,8 @@ class NTK:
             raise ValueError(f"{name} must be contiguous")
 
     def compute(self, params, X1, X2=None, out=None):
-        """Enqueue Theta(X1, X2) on the handle's stream; returns the [N1,N2,O,O] tensor."""
+        """Enqueue Theta(X1, X2) on the handle's stream; returns the [N1,N2,O,O] tensor (or the
+        variant's shape, `out_shape`)."""
         if X2 is None:
             X2 = X1
         for i, p in enumerate(params):
@@ -63,13 +85,13 @@ class NTK:
         self._check_tensor(X1, "X1")
         self._check_tensor(X2, "X2")
         n1, n2 = X1.shape[0], X2.shape[0]
-        O = self.out_dim
+        shape = self.out_shape(n1, n2)
         if out is None:
-            out = torch.empty((n1, n2, O, O), dtype=torch.float32, device=self.device)
+            out = torch.empty(shape, dtype=torch.float32, device=self.device)
         else:
             self._check_tensor(out, "out")
-            if tuple(out.shape) != (n1, n2, O, O):
-                raise ValueError("out has the wrong shape")
+            if tuple(out.shape) != shape:
+                raise ValueError(f"out has shape {tuple(out.shape)}, expected {shape}")
         ptrs = (ctypes.c_void_p * len(params))(*[p.data_ptr() for p in params])
         _lib.check(self._lib.ntk_compute(self._h, ptrs, ctypes.c_void_p(X1.data_ptr()), n1,
                                          ctypes.c_void_p(X2.data_ptr()), n2,
@@ -103,11 +125,12 @@ class NTK:
             pass
 
 
-def compute(spec, params, X1, X2=None):
+def compute(spec, params, X1, X2=None, output="full", batch="full", logit=0):
     """One-shot Theta(X1, X2) (allocates a handle sized for these batches)."""
     X2 = X1 if X2 is None else X2
     h = NTK(spec, X1.shape[0], X2.shape[0])
     try:
+        h.set_variant(output, batch, logit)
         out = h.compute(params, X1, X2)
         torch.cuda.current_stream().synchronize()
         return out

@@ -22,9 +22,10 @@ def to_dev(arrs):
 
 
 def gpu_ntk(spec, params, X1, X2, symmetric=True, handle=None, max_n=None, options=None,
-            profile=None):
+            profile=None, variant=None):
     """Theta from the HIP library.  options: {NTK_OPT_*: value}; profile: a dict that
-    receives the per-kernel-class timing of this call."""
+    receives the per-kernel-class timing of this call; variant: (output, batch, logit) for
+    NTK.set_variant."""
     import torch
     from paper_2206_08720_amd import _lib
     from paper_2206_08720_amd.ntk import NTK
@@ -35,6 +36,7 @@ def gpu_ntk(spec, params, X1, X2, symmetric=True, handle=None, max_n=None, optio
     h.set_option(_lib.NTK_OPT_SYMMETRIC, 1 if symmetric else 0)
     for k, v in (options or {}).items():
         h.set_option(k, v)
+    h.set_variant(*(variant or ("full", "full", 0)))
     if profile is not None:
         h.profile_read()
         h.profile_enable(True)
@@ -60,6 +62,47 @@ def errors(got, ref, d1, d2):
         print(f"[parity] worst entry at (n1, n2, o1, o2) = {tuple(int(i) for i in loc)}: "
               f"got {got[loc]!r} ref {ref[loc]!r}", flush=True)
     return cs, nw
+
+
+def scaled_errors(got, ref, scale):
+    """(cs_err, normwise_err) of got vs ref for any shape, with the per-entry error scale."""
+    diff = np.abs(got.astype(np.float64) - ref)
+    if not diff.size:
+        return 0.0, 0.0
+    cs = float(np.max(diff / np.maximum(scale, 1e-300)))
+    nw = float(np.max(diff) / max(np.max(np.abs(ref)), 1e-300))
+    if cs > TOL:
+        loc = np.unravel_index(np.argmax(diff / np.maximum(scale, 1e-300)), diff.shape)
+        print(f"[parity] worst entry at {tuple(int(i) for i in loc)}: got {got[loc]!r} "
+              f"ref {ref[loc]!r} scale {scale[loc]!r}", flush=True)
+    return cs, nw
+
+
+def variant_of(full, output, batch, logit=0):
+    """The variant read off a full Theta [N1, N2, O, O] (or its error scale)."""
+    if batch == "diagonal":
+        n = np.arange(full.shape[0])
+        full = full[n, n]
+    if output == "trace":
+        return np.trace(full, axis1=-2, axis2=-1)
+    if output == "logit":
+        return full[..., logit, logit]
+    return full
+
+
+def variant_scale(d1, d2, output, batch, logit=0):
+    """Per-entry error scale of a variant from the Jacobian row norms d1 [N1,O], d2 [N2,O]."""
+    if output == "trace":
+        a, b = d1.sum(1), d2.sum(1)
+    elif output == "logit":
+        a, b = d1[:, logit], d2[:, logit]
+    else:
+        a, b = d1, d2
+    if batch == "diagonal":
+        return np.sqrt(a[:, :, None] * b[:, None, :]) if output == "full" else np.sqrt(a * b)
+    if output == "full":
+        return np.sqrt(a[:, None, :, None] * b[None, :, None, :])
+    return np.sqrt(a[:, None] * b[None, :])
 
 
 def diag_norms(theta_xx):
