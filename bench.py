@@ -33,7 +33,8 @@ HBM_PEAK_GBS = 8000.0
 # kernel class -> stage of the FLOP counter
 STAGE_OF = {"dense_fwd": "forward", "dense_bwd": "backward", "gram": "gram",
             "ntk_fcn": "contraction", "conv_fwd": "forward", "conv_bwd": "backward",
-            "conv_wgrad": "wgrad", "ntk_splitk": "contraction", "conv_pairsum": "contraction"}
+            "conv_wgrad": "wgrad", "ntk_splitk": "contraction", "conv_pairsum": "contraction",
+            "ntk_diag": "contraction"}
 
 
 def parse():
@@ -43,6 +44,15 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="relu_mlp_d8_w2048")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--output", default="full", choices=["full", "trace", "logit"],
+                    help="output-axis variant (the default is the full O x O block)")
+    ap.add_argument("--batch", default="full", choices=["full", "diagonal"],
+                    help="batch-axis variant (diagonal: Theta(x1_n, x2_n) only)")
+    ap.add_argument("--logit", type=int, default=0, help="o* of --output logit")
+    ap.add_argument("--method", default="structured", choices=["structured", "jacobian"],
+                    help="structured derivatives (default) or the Jacobian-contraction baseline")
+    ap.add_argument("--samples", type=int, default=0,
+                    help="use only the first N samples of X1 and of X2 (0: the whole workload)")
     ap.add_argument("--cpu-samples", type=int, default=6,
                     help="samples per side of the oracle's bounded sample")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -142,6 +152,10 @@ def main():
     torch.cuda.set_device(0)
     name = args.workload
     spec, params, X1, X2 = wl.make_workload(name)
+    if args.samples:
+        aliased = X2 is X1
+        X1 = X1[:args.samples]
+        X2 = X1 if aliased else X2[:args.samples]
     sym = X2 is X1
     dev = [torch.from_numpy(p).cuda() for p in params]
     x1 = torch.from_numpy(X1).cuda()
@@ -149,7 +163,9 @@ def main():
     n1, n2 = X1.shape[0], X2.shape[0]
     O = spec["layers"][-1]["out"]
     h = NTK(spec, n1, n2)
-    out = torch.empty((n1, n2, O, O), dtype=torch.float32, device="cuda")
+    h.set_variant(args.output, args.batch, args.logit)
+    h.set_method(args.method)
+    out = torch.empty(h.out_shape(n1, n2), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
 
     for _ in range(args.warmup):
@@ -173,8 +189,9 @@ def main():
     prof = h.profile_read()
     h.profile_enable(False)
 
-    entries = ntk_entries(spec, n1, n2)
-    fl = ntk_flops(spec, n1, n2, symmetric=sym)
+    entries = ntk_entries(spec, n1, n2, args.output, args.batch)
+    fl = ntk_flops(spec, n1, n2, symmetric=sym, output=args.output, batch=args.batch,
+                   method=args.method)
     value = entries / (ms * 1e-3)
     tflops = fl["total"] / (ms * 1e-3) / 1e12
 
@@ -185,7 +202,7 @@ def main():
         st = STAGE_OF.get(k)
         if st and st in fl and cnt:
             kernels[k]["tflops"] = fl[st] / (tot / args.steps * 1e-3) / 1e12
-    dom = max(prof, key=lambda k: prof[k][0])
+    dom = max((k for k in prof if STAGE_OF.get(k) in fl), key=lambda k: prof[k][0])
     tot, cnt = prof[dom]
     avg_ms = tot / cnt
     flop_per_launch = fl[STAGE_OF[dom]] / (cnt / args.steps)
@@ -210,7 +227,10 @@ def main():
         "data": "synthetic (seeded N(0,1) inputs, He-init weights)",
         "config": {"workload": name, "n1": n1, "n2": n2, "O": O,
                    "layers": [[L.get("in"), L.get("out"), L.get("act")] for L in spec["layers"]],
-                   "symmetric_schedule": sym, "parallelism": "single GPU"},
+                   "symmetric_schedule": sym, "parallelism": "single GPU",
+                   "method": args.method,
+                   "variant": {"output": args.output, "batch": args.batch,
+                               **({"logit": args.logit} if args.output == "logit" else {})}},
         "tflops": tflops, "frac_of_fp32_mfma_peak": tflops / FP32_MFMA_PEAK_TFLOPS,
         "algorithmic_flops": fl, "kernels": kernels, "roofline": roofline,
         "mfma_ceiling_measured": ceiling,
@@ -218,7 +238,8 @@ def main():
                    "peak_clock_mhz": clock_khz / 1000.0},
         "wall_s_timed_region": wall,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.output == "full" and args.batch == "full" \
+            and not args.samples:
         res["cpu_baseline"] = cpu_baseline(name, min(args.cpu_samples, n1, n2), n1, n2)
     print(json.dumps(res), flush=True)
 

@@ -121,6 +121,18 @@ typedef struct ntk_handle ntk_handle;
 #define NTK_OPT_BATCH       5
 #define NTK_BATCH_FULL      0
 #define NTK_BATCH_DIAGONAL  1
+/* NTK_OPT_METHOD: how Theta is computed.
+ *   NTK_METHOD_STRUCTURED (default) the structured-derivatives method of Section 3.4;
+ *   NTK_METHOD_JACOBIAN   the Jacobian-contraction baseline of Section 3.2: the per-sample
+ *                         Jacobian df/dtheta (reverse mode, O vector-Jacobian products) is
+ *                         formed explicitly, block by block, and Theta = J(x1) J(x2)^T is
+ *                         contracted on the matrix cores (N1 N2 O^2 P multiply-adds).  Conv
+ *                         layers then use the outside-in order.  It exists for comparison;
+ *                         the first call on a handle allocates its Jacobian buffers.
+ * Every variant of NTK_OPT_OUTPUT / NTK_OPT_BATCH is available with both methods.          */
+#define NTK_OPT_METHOD             6
+#define NTK_METHOD_STRUCTURED      0
+#define NTK_METHOD_JACOBIAN        1
 
 /*
  * ntk_init -- validate a model descriptor, plan and allocate the workspace.

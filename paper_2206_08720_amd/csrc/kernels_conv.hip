@@ -459,8 +459,14 @@ __global__ void k_ntk_reduce(const float* __restrict__ part, int splits, int N1,
     const int r1 = (int)(i / R2), r2 = (int)(i - (long long)r1 * R2);
     long long src = i;
     if (symmetric && (r1 / tile) > (r2 / tile)) src = (long long)r2 * R2 + r1;
-    float v = 0.f;
-    for (int z = 0; z < splits; ++z) v += part[(long long)z * total + src];
+    float a[4] = {0.f, 0.f, 0.f, 0.f};   // four independent chains keep several loads in flight
+    int z = 0;
+    for (; z + 4 <= splits; z += 4) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) a[u] += part[(long long)(z + u) * total + src];
+    }
+    for (; z < splits; ++z) a[0] += part[(long long)z * total + src];
+    float v = (a[0] + a[1]) + (a[2] + a[3]);
     const int n1 = r1 / O, o1 = r1 - n1 * O, n2 = r2 / O, o2 = r2 - n2 * O;
     if (w) v *= w[(long long)n1 * N2 + n2];
     float* dst = theta + (((long long)n1 * N2 + n2) * O + o1) * O + o2;

@@ -115,8 +115,62 @@ k_ntk_diag_block(DiagTerms t, int O, int tiles_o, int accumulate, float* __restr
   });
 }
 
+// K-segmented form: segment g covers columns [kb, ke) of one term l; every (segment, sample,
+// tile) is one wave writing w_l[n] times its partial product to part[g][n][o1][o2], and
+// k_ntk_diag_reduce adds the segments in order.
+struct DiagSegs {
+  int base[kMaxLayers + 1];   // first segment of term l; base[count] = number of segments
+  int len[kMaxLayers];        // columns per segment of term l (a multiple of the K tile)
+};
+
+template <bool VEC>
+__global__ void __launch_bounds__(64)
+k_ntk_diag_seg(DiagTerms t, DiagSegs sg, int N, int O, int tiles_o, float* __restrict__ part) {
+  using Cfg = CfgDiag;
+  extern __shared__ float smem[];
+  const int tiles = tiles_o * tiles_o;
+  const int per_seg = N * tiles;
+  const int g = blockIdx.x / per_seg, rem = blockIdx.x % per_seg;
+  const int n = rem / tiles, tt = rem % tiles;
+  int l = 0;
+  while (sg.base[l + 1] <= g) ++l;
+  const int K = (int)t.K[l];
+  const int kb = (g - sg.base[l]) * sg.len[l], ke = min(K, kb + sg.len[l]);
+  const int m0 = (tt / tiles_o) * Cfg::BM, n0 = (tt % tiles_o) * Cfg::BN;
+  LoadKInnerT<VEC> la{t.A[l] + (long long)n * O * K, O, K, K};
+  LoadKInnerT<VEC> lb{t.B[l] + (long long)n * O * K, O, K, K};
+  f32x16 acc[1][1];
+  zero_acc<Cfg>(acc);
+  gemm_mainloop<Cfg>(la, lb, m0, n0, kb, ke, smem, acc);
+  const float w = t.w[l] ? t.w[l][n] : 1.f;
+  float* out = part + ((long long)g * N + n) * O * O;
+  for_each_acc<Cfg>(acc, m0, n0, [&](int o1, int o2, float v) {
+    if (o1 < O && o2 < O) out[(long long)o1 * O + o2] = w * v;
+  });
+}
+
+__global__ void __launch_bounds__(256)
+k_ntk_diag_reduce(const float* __restrict__ part, int nseg, int N, int O, const float* __restrict__ readout,
+                  float rscale, int accumulate, float* __restrict__ theta) {
+  const long long total = (long long)N * O * O;
+  for (long long i = blockIdx.x * 256LL + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
+    float acc[4] = {0.f, 0.f, 0.f, 0.f};
+    int g = 0;
+    for (; g + 4 <= nseg; g += 4) {
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[u] += part[(long long)(g + u) * total + i];
+    }
+    for (; g < nseg; ++g) acc[0] += part[(long long)g * total + i];
+    float v = (acc[0] + acc[1]) + (acc[2] + acc[3]);
+    const int n = (int)(i / ((long long)O * O));
+    const int q = (int)(i - (long long)n * O * O);
+    if (readout && q / O == q % O) v += rscale * readout[n];
+    theta[i] = accumulate ? theta[i] + v : v;
+  }
+}
+
 hipError_t launch_ntk_diag(hipStream_t s, const DiagTerms& t, int N, int O, int accumulate,
-                           float* theta) {
+                           float* theta, float* part, long long part_capacity) {
   if (N <= 0) return hipSuccess;
   if (O == 0) {   // traced: one value per sample
     k_ntk_diag_flat<<<dim3(N), dim3(256), 0, s>>>(t, accumulate, theta);
@@ -127,12 +181,46 @@ hipError_t launch_ntk_diag(hipStream_t s, const DiagTerms& t, int N, int O, int 
   const int tiles_o = (O + CfgDiag::BM - 1) / CfgDiag::BM;
   using L = LoadKInnerT<true>;
   constexpr int bytes = gemm_smem_bytes<CfgDiag, L, L>();
+  // segments: about 2048 waves in all, at least 8 K tiles per segment, whole terms at least
+  const long long waves_per_seg = (long long)N * tiles_o * tiles_o;
+  long long Ktot = 0;
+  for (int l = 0; l < t.count; ++l) Ktot += t.K[l];
+  const long long want = std::max<long long>(1, (2048 + waves_per_seg - 1) / waves_per_seg);
+  DiagSegs sg{};
+  int nseg = 0;
+  for (int l = 0; l < t.count; ++l) {
+    const long long K = t.K[l];
+    long long nl = std::max<long long>(1, (want * K + Ktot - 1) / std::max<long long>(Ktot, 1));
+    nl = std::min<long long>(nl, std::max<long long>(1, K / (8 * CfgDiag::BK)));
+    long long len = (K + nl - 1) / nl;
+    len = ((len + CfgDiag::BK - 1) / CfgDiag::BK) * CfgDiag::BK;
+    sg.base[l] = nseg;
+    sg.len[l] = (int)len;
+    nseg += (int)((K + len - 1) / len);
+  }
+  sg.base[t.count] = nseg;
+  const bool seg_ok = part && t.count > 0 && (long long)nseg * N * O * O <= part_capacity &&
+                      Ktot < (1LL << 31);
+  if (!seg_ok) {
+    if (v)
+      k_ntk_diag_block<true><<<dim3(N * tiles_o * tiles_o), dim3(CfgDiag::THREADS), bytes, s>>>(
+          t, O, tiles_o, accumulate, theta);
+    else
+      k_ntk_diag_block<false><<<dim3(N * tiles_o * tiles_o), dim3(CfgDiag::THREADS), bytes, s>>>(
+          t, O, tiles_o, accumulate, theta);
+    return hipGetLastError();
+  }
+  const long long grid = (long long)nseg * waves_per_seg;
   if (v)
-    k_ntk_diag_block<true><<<dim3(N * tiles_o * tiles_o), dim3(CfgDiag::THREADS), bytes, s>>>(
-        t, O, tiles_o, accumulate, theta);
+    k_ntk_diag_seg<true><<<dim3((unsigned)grid), dim3(CfgDiag::THREADS), bytes, s>>>(t, sg, N, O, tiles_o, part);
   else
-    k_ntk_diag_block<false><<<dim3(N * tiles_o * tiles_o), dim3(CfgDiag::THREADS), bytes, s>>>(
-        t, O, tiles_o, accumulate, theta);
+    k_ntk_diag_seg<false><<<dim3((unsigned)grid), dim3(CfgDiag::THREADS), bytes, s>>>(t, sg, N, O, tiles_o, part);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  const long long total = (long long)N * O * O;
+  const int blocks = (int)std::min<long long>((total + 255) / 256, 4096);
+  k_ntk_diag_reduce<<<dim3(blocks), dim3(256), 0, s>>>(part, nseg, N, O, t.readout, t.readout_scale,
+                                                       accumulate, theta);
   return hipGetLastError();
 }
 

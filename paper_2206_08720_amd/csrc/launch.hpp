@@ -2,6 +2,8 @@
 #pragma once
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 namespace ntk {
 
 constexpr int kMaxLayers = 64;  // parametrised layers a model may have
@@ -28,6 +30,7 @@ enum KernelClass {
   KC_CONV_PAIRSUM,
   KC_COPY,
   KC_NTK_DIAG,
+  KC_JC_JACOBIAN,
   KC_COUNT
 };
 const char* kernel_class_name(int cls);
@@ -97,7 +100,17 @@ struct DiagTerms {
 };
 // O > 0: theta[n, o1, o2] (+)= sum_l w_l[n] (A_l[n] B_l[n]^T)[o1, o2] + readout_scale readout[n] delta.
 // O = 0 (traced): theta[n] (+)= sum_l w_l[n] (A_l[n] . B_l[n]) + readout_scale readout[n].
-// accumulate != 0 adds to theta.
-hipError_t launch_ntk_diag(hipStream_t s, const DiagTerms& t, int N, int O, int accumulate, float* theta);
+// accumulate != 0 adds to theta.  `part` (capacity floats, may be null) holds partial products
+// of K segments when the samples alone are too few to fill the device.
+hipError_t launch_ntk_diag(hipStream_t s, const DiagTerms& t, int N, int O, int accumulate, float* theta,
+                           float* part, long long part_capacity);
+
+// ---- Jacobian-contraction baseline -----------------------------------------------------
+// One column chunk of a dense layer's explicit Jacobian block (see kernels_jc.hip):
+// out [R, cc*d (+cc)] with rows (n, o), Oe rows per sample.  G [R, ldG] is the cotangent of
+// the layer output, or null for the readout layer (identity cotangent; only_o >= 0 when the
+// rows are the one output only_o).
+hipError_t launch_jc_dense(hipStream_t s, const float* G, long long ldG, const float* h, int d, int R,
+                           int Oe, int only_o, int c0, int cc, int bias, float* out);
 
 }  // namespace ntk

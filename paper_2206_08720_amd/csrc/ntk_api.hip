@@ -24,7 +24,7 @@ const char* kernel_class_name(int cls) {
   static const char* names[KC_COUNT] = {
       "dense_fwd", "dense_bwd", "bwd_seed",  "gram",       "ntk_fcn",    "transpose",    "conv_fwd",
       "conv_bwd",  "conv_seed", "gap",       "conv_wgrad", "ntk_splitk", "ntk_reduce", "conv_pairsum",
-      "copy",      "ntk_diag"};
+      "copy",      "ntk_diag",  "jc_jacobian"};
   return (cls >= 0 && cls < KC_COUNT) ? names[cls] : "?";
 }
 
@@ -94,6 +94,12 @@ struct ntk_handle {
   int opt_output = NTK_OUTPUT_FULL;
   int opt_logit = 0;
   int opt_batch = NTK_BATCH_FULL;
+  int opt_method = NTK_METHOD_STRUCTURED;
+  // Jacobian-contraction baseline: explicit Jacobian chunks of both batches and the split-K
+  // partials of their product, allocated by the first call that needs them
+  char* jc_ws = nullptr;
+  size_t jc_side_floats = 0;
+  long long jc_part_capacity = 0;
   std::string err;
   Profiler prof;
 
@@ -329,6 +335,101 @@ extern "C" int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, voi
   return NTK_OK;
 }
 
+
+// ------------------------------------------------------------------------------ shared contraction
+// theta (+)= the selected variant of A B^T, for row blocks A [n1*Oe, K] and B [n2*Oe, K]
+// (rows (n, o), row stride K): the full product through split-K partials in `part`, the
+// output trace as rows (n) of Oe*K columns, the batch diagonal per sample.  No readout term.
+static hipError_t contract_rows(ntk_handle* h, const float* A, const float* B, int n1, int n2, int Oe,
+                                bool trace, bool diag, bool sym, long long K, int accumulate,
+                                float* theta, float* part, long long part_capacity) {
+  hipStream_t s = h->stream;
+  Profiler* P = &h->prof;
+  hipError_t e;
+  const bool flat = trace || Oe == 1;
+  if (diag) {
+    DiagTerms t{};
+    t.count = 1;
+    t.A[0] = A;
+    t.B[0] = B;
+    t.w[0] = nullptr;
+    t.K[0] = flat ? (long long)Oe * K : K;
+    t.readout = nullptr;
+    t.readout_scale = 0.f;
+    prof_begin(P, s, KC_NTK_DIAG);
+    e = launch_ntk_diag(s, t, n1, flat ? 0 : Oe, accumulate, theta, part, part_capacity);
+    prof_end(P, s, KC_NTK_DIAG);
+    return e;
+  }
+  const int Or = trace ? 1 : Oe;
+  const long long Kc = trace ? (long long)Oe * K : K;
+  int chunk = 0;
+  const int splits = splitk_plan(n1 * Or, n2 * Or, Kc, sym ? 1 : 0, part_capacity, &chunk);
+  prof_begin(P, s, KC_NTK_SPLITK);
+  e = launch_ntk_splitk(s, A, B, n1 * Or, n2 * Or, Kc, Kc, sym ? 1 : 0, chunk, splits, part);
+  prof_end(P, s, KC_NTK_SPLITK);
+  if (e != hipSuccess) return e;
+  prof_begin(P, s, KC_NTK_REDUCE);
+  e = launch_ntk_reduce(s, part, splits, n1, n2, Or, sym ? 1 : 0, nullptr, nullptr, 1.f, accumulate, theta);
+  prof_end(P, s, KC_NTK_REDUCE);
+  return e;
+}
+
+// The Jacobian-contraction buffers: two chunks of explicit Jacobian rows (one per batch) of at
+// least one output unit of the widest layer each, and split-K partials of the full product.
+static int ensure_jc_workspace(ntk_handle* h) {
+  if (h->jc_ws) return NTK_OK;
+  const long long O = h->out_dim;
+  const long long R = (long long)std::max(h->max_n1, h->max_n2) * O;
+  long long widest = 1;
+  if (h->cnn)
+    widest = h->ch[h->nc] + 1;
+  else
+    for (int l = 0; l <= h->L; ++l) widest = std::max<long long>(widest, h->dims[l] + 1);
+  h->jc_side_floats = (size_t)std::max<long long>(64LL << 20, R * widest);
+  const int T = splitk_tile();
+  const long long tiles = (long long)((h->max_n1 * O + T - 1) / T) * ((h->max_n2 * O + T - 1) / T);
+  h->jc_part_capacity = (1024 + tiles) * T * T;
+  const size_t bytes = (2 * align_up(h->jc_side_floats * 4)) + align_up((size_t)h->jc_part_capacity * 4);
+  hipError_t e = hipMalloc((void**)&h->jc_ws, bytes);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    h->jc_ws = nullptr;
+    return fail(h, NTK_E_OOM, "Jacobian-contraction buffers of " + std::to_string(bytes) + " bytes");
+  }
+  return NTK_OK;
+}
+
+// theta (+)= sum over the column chunks of one dense layer's explicit Jacobian block of the
+// variant of J1 J2^T.  G1/G2: cotangent rows of the layer output (null for the readout);
+// h1/h2: layer inputs [n, d]; `first` says whether theta is still to be written.
+static int jc_dense_layer(ntk_handle* h, const float* G1, const float* G2, long long ldG, const float* h1,
+                          const float* h2, int d, int units, bool bias, int n1, int n2, int Oe, int only_o,
+                          bool trace, bool diag, bool sym, bool& first, float* theta) {
+  hipStream_t s = h->stream;
+  Profiler* P = &h->prof;
+  float* J1 = reinterpret_cast<float*>(h->jc_ws);
+  float* J2 = reinterpret_cast<float*>(h->jc_ws + align_up(h->jc_side_floats * 4));
+  float* part = reinterpret_cast<float*>(h->jc_ws + 2 * align_up(h->jc_side_floats * 4));
+  const long long R = (long long)std::max(n1, n2) * Oe;
+  const int cc = (int)std::max<long long>(1, std::min<long long>(units, (long long)h->jc_side_floats / (R * (d + 1))));
+  for (int c0 = 0; c0 < units; c0 += cc) {
+    const int c = std::min(cc, units - c0);
+    const long long K = (long long)c * d + (bias ? c : 0);
+    prof_begin(P, s, KC_JC_JACOBIAN);
+    hipError_t e = launch_jc_dense(s, G1, ldG, h1, d, n1 * Oe, Oe, only_o, c0, c, bias ? 1 : 0, J1);
+    if (e == hipSuccess && !sym)
+      e = launch_jc_dense(s, G2, ldG, h2, d, n2 * Oe, Oe, only_o, c0, c, bias ? 1 : 0, J2);
+    prof_end(P, s, KC_JC_JACOBIAN);
+    if (e != hipSuccess) return hip_fail(h, e, "explicit Jacobian block");
+    e = contract_rows(h, J1, sym ? J1 : J2, n1, n2, Oe, trace, diag, sym, K, first ? 0 : 1, theta, part,
+                      h->jc_part_capacity);
+    if (e != hipSuccess) return hip_fail(h, e, "Jacobian contraction");
+    first = false;
+  }
+  return NTK_OK;
+}
+
 static int compute_fcn(ntk_handle* h, const float* const* params, const float* X1, int n1,
                        const float* X2, int n2, float* theta) {
   const int L = h->L;
@@ -399,6 +500,22 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   };
   auto H2 = [&](int l) -> const float* { return sym ? hptr(l) : hptr(l) + (size_t)n1 * h->dims[l]; };
   const float rscale = trace ? (float)O : 1.f;   // sum over o of delta_{oo} for the trace
+  if (h->opt_method == NTK_METHOD_JACOBIAN) {
+    // Jacobian-contraction baseline: every weight tensor's explicit Jacobian block, chunk by
+    // chunk, contracted into theta (the readout's cotangent is the identity)
+    int rc = ensure_jc_workspace(h);
+    if (rc != NTK_OK) return rc;
+    bool first = true;
+    const int only_o = logit ? h->opt_logit : -1;
+    for (int l = 0; l <= L; ++l) {
+      const bool readout = l == L;
+      rc = jc_dense_layer(h, readout ? nullptr : G1(l), readout ? nullptr : G2(l), h->dims[l + 1], hptr(l),
+                          H2(l), h->dims[l], h->dims[l + 1], h->layers[l].has_bias != 0, n1, n2, Oe, only_o,
+                          trace, diag, sym, first, theta);
+      if (rc != NTK_OK) return rc;
+    }
+    return NTK_OK;
+  }
   if (diag) {
     // 3'. batch diagonal: per-sample layer-input scalars d_l[n] = h1_l[n] . h2_l[n] (+1), then
     //     theta[n] = sum_l d_l[n] G1_l[n] G2_l[n]^T + d_L[n] I (traced: a dot of O*K_l columns)
@@ -427,7 +544,7 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     t.readout = F(h->off_gram[L]);
     t.readout_scale = rscale;
     prof_begin(P, s, KC_NTK_DIAG);
-    e = launch_ntk_diag(s, t, n1, flat ? 0 : O, 0, theta);
+    e = launch_ntk_diag(s, t, n1, flat ? 0 : O, 0, theta, F(h->off_vpart), h->vpart_capacity);
     prof_end(P, s, KC_NTK_DIAG);
     if (e != hipSuccess) return hip_fail(h, e, "diagonal contraction");
     return NTK_OK;
@@ -517,7 +634,8 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
     const double Cin = h->ch[l], Co = h->ch[l + 1];
     const double oi = pairs * Oc * 9 * Cin * Co + (double)M * Oe * D * 9 * Cin * Co;
     const double io = pairs * ((double)D * D * 9 * Cin + (double)Oe * D * D * Co + Oc * D * Co);
-    if (h->opt_conv_order == NTK_CONV_ORDER_INSIDE_OUT) inside[l] = 1;
+    if (h->opt_method == NTK_METHOD_JACOBIAN) inside[l] = 0;   // explicit J_l: outside-in
+    else if (h->opt_conv_order == NTK_CONV_ORDER_INSIDE_OUT) inside[l] = 1;
     else if (h->opt_conv_order == NTK_CONV_ORDER_AUTO) inside[l] = (io_ok && io < oi) ? 1 : 0;
   }
   long long Kcall = 0;
@@ -632,6 +750,19 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   // 3. Theta += J1 J2^T over the outside-in layers (deterministic split over K).  The J rows
   //    of one sample are contiguous, so the traced variant contracts rows (n) of Oe*Kcall
   //    columns; the batch diagonal contracts each sample's rows with its own.
+  if (h->opt_method == NTK_METHOD_JACOBIAN) {
+    // Jacobian-contraction baseline: the conv layers' explicit J (all of them, outside-in),
+    // then the readout layer's explicit block delta_{o o'} g[n, j]
+    int rc = ensure_jc_workspace(h);
+    if (rc != NTK_OK) return rc;
+    const float* J2 = sym ? J : J + (size_t)n1 * Oe * Kcall;
+    e = contract_rows(h, J, J2, n1, n2, Oe, trace, diag, sym, Kcall, 0, theta, F(h->off_part),
+                      h->part_capacity);
+    if (e != hipSuccess) return hip_fail(h, e, "Jacobian contraction");
+    bool first = false;
+    return jc_dense_layer(h, nullptr, nullptr, 0, F(h->off_g), g2p, C, O, false, n1, n2, Oe,
+                          logit ? h->opt_logit : -1, trace, diag, sym, first, theta);
+  }
   if (Kcall > 0) {
     const float* J2 = sym ? J : J + (size_t)n1 * Oe * Kcall;
     const float rscale = trace ? (float)O : 1.f;
@@ -646,7 +777,8 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
       t.readout = F(h->off_gram_r);
       t.readout_scale = rscale;
       prof_begin(P, s, KC_NTK_DIAG);
-      e = launch_ntk_diag(s, t, n1, flat ? 0 : O, theta_written ? 1 : 0, theta);
+      e = launch_ntk_diag(s, t, n1, flat ? 0 : O, theta_written ? 1 : 0, theta, F(h->off_part),
+                          h->part_capacity);
       prof_end(P, s, KC_NTK_DIAG);
       if (e != hipSuccess) return hip_fail(h, e, "diagonal contraction");
       return NTK_OK;
@@ -689,6 +821,7 @@ extern "C" int ntk_free(ntk_handle* h) {
   if (!h) return NTK_OK;
   (void)hipStreamSynchronize(h->stream);
   if (h->ws) (void)hipFree(h->ws);
+  if (h->jc_ws) (void)hipFree(h->jc_ws);
   delete h;
   return NTK_OK;
 }
@@ -719,6 +852,12 @@ extern "C" int ntk_set_option(ntk_handle* h, int option, int value) {
   if (option == NTK_OPT_LOGIT) {
     if (value < 0 || value >= h->out_dim) return fail(h, NTK_E_ARG, "NTK_OPT_LOGIT must be in [0, O)");
     h->opt_logit = value;
+    return NTK_OK;
+  }
+  if (option == NTK_OPT_METHOD) {
+    if (value != NTK_METHOD_STRUCTURED && value != NTK_METHOD_JACOBIAN)
+      return fail(h, NTK_E_ARG, "NTK_OPT_METHOD takes NTK_METHOD_STRUCTURED or NTK_METHOD_JACOBIAN");
+    h->opt_method = value;
     return NTK_OK;
   }
   if (option == NTK_OPT_BATCH) {

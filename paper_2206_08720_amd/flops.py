@@ -15,55 +15,97 @@ CNN (conv3x3 layers l with Cin_l -> Cout_l on D pixels, GAP, dense readout):
   backward     sum_{l>=1} 2 (M O D) 9 Cout_l Cin_l
   wgrad        sum_l 2 M (O Cout_l) (9 Cin_l) D           (outside-in weight-space Jacobian)
   contraction  2 (N1 O)(N2 O) sum_l Cout_l 9 Cin_l + readout gram 2 N1 N2 C
+
+Variants (output = "trace" | "logit", batch = "diagonal"): the backward pass and the
+weight-space cotangents run for Oe = 1 output with "logit" (O otherwise); the contraction
+covers `pairs` input pairs (N1 N2, or N on the batch diagonal) and Oc output pairs per input
+pair (O^2 full, O for the trace, 1 for one logit).
+
+Jacobian contraction (method = "jacobian", the baseline of Section 3.2): the same forward
+and backward passes (and, for the CNN, the weight-space Jacobians of every conv layer), then
+the explicit contraction, 2 pairs Oc P for P parameters in total.
 """
 from __future__ import annotations
 
 
-def fcn_flops(spec, n1, n2, symmetric=False):
+def _variant(O, n1, n2, output, batch):
+    Oe = 1 if output == "logit" else O
+    Oc = {"full": O * O, "trace": O, "logit": 1}[output]
+    pairs = n1 if batch == "diagonal" else n1 * n2
+    return Oe, Oc, pairs
+
+
+def fcn_flops(spec, n1, n2, symmetric=False, output="full", batch="full"):
     layers = spec["layers"]
     L = len(layers) - 1
     d = [layers[0]["in"]] + [Lr["out"] for Lr in layers]
     O = d[-1]
+    Oe, Oc, pairs = _variant(O, n1, n2, output, batch)
     M = n1 if symmetric else n1 + n2
     st = {
         "forward": sum(2.0 * M * d[l] * d[l + 1] for l in range(L)),
-        "backward": sum(2.0 * M * O * d[l + 1] * d[l] for l in range(1, L)),
-        "gram": sum(2.0 * n1 * n2 * d[l] for l in range(L + 1)),
-        "contraction": sum(2.0 * (n1 * O) * (n2 * O) * d[l + 1] for l in range(L)),
+        "backward": sum(2.0 * M * Oe * d[l + 1] * d[l] for l in range(1, L)),
+        "gram": sum(2.0 * pairs * d[l] for l in range(L + 1)),
+        "contraction": sum(2.0 * pairs * Oc * d[l + 1] for l in range(L)),
     }
     st["total"] = sum(st.values())
     return st
 
 
-def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in"):
+def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", batch="full"):
     layers = spec["layers"]
     H, W, _ = spec["input_shape"]
     D = H * W
     convs = [Lr for Lr in layers if Lr["kind"] == "conv3x3"]
     O = layers[-1]["out"]
     C = convs[-1]["out"]
+    Oe, Oc, pairs = _variant(O, n1, n2, output, batch)
     M = n1 if symmetric else n1 + n2
     st = {
         "forward": sum(2.0 * M * D * 9 * c["in"] * c["out"] for c in convs),
-        "backward": sum(2.0 * M * O * D * 9 * c["out"] * c["in"] for c in convs[1:]),
-        "gram": 2.0 * n1 * n2 * C,
+        "backward": sum(2.0 * M * Oe * D * 9 * c["out"] * c["in"] for c in convs[1:]),
+        "gram": 2.0 * pairs * C,
     }
     if order == "outside_in":
-        st["wgrad"] = sum(2.0 * M * (O * c["out"]) * (9 * c["in"]) * D for c in convs)
-        st["contraction"] = 2.0 * (n1 * O) * (n2 * O) * sum(c["out"] * 9 * c["in"] for c in convs)
+        st["wgrad"] = sum(2.0 * M * (Oe * c["out"]) * (9 * c["in"]) * D for c in convs)
+        st["contraction"] = 2.0 * pairs * Oc * sum(c["out"] * 9 * c["in"] for c in convs)
     else:  # inside-out: patch Gram, one-sided cotangent contraction, then the O x O product
-        st["contraction"] = sum(2.0 * n1 * n2 * (D * D * 9 * c["in"] + O * D * D * c["out"]
-                                                 + O * O * D * c["out"]) for c in convs)
+        st["contraction"] = sum(2.0 * pairs * (D * D * 9 * c["in"] + Oe * D * D * c["out"]
+                                               + Oc * D * c["out"]) for c in convs)
     st["total"] = sum(st.values())
     return st
 
 
-def ntk_flops(spec, n1, n2, symmetric=False, **kw):
-    if any(Lr["kind"] == "conv3x3" for Lr in spec["layers"]):
-        return cnn_flops(spec, n1, n2, symmetric, **kw)
-    return fcn_flops(spec, n1, n2, symmetric)
+def param_total(spec):
+    P = 0
+    for Lr in spec["layers"]:
+        if Lr["kind"] == "dense":
+            P += Lr["out"] * Lr["in"] + (Lr["out"] if Lr.get("bias") else 0)
+        elif Lr["kind"] == "conv3x3":
+            P += Lr["out"] * 9 * Lr["in"]
+    return P
 
 
-def ntk_entries(spec, n1, n2):
+def ntk_flops(spec, n1, n2, symmetric=False, method="structured", **kw):
+    cnn = any(Lr["kind"] == "conv3x3" for Lr in spec["layers"])
+    if method == "jacobian":
+        kw["order"] = "outside_in"
+    if cnn:
+        st = cnn_flops(spec, n1, n2, symmetric, **kw)
+    else:
+        kw.pop("order", None)
+        st = fcn_flops(spec, n1, n2, symmetric, **kw)
+    if method == "jacobian":
+        O = spec["layers"][-1]["out"]
+        _, Oc, pairs = _variant(O, n1, n2, kw.get("output", "full"), kw.get("batch", "full"))
+        st.pop("gram", None)
+        st.pop("total")
+        st["contraction"] = 2.0 * pairs * Oc * param_total(spec)
+        st["total"] = sum(st.values())
+    return st
+
+
+def ntk_entries(spec, n1, n2, output="full", batch="full"):
     O = spec["layers"][-1]["out"]
-    return n1 * n2 * O * O
+    pairs = n1 if batch == "diagonal" else n1 * n2
+    return pairs * (O * O if output == "full" else 1)

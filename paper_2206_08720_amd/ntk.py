@@ -54,6 +54,12 @@ class NTK:
         self.set_option(_lib.NTK_OPT_BATCH, {"full": _lib.NTK_BATCH_FULL,
                                              "diagonal": _lib.NTK_BATCH_DIAGONAL}[batch])
 
+    def set_method(self, method="structured"):
+        """"structured" (Section 3.4, the default) or "jacobian" (the Jacobian-contraction
+        baseline of Section 3.2, explicit Jacobians contracted on the GPU)."""
+        self.set_option(_lib.NTK_OPT_METHOD, {"structured": _lib.NTK_METHOD_STRUCTURED,
+                                              "jacobian": _lib.NTK_METHOD_JACOBIAN}[method])
+
     def out_shape(self, n1, n2):
         """Shape of theta for batches of n1 and n2 under the current variant options."""
         O = self.out_dim
@@ -125,12 +131,13 @@ class NTK:
             pass
 
 
-def compute(spec, params, X1, X2=None, output="full", batch="full", logit=0):
+def compute(spec, params, X1, X2=None, output="full", batch="full", logit=0, method="structured"):
     """One-shot Theta(X1, X2) (allocates a handle sized for these batches)."""
     X2 = X1 if X2 is None else X2
     h = NTK(spec, X1.shape[0], X2.shape[0])
     try:
         h.set_variant(output, batch, logit)
+        h.set_method(method)
         out = h.compute(params, X1, X2)
         torch.cuda.current_stream().synchronize()
         return out

@@ -47,3 +47,32 @@ def test_cnn_terms_match_complexities_cnn():
     assert oi["wgrad"] == 2 * (2 * N) * O * W * Fs * W * D * 2
     # inside-out: N^2 (D^2 F W + O D^2 W + O^2 D W) per layer
     assert io["contraction"] == 2 * 2 * N * N * (D * D * Fs * W + O * D * D * W + O * O * D * W)
+
+
+def test_variant_counts():
+    N, O, L, W = 16, 7, 5, 96
+    spec = wl.fcn_spec("f", W, [W] * L, O)
+    full = fcn_flops(spec, N, N)
+    tr = fcn_flops(spec, N, N, output="trace")
+    lg = fcn_flops(spec, N, N, output="logit")
+    dg = fcn_flops(spec, N, N, batch="diagonal")
+    assert tr["contraction"] == full["contraction"] / O and tr["backward"] == full["backward"]
+    assert lg["contraction"] == full["contraction"] / O ** 2 and lg["backward"] == full["backward"] / O
+    assert dg["contraction"] == full["contraction"] / N and dg["gram"] == full["gram"] / N
+    assert ntk_entries(spec, N, N, "trace") == N * N and ntk_entries(spec, N, N, "full", "diagonal") == N * O * O
+    cs = wl.cnn_spec("c", (4, 4), 3, [8, 8], O)
+    cf, cl = cnn_flops(cs, N, N), cnn_flops(cs, N, N, output="logit")
+    assert cl["wgrad"] == cf["wgrad"] / O and cl["contraction"] == cf["contraction"] / O ** 2
+
+
+def test_jacobian_contraction_count_is_the_papers_n2_o2_p():
+    import oracle
+    from paper_2206_08720_amd.flops import ntk_flops, param_total
+    for name in ("relu_mlp_d8_w2048", "cnn4_c64_32x32", "tiny_relu_mlp"):
+        spec, params, X1, X2 = wl.make_workload(name)
+        assert param_total(spec) == oracle.param_count(spec)
+        n1, n2, O = X1.shape[0], X2.shape[0], spec["layers"][-1]["out"]
+        jc = ntk_flops(spec, n1, n2, method="jacobian")
+        assert jc["contraction"] == 2 * n1 * n2 * O * O * oracle.param_count(spec)
+    spec, _, _, _ = wl.make_workload("relu_mlp_d8_w2048")
+    assert ntk_flops(spec, 512, 512, method="jacobian")["contraction"] == pytest.approx(1.87e15, rel=1e-2)
