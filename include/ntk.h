@@ -165,6 +165,21 @@ int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, void* hip_stre
 int ntk_compute(ntk_handle* h, const float* const* params, const float* X1, int n1,
                 const float* X2, int n2, float* theta);
 
+/*
+ * ntk_vector_product -- enqueue out = Theta(X1, X2) v without forming Theta (the NTK-vector
+ * product of Section 3.3, Eq. ntk_vp_main): the VJP of batch 2 at v gives the weight-space
+ * vector theta_c = J(X2)^T v, and the JVP of batch 1 along theta_c gives J(X1) theta_c.
+ *   params, X1, n1, X2, n2  as for ntk_compute.
+ *   v    device [n2, O] fp32: v[n2*O + o2].
+ *   out  device [n1, O] fp32: out[n1*O + o1] = sum_{n2, o2} Theta(x1_{n1}, x2_{n2})[o1, o2] v[n2, o2].
+ * Time about 3 forward passes of the batches (no N1 N2 O^2 term).  The output and batch
+ * variants and NTK_OPT_METHOD do not apply.  The first call on a handle allocates the
+ * weight-space vector (one float per parameter) and the tangent buffers.  Stream-ordered,
+ * asynchronous, deterministic; NTK_E_ARG for null pointers or sizes out of range.
+ */
+int ntk_vector_product(ntk_handle* h, const float* const* params, const float* X1, int n1,
+                       const float* X2, int n2, const float* v, float* out);
+
 /* ntk_free -- release the workspace and the handle.  NULL is a no-op.  Synchronises
  * the handle's stream first. */
 int ntk_free(ntk_handle* h);

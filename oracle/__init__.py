@@ -17,6 +17,8 @@ Contents
 * `ntk_jc_variant` -- the output-trace, single-logit and batch-diagonal parts of
   Theta, contracted directly from the Jacobian rows they need (appendix
   "Pseudo-NTK").
+* `ntk_vp` -- the NTK-vector product Theta(X1, X2) v = J(x1) (J(x2)^T v)
+  (Section 3.3), from the explicit Jacobian blocks.
 * `ntk_structured_fp64` -- a secondary fp64 reference for fully-connected nets
   that evaluates the per-layer formula of Section 4.1 (input Gram times
   cotangent Gram, summed over layers).  It is not the definition: the tests pin
@@ -31,6 +33,7 @@ positive semi-definiteness and homogeneity.
 from .ntk_jc import forward, jacobian, ntk_jc, ntk_jc_with_norms, param_count
 from .structured_fp64 import ntk_structured_diag_fp64, ntk_structured_fp64
 from .variants import ntk_jc_variant
+from .vector_product import ntk_vp
 
 __all__ = ["forward", "jacobian", "ntk_jc", "ntk_jc_with_norms", "param_count",
-           "ntk_structured_fp64", "ntk_structured_diag_fp64", "ntk_jc_variant"]
+           "ntk_structured_fp64", "ntk_structured_diag_fp64", "ntk_jc_variant", "ntk_vp"]

@@ -33,7 +33,8 @@ NTK_OPT_METHOD, NTK_METHOD_STRUCTURED, NTK_METHOD_JACOBIAN = 6, 0, 1
 
 EXPORTED_SYMBOLS = ("ntk_init", "ntk_compute", "ntk_free", "ntk_last_error", "ntk_set_option",
                     "ntk_set_stream", "ntk_workspace_bytes", "ntk_profile_enable",
-                    "ntk_profile_read", "ntk_device_info", "ntk_mfma_peak")
+                    "ntk_profile_read", "ntk_device_info", "ntk_mfma_peak",
+                    "ntk_vector_product")
 
 
 class ntk_layer_desc(ctypes.Structure):
@@ -87,6 +88,8 @@ def load():
                                      ctypes.POINTER(ctypes.c_double),
                                      ctypes.POINTER(ctypes.c_longlong), ctypes.c_int]
     lib.ntk_profile_read.restype = ctypes.c_int
+    lib.ntk_vector_product.argtypes = [P, ctypes.POINTER(P), P, ctypes.c_int, P, ctypes.c_int, P, P]
+    lib.ntk_vector_product.restype = ctypes.c_int
     lib.ntk_device_info.argtypes = [ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int)]
     lib.ntk_device_info.restype = ctypes.c_int
     lib.ntk_mfma_peak.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double)]

@@ -31,6 +31,7 @@ enum KernelClass {
   KC_COPY,
   KC_NTK_DIAG,
   KC_JC_JACOBIAN,
+  KC_VP_ELEMENTWISE,
   KC_COUNT
 };
 const char* kernel_class_name(int cls);
@@ -112,5 +113,15 @@ hipError_t launch_ntk_diag(hipStream_t s, const DiagTerms& t, int N, int O, int 
 // rows are the one output only_o).
 hipError_t launch_jc_dense(hipStream_t s, const float* G, long long ldG, const float* h, int d, int R,
                            int Oe, int only_o, int c0, int cc, int bias, float* out);
+
+// ---- NTK-vector products ----------------------------------------------------------------
+// out[r, c] = (a[r, c] + b[r, c] + bias[c]) * dphi[r, c]; a, bias, dphi may be null.
+hipError_t launch_jvp_combine(hipStream_t s, const float* a, const float* b, const float* bias,
+                              const float* dphi, int R, int C, float* out);
+// out[c] = sum_r x[r, c] for x [R, C].
+hipError_t launch_colsum(hipStream_t s, const float* x, int R, int C, float* out);
+// out [n, D, C] = u[n, c] / D * dphi[n, p, c]  (adjoint of global average pooling, times act').
+hipError_t launch_gap_adjoint(hipStream_t s, const float* u, const float* dphi, int n, int D, int C,
+                              float* out);
 
 }  // namespace ntk

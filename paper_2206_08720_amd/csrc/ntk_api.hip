@@ -24,7 +24,7 @@ const char* kernel_class_name(int cls) {
   static const char* names[KC_COUNT] = {
       "dense_fwd", "dense_bwd", "bwd_seed",  "gram",       "ntk_fcn",    "transpose",    "conv_fwd",
       "conv_bwd",  "conv_seed", "gap",       "conv_wgrad", "ntk_splitk", "ntk_reduce", "conv_pairsum",
-      "copy",      "ntk_diag",  "jc_jacobian"};
+      "copy",      "ntk_diag",  "jc_jacobian", "vp_elementwise"};
   return (cls >= 0 && cls < KC_COUNT) ? names[cls] : "?";
 }
 
@@ -100,6 +100,13 @@ struct ntk_handle {
   char* jc_ws = nullptr;
   size_t jc_side_floats = 0;
   long long jc_part_capacity = 0;
+  // NTK-vector products: the weight-space cotangent and the tangents, allocated by the first
+  // ntk_vector_product call
+  char* vp_ws = nullptr;
+  std::vector<size_t> vp_off_tc, vp_off_tcb;    // theta_c of each weight tensor and bias
+  size_t vp_off_dT = 0, vp_off_hT = 0, vp_off_t0 = 0, vp_off_t1 = 0, vp_off_ga = 0, vp_off_gb = 0,
+         vp_off_WLt = 0;
+  size_t vp_off_u = 0, vp_off_ca = 0, vp_off_cb = 0, vp_off_cd = 0, vp_off_gdot = 0;   // CNN
   std::string err;
   Profiler prof;
 
@@ -430,11 +437,11 @@ static int jc_dense_layer(ntk_handle* h, const float* G1, const float* G2, long 
   return NTK_OK;
 }
 
-static int compute_fcn(ntk_handle* h, const float* const* params, const float* X1, int n1,
-                       const float* X2, int n2, float* theta) {
+// Forward pass of the stacked batch [X1; X2] (or X1 alone when sym) keeping every layer input
+// h_l and act'(z_l); *h0 receives the layer-0 input (X1 itself when sym).
+static int fcn_forward(ntk_handle* h, const float* const* params, const float* X1, int n1,
+                       const float* X2, int n2, bool sym, const float** h0) {
   const int L = h->L;
-  const int O = h->out_dim;
-  const bool sym = h->opt_symmetric && X1 == X2 && n1 == n2;
   const int M = sym ? n1 : n1 + n2;
   hipStream_t s = h->stream;
   Profiler* P = &h->prof;
@@ -445,7 +452,7 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   }
   hipError_t e;
   const int d0 = h->dims[0];
-  const float* h0 = X1;
+  *h0 = X1;
   if (!sym) {
     prof_begin(P, s, KC_COPY);
     e = hipMemcpyAsync(F(h->off_h[0]), X1, sizeof(float) * (size_t)n1 * d0, hipMemcpyDeviceToDevice, s);
@@ -454,20 +461,36 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
                          hipMemcpyDeviceToDevice, s);
     prof_end(P, s, KC_COPY);
     if (e != hipSuccess) return hip_fail(h, e, "stacking X1/X2");
-    h0 = F(h->off_h[0]);
+    *h0 = F(h->off_h[0]);
   }
-  auto hptr = [&](int l) -> const float* { return l == 0 ? h0 : F(h->off_h[l]); };
-
-  // 1. forward pass (the readout's own output f is not needed for Theta)
+  // the readout's own output f is not needed
   for (int l = 0; l < L; ++l) {
     const float* W = params[h->param_index[l]];
     const float* b = h->layers[l].has_bias ? params[h->param_index[l] + 1] : nullptr;
     prof_begin(P, s, KC_DENSE_FWD);
-    e = launch_dense_fwd(s, hptr(l), W, b, M, h->dims[l + 1], h->dims[l], h->layers[l].act,
-                         F(h->off_h[l + 1]), F(h->off_dphi[l]));
+    e = launch_dense_fwd(s, l == 0 ? *h0 : F(h->off_h[l]), W, b, M, h->dims[l + 1], h->dims[l],
+                         h->layers[l].act, F(h->off_h[l + 1]), F(h->off_dphi[l]));
     prof_end(P, s, KC_DENSE_FWD);
     if (e != hipSuccess) return hip_fail(h, e, "dense forward");
   }
+  return NTK_OK;
+}
+
+static int compute_fcn(ntk_handle* h, const float* const* params, const float* X1, int n1,
+                       const float* X2, int n2, float* theta) {
+  const int L = h->L;
+  const int O = h->out_dim;
+  const bool sym = h->opt_symmetric && X1 == X2 && n1 == n2;
+  const int M = sym ? n1 : n1 + n2;
+  hipStream_t s = h->stream;
+  Profiler* P = &h->prof;
+  auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
+  hipError_t e;
+  // 1. forward pass keeping the layer inputs
+  const float* h0 = nullptr;
+  int rc0 = fcn_forward(h, params, X1, n1, X2, n2, sym, &h0);
+  if (rc0 != NTK_OK) return rc0;
+  auto hptr = [&](int l) -> const float* { return l == 0 ? h0 : F(h->off_h[l]); };
   // 2. cotangents of every hidden pre-activation for all O outputs at once (for the one
   //    logit o* alone in NTK_OUTPUT_LOGIT: the cotangent rows are then (n) instead of (n, o))
   const bool logit = h->opt_output == NTK_OUTPUT_LOGIT;
@@ -607,6 +630,44 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   return NTK_OK;
 }
 
+// CNN forward pass of the stacked batch [X1; X2] (or X1 alone when sym), keeping every conv
+// layer input and act'(z_l), then the global average pool g; *h0 receives the layer-0 input.
+static int cnn_forward(ntk_handle* h, const float* const* params, const float* X1, int n1,
+                       const float* X2, int n2, bool sym, const float** h0) {
+  const int nc = h->nc, H = h->H, W = h->W, D = h->D;
+  const int M = sym ? n1 : n1 + n2;
+  hipStream_t s = h->stream;
+  Profiler* P = &h->prof;
+  auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
+  for (int l = 0; l <= nc; ++l)
+    if (!params[l]) return fail(h, NTK_E_ARG, "null weight pointer");
+  hipError_t e;
+  const size_t img_floats = (size_t)D * h->ch[0];
+  *h0 = X1;
+  if (!sym) {
+    prof_begin(P, s, KC_COPY);
+    e = hipMemcpyAsync(F(h->off_ch[0]), X1, sizeof(float) * n1 * img_floats, hipMemcpyDeviceToDevice, s);
+    if (e == hipSuccess)
+      e = hipMemcpyAsync(F(h->off_ch[0]) + n1 * img_floats, X2, sizeof(float) * n2 * img_floats,
+                         hipMemcpyDeviceToDevice, s);
+    prof_end(P, s, KC_COPY);
+    if (e != hipSuccess) return hip_fail(h, e, "stacking X1/X2");
+    *h0 = F(h->off_ch[0]);
+  }
+  for (int l = 0; l < nc; ++l) {
+    prof_begin(P, s, KC_CONV_FWD);
+    e = launch_conv_fwd(s, l == 0 ? *h0 : F(h->off_ch[l]), M, H, W, h->ch[l], params[l], h->ch[l + 1],
+                        h->layers[l].act, F(h->off_ch[l + 1]), F(h->off_cdphi[l]));
+    prof_end(P, s, KC_CONV_FWD);
+    if (e != hipSuccess) return hip_fail(h, e, "conv forward");
+  }
+  prof_begin(P, s, KC_GAP);
+  e = launch_gap(s, F(h->off_ch[nc]), M, D, h->ch[nc], F(h->off_g));
+  prof_end(P, s, KC_GAP);
+  if (e != hipSuccess) return hip_fail(h, e, "global average pooling");
+  return NTK_OK;
+}
+
 static int compute_cnn(ntk_handle* h, const float* const* params, const float* X1, int n1,
                        const float* X2, int n2, float* theta) {
   const int nc = h->nc, O = h->out_dim, H = h->H, W = h->W, D = h->D;
@@ -648,32 +709,12 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   if (Kcall < h->Ktot && !io_ok)
     return fail(h, NTK_E_UNSUPPORTED, "the inside-out order needs D <= 64 pixels and O <= 64");
   hipError_t e;
-  const size_t img_floats = (size_t)D * h->ch[0];
-  const float* h0 = X1;
-  if (!sym) {
-    prof_begin(P, s, KC_COPY);
-    e = hipMemcpyAsync(F(h->off_ch[0]), X1, sizeof(float) * n1 * img_floats, hipMemcpyDeviceToDevice, s);
-    if (e == hipSuccess)
-      e = hipMemcpyAsync(F(h->off_ch[0]) + n1 * img_floats, X2, sizeof(float) * n2 * img_floats,
-                         hipMemcpyDeviceToDevice, s);
-    prof_end(P, s, KC_COPY);
-    if (e != hipSuccess) return hip_fail(h, e, "stacking X1/X2");
-    h0 = F(h->off_ch[0]);
-  }
-  auto hptr = [&](int l) -> const float* { return l == 0 ? h0 : F(h->off_ch[l]); };
   // 1. forward pass keeping every conv layer input, then global average pooling
-  for (int l = 0; l < nc; ++l) {
-    prof_begin(P, s, KC_CONV_FWD);
-    e = launch_conv_fwd(s, hptr(l), M, H, W, h->ch[l], params[l], h->ch[l + 1], h->layers[l].act,
-                        F(h->off_ch[l + 1]), F(h->off_cdphi[l]));
-    prof_end(P, s, KC_CONV_FWD);
-    if (e != hipSuccess) return hip_fail(h, e, "conv forward");
-  }
+  const float* h0 = nullptr;
+  int rc0 = cnn_forward(h, params, X1, n1, X2, n2, sym, &h0);
+  if (rc0 != NTK_OK) return rc0;
+  auto hptr = [&](int l) -> const float* { return l == 0 ? h0 : F(h->off_ch[l]); };
   const int C = h->ch[nc];
-  prof_begin(P, s, KC_GAP);
-  e = launch_gap(s, F(h->off_ch[nc]), M, D, C, F(h->off_g));
-  prof_end(P, s, KC_GAP);
-  if (e != hipSuccess) return hip_fail(h, e, "global average pooling");
   // readout summand: (g1 . g2) delta_{o1 o2} ([n1, n2], or [n] on the batch diagonal)
   const float* g2p = sym ? F(h->off_g) : F(h->off_g) + (size_t)n1 * C;
   if (diag) {
@@ -801,6 +842,311 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   return NTK_OK;
 }
 
+
+// ------------------------------------------------------------------------------ NTK-vector products
+static int ensure_vp_workspace_fcn(ntk_handle* h) {
+  if (h->vp_ws) return NTK_OK;
+  const int L = h->L;
+  size_t off = 0;
+  auto take = [&](size_t floats) {
+    size_t o = off;
+    off = align_up(off + floats * 4);
+    return o;
+  };
+  int dmax = 1;
+  for (int d : h->dims) dmax = std::max(dmax, d);
+  h->vp_off_tc.assign(L + 1, 0);
+  h->vp_off_tcb.assign(L + 1, 0);
+  for (int l = 0; l <= L; ++l) {
+    h->vp_off_tc[l] = take((size_t)h->dims[l + 1] * h->dims[l]);
+    h->vp_off_tcb[l] = take((size_t)h->dims[l + 1]);
+  }
+  h->vp_off_dT = take((size_t)dmax * h->max_n2);
+  h->vp_off_hT = take((size_t)dmax * h->max_n2);
+  h->vp_off_t0 = take((size_t)dmax * h->max_n1);
+  h->vp_off_t1 = take((size_t)dmax * h->max_n1);
+  h->vp_off_ga = take((size_t)dmax * h->max_n1);
+  h->vp_off_gb = take((size_t)dmax * h->max_n1);
+  h->vp_off_WLt = take((size_t)h->dims[L] * h->out_dim);
+  hipError_t e = hipMalloc((void**)&h->vp_ws, off);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    h->vp_ws = nullptr;
+    return fail(h, NTK_E_OOM, "NTK-vector product buffers of " + std::to_string(off) + " bytes");
+  }
+  return NTK_OK;
+}
+
+// out [n1, O] = Theta(X1, X2) v for v [n2, O]: theta_c = VJP of batch 2 at v (weight space),
+// then the JVP of batch 1 along theta_c (Section 3.3, Eq. "ntk_vp_main").
+static int vector_product_fcn(ntk_handle* h, const float* const* params, const float* X1, int n1,
+                              const float* X2, int n2, const float* v, float* out) {
+  const int L = h->L, O = h->out_dim;
+  const bool sym = h->opt_symmetric && X1 == X2 && n1 == n2;
+  hipStream_t s = h->stream;
+  Profiler* P = &h->prof;
+  int rc = ensure_vp_workspace_fcn(h);
+  if (rc != NTK_OK) return rc;
+  const float* h0 = nullptr;
+  rc = fcn_forward(h, params, X1, n1, X2, n2, sym, &h0);
+  if (rc != NTK_OK) return rc;
+  auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
+  auto V = [&](size_t off) { return reinterpret_cast<float*>(h->vp_ws + off); };
+  auto hptr = [&](int l) -> const float* { return l == 0 ? h0 : F(h->off_h[l]); };
+  const size_t r2 = sym ? 0 : (size_t)n1;   // first row of batch 2 in the stacked arrays
+  auto W = [&](int l) { return params[h->param_index[l]]; };
+  hipError_t e;
+  // ---- VJP of batch 2 at v: cotangents delta_l of every pre-activation z_l (delta_L = v)
+  for (int l = 1; l < L; ++l) {
+    prof_begin(P, s, KC_TRANSPOSE);
+    e = launch_transpose(s, W(l), h->dims[l + 1], h->dims[l], F(h->off_Wt[l]));
+    prof_end(P, s, KC_TRANSPOSE);
+    if (e != hipSuccess) return hip_fail(h, e, "weight transpose");
+  }
+  auto delta = [&](int l) -> const float* { return l == L ? v : F(h->off_G[l]); };
+  if (L >= 1) {
+    prof_begin(P, s, KC_TRANSPOSE);
+    e = launch_transpose(s, W(L), O, h->dims[L], V(h->vp_off_WLt));
+    prof_end(P, s, KC_TRANSPOSE);
+    if (e != hipSuccess) return hip_fail(h, e, "weight transpose");
+    for (int l = L; l >= 1; --l) {
+      // delta_{l-1} = (delta_l W_l) * act'(z_{l-1}) on the rows of batch 2
+      const float* Wt = l == L ? V(h->vp_off_WLt) : F(h->off_Wt[l]);
+      prof_begin(P, s, KC_DENSE_BWD);
+      e = launch_dense_bwd(s, delta(l), Wt, F(h->off_dphi[l - 1]) + r2 * h->dims[l], n2, h->dims[l],
+                           h->dims[l + 1], 1, F(h->off_G[l - 1]));
+      prof_end(P, s, KC_DENSE_BWD);
+      if (e != hipSuccess) return hip_fail(h, e, "VJP backward");
+    }
+  }
+  // weight-space cotangent: theta_c^l = delta_l^T h2_l, bias part sum_n delta_l[n]
+  for (int l = 0; l <= L; ++l) {
+    const int dout = h->dims[l + 1], din = h->dims[l];
+    prof_begin(P, s, KC_TRANSPOSE);
+    e = launch_transpose(s, delta(l), n2, dout, V(h->vp_off_dT));
+    if (e == hipSuccess) e = launch_transpose(s, hptr(l) + r2 * din, n2, din, V(h->vp_off_hT));
+    prof_end(P, s, KC_TRANSPOSE);
+    if (e != hipSuccess) return hip_fail(h, e, "VJP transposes");
+    GramBatch gb{};
+    gb.count = 1;
+    gb.h1[0] = V(h->vp_off_dT);
+    gb.h2[0] = V(h->vp_off_hT);
+    gb.out[0] = V(h->vp_off_tc[l]);
+    gb.K[0] = n2;
+    gb.beta[0] = 0.f;
+    prof_begin(P, s, KC_GRAM);
+    e = launch_gram(s, gb, dout, din);
+    prof_end(P, s, KC_GRAM);
+    if (e != hipSuccess) return hip_fail(h, e, "weight-space cotangent");
+    if (h->layers[l].has_bias) {
+      prof_begin(P, s, KC_VP_ELEMENTWISE);
+      e = launch_colsum(s, delta(l), n2, dout, V(h->vp_off_tcb[l]));
+      prof_end(P, s, KC_VP_ELEMENTWISE);
+      if (e != hipSuccess) return hip_fail(h, e, "bias cotangent");
+    }
+  }
+  // ---- JVP of batch 1 along theta_c: tangent t_l of the layer inputs (t_0 = 0),
+  //      z'_l = t_l W_l^T + h1_l theta_c^l^T + b'_l,  t_{l+1} = act'(z_l) * z'_l,  out = z'_L
+  float* tcur = V(h->vp_off_t0);
+  float* tnext = V(h->vp_off_t1);
+  for (int l = 0; l <= L; ++l) {
+    const int dout = h->dims[l + 1], din = h->dims[l];
+    GramBatch gb{};
+    gb.count = l > 0 ? 2 : 1;
+    gb.h1[0] = hptr(l);
+    gb.h2[0] = V(h->vp_off_tc[l]);
+    gb.out[0] = V(h->vp_off_ga);
+    gb.K[0] = din;
+    gb.beta[0] = 0.f;
+    if (l > 0) {
+      gb.h1[1] = tcur;
+      gb.h2[1] = W(l);
+      gb.out[1] = V(h->vp_off_gb);
+      gb.K[1] = din;
+      gb.beta[1] = 0.f;
+    }
+    prof_begin(P, s, KC_GRAM);
+    e = launch_gram(s, gb, n1, dout);
+    prof_end(P, s, KC_GRAM);
+    if (e != hipSuccess) return hip_fail(h, e, "JVP products");
+    const float* bias_t = h->layers[l].has_bias ? V(h->vp_off_tcb[l]) : nullptr;
+    const bool last = l == L;
+    prof_begin(P, s, KC_VP_ELEMENTWISE);
+    e = launch_jvp_combine(s, l > 0 ? V(h->vp_off_gb) : nullptr, V(h->vp_off_ga), bias_t,
+                           last ? nullptr : F(h->off_dphi[l]), n1, dout, last ? out : tnext);
+    prof_end(P, s, KC_VP_ELEMENTWISE);
+    if (e != hipSuccess) return hip_fail(h, e, "JVP step");
+    std::swap(tcur, tnext);
+  }
+  return NTK_OK;
+}
+
+
+static int ensure_vp_workspace_cnn(ntk_handle* h) {
+  if (h->vp_ws) return NTK_OK;
+  const int nc = h->nc, O = h->out_dim, D = h->D, C = h->ch[nc];
+  int cmax = 1;
+  for (int c : h->ch) cmax = std::max(cmax, c);
+  size_t off = 0;
+  auto take = [&](size_t floats) {
+    size_t o = off;
+    off = align_up(off + floats * 4);
+    return o;
+  };
+  h->vp_off_tc.assign(1, take((size_t)h->Ktot + (size_t)O * C));   // conv layers, then the readout
+  h->vp_off_dT = take((size_t)O * h->max_n2);
+  h->vp_off_hT = take((size_t)C * h->max_n2);
+  h->vp_off_WLt = take((size_t)C * O);
+  h->vp_off_u = take((size_t)h->max_n2 * C);
+  const size_t img = (size_t)h->max_n1 * D * cmax;
+  h->vp_off_t0 = take(img);
+  h->vp_off_t1 = take(img);
+  h->vp_off_ca = take(img);
+  h->vp_off_cb = take(img);
+  h->vp_off_cd = take(img);
+  h->vp_off_gdot = take((size_t)h->max_n1 * C);
+  h->vp_off_ga = take((size_t)h->max_n1 * O);
+  h->vp_off_gb = take((size_t)h->max_n1 * O);
+  hipError_t e = hipMalloc((void**)&h->vp_ws, off);
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    h->vp_ws = nullptr;
+    return fail(h, NTK_E_OOM, "NTK-vector product buffers of " + std::to_string(off) + " bytes");
+  }
+  return NTK_OK;
+}
+
+// CNN form of vector_product_fcn: the VJP of batch 2 runs back through the readout, the global
+// average pool and the conv layers (the conv weight cotangent sum_{n,p} delta (x) patch is the
+// per-sample weight-space cotangent summed over samples); the JVP of batch 1 pushes the
+// weight-space vector forward through the convolutions, the pool and the readout.
+static int vector_product_cnn(ntk_handle* h, const float* const* params, const float* X1, int n1,
+                              const float* X2, int n2, const float* v, float* out) {
+  const int nc = h->nc, O = h->out_dim, H = h->H, W = h->W, D = h->D, C = h->ch[nc];
+  const bool sym = h->opt_symmetric && X1 == X2 && n1 == n2;
+  hipStream_t s = h->stream;
+  Profiler* P = &h->prof;
+  int rc = ensure_vp_workspace_cnn(h);
+  if (rc != NTK_OK) return rc;
+  const float* h0 = nullptr;
+  rc = cnn_forward(h, params, X1, n1, X2, n2, sym, &h0);
+  if (rc != NTK_OK) return rc;
+  auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
+  auto V = [&](size_t off) { return reinterpret_cast<float*>(h->vp_ws + off); };
+  auto hptr = [&](int l) -> const float* { return l == 0 ? h0 : F(h->off_ch[l]); };
+  const size_t r2 = sym ? 0 : (size_t)n1;
+  float* tc = V(h->vp_off_tc[0]);
+  float* tc_d = tc + h->Ktot;              // readout part [O, C]
+  const float* Wd = params[nc];
+  const float* g1 = F(h->off_g);
+  const float* g2 = F(h->off_g) + r2 * C;
+  hipError_t e;
+  // ---- VJP of batch 2 at v
+  prof_begin(P, s, KC_TRANSPOSE);
+  e = launch_transpose(s, Wd, O, C, V(h->vp_off_WLt));
+  if (e == hipSuccess) e = launch_transpose(s, v, n2, O, V(h->vp_off_dT));
+  if (e == hipSuccess) e = launch_transpose(s, g2, n2, C, V(h->vp_off_hT));
+  prof_end(P, s, KC_TRANSPOSE);
+  if (e != hipSuccess) return hip_fail(h, e, "VJP transposes");
+  GramBatch gb{};
+  gb.count = 1;
+  gb.h1[0] = V(h->vp_off_dT);     // readout weight cotangent v^T g2 [O, C]
+  gb.h2[0] = V(h->vp_off_hT);
+  gb.out[0] = tc_d;
+  gb.K[0] = n2;
+  gb.beta[0] = 0.f;
+  prof_begin(P, s, KC_GRAM);
+  e = launch_gram(s, gb, O, C);
+  prof_end(P, s, KC_GRAM);
+  if (e != hipSuccess) return hip_fail(h, e, "readout weight cotangent");
+  GramBatch gu{};
+  gu.count = 1;                   // u = v W_d [n2, C], the cotangent of the pooled features
+  gu.h1[0] = v;
+  gu.h2[0] = V(h->vp_off_WLt);
+  gu.out[0] = V(h->vp_off_u);
+  gu.K[0] = O;
+  gu.beta[0] = 0.f;
+  prof_begin(P, s, KC_GRAM);
+  e = launch_gram(s, gu, n2, C);
+  prof_end(P, s, KC_GRAM);
+  if (e != hipSuccess) return hip_fail(h, e, "pooled-feature cotangent");
+  float* Gcur = F(h->off_Gping);
+  float* Gnext = F(h->off_Gpong);
+  prof_begin(P, s, KC_VP_ELEMENTWISE);
+  e = launch_gap_adjoint(s, V(h->vp_off_u), F(h->off_cdphi[nc - 1]) + r2 * D * C, n2, D, C, Gcur);
+  prof_end(P, s, KC_VP_ELEMENTWISE);
+  if (e != hipSuccess) return hip_fail(h, e, "pooling adjoint");
+  float* J = F(h->off_J);
+  for (int l = nc - 1; l >= 0; --l) {
+    prof_begin(P, s, KC_CONV_WGRAD);
+    e = launch_conv_wgrad(s, Gcur, hptr(l) + r2 * D * h->ch[l], n2, 1, H, W, h->ch[l + 1], h->ch[l], J,
+                          h->Ktot, h->joff[l]);
+    prof_end(P, s, KC_CONV_WGRAD);
+    if (e != hipSuccess) return hip_fail(h, e, "conv weight cotangent");
+    if (l >= 1) {
+      prof_begin(P, s, KC_TRANSPOSE);
+      e = launch_conv_flip(s, params[l], h->ch[l + 1], h->ch[l], F(h->off_Kt[l]));
+      prof_end(P, s, KC_TRANSPOSE);
+      if (e != hipSuccess) return hip_fail(h, e, "kernel flip");
+      prof_begin(P, s, KC_CONV_BWD);
+      e = launch_conv_bwd(s, Gcur, n2, 1, H, W, h->ch[l + 1], F(h->off_Kt[l]), h->ch[l],
+                          F(h->off_cdphi[l - 1]) + r2 * D * h->ch[l], Gnext);
+      prof_end(P, s, KC_CONV_BWD);
+      if (e != hipSuccess) return hip_fail(h, e, "VJP conv backward");
+      std::swap(Gcur, Gnext);
+    }
+  }
+  prof_begin(P, s, KC_VP_ELEMENTWISE);
+  e = launch_colsum(s, J, n2, (int)h->Ktot, tc);   // sum of the per-sample cotangents
+  prof_end(P, s, KC_VP_ELEMENTWISE);
+  if (e != hipSuccess) return hip_fail(h, e, "conv weight cotangent sum");
+  // ---- JVP of batch 1 along theta_c
+  float* tcur = V(h->vp_off_t0);
+  float* tnext = V(h->vp_off_t1);
+  for (int l = 0; l < nc; ++l) {
+    const int co = h->ch[l + 1];
+    prof_begin(P, s, KC_CONV_FWD);
+    e = launch_conv_fwd(s, hptr(l), n1, H, W, h->ch[l], tc + h->joff[l], co, NTK_ACT_NONE,
+                        V(h->vp_off_cb), V(h->vp_off_cd));
+    if (e == hipSuccess && l > 0)
+      e = launch_conv_fwd(s, tcur, n1, H, W, h->ch[l], params[l], co, NTK_ACT_NONE, V(h->vp_off_ca),
+                          V(h->vp_off_cd));
+    prof_end(P, s, KC_CONV_FWD);
+    if (e != hipSuccess) return hip_fail(h, e, "JVP convolution");
+    prof_begin(P, s, KC_VP_ELEMENTWISE);
+    e = launch_jvp_combine(s, l > 0 ? V(h->vp_off_ca) : nullptr, V(h->vp_off_cb), nullptr,
+                           F(h->off_cdphi[l]), n1 * D, co, tnext);
+    prof_end(P, s, KC_VP_ELEMENTWISE);
+    if (e != hipSuccess) return hip_fail(h, e, "JVP step");
+    std::swap(tcur, tnext);
+  }
+  prof_begin(P, s, KC_GAP);
+  e = launch_gap(s, tcur, n1, D, C, V(h->vp_off_gdot));
+  prof_end(P, s, KC_GAP);
+  if (e != hipSuccess) return hip_fail(h, e, "JVP pooling");
+  GramBatch gr{};
+  gr.count = 2;                    // out = gdot W_d^T + g1 theta_c^d^T
+  gr.h1[0] = V(h->vp_off_gdot);
+  gr.h2[0] = Wd;
+  gr.out[0] = V(h->vp_off_ga);
+  gr.K[0] = C;
+  gr.beta[0] = 0.f;
+  gr.h1[1] = g1;
+  gr.h2[1] = tc_d;
+  gr.out[1] = V(h->vp_off_gb);
+  gr.K[1] = C;
+  gr.beta[1] = 0.f;
+  prof_begin(P, s, KC_GRAM);
+  e = launch_gram(s, gr, n1, O);
+  prof_end(P, s, KC_GRAM);
+  if (e != hipSuccess) return hip_fail(h, e, "JVP readout");
+  prof_begin(P, s, KC_VP_ELEMENTWISE);
+  e = launch_jvp_combine(s, V(h->vp_off_ga), V(h->vp_off_gb), nullptr, nullptr, n1, O, out);
+  prof_end(P, s, KC_VP_ELEMENTWISE);
+  if (e != hipSuccess) return hip_fail(h, e, "JVP output");
+  return NTK_OK;
+}
+
 extern "C" int ntk_compute(ntk_handle* h, const float* const* params, const float* X1, int n1,
                            const float* X2, int n2, float* theta) {
   if (!h) return fail(nullptr, NTK_E_ARG, "handle is NULL");
@@ -817,11 +1163,24 @@ extern "C" int ntk_compute(ntk_handle* h, const float* const* params, const floa
   return compute_fcn(h, params, X1, n1, X2, n2, theta);
 }
 
+extern "C" int ntk_vector_product(ntk_handle* h, const float* const* params, const float* X1, int n1,
+                                  const float* X2, int n2, const float* v, float* out) {
+  if (!h) return fail(nullptr, NTK_E_ARG, "handle is NULL");
+  if (!params || !X1 || !X2 || !v || !out) return fail(h, NTK_E_ARG, "null pointer argument");
+  if (n1 <= 0 || n2 <= 0) return fail(h, NTK_E_ARG, "n1 and n2 must be positive");
+  if (n1 > h->max_n1 || n2 > h->max_n2)
+    return fail(h, NTK_E_ARG, "n1/n2 exceed the max_n1/max_n2 given to ntk_init");
+  h->err.clear();
+  if (h->cnn) return vector_product_cnn(h, params, X1, n1, X2, n2, v, out);
+  return vector_product_fcn(h, params, X1, n1, X2, n2, v, out);
+}
+
 extern "C" int ntk_free(ntk_handle* h) {
   if (!h) return NTK_OK;
   (void)hipStreamSynchronize(h->stream);
   if (h->ws) (void)hipFree(h->ws);
   if (h->jc_ws) (void)hipFree(h->jc_ws);
+  if (h->vp_ws) (void)hipFree(h->vp_ws);
   delete h;
   return NTK_OK;
 }

@@ -104,6 +104,28 @@ class NTK:
                                          ctypes.c_void_p(out.data_ptr())), self._h)
         return out
 
+    def vector_product(self, params, X1, X2, v, out=None):
+        """Enqueue Theta(X1, X2) v for v [n2, O] without forming Theta; returns [n1, O]."""
+        for i, p in enumerate(params):
+            self._check_tensor(p, f"params[{i}]")
+        self._check_tensor(X1, "X1")
+        self._check_tensor(X2, "X2")
+        self._check_tensor(v, "v")
+        n1, n2, O = X1.shape[0], X2.shape[0], self.out_dim
+        if tuple(v.shape) != (n2, O):
+            raise ValueError(f"v has shape {tuple(v.shape)}, expected {(n2, O)}")
+        if out is None:
+            out = torch.empty((n1, O), dtype=torch.float32, device=self.device)
+        else:
+            self._check_tensor(out, "out")
+            if tuple(out.shape) != (n1, O):
+                raise ValueError(f"out has shape {tuple(out.shape)}, expected {(n1, O)}")
+        ptrs = (ctypes.c_void_p * len(params))(*[p.data_ptr() for p in params])
+        _lib.check(self._lib.ntk_vector_product(
+            self._h, ptrs, ctypes.c_void_p(X1.data_ptr()), n1, ctypes.c_void_p(X2.data_ptr()), n2,
+            ctypes.c_void_p(v.data_ptr()), ctypes.c_void_p(out.data_ptr())), self._h)
+        return out
+
     # -- per-kernel timing -------------------------------------------------------------
     def profile_enable(self, on=True):
         _lib.check(self._lib.ntk_profile_enable(self._h, 1 if on else 0), self._h)

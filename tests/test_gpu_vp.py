@@ -1,0 +1,133 @@
+"""GPU parity of the NTK-vector product Theta(X1, X2) v (ntk_vector_product; needs an MI355X).
+
+Reference: the oracle's J(x1) (J(x2)^T v) in fp64 (float32 layer storage, see
+tests/test_gpu_fcn.py), with the Cauchy-Schwarz error scale ||J(x1)[n1, o1]|| ||J(x2)^T v||
+of every entry.  At the depth-8 width-2048 size the reference is the fp64 structured Theta
+(pinned to the Jacobian contraction) times v.
+"""
+import numpy as np
+import pytest
+
+import oracle
+import workloads as wl
+from tests.gpu_helpers import TOL, report, scaled_errors, to_dev
+
+pytestmark = pytest.mark.gpu
+S = "fp32"
+
+
+def gpu_vp(spec, params, X1, X2, v, symmetric=True, handle=None):
+    import torch
+    from paper_2206_08720_amd import _lib
+    from paper_2206_08720_amd.ntk import NTK
+    ps = to_dev(params)
+    x1 = to_dev([X1])[0]
+    x2 = x1 if X2 is X1 else to_dev([X2])[0]
+    vv = to_dev([v])[0]
+    h = handle or NTK(spec, X1.shape[0], X2.shape[0])
+    h.set_option(_lib.NTK_OPT_SYMMETRIC, 1 if symmetric else 0)
+    out = h.vector_product(ps, x1, x2, vv)
+    torch.cuda.synchronize()
+    res = out.cpu().numpy()
+    if handle is None:
+        h.close()
+    return res
+
+
+CASES = [
+    ("tiny relu mlp with biases", wl.fcn_spec("p1", 16, [32, 32], 4, bias=True), 8, 8),
+    ("ragged relu 64-96-80-7", wl.fcn_spec("p2", 64, [96, 80], 7), 150, 133),
+    ("readout only, bias", wl.fcn_spec("p3", 6, [], 4, bias=True), 5, 3),
+    ("erf 24-40-3", wl.fcn_spec("p4", 24, [40], 3, act="erf"), 33, 17),
+    ("cnn 5x6, 2 conv layers", wl.cnn_spec("p5", (5, 6), 3, [8, 12], 5), 6, 9),
+    ("cnn erf 4x4, O=3", wl.cnn_spec("p6", (4, 4), 2, [10], 3, act="erf"), 7, 4),
+    ("cnn 8x8, 3 layers of 32", wl.cnn_spec("p7", (8, 8), 3, [32, 32, 32], 10), 12, 11),
+]
+
+
+@pytest.mark.parametrize("case", CASES, ids=[c[0] for c in CASES])
+def test_vector_product(case):
+    label, spec, n1, n2 = case
+    params = wl.make_params(spec, 2100 + n1, "2/fan_in", bias_var=0.1)
+    X1 = wl.make_inputs(spec, n1, 2200 + n1)
+    X2 = wl.make_inputs(spec, n2, 2300 + n2)
+    O = spec["layers"][-1]["out"]
+    rng = np.random.default_rng(2400 + n2)
+    v = rng.standard_normal((n2, O)).astype(np.float32)
+    ref, scale = oracle.ntk_vp(spec, params, X1, X2, v, layer_storage=S)
+    got = gpu_vp(spec, params, X1, X2, v)
+    cs, nw = scaled_errors(got, ref, scale)
+    report(f"vp {label}", cs, nw)
+    assert got.shape == ref.shape and cs <= TOL and nw <= TOL
+    # aliased batch, symmetric schedule on and off
+    vx = rng.standard_normal((n1, O)).astype(np.float32)
+    ref, scale = oracle.ntk_vp(spec, params, X1, X1, vx, layer_storage=S)
+    for sym in (True, False):
+        got = gpu_vp(spec, params, X1, X1, vx, symmetric=sym)
+        cs, nw = scaled_errors(got, ref, scale)
+        report(f"vp {label} aliased sym={sym}", cs, nw)
+        assert cs <= TOL and nw <= TOL
+
+
+def test_vector_product_cnn4_c64_32x32_full_size():
+    spec, params, X1, X2 = wl.make_workload("cnn4_c64_32x32")
+    v = np.random.default_rng(5).standard_normal((X2.shape[0], 10)).astype(np.float32)
+    ref, scale = oracle.ntk_vp(spec, params, X1, X2, v, layer_storage=S)
+    got = gpu_vp(spec, params, X1, X2, v)
+    cs, nw = scaled_errors(got, ref, scale)
+    report("vp cnn4_c64_32x32", cs, nw)
+    assert cs <= TOL and nw <= TOL
+
+
+def test_vector_product_relu_mlp_d8_w2048_full_size():
+    spec, params, X1, X2 = wl.make_workload("relu_mlp_d8_w2048")
+    O = 10
+    v = np.random.default_rng(6).standard_normal((X2.shape[0], O)).astype(np.float32)
+    theta = oracle.ntk_structured_fp64(spec, params, X1, X2, layer_storage=S)
+    ref = np.einsum("abij,bj->ai", theta, v.astype(np.float64))
+    del theta
+    t22 = oracle.ntk_structured_fp64(spec, params, X2, X2, layer_storage=S)
+    vv = v.astype(np.float64)
+    tc_sq = float(np.einsum("ai,abij,bj->", vv, t22, vv))      # ||J(X2)^T v||^2
+    del t22
+    d1 = oracle.ntk_structured_diag_fp64(spec, params, X1, layer_storage=S)
+    scale = np.sqrt(d1 * tc_sq)
+    got = gpu_vp(spec, params, X1, X2, v)
+    cs, nw = scaled_errors(got, ref, scale)
+    report("vp relu_mlp_d8_w2048", cs, nw)
+    assert cs <= TOL and nw <= TOL
+
+
+def test_vector_product_handle_reuse_and_errors():
+    import torch
+    from paper_2206_08720_amd import _lib
+    from paper_2206_08720_amd.ntk import NTK
+    spec = wl.fcn_spec("pr", 12, [20, 16], 3, bias=True)
+    params = wl.make_params(spec, 3, bias_var=0.1)
+    X1 = wl.make_inputs(spec, 9, 4)
+    X2 = wl.make_inputs(spec, 7, 5)
+    v = np.random.default_rng(1).standard_normal((7, 3)).astype(np.float32)
+    h = NTK(spec, 9, 9)
+    try:
+        a = gpu_vp(spec, params, X1, X2, v, handle=h)
+        b = gpu_vp(spec, params, X1, X2, v, handle=h)
+        assert np.array_equal(a, b), "two calls must be bit-identical"
+        c = gpu_vp(spec, params, X1[:4], X2[:2], v[:2], handle=h)
+        ref, scale = oracle.ntk_vp(spec, params, X1[:4], X2[:2], v[:2], layer_storage=S)
+        cs, nw = scaled_errors(c, ref, scale)
+        assert cs <= TOL and nw <= TOL
+        out = torch.full((9, 3), 7.0, device="cuda")
+        import ctypes
+        ps = to_dev(params)
+        ptrs = (ctypes.c_void_p * len(ps))(*[p.data_ptr() for p in ps])
+        x = to_dev([X1])[0]
+        rc = h._lib.ntk_vector_product(h._h, ptrs, ctypes.c_void_p(x.data_ptr()), 9, ctypes.c_void_p(x.data_ptr()),
+                                       10, ctypes.c_void_p(x.data_ptr()), ctypes.c_void_p(out.data_ptr()))
+        assert rc == _lib.NTK_E_ARG
+        rc = h._lib.ntk_vector_product(h._h, ptrs, ctypes.c_void_p(x.data_ptr()), 9, ctypes.c_void_p(x.data_ptr()),
+                                       9, None, ctypes.c_void_p(out.data_ptr()))
+        assert rc == _lib.NTK_E_ARG
+        torch.cuda.synchronize()
+        assert bool((out == 7.0).all())
+    finally:
+        h.close()
