@@ -35,6 +35,10 @@ STAGE_OF = {"dense_fwd": "forward", "dense_bwd": "backward", "gram": "gram",
             "ntk_fcn": "contraction", "conv_fwd": "forward", "conv_bwd": "backward",
             "conv_wgrad": "wgrad", "ntk_splitk": "contraction", "conv_pairsum": "contraction",
             "ntk_diag": "contraction"}
+# kernel class -> stage of the NTK-vector product's counter
+VP_STAGE_OF = {"dense_fwd": "forward", "dense_bwd": "vjp_backward", "gram": "gram_products",
+               "conv_fwd": "forward_and_jvp", "conv_bwd": "vjp_backward",
+               "conv_wgrad": "weight_cotangent"}
 
 
 def parse():
@@ -51,6 +55,8 @@ def parse():
     ap.add_argument("--logit", type=int, default=0, help="o* of --output logit")
     ap.add_argument("--method", default="structured", choices=["structured", "jacobian"],
                     help="structured derivatives (default) or the Jacobian-contraction baseline")
+    ap.add_argument("--op", default="ntk", choices=["ntk", "vp"],
+                    help="ntk: Theta(X1, X2); vp: the NTK-vector product Theta(X1, X2) v")
     ap.add_argument("--samples", type=int, default=0,
                     help="use only the first N samples of X1 and of X2 (0: the whole workload)")
     ap.add_argument("--cpu-samples", type=int, default=6,
@@ -143,7 +149,7 @@ def main():
 
     import workloads as wl
     from paper_2206_08720_amd import _lib
-    from paper_2206_08720_amd.flops import ntk_entries, ntk_flops
+    from paper_2206_08720_amd.flops import ntk_entries, ntk_flops, vp_flops
     from paper_2206_08720_amd.ntk import NTK
 
     if args.copy_calibration:
@@ -165,11 +171,21 @@ def main():
     h = NTK(spec, n1, n2)
     h.set_variant(args.output, args.batch, args.logit)
     h.set_method(args.method)
-    out = torch.empty(h.out_shape(n1, n2), dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
+    if args.op == "vp":
+        vvec = torch.from_numpy(np.random.default_rng(0).standard_normal((n2, O)).astype(np.float32)).cuda()
+        out = torch.empty((n1, O), dtype=torch.float32, device="cuda")
+
+        def step():
+            h.vector_product(dev, x1, x2, vvec, out=out)
+    else:
+        out = torch.empty(h.out_shape(n1, n2), dtype=torch.float32, device="cuda")
+
+        def step():
+            h.compute(dev, x1, x2, out=out)
 
     for _ in range(args.warmup):
-        h.compute(dev, x1, x2, out=out)
+        step()
     torch.cuda.synchronize()
     h.profile_read()                       # drop anything recorded so far
     h.profile_enable(True)
@@ -178,7 +194,7 @@ def main():
     t0 = time.perf_counter()
     evs[0].record(stream)
     for i in range(args.steps):
-        h.compute(dev, x1, x2, out=out)
+        step()
         evs[i + 1].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
@@ -192,6 +208,11 @@ def main():
     entries = ntk_entries(spec, n1, n2, args.output, args.batch)
     fl = ntk_flops(spec, n1, n2, symmetric=sym, output=args.output, batch=args.batch,
                    method=args.method)
+    stage_of = STAGE_OF
+    if args.op == "vp":
+        entries = n1 * O                    # outputs of one NTK-vector product
+        fl = vp_flops(spec, n1, n2, symmetric=sym)
+        stage_of = VP_STAGE_OF
     value = entries / (ms * 1e-3)
     tflops = fl["total"] / (ms * 1e-3) / 1e12
 
@@ -199,13 +220,13 @@ def main():
     for k, (tot, cnt) in prof.items():
         per_step = cnt / args.steps
         kernels[k] = {"ms_per_step": tot / args.steps, "launches_per_step": per_step}
-        st = STAGE_OF.get(k)
+        st = stage_of.get(k)
         if st and st in fl and cnt:
             kernels[k]["tflops"] = fl[st] / (tot / args.steps * 1e-3) / 1e12
-    dom = max((k for k in prof if STAGE_OF.get(k) in fl), key=lambda k: prof[k][0])
+    dom = max((k for k in prof if stage_of.get(k) in fl), key=lambda k: prof[k][0])
     tot, cnt = prof[dom]
     avg_ms = tot / cnt
-    flop_per_launch = fl[STAGE_OF[dom]] / (cnt / args.steps)
+    flop_per_launch = fl[stage_of[dom]] / (cnt / args.steps)
     achieved = flop_per_launch / (avg_ms * 1e-3) / 1e12
     roofline = {"kernel": dom, "bound": "mfma", "achieved": achieved,
                 "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
@@ -220,7 +241,9 @@ def main():
     roofline["frac_of_measured_ceiling"] = achieved / ceiling["fp32_tflops"]
 
     res = {
-        "metric": METRIC, "value": value, "unit": "NTK entries/s", "n_gpus": 1,
+        "metric": METRIC if args.op == "ntk" else "NTK-vector product outputs/sec (N1 O)",
+        "value": value, "unit": "NTK entries/s" if args.op == "ntk" else "(Theta v) entries/s",
+        "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
         "ms_per_step_median": ms_median, "ms_per_step_min": step_ms[0],
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
@@ -228,7 +251,7 @@ def main():
         "config": {"workload": name, "n1": n1, "n2": n2, "O": O,
                    "layers": [[L.get("in"), L.get("out"), L.get("act")] for L in spec["layers"]],
                    "symmetric_schedule": sym, "parallelism": "single GPU",
-                   "method": args.method,
+                   "method": args.method, "op": args.op,
                    "variant": {"output": args.output, "batch": args.batch,
                                **({"logit": args.logit} if args.output == "logit" else {})}},
         "tflops": tflops, "frac_of_fp32_mfma_peak": tflops / FP32_MFMA_PEAK_TFLOPS,
@@ -239,7 +262,7 @@ def main():
         "wall_s_timed_region": wall,
     }
     if not args.no_cpu_baseline and args.output == "full" and args.batch == "full" \
-            and not args.samples:
+            and not args.samples and args.op == "ntk":
         res["cpu_baseline"] = cpu_baseline(name, min(args.cpu_samples, n1, n2), n1, n2)
     print(json.dumps(res), flush=True)
 

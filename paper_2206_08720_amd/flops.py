@@ -109,3 +109,38 @@ def ntk_entries(spec, n1, n2, output="full", batch="full"):
     O = spec["layers"][-1]["out"]
     pairs = n1 if batch == "diagonal" else n1 * n2
     return pairs * (O * O if output == "full" else 1)
+
+
+def vp_flops(spec, n1, n2, symmetric=False):
+    """Operation count of one NTK-vector product Theta(X1, X2) v (ntk_vector_product), by the
+    kernel groups that run it: the forward pass of both batches, the VJP of batch 2 (one
+    cotangent row per sample), the weight-space cotangent (sum over batch 2) and the JVP of
+    batch 1.  FCN: `gram_products` is the weight-space cotangent plus the JVP (both run on the
+    Gram kernel).  CNN: `forward_and_jvp` is the forward pass plus the JVP convolutions."""
+    M = n1 if symmetric else n1 + n2
+    layers = spec["layers"]
+    if any(Lr["kind"] == "conv3x3" for Lr in layers):
+        H, W, _ = spec["input_shape"]
+        D = H * W
+        convs = [Lr for Lr in layers if Lr["kind"] == "conv3x3"]
+        O, C = layers[-1]["out"], convs[-1]["out"]
+        conv = [9 * c["in"] * c["out"] for c in convs]
+        st = {
+            "forward_and_jvp": sum(2.0 * M * D * k for k in conv) + sum(2.0 * n1 * D * k for k in conv)
+            + sum(2.0 * n1 * D * k for k in conv[1:]),
+            "vjp_backward": sum(2.0 * n2 * D * k for k in conv[1:]),
+            "weight_cotangent": sum(2.0 * n2 * D * k for k in conv),
+            "gram": 2.0 * n2 * O * C * 2 + 2.0 * n1 * O * C * 2,
+        }
+    else:
+        L = len(layers) - 1
+        d = [layers[0]["in"]] + [Lr["out"] for Lr in layers]
+        st = {
+            "forward": sum(2.0 * M * d[l] * d[l + 1] for l in range(L)),
+            "vjp_backward": sum(2.0 * n2 * d[l + 1] * d[l] for l in range(1, L + 1)),
+            "gram_products": sum(2.0 * n2 * d[l + 1] * d[l] for l in range(L + 1))
+            + sum(2.0 * n1 * d[l] * d[l + 1] for l in range(L + 1))
+            + sum(2.0 * n1 * d[l] * d[l + 1] for l in range(1, L + 1)),
+        }
+    st["total"] = sum(st.values())
+    return st
