@@ -21,6 +21,9 @@ namespace ntk {
 using CfgBig = TileCfg<128, 128, 32, 64, 64>;   // 4 waves, 64x64 per wave
 using CfgBig8 = TileCfg<128, 128, 32, 32, 64>;  // 8 waves, 32x64 per wave
 using CfgSK = CfgBig8;                          // stream-K contraction
+// The stream-K contraction keeps two workgroups per compute unit (two LDS stages each, so
+// both fit the 160 KB of LDS): one workgroup's barrier waits are covered by the other's MFMAs.
+constexpr int kSkPerCu = 2, kSkStages = 2;
 using CfgSmall = TileCfg<64, 64, 32, 32, 32>;   // 4 waves, 32x32 per wave
 using CfgFwd64 = TileCfg<64, 64, 32, 32, 16>;   // fp64 forward: 8 waves, 32x16 per wave
 using TrueT = std::true_type;
@@ -332,8 +335,8 @@ k_ntk_fcn(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __
 }
 
 // ------------------------------------------------------------------------------ stream-K contraction
-// The contraction's work is T tiles x L layers over P persistent workgroups (one per compute
-// unit; P = 8 * P8, P8 per XCD).  Workgroup ids are dispatched round robin over the 8 XCDs,
+// The contraction's work is T tiles x L layers over P persistent workgroups (kSkPerCu per
+// compute unit; P = 8 * P8, P8 per XCD).  Workgroup ids are dispatched round robin over the 8 XCDs,
 // each with its own L2, so the schedule is built per XCD:
 //   * tile order: the tile grid is cut into 8 bands of columns and ordered band by band,
 //     row by row inside a band; XCD x takes the x-th contiguous eighth of that order, so its
@@ -379,7 +382,7 @@ __device__ __forceinline__ void fcn_tile_layers(const FcnContraction& c, int l0,
     f32x16 acc[Cfg::FM][Cfg::FN];
     zero_acc<Cfg>(acc);
     if (DMA) {
-      gemm_mainloop_dma<Cfg>(c.G1[l], K, R1, c.G2[l], K, R2, m0, n0, 0, K, smem, acc);
+      gemm_mainloop_dma<Cfg, kSkStages>(c.G1[l], K, R1, c.G2[l], K, R2, m0, n0, 0, K, smem, acc);
     } else {
       LoadKInnerT<VEC> la{c.G1[l], R1, K, K};
       LoadKInnerT<VEC> lb{c.G2[l], R2, K, K};
@@ -516,7 +519,7 @@ constexpr bool gram_block_fits() {
 }
 
 long long ntk_fcn_part_floats(int num_cu) {
-  return (long long)num_cu * 2 * CfgSK::BM * CfgSK::BN;
+  return (long long)kSkPerCu * num_cu * 2 * CfgSK::BM * CfgSK::BN;
 }
 
 hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2, int O,
@@ -547,9 +550,12 @@ hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2
     using L = LoadKInnerT<VEC>;
     const int tm = cdiv(R1, Cfg::BM), tn = cdiv(R2, Cfg::BN);
     const int T = symmetric ? tn * (tn + 1) / 2 : tm * tn;
-    const int P = num_cu;
-    constexpr int bytes = DMA ? gemm_dma_smem_bytes<Cfg>() : gemm_smem_bytes<Cfg, L, L>();
-    static_assert((Cfg::BM + 1) * (Cfg::BN + 1) * 4 <= bytes, "Gram block must fit the LDS area");
+    const int P = kSkPerCu * num_cu;
+    // LDS: the main loop's stages, or the Gram block of a tile if larger
+    constexpr int loop_bytes = DMA ? gemm_dma_smem_bytes<Cfg, kSkStages>() : gemm_smem_bytes<Cfg, L, L>();
+    constexpr int gram_bytes = (Cfg::BM + 1) * (Cfg::BN + 1) * 4;
+    constexpr int bytes = loop_bytes > gram_bytes ? loop_bytes : gram_bytes;
+    static_assert(kSkPerCu * bytes <= 160 * 1024, "the workgroups of one CU must fit its LDS");
     hipError_t e = hipFuncSetAttribute((const void*)k_ntk_fcn_sk<Cfg, VEC, DMA>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (e != hipSuccess) return e;
@@ -563,9 +569,9 @@ hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2
     return hipGetLastError();
   };
   const long long big_tiles = (long long)cdiv(R1, 128) * cdiv(R2, 128);
-  // stream-K when there are at least as many whole tiles as compute units (P must be a
-  // multiple of 8 for the XCD-aware range order)
-  if (c.L >= 1 && part && num_cu >= 16 && num_cu % 8 == 0 && big_tiles >= num_cu)
+  // stream-K when there are at least as many whole tiles as persistent workgroups (P must be
+  // a multiple of 8 for the XCD-aware range order)
+  if (c.L >= 1 && part && num_cu >= 16 && num_cu % 8 == 0 && big_tiles >= kSkPerCu * num_cu)
     return dma ? go_sk(TrueT{}, TrueT{}) : (v ? go_sk(TrueT{}, FalseT{}) : go_sk(FalseT{}, FalseT{}));
   if (big_tiles >= 512) return v ? go(CfgBig8{}, TrueT{}) : go(CfgBig8{}, FalseT{});
   return v ? go(CfgSmall{}, TrueT{}) : go(CfgSmall{}, FalseT{});

@@ -172,7 +172,7 @@ int main() {
   check_fastdiv();
   check_tile_orders();
   long long n = 0;
-  const int Ps[] = {16, 24, 32, 64, 80, 128, 256, 304};
+  const int Ps[] = {16, 24, 32, 64, 80, 128, 256, 304, 512};
   const int Ls[] = {1, 2, 3, 5, 8, 9, 17};
   for (int P : Ps)
     for (int L : Ls) {

@@ -164,19 +164,20 @@ def test_argument_errors_leave_output_untouched():
         h.close()
 
 
-# ---- stream-K schedule of the contraction (used once the output has >= one tile per CU) ----
+# ---- stream-K schedule of the contraction (used once the output has at least as many 128 x 128
+# tiles as persistent workgroups: two per compute unit, 512 on the 256 CUs of an MI355X) ----
 SK_CASES = [
     # label, spec, n1, n2, X2 is X1
-    # symmetric: 17 x 17 tiles -> 153 triangle tiles x 8 layers over 256 ranges, so a tile
-    # spans 2-3 ranges
-    ("tiles over 3 ranges, 8 hidden layers, symmetric", wl.fcn_spec("sk1", 24, [64] * 8, 10), 205, 205, True),
-    ("split tiles, 2 hidden layers, symmetric", wl.fcn_spec("sk1b", 24, [64, 64], 10), 256, 256, True),
-    # one hidden layer: a unit is a whole tile (no splits); 153 units over 256 ranges leaves
+    # symmetric: 23 x 23 tiles -> 276 triangle tiles x 8 layers over 512 ranges, so a tile
+    # spans about 2 ranges
+    ("tiles over 2-3 ranges, 8 hidden layers, symmetric", wl.fcn_spec("sk1", 24, [64] * 8, 10), 290, 290, True),
+    ("split tiles, 2 hidden layers, symmetric", wl.fcn_spec("sk1b", 24, [64, 64], 10), 300, 300, True),
+    # one hidden layer: a unit is a whole tile (no splits); 276 units over 512 ranges leaves
     # empty ranges
     ("one hidden layer, symmetric, empty ranges", wl.fcn_spec("sk2", 16, [24], 10, bias=True),
-     205, 205, True),
-    ("ragged R1 != R2, 3 layers", wl.fcn_spec("sk3", 20, [48, 40], 8, act="erf", bias=True), 300, 250, False),
-    ("8 hidden layers, R1 != R2", wl.fcn_spec("sk4", 12, [32] * 8, 9), 240, 231, False),
+     290, 290, True),
+    ("ragged R1 != R2, 3 layers", wl.fcn_spec("sk3", 20, [48, 40], 8, act="erf", bias=True), 420, 310, False),
+    ("8 hidden layers, R1 != R2", wl.fcn_spec("sk4", 12, [32] * 8, 9), 330, 301, False),
 ]
 
 
@@ -187,7 +188,7 @@ def test_stream_k_contraction(case):
     X1 = wl.make_inputs(spec, n1, 910 + n1)
     X2 = X1 if alias else wl.make_inputs(spec, n2, 920 + n2)
     O = spec["layers"][-1]["out"]
-    assert (n1 * O // 128) * (n2 * O // 128) >= 256, "case must take the stream-K path"
+    assert -(-n1 * O // 128) * -(-n2 * O // 128) >= 512, "case must take the stream-K path"
     got = _vs_jc(f"stream-K {label}", spec, params, X1, X2)
     if alias:
         N = got.shape[0]
