@@ -152,10 +152,12 @@ static hipError_t dense_bwd_cfg(hipStream_t s, const float* G, const float* Wt, 
   return hipGetLastError();
 }
 
-// Two 8-wave workgroups share a compute unit (4 waves per SIMD).  A stream-K schedule with one
-// workgroup per compute unit removes the partial last round (1280 tiles over 512 slots at the
-// depth-8 width-2048 shape) but measured slower (113 vs 122 TFLOP/s): the extra waves per SIMD
-// are worth more than the tail here.
+// Two 8-wave workgroups share a compute unit (4 waves per SIMD).  At the depth-8 width-2048
+// shape 1280 tiles over 512 slots leave the last round half empty, but both alternatives that
+// remove it measured slower: a full stream-K schedule at one workgroup per CU (113 vs 122
+// TFLOP/s), and persistent data-parallel rounds with a stream-K tail split along K at two
+// workgroups per CU (4.91 vs 4.61 ms for the 7 layers) -- the tail round runs one workgroup
+// per CU, faster than a full round.
 hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, const float* dphi,
                             int R, int N, int K, int O, float* out) {
   const long long big_tiles = (long long)cdiv(R, 128) * cdiv(N, 128);

@@ -194,3 +194,24 @@ def test_stream_k_contraction(case):
         N = got.shape[0]
         M = got.transpose(0, 2, 1, 3).reshape(N * O, N * O)
         np.testing.assert_allclose(M, M.T, rtol=0, atol=1e-5 * np.abs(M).max())
+
+
+def test_width_2048_with_a_partial_last_round_of_backward_tiles():
+    # 480 stacked samples x O = 10 -> 38 x 16 = 608 backward tiles of 128 x 128, a partial
+    # second round over the 512 slots of two workgroups per CU
+    spec = wl.fcn_spec("bwsk", 64, [2048, 2048], 10)
+    params = wl.make_params(spec, 61, "2/fan_in")
+    X1 = wl.make_inputs(spec, 250, 62)
+    X2 = wl.make_inputs(spec, 230, 63)
+    got = gpu_ntk(spec, params, X1, X2)
+    ref = oracle.ntk_structured_fp64(spec, params, X1, X2, layer_storage=S)
+    d1 = oracle.ntk_structured_diag_fp64(spec, params, X1, layer_storage=S)
+    d2 = oracle.ntk_structured_diag_fp64(spec, params, X2, layer_storage=S)
+    cs, nw = errors(got, ref, d1, d2)
+    report("width 2048, partial last backward round, vs structured fp64", cs, nw)
+    assert cs <= TOL and nw <= TOL
+    # the structured reference itself against the Jacobian contraction on a few rows
+    sub = [0, 117, 249]
+    jc, e1, e2 = oracle.ntk_jc_with_norms(spec, params, X1[sub], X2[[0, 229]], layer_storage=S)
+    cs, nw = errors(got[np.ix_(sub, [0, 229])], jc, e1, e2)
+    assert cs <= TOL and nw <= TOL
