@@ -24,6 +24,8 @@ using CfgSK = CfgBig8;                          // stream-K contraction
 // The stream-K contraction keeps two workgroups per compute unit (two LDS stages each, so
 // both fit the 160 KB of LDS): one workgroup's barrier waits are covered by the other's MFMAs.
 constexpr int kSkPerCu = 2, kSkStages = 2;
+// the forward splits K (up to kFwdMaxSplits ways) below kFwdSplitTiles output tiles
+constexpr int kFwdSplitTiles = 256, kFwdMaxSplits = 8;
 using CfgSmall = TileCfg<64, 64, 32, 32, 32>;   // 4 waves, 32x32 per wave
 using CfgFwd64 = TileCfg<64, 64, 32, 32, 16>;   // fp64 forward: 8 waves, 32x16 per wave
 using TrueT = std::true_type;
@@ -42,6 +44,17 @@ static hipError_t set_smem(const void* fn) {
 // ------------------------------------------------------------------------------ forward
 // The pre-activation is accumulated in fp64 from the fp32 layer input and weights, then
 // the activation's decision (ReLU sign) is taken on that value and h_{l+1} is stored in fp32.
+__device__ __forceinline__ void fwd_epilogue(double z, int act, float& h, float& d) {
+  if (act == 1) {
+    h = z > 0.0 ? (float)z : 0.f;
+    d = z > 0.0 ? 1.f : 0.f;
+  } else {
+    const float zf = (float)z;
+    h = act_fwd(act, zf);
+    d = act_deriv(act, zf);
+  }
+}
+
 template <class Cfg, bool VEC, bool DMA>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_dense_fwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restrict__ bias, int M, int N,
@@ -57,16 +70,8 @@ k_dense_fwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restrict__ 
     gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
   for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, double v) {
     const double b = bias ? (double)bias[min(c, N - 1)] : 0.0;
-    const double z = v + b;
     float h, d;
-    if (act == 1) {
-      h = z > 0.0 ? (float)z : 0.f;
-      d = z > 0.0 ? 1.f : 0.f;
-    } else {
-      const float zf = (float)z;
-      h = act_fwd(act, zf);
-      d = act_deriv(act, zf);
-    }
+    fwd_epilogue(v + b, act, h, d);
     if (r < M && c < N) {
       hn[(long long)r * N + c] = h;
       dphi[(long long)r * N + c] = d;
@@ -74,14 +79,80 @@ k_dense_fwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restrict__ 
   });
 }
 
+// Split-K form for a small batch (few output tiles): workgroup (tile, z) accumulates the K
+// range [z chunk, (z+1) chunk) in fp64 and stores it; k_dense_fwd_reduce adds the partials in
+// order, in fp64, and takes the activation's decision on that sum.
+template <class Cfg, bool VEC, bool DMA>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_dense_fwd_part(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, int M, int N, int chunk,
+                 double* __restrict__ part, int tiles_n) {
+  extern __shared__ float smem[];
+  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n, z = blockIdx.y;
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  const int k0 = z * chunk, k1 = min(la.K, k0 + chunk);
+  f64x4 acc[Cfg::FM16][Cfg::FN16];
+  zero_acc<Cfg>(acc);
+  if (DMA)
+    gemm_mainloop_dma<Cfg, 3>(la.p, la.ld, la.rows, lb.p, lb.ld, lb.rows, m0, n0, k0, k1, smem, acc);
+  else
+    gemm_mainloop<Cfg>(la, lb, m0, n0, k0, k1, smem, acc);
+  double* P = part + (long long)z * M * N;
+  for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, double v) {
+    if (r < M && c < N) P[(long long)r * N + c] = v;
+  });
+}
+
+__global__ void __launch_bounds__(256)
+k_dense_fwd_reduce(const double* __restrict__ part, int splits, int M, int N, const float* __restrict__ bias,
+                   int act, float* __restrict__ hn, float* __restrict__ dphi) {
+  const long long total = (long long)M * N;
+  for (long long i = blockIdx.x * 256LL + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
+    double z = 0.0;
+    for (int q = 0; q < splits; ++q) z += part[(long long)q * total + i];
+    if (bias) z += (double)bias[i % N];
+    float h, d;
+    fwd_epilogue(z, act, h, d);
+    hn[i] = h;
+    dphi[i] = d;
+  }
+}
+
+long long dense_fwd_part_doubles(long long max_rows, long long max_cols) {
+  // the split form only runs below kFwdSplitTiles output tiles of 64 x 64
+  return std::min<long long>(kFwdMaxSplits * max_rows * max_cols,
+                             (long long)kFwdMaxSplits * kFwdSplitTiles * 64 * 64);
+}
+
 template <class Cfg, bool VEC, bool DMA = false>
 static hipError_t dense_fwd_cfg(hipStream_t s, const float* h, const float* W, const float* b, int M,
-                                int N, int K, int act, float* hn, float* dphi) {
+                                int N, int K, int act, float* hn, float* dphi, double* part,
+                                long long part_capacity) {
   using L = LoadKInnerT<VEC>;
   L la{h, M, K, K};
   L lb{W, N, K, K};
   const int tn = cdiv(N, Cfg::BN), tm = cdiv(M, Cfg::BM);
   constexpr int bytes = DMA ? gemm_dma_smem_bytes<Cfg, 3>() : gemm_smem_bytes<Cfg, L, L>();
+  // split K when the tiles alone would leave most compute units idle
+  int splits = 1, chunk = K;
+  if (part && tm * tn < kFwdSplitTiles) {
+    const int want = std::min<int>(kFwdMaxSplits, cdiv(2 * kFwdSplitTiles, tm * tn));
+    chunk = std::max(2 * Cfg::BK, cdiv(cdiv(K, want), Cfg::BK) * Cfg::BK);
+    splits = cdiv(K, chunk);
+    if ((long long)splits * M * N > part_capacity) splits = 1;
+  }
+  if (splits > 1) {
+    hipError_t e = hipFuncSetAttribute((const void*)k_dense_fwd_part<Cfg, VEC, DMA>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess) return e;
+    k_dense_fwd_part<Cfg, VEC, DMA><<<dim3(tm * tn, splits), dim3(Cfg::THREADS), bytes, s>>>(
+        la, lb, M, N, chunk, part, tn);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    const long long total = (long long)M * N;
+    k_dense_fwd_reduce<<<dim3((unsigned)std::min<long long>((total + 255) / 256, 4096)), dim3(256), 0, s>>>(
+        part, splits, M, N, b, act, hn, dphi);
+    return hipGetLastError();
+  }
   hipError_t e = hipFuncSetAttribute((const void*)k_dense_fwd<Cfg, VEC, DMA>,
                                      hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   if (e != hipSuccess) return e;
@@ -91,11 +162,13 @@ static hipError_t dense_fwd_cfg(hipStream_t s, const float* h, const float* W, c
 }
 
 hipError_t launch_dense_fwd(hipStream_t s, const float* h, const float* W, const float* b, int M,
-                            int N, int K, int act, float* hn, float* dphi) {
+                            int N, int K, int act, float* hn, float* dphi, double* part,
+                            long long part_capacity) {
   const bool v = vec_ok(h, K, K) && vec_ok(W, K, K);
-  if (v && K % 32 == 0) return dense_fwd_cfg<CfgFwd64, true, true>(s, h, W, b, M, N, K, act, hn, dphi);
-  if (v) return dense_fwd_cfg<CfgFwd64, true>(s, h, W, b, M, N, K, act, hn, dphi);
-  return dense_fwd_cfg<CfgFwd64, false>(s, h, W, b, M, N, K, act, hn, dphi);
+  if (v && K % 32 == 0)
+    return dense_fwd_cfg<CfgFwd64, true, true>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity);
+  if (v) return dense_fwd_cfg<CfgFwd64, true>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity);
+  return dense_fwd_cfg<CfgFwd64, false>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity);
 }
 
 // ------------------------------------------------------------------------------ backward

@@ -38,8 +38,11 @@ const char* kernel_class_name(int cls);
 
 // ---- fully-connected path ------------------------------------------------------------
 // z = h W^T (+ b);  hn = act(z);  dphi = act'(z).  h [M, K], W [N, K], hn/dphi [M, N].
+// Small batches split K over fp64 partials in `part` (capacity in doubles; may be null).
+long long dense_fwd_part_doubles(long long max_rows, long long max_cols);
 hipError_t launch_dense_fwd(hipStream_t s, const float* h, const float* W, const float* b, int M,
-                            int N, int K, int act, float* hn, float* dphi);
+                            int N, int K, int act, float* hn, float* dphi, double* part,
+                            long long part_capacity);
 // out[r, c] = (sum_k G[r, k] Wt[c, k]) * dphi[(r / O), c].  G [R, K], Wt [N, K], dphi [R/O, N].
 hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, const float* dphi,
                             int R, int N, int K, int O, float* out);

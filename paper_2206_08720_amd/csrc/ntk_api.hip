@@ -121,6 +121,8 @@ struct ntk_handle {
   std::vector<int> param_index;   // first parameter slot of dense layer l
   int num_cu = 0;                 // compute units of the device (stream-K workgroup count)
   size_t off_skpart = 0;          // stream-K partial tiles of the contraction
+  size_t off_fpart = 0;           // fp64 split-K partials of the small-batch forward
+  long long fpart_capacity = 0;   // doubles
   size_t off_vpart = 0;           // split-K partials of the one-output variants (trace, logit)
   long long vpart_capacity = 0;
 
@@ -237,6 +239,12 @@ static void plan_fcn(ntk_handle* h) {
   for (int l = 1; l < L; ++l) h->off_Wt[l] = take((size_t)h->dims[l] * h->dims[l + 1]);
   for (int l = 0; l <= L; ++l) h->off_gram[l] = take((size_t)h->max_n1 * h->max_n2);
   h->off_skpart = take((size_t)ntk_fcn_part_floats(h->num_cu));
+  {
+    long long dmax = 1;
+    for (int d : h->dims) dmax = std::max<long long>(dmax, d);
+    h->fpart_capacity = dense_fwd_part_doubles((long long)Mmax, dmax);
+    h->off_fpart = take((size_t)h->fpart_capacity * 2);
+  }
   {
     const int T = splitk_tile();
     const size_t tiles_max = (size_t)((h->max_n1 + T - 1) / T) * ((h->max_n2 + T - 1) / T);
@@ -469,7 +477,8 @@ static int fcn_forward(ntk_handle* h, const float* const* params, const float* X
     const float* b = h->layers[l].has_bias ? params[h->param_index[l] + 1] : nullptr;
     prof_begin(P, s, KC_DENSE_FWD);
     e = launch_dense_fwd(s, l == 0 ? *h0 : F(h->off_h[l]), W, b, M, h->dims[l + 1], h->dims[l],
-                         h->layers[l].act, F(h->off_h[l + 1]), F(h->off_dphi[l]));
+                         h->layers[l].act, F(h->off_h[l + 1]), F(h->off_dphi[l]),
+                         reinterpret_cast<double*>(h->ws + h->off_fpart), h->fpart_capacity);
     prof_end(P, s, KC_DENSE_FWD);
     if (e != hipSuccess) return hip_fail(h, e, "dense forward");
   }
