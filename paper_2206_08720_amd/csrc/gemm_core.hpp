@@ -19,6 +19,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <type_traits>
+
 #include "index_math.hpp"
 
 namespace ntk {
@@ -58,26 +60,66 @@ struct LdsGeom {
 // clamped in-range addresses, with bit j of `valid` set when element j is inside the
 // operand.  The zero fill of invalid elements happens at the LDS store, so the selects do
 // not wait on the global loads and the prefetch stays in flight across the MFMA stage.
+//
+// A loader may also keep per-row state: it then defines
+//   struct RowState;  __device__ RowState row_state(int row) const;
+//   __device__ f32x4 load4s(const RowState&, int k, uint32_t& valid) const;
+// and TileIO computes the state of each of its rows once per tile (prepare), so the index
+// arithmetic that depends only on the row (image, pixel, channel block, ...) leaves the K loop.
+template <class L, class = void>
+struct has_row_state : std::false_type {};
+template <class L>
+struct has_row_state<L, std::void_t<typename L::RowState>> : std::true_type {};
+// A loader whose 4 elements are always valid together (all or none) sets
+//   static constexpr bool UNIFORM_VALID = true;
+// and the LDS store then tests one condition instead of four bits.
+template <class L, class = void>
+struct uniform_valid : std::false_type {};
+template <class L>
+struct uniform_valid<L, std::void_t<decltype(L::UNIFORM_VALID)>> : std::integral_constant<bool, L::UNIFORM_VALID> {};
+
+template <class L, bool = has_row_state<L>::value>
+struct row_state_of {
+  using type = int;
+};
+template <class L>
+struct row_state_of<L, true> {
+  using type = typename L::RowState;
+};
+
 template <class Loader, int ROWS, int BK, int THREADS>
 struct TileIO {
   static constexpr bool KI = Loader::K_INNER;
+  static constexpr bool RS = has_row_state<Loader>::value;
   static constexpr int NV = ROWS * BK / (4 * THREADS);
   static_assert(ROWS * BK % (4 * THREADS) == 0, "tile must split evenly into float4 per thread");
   using G = LdsGeom<ROWS, BK, KI>;
+  using State = typename row_state_of<Loader>::type;
   f32x4 r[NV];
   uint32_t m[NV];
+  State st[NV];
 
+  // row and k offset of this thread's i-th float4 of the tile
+  __device__ __forceinline__ static int slot_row(int q) {
+    return KI ? q / (BK / 4) : (q % (ROWS / 4)) * 4;
+  }
+  __device__ __forceinline__ static int slot_k(int q) {
+    return KI ? (q % (BK / 4)) * 4 : q / (ROWS / 4);
+  }
+  __device__ __forceinline__ void prepare(const Loader& ld, int row0, int tid) {
+    if constexpr (RS) {
+#pragma unroll
+      for (int i = 0; i < NV; ++i) st[i] = ld.row_state(row0 + slot_row(tid + i * THREADS));
+    }
+  }
   __device__ __forceinline__ void load(const Loader& ld, int row0, int k0, int tid) {
 #pragma unroll
     for (int i = 0; i < NV; ++i) {
       const int q = tid + i * THREADS;
-      if (KI) {
-        const int row = q / (BK / 4), kq = (q % (BK / 4)) * 4;
-        r[i] = ld.load4(row0 + row, k0 + kq, m[i]);
-      } else {
-        const int k = q / (ROWS / 4), rq = (q % (ROWS / 4)) * 4;
-        r[i] = ld.load4(row0 + rq, k0 + k, m[i]);
-      }
+      if constexpr (RS)
+        r[i] = ld.load4s(st[i], k0 + slot_k(q), m[i]);
+      else
+        r[i] = ld.load4(row0 + slot_row(q), k0 + slot_k(q), m[i]);
     }
   }
   __device__ __forceinline__ void store(float* lds, int tid) const {
@@ -85,17 +127,22 @@ struct TileIO {
     for (int i = 0; i < NV; ++i) {
       const int q = tid + i * THREADS;
       f32x4 v = r[i];
-      v[0] = (m[i] & 1u) ? v[0] : 0.f;
-      v[1] = (m[i] & 2u) ? v[1] : 0.f;
-      v[2] = (m[i] & 4u) ? v[2] : 0.f;
-      v[3] = (m[i] & 8u) ? v[3] : 0.f;
-      if (KI) {
-        const int row = q / (BK / 4), kq = (q % (BK / 4)) * 4;
-        *reinterpret_cast<f32x4*>(&lds[row * G::LD + kq]) = v;
+      if constexpr (uniform_valid<Loader>::value) {
+        const bool ok = m[i] != 0u;
+        v[0] = ok ? v[0] : 0.f;
+        v[1] = ok ? v[1] : 0.f;
+        v[2] = ok ? v[2] : 0.f;
+        v[3] = ok ? v[3] : 0.f;
       } else {
-        const int k = q / (ROWS / 4), rq = (q % (ROWS / 4)) * 4;
-        *reinterpret_cast<f32x4*>(&lds[k * G::LD + rq]) = v;
+        v[0] = (m[i] & 1u) ? v[0] : 0.f;
+        v[1] = (m[i] & 2u) ? v[1] : 0.f;
+        v[2] = (m[i] & 4u) ? v[2] : 0.f;
+        v[3] = (m[i] & 8u) ? v[3] : 0.f;
       }
+      if (KI)
+        *reinterpret_cast<f32x4*>(&lds[slot_row(q) * G::LD + slot_k(q)]) = v;
+      else
+        *reinterpret_cast<f32x4*>(&lds[slot_k(q) * G::LD + slot_row(q)]) = v;
     }
   }
 };
@@ -245,6 +292,8 @@ __device__ __forceinline__ void gemm_mainloop(const LA& la, const LB& lb, int m0
   if (nk <= 0) return;
   TileIO<LA, Cfg::BM, Cfg::BK, Cfg::THREADS> ia;
   TileIO<LB, Cfg::BN, Cfg::BK, Cfg::THREADS> ib;
+  ia.prepare(la, m0, tid);
+  ib.prepare(lb, n0, tid);
   ia.load(la, m0, k_begin, tid);
   ib.load(lb, n0, k_begin, tid);
   ia.store(smem, tid);
@@ -340,6 +389,7 @@ __device__ __forceinline__ void for_each_acc_aux(f32x16 (&acc)[Cfg::FM][Cfg::FN]
 template <bool VEC>
 struct LoadKInnerT {
   static constexpr bool K_INNER = true;
+  static constexpr bool UNIFORM_VALID = VEC;   // VEC: the 4 elements are valid together
   const float* p;
   int rows, K;
   long long ld;

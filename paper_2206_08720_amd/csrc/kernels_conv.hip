@@ -46,6 +46,7 @@ static hipError_t set_smem(const void* fn) {
 template <bool VEC>
 struct LoadPatchesKInnerT {
   static constexpr bool K_INNER = true;
+  static constexpr bool UNIFORM_VALID = VEC;   // VEC: the 4 elements are valid together
   const float* x;
   int rows, H, W, C, K;  // K = 9*C
   FastDiv fD, fW, fC;
@@ -57,6 +58,46 @@ struct LoadPatchesKInnerT {
     ok = k < K && yy >= 0 && yy < H && xq >= 0 && xq < W;
     const int yc = min(max(yy, 0), H - 1), xc = min(max(xq, 0), W - 1);
     return x[(((long long)img * H + yc) * W + xc) * C + ci];
+  }
+  // the row's pixel, computed once per tile: element offset of (img, y, x) (clamped row), y, x
+  struct RowState {
+    long long base;
+    int y, x, ok;
+  };
+  __device__ __forceinline__ RowState row_state(int row) const {
+    const int rc = min(row, rows - 1);
+    const int img = (int)fD.div(rc), p = rc - img * (int)fD.d;
+    const int y = (int)fW.div(p), xx = p - y * W;
+    return {(((long long)img * H + y) * W + xx) * C, y, xx, row < rows ? 1 : 0};
+  }
+  // element (row, k): tap (kh, kw) = k / C reads the pixel (y + kh - 1, x + kw - 1); outside the
+  // image the row's own pixel is read and masked
+  __device__ __forceinline__ f32x4 load4s(const RowState& s, int k, uint32_t& valid) const {
+    if (VEC) {
+      const int kc = min(k, K - 4);
+      const int t = (int)fC.div(kc), ci = kc - t * C;
+      const int kh = (t * 11) >> 5, kw = t - 3 * kh;
+      const int yy = s.y + kh - 1, xq = s.x + kw - 1;
+      const bool ok = s.ok & (k < K) & ((unsigned)yy < (unsigned)H) & ((unsigned)xq < (unsigned)W);
+      const int off = ok ? ((kh - 1) * W + (kw - 1)) * C + ci : ci;
+      valid = ok ? 0xFu : 0u;
+      return *reinterpret_cast<const f32x4*>(x + s.base + off);
+    } else {
+      f32x4 v;
+      valid = 0;
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        const int kc = min(k + j, K - 1);
+        const int t = (int)fC.div(kc), ci = kc - t * C;
+        const int kh = (t * 11) >> 5, kw = t - 3 * kh;
+        const int yy = s.y + kh - 1, xq = s.x + kw - 1;
+        const bool ok = s.ok && k + j < K && yy >= 0 && yy < H && xq >= 0 && xq < W;
+        const long long off = ok ? (long long)((kh - 1) * W + (kw - 1)) * C : 0;
+        v[j] = x[s.base + off + ci];
+        valid |= ok ? (1u << j) : 0u;
+      }
+      return v;
+    }
   }
   __device__ __forceinline__ f32x4 load4(int row, int k, uint32_t& valid) const {
     const int rc = min(row, rows - 1);
@@ -91,9 +132,28 @@ struct LoadPatchesKInnerT {
 template <bool VEC>
 struct LoadCotangentKOuterT {
   static constexpr bool K_INNER = false;
+  static constexpr bool UNIFORM_VALID = VEC;
   const float* g;
   int rows, K, C, D;     // rows = O*C, K = D
   FastDiv fC;
+  // offset o*D*C + c of the row block (VEC: rows row..row+3 are contiguous), once per tile
+  struct RowState {
+    long long off;
+    int row;
+  };
+  __device__ __forceinline__ RowState row_state(int row) const {
+    const int rc = min(row, VEC ? rows - 4 : rows - 1);
+    const int o = (int)fC.div(rc), c = rc - o * C;
+    return {(long long)o * D * C + c, row};
+  }
+  __device__ __forceinline__ f32x4 load4s(const RowState& s, int k, uint32_t& valid) const {
+    if (VEC) {
+      const int kc = min(k, K - 1);
+      valid = (s.row < rows && k < K) ? 0xFu : 0u;
+      return *reinterpret_cast<const f32x4*>(g + s.off + (long long)kc * C);
+    }
+    return load4(s.row, k, valid);
+  }
   __device__ __forceinline__ f32x4 load4(int row, int k, uint32_t& valid) const {
     const int kc = min(k, K - 1);
     if (VEC) {
@@ -121,9 +181,33 @@ struct LoadCotangentKOuterT {
 template <bool VEC>
 struct LoadPatchesKOuterT {
   static constexpr bool K_INNER = false;
+  static constexpr bool UNIFORM_VALID = VEC;
   const float* x;        // sample base, [H, W, C]
   int rows, K, H, W, C;  // rows = 9*C, K = D
   FastDiv fW, fC;
+  // the rows' tap offset (dy, dx) and first channel (VEC: 4 consecutive channels of one
+  // tap), once per tile
+  struct RowState {
+    int dy, dx, dd, ci, row;   // dd = dy * W + dx
+  };
+  __device__ __forceinline__ RowState row_state(int row) const {
+    const int rc = min(row, VEC ? rows - 4 : rows - 1);
+    const int t = (int)fC.div(rc), ci = rc - t * C;
+    const int kh = (t * 11) >> 5, kw = t - 3 * kh;
+    return {kh - 1, kw - 1, (kh - 1) * W + (kw - 1), ci, row};
+  }
+  __device__ __forceinline__ f32x4 load4s(const RowState& s, int p, uint32_t& valid) const {
+    if (VEC) {
+      const int pc = min(p, K - 1);
+      const int y = (int)fW.div(pc), xx = pc - y * W;
+      const int yy = y + s.dy, xq = xx + s.dx;
+      const bool ok = (s.row < rows) & (p < K) & ((unsigned)yy < (unsigned)H) & ((unsigned)xq < (unsigned)W);
+      valid = ok ? 0xFu : 0u;
+      const int q = ok ? pc + s.dd : pc;   // outside the image: the pixel itself, masked
+      return *reinterpret_cast<const f32x4*>(x + (long long)q * C + s.ci);
+    }
+    return load4(s.row, p, valid);
+  }
   __device__ __forceinline__ f32x4 load4(int row, int p, uint32_t& valid) const {
     const int pc = min(p, K - 1);
     const int y = (int)fW.div(pc), xx = pc - y * W;
@@ -252,28 +336,31 @@ hipError_t launch_gap(hipStream_t s, const float* h, int images, int D, int C, f
   return hipGetLastError();
 }
 
-// G[(img*O + o), p, c] = Wd[o, c] / D * dphi[img, p, c]
-__global__ void k_conv_seed(const float* __restrict__ Wd, const float* __restrict__ dphi, int images,
-                            int O, int D, int C, float* __restrict__ G) {
-  const long long total = (long long)images * O * D * C;
-  const float inv = 1.0f / (float)D;
-  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
-       i += (long long)gridDim.x * blockDim.x) {
-    const int c = (int)(i % C);
-    const long long rest = i / C;
-    const int p = (int)(rest % D);
-    const long long io = rest / D;
-    const int o = (int)(io % O);
-    const long long img = io / O;
-    G[i] = Wd[(long long)o * C + c] * inv * dphi[(img * D + p) * C + c];
+// G[(img*O + o), p, c] = Wd[o, c] / D * dphi[img, p, c]; blockIdx.y = img*O + o, the x-blocks
+// stride over the D*C elements of that cotangent image (no 64-bit division per element).
+__global__ void __launch_bounds__(256)
+k_conv_seed(const float* __restrict__ Wd, const float* __restrict__ dphi, int IO, int O, int DC, FastDiv fC,
+            float inv_d, float* __restrict__ G) {
+  const int C = (int)fC.d;
+  for (int io = blockIdx.y; io < IO; io += gridDim.y) {
+    const int img = io / O, o = io - img * O;
+    const float* wrow = Wd + (long long)o * C;
+    const float* drow = dphi + (long long)img * DC;
+    float* grow = G + (long long)io * DC;
+    for (int q = blockIdx.x * 256 + threadIdx.x; q < DC; q += gridDim.x * 256) {
+      const int c = q - (int)fC.div(q) * C;
+      grow[q] = wrow[c] * inv_d * drow[q];
+    }
   }
 }
 
 hipError_t launch_conv_seed(hipStream_t s, const float* Wd, const float* dphi, int images, int O, int D,
                             int C, float* G) {
-  const long long total = (long long)images * O * D * C;
-  const int blocks = (int)std::min<long long>((total + 255) / 256, 256 * 128);
-  k_conv_seed<<<dim3(blocks), dim3(256), 0, s>>>(Wd, dphi, images, O, D, C, G);
+  const int DC = D * C;
+  const int bx = std::min(cdiv(DC, 256), 64);
+  const int IO = images * O;
+  k_conv_seed<<<dim3(bx, std::min(IO, 32768)), dim3(256), 0, s>>>(Wd, dphi, IO, O, DC, FastDiv((uint32_t)C),
+                                                                 1.0f / (float)D, G);
   return hipGetLastError();
 }
 
