@@ -557,19 +557,35 @@ constexpr int gemm_dma_smem_bytes() {
   return NSTAGE * (DmaTile<Cfg::BM>::FLOATS + DmaTile<Cfg::BN>::FLOATS) * 4;
 }
 
+// An operand of the direct-to-LDS loop is an "issuer": prepare(row0, wave, lane) once per
+// tile, then issue<WAVES>(k0, lds, wave, lane) per K tile, OPS<WAVES> instructions per wave.
+// DmaRowMajor: a K-contiguous row-major operand (the rows clamped to the last one).
+template <int ROWS>
+struct DmaRowMajor {
+  const float* __restrict__ p;
+  long long ld;
+  int rows;
+  int row0 = 0;
+  template <int WAVES>
+  static constexpr int OPS = ROWS / (8 * WAVES);
+  __device__ __forceinline__ void prepare(int r0, int, int) { row0 = r0; }
+  template <int WAVES>
+  __device__ __forceinline__ void issue(int k0, float* lds, int wave, int lane) const {
+    DmaTile<ROWS>::template issue<WAVES>(p, ld, rows, row0, k0, lds, wave, lane);
+  }
+};
+
 // K loop over [k_begin, k_end) (both multiples of 32) for the tile (m0, n0), with NSTAGE LDS
 // stages (2: tile kt+1 in flight during tile kt; 3: tiles kt+1 and kt+2).  Ends with a
 // barrier, so the caller may reuse `smem` afterwards.
-template <class Cfg, int NSTAGE = kDmaStages, class AccT>
-__device__ __forceinline__ void gemm_mainloop_dma(const float* __restrict__ A, long long lda, int rowsA,
-                                                  const float* __restrict__ B, long long ldb, int rowsB,
-                                                  int m0, int n0, int k_begin, int k_end, float* smem,
-                                                  AccT& acc) {
+template <class Cfg, int NSTAGE, class IA, class IB, class AccT>
+__device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, int n0, int k_begin, int k_end,
+                                                      float* smem, AccT& acc) {
   static_assert(Cfg::BK == 32, "direct-to-LDS main loop uses BK = 32");
   using TA = DmaTile<Cfg::BM>;
   using TB = DmaTile<Cfg::BN>;
   constexpr int STAGE = TA::FLOATS + TB::FLOATS;
-  constexpr int PER_TILE = Cfg::BM / (8 * Cfg::WAVES) + Cfg::BN / (8 * Cfg::WAVES);  // DMA ops per wave
+  constexpr int PER_TILE = IA::template OPS<Cfg::WAVES> + IB::template OPS<Cfg::WAVES>;  // DMA ops per wave
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
@@ -577,10 +593,12 @@ __device__ __forceinline__ void gemm_mainloop_dma(const float* __restrict__ A, l
   const int nk = (k_end - k_begin) / 32;
   if (nk <= 0) return;
   static_assert(NSTAGE == 2 || NSTAGE == 3, "two or three LDS stages");
+  ia.prepare(m0, wave, lane);
+  ib.prepare(n0, wave, lane);
   auto issue = [&](int kt) {
     float* st = smem + (kt % NSTAGE) * STAGE;
-    TA::template issue<Cfg::WAVES>(A, lda, rowsA, m0, k_begin + kt * 32, st, wave, lane);
-    TB::template issue<Cfg::WAVES>(B, ldb, rowsB, n0, k_begin + kt * 32, st + TA::FLOATS, wave, lane);
+    ia.template issue<Cfg::WAVES>(k_begin + kt * 32, st, wave, lane);
+    ib.template issue<Cfg::WAVES>(k_begin + kt * 32, st + TA::FLOATS, wave, lane);
   };
   issue(0);
   if (NSTAGE == 3 && nk > 1) issue(1);
@@ -600,6 +618,17 @@ __device__ __forceinline__ void gemm_mainloop_dma(const float* __restrict__ A, l
     mma_stage_dma<Cfg>(st, st + TA::FLOATS, acc, wm0, wn0, lane);
   }
   __syncthreads();
+}
+
+// Both operands K-contiguous row-major (LoadKInnerT<true> conditions, K % 32 == 0).
+template <class Cfg, int NSTAGE = kDmaStages, class AccT>
+__device__ __forceinline__ void gemm_mainloop_dma(const float* __restrict__ A, long long lda, int rowsA,
+                                                  const float* __restrict__ B, long long ldb, int rowsB,
+                                                  int m0, int n0, int k_begin, int k_end, float* smem,
+                                                  AccT& acc) {
+  DmaRowMajor<Cfg::BM> ia{A, lda, rowsA};
+  DmaRowMajor<Cfg::BN> ib{B, ldb, rowsB};
+  gemm_mainloop_dma_ops<Cfg, NSTAGE>(ia, ib, m0, n0, k_begin, k_end, smem, acc);
 }
 
 }  // namespace ntk

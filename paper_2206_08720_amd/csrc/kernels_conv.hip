@@ -254,17 +254,80 @@ static LoadPatchesKInnerT<VEC> patches_kinner(const float* x, int images, int H,
   return l;
 }
 
+// Patch matrix of an NHWC batch as a direct-to-LDS operand (see DmaTile): row = img*D + p,
+// column k = tap*C + ci with C % 32 == 0, so the 32 columns of a K tile lie inside one tap.
+// Every lane loads 16 bytes of one row; a tap that falls outside the image (the zero padding)
+// reads a page of zeros instead.  The rows' pixels are computed once per tile (prepare).
+template <int ROWS, int WAVES>
+struct DmaPatches {
+  const float* __restrict__ x;
+  const float* __restrict__ zero;   // >= 16 bytes of zeros, 16-byte aligned
+  int rows, H, W, C;
+  FastDiv fD, fW, fC;
+  static constexpr int NI = ROWS / (8 * WAVES);
+  template <int WV>
+  static constexpr int OPS = ROWS / (8 * WV);
+  long long base[NI];
+  int y[NI], xx[NI], ok[NI];
+  __device__ __forceinline__ void prepare(int row0, int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int row = row0 + (i * WAVES + wave) * 8 + (lane >> 3);
+      const int rc = min(row, rows - 1);
+      const int img = (int)fD.div(rc), p = rc - img * (int)fD.d;
+      const int yy = (int)fW.div(p), xq = p - yy * W;
+      base[i] = (((long long)img * H + yy) * W + xq) * C;
+      y[i] = yy;
+      xx[i] = xq;
+      ok[i] = row < rows ? 1 : 0;
+    }
+  }
+  template <int WV>
+  __device__ __forceinline__ void issue(int k0, float* lds, int wave, int lane) const {
+    static_assert(WV == WAVES, "issuer built for this workgroup shape");
+    const int t = (int)fC.div(k0), cb = k0 - t * C;
+    const int kh = (t * 11) >> 5, kw = t - 3 * kh;
+    const int tapoff = ((kh - 1) * W + (kw - 1)) * C + cb;
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int r0 = (i * WAVES + wave) * 8;
+      const int r = r0 + (lane >> 3);
+      const int c = DmaTile<ROWS>::swz(r, lane & 7);
+      const int yy = y[i] + kh - 1, xq = xx[i] + kw - 1;
+      const bool good = ok[i] & ((unsigned)yy < (unsigned)H) & ((unsigned)xq < (unsigned)W);
+      const float* src = good ? x + base[i] + tapoff + 4 * c : zero;
+      float* dst = lds + __builtin_amdgcn_readfirstlane(r0 * DmaTile<ROWS>::BK);
+      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+    }
+  }
+};
+
+template <int ROWS, int WAVES>
+static DmaPatches<ROWS, WAVES> dma_patches(const float* x, const float* zero, int images, int H, int W,
+                                           int C) {
+  DmaPatches<ROWS, WAVES> d;
+  d.x = x;
+  d.zero = zero;
+  d.rows = images * H * W;
+  d.H = H;
+  d.W = W;
+  d.C = C;
+  d.fD = FastDiv((uint32_t)(H * W));
+  d.fW = FastDiv((uint32_t)W);
+  d.fC = FastDiv((uint32_t)C);
+  return d;
+}
+
+// The direct-to-LDS path needs C % 32 == 0 and 16-byte aligned operands.
+static bool conv_dma_ok(const void* x, int C, const void* K, const void* zero) {
+  return zero && C % 32 == 0 && aligned16(x) && aligned16(K);
+}
+
 // ------------------------------------------------------------------------------ forward
-template <class Cfg, bool VEC>
-__global__ void __launch_bounds__(Cfg::THREADS)
-k_conv_fwd(LoadPatchesKInnerT<VEC> la, LoadKInnerT<VEC> lb, int M, int N, int act,
-           float* __restrict__ hn, float* __restrict__ dphi, int tiles_n) {
-  extern __shared__ float smem[];
-  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
-  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
-  f64x4 acc[Cfg::FM16][Cfg::FN16];
-  zero_acc<Cfg>(acc);
-  gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
+template <class Cfg>
+__device__ __forceinline__ void conv_fwd_epilogue(f64x4 (&acc)[Cfg::FM16][Cfg::FN16], int m0, int n0,
+                                                  int M, int N, int act, float* __restrict__ hn,
+                                                  float* __restrict__ dphi) {
   for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, double z) {
     float h, d;
     if (act == 1) {
@@ -280,6 +343,33 @@ k_conv_fwd(LoadPatchesKInnerT<VEC> la, LoadKInnerT<VEC> lb, int M, int N, int ac
       dphi[(long long)r * N + c] = d;
     }
   });
+}
+
+// direct-to-LDS form (C % 32 == 0): patches gathered by the DMA, three LDS stages
+template <class Cfg>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_conv_fwd_dma(DmaPatches<Cfg::BM, Cfg::WAVES> pa, DmaRowMajor<Cfg::BN> pb, int K, int M, int N, int act,
+               float* __restrict__ hn, float* __restrict__ dphi, int tiles_n) {
+  extern __shared__ float smem[];
+  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  f64x4 acc[Cfg::FM16][Cfg::FN16];
+  zero_acc<Cfg>(acc);
+  gemm_mainloop_dma_ops<Cfg, 3>(pa, pb, m0, n0, 0, K, smem, acc);
+  conv_fwd_epilogue<Cfg>(acc, m0, n0, M, N, act, hn, dphi);
+}
+
+template <class Cfg, bool VEC>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_conv_fwd(LoadPatchesKInnerT<VEC> la, LoadKInnerT<VEC> lb, int M, int N, int act,
+           float* __restrict__ hn, float* __restrict__ dphi, int tiles_n) {
+  extern __shared__ float smem[];
+  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  f64x4 acc[Cfg::FM16][Cfg::FN16];
+  zero_acc<Cfg>(acc);
+  gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
+  conv_fwd_epilogue<Cfg>(acc, m0, n0, M, N, act, hn, dphi);
 }
 
 template <bool VEC>
@@ -300,7 +390,20 @@ static hipError_t conv_fwd_vec(hipStream_t s, const float* x, int images, int H,
 }
 
 hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int W, int Cin,
-                           const float* K, int Cout, int act, float* hn, float* dphi) {
+                           const float* K, int Cout, int act, float* hn, float* dphi, const float* zero) {
+  if (conv_dma_ok(x, Cin, K, zero)) {
+    using Cfg = CfgConvF64;
+    const int M = images * H * W, Kd = 9 * Cin;
+    const int tn = cdiv(Cout, Cfg::BN), tm = cdiv(M, Cfg::BM);
+    auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(x, zero, images, H, W, Cin);
+    DmaRowMajor<Cfg::BN> pb{K, Kd, Cout};
+    constexpr int bytes = gemm_dma_smem_bytes<Cfg, 3>();
+    hipError_t e = hipFuncSetAttribute((const void*)k_conv_fwd_dma<Cfg>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess) return e;
+    k_conv_fwd_dma<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(pa, pb, Kd, M, Cout, act, hn, dphi, tn);
+    return hipGetLastError();
+  }
   if (Cin % 4 == 0 && aligned16(x) && vec_ok(K, 9 * Cin, 9 * Cin))
     return conv_fwd_vec<true>(s, x, images, H, W, Cin, K, Cout, act, hn, dphi);
   return conv_fwd_vec<false>(s, x, images, H, W, Cin, K, Cout, act, hn, dphi);
@@ -406,6 +509,30 @@ k_conv_bwd(LoadPatchesKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restr
   });
 }
 
+// direct-to-LDS form (Cg % 32 == 0): the cotangent patches gathered by the DMA, 3 LDS stages
+template <class Cfg>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_conv_bwd_dma(DmaPatches<Cfg::BM, Cfg::WAVES> pa, DmaRowMajor<Cfg::BN> pb, int K,
+               const float* __restrict__ dphi, int R, int N, FastDiv fOD, FastDiv fD, float* __restrict__ out,
+               int tiles_n) {
+  extern __shared__ float smem[];
+  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  f32x16 acc[Cfg::FM][Cfg::FN];
+  zero_acc<Cfg>(acc);
+  gemm_mainloop_dma_ops<Cfg, 3>(pa, pb, m0, n0, 0, K, smem, acc);
+  float g[Cfg::FM][Cfg::FN][16];
+  gather_acc<Cfg>(g, m0, n0, [&](int r, int c) {
+    const int rc = min(r, R - 1), cc = min(c, N - 1);
+    const int img = (int)fOD.div(rc);
+    const int p = rc - (int)fD.div(rc) * (int)fD.d;
+    return dphi[((long long)img * fD.d + p) * N + cc];
+  });
+  for_each_acc_aux<Cfg>(acc, g, m0, n0, [&](int r, int c, float v, float d) {
+    if (r < R && c < N) out[(long long)r * N + c] = v * d;
+  });
+}
+
 template <bool VEC>
 static hipError_t conv_bwd_vec(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
                                const float* Kt, int Cin, const float* dphi, float* out) {
@@ -425,7 +552,22 @@ static hipError_t conv_bwd_vec(hipStream_t s, const float* G, int images, int O,
 }
 
 hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
-                           const float* Kt, int Cin, const float* dphi, float* out) {
+                           const float* Kt, int Cin, const float* dphi, float* out, const float* zero) {
+  if (conv_dma_ok(G, Cg, Kt, zero)) {
+    using Cfg = CfgConv;
+    const int D = H * W, Kd = 9 * Cg;
+    const int R = images * O * D;
+    const int tn = cdiv(Cin, Cfg::BN), tm = cdiv(R, Cfg::BM);
+    auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(G, zero, images * O, H, W, Cg);
+    DmaRowMajor<Cfg::BN> pb{Kt, Kd, Cin};
+    constexpr int bytes = gemm_dma_smem_bytes<Cfg, 3>();
+    hipError_t e = hipFuncSetAttribute((const void*)k_conv_bwd_dma<Cfg>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess) return e;
+    k_conv_bwd_dma<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(
+        pa, pb, Kd, dphi, R, Cin, FastDiv((uint32_t)(O * D)), FastDiv((uint32_t)D), out, tn);
+    return hipGetLastError();
+  }
   if (Cg % 4 == 0 && aligned16(G) && vec_ok(Kt, 9 * Cg, 9 * Cg))
     return conv_bwd_vec<true>(s, G, images, O, H, W, Cg, Kt, Cin, dphi, out);
   return conv_bwd_vec<false>(s, G, images, O, H, W, Cg, Kt, Cin, dphi, out);

@@ -50,6 +50,10 @@ CASES = [
     ("ragged 7x9, 3 layers", wl.cnn_spec("c3", (7, 9), 3, [16, 12, 20], 10), 9, 4),
     ("O=1, n1=n2=1", wl.cnn_spec("c4", (6, 6), 4, [8, 8], 1), 1, 1),
     ("tile-spanning rows, 8x8", wl.cnn_spec("c5", (8, 8), 3, [32, 32], 10), 23, 17),
+    # 32-channel layers take the direct-to-LDS patch loads; 5 x 7 images leave ragged row
+    # tiles and padding taps on every border
+    ("direct-to-LDS patches, ragged 5x7", wl.cnn_spec("c6", (5, 7), 3, [32, 32, 32], 3), 5, 4),
+    ("direct-to-LDS patches, 1x1 images", wl.cnn_spec("c7", (1, 1), 4, [32, 64], 2), 3, 7),
 ]
 
 
