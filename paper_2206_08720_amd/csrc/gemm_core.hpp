@@ -483,12 +483,34 @@ struct DmaTile {
   }
 };
 
-template <class Cfg>
+// K-outer form of the tile, for operands whose global memory holds 4 consecutive rows at one
+// k (16 bytes): stored [BK][ROWS] (k-major), unpadded.  The 16-byte chunk c of k-row k sits at
+// position c ^ (((k >> 2) & 1) << 3): a fragment read takes k-rows k and k + 4 in the two
+// half-waves, which then fall 32 floats apart, in disjoint bank halves.
+template <int ROWS>
+struct DmaTileKOuter {
+  static constexpr int BK = 32;
+  static constexpr int FLOATS = ROWS * BK;
+  static_assert(ROWS % 64 == 0, "k-rows of at least 16 chunks");
+  __device__ static __forceinline__ int swz(int k, int pos) { return pos ^ (((k >> 2) & 1) << 3); }
+  __device__ static __forceinline__ float at(const float* lds, int k, int row) {
+    return lds[k * ROWS + (swz(k, row >> 2) << 2) + (row & 3)];
+  }
+  // k .. k+3 of one row
+  __device__ static __forceinline__ f32x4 frag(const float* lds, int row, int k) {
+    f32x4 v;
+    v[0] = at(lds, k, row);
+    v[1] = at(lds, k + 1, row);
+    v[2] = at(lds, k + 2, row);
+    v[3] = at(lds, k + 3, row);
+    return v;
+  }
+};
+
+template <class Cfg, class TA = DmaTile<Cfg::BM>, class TB = DmaTile<Cfg::BN>>
 __device__ __forceinline__ void mma_stage_dma(const float* As, const float* Bs,
                                               f32x16 (&acc)[Cfg::FM][Cfg::FN], int wm0, int wn0,
                                               int lane) {
-  using TA = DmaTile<Cfg::BM>;
-  using TB = DmaTile<Cfg::BN>;
   const int lr = lane & 31, lk = (lane >> 5) * 4;
   f32x4 a[2][Cfg::FM], b[2][Cfg::FN];
 #pragma unroll
@@ -516,12 +538,10 @@ __device__ __forceinline__ void mma_stage_dma(const float* As, const float* Bs,
 }
 
 // fp64 16x16x4 flavour of the stage (pre-activations of the forward pass), same tiles.
-template <class Cfg>
+template <class Cfg, class TA = DmaTile<Cfg::BM>, class TB = DmaTile<Cfg::BN>>
 __device__ __forceinline__ void mma_stage_dma(const float* As, const float* Bs,
                                               f64x4 (&acc)[Cfg::FM16][Cfg::FN16], int wm0, int wn0,
                                               int lane) {
-  using TA = DmaTile<Cfg::BM>;
-  using TB = DmaTile<Cfg::BN>;
   const int lr = lane & 15, lk = (lane >> 4) * 4;
 #pragma unroll
   for (int kk = 0; kk < 32; kk += 16) {
@@ -562,6 +582,7 @@ constexpr int gemm_dma_smem_bytes() {
 // DmaRowMajor: a K-contiguous row-major operand (the rows clamped to the last one).
 template <int ROWS>
 struct DmaRowMajor {
+  using Tile = DmaTile<ROWS>;
   const float* __restrict__ p;
   long long ld;
   int rows;
@@ -575,22 +596,22 @@ struct DmaRowMajor {
   }
 };
 
-// K loop over [k_begin, k_end) (both multiples of 32) for the tile (m0, n0), with NSTAGE LDS
-// stages (2: tile kt+1 in flight during tile kt; 3: tiles kt+1 and kt+2).  Ends with a
-// barrier, so the caller may reuse `smem` afterwards.
+// K loop over [k_begin, k_end) (k_begin a multiple of 32; a ragged last K tile is the issuers'
+// business) for the tile (m0, n0), with NSTAGE LDS stages (2: tile kt+1 in flight during tile
+// kt; 3: tiles kt+1 and kt+2).  Ends with a barrier, so the caller may reuse `smem` afterwards.
 template <class Cfg, int NSTAGE, class IA, class IB, class AccT>
 __device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, int n0, int k_begin, int k_end,
                                                       float* smem, AccT& acc) {
   static_assert(Cfg::BK == 32, "direct-to-LDS main loop uses BK = 32");
-  using TA = DmaTile<Cfg::BM>;
-  using TB = DmaTile<Cfg::BN>;
+  using TA = typename IA::Tile;
+  using TB = typename IB::Tile;
   constexpr int STAGE = TA::FLOATS + TB::FLOATS;
   constexpr int PER_TILE = IA::template OPS<Cfg::WAVES> + IB::template OPS<Cfg::WAVES>;  // DMA ops per wave
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
   const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
-  const int nk = (k_end - k_begin) / 32;
+  const int nk = (k_end - k_begin + 31) / 32;
   if (nk <= 0) return;
   static_assert(NSTAGE == 2 || NSTAGE == 3, "two or three LDS stages");
   ia.prepare(m0, wave, lane);
@@ -615,7 +636,7 @@ __device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, in
     __builtin_amdgcn_sched_barrier(0);
     if (kt + NSTAGE - 1 < nk) issue(kt + NSTAGE - 1);
     const float* st = smem + (kt % NSTAGE) * STAGE;
-    mma_stage_dma<Cfg>(st, st + TA::FLOATS, acc, wm0, wn0, lane);
+    mma_stage_dma<Cfg, TA, TB>(st, st + TA::FLOATS, acc, wm0, wn0, lane);
   }
   __syncthreads();
 }

@@ -260,6 +260,7 @@ static LoadPatchesKInnerT<VEC> patches_kinner(const float* x, int images, int H,
 // reads a page of zeros instead.  The rows' pixels are computed once per tile (prepare).
 template <int ROWS, int WAVES>
 struct DmaPatches {
+  using Tile = DmaTile<ROWS>;
   const float* __restrict__ x;
   const float* __restrict__ zero;   // >= 16 bytes of zeros, 16-byte aligned
   int rows, H, W, C;
@@ -322,6 +323,94 @@ static DmaPatches<ROWS, WAVES> dma_patches(const float* x, const float* zero, in
 static bool conv_dma_ok(const void* x, int C, const void* K, const void* zero) {
   return zero && C % 32 == 0 && aligned16(x) && aligned16(K);
 }
+
+// K-outer direct-to-LDS operands of the weight-space cotangent product of one sample (k = the
+// pixel p, 4 consecutive rows per 16-byte load, see DmaTileKOuter).  Each lane's (k-row, row
+// chunk) inside the tile is fixed, so its row part is computed once per tile; pixels past D and
+// padding taps read the zero page.
+// G of the sample: rows (o, c) of O*C (C % 4 == 0), element G[o, p, c].
+template <int ROWS, int WAVES>
+struct DmaCotangentKOuter {
+  using Tile = DmaTileKOuter<ROWS>;
+  const float* __restrict__ g;
+  const float* __restrict__ zero;
+  int rows, D, C;
+  FastDiv fC;
+  static constexpr int NI = ROWS / (8 * WAVES);
+  template <int WV>
+  static constexpr int OPS = ROWS / (8 * WV);
+  long long off[NI];
+  int kl[NI], ok[NI];
+  __device__ __forceinline__ void prepare(int row0, int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int o = (i * WAVES + wave) * 256 + 4 * lane;     // float offset in the tile
+      const int k = o / ROWS, pos = (o % ROWS) >> 2;
+      const int row = row0 + 4 * Tile::swz(k, pos);
+      const int rc = min(row, rows - 4);
+      const int oo = (int)fC.div(rc), cc = rc - oo * C;
+      off[i] = (long long)oo * D * C + cc;
+      kl[i] = k;
+      ok[i] = row < rows ? 1 : 0;
+    }
+  }
+  template <int WV>
+  __device__ __forceinline__ void issue(int k0, float* lds, int wave, int lane) const {
+    static_assert(WV == WAVES, "issuer built for this workgroup shape");
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int p = k0 + kl[i];
+      const float* src = (ok[i] & (p < D)) ? g + off[i] + (long long)p * C : zero;
+      float* dst = lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256);
+      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+    }
+  }
+};
+
+// Patches of the sample's layer input [H, W, C] (C % 4 == 0): rows (tap, ci) of 9*C.
+template <int ROWS, int WAVES>
+struct DmaPatchesKOuter {
+  using Tile = DmaTileKOuter<ROWS>;
+  const float* __restrict__ x;
+  const float* __restrict__ zero;
+  int rows, K, H, W, C;   // K = D pixels
+  FastDiv fW, fC;
+  static constexpr int NI = ROWS / (8 * WAVES);
+  template <int WV>
+  static constexpr int OPS = ROWS / (8 * WV);
+  int kl[NI], dy[NI], dx[NI], ci[NI], ok[NI];
+  __device__ __forceinline__ void prepare(int row0, int wave, int lane) {
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int o = (i * WAVES + wave) * 256 + 4 * lane;
+      const int k = o / ROWS, pos = (o % ROWS) >> 2;
+      const int row = row0 + 4 * Tile::swz(k, pos);
+      const int rc = min(row, rows - 4);
+      const int t = (int)fC.div(rc);
+      const int kh = (t * 11) >> 5, kw = t - 3 * kh;
+      kl[i] = k;
+      dy[i] = kh - 1;
+      dx[i] = kw - 1;
+      ci[i] = rc - t * C;
+      ok[i] = row < rows ? 1 : 0;
+    }
+  }
+  template <int WV>
+  __device__ __forceinline__ void issue(int k0, float* lds, int wave, int lane) const {
+    static_assert(WV == WAVES, "issuer built for this workgroup shape");
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int p = k0 + kl[i];
+      const int pc = min(p, K - 1);
+      const int y = (int)fW.div(pc), xx = pc - y * W;
+      const int yy = y + dy[i], xq = xx + dx[i];
+      const bool good = ok[i] & (p < K) & ((unsigned)yy < (unsigned)H) & ((unsigned)xq < (unsigned)W);
+      const float* src = good ? x + (long long)(yy * W + xq) * C + ci[i] : zero;
+      float* dst = lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256);
+      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+    }
+  }
+};
 
 // ------------------------------------------------------------------------------ forward
 template <class Cfg>
@@ -614,6 +703,47 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
   });
 }
 
+// direct-to-LDS form (C % 4 == 0 and Cin % 4 == 0): both operands K-outer, three LDS stages
+template <class Cfg>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, const float* __restrict__ zero,
+                 int O, int H, int W, int C, int Cin, FastDiv fC, FastDiv fW, FastDiv fCin,
+                 float* __restrict__ J, long long ldJ, long long off, int tiles_n) {
+  extern __shared__ float smem[];
+  const int s = blockIdx.y;
+  const int D = H * W;
+  const int KC = 9 * Cin;
+  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  DmaCotangentKOuter<Cfg::BM, Cfg::WAVES> ia;
+  ia.g = G + (long long)s * O * D * C;
+  ia.zero = zero;
+  ia.rows = O * C;
+  ia.D = D;
+  ia.C = C;
+  ia.fC = fC;
+  DmaPatchesKOuter<Cfg::BN, Cfg::WAVES> ib;
+  ib.x = h + (long long)s * D * Cin;
+  ib.zero = zero;
+  ib.rows = KC;
+  ib.K = D;
+  ib.H = H;
+  ib.W = W;
+  ib.C = Cin;
+  ib.fW = fW;
+  ib.fC = fCin;
+  f32x16 acc[Cfg::FM][Cfg::FN];
+  zero_acc<Cfg>(acc);
+  gemm_mainloop_dma_ops<Cfg, 3>(ia, ib, m0, n0, 0, D, smem, acc);
+  const int R = O * C;
+  for_each_acc<Cfg>(acc, m0, n0, [&](int r, int k, float v) {
+    if (r < R && k < KC) {
+      const int o = (int)fC.div(r), c = r - o * C;
+      J[((long long)s * O + o) * ldJ + off + (long long)c * KC + k] = v;
+    }
+  });
+}
+
 template <bool VEC>
 static hipError_t conv_wgrad_vec(hipStream_t s, const float* G, const float* h, int images, int O,
                                  int H, int W, int C, int Cin, float* J, long long ldJ, long long off) {
@@ -630,7 +760,19 @@ static hipError_t conv_wgrad_vec(hipStream_t s, const float* G, const float* h, 
 }
 
 hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
-                             int W, int C, int Cin, float* J, long long ldJ, long long off) {
+                             int W, int C, int Cin, float* J, long long ldJ, long long off, const float* zero) {
+  if (zero && C % 4 == 0 && Cin % 4 == 0 && aligned16(G) && aligned16(h)) {
+    using Cfg = CfgConv;
+    const int tn = cdiv(9 * Cin, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
+    constexpr int bytes = gemm_dma_smem_bytes<Cfg, 3>();
+    hipError_t e = hipFuncSetAttribute((const void*)k_conv_wgrad_dma<Cfg>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess) return e;
+    k_conv_wgrad_dma<Cfg><<<dim3(tm * tn, images), dim3(Cfg::THREADS), bytes, s>>>(
+        G, h, zero, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
+        ldJ, off, tn);
+    return hipGetLastError();
+  }
   if (C % 4 == 0 && Cin % 4 == 0 && aligned16(G) && aligned16(h))
     return conv_wgrad_vec<true>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
   return conv_wgrad_vec<false>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);

@@ -23,8 +23,9 @@ hipError_t launch_conv_flip(hipStream_t s, const float* K, int Cout, int Cin, fl
 hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
                            const float* Kt, int Cin, const float* dphi, float* out, const float* zero);
 // J[(s*O + o), off + c*9*Cin + k] = sum_p G[s, o, p, c] patch(h)[s, p, k] for every sample s.
+// `zero` as for launch_conv_fwd.
 hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
-                             int W, int C, int Cin, float* J, long long ldJ, long long off);
+                             int W, int C, int Cin, float* J, long long ldJ, long long off, const float* zero);
 // Deterministic split-K product J1 J2^T: plan, partial products, reduction into theta.
 int splitk_tile();
 // splits * R1 * R2 <= part_capacity (floats) always holds for the returned plan.

@@ -795,7 +795,8 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
       theta_written = true;
     } else {
       prof_begin(P, s, KC_CONV_WGRAD);
-      e = launch_conv_wgrad(s, Gcur, hptr(l), M, Oe, H, W, h->ch[l + 1], h->ch[l], J, Kcall, jo[l]);
+      e = launch_conv_wgrad(s, Gcur, hptr(l), M, Oe, H, W, h->ch[l + 1], h->ch[l], J, Kcall, jo[l],
+                            F(h->off_zero));
       prof_end(P, s, KC_CONV_WGRAD);
       if (e != hipSuccess) return hip_fail(h, e, "conv weight-space cotangent");
     }
@@ -1100,7 +1101,7 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
   for (int l = nc - 1; l >= 0; --l) {
     prof_begin(P, s, KC_CONV_WGRAD);
     e = launch_conv_wgrad(s, Gcur, hptr(l) + r2 * D * h->ch[l], n2, 1, H, W, h->ch[l + 1], h->ch[l], J,
-                          h->Ktot, h->joff[l]);
+                          h->Ktot, h->joff[l], F(h->off_zero));
     prof_end(P, s, KC_CONV_WGRAD);
     if (e != hipSuccess) return hip_fail(h, e, "conv weight cotangent");
     if (l >= 1) {
