@@ -86,6 +86,10 @@ struct ntk_handle {
   bool cnn = false;
   int max_n1 = 0, max_n2 = 0;
   hipStream_t stream = nullptr;
+  // a second stream of the library's own for the independent steps (weight transposes during
+  // the forward pass, layer-input Grams during the backward), joined back with events
+  hipStream_t aux = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_tr = nullptr, ev_fwd = nullptr, ev_gram = nullptr;
   int device = 0;
   char* ws = nullptr;
   size_t ws_bytes = 0;
@@ -307,6 +311,16 @@ static void plan_cnn(ntk_handle* h) {
   h->ws_bytes = off;
 }
 
+static void destroy_sync_objects(ntk_handle* h) {
+  if (h->aux) (void)hipStreamSynchronize(h->aux);
+  for (hipEvent_t* ev : {&h->ev_fork, &h->ev_tr, &h->ev_fwd, &h->ev_gram}) {
+    if (*ev) (void)hipEventDestroy(*ev);
+    *ev = nullptr;
+  }
+  if (h->aux) (void)hipStreamDestroy(h->aux);
+  h->aux = nullptr;
+}
+
 // ------------------------------------------------------------------------------ C ABI
 extern "C" int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, void* hip_stream,
                         ntk_handle** out) {
@@ -348,10 +362,19 @@ extern "C" int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, voi
     delete h;
     return fail(nullptr, NTK_E_OOM, "workspace allocation of " + std::to_string(bytes) + " bytes failed");
   }
+  if (hipStreamCreateWithFlags(&h->aux, hipStreamNonBlocking) != hipSuccess ||
+      hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&h->ev_tr, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&h->ev_fwd, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&h->ev_gram, hipEventDisableTiming) != hipSuccess) {
+    (void)hipGetLastError();
+    destroy_sync_objects(h);   // run everything on the one stream
+  }
   if (h->cnn) {
     e = hipMemsetAsync(h->ws + h->off_zero, 0, 256, h->stream);
     if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
     if (e != hipSuccess) {
+      destroy_sync_objects(h);
       (void)hipFree(h->ws);
       delete h;
       return hip_fail(nullptr, e, "clearing the zero page");
@@ -503,27 +526,78 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   const bool sym = h->opt_symmetric && X1 == X2 && n1 == n2;
   const int M = sym ? n1 : n1 + n2;
   hipStream_t s = h->stream;
+  // independent steps go to the library's second stream when it exists
+  hipStream_t sa = h->aux ? h->aux : s;
   Profiler* P = &h->prof;
   auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
   hipError_t e;
+  const bool logit = h->opt_output == NTK_OUTPUT_LOGIT;
+  const bool trace = h->opt_output == NTK_OUTPUT_TRACE;
+  const bool diag = h->opt_batch == NTK_BATCH_DIAGONAL;
+  const bool jc = h->opt_method == NTK_METHOD_JACOBIAN;
+  const int Oe = logit ? 1 : O;
+  for (int l = 0; l <= L; ++l)
+    if (!params[h->param_index[l]]) return fail(h, NTK_E_ARG, "null weight pointer");
+  // 0. weight transposes for the backward, on the second stream while the forward runs
+  if (h->aux) {
+    if ((e = hipEventRecord(h->ev_fork, s)) != hipSuccess || (e = hipStreamWaitEvent(sa, h->ev_fork, 0)) != hipSuccess)
+      return hip_fail(h, e, "stream fork");
+  }
+  for (int l = 1; l < L; ++l) {
+    prof_begin(P, sa, KC_TRANSPOSE);
+    e = launch_transpose(sa, params[h->param_index[l]], h->dims[l + 1], h->dims[l], F(h->off_Wt[l]));
+    prof_end(P, sa, KC_TRANSPOSE);
+    if (e != hipSuccess) return hip_fail(h, e, "weight transpose");
+  }
+  if (h->aux && (e = hipEventRecord(h->ev_tr, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
   // 1. forward pass keeping the layer inputs
   const float* h0 = nullptr;
   int rc0 = fcn_forward(h, params, X1, n1, X2, n2, sym, &h0);
   if (rc0 != NTK_OK) return rc0;
   auto hptr = [&](int l) -> const float* { return l == 0 ? h0 : F(h->off_h[l]); };
-  // 2. cotangents of every hidden pre-activation for all O outputs at once (for the one
-  //    logit o* alone in NTK_OUTPUT_LOGIT: the cotangent rows are then (n) instead of (n, o))
-  const bool logit = h->opt_output == NTK_OUTPUT_LOGIT;
-  const bool trace = h->opt_output == NTK_OUTPUT_TRACE;
-  const bool diag = h->opt_batch == NTK_BATCH_DIAGONAL;
-  const int Oe = logit ? 1 : O;
-  if (L >= 1) {
-    for (int l = 1; l < L; ++l) {
-      prof_begin(P, s, KC_TRANSPOSE);
-      e = launch_transpose(s, params[h->param_index[l]], h->dims[l + 1], h->dims[l], F(h->off_Wt[l]));
-      prof_end(P, s, KC_TRANSPOSE);
-      if (e != hipSuccess) return hip_fail(h, e, "weight transpose");
+  auto H2 = [&](int l) -> const float* { return sym ? hptr(l) : hptr(l) + (size_t)n1 * h->dims[l]; };
+  // 2. layer-input Grams (the x1.x2 scalars; per-sample scalars on the batch diagonal), on the
+  //    second stream while the backward runs
+  if (!jc) {
+    if (h->aux) {
+      if ((e = hipEventRecord(h->ev_fwd, s)) != hipSuccess || (e = hipStreamWaitEvent(sa, h->ev_fwd, 0)) != hipSuccess)
+        return hip_fail(h, e, "stream fork");
     }
+    if (diag) {
+      RowdotBatch rb{};
+      rb.count = L + 1;
+      for (int l = 0; l <= L; ++l) {
+        rb.a[l] = hptr(l);
+        rb.b[l] = H2(l);
+        rb.out[l] = F(h->off_gram[l]);
+        rb.K[l] = h->dims[l];
+        rb.beta[l] = h->layers[l].has_bias ? 1.0f : 0.0f;
+      }
+      prof_begin(P, sa, KC_GRAM);
+      e = launch_rowdot(sa, rb, n1);
+      prof_end(P, sa, KC_GRAM);
+      if (e != hipSuccess) return hip_fail(h, e, "diagonal layer-input scalars");
+    } else {
+      GramBatch gb{};
+      gb.count = L + 1;
+      for (int l = 0; l <= L; ++l) {
+        gb.h1[l] = hptr(l);
+        gb.h2[l] = H2(l);
+        gb.out[l] = F(h->off_gram[l]);
+        gb.K[l] = h->dims[l];
+        gb.beta[l] = h->layers[l].has_bias ? 1.0f : 0.0f;
+      }
+      prof_begin(P, sa, KC_GRAM);
+      e = launch_gram(sa, gb, n1, n2);
+      prof_end(P, sa, KC_GRAM);
+      if (e != hipSuccess) return hip_fail(h, e, "gram");
+    }
+    if (h->aux && (e = hipEventRecord(h->ev_gram, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
+  }
+  // 3. cotangents of every hidden pre-activation for all O outputs at once (for the one
+  //    logit o* alone in NTK_OUTPUT_LOGIT: the cotangent rows are then (n) instead of (n, o))
+  if (h->aux && (e = hipStreamWaitEvent(s, h->ev_tr, 0)) != hipSuccess) return hip_fail(h, e, "stream join");
+  if (L >= 1) {
     const float* WL = params[h->param_index[L]] + (logit ? (size_t)h->opt_logit * h->dims[L] : 0);
     prof_begin(P, s, KC_BWD_SEED);
     e = launch_bwd_seed(s, WL, F(h->off_dphi[L - 1]), M, Oe, h->dims[L], F(h->off_G[L - 1]));
@@ -537,11 +611,12 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
       if (e != hipSuccess) return hip_fail(h, e, "dense backward");
     }
   }
+  if (!jc && h->aux && (e = hipStreamWaitEvent(s, h->ev_gram, 0)) != hipSuccess)
+    return hip_fail(h, e, "stream join");
   auto G1 = [&](int l) -> const float* { return F(h->off_G[l]); };
   auto G2 = [&](int l) -> const float* {
     return sym ? F(h->off_G[l]) : F(h->off_G[l]) + (size_t)n1 * Oe * h->dims[l + 1];
   };
-  auto H2 = [&](int l) -> const float* { return sym ? hptr(l) : hptr(l) + (size_t)n1 * h->dims[l]; };
   const float rscale = trace ? (float)O : 1.f;   // sum over o of delta_{oo} for the trace
   if (h->opt_method == NTK_METHOD_JACOBIAN) {
     // Jacobian-contraction baseline: every weight tensor's explicit Jacobian block, chunk by
@@ -560,21 +635,8 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     return NTK_OK;
   }
   if (diag) {
-    // 3'. batch diagonal: per-sample layer-input scalars d_l[n] = h1_l[n] . h2_l[n] (+1), then
-    //     theta[n] = sum_l d_l[n] G1_l[n] G2_l[n]^T + d_L[n] I (traced: a dot of O*K_l columns)
-    RowdotBatch rb{};
-    rb.count = L + 1;
-    for (int l = 0; l <= L; ++l) {
-      rb.a[l] = hptr(l);
-      rb.b[l] = H2(l);
-      rb.out[l] = F(h->off_gram[l]);
-      rb.K[l] = h->dims[l];
-      rb.beta[l] = h->layers[l].has_bias ? 1.0f : 0.0f;
-    }
-    prof_begin(P, s, KC_GRAM);
-    e = launch_rowdot(s, rb, n1);
-    prof_end(P, s, KC_GRAM);
-    if (e != hipSuccess) return hip_fail(h, e, "diagonal layer-input scalars");
+    // batch diagonal: theta[n] = sum_l d_l[n] G1_l[n] G2_l[n]^T + d_L[n] I with the per-sample
+    // layer-input scalars d_l[n] = h1_l[n] . h2_l[n] (+1) (traced: a dot of O*K_l columns)
     DiagTerms t{};
     t.count = L;
     const bool flat = trace || logit;
@@ -592,20 +654,6 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     if (e != hipSuccess) return hip_fail(h, e, "diagonal contraction");
     return NTK_OK;
   }
-  // 3. layer-input Grams (the x1.x2 scalars), one batched launch
-  GramBatch gb{};
-  gb.count = L + 1;
-  for (int l = 0; l <= L; ++l) {
-    gb.h1[l] = hptr(l);
-    gb.h2[l] = H2(l);
-    gb.out[l] = F(h->off_gram[l]);
-    gb.K[l] = h->dims[l];
-    gb.beta[l] = h->layers[l].has_bias ? 1.0f : 0.0f;
-  }
-  prof_begin(P, s, KC_GRAM);
-  e = launch_gram(s, gb, n1, n2);
-  prof_end(P, s, KC_GRAM);
-  if (e != hipSuccess) return hip_fail(h, e, "gram");
   if (trace || logit) {
     // 4'. one output: per layer a split-K product of the cotangent rows (n) of Oe*K_l columns,
     //     weighted by gram_l and accumulated into theta [n1, n2] layer by layer
@@ -1200,6 +1248,7 @@ extern "C" int ntk_free(ntk_handle* h) {
   if (!h) return NTK_OK;
   (void)hipStreamSynchronize(h->stream);
   if (h->ws) (void)hipFree(h->ws);
+  destroy_sync_objects(h);
   if (h->jc_ws) (void)hipFree(h->jc_ws);
   if (h->vp_ws) (void)hipFree(h->vp_ws);
   delete h;

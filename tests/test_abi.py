@@ -65,6 +65,10 @@ def test_init_rejects_bad_models_before_any_device_call(lib):
 
     assert _init(lib, wl.fcn_spec("b", 8, [16], 3), 0, 4)[0] == _lib.NTK_E_ARG
 
+    # 64 hidden layers is the limit; 65 are refused before any device call
+    assert _init(lib, wl.fcn_spec("b", 8, [4] * 65, 3))[0] == _lib.NTK_E_UNSUPPORTED
+    assert "hidden layers" in _lib.last_error()
+
     desc = _lib.ntk_model_desc(0, None, 1, 1, 8, 3)
     h = ctypes.c_void_p()
     assert lib.ntk_init(ctypes.byref(desc), 4, 4, None, ctypes.byref(h)) == _lib.NTK_E_ARG
@@ -75,6 +79,7 @@ def test_null_handle_calls(lib):
     assert lib.ntk_free(None) == _lib.NTK_OK
     assert lib.ntk_compute(None, None, None, 1, None, 1, None) == _lib.NTK_E_ARG
     assert lib.ntk_set_option(None, 1, 1) == _lib.NTK_E_ARG
+    assert lib.ntk_vector_product(None, None, None, 1, None, 1, None, None) == _lib.NTK_E_ARG
     assert lib.ntk_workspace_bytes(None) == 0
     assert isinstance(lib.ntk_last_error(None), bytes)
 

@@ -101,6 +101,9 @@ EDGE = [
     ("two linear layers", wl.fcn_spec("e6", 6, [11], 5, act="none"), 7, 4),
     ("input size 3 (paper's FCN inputs), deep", wl.fcn_spec("e7", 3, [64] * 9, 10), 12, 12),
     ("tile-spanning R=N*O, erf", wl.fcn_spec("e8", 64, [96, 96], 10, act="erf"), 29, 41),
+    ("64 hidden layers (the maximum)", wl.fcn_spec("e9", 8, [16] * 64, 3, bias=True), 6, 5),
+    ("one hidden layer of width 8192", wl.fcn_spec("e10", 16, [8192], 10), 8, 7),
+    ("O=128 outputs", wl.fcn_spec("e11", 12, [40], 128, act="erf"), 6, 4),
 ]
 
 
