@@ -133,6 +133,13 @@ typedef struct ntk_handle ntk_handle;
 #define NTK_OPT_METHOD             6
 #define NTK_METHOD_STRUCTURED      0
 #define NTK_METHOD_JACOBIAN        1
+/* NTK_OPT_GRAPH: 1 = ntk_compute records its launches into a HIP graph on the first call and
+ * replays the graph on later calls with the same arguments (parameter, input and output
+ * pointers, batch sizes, options) -- the contents of the buffers may change; other arguments
+ * record a new graph.  Cuts the per-launch host overhead of small problems.  Not used while
+ * per-kernel timing is enabled or when the caller's stream is itself being captured.
+ * 0 (default) = launch eagerly.                                                           */
+#define NTK_OPT_GRAPH              7
 
 /*
  * ntk_init -- validate a model descriptor, plan and allocate the workspace.

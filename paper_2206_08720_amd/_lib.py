@@ -30,6 +30,7 @@ NTK_OPT_OUTPUT, NTK_OPT_LOGIT, NTK_OPT_BATCH = 3, 4, 5
 NTK_OUTPUT_FULL, NTK_OUTPUT_TRACE, NTK_OUTPUT_LOGIT = 0, 1, 2
 NTK_BATCH_FULL, NTK_BATCH_DIAGONAL = 0, 1
 NTK_OPT_METHOD, NTK_METHOD_STRUCTURED, NTK_METHOD_JACOBIAN = 6, 0, 1
+NTK_OPT_GRAPH = 7
 
 EXPORTED_SYMBOLS = ("ntk_init", "ntk_compute", "ntk_free", "ntk_last_error", "ntk_set_option",
                     "ntk_set_stream", "ntk_workspace_bytes", "ntk_profile_enable",

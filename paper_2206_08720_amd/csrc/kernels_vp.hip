@@ -79,4 +79,34 @@ hipError_t launch_gap_adjoint(hipStream_t s, const float* u, const float* dphi, 
   return hipGetLastError();
 }
 
+// dst = [a (na floats); b (nb floats)], one launch (the stacked batch [X1; X2]); float4 copies
+// when every pointer and both counts allow them.
+__global__ void __launch_bounds__(256)
+k_stack2(const float* __restrict__ a, long long na, const float* __restrict__ b, long long nb, int vec,
+         float* __restrict__ dst) {
+  const long long stride = (long long)gridDim.x * 256;
+  if (vec) {
+    const long long qa = na >> 2, qt = (na + nb) >> 2;
+    for (long long i = blockIdx.x * 256LL + threadIdx.x; i < qt; i += stride) {
+      const float4 v = i < qa ? reinterpret_cast<const float4*>(a)[i] : reinterpret_cast<const float4*>(b)[i - qa];
+      reinterpret_cast<float4*>(dst)[i] = v;
+    }
+  } else {
+    for (long long i = blockIdx.x * 256LL + threadIdx.x; i < na + nb; i += stride)
+      dst[i] = i < na ? a[i] : b[i - na];
+  }
+}
+
+hipError_t launch_stack2(hipStream_t s, const float* a, long long na, const float* b, long long nb,
+                         float* dst) {
+  const long long total = na + nb;
+  if (total <= 0) return hipSuccess;
+  const int vec = ((reinterpret_cast<uintptr_t>(a) | reinterpret_cast<uintptr_t>(b) |
+                    reinterpret_cast<uintptr_t>(dst)) & 15) == 0 && na % 4 == 0 && nb % 4 == 0;
+  const long long work = vec ? total / 4 : total;
+  const int blocks = (int)std::min<long long>((work + 255) / 256, 4096);
+  k_stack2<<<dim3(blocks), dim3(256), 0, s>>>(a, na, b, nb, vec, dst);
+  return hipGetLastError();
+}
+
 }  // namespace ntk

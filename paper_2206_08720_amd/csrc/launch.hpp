@@ -121,6 +121,9 @@ hipError_t launch_jc_dense(hipStream_t s, const float* G, long long ldG, const f
 // out[r, c] = (a[r, c] + b[r, c] + bias[c]) * dphi[r, c]; a, bias, dphi may be null.
 hipError_t launch_jvp_combine(hipStream_t s, const float* a, const float* b, const float* bias,
                               const float* dphi, int R, int C, float* out);
+// dst = [a (na floats); b (nb floats)] (stacking two batches, one launch).
+hipError_t launch_stack2(hipStream_t s, const float* a, long long na, const float* b, long long nb,
+                         float* dst);
 // out[c] = sum_r x[r, c] for x [R, C].
 hipError_t launch_colsum(hipStream_t s, const float* x, int R, int C, float* out);
 // out [n, D, C] = u[n, c] / D * dphi[n, p, c]  (adjoint of global average pooling, times act').

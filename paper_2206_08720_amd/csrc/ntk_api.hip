@@ -99,6 +99,15 @@ struct ntk_handle {
   int opt_logit = 0;
   int opt_batch = NTK_BATCH_FULL;
   int opt_method = NTK_METHOD_STRUCTURED;
+  int opt_graph = 0;
+  // NTK_OPT_GRAPH: the recorded graph and the arguments it was recorded with
+  hipGraphExec_t graph_exec = nullptr;
+  std::vector<uintptr_t> graph_key;
+  // graphs are recorded and replayed on a stream of the library's own (the caller's stream may
+  // be the null stream, which cannot be captured), ordered after/before the caller's stream by
+  // two events
+  hipStream_t gstream = nullptr;
+  hipEvent_t ev_gin = nullptr, ev_gout = nullptr;
   // Jacobian-contraction baseline: explicit Jacobian chunks of both batches and the split-K
   // partials of their product, allocated by the first call that needs them
   char* jc_ws = nullptr;
@@ -497,10 +506,7 @@ static int fcn_forward(ntk_handle* h, const float* const* params, const float* X
   *h0 = X1;
   if (!sym) {
     prof_begin(P, s, KC_COPY);
-    e = hipMemcpyAsync(F(h->off_h[0]), X1, sizeof(float) * (size_t)n1 * d0, hipMemcpyDeviceToDevice, s);
-    if (e == hipSuccess)
-      e = hipMemcpyAsync(F(h->off_h[0]) + (size_t)n1 * d0, X2, sizeof(float) * (size_t)n2 * d0,
-                         hipMemcpyDeviceToDevice, s);
+    e = launch_stack2(s, X1, (long long)n1 * d0, X2, (long long)n2 * d0, F(h->off_h[0]));
     prof_end(P, s, KC_COPY);
     if (e != hipSuccess) return hip_fail(h, e, "stacking X1/X2");
     *h0 = F(h->off_h[0]);
@@ -714,10 +720,7 @@ static int cnn_forward(ntk_handle* h, const float* const* params, const float* X
   *h0 = X1;
   if (!sym) {
     prof_begin(P, s, KC_COPY);
-    e = hipMemcpyAsync(F(h->off_ch[0]), X1, sizeof(float) * n1 * img_floats, hipMemcpyDeviceToDevice, s);
-    if (e == hipSuccess)
-      e = hipMemcpyAsync(F(h->off_ch[0]) + n1 * img_floats, X2, sizeof(float) * n2 * img_floats,
-                         hipMemcpyDeviceToDevice, s);
+    e = launch_stack2(s, X1, (long long)n1 * img_floats, X2, (long long)n2 * img_floats, F(h->off_ch[0]));
     prof_end(P, s, KC_COPY);
     if (e != hipSuccess) return hip_fail(h, e, "stacking X1/X2");
     *h0 = F(h->off_ch[0]);
@@ -1216,6 +1219,80 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
   return NTK_OK;
 }
 
+static int compute_eager(ntk_handle* h, const float* const* params, const float* X1, int n1, const float* X2,
+                         int n2, float* theta) {
+  if (h->cnn) return compute_cnn(h, params, X1, n1, X2, n2, theta);
+  return compute_fcn(h, params, X1, n1, X2, n2, theta);
+}
+
+static int param_tensor_count(const ntk_handle* h) {
+  if (h->cnn) return h->nc + 1;
+  int n = 0;
+  for (const auto& L : h->layers) n += 1 + (L.has_bias ? 1 : 0);
+  return n;
+}
+
+// NTK_OPT_GRAPH: replay the recorded graph when every argument and option matches, else record.
+static int compute_graph(ntk_handle* h, const float* const* params, const float* X1, int n1, const float* X2,
+                         int n2, float* theta) {
+  std::vector<uintptr_t> key;
+  const int np = param_tensor_count(h);
+  for (int i = 0; i < np; ++i) key.push_back(reinterpret_cast<uintptr_t>(params[i]));
+  for (uintptr_t v : {reinterpret_cast<uintptr_t>(X1), reinterpret_cast<uintptr_t>(X2),
+                      reinterpret_cast<uintptr_t>(theta), reinterpret_cast<uintptr_t>(h->stream)})
+    key.push_back(v);
+  for (int v : {n1, n2, h->opt_symmetric, h->opt_conv_order, h->opt_output, h->opt_logit, h->opt_batch,
+                h->opt_method})
+    key.push_back((uintptr_t)(unsigned)v);
+  hipError_t e;
+  if (!h->gstream) {
+    if ((e = hipStreamCreateWithFlags(&h->gstream, hipStreamNonBlocking)) != hipSuccess ||
+        (e = hipEventCreateWithFlags(&h->ev_gin, hipEventDisableTiming)) != hipSuccess ||
+        (e = hipEventCreateWithFlags(&h->ev_gout, hipEventDisableTiming)) != hipSuccess)
+      return hip_fail(h, e, "graph stream");
+  }
+  const hipStream_t user = h->stream;
+  // the graph's work starts after everything enqueued on the caller's stream so far
+  if ((e = hipEventRecord(h->ev_gin, user)) != hipSuccess ||
+      (e = hipStreamWaitEvent(h->gstream, h->ev_gin, 0)) != hipSuccess)
+    return hip_fail(h, e, "graph stream fork");
+  if (!(h->graph_exec && key == h->graph_key)) {
+    if (h->graph_exec) (void)hipGraphExecDestroy(h->graph_exec);
+    h->graph_exec = nullptr;
+    h->graph_key.clear();
+    if (h->opt_method == NTK_METHOD_JACOBIAN) {   // no allocation while recording
+      int rc = ensure_jc_workspace(h);
+      if (rc != NTK_OK) return rc;
+    }
+    // relaxed: the launchers set kernel attributes (LDS size), which is not a stream operation
+    if ((e = hipStreamBeginCapture(h->gstream, hipStreamCaptureModeRelaxed)) != hipSuccess)
+      return hip_fail(h, e, "graph capture");
+    h->stream = h->gstream;
+    const int rc = compute_eager(h, params, X1, n1, X2, n2, theta);
+    h->stream = user;
+    hipGraph_t g = nullptr;
+    e = hipStreamEndCapture(h->gstream, &g);
+    if (rc != NTK_OK) {
+      if (g) (void)hipGraphDestroy(g);
+      return rc;
+    }
+    if (e != hipSuccess) return hip_fail(h, e, "graph capture");
+    e = hipGraphInstantiate(&h->graph_exec, g, nullptr, nullptr, 0);
+    (void)hipGraphDestroy(g);
+    if (e != hipSuccess) {
+      h->graph_exec = nullptr;
+      return hip_fail(h, e, "graph instantiation");
+    }
+    h->graph_key = key;
+  }
+  if ((e = hipGraphLaunch(h->graph_exec, h->gstream)) != hipSuccess) return hip_fail(h, e, "graph launch");
+  // and the caller's later work waits for the graph
+  if ((e = hipEventRecord(h->ev_gout, h->gstream)) != hipSuccess ||
+      (e = hipStreamWaitEvent(user, h->ev_gout, 0)) != hipSuccess)
+    return hip_fail(h, e, "graph stream join");
+  return NTK_OK;
+}
+
 extern "C" int ntk_compute(ntk_handle* h, const float* const* params, const float* X1, int n1,
                            const float* X2, int n2, float* theta) {
   if (!h) return fail(nullptr, NTK_E_ARG, "handle is NULL");
@@ -1227,9 +1304,16 @@ extern "C" int ntk_compute(ntk_handle* h, const float* const* params, const floa
     return fail(h, NTK_E_ARG, "NTK_OPT_LOGIT must be below the number of outputs");
   if (h->opt_batch == NTK_BATCH_DIAGONAL && n1 != n2)
     return fail(h, NTK_E_ARG, "NTK_BATCH_DIAGONAL needs n1 == n2");
+  const int np = param_tensor_count(h);
+  for (int i = 0; i < np; ++i)
+    if (!params[i]) return fail(h, NTK_E_ARG, "null parameter pointer");
   h->err.clear();
-  if (h->cnn) return compute_cnn(h, params, X1, n1, X2, n2, theta);
-  return compute_fcn(h, params, X1, n1, X2, n2, theta);
+  if (h->opt_graph && !h->prof.enabled) {
+    hipStreamCaptureStatus st = hipStreamCaptureStatusNone;
+    if (hipStreamIsCapturing(h->stream, &st) == hipSuccess && st == hipStreamCaptureStatusNone)
+      return compute_graph(h, params, X1, n1, X2, n2, theta);
+  }
+  return compute_eager(h, params, X1, n1, X2, n2, theta);
 }
 
 extern "C" int ntk_vector_product(ntk_handle* h, const float* const* params, const float* X1, int n1,
@@ -1247,6 +1331,11 @@ extern "C" int ntk_vector_product(ntk_handle* h, const float* const* params, con
 extern "C" int ntk_free(ntk_handle* h) {
   if (!h) return NTK_OK;
   (void)hipStreamSynchronize(h->stream);
+  if (h->graph_exec) (void)hipGraphExecDestroy(h->graph_exec);
+  if (h->gstream) (void)hipStreamSynchronize(h->gstream);
+  if (h->ev_gin) (void)hipEventDestroy(h->ev_gin);
+  if (h->ev_gout) (void)hipEventDestroy(h->ev_gout);
+  if (h->gstream) (void)hipStreamDestroy(h->gstream);
   if (h->ws) (void)hipFree(h->ws);
   destroy_sync_objects(h);
   if (h->jc_ws) (void)hipFree(h->jc_ws);
@@ -1287,6 +1376,16 @@ extern "C" int ntk_set_option(ntk_handle* h, int option, int value) {
     if (value != NTK_METHOD_STRUCTURED && value != NTK_METHOD_JACOBIAN)
       return fail(h, NTK_E_ARG, "NTK_OPT_METHOD takes NTK_METHOD_STRUCTURED or NTK_METHOD_JACOBIAN");
     h->opt_method = value;
+    return NTK_OK;
+  }
+  if (option == NTK_OPT_GRAPH) {
+    if (value != 0 && value != 1) return fail(h, NTK_E_ARG, "NTK_OPT_GRAPH takes 0 or 1");
+    h->opt_graph = value;
+    if (!value && h->graph_exec) {
+      (void)hipGraphExecDestroy(h->graph_exec);
+      h->graph_exec = nullptr;
+      h->graph_key.clear();
+    }
     return NTK_OK;
   }
   if (option == NTK_OPT_BATCH) {
