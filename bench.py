@@ -57,6 +57,9 @@ def parse():
                     help="structured derivatives (default) or the Jacobian-contraction baseline")
     ap.add_argument("--op", default="ntk", choices=["ntk", "vp"],
                     help="ntk: Theta(X1, X2); vp: the NTK-vector product Theta(X1, X2) v")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the steps replayed from a HIP graph (NTK_OPT_GRAPH); the per-kernel "
+                         "timing then comes from as many further eager steps")
     ap.add_argument("--samples", type=int, default=0,
                     help="use only the first N samples of X1 and of X2 (0: the whole workload)")
     ap.add_argument("--cpu-samples", type=int, default=6,
@@ -184,26 +187,40 @@ def main():
         def step():
             h.compute(dev, x1, x2, out=out)
 
+    def timed(k, profiled):
+        """Run k steps between HIP events on the stream; (mean ms, sorted per-step ms, wall s,
+        per-kernel profile or None)."""
+        if profiled:
+            h.profile_read()                       # drop anything recorded so far
+            h.profile_enable(True)
+        torch.cuda.synchronize()
+        evs = [torch.cuda.Event(enable_timing=True) for _ in range(k + 1)]
+        t0 = time.perf_counter()
+        evs[0].record(stream)
+        for i in range(k):
+            step()
+            evs[i + 1].record(stream)
+        torch.cuda.synchronize()
+        wall_s = time.perf_counter() - t0
+        per = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(k))
+        prof_ = None
+        if profiled:
+            prof_ = h.profile_read()
+            h.profile_enable(False)
+        return evs[0].elapsed_time(evs[-1]) / k, per, wall_s, prof_
+
+    if args.graph:
+        h.set_option(_lib.NTK_OPT_GRAPH, 1)
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    h.profile_read()                       # drop anything recorded so far
-    h.profile_enable(True)
-    torch.cuda.synchronize()
-    evs = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps + 1)]
-    t0 = time.perf_counter()
-    evs[0].record(stream)
-    for i in range(args.steps):
+    ms, step_ms, wall, prof = timed(args.steps, profiled=not args.graph)
+    if args.graph:                             # per-kernel timing from eager steps
+        h.set_option(_lib.NTK_OPT_GRAPH, 0)
         step()
-        evs[i + 1].record(stream)
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
-    ms = evs[0].elapsed_time(evs[-1]) / args.steps
-    step_ms = sorted(evs[i].elapsed_time(evs[i + 1]) for i in range(args.steps))
+        _, _, _, prof = timed(args.steps, profiled=True)
     ms_median = step_ms[len(step_ms) // 2] if len(step_ms) % 2 else \
         0.5 * (step_ms[len(step_ms) // 2 - 1] + step_ms[len(step_ms) // 2])
-    prof = h.profile_read()
-    h.profile_enable(False)
 
     entries = ntk_entries(spec, n1, n2, args.output, args.batch)
     fl = ntk_flops(spec, n1, n2, symmetric=sym, output=args.output, batch=args.batch,
@@ -251,7 +268,7 @@ def main():
         "config": {"workload": name, "n1": n1, "n2": n2, "O": O,
                    "layers": [[L.get("in"), L.get("out"), L.get("act")] for L in spec["layers"]],
                    "symmetric_schedule": sym, "parallelism": "single GPU",
-                   "method": args.method, "op": args.op,
+                   "method": args.method, "op": args.op, "hip_graph": bool(args.graph),
                    "variant": {"output": args.output, "batch": args.batch,
                                **({"logit": args.logit} if args.output == "logit" else {})}},
         "tflops": tflops, "frac_of_fp32_mfma_peak": tflops / FP32_MFMA_PEAK_TFLOPS,

@@ -532,8 +532,12 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   const bool sym = h->opt_symmetric && X1 == X2 && n1 == n2;
   const int M = sym ? n1 : n1 + n2;
   hipStream_t s = h->stream;
-  // independent steps go to the library's second stream when it exists
-  hipStream_t sa = h->aux ? h->aux : s;
+  // independent steps go to the library's second stream when it exists and the problem is big
+  // enough for the overlap to outweigh the cross-stream synchronisation (a few microseconds)
+  double fwd_flops = 0;
+  for (int l = 0; l < L; ++l) fwd_flops += 2.0 * M * h->dims[l] * h->dims[l + 1];
+  hipStream_t aux = fwd_flops >= 1e7 ? h->aux : nullptr;
+  hipStream_t sa = aux ? aux : s;
   Profiler* P = &h->prof;
   auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
   hipError_t e;
@@ -545,7 +549,7 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   for (int l = 0; l <= L; ++l)
     if (!params[h->param_index[l]]) return fail(h, NTK_E_ARG, "null weight pointer");
   // 0. weight transposes for the backward, on the second stream while the forward runs
-  if (h->aux) {
+  if (aux) {
     if ((e = hipEventRecord(h->ev_fork, s)) != hipSuccess || (e = hipStreamWaitEvent(sa, h->ev_fork, 0)) != hipSuccess)
       return hip_fail(h, e, "stream fork");
   }
@@ -555,7 +559,7 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     prof_end(P, sa, KC_TRANSPOSE);
     if (e != hipSuccess) return hip_fail(h, e, "weight transpose");
   }
-  if (h->aux && (e = hipEventRecord(h->ev_tr, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
+  if (aux && (e = hipEventRecord(h->ev_tr, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
   // 1. forward pass keeping the layer inputs
   const float* h0 = nullptr;
   int rc0 = fcn_forward(h, params, X1, n1, X2, n2, sym, &h0);
@@ -565,7 +569,7 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   // 2. layer-input Grams (the x1.x2 scalars; per-sample scalars on the batch diagonal), on the
   //    second stream while the backward runs
   if (!jc) {
-    if (h->aux) {
+    if (aux) {
       if ((e = hipEventRecord(h->ev_fwd, s)) != hipSuccess || (e = hipStreamWaitEvent(sa, h->ev_fwd, 0)) != hipSuccess)
         return hip_fail(h, e, "stream fork");
     }
@@ -598,11 +602,11 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
       prof_end(P, sa, KC_GRAM);
       if (e != hipSuccess) return hip_fail(h, e, "gram");
     }
-    if (h->aux && (e = hipEventRecord(h->ev_gram, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
+    if (aux && (e = hipEventRecord(h->ev_gram, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
   }
   // 3. cotangents of every hidden pre-activation for all O outputs at once (for the one
   //    logit o* alone in NTK_OUTPUT_LOGIT: the cotangent rows are then (n) instead of (n, o))
-  if (h->aux && (e = hipStreamWaitEvent(s, h->ev_tr, 0)) != hipSuccess) return hip_fail(h, e, "stream join");
+  if (aux && (e = hipStreamWaitEvent(s, h->ev_tr, 0)) != hipSuccess) return hip_fail(h, e, "stream join");
   if (L >= 1) {
     const float* WL = params[h->param_index[L]] + (logit ? (size_t)h->opt_logit * h->dims[L] : 0);
     prof_begin(P, s, KC_BWD_SEED);
@@ -617,7 +621,7 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
       if (e != hipSuccess) return hip_fail(h, e, "dense backward");
     }
   }
-  if (!jc && h->aux && (e = hipStreamWaitEvent(s, h->ev_gram, 0)) != hipSuccess)
+  if (!jc && aux && (e = hipStreamWaitEvent(s, h->ev_gram, 0)) != hipSuccess)
     return hip_fail(h, e, "stream join");
   auto G1 = [&](int l) -> const float* { return F(h->off_G[l]); };
   auto G2 = [&](int l) -> const float* {
