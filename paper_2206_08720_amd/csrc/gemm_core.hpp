@@ -443,16 +443,21 @@ namespace ntk {
 namespace ntk {
 
 // ------------------------------------------------------------------------------ direct-to-LDS main loop
-// gfx950 loads global memory straight into LDS (global_load_lds_dwordx4): lane l of a wave
-// writes its 16 bytes at M0 + 16 l, so one instruction fills 1 KB of LDS with no register
+// gfx950 loads global memory straight into LDS (buffer_load_dwordx4 ... lds): lane l of a
+// wave writes its 16 bytes at M0 + 16 l, so one instruction fills 1 KB of LDS with no register
 // staging and no ds_write.  Tiles are stored unpadded, [rows][BK] with BK = 32 (8 chunks of
 // 16 bytes per row), and the chunk c of row r sits at position c ^ ((r >> 1) & 7): the 16
-// rows read by a ds_read_b128 then hit 16 distinct 16-byte bank groups.  Three LDS stages:
-// tile kt + 2 is in flight while tile kt is multiplied, one barrier per K tile.
+// rows read by a ds_read_b128 then hit 16 distinct 16-byte bank groups.  Two or three LDS
+// stages: the next tiles are in flight while tile kt is multiplied, one barrier per K tile.
+//
+// The row-major operands load through a buffer resource (MUBUF) rather than global_load_lds:
+// with a FLAT-encoded LDS load in flight the compiler makes every use of an LDS read wait for
+// all LDS reads of the wave, which defeats the fragment prefetch of the main loop.
 //
 // Requirements (checked by the host): both operands K-contiguous with 16-byte aligned rows
-// (LoadKInnerT<true> conditions) and K % 32 == 0.  Rows past the operand are read from the
-// last row (clamped): they only feed output rows/columns that are discarded.
+// (LoadKInnerT<true> conditions), K % 32 == 0, and a tile's rows spanning less than 2 GiB.
+// Rows past the operand are read from the last row (clamped): they only feed output
+// rows/columns that are discarded.
 constexpr int kDmaStages = 3;
 
 template <int ROWS>
@@ -460,24 +465,6 @@ struct DmaTile {
   static constexpr int BK = 32;
   static constexpr int FLOATS = ROWS * BK;
   __device__ static __forceinline__ int swz(int row, int chunk) { return chunk ^ ((row >> 1) & 7); }
-  // Issue this wave's share of the tile (rows split over the workgroup's waves, 8 rows per
-  // instruction).
-  template <int WAVES>
-  __device__ static __forceinline__ void issue(const float* __restrict__ p, long long ld, int rows,
-                                               int row0, int k0, float* lds, int wave, int lane) {
-    static_assert(ROWS % (8 * WAVES) == 0, "tile rows must split over the waves");
-#pragma unroll
-    for (int i = 0; i < ROWS / (8 * WAVES); ++i) {
-      const int r0 = (i * WAVES + wave) * 8;                 // first tile row of this instruction
-      const int r = r0 + (lane >> 3);
-      const int pos = lane & 7;
-      const int c = swz(r, pos);                              // global chunk stored at `pos`
-      const int gr = min(row0 + r, rows - 1);
-      const float* src = p + (long long)gr * ld + k0 + 4 * c;
-      float* dst = lds + __builtin_amdgcn_readfirstlane(r0 * BK);
-      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
-    }
-  }
   __device__ static __forceinline__ f32x4 frag(const float* lds, int row, int k) {
     return *reinterpret_cast<const f32x4*>(&lds[row * BK + (swz(row, k >> 2) << 2)]);
   }
@@ -507,59 +494,64 @@ struct DmaTileKOuter {
   }
 };
 
-template <class Cfg, class TA = DmaTile<Cfg::BM>, class TB = DmaTile<Cfg::BN>>
-__device__ __forceinline__ void mma_stage_dma(const float* As, const float* Bs,
-                                              f32x16 (&acc)[Cfg::FM][Cfg::FN], int wm0, int wn0,
-                                              int lane) {
-  const int lr = lane & 31, lk = (lane >> 5) * 4;
-  f32x4 a[2][Cfg::FM], b[2][Cfg::FN];
+// The MFMA work of one 32-wide K tile, cut into NB blocks.  The main loop reads a block's
+// operand fragments from LDS while the previous block's MFMAs run, also across the K tiles.
+template <class Cfg, class TA, class TB, class E>
+struct MmaBlocks;
+
+// fp32: four blocks of 8 k, each 4 MFMA steps of 32x32x2 on every 32x32 fragment of the wave.
+template <class Cfg, class TA, class TB>
+struct MmaBlocks<Cfg, TA, TB, f32x16> {
+  static constexpr int NB = 4;
+  struct Frag {
+    f32x4 a[Cfg::FM], b[Cfg::FN];
+  };
+  __device__ static __forceinline__ void load(const float* As, const float* Bs, int blk, int wm0, int wn0,
+                                              int lane, Frag& f) {
+    const int lr = lane & 31, k = blk * 8 + (lane >> 5) * 4;
 #pragma unroll
-  for (int fm = 0; fm < Cfg::FM; ++fm) a[0][fm] = TA::frag(As, wm0 + fm * 32 + lr, lk);
+    for (int fm = 0; fm < Cfg::FM; ++fm) f.a[fm] = TA::frag(As, wm0 + fm * 32 + lr, k);
 #pragma unroll
-  for (int fn = 0; fn < Cfg::FN; ++fn) b[0][fn] = TB::frag(Bs, wn0 + fn * 32 + lr, lk);
-#pragma unroll
-  for (int kk = 0; kk < 32; kk += 8) {
-    const int cur = (kk / 8) & 1;
-    if (kk + 8 < 32) {
-#pragma unroll
-      for (int fm = 0; fm < Cfg::FM; ++fm) a[cur ^ 1][fm] = TA::frag(As, wm0 + fm * 32 + lr, kk + 8 + lk);
-#pragma unroll
-      for (int fn = 0; fn < Cfg::FN; ++fn) b[cur ^ 1][fn] = TB::frag(Bs, wn0 + fn * 32 + lr, kk + 8 + lk);
-    }
+    for (int fn = 0; fn < Cfg::FN; ++fn) f.b[fn] = TB::frag(Bs, wn0 + fn * 32 + lr, k);
+  }
+  __device__ static __forceinline__ void mma(const Frag& f, f32x16 (&acc)[Cfg::FM][Cfg::FN]) {
 #pragma unroll
     for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int fm = 0; fm < Cfg::FM; ++fm)
 #pragma unroll
         for (int fn = 0; fn < Cfg::FN; ++fn)
-          acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x2f32(a[cur][fm][t], b[cur][fn][t], acc[fm][fn], 0, 0, 0);
-    __builtin_amdgcn_sched_barrier(0);
+          acc[fm][fn] = __builtin_amdgcn_mfma_f32_32x32x2f32(f.a[fm][t], f.b[fn][t], acc[fm][fn], 0, 0, 0);
   }
-}
+};
 
-// fp64 16x16x4 flavour of the stage (pre-activations of the forward pass), same tiles.
-template <class Cfg, class TA = DmaTile<Cfg::BM>, class TB = DmaTile<Cfg::BN>>
-__device__ __forceinline__ void mma_stage_dma(const float* As, const float* Bs,
-                                              f64x4 (&acc)[Cfg::FM16][Cfg::FN16], int wm0, int wn0,
-                                              int lane) {
-  const int lr = lane & 15, lk = (lane >> 4) * 4;
-#pragma unroll
-  for (int kk = 0; kk < 32; kk += 16) {
+// fp64 (pre-activations of the forward pass): two blocks of 16 k, each 4 MFMA steps of
+// 16x16x4 f64 on the fp32 tile values widened exactly.
+template <class Cfg, class TA, class TB>
+struct MmaBlocks<Cfg, TA, TB, f64x4> {
+  static constexpr int NB = 2;
+  struct Frag {
     f32x4 a[Cfg::FM16], b[Cfg::FN16];
+  };
+  __device__ static __forceinline__ void load(const float* As, const float* Bs, int blk, int wm0, int wn0,
+                                              int lane, Frag& f) {
+    const int lr = lane & 15, k = blk * 16 + (lane >> 4) * 4;
 #pragma unroll
-    for (int fm = 0; fm < Cfg::FM16; ++fm) a[fm] = TA::frag(As, wm0 + fm * 16 + lr, kk + lk);
+    for (int fm = 0; fm < Cfg::FM16; ++fm) f.a[fm] = TA::frag(As, wm0 + fm * 16 + lr, k);
 #pragma unroll
-    for (int fn = 0; fn < Cfg::FN16; ++fn) b[fn] = TB::frag(Bs, wn0 + fn * 16 + lr, kk + lk);
+    for (int fn = 0; fn < Cfg::FN16; ++fn) f.b[fn] = TB::frag(Bs, wn0 + fn * 16 + lr, k);
+  }
+  __device__ static __forceinline__ void mma(const Frag& f, f64x4 (&acc)[Cfg::FM16][Cfg::FN16]) {
 #pragma unroll
     for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int fm = 0; fm < Cfg::FM16; ++fm)
 #pragma unroll
         for (int fn = 0; fn < Cfg::FN16; ++fn)
-          acc[fm][fn] = __builtin_amdgcn_mfma_f64_16x16x4f64((double)a[fm][t], (double)b[fn][t],
+          acc[fm][fn] = __builtin_amdgcn_mfma_f64_16x16x4f64((double)f.a[fm][t], (double)f.b[fn][t],
                                                              acc[fm][fn], 0, 0, 0);
   }
-}
+};
 
 // s_waitcnt immediate (gfx9 encoding) that waits until at most n vector-memory operations of
 // this wave are outstanding and does not wait on the other counters.
@@ -572,39 +564,91 @@ __device__ __forceinline__ void wait_vmcnt_dyn(int n) {
   else __builtin_amdgcn_s_waitcnt(0x0F70);
 }
 
+// The same, and also until every LDS read of this wave has returned (lgkmcnt 0).
+__device__ __forceinline__ void wait_vmcnt_lgkm0_dyn(int n) {
+  if (n <= 0) __builtin_amdgcn_s_waitcnt(0x0070);
+  else if (n == 2) __builtin_amdgcn_s_waitcnt(0x0072);
+  else if (n == 4) __builtin_amdgcn_s_waitcnt(0x0074);
+  else if (n == 8) __builtin_amdgcn_s_waitcnt(0x0078);
+  else __builtin_amdgcn_s_waitcnt(0x0070);
+}
+
 template <class Cfg, int NSTAGE = kDmaStages>
 constexpr int gemm_dma_smem_bytes() {
   return NSTAGE * (DmaTile<Cfg::BM>::FLOATS + DmaTile<Cfg::BN>::FLOATS) * 4;
 }
 
+// Buffer resource (V#) of a raw byte range: base address, stride 0, num_records = `bytes`
+// (a load at or past it reads zeros), 32-bit data format.
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t buffer_rsrc(const void* base, uint32_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+// One 16-byte load per lane into LDS: lane l writes bytes [16 l, 16 l + 16) at `lds`, read
+// from byte offset voff + soff of the resource.
+__device__ __forceinline__ void buffer_dma16(__amdgpu_buffer_rsrc_t r, uint32_t voff, uint32_t soff,
+                                             float* lds) {
+  __builtin_amdgcn_raw_ptr_buffer_load_lds(r, (__attribute__((address_space(3))) void*)lds, 16, voff, soff, 0, 0);
+}
+
 // An operand of the direct-to-LDS loop is an "issuer": prepare(row0, wave, lane) once per
 // tile, then issue<WAVES>(k0, lds, wave, lane) per K tile, OPS<WAVES> instructions per wave.
-// DmaRowMajor: a K-contiguous row-major operand (the rows clamped to the last one).
-template <int ROWS>
+// DmaRowMajor: a K-contiguous row-major operand (the rows clamped to the last one), loaded by
+// WAVES waves, 8 rows per instruction.  The resource starts at the tile's first row; each
+// lane's byte offset inside it is fixed for the tile and the K position is the scalar offset.
+template <int ROWS, int WAVES>
 struct DmaRowMajor {
   using Tile = DmaTile<ROWS>;
+  static_assert(ROWS % (8 * WAVES) == 0, "tile rows must split over the waves");
+  static constexpr int NI = ROWS / (8 * WAVES);
+  template <int WV>
+  static constexpr int OPS = ROWS / (8 * WV);
   const float* __restrict__ p;
   long long ld;
   int rows;
-  int row0 = 0;
-  template <int WAVES>
-  static constexpr int OPS = ROWS / (8 * WAVES);
-  __device__ __forceinline__ void prepare(int r0, int, int) { row0 = r0; }
-  template <int WAVES>
-  __device__ __forceinline__ void issue(int k0, float* lds, int wave, int lane) const {
-    DmaTile<ROWS>::template issue<WAVES>(p, ld, rows, row0, k0, lds, wave, lane);
+  __amdgpu_buffer_rsrc_t rsrc;
+  uint32_t voff[NI];
+  __device__ __forceinline__ void prepare(int row0, int wave, int lane) {
+    const int span = min(rows - row0, ROWS);
+    rsrc = buffer_rsrc(p + (long long)row0 * ld, (uint32_t)((long long)span * ld * 4));
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int r = (i * WAVES + wave) * 8 + (lane >> 3);
+      const int c = Tile::swz(r, lane & 7);                  // global chunk stored at lane & 7
+      const int gr = min(r, span - 1);
+      voff[i] = (uint32_t)(((long long)gr * ld + 4 * c) * 4);
+    }
+  }
+  template <int WV>
+  __device__ __forceinline__ void issue(int k0, float* lds, int wave, int) const {
+    static_assert(WV == WAVES, "issuer built for this workgroup shape");
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      buffer_dma16(rsrc, voff[i], (uint32_t)k0 * 4u,
+                   lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 8 * Tile::BK));
   }
 };
 
+// Host check of the resource limit: a tile of `rows` rows of stride `ld` floats, read up to
+// column K, spans less than 2 GiB.
+__host__ inline bool dma_span_ok(long long ld, long long K, int rows) {
+  return (long long)rows * ld * 4 + K * 4 < (1LL << 31);
+}
+
 // K loop over [k_begin, k_end) (k_begin a multiple of 32; a ragged last K tile is the issuers'
 // business) for the tile (m0, n0), with NSTAGE LDS stages (2: tile kt+1 in flight during tile
-// kt; 3: tiles kt+1 and kt+2).  Ends with a barrier, so the caller may reuse `smem` afterwards.
+// kt; 3: tiles kt+1 and kt+2).  One barrier per K tile, placed before the tile's last MFMA
+// block: by then every wave holds that block's fragments in registers (so the stage may be
+// overwritten afterwards) and has seen its own loads of tile kt+1 land, and the fragments of
+// tile kt+1's first block are read while the last block's MFMAs run.  Ends with a barrier, so
+// the caller may reuse `smem` afterwards.
 template <class Cfg, int NSTAGE, class IA, class IB, class AccT>
 __device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, int n0, int k_begin, int k_end,
                                                       float* smem, AccT& acc) {
   static_assert(Cfg::BK == 32, "direct-to-LDS main loop uses BK = 32");
   using TA = typename IA::Tile;
   using TB = typename IB::Tile;
+  using MB = MmaBlocks<Cfg, TA, TB, std::remove_all_extents_t<AccT>>;
+  static_assert(MB::NB % 2 == 0, "fragment buffers alternate within a K tile");
   constexpr int STAGE = TA::FLOATS + TB::FLOATS;
   constexpr int PER_TILE = IA::template OPS<Cfg::WAVES> + IB::template OPS<Cfg::WAVES>;  // DMA ops per wave
   const int tid = threadIdx.x;
@@ -616,27 +660,43 @@ __device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, in
   static_assert(NSTAGE == 2 || NSTAGE == 3, "two or three LDS stages");
   ia.prepare(m0, wave, lane);
   ib.prepare(n0, wave, lane);
+  auto stage = [&](int kt) { return smem + (kt % NSTAGE) * STAGE; };
   auto issue = [&](int kt) {
-    float* st = smem + (kt % NSTAGE) * STAGE;
+    float* st = stage(kt);
     ia.template issue<Cfg::WAVES>(k_begin + kt * 32, st, wave, lane);
     ib.template issue<Cfg::WAVES>(k_begin + kt * 32, st + TA::FLOATS, wave, lane);
   };
   issue(0);
   if (NSTAGE == 3 && nk > 1) issue(1);
+  // tile 0 in LDS (with three stages tile 1's loads may stay in flight); a bare s_barrier (no
+  // fence, which would drain every outstanding load) makes it visible to every wave
+  wait_vmcnt_dyn(NSTAGE == 3 && nk > 1 ? PER_TILE : 0);
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_sched_barrier(0);
+  typename MB::Frag f[2];
+  MB::load(stage(0), stage(0) + TA::FLOATS, 0, wm0, wn0, lane, f[0]);
   for (int kt = 0; kt < nk; ++kt) {
-    // wait for this wave's loads of tile kt (with three stages tile kt+1's may stay in
-    // flight); a bare s_barrier (no fence, which would drain every outstanding load) then
-    // makes tile kt visible to every wave and guarantees all waves are done reading the stage
-    // that the next issue overwrites
-    if (NSTAGE == 3)
-      wait_vmcnt_dyn(kt + 1 < nk ? PER_TILE : 0);
-    else
-      wait_vmcnt_dyn(0);
-    __builtin_amdgcn_s_barrier();
-    __builtin_amdgcn_sched_barrier(0);
+    const float* st = stage(kt);
     if (kt + NSTAGE - 1 < nk) issue(kt + NSTAGE - 1);
-    const float* st = smem + (kt % NSTAGE) * STAGE;
-    mma_stage_dma<Cfg, TA, TB>(st, st + TA::FLOATS, acc, wm0, wn0, lane);
+#pragma unroll
+    for (int blk = 0; blk + 1 < MB::NB; ++blk) {
+      MB::load(st, st + TA::FLOATS, blk + 1, wm0, wn0, lane, f[(blk + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+      MB::mma(f[blk & 1], acc);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (kt + 1 < nk) {
+      // this wave's loads of tile kt+1 landed (with three stages tile kt+2's may stay in
+      // flight) and its reads of tile kt returned; after the barrier every wave's have
+      wait_vmcnt_lgkm0_dyn(NSTAGE == 3 && kt + 2 < nk ? PER_TILE : 0);
+      __builtin_amdgcn_s_barrier();
+      __builtin_amdgcn_sched_barrier(0);
+      const float* sn = stage(kt + 1);
+      MB::load(sn, sn + TA::FLOATS, 0, wm0, wn0, lane, f[0]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    MB::mma(f[(MB::NB - 1) & 1], acc);
+    __builtin_amdgcn_sched_barrier(0);
   }
   __syncthreads();
 }
@@ -647,8 +707,8 @@ __device__ __forceinline__ void gemm_mainloop_dma(const float* __restrict__ A, l
                                                   const float* __restrict__ B, long long ldb, int rowsB,
                                                   int m0, int n0, int k_begin, int k_end, float* smem,
                                                   AccT& acc) {
-  DmaRowMajor<Cfg::BM> ia{A, lda, rowsA};
-  DmaRowMajor<Cfg::BN> ib{B, ldb, rowsB};
+  DmaRowMajor<Cfg::BM, Cfg::WAVES> ia{A, lda, rowsA};
+  DmaRowMajor<Cfg::BN, Cfg::WAVES> ib{B, ldb, rowsB};
   gemm_mainloop_dma_ops<Cfg, NSTAGE>(ia, ib, m0, n0, k_begin, k_end, smem, acc);
 }
 

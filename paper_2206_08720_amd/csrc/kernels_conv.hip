@@ -319,9 +319,10 @@ static DmaPatches<ROWS, WAVES> dma_patches(const float* x, const float* zero, in
   return d;
 }
 
-// The direct-to-LDS path needs C % 32 == 0 and 16-byte aligned operands.
+// The direct-to-LDS path needs C % 32 == 0, 16-byte aligned operands and weight tiles within
+// the buffer-resource span.
 static bool conv_dma_ok(const void* x, int C, const void* K, const void* zero) {
-  return zero && C % 32 == 0 && aligned16(x) && aligned16(K);
+  return zero && C % 32 == 0 && aligned16(x) && aligned16(K) && dma_span_ok(9LL * C, 9LL * C, 256);
 }
 
 // K-outer direct-to-LDS operands of the weight-space cotangent product of one sample (k = the
@@ -437,7 +438,7 @@ __device__ __forceinline__ void conv_fwd_epilogue(f64x4 (&acc)[Cfg::FM16][Cfg::F
 // direct-to-LDS form (C % 32 == 0): patches gathered by the DMA, three LDS stages
 template <class Cfg>
 __global__ void __launch_bounds__(Cfg::THREADS)
-k_conv_fwd_dma(DmaPatches<Cfg::BM, Cfg::WAVES> pa, DmaRowMajor<Cfg::BN> pb, int K, int M, int N, int act,
+k_conv_fwd_dma(DmaPatches<Cfg::BM, Cfg::WAVES> pa, DmaRowMajor<Cfg::BN, Cfg::WAVES> pb, int K, int M, int N, int act,
                float* __restrict__ hn, float* __restrict__ dphi, int tiles_n) {
   extern __shared__ float smem[];
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
@@ -485,7 +486,7 @@ hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int
     const int M = images * H * W, Kd = 9 * Cin;
     const int tn = cdiv(Cout, Cfg::BN), tm = cdiv(M, Cfg::BM);
     auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(x, zero, images, H, W, Cin);
-    DmaRowMajor<Cfg::BN> pb{K, Kd, Cout};
+    DmaRowMajor<Cfg::BN, Cfg::WAVES> pb{K, Kd, Cout};
     constexpr int bytes = gemm_dma_smem_bytes<Cfg, 3>();
     hipError_t e = hipFuncSetAttribute((const void*)k_conv_fwd_dma<Cfg>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
@@ -601,7 +602,7 @@ k_conv_bwd(LoadPatchesKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restr
 // direct-to-LDS form (Cg % 32 == 0): the cotangent patches gathered by the DMA, 3 LDS stages
 template <class Cfg>
 __global__ void __launch_bounds__(Cfg::THREADS)
-k_conv_bwd_dma(DmaPatches<Cfg::BM, Cfg::WAVES> pa, DmaRowMajor<Cfg::BN> pb, int K,
+k_conv_bwd_dma(DmaPatches<Cfg::BM, Cfg::WAVES> pa, DmaRowMajor<Cfg::BN, Cfg::WAVES> pb, int K,
                const float* __restrict__ dphi, int R, int N, FastDiv fOD, FastDiv fD, float* __restrict__ out,
                int tiles_n) {
   extern __shared__ float smem[];
@@ -648,7 +649,7 @@ hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int
     const int R = images * O * D;
     const int tn = cdiv(Cin, Cfg::BN), tm = cdiv(R, Cfg::BM);
     auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(G, zero, images * O, H, W, Cg);
-    DmaRowMajor<Cfg::BN> pb{Kt, Kd, Cin};
+    DmaRowMajor<Cfg::BN, Cfg::WAVES> pb{Kt, Kd, Cin};
     constexpr int bytes = gemm_dma_smem_bytes<Cfg, 3>();
     hipError_t e = hipFuncSetAttribute((const void*)k_conv_bwd_dma<Cfg>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);

@@ -165,7 +165,7 @@ hipError_t launch_dense_fwd(hipStream_t s, const float* h, const float* W, const
                             int N, int K, int act, float* hn, float* dphi, double* part,
                             long long part_capacity) {
   const bool v = vec_ok(h, K, K) && vec_ok(W, K, K);
-  if (v && K % 32 == 0)
+  if (v && K % 32 == 0 && dma_span_ok(K, K, 256))
     return dense_fwd_cfg<CfgFwd64, true, true>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity);
   if (v) return dense_fwd_cfg<CfgFwd64, true>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity);
   return dense_fwd_cfg<CfgFwd64, false>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity);
@@ -236,7 +236,7 @@ hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, cons
   const long long big_tiles = (long long)cdiv(R, 128) * cdiv(N, 128);
   const bool v = vec_ok(G, K, K) && vec_ok(Wt, K, K);
   if (big_tiles >= 512) {
-    if (v && K % 32 == 0) return dense_bwd_cfg<CfgBig8, true, true>(s, G, Wt, dphi, R, N, K, O, out);
+    if (v && K % 32 == 0 && dma_span_ok(K, K, 256)) return dense_bwd_cfg<CfgBig8, true, true>(s, G, Wt, dphi, R, N, K, O, out);
     return v ? dense_bwd_cfg<CfgBig8, true>(s, G, Wt, dphi, R, N, K, O, out)
              : dense_bwd_cfg<CfgBig8, false>(s, G, Wt, dphi, R, N, K, O, out);
   }
@@ -617,7 +617,7 @@ hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2
     return hipGetLastError();
   };
   bool dma = v;
-  for (int l = 0; l < c.L; ++l) dma = dma && c.K[l] % 32 == 0;
+  for (int l = 0; l < c.L; ++l) dma = dma && c.K[l] % 32 == 0 && dma_span_ok(c.K[l], c.K[l], 256);
   auto go_sk = [&](auto vec_tag, auto dma_tag) -> hipError_t {
     using Cfg = CfgSK;
     constexpr bool VEC = decltype(vec_tag)::value;
