@@ -256,28 +256,31 @@ static LoadPatchesKInnerT<VEC> patches_kinner(const float* x, int images, int H,
 
 // Patch matrix of an NHWC batch as a direct-to-LDS operand (see DmaTile): row = img*D + p,
 // column k = tap*C + ci with C % 32 == 0, so the 32 columns of a K tile lie inside one tap.
-// Every lane loads 16 bytes of one row; a tap that falls outside the image (the zero padding)
-// reads a page of zeros instead.  The rows' pixels are computed once per tile (prepare).
+// Every lane loads 16 bytes of one row through a buffer resource over the whole batch (less
+// than 2 GiB); a tap that falls outside the image (the zero padding) takes an offset past the
+// resource, which reads zeros.  The rows' pixels are computed once per tile (prepare).
+constexpr uint32_t kDmaPastEnd = 0x80000000u;   // past every resource: the load reads zeros
+
 template <int ROWS, int WAVES>
 struct DmaPatches {
   using Tile = DmaTile<ROWS>;
   const float* __restrict__ x;
-  const float* __restrict__ zero;   // >= 16 bytes of zeros, 16-byte aligned
   int rows, H, W, C;
   FastDiv fD, fW, fC;
   static constexpr int NI = ROWS / (8 * WAVES);
   template <int WV>
   static constexpr int OPS = ROWS / (8 * WV);
-  long long base[NI];
-  int y[NI], xx[NI], ok[NI];
+  __amdgpu_buffer_rsrc_t rsrc;
+  int base[NI], y[NI], xx[NI], ok[NI];
   __device__ __forceinline__ void prepare(int row0, int wave, int lane) {
+    rsrc = buffer_rsrc(x, (uint32_t)((long long)rows * C * 4));
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int row = row0 + (i * WAVES + wave) * 8 + (lane >> 3);
       const int rc = min(row, rows - 1);
       const int img = (int)fD.div(rc), p = rc - img * (int)fD.d;
       const int yy = (int)fW.div(p), xq = p - yy * W;
-      base[i] = (((long long)img * H + yy) * W + xq) * C;
+      base[i] = ((img * H + yy) * W + xq) * C;
       y[i] = yy;
       xx[i] = xq;
       ok[i] = row < rows ? 1 : 0;
@@ -296,19 +299,16 @@ struct DmaPatches {
       const int c = DmaTile<ROWS>::swz(r, lane & 7);
       const int yy = y[i] + kh - 1, xq = xx[i] + kw - 1;
       const bool good = ok[i] & ((unsigned)yy < (unsigned)H) & ((unsigned)xq < (unsigned)W);
-      const float* src = good ? x + base[i] + tapoff + 4 * c : zero;
-      float* dst = lds + __builtin_amdgcn_readfirstlane(r0 * DmaTile<ROWS>::BK);
-      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+      const uint32_t voff = good ? (uint32_t)(base[i] + tapoff + 4 * c) * 4u : kDmaPastEnd;
+      buffer_dma16(rsrc, voff, 0, lds + __builtin_amdgcn_readfirstlane(r0 * DmaTile<ROWS>::BK));
     }
   }
 };
 
 template <int ROWS, int WAVES>
-static DmaPatches<ROWS, WAVES> dma_patches(const float* x, const float* zero, int images, int H, int W,
-                                           int C) {
+static DmaPatches<ROWS, WAVES> dma_patches(const float* x, int images, int H, int W, int C) {
   DmaPatches<ROWS, WAVES> d;
   d.x = x;
-  d.zero = zero;
   d.rows = images * H * W;
   d.H = H;
   d.W = W;
@@ -319,30 +319,31 @@ static DmaPatches<ROWS, WAVES> dma_patches(const float* x, const float* zero, in
   return d;
 }
 
-// The direct-to-LDS path needs C % 32 == 0, 16-byte aligned operands and weight tiles within
-// the buffer-resource span.
-static bool conv_dma_ok(const void* x, int C, const void* K, const void* zero) {
-  return zero && C % 32 == 0 && aligned16(x) && aligned16(K) && dma_span_ok(9LL * C, 9LL * C, 256);
+// The direct-to-LDS path needs C % 32 == 0, 16-byte aligned operands, an activation batch of
+// `elems` floats and weight tiles within the buffer-resource span.
+static bool conv_dma_ok(const void* x, long long elems, int C, const void* K) {
+  return C % 32 == 0 && aligned16(x) && aligned16(K) && elems * 4 < (1LL << 31) &&
+         dma_span_ok(9LL * C, 9LL * C, 256);
 }
 
 // K-outer direct-to-LDS operands of the weight-space cotangent product of one sample (k = the
-// pixel p, 4 consecutive rows per 16-byte load, see DmaTileKOuter).  Each lane's (k-row, row
-// chunk) inside the tile is fixed, so its row part is computed once per tile; pixels past D and
-// padding taps read the zero page.
+// pixel p, 4 consecutive rows per 16-byte load, see DmaTileKOuter), through a buffer resource
+// over the sample's tensor.  Each lane's (k-row, row chunk) inside the tile is fixed, so its row
+// part is computed once per tile; pixels past D and padding taps read past the resource (zeros).
 // G of the sample: rows (o, c) of O*C (C % 4 == 0), element G[o, p, c].
 template <int ROWS, int WAVES>
 struct DmaCotangentKOuter {
   using Tile = DmaTileKOuter<ROWS>;
   const float* __restrict__ g;
-  const float* __restrict__ zero;
   int rows, D, C;
   FastDiv fC;
   static constexpr int NI = ROWS / (8 * WAVES);
   template <int WV>
   static constexpr int OPS = ROWS / (8 * WV);
-  long long off[NI];
-  int kl[NI], ok[NI];
+  __amdgpu_buffer_rsrc_t rsrc;
+  int off[NI], kl[NI], ok[NI];
   __device__ __forceinline__ void prepare(int row0, int wave, int lane) {
+    rsrc = buffer_rsrc(g, (uint32_t)((long long)rows * D * 4));
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int o = (i * WAVES + wave) * 256 + 4 * lane;     // float offset in the tile
@@ -350,7 +351,7 @@ struct DmaCotangentKOuter {
       const int row = row0 + 4 * Tile::swz(k, pos);
       const int rc = min(row, rows - 4);
       const int oo = (int)fC.div(rc), cc = rc - oo * C;
-      off[i] = (long long)oo * D * C + cc;
+      off[i] = oo * D * C + cc;
       kl[i] = k;
       ok[i] = row < rows ? 1 : 0;
     }
@@ -361,9 +362,8 @@ struct DmaCotangentKOuter {
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int p = k0 + kl[i];
-      const float* src = (ok[i] & (p < D)) ? g + off[i] + (long long)p * C : zero;
-      float* dst = lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256);
-      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+      const uint32_t voff = (ok[i] & (p < D)) ? (uint32_t)(off[i] + p * C) * 4u : kDmaPastEnd;
+      buffer_dma16(rsrc, voff, 0, lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256));
     }
   }
 };
@@ -373,14 +373,15 @@ template <int ROWS, int WAVES>
 struct DmaPatchesKOuter {
   using Tile = DmaTileKOuter<ROWS>;
   const float* __restrict__ x;
-  const float* __restrict__ zero;
   int rows, K, H, W, C;   // K = D pixels
   FastDiv fW, fC;
   static constexpr int NI = ROWS / (8 * WAVES);
   template <int WV>
   static constexpr int OPS = ROWS / (8 * WV);
+  __amdgpu_buffer_rsrc_t rsrc;
   int kl[NI], dy[NI], dx[NI], ci[NI], ok[NI];
   __device__ __forceinline__ void prepare(int row0, int wave, int lane) {
+    rsrc = buffer_rsrc(x, (uint32_t)((long long)K * C * 4));
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int o = (i * WAVES + wave) * 256 + 4 * lane;
@@ -406,9 +407,8 @@ struct DmaPatchesKOuter {
       const int y = (int)fW.div(pc), xx = pc - y * W;
       const int yy = y + dy[i], xq = xx + dx[i];
       const bool good = ok[i] & (p < K) & ((unsigned)yy < (unsigned)H) & ((unsigned)xq < (unsigned)W);
-      const float* src = good ? x + (long long)(yy * W + xq) * C + ci[i] : zero;
-      float* dst = lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256);
-      __builtin_amdgcn_global_load_lds(src, (__attribute__((address_space(3))) void*)dst, 16, 0, 0);
+      const uint32_t voff = good ? (uint32_t)((yy * W + xq) * C + ci[i]) * 4u : kDmaPastEnd;
+      buffer_dma16(rsrc, voff, 0, lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256));
     }
   }
 };
@@ -480,12 +480,12 @@ static hipError_t conv_fwd_vec(hipStream_t s, const float* x, int images, int H,
 }
 
 hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int W, int Cin,
-                           const float* K, int Cout, int act, float* hn, float* dphi, const float* zero) {
-  if (conv_dma_ok(x, Cin, K, zero)) {
+                           const float* K, int Cout, int act, float* hn, float* dphi) {
+  if (conv_dma_ok(x, (long long)images * H * W * Cin, Cin, K)) {
     using Cfg = CfgConvF64;
     const int M = images * H * W, Kd = 9 * Cin;
     const int tn = cdiv(Cout, Cfg::BN), tm = cdiv(M, Cfg::BM);
-    auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(x, zero, images, H, W, Cin);
+    auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(x, images, H, W, Cin);
     DmaRowMajor<Cfg::BN, Cfg::WAVES> pb{K, Kd, Cout};
     constexpr int bytes = gemm_dma_smem_bytes<Cfg, 3>();
     hipError_t e = hipFuncSetAttribute((const void*)k_conv_fwd_dma<Cfg>,
@@ -642,13 +642,13 @@ static hipError_t conv_bwd_vec(hipStream_t s, const float* G, int images, int O,
 }
 
 hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
-                           const float* Kt, int Cin, const float* dphi, float* out, const float* zero) {
-  if (conv_dma_ok(G, Cg, Kt, zero)) {
+                           const float* Kt, int Cin, const float* dphi, float* out) {
+  if (conv_dma_ok(G, (long long)images * O * H * W * Cg, Cg, Kt)) {
     using Cfg = CfgConv;
     const int D = H * W, Kd = 9 * Cg;
     const int R = images * O * D;
     const int tn = cdiv(Cin, Cfg::BN), tm = cdiv(R, Cfg::BM);
-    auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(G, zero, images * O, H, W, Cg);
+    auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(G, images * O, H, W, Cg);
     DmaRowMajor<Cfg::BN, Cfg::WAVES> pb{Kt, Kd, Cin};
     constexpr int bytes = gemm_dma_smem_bytes<Cfg, 3>();
     hipError_t e = hipFuncSetAttribute((const void*)k_conv_bwd_dma<Cfg>,
@@ -707,8 +707,7 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
 // direct-to-LDS form (C % 4 == 0 and Cin % 4 == 0): both operands K-outer, three LDS stages
 template <class Cfg>
 __global__ void __launch_bounds__(Cfg::THREADS)
-k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, const float* __restrict__ zero,
-                 int O, int H, int W, int C, int Cin, FastDiv fC, FastDiv fW, FastDiv fCin,
+k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O, int H, int W, int C, int Cin, FastDiv fC, FastDiv fW, FastDiv fCin,
                  float* __restrict__ J, long long ldJ, long long off, int tiles_n) {
   extern __shared__ float smem[];
   const int s = blockIdx.y;
@@ -718,14 +717,12 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, const
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   DmaCotangentKOuter<Cfg::BM, Cfg::WAVES> ia;
   ia.g = G + (long long)s * O * D * C;
-  ia.zero = zero;
   ia.rows = O * C;
   ia.D = D;
   ia.C = C;
   ia.fC = fC;
   DmaPatchesKOuter<Cfg::BN, Cfg::WAVES> ib;
   ib.x = h + (long long)s * D * Cin;
-  ib.zero = zero;
   ib.rows = KC;
   ib.K = D;
   ib.H = H;
@@ -761,8 +758,10 @@ static hipError_t conv_wgrad_vec(hipStream_t s, const float* G, const float* h, 
 }
 
 hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
-                             int W, int C, int Cin, float* J, long long ldJ, long long off, const float* zero) {
-  if (zero && C % 4 == 0 && Cin % 4 == 0 && aligned16(G) && aligned16(h)) {
+                             int W, int C, int Cin, float* J, long long ldJ, long long off) {
+  // direct-to-LDS: one sample's cotangents and layer input each within a buffer resource
+  if (C % 4 == 0 && Cin % 4 == 0 && aligned16(G) && aligned16(h) && (long long)O * H * W * C * 4 < (1LL << 31) &&
+      (long long)H * W * Cin * 4 < (1LL << 31)) {
     using Cfg = CfgConv;
     const int tn = cdiv(9 * Cin, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
     constexpr int bytes = gemm_dma_smem_bytes<Cfg, 3>();
@@ -770,7 +769,7 @@ hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int 
                                        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (e != hipSuccess) return e;
     k_conv_wgrad_dma<Cfg><<<dim3(tm * tn, images), dim3(Cfg::THREADS), bytes, s>>>(
-        G, h, zero, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
+        G, h, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
         ldJ, off, tn);
     return hipGetLastError();
   }

@@ -245,24 +245,37 @@ hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, cons
 }
 
 // ------------------------------------------------------------------------------ seed, transpose
-__global__ void k_bwd_seed(const float* __restrict__ W, const float* __restrict__ dphi, int M,
-                           int O, int C, float* __restrict__ G) {
-  const long long total = (long long)M * O * C;
-  for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
-       i += (long long)gridDim.x * blockDim.x) {
-    const int c = (int)(i % C);
-    const long long mo = i / C;
-    const int o = (int)(mo % O);
-    const long long m = mo / O;
-    G[i] = W[(long long)o * C + c] * dphi[m * C + c];
+// G[(m, o), c] = W[o, c] * dphi[m, c]: one workgroup per sample row m, float4 columns when
+// `vec` (C % 4 == 0, 16-byte aligned buffers).
+__global__ void __launch_bounds__(256)
+k_bwd_seed(const float* __restrict__ W, const float* __restrict__ dphi, int M, int O, int C, int vec,
+           float* __restrict__ G) {
+  for (int m = blockIdx.x; m < M; m += gridDim.x) {
+    const float* dm = dphi + (long long)m * C;
+    float* gm = G + (long long)m * O * C;
+    if (vec) {
+      const int C4 = C >> 2;
+      for (int c4 = threadIdx.x; c4 < C4; c4 += blockDim.x) {
+        const float4 d = reinterpret_cast<const float4*>(dm)[c4];
+        for (int o = 0; o < O; ++o) {
+          const float4 w = reinterpret_cast<const float4*>(W + (long long)o * C)[c4];
+          reinterpret_cast<float4*>(gm + (long long)o * C)[c4] = make_float4(w.x * d.x, w.y * d.y, w.z * d.z, w.w * d.w);
+        }
+      }
+    } else {
+      for (int c = threadIdx.x; c < C; c += blockDim.x) {
+        const float d = dm[c];
+        for (int o = 0; o < O; ++o) gm[(long long)o * C + c] = W[(long long)o * C + c] * d;
+      }
+    }
   }
 }
 
 hipError_t launch_bwd_seed(hipStream_t s, const float* W, const float* dphi, int M, int O, int C,
                            float* G) {
-  const long long total = (long long)M * O * C;
-  const int blocks = (int)std::min<long long>((total + 255) / 256, 256 * 64);
-  k_bwd_seed<<<dim3(blocks), dim3(256), 0, s>>>(W, dphi, M, O, C, G);
+  if (M <= 0 || O <= 0 || C <= 0) return hipSuccess;
+  const int vec = vec_ok(W, C, C) && vec_ok(dphi, C, C) && vec_ok(G, C, C);
+  k_bwd_seed<<<dim3(std::min(M, 65535)), dim3(256), 0, s>>>(W, dphi, M, O, C, vec, G);
   return hipGetLastError();
 }
 
@@ -450,7 +463,7 @@ template <class Cfg, bool VEC, bool DMA>
 __device__ __forceinline__ void fcn_tile_layers(const FcnContraction& c, int l0, int l1, int N2,
                                                 FastDiv fO, int R1, int R2, int m0, int n0,
                                                 float* smem, f32x16 (&tot)[Cfg::FM][Cfg::FN]) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lane_id = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM, wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
   for (int l = l0; l < l1; ++l) {
     const int K = c.K[l];
@@ -465,6 +478,11 @@ __device__ __forceinline__ void fcn_tile_layers(const FcnContraction& c, int l0,
     }
     int n1lo, n2lo, S2;
     stage_gram<Cfg>(c.gram[l], N2, R1, R2, fO, m0, n0, smem, n1lo, n2lo, S2);
+    // The Gram addresses below do not change from layer to layer; computed once they would
+    // hold ~30 registers through the main loop.  An opaque copy of the lane index keeps
+    // them inside the epilogue.
+    int lane = lane_id;
+    asm volatile("" : "+v"(lane));
 #pragma unroll
     for (int fn = 0; fn < Cfg::FN; ++fn) {
       const int sc = min(n0 + wn0 + fn * 32 + (lane & 31), R2 - 1);
@@ -497,24 +515,24 @@ k_ntk_fcn_sk(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float*
   const SkShare sh = sk_share(x, T, P8, L);
   const int O = (int)fO.d;
   const int R1 = N1 * O, R2 = N2 * O;
-  // data-parallel rounds over the XCD's tiles
-  for (int i = 0; i < sh.rounds; ++i) {
-    int tm, tn;
-    tile_coords(sh.base + i * P8 + j, symmetric, tiles_m, tiles_n, tm, tn);
-    const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
-    f32x16 tot[Cfg::FM][Cfg::FN];
-    zero_acc<Cfg>(tot);
-    fcn_tile_layers<Cfg, VEC, DMA>(c, 0, L, N2, fO, R1, R2, m0, n0, smem, tot);
-    fcn_tile_out<Cfg>(tot, c.gram_readout, c.readout_scale, N1, N2, fO, R1, R2, m0, n0, symmetric && tm != tn, smem, theta);
-  }
-  // stream-K over the XCD's remaining tiles
+  // The XCD's data-parallel rounds (whole tiles), then its stream-K range of (tile, layer)
+  // units, as one loop so that the main loop is instantiated once.
   const long long beg = sk_start(j, sh.U, P8), end = sk_start(j + 1, sh.U, P8);
-  for (long long u = beg; u < end;) {
-    const int ts = (int)(u / L);
-    const int l0 = (int)(u - (long long)ts * L);
-    const int l1 = (int)min((long long)L, l0 + (end - u));
+  int i = 0;
+  long long u = beg;
+  while (true) {
+    int t, ts = 0, l0 = 0, l1 = L;
+    if (i < sh.rounds) {
+      t = sh.base + i * P8 + j;
+    } else {
+      if (u >= end) break;
+      ts = (int)(u / L);
+      l0 = (int)(u - (long long)ts * L);
+      l1 = (int)min((long long)L, l0 + (end - u));
+      t = sh.first_sk + ts;
+    }
     int tm, tn;
-    tile_coords(sh.first_sk + ts, symmetric, tiles_m, tiles_n, tm, tn);
+    tile_coords(t, symmetric, tiles_m, tiles_n, tm, tn);
     const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
     f32x16 tot[Cfg::FM][Cfg::FN];
     zero_acc<Cfg>(tot);
@@ -524,9 +542,12 @@ k_ntk_fcn_sk(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float*
                         theta);
     } else {
       float* dst = part + ((long long)lam * 2 + sk_slot(beg, L, ts)) * (Cfg::BM * Cfg::BN);
-      for_each_acc<Cfg>(tot, 0, 0, [&](int ii, int jj, float v) { dst[ii * Cfg::BN + jj] = v; });
+      int z = 0;   // opaque zero: keeps the 32 store offsets from being computed up front
+      asm volatile("" : "+v"(z));
+      for_each_acc<Cfg>(tot, z, z, [&](int ii, int jj, float v) { dst[ii * Cfg::BN + jj] = v; });
     }
-    u += l1 - l0;
+    if (i < sh.rounds) ++i;
+    else u += l1 - l0;
   }
 }
 

@@ -7,10 +7,9 @@
 namespace ntk {
 
 // hn/dphi [images, H, W, Cout] = act / act' of the SAME 3x3 convolution of x [images, H, W, Cin]
-// with K [Cout, 3, 3, Cin] (fp64 accumulation).  `zero`: 16-byte aligned page of >= 16 zero
-// bytes read for the padding taps by the direct-to-LDS path (may be null: no such path).
+// with K [Cout, 3, 3, Cin] (fp64 accumulation).
 hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int W, int Cin,
-                           const float* K, int Cout, int act, float* hn, float* dphi, const float* zero);
+                           const float* K, int Cout, int act, float* hn, float* dphi);
 // g [images, C] = mean over the D pixels of h [images, D, C].
 hipError_t launch_gap(hipStream_t s, const float* h, int images, int D, int C, float* g);
 // G [images*O, D, C] = Wd[o, c] / D * dphi[img, p, c].
@@ -19,13 +18,11 @@ hipError_t launch_conv_seed(hipStream_t s, const float* Wd, const float* dphi, i
 // Kt [Cin, 3, 3, Cout] = K [Cout, 2-kh, 2-kw, Cin]  (the kernel of the transposed convolution).
 hipError_t launch_conv_flip(hipStream_t s, const float* K, int Cout, int Cin, float* Kt);
 // out [images*O, D, Cin] = conv3x3(G [images*O, H, W, Cg], Kt [Cin, 3, 3, Cg]) * dphi [images, D, Cin].
-// `zero` as for launch_conv_fwd.
 hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
-                           const float* Kt, int Cin, const float* dphi, float* out, const float* zero);
+                           const float* Kt, int Cin, const float* dphi, float* out);
 // J[(s*O + o), off + c*9*Cin + k] = sum_p G[s, o, p, c] patch(h)[s, p, k] for every sample s.
-// `zero` as for launch_conv_fwd.
 hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
-                             int W, int C, int Cin, float* J, long long ldJ, long long off, const float* zero);
+                             int W, int C, int Cin, float* J, long long ldJ, long long off);
 // Deterministic split-K product J1 J2^T: plan, partial products, reduction into theta.
 int splitk_tile();
 // splits * R1 * R2 <= part_capacity (floats) always holds for the returned plan.

@@ -148,7 +148,6 @@ struct ntk_handle {
   std::vector<long long> joff;    // column offset of layer l in J
   long long Ktot = 0;             // columns of J = sum_l 9 c_l c_{l+1}
   size_t off_g = 0, off_Gping = 0, off_Gpong = 0, off_J = 0, off_gram_r = 0, off_part = 0;
-  size_t off_zero = 0;            // a page of zeros (the padding taps of the direct-to-LDS convs)
   long long part_capacity = 0;    // floats of the split-K partial buffer
 };
 
@@ -316,7 +315,6 @@ static void plan_cnn(ntk_handle* h) {
   const size_t tiles_max = (size_t)((h->max_n1 * O + T - 1) / T) * ((h->max_n2 * O + T - 1) / T);
   h->part_capacity = (long long)(1024 + tiles_max) * T * T;   // >= R1max * R2max
   h->off_part = take((size_t)h->part_capacity);
-  h->off_zero = take(64);
   h->ws_bytes = off;
 }
 
@@ -378,16 +376,6 @@ extern "C" int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, voi
       hipEventCreateWithFlags(&h->ev_gram, hipEventDisableTiming) != hipSuccess) {
     (void)hipGetLastError();
     destroy_sync_objects(h);   // run everything on the one stream
-  }
-  if (h->cnn) {
-    e = hipMemsetAsync(h->ws + h->off_zero, 0, 256, h->stream);
-    if (e == hipSuccess) e = hipStreamSynchronize(h->stream);
-    if (e != hipSuccess) {
-      destroy_sync_objects(h);
-      (void)hipFree(h->ws);
-      delete h;
-      return hip_fail(nullptr, e, "clearing the zero page");
-    }
   }
   *out = h;
   return NTK_OK;
@@ -732,7 +720,7 @@ static int cnn_forward(ntk_handle* h, const float* const* params, const float* X
   for (int l = 0; l < nc; ++l) {
     prof_begin(P, s, KC_CONV_FWD);
     e = launch_conv_fwd(s, l == 0 ? *h0 : F(h->off_ch[l]), M, H, W, h->ch[l], params[l], h->ch[l + 1],
-                        h->layers[l].act, F(h->off_ch[l + 1]), F(h->off_cdphi[l]), F(h->off_zero));
+                        h->layers[l].act, F(h->off_ch[l + 1]), F(h->off_cdphi[l]));
     prof_end(P, s, KC_CONV_FWD);
     if (e != hipSuccess) return hip_fail(h, e, "conv forward");
   }
@@ -850,15 +838,14 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
       theta_written = true;
     } else {
       prof_begin(P, s, KC_CONV_WGRAD);
-      e = launch_conv_wgrad(s, Gcur, hptr(l), M, Oe, H, W, h->ch[l + 1], h->ch[l], J, Kcall, jo[l],
-                            F(h->off_zero));
+      e = launch_conv_wgrad(s, Gcur, hptr(l), M, Oe, H, W, h->ch[l + 1], h->ch[l], J, Kcall, jo[l]);
       prof_end(P, s, KC_CONV_WGRAD);
       if (e != hipSuccess) return hip_fail(h, e, "conv weight-space cotangent");
     }
     if (l >= 1) {
       prof_begin(P, s, KC_CONV_BWD);
       e = launch_conv_bwd(s, Gcur, M, Oe, H, W, h->ch[l + 1], F(h->off_Kt[l]), h->ch[l],
-                          F(h->off_cdphi[l - 1]), Gnext, F(h->off_zero));
+                          F(h->off_cdphi[l - 1]), Gnext);
       prof_end(P, s, KC_CONV_BWD);
       if (e != hipSuccess) return hip_fail(h, e, "conv backward");
       std::swap(Gcur, Gnext);
@@ -1156,7 +1143,7 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
   for (int l = nc - 1; l >= 0; --l) {
     prof_begin(P, s, KC_CONV_WGRAD);
     e = launch_conv_wgrad(s, Gcur, hptr(l) + r2 * D * h->ch[l], n2, 1, H, W, h->ch[l + 1], h->ch[l], J,
-                          h->Ktot, h->joff[l], F(h->off_zero));
+                          h->Ktot, h->joff[l]);
     prof_end(P, s, KC_CONV_WGRAD);
     if (e != hipSuccess) return hip_fail(h, e, "conv weight cotangent");
     if (l >= 1) {
@@ -1166,7 +1153,7 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
       if (e != hipSuccess) return hip_fail(h, e, "kernel flip");
       prof_begin(P, s, KC_CONV_BWD);
       e = launch_conv_bwd(s, Gcur, n2, 1, H, W, h->ch[l + 1], F(h->off_Kt[l]), h->ch[l],
-                          F(h->off_cdphi[l - 1]) + r2 * D * h->ch[l], Gnext, F(h->off_zero));
+                          F(h->off_cdphi[l - 1]) + r2 * D * h->ch[l], Gnext);
       prof_end(P, s, KC_CONV_BWD);
       if (e != hipSuccess) return hip_fail(h, e, "VJP conv backward");
       std::swap(Gcur, Gnext);
@@ -1183,10 +1170,10 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
     const int co = h->ch[l + 1];
     prof_begin(P, s, KC_CONV_FWD);
     e = launch_conv_fwd(s, hptr(l), n1, H, W, h->ch[l], tc + h->joff[l], co, NTK_ACT_NONE,
-                        V(h->vp_off_cb), V(h->vp_off_cd), F(h->off_zero));
+                        V(h->vp_off_cb), V(h->vp_off_cd));
     if (e == hipSuccess && l > 0)
       e = launch_conv_fwd(s, tcur, n1, H, W, h->ch[l], params[l], co, NTK_ACT_NONE, V(h->vp_off_ca),
-                          V(h->vp_off_cd), F(h->off_zero));
+                          V(h->vp_off_cd));
     prof_end(P, s, KC_CONV_FWD);
     if (e != hipSuccess) return hip_fail(h, e, "JVP convolution");
     prof_begin(P, s, KC_VP_ELEMENTWISE);
