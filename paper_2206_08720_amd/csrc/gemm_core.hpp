@@ -541,15 +541,25 @@ struct MmaBlocks<Cfg, TA, TB, f64x4> {
 #pragma unroll
     for (int fn = 0; fn < Cfg::FN16; ++fn) f.b[fn] = TB::frag(Bs, wn0 + fn * 16 + lr, k);
   }
+  // The widening conversions of the whole block come first, so that the MFMAs issue back to
+  // back instead of each waiting on the VALU conversion just before it.
   __device__ static __forceinline__ void mma(const Frag& f, f64x4 (&acc)[Cfg::FM16][Cfg::FN16]) {
+    double a[Cfg::FM16][4], b[Cfg::FN16][4];
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+#pragma unroll
+      for (int fm = 0; fm < Cfg::FM16; ++fm) a[fm][t] = (double)f.a[fm][t];
+#pragma unroll
+      for (int fn = 0; fn < Cfg::FN16; ++fn) b[fn][t] = (double)f.b[fn][t];
+    }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int fm = 0; fm < Cfg::FM16; ++fm)
 #pragma unroll
         for (int fn = 0; fn < Cfg::FN16; ++fn)
-          acc[fm][fn] = __builtin_amdgcn_mfma_f64_16x16x4f64((double)f.a[fm][t], (double)f.b[fn][t],
-                                                             acc[fm][fn], 0, 0, 0);
+          acc[fm][fn] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[fm][t], b[fn][t], acc[fm][fn], 0, 0, 0);
   }
 };
 

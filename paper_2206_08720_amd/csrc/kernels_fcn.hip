@@ -245,27 +245,33 @@ hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, cons
 }
 
 // ------------------------------------------------------------------------------ seed, transpose
-// G[(m, o), c] = W[o, c] * dphi[m, c]: one workgroup per sample row m, float4 columns when
-// `vec` (C % 4 == 0, 16-byte aligned buffers).
+// G[(m, o), c] = W[o, c] * dphi[m, c]: workgroup w takes sample row m = w / ob and the outputs
+// o = (w % ob) * kSeedO ... (at most kSeedO of them), float4 columns when `vec` (C % 4 == 0,
+// 16-byte aligned buffers).
+constexpr int kSeedO = 4;
 __global__ void __launch_bounds__(256)
 k_bwd_seed(const float* __restrict__ W, const float* __restrict__ dphi, int M, int O, int C, int vec,
            float* __restrict__ G) {
-  for (int m = blockIdx.x; m < M; m += gridDim.x) {
+  const int ob = (O + kSeedO - 1) / kSeedO;
+  for (long long w = blockIdx.x; w < (long long)M * ob; w += gridDim.x) {
+    const int m = (int)(w / ob);
+    const int o0 = (int)(w - (long long)m * ob) * kSeedO, o1 = min(O, o0 + kSeedO);
     const float* dm = dphi + (long long)m * C;
     float* gm = G + (long long)m * O * C;
     if (vec) {
       const int C4 = C >> 2;
       for (int c4 = threadIdx.x; c4 < C4; c4 += blockDim.x) {
         const float4 d = reinterpret_cast<const float4*>(dm)[c4];
-        for (int o = 0; o < O; ++o) {
-          const float4 w = reinterpret_cast<const float4*>(W + (long long)o * C)[c4];
-          reinterpret_cast<float4*>(gm + (long long)o * C)[c4] = make_float4(w.x * d.x, w.y * d.y, w.z * d.z, w.w * d.w);
+        for (int o = o0; o < o1; ++o) {
+          const float4 wv = reinterpret_cast<const float4*>(W + (long long)o * C)[c4];
+          reinterpret_cast<float4*>(gm + (long long)o * C)[c4] =
+              make_float4(wv.x * d.x, wv.y * d.y, wv.z * d.z, wv.w * d.w);
         }
       }
     } else {
       for (int c = threadIdx.x; c < C; c += blockDim.x) {
         const float d = dm[c];
-        for (int o = 0; o < O; ++o) gm[(long long)o * C + c] = W[(long long)o * C + c] * d;
+        for (int o = o0; o < o1; ++o) gm[(long long)o * C + c] = W[(long long)o * C + c] * d;
       }
     }
   }
@@ -275,7 +281,8 @@ hipError_t launch_bwd_seed(hipStream_t s, const float* W, const float* dphi, int
                            float* G) {
   if (M <= 0 || O <= 0 || C <= 0) return hipSuccess;
   const int vec = vec_ok(W, C, C) && vec_ok(dphi, C, C) && vec_ok(G, C, C);
-  k_bwd_seed<<<dim3(std::min(M, 65535)), dim3(256), 0, s>>>(W, dphi, M, O, C, vec, G);
+  const long long work = (long long)M * ((O + kSeedO - 1) / kSeedO);
+  k_bwd_seed<<<dim3((unsigned)std::min<long long>(work, 65535)), dim3(256), 0, s>>>(W, dphi, M, O, C, vec, G);
   return hipGetLastError();
 }
 
