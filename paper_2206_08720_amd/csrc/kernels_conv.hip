@@ -23,6 +23,14 @@ namespace ntk {
 
 using CfgConvF64 = TileCfg<64, 64, 32, 32, 32>;    // forward, fp64 MFMA
 using CfgConv = TileCfg<128, 64, 32, 32, 32>;      // backward / wgrad, fp32 MFMA: 8 waves
+// direct-to-LDS backward and weight-space cotangent kernels: tiles and LDS stages.  The
+// backward takes 256-row tiles with a 32x64 block per wave (two independent accumulators per
+// wave) and two stages (80 KB: two workgroups per CU); the weight-space product keeps 128x64
+// tiles and two stages (48 KB: three workgroups per CU).  Both measured best among 128/256-row
+// tiles, 4/8 waves and 2/3 stages at the CNN workload.
+using CfgConvBwd = TileCfg<256, 64, 32, 32, 64>;
+using CfgConvWg = CfgConv;
+constexpr int kConvBwdStages = 2, kConvWgStages = 2;
 using CfgSplitK = TileCfg<128, 128, 32, 64, 64>;   // J1 J2^T partial products
 
 static inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
@@ -599,8 +607,8 @@ k_conv_bwd(LoadPatchesKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restr
   });
 }
 
-// direct-to-LDS form (Cg % 32 == 0): the cotangent patches gathered by the DMA, 3 LDS stages
-template <class Cfg>
+// direct-to-LDS form (Cg % 32 == 0): the cotangent patches gathered by the DMA, NS LDS stages
+template <class Cfg, int NS>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_conv_bwd_dma(DmaPatches<Cfg::BM, Cfg::WAVES> pa, DmaRowMajor<Cfg::BN, Cfg::WAVES> pb, int K,
                const float* __restrict__ dphi, int R, int N, FastDiv fOD, FastDiv fD, float* __restrict__ out,
@@ -610,7 +618,7 @@ k_conv_bwd_dma(DmaPatches<Cfg::BM, Cfg::WAVES> pa, DmaRowMajor<Cfg::BN, Cfg::WAV
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
-  gemm_mainloop_dma_ops<Cfg, 3>(pa, pb, m0, n0, 0, K, smem, acc);
+  gemm_mainloop_dma_ops<Cfg, NS>(pa, pb, m0, n0, 0, K, smem, acc);
   float g[Cfg::FM][Cfg::FN][16];
   gather_acc<Cfg>(g, m0, n0, [&](int r, int c) {
     const int rc = min(r, R - 1), cc = min(c, N - 1);
@@ -644,17 +652,18 @@ static hipError_t conv_bwd_vec(hipStream_t s, const float* G, int images, int O,
 hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
                            const float* Kt, int Cin, const float* dphi, float* out) {
   if (conv_dma_ok(G, (long long)images * O * H * W * Cg, Cg, Kt)) {
-    using Cfg = CfgConv;
+    using Cfg = CfgConvBwd;
+    constexpr int NS = kConvBwdStages;
     const int D = H * W, Kd = 9 * Cg;
     const int R = images * O * D;
     const int tn = cdiv(Cin, Cfg::BN), tm = cdiv(R, Cfg::BM);
     auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(G, images * O, H, W, Cg);
     DmaRowMajor<Cfg::BN, Cfg::WAVES> pb{Kt, Kd, Cin};
-    constexpr int bytes = gemm_dma_smem_bytes<Cfg, 3>();
-    hipError_t e = hipFuncSetAttribute((const void*)k_conv_bwd_dma<Cfg>,
+    constexpr int bytes = gemm_dma_smem_bytes<Cfg, NS>();
+    hipError_t e = hipFuncSetAttribute((const void*)k_conv_bwd_dma<Cfg, NS>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (e != hipSuccess) return e;
-    k_conv_bwd_dma<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(
+    k_conv_bwd_dma<Cfg, NS><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(
         pa, pb, Kd, dphi, R, Cin, FastDiv((uint32_t)(O * D)), FastDiv((uint32_t)D), out, tn);
     return hipGetLastError();
   }
@@ -705,7 +714,7 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
 }
 
 // direct-to-LDS form (C % 4 == 0 and Cin % 4 == 0): both operands K-outer, three LDS stages
-template <class Cfg>
+template <class Cfg, int NS>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O, int H, int W, int C, int Cin, FastDiv fC, FastDiv fW, FastDiv fCin,
                  float* __restrict__ J, long long ldJ, long long off, int tiles_n) {
@@ -732,7 +741,7 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
   ib.fC = fCin;
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
-  gemm_mainloop_dma_ops<Cfg, 3>(ia, ib, m0, n0, 0, D, smem, acc);
+  gemm_mainloop_dma_ops<Cfg, NS>(ia, ib, m0, n0, 0, D, smem, acc);
   const int R = O * C;
   for_each_acc<Cfg>(acc, m0, n0, [&](int r, int k, float v) {
     if (r < R && k < KC) {
@@ -762,13 +771,14 @@ hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int 
   // direct-to-LDS: one sample's cotangents and layer input each within a buffer resource
   if (C % 4 == 0 && Cin % 4 == 0 && aligned16(G) && aligned16(h) && (long long)O * H * W * C * 4 < (1LL << 31) &&
       (long long)H * W * Cin * 4 < (1LL << 31)) {
-    using Cfg = CfgConv;
+    using Cfg = CfgConvWg;
+    constexpr int NS = kConvWgStages;
     const int tn = cdiv(9 * Cin, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
-    constexpr int bytes = gemm_dma_smem_bytes<Cfg, 3>();
-    hipError_t e = hipFuncSetAttribute((const void*)k_conv_wgrad_dma<Cfg>,
+    constexpr int bytes = gemm_dma_smem_bytes<Cfg, NS>();
+    hipError_t e = hipFuncSetAttribute((const void*)k_conv_wgrad_dma<Cfg, NS>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (e != hipSuccess) return e;
-    k_conv_wgrad_dma<Cfg><<<dim3(tm * tn, images), dim3(Cfg::THREADS), bytes, s>>>(
+    k_conv_wgrad_dma<Cfg, NS><<<dim3(tm * tn, images), dim3(Cfg::THREADS), bytes, s>>>(
         G, h, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
         ldJ, off, tn);
     return hipGetLastError();
