@@ -508,8 +508,11 @@ hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int
 }
 
 // ------------------------------------------------------------------------------ GAP, seed
-// g[img, c] = mean over the D pixels of h[img, p, c]; one workgroup per image, fixed order.
-__global__ void k_gap(const float* __restrict__ h, int D, int C, float* __restrict__ g) {
+// g[img, c] = mean over the D pixels of h[img, p, c]: one workgroup per image.  Generic form:
+// 256 threads, lanes over channels and groups of pixels; vector form (C % 4 == 0, C / 4 dividing
+// 1024, 16-byte aligned): 1024 threads, a float4 of channels per lane, groups of pixels over the
+// rest.  The groups' partial sums are added in a fixed order.
+__global__ void __launch_bounds__(256) k_gap(const float* __restrict__ h, int D, int C, float* __restrict__ g) {
   __shared__ float part[256];
   const int img = blockIdx.x;
   const int lanes_c = C < 256 ? C : 256;
@@ -532,8 +535,45 @@ __global__ void k_gap(const float* __restrict__ h, int D, int C, float* __restri
   }
 }
 
+__global__ void __launch_bounds__(1024) k_gap4(const float* __restrict__ h, int D, int C, float* __restrict__ g) {
+  __shared__ float4 part[1024];
+  const int img = blockIdx.x;
+  const int C4 = C >> 2, groups = 1024 / C4;
+  const int t = threadIdx.x, grp = t / C4, c4 = t - grp * C4;
+  const float4* src = reinterpret_cast<const float4*>(h + (long long)img * D * C);
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int p = grp; p < D; p += groups) {
+    const float4 v = src[(long long)p * C4 + c4];
+    acc.x += v.x;
+    acc.y += v.y;
+    acc.z += v.z;
+    acc.w += v.w;
+  }
+  part[t] = acc;
+  __syncthreads();
+  if (t < C4) {
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int q = 0; q < groups; ++q) {
+      const float4 w = part[q * C4 + t];
+      v.x += w.x;
+      v.y += w.y;
+      v.z += w.z;
+      v.w += w.w;
+    }
+    const float d = (float)D;
+    float* dst = g + (long long)img * C + 4 * t;
+    dst[0] = v.x / d;
+    dst[1] = v.y / d;
+    dst[2] = v.z / d;
+    dst[3] = v.w / d;
+  }
+}
+
 hipError_t launch_gap(hipStream_t s, const float* h, int images, int D, int C, float* g) {
-  k_gap<<<dim3(images), dim3(256), 0, s>>>(h, D, C, g);
+  if (C % 4 == 0 && C / 4 <= 1024 && 1024 % (C / 4) == 0 && aligned16(h))
+    k_gap4<<<dim3(images), dim3(1024), 0, s>>>(h, D, C, g);
+  else
+    k_gap<<<dim3(images), dim3(256), 0, s>>>(h, D, C, g);
   return hipGetLastError();
 }
 
@@ -555,9 +595,37 @@ k_conv_seed(const float* __restrict__ Wd, const float* __restrict__ dphi, int IO
   }
 }
 
+// Vector form (C % 4 == 0, 16-byte aligned): workgroup w takes image w / pb and 256 float4s of
+// its [D, C] plane (pixel-block w % pb); each lane loads its float4 of dphi once and writes it,
+// scaled by Wd[o, c] / D, into the O cotangent images.
+__global__ void __launch_bounds__(256)
+k_conv_seed4(const float* __restrict__ Wd, const float* __restrict__ dphi, int images, int O, int DC4, int C4,
+             float inv_d, float* __restrict__ G) {
+  const int pb = (DC4 + 255) / 256;
+  for (long long w = blockIdx.x; w < (long long)images * pb; w += gridDim.x) {
+    const int img = (int)(w / pb);
+    const int q = (int)(w - (long long)img * pb) * 256 + threadIdx.x;   // float4 index in the plane
+    if (q >= DC4) continue;
+    const int c4 = q % C4;
+    const float4 d = reinterpret_cast<const float4*>(dphi)[(long long)img * DC4 + q];
+    for (int o = 0; o < O; ++o) {
+      const float4 wv = reinterpret_cast<const float4*>(Wd)[(long long)o * C4 + c4];
+      reinterpret_cast<float4*>(G)[((long long)img * O + o) * DC4 + q] =
+          make_float4(wv.x * inv_d * d.x, wv.y * inv_d * d.y, wv.z * inv_d * d.z, wv.w * inv_d * d.w);
+    }
+  }
+}
+
 hipError_t launch_conv_seed(hipStream_t s, const float* Wd, const float* dphi, int images, int O, int D,
                             int C, float* G) {
   const int DC = D * C;
+  if (C % 4 == 0 && aligned16(Wd) && aligned16(dphi) && aligned16(G)) {
+    const int DC4 = DC / 4, pb = cdiv(DC4, 256);
+    const long long work = (long long)images * pb;
+    k_conv_seed4<<<dim3((unsigned)std::min<long long>(work, 1 << 20)), dim3(256), 0, s>>>(
+        Wd, dphi, images, O, DC4, C / 4, 1.0f / (float)D, G);
+    return hipGetLastError();
+  }
   const int bx = std::min(cdiv(DC, 256), 64);
   const int IO = images * O;
   k_conv_seed<<<dim3(bx, std::min(IO, 32768)), dim3(256), 0, s>>>(Wd, dphi, IO, O, DC, FastDiv((uint32_t)C),
@@ -674,7 +742,8 @@ hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int
 
 // ------------------------------------------------------------------------------ weight-space cotangent
 // For sample s = blockIdx.y:  J[s*O + o][off + c*KC + k] = sum_p G[s,o,p,c] patch[s,p,k]
-template <class Cfg, bool VEC>
+// (VA / VB: float4 loads of the cotangent / patch operand)
+template <class Cfg, bool VA, bool VB>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, int H, int W, int C,
              int Cin, FastDiv fC, FastDiv fW, FastDiv fCin, float* __restrict__ J, long long ldJ,
@@ -685,14 +754,14 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
   const int KC = 9 * Cin;
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
-  LoadCotangentKOuterT<VEC> la;
+  LoadCotangentKOuterT<VA> la;
   la.g = G + (long long)s * O * D * C;
   la.rows = O * C;
   la.K = D;
   la.C = C;
   la.D = D;
   la.fC = fC;
-  LoadPatchesKOuterT<VEC> lb;
+  LoadPatchesKOuterT<VB> lb;
   lb.x = h + (long long)s * D * Cin;
   lb.rows = KC;
   lb.K = D;
@@ -751,16 +820,16 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
   });
 }
 
-template <bool VEC>
+template <bool VA, bool VB>
 static hipError_t conv_wgrad_vec(hipStream_t s, const float* G, const float* h, int images, int O,
                                  int H, int W, int C, int Cin, float* J, long long ldJ, long long off) {
   using Cfg = CfgConv;
-  using LA = LoadCotangentKOuterT<VEC>;
-  using LB = LoadPatchesKOuterT<VEC>;
+  using LA = LoadCotangentKOuterT<VA>;
+  using LB = LoadPatchesKOuterT<VB>;
   const int tn = cdiv(9 * Cin, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
-  hipError_t e = set_smem<Cfg, LA, LB>((const void*)k_conv_wgrad<Cfg, VEC>);
+  hipError_t e = set_smem<Cfg, LA, LB>((const void*)k_conv_wgrad<Cfg, VA, VB>);
   if (e != hipSuccess) return e;
-  k_conv_wgrad<Cfg, VEC><<<dim3(tm * tn, images), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LA, LB>(), s>>>(
+  k_conv_wgrad<Cfg, VA, VB><<<dim3(tm * tn, images), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LA, LB>(), s>>>(
       G, h, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
       ldJ, off, tn);
   return hipGetLastError();
@@ -783,9 +852,10 @@ hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int 
         ldJ, off, tn);
     return hipGetLastError();
   }
-  if (C % 4 == 0 && Cin % 4 == 0 && aligned16(G) && aligned16(h))
-    return conv_wgrad_vec<true>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
-  return conv_wgrad_vec<false>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
+  const bool va = C % 4 == 0 && aligned16(G), vb = Cin % 4 == 0 && aligned16(h);
+  if (va && vb) return conv_wgrad_vec<true, true>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
+  if (va) return conv_wgrad_vec<true, false>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
+  return conv_wgrad_vec<false, false>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
 }
 
 // ------------------------------------------------------------------------------ split-K J1 J2^T
