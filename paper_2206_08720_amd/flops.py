@@ -21,6 +21,10 @@ weight-space cotangents run for Oe = 1 output with "logit" (O otherwise); the co
 covers `pairs` input pairs (N1 N2, or N on the batch diagonal) and Oc output pairs per input
 pair (O^2 full, O for the trace, 1 for one logit).
 
+Symmetric schedule (X2 is X1, N1 = N2 = N): the stacked rows are the N samples once, and the
+contraction runs for the N (N + 1) / 2 pairs n1 <= n2 (the mirror image fills the rest), so
+its count uses that many pairs.
+
 Jacobian contraction (method = "jacobian", the baseline of Section 3.2): the same forward
 and backward passes (and, for the CNN, the weight-space Jacobians of every conv layer), then
 the explicit contraction, 2 pairs Oc P for P parameters in total.
@@ -28,10 +32,16 @@ the explicit contraction, 2 pairs Oc P for P parameters in total.
 from __future__ import annotations
 
 
-def _variant(O, n1, n2, output, batch):
+def _variant(O, n1, n2, output, batch, symmetric=False):
+    """(cotangent rows per sample, output pairs per input pair, input pairs contracted)."""
     Oe = 1 if output == "logit" else O
     Oc = {"full": O * O, "trace": O, "logit": 1}[output]
-    pairs = n1 if batch == "diagonal" else n1 * n2
+    if batch == "diagonal":
+        pairs = n1
+    elif symmetric:
+        pairs = n1 * (n1 + 1) // 2
+    else:
+        pairs = n1 * n2
     return Oe, Oc, pairs
 
 
@@ -40,12 +50,13 @@ def fcn_flops(spec, n1, n2, symmetric=False, output="full", batch="full"):
     L = len(layers) - 1
     d = [layers[0]["in"]] + [Lr["out"] for Lr in layers]
     O = d[-1]
-    Oe, Oc, pairs = _variant(O, n1, n2, output, batch)
+    Oe, Oc, pairs = _variant(O, n1, n2, output, batch, symmetric)
+    gpairs = n1 if batch == "diagonal" else n1 * n2     # the Gram kernels form the full block
     M = n1 if symmetric else n1 + n2
     st = {
         "forward": sum(2.0 * M * d[l] * d[l + 1] for l in range(L)),
         "backward": sum(2.0 * M * Oe * d[l + 1] * d[l] for l in range(1, L)),
-        "gram": sum(2.0 * pairs * d[l] for l in range(L + 1)),
+        "gram": sum(2.0 * gpairs * d[l] for l in range(L + 1)),
         "contraction": sum(2.0 * pairs * Oc * d[l + 1] for l in range(L)),
     }
     st["total"] = sum(st.values())
@@ -59,19 +70,21 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
     convs = [Lr for Lr in layers if Lr["kind"] == "conv3x3"]
     O = layers[-1]["out"]
     C = convs[-1]["out"]
-    Oe, Oc, pairs = _variant(O, n1, n2, output, batch)
+    Oe, Oc, pairs = _variant(O, n1, n2, output, batch, symmetric)
+    gpairs = n1 if batch == "diagonal" else n1 * n2
     M = n1 if symmetric else n1 + n2
     st = {
         "forward": sum(2.0 * M * D * 9 * c["in"] * c["out"] for c in convs),
         "backward": sum(2.0 * M * Oe * D * 9 * c["out"] * c["in"] for c in convs[1:]),
-        "gram": 2.0 * pairs * C,
+        "gram": 2.0 * gpairs * C,
     }
     if order == "outside_in":
         st["wgrad"] = sum(2.0 * M * (Oe * c["out"]) * (9 * c["in"]) * D for c in convs)
         st["contraction"] = 2.0 * pairs * Oc * sum(c["out"] * 9 * c["in"] for c in convs)
     else:  # inside-out: patch Gram, one-sided cotangent contraction, then the O x O product
-        st["contraction"] = sum(2.0 * pairs * (D * D * 9 * c["in"] + Oe * D * D * c["out"]
-                                               + Oc * D * c["out"]) for c in convs)
+        # (every input pair, also on the symmetric schedule)
+        st["contraction"] = sum(2.0 * gpairs * (D * D * 9 * c["in"] + Oe * D * D * c["out"]
+                                                + Oc * D * c["out"]) for c in convs)
     st["total"] = sum(st.values())
     return st
 
@@ -97,7 +110,7 @@ def ntk_flops(spec, n1, n2, symmetric=False, method="structured", **kw):
         st = fcn_flops(spec, n1, n2, symmetric, **kw)
     if method == "jacobian":
         O = spec["layers"][-1]["out"]
-        _, Oc, pairs = _variant(O, n1, n2, kw.get("output", "full"), kw.get("batch", "full"))
+        _, Oc, pairs = _variant(O, n1, n2, kw.get("output", "full"), kw.get("batch", "full"), symmetric)
         st.pop("gram", None)
         st.pop("total")
         st["contraction"] = 2.0 * pairs * Oc * param_total(spec)

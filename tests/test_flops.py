@@ -24,6 +24,9 @@ def test_fcn_terms_match_section_4_1():
     assert f["gram"] == 2 * N * N * (L + 1) * W
     sym = fcn_flops(spec, N, N, symmetric=True)
     assert sym["forward"] == f["forward"] / 2 and sym["backward"] == f["backward"] / 2
+    # the symmetric schedule contracts the N (N + 1) / 2 pairs n1 <= n2
+    assert sym["contraction"] == 2 * (N * (N + 1) // 2) * O * O * L * W
+    assert sym["gram"] == f["gram"]
 
 
 def test_workload_totals():
