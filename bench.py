@@ -69,11 +69,12 @@ def parse():
     return ap.parse_args()
 
 
-def sources_sha16():
+def sources_sha16(kernel_file="kernels_fcn.hip"):
+    """Hash of the sources a kernel is compiled from: its .hip file and every shared header."""
     import glob
     import hashlib
     csrc = os.path.join(ROOT, "paper_2206_08720_amd", "csrc")
-    files = sorted(glob.glob(os.path.join(csrc, "*.hip"))) + sorted(glob.glob(os.path.join(csrc, "*.hpp")))
+    files = [os.path.join(csrc, kernel_file)] + sorted(glob.glob(os.path.join(csrc, "*.hpp")))
     h = hashlib.sha256()
     for f in files:
         h.update(open(f, "rb").read())
@@ -87,7 +88,8 @@ def measured_traffic(name, kernel):
     if not os.path.exists(path):
         return None
     rec = json.load(open(path))
-    if rec.get("kernel") != kernel or rec.get("sources_sha256_16") != sources_sha16():
+    if rec.get("kernel") != kernel or \
+            rec.get("sources_sha256_16") != sources_sha16(rec.get("kernel_source", "kernels_fcn.hip")):
         return None
     return (rec["fetch_size_kib_per_launch"] * rec["fetch_scale"]
             + rec["write_size_kib_per_launch"] * rec["write_scale"]) * 1024.0
