@@ -90,6 +90,7 @@ struct ntk_handle {
   // the forward pass, layer-input Grams during the backward), joined back with events
   hipStream_t aux = nullptr;
   hipEvent_t ev_fork = nullptr, ev_tr = nullptr, ev_fwd = nullptr, ev_gram = nullptr;
+  hipEvent_t ev_seed = nullptr, ev_bwd = nullptr;   // split backward: seed done, second half done
   int device = 0;
   char* ws = nullptr;
   size_t ws_bytes = 0;
@@ -320,7 +321,7 @@ static void plan_cnn(ntk_handle* h) {
 
 static void destroy_sync_objects(ntk_handle* h) {
   if (h->aux) (void)hipStreamSynchronize(h->aux);
-  for (hipEvent_t* ev : {&h->ev_fork, &h->ev_tr, &h->ev_fwd, &h->ev_gram}) {
+  for (hipEvent_t* ev : {&h->ev_fork, &h->ev_tr, &h->ev_fwd, &h->ev_gram, &h->ev_seed, &h->ev_bwd}) {
     if (*ev) (void)hipEventDestroy(*ev);
     *ev = nullptr;
   }
@@ -373,7 +374,9 @@ extern "C" int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, voi
       hipEventCreateWithFlags(&h->ev_fork, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&h->ev_tr, hipEventDisableTiming) != hipSuccess ||
       hipEventCreateWithFlags(&h->ev_fwd, hipEventDisableTiming) != hipSuccess ||
-      hipEventCreateWithFlags(&h->ev_gram, hipEventDisableTiming) != hipSuccess) {
+      hipEventCreateWithFlags(&h->ev_gram, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&h->ev_seed, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&h->ev_bwd, hipEventDisableTiming) != hipSuccess) {
     (void)hipGetLastError();
     destroy_sync_objects(h);   // run everything on the one stream
   }
@@ -601,13 +604,35 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     e = launch_bwd_seed(s, WL, F(h->off_dphi[L - 1]), M, Oe, h->dims[L], F(h->off_G[L - 1]));
     prof_end(P, s, KC_BWD_SEED);
     if (e != hipSuccess) return hip_fail(h, e, "backward seed");
+    // The rows (n, o) are independent through the backward, so with a second stream the
+    // samples are split in two halves, each a chain of layer GEMMs on its own stream: the
+    // partial last round of one half's layer overlaps the other half's work.  Split only when
+    // every layer of a half still fills the chip (at least 2 tiles of 128 x 128 per CU).
+    long long min_tiles = -1;
     for (int l = L - 1; l >= 1; --l) {
-      prof_begin(P, s, KC_DENSE_BWD);
-      e = launch_dense_bwd(s, F(h->off_G[l]), F(h->off_Wt[l]), F(h->off_dphi[l - 1]), M * Oe,
-                           h->dims[l], h->dims[l + 1], Oe, F(h->off_G[l - 1]));
-      prof_end(P, s, KC_DENSE_BWD);
+      const long long t = ((long long)(M / 2) * Oe + 127) / 128 * ((h->dims[l] + 127) / 128);
+      min_tiles = min_tiles < 0 ? t : std::min(min_tiles, t);
+    }
+    const bool split = aux && L >= 2 && M >= 2 && min_tiles >= 2LL * h->num_cu;
+    const int MA = split ? M / 2 : M;   // samples on the main stream; the rest on the second
+    if (split && ((e = hipEventRecord(h->ev_seed, s)) != hipSuccess ||
+                  (e = hipStreamWaitEvent(aux, h->ev_seed, 0)) != hipSuccess))
+      return hip_fail(h, e, "stream fork");
+    prof_begin(P, s, KC_DENSE_BWD);
+    for (int l = L - 1; l >= 1; --l) {
+      const size_t K = h->dims[l + 1], N = h->dims[l];
+      e = launch_dense_bwd(s, F(h->off_G[l]), F(h->off_Wt[l]), F(h->off_dphi[l - 1]), MA * Oe, N, K, Oe,
+                           F(h->off_G[l - 1]));
+      if (e == hipSuccess && split)
+        e = launch_dense_bwd(aux, F(h->off_G[l]) + (size_t)MA * Oe * K, F(h->off_Wt[l]),
+                             F(h->off_dphi[l - 1]) + (size_t)MA * N, (M - MA) * Oe, N, K, Oe,
+                             F(h->off_G[l - 1]) + (size_t)MA * Oe * N);
       if (e != hipSuccess) return hip_fail(h, e, "dense backward");
     }
+    if (split && ((e = hipEventRecord(h->ev_bwd, aux)) != hipSuccess ||
+                  (e = hipStreamWaitEvent(s, h->ev_bwd, 0)) != hipSuccess))
+      return hip_fail(h, e, "stream join");
+    prof_end(P, s, KC_DENSE_BWD);
   }
   if (!jc && aux && (e = hipStreamWaitEvent(s, h->ev_gram, 0)) != hipSuccess)
     return hip_fail(h, e, "stream join");
