@@ -218,3 +218,25 @@ def test_width_2048_with_a_partial_last_round_of_backward_tiles():
     jc, e1, e2 = oracle.ntk_jc_with_norms(spec, params, X1[sub], X2[[0, 229]], layer_storage=S)
     cs, nw = errors(got[np.ix_(sub, [0, 229])], jc, e1, e2)
     assert cs <= TOL and nw <= TOL
+
+
+def test_backward_split_over_two_streams_with_an_odd_batch():
+    # 411 + 412 stacked samples: each half (411 and 412 samples x O = 10 rows) still has
+    # 33 x 16 = 528 >= 2 x 256 backward tiles, so the two halves of the backward run on the
+    # two streams; the odd total puts the boundary inside no sample
+    spec = wl.fcn_spec("bwsplit", 64, [2048, 2048, 2048], 10)
+    params = wl.make_params(spec, 71, "2/fan_in")
+    X1 = wl.make_inputs(spec, 411, 72)
+    X2 = wl.make_inputs(spec, 412, 73)
+    got = gpu_ntk(spec, params, X1, X2)
+    print("[parity] split backward: GPU done, computing fp64 references", flush=True)
+    ref = oracle.ntk_structured_fp64(spec, params, X1, X2, layer_storage=S)
+    d1 = oracle.ntk_structured_diag_fp64(spec, params, X1, layer_storage=S)
+    d2 = oracle.ntk_structured_diag_fp64(spec, params, X2, layer_storage=S)
+    cs, nw = errors(got, ref, d1, d2)
+    report("backward split over two streams, vs structured fp64", cs, nw)
+    assert cs <= TOL and nw <= TOL
+    # rows on both sides of the split (stacked sample 411 = X2[0]) against the definition
+    jc, e1, e2 = oracle.ntk_jc_with_norms(spec, params, X1[[0, 410]], X2[[0, 1, 411]], layer_storage=S)
+    cs, nw = errors(got[np.ix_([0, 410], [0, 1, 411])], jc, e1, e2)
+    assert cs <= TOL and nw <= TOL
