@@ -19,6 +19,10 @@ CASES = [
     ("trace over outputs", wl.fcn_spec("g4", 24, [40, 40], 5), 9, 7, {"output": "trace"}),
     ("batch diagonal", wl.fcn_spec("g5", 24, [40, 40], 5), 9, 9, {"batch": "diagonal"}),
     ("Jacobian contraction", wl.fcn_spec("g6", 12, [20], 3, bias=True), 5, 4, {"method": "jacobian"}),
+    # the full depth-8 width-2048 shape: second stream (transposes, Grams, half of the
+    # backward's rows), stream-K contraction, direct-to-LDS loops
+    ("depth 8, width 2048, 512 + 512 samples", wl.fcn_spec("g7", 3072, [2048] * 8, 10), 512, 512, {}),
+    ("4 conv layers of 64 channels, 64 + 64 images", wl.cnn_spec("g8", (32, 32), 3, [64] * 4, 10), 64, 64, {}),
 ]
 
 
