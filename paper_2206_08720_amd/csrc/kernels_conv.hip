@@ -32,6 +32,7 @@ using CfgConvBwd = TileCfg<256, 64, 32, 32, 64>;
 using CfgConvWg = CfgConv;
 constexpr int kConvBwdStages = 2, kConvWgStages = 2;
 using CfgSplitK = TileCfg<128, 128, 32, 64, 64>;   // J1 J2^T partial products
+using CfgSplitKDma = TileCfg<128, 128, 32, 32, 64>;  // the same, direct-to-LDS: 8 waves of 32x64
 
 static inline int cdiv(long long a, long long b) { return (int)((a + b - 1) / b); }
 static inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -896,6 +897,42 @@ k_ntk_splitk(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, int chunk, int symmetric,
   });
 }
 
+// Direct-to-LDS form (K-contiguous 16-byte aligned rows, K % 32 == 0): the same products, with
+// the work items ordered per XCD.  The items (chunk z, tile t) are numbered chunk by chunk,
+// i = z * tiles + t, and cut into 8 equal contiguous ranges, one per XCD.  Workgroup b runs on
+// XCD x = b % 8 (the hardware hands out workgroup ids round robin over the 8 XCDs) and takes
+// the (b / 8)-th item of range x, so the tiles of a chunk run together on one XCD and share its
+// L2 for the rows of J1 and J2 they read.
+template <class Cfg>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_ntk_splitk_dma(const float* __restrict__ J1, const float* __restrict__ J2, int R1, int R2, int K,
+                 long long ld, int chunk, int splits, int tiles, int symmetric, float* __restrict__ part,
+                 int tiles_n) {
+  extern __shared__ float smem[];
+  const int x = blockIdx.x & 7, j = blockIdx.x >> 3;
+  const long long items = (long long)tiles * splits;
+  const long long i = x * items / 8 + j;
+  if (i >= (x + 1) * items / 8) return;
+  const int z = (int)(i / tiles), t = (int)(i - (long long)z * tiles);
+  int tm, tn;
+  if (symmetric) {
+    tri_index_c(t, tiles_n, tm, tn);
+  } else {
+    tm = t / tiles_n;
+    tn = t % tiles_n;
+  }
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  const int k0 = z * chunk;
+  const int k1 = min(K, k0 + chunk);
+  f32x16 acc[Cfg::FM][Cfg::FN];
+  zero_acc<Cfg>(acc);
+  gemm_mainloop_dma<Cfg, 2>(J1, ld, R1, J2, ld, R2, m0, n0, k0, k1, smem, acc);
+  float* P = part + (long long)z * R1 * R2;
+  for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, float v) {
+    if (r < R1 && c < R2) P[(long long)r * R2 + c] = v;
+  });
+}
+
 // theta[n1][n2][o1][o2] = w[n1, n2] sum_z part[z][r1][r2] + (o1 == o2) rscale gram[n1, n2], or,
 // with accumulate, theta += w[n1, n2] sum_z part[z][r1][r2] (the readout summand is then
 // already in theta).  w = null means 1; gram = null means no readout summand.
@@ -967,6 +1004,20 @@ static hipError_t splitk_vec(hipStream_t s, const float* J1, const float* J2, in
 hipError_t launch_ntk_splitk(hipStream_t s, const float* J1, const float* J2, int R1, int R2,
                              long long K, long long ld, int symmetric, int chunk, int splits,
                              float* part) {
+  if (vec_ok(J1, ld, K) && vec_ok(J2, ld, K) && K % 32 == 0 && chunk % 32 == 0 && dma_span_ok(ld, K, 128)) {
+    using Cfg = CfgSplitKDma;
+    static_assert(Cfg::BM == CfgSplitK::BM && Cfg::BN == CfgSplitK::BN, "the reduction's tile grid");
+    const int tm = cdiv(R1, Cfg::BM), tn = cdiv(R2, Cfg::BN);
+    const int tiles = symmetric ? tn * (tn + 1) / 2 : tm * tn;
+    constexpr int bytes = gemm_dma_smem_bytes<Cfg, 2>();
+    hipError_t e = hipFuncSetAttribute((const void*)k_ntk_splitk_dma<Cfg>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess) return e;
+    const long long blocks = 8 * (((long long)tiles * splits + 7) / 8);
+    k_ntk_splitk_dma<Cfg><<<dim3((unsigned)blocks), dim3(Cfg::THREADS), bytes, s>>>(
+        J1, J2, R1, R2, (int)K, ld, chunk, splits, tiles, symmetric, part, tn);
+    return hipGetLastError();
+  }
   if (vec_ok(J1, ld, K) && vec_ok(J2, ld, K))
     return splitk_vec<true>(s, J1, J2, R1, R2, K, ld, symmetric, chunk, splits, part);
   return splitk_vec<false>(s, J1, J2, R1, R2, K, ld, symmetric, chunk, splits, part);
