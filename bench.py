@@ -8,14 +8,14 @@ on the synthetic workload, with all inputs already resident in HBM.  The default
 workload is the ReLU MLP of depth 8 and width 2048 (input 3072, O = 10,
 X1 and X2 of 512 samples each).  One JSON line is printed on stdout.
 
-The timed NTK steps are replays of the HIP graph the library records of one ntk_compute
-(NTK_OPT_GRAPH: every kernel of the step runs again on every replay, on the same device
-buffers); the graph is recorded by one untimed call before the warm-up, like the handle's
-set-up.  --eager times eagerly launched steps instead.
+The timed steps are launched eagerly.  --graph times replays of the HIP graph the library
+records of one ntk_compute instead (NTK_OPT_GRAPH: every kernel of the step runs again on
+every replay, on the same device buffers; the graph is recorded by one untimed call before the
+warm-up, like the handle's set-up).
 
 roofline: the dominant kernel class (largest time share) is timed live with HIP
-events recorded by the library around each launch on its own stream, during the timed
-steps when they are eager, else during as many further eager steps;
+events recorded by the library around each launch on its own stream during the timed steps
+(with --graph: during as many further eager steps);
 `achieved` = its algorithmic FLOPs per launch / average launch time.
 cpu_baseline: the fp64 Jacobian-contraction oracle on a bounded sample of the same
 workload (a few samples of X1 x X2, all outputs), timed on this host.
@@ -63,10 +63,10 @@ def parse():
                     help="structured derivatives (default) or the Jacobian-contraction baseline")
     ap.add_argument("--op", default="ntk", choices=["ntk", "vp"],
                     help="ntk: Theta(X1, X2); vp: the NTK-vector product Theta(X1, X2) v")
-    ap.add_argument("--eager", action="store_true",
-                    help="time eagerly launched steps; by default the NTK steps (op ntk, structured "
-                         "method) are replayed from a HIP graph (NTK_OPT_GRAPH) and the per-kernel "
-                         "timing comes from as many further eager steps")
+    ap.add_argument("--graph", action="store_true",
+                    help="time the NTK steps (op ntk, structured method) replayed from a HIP graph "
+                         "(NTK_OPT_GRAPH); the per-kernel timing then comes from as many further "
+                         "eager steps")
     ap.add_argument("--samples", type=int, default=0,
                     help="use only the first N samples of X1 and of X2 (0: the whole workload)")
     ap.add_argument("--cpu-samples", type=int, default=6,
@@ -218,7 +218,7 @@ def main():
             h.profile_enable(False)
         return evs[0].elapsed_time(evs[-1]) / k, per, wall_s, prof_
 
-    use_graph = not args.eager and args.op == "ntk" and args.method == "structured"
+    use_graph = args.graph and args.op == "ntk" and args.method == "structured"
     if use_graph:
         h.set_option(_lib.NTK_OPT_GRAPH, 1)
         step()                                  # records the graph (set-up, not a warm-up)
