@@ -25,8 +25,21 @@ inputs, the values the GPU library decides on.
 
 Conventions (the paper leaves them to the framework): ReLU'(0) = 0;
 erf'(z) = 2/sqrt(pi) exp(-z^2); convolutions are SAME (zero pad 1), stride 1,
-cross-correlation, NHWC activations, OHWI weights; "gap" is the mean over the
-H*W pixels.  Inputs arrive as float32 and are upcast exactly to float64.
+cross-correlation, NHWC activations, OHWI weights ([3, 3, C] for a depthwise
+convolution); a scale layer multiplies channel c (or feature c) by w[c];
+"avgpool2" is the mean over 2x2 windows with stride 2; "gap" is the mean over
+the H*W pixels.  Inputs arrive as float32 and are upcast exactly to float64.
+
+Layer kinds and the structure of their weight-space Jacobian dz/dtheta (the
+paper's appendix on structured derivatives; the oracle forms each block
+explicitly all the same):
+* dense, conv3x3: constant-block-diagonal (a matrix product along one axis);
+* dwconv3x3: block-diagonal over channels (channel c's filter only feeds
+  output channel c);
+* scale: block-diagonal over channels, and for images also output block-tiled
+  (the same w[c] multiplies every pixel);
+* biases of conv, depthwise and scale layers: output block-tiled (one value
+  broadcast over the pixels).
 """
 from __future__ import annotations
 
@@ -85,12 +98,16 @@ def _patches_transpose(dp, H, W, C):
 
 
 # ----------------------------------------------------------------------------- parameters
+# layer kinds with a weight (then an optional bias) and an activation
+_PARAM_KINDS = ("dense", "conv3x3", "dwconv3x3", "scale")
+
+
 def _split_params(spec, params):
     """Pair each parametrised layer with its (weight, bias-or-None), as float64."""
     out = []
     i = 0
     for L in spec["layers"]:
-        if L["kind"] in ("dense", "conv3x3"):
+        if L["kind"] in _PARAM_KINDS:
             w = np.asarray(params[i], dtype=np.float64)
             i += 1
             b = None
@@ -112,6 +129,10 @@ def param_count(spec):
             P += L["out"] * L["in"] + (L["out"] if L["bias"] else 0)
         elif L["kind"] == "conv3x3":
             P += L["out"] * 9 * L["in"] + (L["out"] if L["bias"] else 0)
+        elif L["kind"] == "dwconv3x3":
+            P += 9 * L["out"] + (L["out"] if L["bias"] else 0)
+        elif L["kind"] == "scale":
+            P += L["out"] + (L["out"] if L["bias"] else 0)
     return P
 
 
@@ -148,6 +169,29 @@ def _forward_record(spec, params, X, layer_storage="fp64"):
             z = z.reshape(N, H, W, w.shape[0])
             rec.append({"h": h, "z": z, "patches": pt})
             h = _store(_phi(L["act"], z), layer_storage)
+        elif L["kind"] == "dwconv3x3":
+            w, b = p                                          # [3, 3, C]
+            N, H, W, C = h.shape
+            pt = _patches(h).reshape(N, H * W, 9, C)          # tap t = (kh, kw), channel c
+            z = np.einsum("nptc,tc->npc", pt, w.reshape(9, C))
+            if b is not None:
+                z = z + b
+            z = z.reshape(N, H, W, C)
+            rec.append({"h": h, "z": z, "patches": pt})
+            h = _store(_phi(L["act"], z), layer_storage)
+        elif L["kind"] == "scale":
+            w, b = p                                          # [C], on the last axis
+            z = h * w
+            if b is not None:
+                z = z + b
+            rec.append({"h": h, "z": z})
+            h = _store(_phi(L["act"], z), layer_storage)
+        elif L["kind"] == "avgpool2":
+            N, H, W, C = h.shape
+            if H % 2 or W % 2:
+                raise ValueError("avgpool2 needs an even image height and width")
+            rec.append({"h": h})
+            h = _store(h.reshape(N, H // 2, 2, W // 2, 2, C).mean(axis=(2, 4)), layer_storage)
         elif L["kind"] == "gap":
             rec.append({"h": h})
             h = _store(h.mean(axis=(1, 2)), layer_storage)
@@ -188,12 +232,26 @@ def _output_cotangents(spec, params, rec, outputs):
             Cin = w.shape[3]
             dp = g.reshape(N, g.shape[1], H * W, Cout) @ w.reshape(Cout, -1)   # [N,Os,D,9Cin]
             g = _patches_transpose(dp, H, W, Cin)        # df/dh_li: [N, Os, H, W, Cin]
+        elif L["kind"] == "dwconv3x3":
+            G[li] = g
+            w, _ = wb[li]
+            N_, H, W, C = rec[li]["z"].shape
+            # patch entry (p, t, c) fed z[p, c] with weight w[t, c]
+            dp = g.reshape(N, g.shape[1], H * W, 1, C) * w.reshape(9, C)      # [N,Os,D,9,C]
+            g = _patches_transpose(dp.reshape(N, g.shape[1], H * W, 9 * C), H, W, C)
+        elif L["kind"] == "scale":
+            G[li] = g
+            w, _ = wb[li]
+            g = g * w
+        elif L["kind"] == "avgpool2":
+            # every input pixel of a 2x2 window feeds that window's mean with weight 1/4
+            g = np.repeat(np.repeat(g, 2, axis=2), 2, axis=3) / 4.0
         elif L["kind"] == "gap":
             hin = rec[li]["h"]
             D = hin.shape[1] * hin.shape[2]
             g = np.broadcast_to(g[:, :, None, None, :] / D,
                                 g.shape[:2] + hin.shape[1:]).copy()
-        if li > 0 and layers[li - 1]["kind"] in ("dense", "conv3x3"):
+        if li > 0 and layers[li - 1]["kind"] in _PARAM_KINDS:
             # through the activation of the previous layer: h_li = phi(z_{li-1})
             zprev = rec[li - 1]["z"]
             g = g * _dphi(layers[li - 1]["act"], zprev)[:, None]
@@ -246,6 +304,26 @@ def jacobian_blocks(spec, params, X, outputs=None, max_block_bytes=256 << 20, ch
                 yield J.reshape(R, (c1 - c0) * k9)
             if L["bias"]:
                 yield gf.sum(axis=2).reshape(R, cout)
+        elif L["kind"] == "dwconv3x3":
+            pt = rec[li]["patches"]                        # [N, D, 9, C]
+            C = L["out"]
+            D = pt.shape[1]
+            gf = G[li].reshape(N, len(outputs), D, C)
+            # dz[p, c] / dw[t, c'] = delta_{c c'} patch[p, t, c], shared by every pixel p:
+            # J[n, o, t, c] = sum_p G[n, o, p, c] patch[n, p, t, c]
+            J = np.einsum("nopc,nptc->notc", gf, pt, optimize=True)
+            yield J.reshape(R, 9 * C)
+            if L["bias"]:
+                yield gf.sum(axis=2).reshape(R, C)
+        elif L["kind"] == "scale":
+            h = rec[li]["h"]                               # [N, C] or [N, H, W, C]
+            C = L["out"]
+            g = G[li].reshape(N, len(outputs), -1, C)      # pixels (if any) on axis 2
+            # dz[p, c] / dw[c'] = delta_{c c'} h[p, c], shared by every pixel p
+            J = (g * h.reshape(N, 1, -1, C)).sum(axis=2)
+            yield J.reshape(R, C)
+            if L["bias"]:
+                yield g.sum(axis=2).reshape(R, C)
 
 
 def jacobian(spec, params, X, outputs=None, layer_storage="fp64"):

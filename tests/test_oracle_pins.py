@@ -28,10 +28,19 @@ def _tiny_specs():
         (wl.fcn_spec("fcn_linear", 4, [5], 2, act="none", bias=True), "1/fan_in"),
         (wl.cnn_spec("cnn_relu", (4, 3), 2, [3, 4], 3, act="relu"), "2/fan_in"),
         (wl.cnn_spec("cnn_erf_bias", (3, 3), 2, [3], 2, act="erf", bias=True), "2/fan_in"),
+        # the further layer kinds: depthwise conv, per-channel scale, 2x2 average pool
+        (wl.cnn_layers_spec("cnn_struct_erf", (4, 6), 2,
+                            [("conv3x3", 3, "erf", True), ("dwconv3x3", "erf", True),
+                             ("avgpool2",), ("scale", "erf", True), ("conv3x3", 2, "erf", False)],
+                            3), "2/fan_in"),
+        (wl.cnn_layers_spec("cnn_struct_relu", (4, 4), 3,
+                            [("dwconv3x3", "relu", False), ("conv3x3", 4, "none", True),
+                             ("scale", "relu", False), ("avgpool2",), ("dwconv3x3", "none", True)],
+                            2), "2/fan_in"),
     ]
 
 
-@pytest.mark.parametrize("idx", range(5))
+@pytest.mark.parametrize("idx", range(7))
 def test_forward_matches_torch_layers(idx):
     spec, wv = _tiny_specs()[idx]
     params = wl.make_params(spec, 11 + idx, wv, bias_var=0.3)
@@ -42,7 +51,7 @@ def test_forward_matches_torch_layers(idx):
     np.testing.assert_allclose(got, ref, rtol=1e-13, atol=1e-13)
 
 
-@pytest.mark.parametrize("idx", range(5))
+@pytest.mark.parametrize("idx", range(7))
 def test_jacobian_matches_torch_autograd(idx):
     spec, wv = _tiny_specs()[idx]
     params = wl.make_params(spec, 31 + idx, wv, bias_var=0.3)
@@ -63,7 +72,7 @@ def _relu_margin_ok(spec, params, X, margin=1e-3):
     return True
 
 
-@pytest.mark.parametrize("idx", [0, 1, 3, 4])
+@pytest.mark.parametrize("idx", [0, 1, 3, 4, 5])
 def test_jacobian_central_finite_differences(idx):
     spec, wv = _tiny_specs()[idx]
     params = wl.make_params(spec, 51 + idx, wv, bias_var=0.3)
@@ -128,7 +137,7 @@ def test_hand_worked_golden(golden_dir, fname):
     np.testing.assert_allclose(th, np.array(d["theta"]), rtol=0, atol=1e-12)
 
 
-@pytest.mark.parametrize("idx", [0, 1, 3])
+@pytest.mark.parametrize("idx", [0, 1, 3, 5, 6])
 def test_symmetry_and_psd(idx):
     spec, wv = _tiny_specs()[idx]
     params = wl.make_params(spec, 71 + idx, wv, bias_var=0.3)
@@ -249,3 +258,113 @@ def test_fp32_storage_rounds_every_stored_layer_output():
         assert np.array_equal(h, h.astype(np.float32).astype(np.float64))
     with pytest.raises(ValueError):
         _forward_record(spec, params, X, layer_storage="fp16")
+
+
+# ---- the further layer kinds: closed forms and reductions to pinned layers ------------------
+def _readout_net(blocks, hw=(4, 6), c=3, O=3):
+    return wl.cnn_layers_spec("closed", hw, c, blocks, O)
+
+
+def test_closed_form_scale_with_bias():
+    # f_o = sum_c Wd[o,c] (w[c] xbar[c] + b[c]) with xbar the pixel mean of x: by linearity
+    # df_o/dw[c] = Wd[o,c] xbar[c], df_o/db[c] = Wd[o,c], df_o/dWd[o',c] = delta (w xbar + b)[c]
+    spec = _readout_net([("scale", "none", True)])
+    params = wl.make_params(spec, 211, bias_var=0.5)
+    w, b, Wd = (p.astype(np.float64) for p in params)
+    X1 = wl.make_inputs(spec, 3, 212).astype(np.float64)
+    X2 = wl.make_inputs(spec, 2, 213).astype(np.float64)
+    m1, m2 = X1.mean(axis=(1, 2)), X2.mean(axis=(1, 2))            # [N, C]
+    g1, g2 = m1 * w + b, m2 * w + b
+    exp = np.einsum("oc,qc,nc,mc->nmoq", Wd, Wd, m1, m2) + np.einsum("oc,qc->oq", Wd, Wd) \
+        + (g1 @ g2.T)[:, :, None, None] * np.eye(3)
+    np.testing.assert_allclose(oracle.ntk_jc(spec, params, X1, X2), exp, rtol=1e-13, atol=1e-13)
+
+
+def test_closed_form_depthwise_with_bias():
+    # f_o = sum_c Wd[o,c] (sum_t w[t,c] s_t[c] + b[c]), s_t[c] = mean over output pixels of the
+    # input pixel at tap offset t (zero outside the image)
+    spec = _readout_net([("dwconv3x3", "none", True)])
+    params = wl.make_params(spec, 221, "2/fan_in", bias_var=0.5)
+    w, b, Wd = (p.astype(np.float64) for p in params)
+    H, W = 4, 6
+
+    def shifted_means(X):
+        N, _, _, C = X.shape
+        s = np.zeros((N, 3, 3, C))
+        for kh in range(3):
+            for kw in range(3):
+                for y in range(H):
+                    for x in range(W):
+                        yy, xx = y + kh - 1, x + kw - 1
+                        if 0 <= yy < H and 0 <= xx < W:
+                            s[:, kh, kw] += X[:, yy, xx]
+        return s / (H * W)
+
+    X1 = wl.make_inputs(spec, 3, 222).astype(np.float64)
+    X2 = wl.make_inputs(spec, 2, 223).astype(np.float64)
+    s1, s2 = shifted_means(X1), shifted_means(X2)                  # [N, 3, 3, C]
+    g1 = np.einsum("nijc,ijc->nc", s1, w) + b
+    g2 = np.einsum("nijc,ijc->nc", s2, w) + b
+    exp = np.einsum("oc,qc,nijc,mijc->nmoq", Wd, Wd, s1, s2) + np.einsum("oc,qc->oq", Wd, Wd) \
+        + (g1 @ g2.T)[:, :, None, None] * np.eye(3)
+    np.testing.assert_allclose(oracle.ntk_jc(spec, params, X1, X2), exp, rtol=1e-13, atol=1e-13)
+
+
+def test_closed_form_conv_bias_summand():
+    # a conv bias is broadcast over the pixels (output block-tiled): with no activation its
+    # Jacobian rows are Wd[o, :] for every input, so it adds Wd Wd^T to every O x O block
+    blocks_b = [("conv3x3", 4, "none", True)]
+    blocks_n = [("conv3x3", 4, "none", False)]
+    sb, sn = _readout_net(blocks_b), _readout_net(blocks_n)
+    params = wl.make_params(sb, 231, "2/fan_in", bias_var=0.5)
+    pn = [params[0], params[2]]
+    X1 = wl.make_inputs(sb, 3, 232)
+    X2 = wl.make_inputs(sb, 2, 233)
+    Wd = params[2].astype(np.float64)
+    # the readout summand changes with the bias (g moves by b); compare the parameter blocks
+    a = oracle.ntk_jc(sb, params, X1, X2)
+    Jb = oracle.jacobian(sb, params, X1)
+    np.testing.assert_allclose(Jb[:, :, 4 * 27:4 * 27 + 4], np.broadcast_to(Wd, (3, 3, 4)),
+                               rtol=1e-14, atol=1e-15)
+    Jn = oracle.jacobian(sn, pn, X1)
+    np.testing.assert_allclose(Jb[:, :, :4 * 27], Jn[:, :, :4 * 27], rtol=1e-14, atol=1e-15)
+    assert a.shape == (3, 2, 3, 3)
+
+
+def test_avgpool_before_gap_is_invisible():
+    # the mean of the 2x2-window means is the mean over all pixels
+    with_pool = _readout_net([("conv3x3", 4, "erf", True), ("avgpool2",)])
+    without = _readout_net([("conv3x3", 4, "erf", True)])
+    params = wl.make_params(with_pool, 241, "2/fan_in", bias_var=0.3)
+    X1 = wl.make_inputs(with_pool, 3, 242)
+    X2 = wl.make_inputs(with_pool, 2, 243)
+    np.testing.assert_allclose(oracle.ntk_jc(with_pool, params, X1, X2),
+                               oracle.ntk_jc(without, params, X1, X2), rtol=1e-13, atol=1e-14)
+
+
+def test_avgpool_between_convs_matches_strided_means():
+    # the pooled image is the mean of each 2x2 block; pin the pooling layer's forward map
+    # through a net whose first layer is an identity scale (w = 1, b = 0, no activation)
+    spec = _readout_net([("scale", "none", False), ("avgpool2",), ("conv3x3", 2, "none", False)],
+                        hw=(4, 6), c=2, O=2)
+    params = wl.make_params(spec, 251, "2/fan_in")
+    params[0] = np.ones_like(params[0])
+    X = wl.make_inputs(spec, 2, 252).astype(np.float64)
+    pooled = np.zeros((2, 2, 3, 2))
+    for y in range(2):
+        for x in range(3):
+            pooled[:, y, x] = X[:, 2 * y:2 * y + 2, 2 * x:2 * x + 2].sum(axis=(1, 2)) / 4
+    ref = wl.cnn_spec("ref", (2, 3), 2, [2], 2, act="none")
+    np.testing.assert_allclose(oracle.forward(spec, params, X),
+                               oracle.forward(ref, params[1:], pooled), rtol=1e-13, atol=1e-14)
+
+
+def test_depthwise_with_one_channel_is_a_3x3_conv():
+    dw = _readout_net([("dwconv3x3", "erf", True)], c=1, O=2)
+    cv = _readout_net([("conv3x3", 1, "erf", True)], c=1, O=2)
+    params = wl.make_params(dw, 261, "2/fan_in", bias_var=0.3)
+    cparams = [params[0].reshape(1, 3, 3, 1), params[1], params[2]]
+    X1 = wl.make_inputs(dw, 3, 262)
+    X2 = wl.make_inputs(dw, 2, 263)
+    np.testing.assert_allclose(oracle.ntk_jc(dw, params, X1, X2),
+                               oracle.ntk_jc(cv, cparams, X1, X2), rtol=1e-13, atol=1e-14)

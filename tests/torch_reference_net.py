@@ -1,7 +1,8 @@
 """A float64 PyTorch (CPU) implementation of the workload networks, used only to pin the oracle.
 
 It builds f(theta, x) from torch's own layer routines (linear, conv2d with
-padding 1, relu, erf, mean) so that torch autograd provides an independent
+padding 1 -- grouped per channel for the depthwise layer --, avg_pool2d, relu,
+erf, mean) so that torch autograd provides an independent
 Jacobian against which the oracle's hand-written reverse-mode Jacobian is
 checked.
 """
@@ -32,6 +33,28 @@ def torch_forward(spec, flat_params, X):
             # NHWC activations, OHWI weights -> torch's NCHW / OIHW
             y = F.conv2d(h.permute(0, 3, 1, 2), w.permute(0, 3, 1, 2), b, stride=1, padding=1)
             h = y.permute(0, 2, 3, 1)
+        elif L["kind"] == "dwconv3x3":
+            w = flat_params[i]
+            i += 1
+            b = None
+            if L["bias"]:
+                b = flat_params[i]
+                i += 1
+            # weights [3, 3, C] -> torch's grouped [C, 1, 3, 3]
+            C = w.shape[2]
+            y = F.conv2d(h.permute(0, 3, 1, 2), w.permute(2, 0, 1).unsqueeze(1), b,
+                         stride=1, padding=1, groups=C)
+            h = y.permute(0, 2, 3, 1)
+        elif L["kind"] == "scale":
+            w = flat_params[i]
+            i += 1
+            h = h * w
+            if L["bias"]:
+                h = h + flat_params[i]
+                i += 1
+        elif L["kind"] == "avgpool2":
+            h = F.avg_pool2d(h.permute(0, 3, 1, 2), kernel_size=2, stride=2).permute(0, 2, 3, 1)
+            continue
         elif L["kind"] == "gap":
             h = h.mean(dim=(1, 2))
             continue

@@ -10,16 +10,24 @@ Network specification (a plain dict)::
 
     {"name": str,
      "input_shape": (d0,)  for a fully-connected net, or (H, W, C) NHWC for a CNN,
-     "layers": [ {"kind": "dense",   "in": int, "out": int, "act": "relu"|"erf"|"none", "bias": bool},
-                 {"kind": "conv3x3", "in": int, "out": int, "act": ..., "bias": bool},
+     "layers": [ {"kind": "dense",     "in": int, "out": int, "act": "relu"|"erf"|"none", "bias": bool},
+                 {"kind": "conv3x3",   "in": int, "out": int, "act": ..., "bias": bool},
+                 {"kind": "dwconv3x3", "in": C,   "out": C,   "act": ..., "bias": bool},
+                 {"kind": "scale",     "in": C,   "out": C,   "act": ..., "bias": bool},
+                 {"kind": "avgpool2"},
                  {"kind": "gap"} ]}
 
 Parameter order: layer by layer, the weight first and then the bias if the
 layer has one.  Dense weights are [out, in] row-major; 3x3 convolution weights
-are [Cout, 3, 3, Cin] (OHWI).  The forward map is z = h W^T (+ b) for a dense
-layer, a SAME (zero pad 1), stride-1 cross-correlation for a conv layer,
-h_next = act(z), and "gap" is the mean over all pixels.  The last layer is a
-dense layer with act "none"; its output is f.
+are [Cout, 3, 3, Cin] (OHWI); depthwise 3x3 weights are [3, 3, C] (one 3x3
+filter per channel, channel fastest); scale weights are [C].  The forward map
+is z = h W^T (+ b) for a dense layer, a SAME (zero pad 1), stride-1
+cross-correlation for a conv layer (per channel for the depthwise one),
+z = h * w (+ b) broadcast over the pixels for a scale layer, and
+h_next = act(z).  "avgpool2" is the mean over non-overlapping 2x2 windows
+(stride 2; H and W even) and "gap" the mean over all pixels; neither has
+parameters or an activation.  The last layer is a dense layer with act
+"none"; its output is f.
 
 The five reference workloads follow the fully-connected and convolutional
 networks of the paper's Section 4 ("Examples"): Section 4.1's FCN with L hidden
@@ -37,6 +45,8 @@ __all__ = [
     "workload_names",
     "fcn_spec",
     "cnn_spec",
+    "cnn_layers_spec",
+    "PARAM_KINDS",
     "make_params",
     "make_inputs",
     "make_workload",
@@ -69,6 +79,37 @@ def cnn_spec(name, hw, c_in, channels, d_out, act="relu", bias=False):
     return {"name": name, "input_shape": (H, W, c_in), "layers": layers}
 
 
+def cnn_layers_spec(name, hw, c_in, blocks, d_out):
+    """CNN from a list of blocks, then global average pooling and a dense readout.
+
+    Each block is one of ("conv3x3", c_out, act, bias), ("dwconv3x3", act, bias),
+    ("scale", act, bias) or ("avgpool2",).
+    """
+    H, W = hw
+    layers = []
+    c = c_in
+    for b in blocks:
+        kind = b[0]
+        if kind == "conv3x3":
+            _, co, act, bias = b
+            layers.append({"kind": kind, "in": c, "out": co, "act": act, "bias": bool(bias)})
+            c = co
+        elif kind in ("dwconv3x3", "scale"):
+            _, act, bias = b
+            layers.append({"kind": kind, "in": c, "out": c, "act": act, "bias": bool(bias)})
+        elif kind == "avgpool2":
+            layers.append({"kind": kind})
+        else:
+            raise ValueError(f"unknown block {kind!r}")
+    layers.append({"kind": "gap"})
+    layers.append({"kind": "dense", "in": c, "out": d_out, "act": "none", "bias": False})
+    return {"name": name, "input_shape": (H, W, c_in), "layers": layers}
+
+
+# layer kinds that carry parameters (a weight, then an optional bias) and an activation
+PARAM_KINDS = ("dense", "conv3x3", "dwconv3x3", "scale")
+
+
 def param_shapes(spec):
     """Shapes of the parameter tensors in order (weight, then bias if present)."""
     shapes = []
@@ -81,6 +122,14 @@ def param_shapes(spec):
             shapes.append((L["out"], 3, 3, L["in"]))
             if L["bias"]:
                 shapes.append((L["out"],))
+        elif L["kind"] == "dwconv3x3":
+            shapes.append((3, 3, L["out"]))
+            if L["bias"]:
+                shapes.append((L["out"],))
+        elif L["kind"] == "scale":
+            shapes.append((L["out"],))
+            if L["bias"]:
+                shapes.append((L["out"],))
     return shapes
 
 
@@ -91,8 +140,10 @@ def output_dim(spec):
 def make_params(spec, seed, weight_var="1/fan_in", bias_var=0.01):
     """Draw float32 parameters.  weight_var is "1/fan_in" or "2/fan_in" (a variance).
 
-    fan_in is `in` for a dense layer and 9*Cin for a 3x3 convolution.  Biases are
-    N(0, bias_var) (bias_var is a variance).
+    fan_in is `in` for a dense layer, 9*Cin for a 3x3 convolution and 9 for a
+    depthwise one.  Scale weights are drawn around 1, as N(1, 0.01), like the
+    affine scale of a normalisation layer.  Biases are N(0, bias_var)
+    (bias_var is a variance).
     """
     rng = np.random.default_rng(seed)
     scale = {"1/fan_in": 1.0, "2/fan_in": 2.0}[weight_var]
@@ -104,6 +155,14 @@ def make_params(spec, seed, weight_var="1/fan_in", bias_var=0.01):
         elif L["kind"] == "conv3x3":
             fan_in = 9 * L["in"]
             shape = (L["out"], 3, 3, L["in"])
+        elif L["kind"] == "dwconv3x3":
+            fan_in = 9
+            shape = (3, 3, L["out"])
+        elif L["kind"] == "scale":
+            params.append((1.0 + 0.1 * rng.standard_normal((L["out"],))).astype(np.float32))
+            if L["bias"]:
+                params.append((rng.standard_normal((L["out"],)) * np.sqrt(bias_var)).astype(np.float32))
+            continue
         else:
             continue
         std = np.sqrt(scale / fan_in)
@@ -144,6 +203,17 @@ WORKLOADS = {
     "cnn4_c64_32x32": dict(
         index=5, spec=cnn_spec("cnn4_c64_32x32", (32, 32), 3, [64] * 4, 10, act="relu"),
         n1=64, n2=64, weight_var="2/fan_in", x_dist="normal", x2_is_x1=False),
+    # The further structure rules of the paper's appendix on structured derivatives, one
+    # layer kind each: convolution biases (output block-tiled), a depthwise convolution
+    # (block-diagonal), a per-channel scale with bias (block-diagonal over channels and
+    # output block-tiled over pixels), and a 2x2 average pool between convolutions.
+    "cnn_struct_c64_32x32": dict(
+        index=6, spec=cnn_layers_spec(
+            "cnn_struct_c64_32x32", (32, 32), 3,
+            [("conv3x3", 64, "relu", True), ("dwconv3x3", "relu", True), ("avgpool2",),
+             ("conv3x3", 64, "relu", True), ("scale", "relu", True), ("conv3x3", 64, "relu", True)],
+            10),
+        n1=64, n2=64, weight_var="2/fan_in", bias_var=0.01, x_dist="normal", x2_is_x1=False),
 }
 
 
