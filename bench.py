@@ -40,7 +40,8 @@ HBM_PEAK_GBS = 8000.0
 STAGE_OF = {"dense_fwd": "forward", "dense_bwd": "backward", "gram": "gram",
             "ntk_fcn": "contraction", "conv_fwd": "forward", "conv_bwd": "backward",
             "conv_wgrad": "wgrad", "ntk_splitk": "contraction", "conv_pairsum": "contraction",
-            "ntk_diag": "contraction"}
+            "ntk_diag": "contraction", "struct_fwd": "forward", "struct_bwd": "backward",
+            "struct_wgrad": "wgrad"}
 # kernel class -> stage of the NTK-vector product's counter
 VP_STAGE_OF = {"dense_fwd": "forward", "dense_bwd": "vjp_backward", "gram": "gram_products",
                "conv_fwd": "forward_and_jvp", "conv_bwd": "vjp_backward",

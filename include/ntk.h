@@ -24,10 +24,26 @@
  *   * FCN: n >= 1 DENSE layers.  Layer l maps d_l -> d_{l+1}:
  *       z_l = h_l W_l^T (+ b_l),  h_{l+1} = act_l(z_l),  h_0 = x,  f = z_last.
  *     The last layer must have act NONE (f is the last pre-activation).
- *   * CNN: k >= 1 CONV3X3_SAME layers (stride 1, zero padding 1,
- *     cross-correlation, NHWC activations, OHWI weights [Cout,3,3,Cin]), then
- *     one GAP layer (mean over the H*W pixels), then one DENSE readout layer
- *     with act NONE and no bias.  Convolution biases are not supported.
+ *   * CNN: 1..64 spatial layers, then one GAP layer (mean over the pixels), then
+ *     one DENSE readout layer with act NONE and no bias.  The spatial layers, in any
+ *     order, at least one of them with parameters:
+ *       CONV3X3_SAME   z = 3x3 cross-correlation, stride 1, zero padding 1, weights
+ *                      [Cout,3,3,Cin] (OHWI), optional bias [Cout];
+ *       DWCONV3X3_SAME depthwise: channel c convolved with its own 3x3 filter, weights
+ *                      [3,3,C], optional bias [C]; in == out;
+ *       SCALE          z = h * w[c], weights [C], optional bias [C]; in == out;
+ *       AVGPOOL2       mean over non-overlapping 2x2 windows (stride 2), no parameters,
+ *                      act NONE; the image height and width must be even there.
+ *     Activations are NHWC.  The three parametrised kinds take any activation.
+ *     How each kind's weight-space Jacobian is structured, and how it is contracted:
+ *     the 3x3 convolution is constant-block-diagonal (the outside-in or inside-out
+ *     orders of NTK_OPT_CONV_ORDER); the depthwise convolution is block-diagonal over
+ *     channels and the scale layer block-diagonal over channels and output
+ *     block-tiled over pixels (appendix "Block Diagonal", "Output Block-tiled"): their
+ *     weight-space cotangents are per-channel pixel sums, 9*C and C columns; every
+ *     bias is output block-tiled, its cotangent the pixel sum of the output cotangent
+ *     (C columns).  These columns are contracted by the same split-K product as the
+ *     outside-in 3x3 convolution columns.
  *
  * Conventions: act'(0) = 0 for ReLU; erf'(z) = 2/sqrt(pi) exp(-z^2).
  *
@@ -62,17 +78,23 @@ extern "C" {
 #define NTK_DENSE          0
 #define NTK_CONV3X3_SAME   1
 #define NTK_GAP            2
+#define NTK_DWCONV3X3_SAME 3
+#define NTK_SCALE          4
+#define NTK_AVGPOOL2       5
 
 #define NTK_ACT_NONE       0
 #define NTK_ACT_RELU       1
 #define NTK_ACT_ERF        2
 
 typedef struct ntk_layer_desc {
-    int kind;      /* NTK_DENSE, NTK_CONV3X3_SAME or NTK_GAP                              */
-    int in;        /* input features / input channels (ignored for GAP)                   */
-    int out;       /* output features / output channels (ignored for GAP)                 */
-    int act;       /* activation applied to this layer's output (NTK_ACT_*; GAP: NONE)    */
-    int has_bias;  /* 1 if the layer has a bias vector of length `out` (DENSE only)       */
+    int kind;      /* NTK_DENSE, NTK_CONV3X3_SAME, NTK_DWCONV3X3_SAME, NTK_SCALE,
+                      NTK_AVGPOOL2 or NTK_GAP                                             */
+    int in;        /* input features / input channels (ignored for AVGPOOL2 and GAP)      */
+    int out;       /* output features / output channels (ignored for AVGPOOL2 and GAP)    */
+    int act;       /* activation applied to this layer's output (NTK_ACT_*; AVGPOOL2 and
+                      GAP: NONE)                                                          */
+    int has_bias;  /* 1 if the layer has a bias vector of length `out` (not AVGPOOL2, GAP,
+                      or the CNN readout)                                                 */
 } ntk_layer_desc;
 
 typedef struct ntk_model_desc {
@@ -157,7 +179,8 @@ int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, void* hip_stre
  * ntk_compute -- enqueue Theta(X1, X2) on the handle's stream.
  *   params  host array of device pointers, one per parameter tensor in layer
  *           order, weight first then bias (if has_bias): dense weight [out, in]
- *           row-major, dense bias [out], conv weight [Cout, 3, 3, Cin] (OHWI).
+ *           row-major, conv weight [Cout, 3, 3, Cin] (OHWI), depthwise weight
+ *           [3, 3, C], scale weight [C], every bias [out]; AVGPOOL2 and GAP have none.
  *   X1      device [n1, in_c] (FCN) or [n1, in_h, in_w, in_c] NHWC (CNN), fp32.
  *   X2      device, same layout with n2 rows.  X2 == X1 with n2 == n1 selects the
  *           symmetric schedule (see NTK_OPT_SYMMETRIC).
@@ -180,7 +203,8 @@ int ntk_compute(ntk_handle* h, const float* const* params, const float* X1, int 
  *   v    device [n2, O] fp32: v[n2*O + o2].
  *   out  device [n1, O] fp32: out[n1*O + o1] = sum_{n2, o2} Theta(x1_{n1}, x2_{n2})[o1, o2] v[n2, o2].
  * Time about 3 forward passes of the batches (no N1 N2 O^2 term).  The output and batch
- * variants and NTK_OPT_METHOD do not apply.  The first call on a handle allocates the
+ * variants and NTK_OPT_METHOD do not apply.  Convolutional models must consist of bias-free
+ * CONV3X3_SAME layers (NTK_E_UNSUPPORTED otherwise).  The first call on a handle allocates the
  * weight-space vector (one float per parameter) and the tangent buffers.  Stream-ordered,
  * asynchronous, deterministic; NTK_E_ARG for null pointers or sizes out of range.
  */

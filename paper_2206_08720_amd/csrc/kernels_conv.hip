@@ -425,9 +425,10 @@ struct DmaPatchesKOuter {
 // ------------------------------------------------------------------------------ forward
 template <class Cfg>
 __device__ __forceinline__ void conv_fwd_epilogue(f64x4 (&acc)[Cfg::FM16][Cfg::FN16], int m0, int n0,
-                                                  int M, int N, int act, float* __restrict__ hn,
-                                                  float* __restrict__ dphi) {
+                                                  int M, int N, int act, const float* __restrict__ bias,
+                                                  float* __restrict__ hn, float* __restrict__ dphi) {
   for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, double z) {
+    if (bias) z += (double)bias[min(c, N - 1)];
     float h, d;
     if (act == 1) {
       h = z > 0.0 ? (float)z : 0.f;
@@ -448,32 +449,32 @@ __device__ __forceinline__ void conv_fwd_epilogue(f64x4 (&acc)[Cfg::FM16][Cfg::F
 template <class Cfg>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_conv_fwd_dma(DmaPatches<Cfg::BM, Cfg::WAVES> pa, DmaRowMajor<Cfg::BN, Cfg::WAVES> pb, int K, int M, int N, int act,
-               float* __restrict__ hn, float* __restrict__ dphi, int tiles_n) {
+               const float* __restrict__ bias, float* __restrict__ hn, float* __restrict__ dphi, int tiles_n) {
   extern __shared__ float smem[];
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   f64x4 acc[Cfg::FM16][Cfg::FN16];
   zero_acc<Cfg>(acc);
   gemm_mainloop_dma_ops<Cfg, 3>(pa, pb, m0, n0, 0, K, smem, acc);
-  conv_fwd_epilogue<Cfg>(acc, m0, n0, M, N, act, hn, dphi);
+  conv_fwd_epilogue<Cfg>(acc, m0, n0, M, N, act, bias, hn, dphi);
 }
 
 template <class Cfg, bool VEC>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_conv_fwd(LoadPatchesKInnerT<VEC> la, LoadKInnerT<VEC> lb, int M, int N, int act,
-           float* __restrict__ hn, float* __restrict__ dphi, int tiles_n) {
+           const float* __restrict__ bias, float* __restrict__ hn, float* __restrict__ dphi, int tiles_n) {
   extern __shared__ float smem[];
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   f64x4 acc[Cfg::FM16][Cfg::FN16];
   zero_acc<Cfg>(acc);
   gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
-  conv_fwd_epilogue<Cfg>(acc, m0, n0, M, N, act, hn, dphi);
+  conv_fwd_epilogue<Cfg>(acc, m0, n0, M, N, act, bias, hn, dphi);
 }
 
 template <bool VEC>
 static hipError_t conv_fwd_vec(hipStream_t s, const float* x, int images, int H, int W, int Cin,
-                               const float* K, int Cout, int act, float* hn, float* dphi) {
+                               const float* K, int Cout, int act, const float* bias, float* hn, float* dphi) {
   using Cfg = CfgConvF64;
   using LA = LoadPatchesKInnerT<VEC>;
   using LB = LoadKInnerT<VEC>;
@@ -484,12 +485,12 @@ static hipError_t conv_fwd_vec(hipStream_t s, const float* x, int images, int H,
   hipError_t e = set_smem<Cfg, LA, LB>((const void*)k_conv_fwd<Cfg, VEC>);
   if (e != hipSuccess) return e;
   k_conv_fwd<Cfg, VEC><<<dim3(tm * tn), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LA, LB>(), s>>>(
-      la, lb, M, Cout, act, hn, dphi, tn);
+      la, lb, M, Cout, act, bias, hn, dphi, tn);
   return hipGetLastError();
 }
 
 hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int W, int Cin,
-                           const float* K, int Cout, int act, float* hn, float* dphi) {
+                           const float* K, int Cout, int act, const float* bias, float* hn, float* dphi) {
   if (conv_dma_ok(x, (long long)images * H * W * Cin, Cin, K)) {
     using Cfg = CfgConvF64;
     const int M = images * H * W, Kd = 9 * Cin;
@@ -500,12 +501,12 @@ hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int
     hipError_t e = hipFuncSetAttribute((const void*)k_conv_fwd_dma<Cfg>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (e != hipSuccess) return e;
-    k_conv_fwd_dma<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(pa, pb, Kd, M, Cout, act, hn, dphi, tn);
+    k_conv_fwd_dma<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(pa, pb, Kd, M, Cout, act, bias, hn, dphi, tn);
     return hipGetLastError();
   }
   if (Cin % 4 == 0 && aligned16(x) && vec_ok(K, 9 * Cin, 9 * Cin))
-    return conv_fwd_vec<true>(s, x, images, H, W, Cin, K, Cout, act, hn, dphi);
-  return conv_fwd_vec<false>(s, x, images, H, W, Cin, K, Cout, act, hn, dphi);
+    return conv_fwd_vec<true>(s, x, images, H, W, Cin, K, Cout, act, bias, hn, dphi);
+  return conv_fwd_vec<false>(s, x, images, H, W, Cin, K, Cout, act, bias, hn, dphi);
 }
 
 // ------------------------------------------------------------------------------ GAP, seed
@@ -587,11 +588,11 @@ k_conv_seed(const float* __restrict__ Wd, const float* __restrict__ dphi, int IO
   for (int io = blockIdx.y; io < IO; io += gridDim.y) {
     const int img = io / O, o = io - img * O;
     const float* wrow = Wd + (long long)o * C;
-    const float* drow = dphi + (long long)img * DC;
+    const float* drow = dphi ? dphi + (long long)img * DC : nullptr;
     float* grow = G + (long long)io * DC;
     for (int q = blockIdx.x * 256 + threadIdx.x; q < DC; q += gridDim.x * 256) {
       const int c = q - (int)fC.div(q) * C;
-      grow[q] = wrow[c] * inv_d * drow[q];
+      grow[q] = drow ? wrow[c] * inv_d * drow[q] : wrow[c] * inv_d;
     }
   }
 }
@@ -608,7 +609,8 @@ k_conv_seed4(const float* __restrict__ Wd, const float* __restrict__ dphi, int i
     const int q = (int)(w - (long long)img * pb) * 256 + threadIdx.x;   // float4 index in the plane
     if (q >= DC4) continue;
     const int c4 = q % C4;
-    const float4 d = reinterpret_cast<const float4*>(dphi)[(long long)img * DC4 + q];
+    const float4 d = dphi ? reinterpret_cast<const float4*>(dphi)[(long long)img * DC4 + q]
+                          : make_float4(1.f, 1.f, 1.f, 1.f);
     for (int o = 0; o < O; ++o) {
       const float4 wv = reinterpret_cast<const float4*>(Wd)[(long long)o * C4 + c4];
       reinterpret_cast<float4*>(G)[((long long)img * O + o) * DC4 + q] =
@@ -669,7 +671,7 @@ k_conv_bwd(LoadPatchesKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restr
     const int rc = min(r, R - 1), cc = min(c, N - 1);
     const int img = (int)fOD.div(rc);              // r = (img*O + o)*D + p
     const int p = rc - (int)fD.div(rc) * (int)fD.d;
-    return dphi[((long long)img * fD.d + p) * N + cc];
+    return dphi ? dphi[((long long)img * fD.d + p) * N + cc] : 1.f;
   });
   for_each_acc_aux<Cfg>(acc, g, m0, n0, [&](int r, int c, float v, float d) {
     if (r < R && c < N) out[(long long)r * N + c] = v * d;
@@ -693,7 +695,7 @@ k_conv_bwd_dma(DmaPatches<Cfg::BM, Cfg::WAVES> pa, DmaRowMajor<Cfg::BN, Cfg::WAV
     const int rc = min(r, R - 1), cc = min(c, N - 1);
     const int img = (int)fOD.div(rc);
     const int p = rc - (int)fD.div(rc) * (int)fD.d;
-    return dphi[((long long)img * fD.d + p) * N + cc];
+    return dphi ? dphi[((long long)img * fD.d + p) * N + cc] : 1.f;
   });
   for_each_acc_aux<Cfg>(acc, g, m0, n0, [&](int r, int c, float v, float d) {
     if (r < R && c < N) out[(long long)r * N + c] = v * d;

@@ -32,6 +32,9 @@ enum KernelClass {
   KC_NTK_DIAG,
   KC_JC_JACOBIAN,
   KC_VP_ELEMENTWISE,
+  KC_STRUCT_FWD,     // depthwise / scale / pool forward
+  KC_STRUCT_BWD,     // depthwise / scale / pool backward
+  KC_STRUCT_WGRAD,   // depthwise / scale / bias weight-space cotangents (pixel sums)
   KC_COUNT
 };
 const char* kernel_class_name(int cls);

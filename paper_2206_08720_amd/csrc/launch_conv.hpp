@@ -7,17 +7,18 @@
 namespace ntk {
 
 // hn/dphi [images, H, W, Cout] = act / act' of the SAME 3x3 convolution of x [images, H, W, Cin]
-// with K [Cout, 3, 3, Cin] (fp64 accumulation).
+// with K [Cout, 3, 3, Cin], plus bias [Cout] when not null (fp64 accumulation).
 hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int W, int Cin,
-                           const float* K, int Cout, int act, float* hn, float* dphi);
+                           const float* K, int Cout, int act, const float* bias, float* hn, float* dphi);
 // g [images, C] = mean over the D pixels of h [images, D, C].
 hipError_t launch_gap(hipStream_t s, const float* h, int images, int D, int C, float* g);
-// G [images*O, D, C] = Wd[o, c] / D * dphi[img, p, c].
+// G [images*O, D, C] = Wd[o, c] / D * dphi[img, p, c]  (dphi null: the identity).
 hipError_t launch_conv_seed(hipStream_t s, const float* Wd, const float* dphi, int images, int O,
                             int D, int C, float* G);
 // Kt [Cin, 3, 3, Cout] = K [Cout, 2-kh, 2-kw, Cin]  (the kernel of the transposed convolution).
 hipError_t launch_conv_flip(hipStream_t s, const float* K, int Cout, int Cin, float* Kt);
-// out [images*O, D, Cin] = conv3x3(G [images*O, H, W, Cg], Kt [Cin, 3, 3, Cg]) * dphi [images, D, Cin].
+// out [images*O, D, Cin] = conv3x3(G [images*O, H, W, Cg], Kt [Cin, 3, 3, Cg]) * dphi [images, D, Cin]
+// (dphi null: the identity).
 hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
                            const float* Kt, int Cin, const float* dphi, float* out);
 // J[(s*O + o), off + c*9*Cin + k] = sum_p G[s, o, p, c] patch(h)[s, p, k] for every sample s.

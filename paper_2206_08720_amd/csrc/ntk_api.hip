@@ -17,6 +17,7 @@
 #include "../../include/ntk.h"
 #include "launch.hpp"
 #include "launch_conv.hpp"
+#include "launch_struct.hpp"
 
 namespace ntk {
 
@@ -24,7 +25,7 @@ const char* kernel_class_name(int cls) {
   static const char* names[KC_COUNT] = {
       "dense_fwd", "dense_bwd", "bwd_seed",  "gram",       "ntk_fcn",    "transpose",    "conv_fwd",
       "conv_bwd",  "conv_seed", "gap",       "conv_wgrad", "ntk_splitk", "ntk_reduce", "conv_pairsum",
-      "copy",      "ntk_diag",  "jc_jacobian", "vp_elementwise"};
+      "copy",      "ntk_diag",  "jc_jacobian", "vp_elementwise", "struct_fwd", "struct_bwd", "struct_wgrad"};
   return (cls >= 0 && cls < KC_COUNT) ? names[cls] : "?";
 }
 
@@ -140,14 +141,20 @@ struct ntk_handle {
   size_t off_vpart = 0;           // split-K partials of the one-output variants (trace, logit)
   long long vpart_capacity = 0;
 
-  // ---- convolutional plan: conv layers 0..nc-1, GAP, dense readout
-  int nc = 0, H = 0, W = 0, D = 0;
-  std::vector<int> ch;            // c_0 .. c_nc (channels)
-  std::vector<size_t> off_ch;     // conv layer inputs h_l, l = 0..nc   [Mmax, D, c_l]
-  std::vector<size_t> off_cdphi;  // act'(z_l), l = 0..nc-1             [Mmax, D, c_{l+1}]
-  std::vector<size_t> off_Kt;     // flipped kernels, l = 1..nc-1       [c_l, 9, c_{l+1}]
-  std::vector<long long> joff;    // column offset of layer l in J
-  long long Ktot = 0;             // columns of J = sum_l 9 c_l c_{l+1}
+  // ---- convolutional plan: spatial layers 0..nc-1 (3x3 and depthwise 3x3 convolutions, scale
+  //      layers, 2x2 average pools), GAP, dense readout
+  int nc = 0, H = 0, W = 0, D = 0;  // the input image
+  std::vector<int> ch;            // c_0 .. c_nc: channels at each layer boundary
+  std::vector<int> bh, bw;        // image height and width at each layer boundary 0..nc
+  std::vector<int> wslot, bslot;  // parameter slots of layer l's weight and bias (-1: none)
+  int rslot = 0;                  // parameter slot of the readout weight
+  bool vp_ok = false;             // only bias-free 3x3 convolutions: NTK-vector products supported
+  std::vector<size_t> off_ch;     // layer inputs h_l, l = 0..nc (nc: the GAP input) [Mmax, bh_l, bw_l, c_l]
+  std::vector<size_t> off_cdphi;  // act'(z_l) of parametrised layers [Mmax, bh_{l+1}, bw_{l+1}, c_{l+1}]
+  std::vector<size_t> off_Kt;     // flipped kernels of the 3x3 convolutions l >= 1 [c_l, 9, c_{l+1}]
+  std::vector<long long> joff;    // column of the 3x3 convolution weights in J when every layer is
+                                  // outside-in (the NTK-vector product's layout)
+  long long Ktot = 0;             // columns of J at most: every weight and bias column
   size_t off_g = 0, off_Gping = 0, off_Gpong = 0, off_J = 0, off_gram_r = 0, off_part = 0;
   long long part_capacity = 0;    // floats of the split-K partial buffer
 };
@@ -167,17 +174,21 @@ static int hip_fail(ntk_handle* h, hipError_t e, const char* what) {
 }
 
 // ------------------------------------------------------------------------------ validation
+static bool is_spatial_kind(int k) {
+  return k == NTK_CONV3X3_SAME || k == NTK_DWCONV3X3_SAME || k == NTK_SCALE || k == NTK_AVGPOOL2;
+}
+
 static int validate(const ntk_model_desc* m, ntk_handle* tmp) {
   if (!m || !m->layers || m->n_layers <= 0) return fail(nullptr, NTK_E_ARG, "null or empty model descriptor");
   if (m->out_dim <= 0) return fail(nullptr, NTK_E_SHAPE, "out_dim must be positive");
   const int n = m->n_layers;
   for (int i = 0; i < n; ++i) {
     const ntk_layer_desc& L = m->layers[i];
-    if (L.kind != NTK_DENSE && L.kind != NTK_CONV3X3_SAME && L.kind != NTK_GAP)
+    if (L.kind != NTK_DENSE && L.kind != NTK_GAP && !is_spatial_kind(L.kind))
       return fail(nullptr, NTK_E_UNSUPPORTED, "layer " + std::to_string(i) + ": unknown kind");
     if (L.act != NTK_ACT_NONE && L.act != NTK_ACT_RELU && L.act != NTK_ACT_ERF)
       return fail(nullptr, NTK_E_UNSUPPORTED, "layer " + std::to_string(i) + ": unknown activation");
-    if (L.kind != NTK_GAP && (L.in <= 0 || L.out <= 0))
+    if (L.kind != NTK_GAP && L.kind != NTK_AVGPOOL2 && (L.in <= 0 || L.out <= 0))
       return fail(nullptr, NTK_E_SHAPE, "layer " + std::to_string(i) + ": in/out must be positive");
   }
   const ntk_layer_desc& last = m->layers[n - 1];
@@ -202,21 +213,36 @@ static int validate(const ntk_model_desc* m, ntk_handle* tmp) {
     tmp->cnn = false;
     return NTK_OK;
   }
-  // CNN: conv3x3 x k, gap, dense readout
+  // CNN: spatial layers (3x3 or depthwise 3x3 convolutions, scale layers, 2x2 average pools),
+  // then gap, then a dense readout
   int i = 0;
   if (m->in_h <= 0 || m->in_w <= 0 || m->in_c <= 0) return fail(nullptr, NTK_E_SHAPE, "bad input shape");
-  int c = m->in_c;
-  while (i < n && m->layers[i].kind == NTK_CONV3X3_SAME) {
+  int c = m->in_c, hh = m->in_h, ww = m->in_w;
+  bool any_param = false;
+  while (i < n && is_spatial_kind(m->layers[i].kind)) {
     const ntk_layer_desc& L = m->layers[i];
-    if (L.in != c) return fail(nullptr, NTK_E_SHAPE, "conv layer " + std::to_string(i) + ": in != previous channels");
-    if (L.has_bias) return fail(nullptr, NTK_E_UNSUPPORTED, "convolution biases are not supported");
-    c = L.out;
+    const std::string at = "layer " + std::to_string(i) + ": ";
+    if (L.kind == NTK_AVGPOOL2) {
+      if (L.act != NTK_ACT_NONE || L.has_bias)
+        return fail(nullptr, NTK_E_UNSUPPORTED, at + "avgpool2 takes no activation and no bias");
+      if (hh % 2 || ww % 2) return fail(nullptr, NTK_E_SHAPE, at + "avgpool2 needs an even height and width");
+      hh /= 2;
+      ww /= 2;
+    } else {
+      if (L.in != c) return fail(nullptr, NTK_E_SHAPE, at + "in != previous channels");
+      if (L.kind != NTK_CONV3X3_SAME && L.out != L.in)
+        return fail(nullptr, NTK_E_SHAPE, at + "depthwise and scale layers keep the channel count (out == in)");
+      c = L.out;
+      any_param = true;
+    }
     ++i;
   }
   if (i == 0 || i > kMaxLayers)
-    return fail(nullptr, NTK_E_UNSUPPORTED, "a CNN is 1..64 conv3x3 layers, then gap, then a dense readout");
+    return fail(nullptr, NTK_E_UNSUPPORTED, "a CNN is 1..64 spatial layers, then gap, then a dense readout");
+  if (!any_param)
+    return fail(nullptr, NTK_E_UNSUPPORTED, "a CNN needs at least one convolution or scale layer before gap");
   if (i != n - 2 || m->layers[i].kind != NTK_GAP)
-    return fail(nullptr, NTK_E_UNSUPPORTED, "a CNN is conv3x3 layers, then gap, then one dense readout");
+    return fail(nullptr, NTK_E_UNSUPPORTED, "a CNN is spatial layers, then gap, then one dense readout");
   if (m->layers[i].act != NTK_ACT_NONE) return fail(nullptr, NTK_E_UNSUPPORTED, "gap takes no activation");
   if (last.in != c) return fail(nullptr, NTK_E_SHAPE, "readout in != conv channels");
   if (last.has_bias) return fail(nullptr, NTK_E_UNSUPPORTED, "the CNN readout has no bias");
@@ -274,6 +300,17 @@ static void plan_fcn(ntk_handle* h) {
   }
 }
 
+// Columns of a spatial layer's weight block in J: 9 Cin Cout (3x3 convolution, outside-in),
+// 9 C (depthwise), C (scale), 0 (pool).
+static long long weight_cols(const ntk_layer_desc& L, int cin) {
+  switch (L.kind) {
+    case NTK_CONV3X3_SAME: return 9LL * cin * L.out;
+    case NTK_DWCONV3X3_SAME: return 9LL * L.out;
+    case NTK_SCALE: return L.out;
+    default: return 0;
+  }
+}
+
 static void plan_cnn(ntk_handle* h) {
   const int n = (int)h->layers.size();
   h->nc = n - 2;
@@ -281,33 +318,57 @@ static void plan_cnn(ntk_handle* h) {
   h->W = h->in_w;
   h->D = h->H * h->W;
   const int nc = h->nc;
-  h->ch.resize(nc + 1);
+  h->ch.assign(nc + 1, 0);
+  h->bh.assign(nc + 1, 0);
+  h->bw.assign(nc + 1, 0);
   h->ch[0] = h->in_c;
-  for (int l = 0; l < nc; ++l) h->ch[l + 1] = h->layers[l].out;
+  h->bh[0] = h->in_h;
+  h->bw[0] = h->in_w;
+  h->wslot.assign(nc, -1);
+  h->bslot.assign(nc, -1);
+  h->vp_ok = true;
+  int slot = 0;
+  for (int l = 0; l < nc; ++l) {
+    const ntk_layer_desc& L = h->layers[l];
+    const bool pool = L.kind == NTK_AVGPOOL2;
+    h->bh[l + 1] = pool ? h->bh[l] / 2 : h->bh[l];
+    h->bw[l + 1] = pool ? h->bw[l] / 2 : h->bw[l];
+    h->ch[l + 1] = pool ? h->ch[l] : L.out;
+    if (!pool) {
+      h->wslot[l] = slot++;
+      if (L.has_bias) h->bslot[l] = slot++;
+    }
+    if (L.kind != NTK_CONV3X3_SAME || L.has_bias) h->vp_ok = false;
+  }
+  h->rslot = slot;
   const size_t Mmax = (size_t)h->max_n1 + h->max_n2;
-  const size_t O = h->out_dim, D = h->D;
+  const size_t O = h->out_dim;
   size_t off = 0;
   auto take = [&](size_t floats) {
     size_t o = off;
     off = align_up(off + floats * 4);
     return o;
   };
-  int cmax = 0;
-  for (int l = 1; l <= nc; ++l) cmax = std::max(cmax, h->ch[l]);
+  auto plane = [&](int b) { return (size_t)h->bh[b] * h->bw[b] * h->ch[b]; };
+  size_t gmax = 0;   // largest cotangent image: the output of some layer
+  for (int b = 1; b <= nc; ++b) gmax = std::max(gmax, plane(b));
   h->off_ch.assign(nc + 1, 0);
   h->off_cdphi.assign(nc, 0);
   h->off_Kt.assign(nc, 0);
   h->joff.assign(nc, 0);
-  for (int l = 0; l <= nc; ++l) h->off_ch[l] = take(Mmax * D * h->ch[l]);
-  for (int l = 0; l < nc; ++l) h->off_cdphi[l] = take(Mmax * D * h->ch[l + 1]);
-  for (int l = 1; l < nc; ++l) h->off_Kt[l] = take((size_t)9 * h->ch[l] * h->ch[l + 1]);
+  for (int l = 0; l <= nc; ++l) h->off_ch[l] = take(Mmax * plane(l));
+  for (int l = 0; l < nc; ++l)
+    if (h->wslot[l] >= 0) h->off_cdphi[l] = take(Mmax * plane(l + 1));
+  for (int l = 1; l < nc; ++l)
+    if (h->layers[l].kind == NTK_CONV3X3_SAME) h->off_Kt[l] = take((size_t)9 * h->ch[l] * h->ch[l + 1]);
   h->off_g = take(Mmax * h->ch[nc]);
-  h->off_Gping = take(Mmax * O * D * cmax);
-  h->off_Gpong = take(Mmax * O * D * cmax);
+  h->off_Gping = take(Mmax * O * gmax);
+  h->off_Gpong = take(Mmax * O * gmax);
   long long kt = 0;
   for (int l = 0; l < nc; ++l) {
+    const ntk_layer_desc& L = h->layers[l];
     h->joff[l] = kt;
-    kt += 9LL * h->ch[l] * h->ch[l + 1];
+    kt += weight_cols(L, h->ch[l]) + (L.has_bias ? L.out : 0);
   }
   h->Ktot = kt;
   h->off_J = take(Mmax * O * (size_t)kt);
@@ -721,19 +782,19 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   return NTK_OK;
 }
 
-// CNN forward pass of the stacked batch [X1; X2] (or X1 alone when sym), keeping every conv
-// layer input and act'(z_l), then the global average pool g; *h0 receives the layer-0 input.
+// CNN forward pass of the stacked batch [X1; X2] (or X1 alone when sym), keeping every spatial
+// layer's input and act'(z_l), then the global average pool g; *h0 receives the layer-0 input.
 static int cnn_forward(ntk_handle* h, const float* const* params, const float* X1, int n1,
                        const float* X2, int n2, bool sym, const float** h0) {
-  const int nc = h->nc, H = h->H, W = h->W, D = h->D;
+  const int nc = h->nc;
   const int M = sym ? n1 : n1 + n2;
   hipStream_t s = h->stream;
   Profiler* P = &h->prof;
   auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
-  for (int l = 0; l <= nc; ++l)
-    if (!params[l]) return fail(h, NTK_E_ARG, "null weight pointer");
+  for (int i = 0; i <= h->rslot; ++i)
+    if (!params[i]) return fail(h, NTK_E_ARG, "null parameter pointer");
   hipError_t e;
-  const size_t img_floats = (size_t)D * h->ch[0];
+  const size_t img_floats = (size_t)h->D * h->ch[0];
   *h0 = X1;
   if (!sym) {
     prof_begin(P, s, KC_COPY);
@@ -743,14 +804,31 @@ static int cnn_forward(ntk_handle* h, const float* const* params, const float* X
     *h0 = F(h->off_ch[0]);
   }
   for (int l = 0; l < nc; ++l) {
-    prof_begin(P, s, KC_CONV_FWD);
-    e = launch_conv_fwd(s, l == 0 ? *h0 : F(h->off_ch[l]), M, H, W, h->ch[l], params[l], h->ch[l + 1],
-                        h->layers[l].act, F(h->off_ch[l + 1]), F(h->off_cdphi[l]));
-    prof_end(P, s, KC_CONV_FWD);
-    if (e != hipSuccess) return hip_fail(h, e, "conv forward");
+    const ntk_layer_desc& L = h->layers[l];
+    const float* x = l == 0 ? *h0 : F(h->off_ch[l]);
+    float* out = F(h->off_ch[l + 1]);
+    float* dphi = F(h->off_cdphi[l]);
+    const float* w = h->wslot[l] >= 0 ? params[h->wslot[l]] : nullptr;
+    const float* b = h->bslot[l] >= 0 ? params[h->bslot[l]] : nullptr;
+    const int Hl = h->bh[l], Wl = h->bw[l], C = h->ch[l];
+    if (L.kind == NTK_CONV3X3_SAME) {
+      prof_begin(P, s, KC_CONV_FWD);
+      e = launch_conv_fwd(s, x, M, Hl, Wl, C, w, L.out, L.act, b, out, dphi);
+      prof_end(P, s, KC_CONV_FWD);
+    } else {
+      prof_begin(P, s, KC_STRUCT_FWD);
+      if (L.kind == NTK_DWCONV3X3_SAME)
+        e = launch_dw_fwd(s, x, M, Hl, Wl, C, w, b, L.act, out, dphi);
+      else if (L.kind == NTK_SCALE)
+        e = launch_scale_fwd(s, x, M, Hl * Wl, C, w, b, L.act, out, dphi);
+      else
+        e = launch_pool_fwd(s, x, M, Hl, Wl, C, out);
+      prof_end(P, s, KC_STRUCT_FWD);
+    }
+    if (e != hipSuccess) return hip_fail(h, e, "forward pass");
   }
   prof_begin(P, s, KC_GAP);
-  e = launch_gap(s, F(h->off_ch[nc]), M, D, h->ch[nc], F(h->off_g));
+  e = launch_gap(s, F(h->off_ch[nc]), M, h->bh[nc] * h->bw[nc], h->ch[nc], F(h->off_g));
   prof_end(P, s, KC_GAP);
   if (e != hipSuccess) return hip_fail(h, e, "global average pooling");
   return NTK_OK;
@@ -758,14 +836,12 @@ static int cnn_forward(ntk_handle* h, const float* const* params, const float* X
 
 static int compute_cnn(ntk_handle* h, const float* const* params, const float* X1, int n1,
                        const float* X2, int n2, float* theta) {
-  const int nc = h->nc, O = h->out_dim, H = h->H, W = h->W, D = h->D;
+  const int nc = h->nc, O = h->out_dim;
   const bool sym = h->opt_symmetric && X1 == X2 && n1 == n2;
   const int M = sym ? n1 : n1 + n2;
   hipStream_t s = h->stream;
   Profiler* P = &h->prof;
   auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
-  for (int l = 0; l <= nc; ++l)
-    if (!params[l]) return fail(h, NTK_E_ARG, "null weight pointer");
   // variants: one logit (the cotangent rows are then (n) instead of (n, o)), the trace over
   // outputs, the batch diagonal (pairs (n, n) only)
   const bool logit = h->opt_output == NTK_OUTPUT_LOGIT;
@@ -774,30 +850,45 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   const int Oe = logit ? 1 : O;
   const double pairs = diag ? (double)n1 : (double)n1 * n2;
   const double Oc = trace ? (double)O : (double)Oe * Oe;   // output pairs per input pair
-  // contraction order per layer: the cost model of the appendix "CNN NTK Complexity"
-  // (outside-in N1 N2 O^2 F Cin Cout plus forming J, N O D F Cin Cout per sample, against
-  // inside-out N1 N2 (D^2 F Cin + O D^2 Cout + O^2 D Cout)), or the forced option
+  // contraction order of each 3x3 convolution: the cost model of the appendix "CNN NTK
+  // Complexity" (outside-in N1 N2 O^2 F Cin Cout plus forming J, N O D F Cin Cout per sample,
+  // against inside-out N1 N2 (D^2 F Cin + O D^2 Cout + O^2 D Cout)), or the forced option.
+  // Depthwise and scale layers (block-diagonal weight-space Jacobians, 9 C and C columns) and
+  // every bias (output block-tiled, C columns) always contract outside-in: their O^2 P term is
+  // the smallest of the orders there.
   std::vector<char> inside(nc, 0);
-  const bool io_ok = pairsum_supported(D, Oe) != 0;
   for (int l = 0; l < nc; ++l) {
+    if (h->layers[l].kind != NTK_CONV3X3_SAME || h->opt_method == NTK_METHOD_JACOBIAN) continue;
+    const double Dl = (double)h->bh[l] * h->bw[l];
+    const bool io_ok = pairsum_supported(h->bh[l] * h->bw[l], Oe) != 0;
     const double Cin = h->ch[l], Co = h->ch[l + 1];
-    const double oi = pairs * Oc * 9 * Cin * Co + (double)M * Oe * D * 9 * Cin * Co;
-    const double io = pairs * ((double)D * D * 9 * Cin + (double)Oe * D * D * Co + Oc * D * Co);
-    if (h->opt_method == NTK_METHOD_JACOBIAN) inside[l] = 0;   // explicit J_l: outside-in
-    else if (h->opt_conv_order == NTK_CONV_ORDER_INSIDE_OUT) inside[l] = 1;
-    else if (h->opt_conv_order == NTK_CONV_ORDER_AUTO) inside[l] = (io_ok && io < oi) ? 1 : 0;
+    const double oi = pairs * Oc * 9 * Cin * Co + (double)M * Oe * Dl * 9 * Cin * Co;
+    const double io = pairs * (Dl * Dl * 9 * Cin + (double)Oe * Dl * Dl * Co + Oc * Dl * Co);
+    if (h->opt_conv_order == NTK_CONV_ORDER_INSIDE_OUT) {
+      if (!io_ok) return fail(h, NTK_E_UNSUPPORTED, "the inside-out order needs D <= 64 pixels and O <= 64");
+      inside[l] = 1;
+    } else if (h->opt_conv_order == NTK_CONV_ORDER_AUTO) {
+      inside[l] = (io_ok && io < oi) ? 1 : 0;
+    }
   }
+  // columns of J in this call: per layer its weight block (unless contracted inside-out), then
+  // its bias
+  std::vector<long long> jw(nc, 0), jb(nc, 0);
   long long Kcall = 0;
-  std::vector<long long> jo(nc, 0);
   for (int l = 0; l < nc; ++l) {
-    if (inside[l]) continue;
-    jo[l] = Kcall;
-    Kcall += 9LL * h->ch[l] * h->ch[l + 1];
+    const ntk_layer_desc& L = h->layers[l];
+    if (L.kind == NTK_AVGPOOL2) continue;
+    if (!(L.kind == NTK_CONV3X3_SAME && inside[l])) {
+      jw[l] = Kcall;
+      Kcall += weight_cols(L, h->ch[l]);
+    }
+    if (L.has_bias) {
+      jb[l] = Kcall;
+      Kcall += L.out;
+    }
   }
-  if (Kcall < h->Ktot && !io_ok)
-    return fail(h, NTK_E_UNSUPPORTED, "the inside-out order needs D <= 64 pixels and O <= 64");
   hipError_t e;
-  // 1. forward pass keeping every conv layer input, then global average pooling
+  // 1. forward pass keeping every spatial layer's input, then global average pooling
   const float* h0 = nullptr;
   int rc0 = cnn_forward(h, params, X1, n1, X2, n2, sym, &h0);
   if (rc0 != NTK_OK) return rc0;
@@ -829,54 +920,86 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
     prof_end(P, s, KC_GRAM);
   }
   if (e != hipSuccess) return hip_fail(h, e, "gram");
-  // 2. cotangents of every conv pre-activation for all O outputs, and per layer the
-  //    weight-space cotangent J_l = sum_p G_l (x) patch_l (outside-in order)
+  // 2. cotangents of every spatial layer's output for all O outputs, and per layer its
+  //    weight-space cotangent columns of J (or its inside-out summand)
   for (int l = 1; l < nc; ++l) {
+    if (h->layers[l].kind != NTK_CONV3X3_SAME) continue;
     prof_begin(P, s, KC_TRANSPOSE);
-    e = launch_conv_flip(s, params[l], h->ch[l + 1], h->ch[l], F(h->off_Kt[l]));
+    e = launch_conv_flip(s, params[h->wslot[l]], h->ch[l + 1], h->ch[l], F(h->off_Kt[l]));
     prof_end(P, s, KC_TRANSPOSE);
     if (e != hipSuccess) return hip_fail(h, e, "kernel flip");
   }
   float* Gcur = F(h->off_Gping);
   float* Gnext = F(h->off_Gpong);
   prof_begin(P, s, KC_CONV_SEED);
-  const float* Wd = params[nc] + (logit ? (size_t)h->opt_logit * C : 0);
-  e = launch_conv_seed(s, Wd, F(h->off_cdphi[nc - 1]), M, Oe, D, C, Gcur);
+  const float* Wd = params[h->rslot] + (logit ? (size_t)h->opt_logit * C : 0);
+  const float* dlast = h->wslot[nc - 1] >= 0 ? F(h->off_cdphi[nc - 1]) : nullptr;
+  e = launch_conv_seed(s, Wd, dlast, M, Oe, h->bh[nc] * h->bw[nc], C, Gcur);
   prof_end(P, s, KC_CONV_SEED);
   if (e != hipSuccess) return hip_fail(h, e, "conv seed");
   float* J = F(h->off_J);
   bool theta_written = false;
   const int n2_off = sym ? 0 : n1;
   for (int l = nc - 1; l >= 0; --l) {
-    if (inside[l]) {
-      PairLayerList pl{};
-      pl.count = 1;
-      pl.h[0] = hptr(l);
-      pl.G[0] = Gcur;
-      pl.Cin[0] = h->ch[l];
-      pl.C[0] = h->ch[l + 1];
-      prof_begin(P, s, KC_CONV_PAIRSUM);
-      e = launch_conv_pairsum(s, pl, n1, n2, n2_off, Oe, H, W, F(h->off_gram_r), theta_written ? 1 : 0,
-                              trace ? 1 : 0, diag ? 1 : 0, theta);
-      prof_end(P, s, KC_CONV_PAIRSUM);
-      if (e != hipSuccess) return hip_fail(h, e, "conv inside-out pair sum");
-      theta_written = true;
-    } else {
-      prof_begin(P, s, KC_CONV_WGRAD);
-      e = launch_conv_wgrad(s, Gcur, hptr(l), M, Oe, H, W, h->ch[l + 1], h->ch[l], J, Kcall, jo[l]);
-      prof_end(P, s, KC_CONV_WGRAD);
-      if (e != hipSuccess) return hip_fail(h, e, "conv weight-space cotangent");
+    const ntk_layer_desc& L = h->layers[l];
+    const int Hl = h->bh[l], Wl = h->bw[l], cin = h->ch[l], cout = h->ch[l + 1];
+    const float* w = h->wslot[l] >= 0 ? params[h->wslot[l]] : nullptr;
+    // Gcur: the cotangent of layer l's pre-activation (of its output for a pool), [M*Oe, ., ., cout]
+    if (L.kind == NTK_CONV3X3_SAME) {
+      if (inside[l]) {
+        PairLayerList pl{};
+        pl.count = 1;
+        pl.h[0] = hptr(l);
+        pl.G[0] = Gcur;
+        pl.Cin[0] = cin;
+        pl.C[0] = cout;
+        prof_begin(P, s, KC_CONV_PAIRSUM);
+        e = launch_conv_pairsum(s, pl, n1, n2, n2_off, Oe, Hl, Wl, F(h->off_gram_r), theta_written ? 1 : 0,
+                                trace ? 1 : 0, diag ? 1 : 0, theta);
+        prof_end(P, s, KC_CONV_PAIRSUM);
+        if (e != hipSuccess) return hip_fail(h, e, "conv inside-out pair sum");
+        theta_written = true;
+      } else {
+        prof_begin(P, s, KC_CONV_WGRAD);
+        e = launch_conv_wgrad(s, Gcur, hptr(l), M, Oe, Hl, Wl, cout, cin, J, Kcall, jw[l]);
+        prof_end(P, s, KC_CONV_WGRAD);
+        if (e != hipSuccess) return hip_fail(h, e, "conv weight-space cotangent");
+      }
+      if (L.has_bias) {
+        prof_begin(P, s, KC_STRUCT_WGRAD);
+        e = launch_pix_wgrad(s, Gcur, nullptr, M, Oe, Hl, Wl, cout, 0, 1, J, Kcall, 0, jb[l]);
+        prof_end(P, s, KC_STRUCT_WGRAD);
+        if (e != hipSuccess) return hip_fail(h, e, "conv bias cotangent");
+      }
+    } else if (L.kind != NTK_AVGPOOL2) {
+      prof_begin(P, s, KC_STRUCT_WGRAD);
+      e = launch_pix_wgrad(s, Gcur, hptr(l), M, Oe, Hl, Wl, cout, L.kind == NTK_DWCONV3X3_SAME ? 9 : 1,
+                           L.has_bias, J, Kcall, jw[l], jb[l]);
+      prof_end(P, s, KC_STRUCT_WGRAD);
+      if (e != hipSuccess) return hip_fail(h, e, "depthwise / scale weight-space cotangent");
     }
     if (l >= 1) {
-      prof_begin(P, s, KC_CONV_BWD);
-      e = launch_conv_bwd(s, Gcur, M, Oe, H, W, h->ch[l + 1], F(h->off_Kt[l]), h->ch[l],
-                          F(h->off_cdphi[l - 1]), Gnext);
-      prof_end(P, s, KC_CONV_BWD);
-      if (e != hipSuccess) return hip_fail(h, e, "conv backward");
+      // to the cotangent of layer l-1's pre-activation (its output, when it has no activation)
+      const float* dprev = h->wslot[l - 1] >= 0 ? F(h->off_cdphi[l - 1]) : nullptr;
+      if (L.kind == NTK_CONV3X3_SAME) {
+        prof_begin(P, s, KC_CONV_BWD);
+        e = launch_conv_bwd(s, Gcur, M, Oe, Hl, Wl, cout, F(h->off_Kt[l]), cin, dprev, Gnext);
+        prof_end(P, s, KC_CONV_BWD);
+      } else {
+        prof_begin(P, s, KC_STRUCT_BWD);
+        if (L.kind == NTK_DWCONV3X3_SAME)
+          e = launch_dw_bwd(s, Gcur, M, Oe, Hl, Wl, cout, w, dprev, Gnext);
+        else if (L.kind == NTK_SCALE)
+          e = launch_scale_bwd(s, Gcur, M, Oe, Hl * Wl, cout, w, dprev, Gnext);
+        else
+          e = launch_pool_bwd(s, Gcur, M, Oe, Hl, Wl, cin, dprev, Gnext);
+        prof_end(P, s, KC_STRUCT_BWD);
+      }
+      if (e != hipSuccess) return hip_fail(h, e, "backward pass");
       std::swap(Gcur, Gnext);
     }
   }
-  // 3. Theta += J1 J2^T over the outside-in layers (deterministic split over K).  The J rows
+  // 3. Theta += J1 J2^T over the columns of J (deterministic split over K).  The J rows
   //    of one sample are contiguous, so the traced variant contracts rows (n) of Oe*Kcall
   //    columns; the batch diagonal contracts each sample's rows with its own.
   if (h->opt_method == NTK_METHOD_JACOBIAN) {
@@ -903,7 +1026,8 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
       t.w[0] = nullptr;
       const bool flat = trace || logit;
       t.K[0] = (flat ? Oe : 1) * Kcall;
-      t.readout = F(h->off_gram_r);
+      // the readout summand is added once: by the first write of theta
+      t.readout = theta_written ? nullptr : F(h->off_gram_r);
       t.readout_scale = rscale;
       prof_begin(P, s, KC_NTK_DIAG);
       e = launch_ntk_diag(s, t, n1, flat ? 0 : O, theta_written ? 1 : 0, theta, F(h->off_part),
@@ -1194,11 +1318,11 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
   for (int l = 0; l < nc; ++l) {
     const int co = h->ch[l + 1];
     prof_begin(P, s, KC_CONV_FWD);
-    e = launch_conv_fwd(s, hptr(l), n1, H, W, h->ch[l], tc + h->joff[l], co, NTK_ACT_NONE,
+    e = launch_conv_fwd(s, hptr(l), n1, H, W, h->ch[l], tc + h->joff[l], co, NTK_ACT_NONE, nullptr,
                         V(h->vp_off_cb), V(h->vp_off_cd));
     if (e == hipSuccess && l > 0)
-      e = launch_conv_fwd(s, tcur, n1, H, W, h->ch[l], params[l], co, NTK_ACT_NONE, V(h->vp_off_ca),
-                          V(h->vp_off_cd));
+      e = launch_conv_fwd(s, tcur, n1, H, W, h->ch[l], params[l], co, NTK_ACT_NONE, nullptr,
+                          V(h->vp_off_ca), V(h->vp_off_cd));
     prof_end(P, s, KC_CONV_FWD);
     if (e != hipSuccess) return hip_fail(h, e, "JVP convolution");
     prof_begin(P, s, KC_VP_ELEMENTWISE);
@@ -1242,7 +1366,7 @@ static int compute_eager(ntk_handle* h, const float* const* params, const float*
 }
 
 static int param_tensor_count(const ntk_handle* h) {
-  if (h->cnn) return h->nc + 1;
+  if (h->cnn) return h->rslot + 1;
   int n = 0;
   for (const auto& L : h->layers) n += 1 + (L.has_bias ? 1 : 0);
   return n;
@@ -1340,6 +1464,9 @@ extern "C" int ntk_vector_product(ntk_handle* h, const float* const* params, con
   if (n1 > h->max_n1 || n2 > h->max_n2)
     return fail(h, NTK_E_ARG, "n1/n2 exceed the max_n1/max_n2 given to ntk_init");
   h->err.clear();
+  if (h->cnn && !h->vp_ok)
+    return fail(h, NTK_E_UNSUPPORTED,
+                "NTK-vector products of convolutional models take bias-free 3x3 convolutions only");
   if (h->cnn) return vector_product_cnn(h, params, X1, n1, X2, n2, v, out);
   return vector_product_fcn(h, params, X1, n1, X2, n2, v, out);
 }

@@ -10,7 +10,8 @@ or N when X2 is X1):
   backward     sum_{1<=l<L} 2 (M O) d_{l+1} d_l          (the N O L W^2 term of Table "FCN")
   gram         sum_{l<=L} 2 N1 N2 d_l                    (the x1.x2 scalars)
   contraction  sum_{l<L} 2 (N1 O)(N2 O) d_{l+1}          (the N^2 O^2 L W term)
-CNN (conv3x3 layers l with Cin_l -> Cout_l on D pixels, GAP, dense readout):
+CNN (conv3x3 layers l with Cin_l -> Cout_l on D pixels, GAP, dense readout; the further
+layer kinds are listed in `cnn_flops`):
   forward      sum_l 2 M D 9 Cin_l Cout_l
   backward     sum_{l>=1} 2 (M O D) 9 Cout_l Cin_l
   wgrad        sum_l 2 M (O Cout_l) (9 Cin_l) D           (outside-in weight-space Jacobian)
@@ -63,28 +64,77 @@ def fcn_flops(spec, n1, n2, symmetric=False, output="full", batch="full"):
     return st
 
 
+def _spatial_layers(spec):
+    """(kind, Cin, Cout, D = pixels of the layer's input, bias) of each layer before the global
+    pool, and the channels that reach the pool."""
+    H, W, c = spec["input_shape"]
+    out = []
+    for Lr in spec["layers"]:
+        k = Lr["kind"]
+        if k in ("gap", "dense"):
+            continue
+        if k == "avgpool2":
+            out.append((k, c, c, H * W, False))
+            H, W = H // 2, W // 2
+        else:
+            out.append((k, c, Lr["out"], H * W, bool(Lr.get("bias"))))
+            c = Lr["out"]
+    return out, c
+
+
+def _weight_cols(kind, cin, cout):
+    return {"conv3x3": 9 * cin * cout, "dwconv3x3": 9 * cout, "scale": cout}.get(kind, 0)
+
+
 def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", batch="full"):
+    """CNN counts per stage.  3x3 convolutions as in the module docstring; the further layer
+    kinds (memory-bound, counted for completeness): depthwise 3x3 forward, backward and
+    weight-space cotangent 2 M (Oe) D 9 C each; scale forward 2 M D C, backward M Oe D C,
+    cotangent 2 M Oe D C; a 2x2 pool M D C forward and M Oe D C backward (D: its input
+    pixels); a bias M D C forward and its cotangent (a pixel sum) M Oe D C.  The contraction
+    covers every weight-space column (9 Cin Cout, 9 C, C, and C per bias)."""
     layers = spec["layers"]
-    H, W, _ = spec["input_shape"]
-    D = H * W
-    convs = [Lr for Lr in layers if Lr["kind"] == "conv3x3"]
+    sp, C = _spatial_layers(spec)
     O = layers[-1]["out"]
-    C = convs[-1]["out"]
     Oe, Oc, pairs = _variant(O, n1, n2, output, batch, symmetric)
     gpairs = n1 if batch == "diagonal" else n1 * n2
     M = n1 if symmetric else n1 + n2
-    st = {
-        "forward": sum(2.0 * M * D * 9 * c["in"] * c["out"] for c in convs),
-        "backward": sum(2.0 * M * Oe * D * 9 * c["out"] * c["in"] for c in convs[1:]),
-        "gram": 2.0 * gpairs * C,
-    }
-    if order == "outside_in":
-        st["wgrad"] = sum(2.0 * M * (Oe * c["out"]) * (9 * c["in"]) * D for c in convs)
-        st["contraction"] = 2.0 * pairs * Oc * sum(c["out"] * 9 * c["in"] for c in convs)
-    else:  # inside-out: patch Gram, one-sided cotangent contraction, then the O x O product
-        # (every input pair, also on the symmetric schedule)
-        st["contraction"] = sum(2.0 * gpairs * (D * D * 9 * c["in"] + Oe * D * D * c["out"]
-                                                + Oc * D * c["out"]) for c in convs)
+    fwd = bwd = wg = cols = io = 0.0
+    for i, (k, cin, cout, D, bias) in enumerate(sp):
+        if k == "conv3x3":
+            fwd += 2.0 * M * D * 9 * cin * cout
+            if i >= 1:
+                bwd += 2.0 * M * Oe * D * 9 * cout * cin
+            if order == "outside_in":
+                wg += 2.0 * M * (Oe * cout) * (9 * cin) * D
+                cols += 9 * cin * cout
+            else:  # inside-out: patch Gram, one-sided cotangent contraction, then the O x O product
+                # (every input pair, also on the symmetric schedule)
+                io += 2.0 * gpairs * (D * D * 9 * cin + Oe * D * D * cout + Oc * D * cout)
+        elif k == "dwconv3x3":
+            fwd += 2.0 * M * D * 9 * cout
+            if i >= 1:
+                bwd += 2.0 * M * Oe * D * 9 * cout
+            wg += 2.0 * M * Oe * D * 9 * cout
+            cols += 9 * cout
+        elif k == "scale":
+            fwd += 2.0 * M * D * cout
+            if i >= 1:
+                bwd += 1.0 * M * Oe * D * cout
+            wg += 2.0 * M * Oe * D * cout
+            cols += cout
+        else:  # avgpool2
+            fwd += 1.0 * M * D * cout
+            if i >= 1:
+                bwd += 1.0 * M * Oe * D * cout
+        if bias:
+            fwd += 1.0 * M * D * cout
+            wg += 1.0 * M * Oe * D * cout
+            cols += cout
+    st = {"forward": fwd, "backward": bwd, "gram": 2.0 * gpairs * C}
+    if wg:
+        st["wgrad"] = wg
+    st["contraction"] = 2.0 * pairs * Oc * cols + io
     st["total"] = sum(st.values())
     return st
 
@@ -92,15 +142,19 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
 def param_total(spec):
     P = 0
     for Lr in spec["layers"]:
-        if Lr["kind"] == "dense":
-            P += Lr["out"] * Lr["in"] + (Lr["out"] if Lr.get("bias") else 0)
-        elif Lr["kind"] == "conv3x3":
-            P += Lr["out"] * 9 * Lr["in"]
+        k = Lr["kind"]
+        if k == "dense":
+            P += Lr["out"] * Lr["in"]
+        elif k in ("conv3x3", "dwconv3x3", "scale"):
+            P += _weight_cols(k, Lr["in"], Lr["out"])
+        else:
+            continue
+        P += Lr["out"] if Lr.get("bias") else 0
     return P
 
 
 def ntk_flops(spec, n1, n2, symmetric=False, method="structured", **kw):
-    cnn = any(Lr["kind"] == "conv3x3" for Lr in spec["layers"])
+    cnn = any(Lr["kind"] != "dense" for Lr in spec["layers"])
     if method == "jacobian":
         kw["order"] = "outside_in"
     if cnn:

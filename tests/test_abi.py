@@ -56,8 +56,10 @@ def test_init_rejects_bad_models_before_any_device_call(lib):
     act_readout["layers"][-1]["act"] = "relu"
     assert _init(lib, act_readout)[0] == _lib.NTK_E_UNSUPPORTED
 
-    conv_bias = wl.cnn_spec("b", (4, 4), 3, [8], 2, bias=True)
-    assert _init(lib, conv_bias)[0] == _lib.NTK_E_UNSUPPORTED
+    # a CNN readout takes no bias
+    readout_bias = wl.cnn_spec("b", (4, 4), 3, [8], 2)
+    readout_bias["layers"][-1]["bias"] = True
+    assert _init(lib, readout_bias)[0] == _lib.NTK_E_UNSUPPORTED
 
     no_gap = wl.cnn_spec("b", (4, 4), 3, [8], 2)
     del no_gap["layers"][1]
@@ -91,3 +93,46 @@ def test_diagnostics_reject_bad_arguments_before_any_device_call(lib):
     assert lib.ntk_mfma_peak(0, None) == _lib.NTK_E_ARG
     cu = ctypes.c_int(0)
     assert lib.ntk_device_info(ctypes.byref(cu), None) == _lib.NTK_E_ARG
+
+
+def _struct(blocks, hw=(4, 6), c=4):
+    return wl.cnn_layers_spec("s", hw, c, blocks, 3)
+
+
+def test_init_validates_the_structured_layer_kinds(lib):
+    from paper_2206_08720_amd import _lib
+    # an average pool needs an even image, and takes no activation
+    assert _init(lib, _struct([("conv3x3", 4, "relu", True), ("avgpool2",)], hw=(5, 6)))[0] == _lib.NTK_E_SHAPE
+    assert "even" in _lib.last_error()
+    s = _struct([("conv3x3", 4, "relu", True), ("avgpool2",)])
+    s["layers"][1]["act"] = "relu"
+    assert _init(lib, s)[0] == _lib.NTK_E_UNSUPPORTED
+    # a second pool of a 2 x 2 image leaves 1 x 1; a third would need an even 1 x 1 image
+    assert _init(lib, _struct([("scale", "none", False)] + [("avgpool2",)] * 3, hw=(4, 4)))[0] == \
+        _lib.NTK_E_SHAPE
+    # depthwise and scale layers keep the channel count
+    s = _struct([("dwconv3x3", "relu", True)])
+    s["layers"][0]["out"] = 8
+    assert _init(lib, s)[0] == _lib.NTK_E_SHAPE
+    s = _struct([("scale", "relu", True)])
+    s["layers"][0]["in"] = 3
+    assert _init(lib, s)[0] == _lib.NTK_E_SHAPE
+    # at least one layer with parameters before the global pool
+    assert _init(lib, _struct([("avgpool2",)]))[0] == _lib.NTK_E_UNSUPPORTED
+    # spatial kinds are not accepted between dense layers
+    fcn = wl.fcn_spec("f", 8, [8], 3)
+    fcn["layers"].insert(1, {"kind": "scale", "in": 8, "out": 8, "act": "none", "bias": False})
+    assert _init(lib, fcn)[0] == _lib.NTK_E_UNSUPPORTED
+
+
+def test_init_accepts_the_structured_layer_kinds(lib):
+    from paper_2206_08720_amd import _lib
+    spec = _struct([("conv3x3", 4, "relu", True), ("dwconv3x3", "erf", True), ("avgpool2",),
+                    ("scale", "none", True), ("conv3x3", 6, "relu", False)])
+    rc, h = _init(lib, spec)
+    try:
+        # validation passes; without a GPU the first device call then fails
+        assert rc in (_lib.NTK_OK, _lib.NTK_E_HIP), _lib.last_error()
+    finally:
+        if h.value:
+            lib.ntk_free(h)

@@ -79,3 +79,21 @@ def test_jacobian_contraction_count_is_the_papers_n2_o2_p():
         assert jc["contraction"] == 2 * n1 * n2 * O * O * oracle.param_count(spec)
     spec, _, _, _ = wl.make_workload("relu_mlp_d8_w2048")
     assert ntk_flops(spec, 512, 512, method="jacobian")["contraction"] == pytest.approx(1.87e15, rel=1e-2)
+
+
+def test_structured_layer_kinds_counts():
+    import oracle
+    from paper_2206_08720_amd.flops import ntk_flops, param_total
+    N, O = 3, 4
+    spec = wl.cnn_layers_spec("s", (4, 6), 2, [("conv3x3", 8, "relu", True), ("avgpool2",),
+                                               ("dwconv3x3", "erf", True), ("scale", "none", False)], O)
+    f = cnn_flops(spec, N, N)
+    M, D0, D1 = 2 * N, 24, 6
+    assert f["forward"] == 2 * M * D0 * 9 * 2 * 8 + M * D0 * 8 + M * D0 * 8 \
+        + 2 * M * D1 * 9 * 8 + M * D1 * 8 + 2 * M * D1 * 8
+    assert f["backward"] == M * O * D0 * 8 + 2 * M * O * D1 * 9 * 8 + M * O * D1 * 8
+    # J columns: 9 Cin Cout + Cout (conv and its bias), 9 C + C (depthwise and bias), C (scale)
+    assert f["contraction"] == 2 * N * N * O * O * (9 * 2 * 8 + 8 + 9 * 8 + 8 + 8)
+    assert param_total(spec) == oracle.param_count(spec) == 9 * 2 * 8 + 8 + 9 * 8 + 8 + 8 + 8 * O
+    jc = ntk_flops(spec, N, N, method="jacobian")
+    assert jc["contraction"] == 2 * N * N * O * O * oracle.param_count(spec)
