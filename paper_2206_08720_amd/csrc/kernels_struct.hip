@@ -80,41 +80,83 @@ dim3 plane_grid(long long rows, long long plane) {
   return dim3(bx, by);
 }
 
+// ------------------------------------------------------------------------------ 3x3 windows
+// A lane computes XS consecutive output pixels of one image row for V channels:
+//   acc[j] = sum_{kh, kw} src(y + kh - 1, x0 + j + kw - 1) * tap[kh*3 + kw]   (zero outside).
+// The 3 x (XS + 2) input pixels the outputs share are loaded first, all at once (each load
+// from a clamped, valid address, the value zeroed outside the image, so no load waits behind a
+// branch), then the XS outputs are formed: 3 (XS + 2) loads instead of 9 XS.
+template <int V, int XS, typename A>
+__device__ __forceinline__ void dw_segment(const float* __restrict__ img, int H, int W, int C, int c0, int y,
+                                           int x0, const Vf<V> (&tap)[9], A (&acc)[XS][V]) {
+  Vf<V> win[3][XS + 2];
+#pragma unroll
+  for (int kh = 0; kh < 3; ++kh) {
+    const int sy = y + kh - 1;
+    const int syc = min(max(sy, 0), H - 1);
+#pragma unroll
+    for (int j = 0; j < XS + 2; ++j) {
+      const int xc = x0 + j - 1;
+      const bool ok = (unsigned)sy < (unsigned)H && (unsigned)xc < (unsigned)W;
+      const int xcc = min(max(xc, 0), W - 1);
+      const Vf<V> t = ldv<V>(img + ((long long)syc * W + xcc) * C + c0);
+#pragma unroll
+      for (int v = 0; v < V; ++v) win[kh][j].v[v] = ok ? t.v[v] : 0.f;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < XS; ++j) {
+#pragma unroll
+    for (int v = 0; v < V; ++v) {
+      A sum = 0;
+#pragma unroll
+      for (int kh = 0; kh < 3; ++kh)
+#pragma unroll
+        for (int kw = 0; kw < 3; ++kw) sum += (A)win[kh][j + kw].v[v] * (A)tap[kh * 3 + kw].v[v];
+      acc[j][v] = sum;
+    }
+  }
+}
+
 // ------------------------------------------------------------------------------ forward
-template <int V>
+// Work item q of an image = ((y * XB + xb) * CG + cg): XS pixels of row y from x0 = xb * XS.
+template <int V, int XS>
 __global__ void __launch_bounds__(256)
-k_dw_fwd(const float* __restrict__ x, int images, int H, int W, FastDiv fCG, FastDiv fW,
+k_dw_fwd(const float* __restrict__ x, int images, int H, int W, FastDiv fCG, FastDiv fXB,
          const float* __restrict__ w, const float* __restrict__ bias, int act, float* __restrict__ hn,
          float* __restrict__ dphi) {
-  const int CG = (int)fCG.d, C = CG * V;
-  const int plane = H * W * CG;
+  const int CG = (int)fCG.d, C = CG * V, XB = (int)fXB.d;
+  const int plane = H * XB * CG;
   const long long img_elems = (long long)H * W * C;
   for (int n = blockIdx.y; n < images; n += gridDim.y) {
     const float* xi = x + (long long)n * img_elems;
     for (int q = blockIdx.x * 256 + threadIdx.x; q < plane; q += gridDim.x * 256) {
-      const int p = (int)fCG.div(q), cg = q - p * CG;
-      const int yy = (int)fW.div(p), xx = p - yy * W;
-      const int c0 = cg * V;
-      double acc[V];
+      const int rest = (int)fCG.div(q), cg = q - rest * CG;
+      const int yy = (int)fXB.div(rest), xb = rest - yy * XB;
+      const int c0 = cg * V, x0 = xb * XS;
+      Vf<V> tap[9];
 #pragma unroll
-      for (int v = 0; v < V; ++v) acc[v] = 0.0;
+      for (int t = 0; t < 9; ++t) tap[t] = ldv<V>(w + t * C + c0);
+      Vf<V> bv;
+      if (bias) {
+        bv = ldv<V>(bias + c0);
+      } else {
 #pragma unroll
-      for (int t = 0; t < 9; ++t) {
-        const int sy = yy + t / 3 - 1, sx = xx + t % 3 - 1;
-        if ((unsigned)sy < (unsigned)H && (unsigned)sx < (unsigned)W) {
-          const Vf<V> a = ldv<V>(xi + (long long)(sy * W + sx) * C + c0);
-          const Vf<V> b = ldv<V>(w + t * C + c0);
+        for (int v = 0; v < V; ++v) bv.v[v] = 0.f;
+      }
+      double acc[XS][V];
+      dw_segment<V, XS, double>(xi, H, W, C, c0, yy, x0, tap, acc);
 #pragma unroll
-          for (int v = 0; v < V; ++v) acc[v] += (double)a.v[v] * (double)b.v[v];
+      for (int j = 0; j < XS; ++j) {
+        if (x0 + j < W) {
+          Vf<V> ho, dv;
+#pragma unroll
+          for (int v = 0; v < V; ++v) act_pair(act, acc[j][v] + (double)bv.v[v], ho.v[v], dv.v[v]);
+          const long long o = n * img_elems + ((long long)yy * W + x0 + j) * C + c0;
+          stv<V>(hn + o, ho);
+          stv<V>(dphi + o, dv);
         }
       }
-      Vf<V> ho, dv;
-#pragma unroll
-      for (int v = 0; v < V; ++v)
-        act_pair(act, acc[v] + (bias ? (double)bias[c0 + v] : 0.0), ho.v[v], dv.v[v]);
-      const long long o = (long long)n * img_elems + (long long)p * C + c0;
-      stv<V>(hn + o, ho);
-      stv<V>(dphi + o, dv);
     }
   }
 }
@@ -167,45 +209,49 @@ k_pool_fwd(const float* __restrict__ x, int images, int Ho, int Wo, FastDiv fCG,
 }
 
 // ------------------------------------------------------------------------------ backward
-// input pixel q receives G at output pixel q - offset(t) through tap t (zero outside the image)
-template <int V>
+// Input pixel q receives G at output pixel q - offset(t) through tap t: the same 3x3 window
+// with the taps flipped, tap'[kh*3 + kw] = w[(2 - kh)*3 + (2 - kw)].
+template <int V, int XS>
 __global__ void __launch_bounds__(256)
-k_dw_bwd(const float* __restrict__ G, int rows, int O, int H, int W, FastDiv fCG, FastDiv fW,
+k_dw_bwd(const float* __restrict__ G, int rows, int O, int H, int W, FastDiv fCG, FastDiv fXB,
          const float* __restrict__ w, const float* __restrict__ dphi, float* __restrict__ out) {
-  const int CG = (int)fCG.d, C = CG * V;
-  const int plane = H * W * CG;
+  const int CG = (int)fCG.d, C = CG * V, XB = (int)fXB.d;
+  const int plane = H * XB * CG;
   const long long img_elems = (long long)H * W * C;
   for (int r = blockIdx.y; r < rows; r += gridDim.y) {
     const float* Gr = G + (long long)r * img_elems;
     const long long dbase = (long long)(r / O) * img_elems;
     for (int q = blockIdx.x * 256 + threadIdx.x; q < plane; q += gridDim.x * 256) {
-      const int p = (int)fCG.div(q), cg = q - p * CG;
-      const int yy = (int)fW.div(p), xx = p - yy * W;
-      const int c0 = cg * V;
-      float acc[V];
+      const int rest = (int)fCG.div(q), cg = q - rest * CG;
+      const int yy = (int)fXB.div(rest), xb = rest - yy * XB;
+      const int c0 = cg * V, x0 = xb * XS;
+      Vf<V> tap[9];
 #pragma unroll
-      for (int v = 0; v < V; ++v) acc[v] = 0.f;
+      for (int t = 0; t < 9; ++t) tap[t] = ldv<V>(w + (8 - t) * C + c0);
+      // act' of the output pixels (clamped column, unused past W), issued with the window's loads
+      Vf<V> d[XS];
+      if (dphi) {
 #pragma unroll
-      for (int t = 0; t < 9; ++t) {
-        const int sy = yy - (t / 3 - 1), sx = xx - (t % 3 - 1);
-        if ((unsigned)sy < (unsigned)H && (unsigned)sx < (unsigned)W) {
-          const Vf<V> g = ldv<V>(Gr + (long long)(sy * W + sx) * C + c0);
-          const Vf<V> b = ldv<V>(w + t * C + c0);
+        for (int j = 0; j < XS; ++j)
+          d[j] = ldv<V>(dphi + dbase + ((long long)yy * W + min(x0 + j, W - 1)) * C + c0);
+      }
+      float acc[XS][V];
+      dw_segment<V, XS, float>(Gr, H, W, C, c0, yy, x0, tap, acc);
+      if (dphi) {
 #pragma unroll
-          for (int v = 0; v < V; ++v) acc[v] += g.v[v] * b.v[v];
+        for (int j = 0; j < XS; ++j)
+#pragma unroll
+          for (int v = 0; v < V; ++v) acc[j][v] *= d[j].v[v];
+      }
+#pragma unroll
+      for (int j = 0; j < XS; ++j) {
+        if (x0 + j < W) {
+          Vf<V> res;
+#pragma unroll
+          for (int v = 0; v < V; ++v) res.v[v] = acc[j][v];
+          stv<V>(out + (long long)r * img_elems + ((long long)yy * W + x0 + j) * C + c0, res);
         }
       }
-      const long long o = (long long)p * C + c0;
-      Vf<V> res;
-      if (dphi) {
-        const Vf<V> d = ldv<V>(dphi + dbase + o);
-#pragma unroll
-        for (int v = 0; v < V; ++v) res.v[v] = acc[v] * d.v[v];
-      } else {
-#pragma unroll
-        for (int v = 0; v < V; ++v) res.v[v] = acc[v];
-      }
-      stv<V>(out + (long long)r * img_elems + o, res);
     }
   }
 }
@@ -238,53 +284,64 @@ k_scale_bwd(const float* __restrict__ G, int rows, int O, int D, FastDiv fCG, co
 }
 
 // H, W: the pool's input; every input pixel of a 2x2 window receives a quarter of the window's
-// cotangent
+// cotangent.  A lane takes one pooled pixel and writes its window.
 template <int V>
 __global__ void __launch_bounds__(256)
-k_pool_bwd(const float* __restrict__ G, int rows, int O, int H, int W, FastDiv fCG, FastDiv fW,
+k_pool_bwd(const float* __restrict__ G, int rows, int O, int H, int W, FastDiv fCG, FastDiv fWo,
            const float* __restrict__ dphi, float* __restrict__ out) {
   const int CG = (int)fCG.d, C = CG * V;
-  const int plane = H * W * CG;
   const int Wo = W / 2;
+  const int plane = (H / 2) * Wo * CG;
   const long long img_elems = (long long)H * W * C;
   const long long gimg_elems = img_elems / 4;
   for (int r = blockIdx.y; r < rows; r += gridDim.y) {
-    const float* Gr = G + (long long)r * gimg_elems;
     const long long dbase = (long long)(r / O) * img_elems;
     for (int q = blockIdx.x * 256 + threadIdx.x; q < plane; q += gridDim.x * 256) {
-      const int p = (int)fCG.div(q), c0 = (q - p * CG) * V;
-      const int yy = (int)fW.div(p), xx = p - yy * W;
-      const Vf<V> g = ldv<V>(Gr + (long long)((yy >> 1) * Wo + (xx >> 1)) * C + c0);
-      const long long o = (long long)p * C + c0;
-      Vf<V> res;
+      const int pq = (int)fCG.div(q), c0 = (q - pq * CG) * V;
+      const int yo = (int)fWo.div(pq), xo = pq - yo * Wo;
+      const Vf<V> g = ldv<V>(G + (long long)r * gimg_elems + (long long)pq * C + c0);
+      long long o[4];
 #pragma unroll
-      for (int v = 0; v < V; ++v) res.v[v] = g.v[v] * 0.25f;
+      for (int i = 0; i < 4; ++i) o[i] = ((long long)(2 * yo + (i >> 1)) * W + 2 * xo + (i & 1)) * C + c0;
+      Vf<V> res[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int v = 0; v < V; ++v) res[i].v[v] = g.v[v] * 0.25f;
       if (dphi) {
-        const Vf<V> d = ldv<V>(dphi + dbase + o);
+        Vf<V> d[4];
 #pragma unroll
-        for (int v = 0; v < V; ++v) res.v[v] *= d.v[v];
+        for (int i = 0; i < 4; ++i) d[i] = ldv<V>(dphi + dbase + o[i]);
+#pragma unroll
+        for (int i = 0; i < 4; ++i)
+#pragma unroll
+          for (int v = 0; v < V; ++v) res[i].v[v] *= d[i].v[v];
       }
-      stv<V>(out + (long long)r * img_elems + o, res);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) stv<V>(out + (long long)r * img_elems + o[i], res[i]);
     }
   }
 }
 
 // ------------------------------------------------------------------------------ pixel sums
-// One workgroup per row r = img*O + o (grid-stride).  Lanes take V-channel groups (at most 256
-// groups per pass) and pixel groups; each lane accumulates NA = TAPS (+1 with a bias) sums over
-// its pixels, and the pixel groups' partial sums are added in a fixed order through LDS.
+// Scale and bias columns (TAPS = 1: sum_p G x, and/or the bias sum_p G).  One workgroup per row
+// r = img*O + o (grid-stride).  Lanes take V-channel groups (at most 256 groups per pass) and
+// pixel groups; each lane accumulates NA = TAPS (+1 with a bias) sums over its pixels, four
+// pixels per step with their loads issued together (clamped pixel index, the sums of pixels past
+// D masked), and the pixel groups' partial sums are added in a fixed order through LDS.
 template <int V, int TAPS, bool BIAS>
 __global__ void __launch_bounds__(256)
-k_pix_wgrad(const float* __restrict__ G, const float* __restrict__ x, int rows, int O, int H, int W,
-            FastDiv fW, int C, float* __restrict__ J, long long ldJ, long long off_w, long long off_b) {
+k_pix_wgrad(const float* __restrict__ G, const float* __restrict__ x, int rows, int O, int D, int C,
+            float* __restrict__ J, long long ldJ, long long off_w, long long off_b) {
+  static_assert(TAPS == 0 || TAPS == 1, "depthwise columns are formed by k_dw_wgrad");
   constexpr int NA = TAPS + (BIAS ? 1 : 0);
+  constexpr int U = 4;
   __shared__ float red[256 * NA * V];
   const int CG = C / V;
   const int cgb = CG < 256 ? CG : 256;   // channel groups per pass
   const int PG = 256 / cgb;              // pixel groups
   const int tid = threadIdx.x;
   const int lcg = tid % cgb, pg = tid / cgb;
-  const int D = H * W;
   const long long img_elems = (long long)D * C;
   for (int r = blockIdx.x; r < rows; r += gridDim.x) {
     const float* Gr = G + (long long)r * img_elems;
@@ -299,28 +356,25 @@ k_pix_wgrad(const float* __restrict__ G, const float* __restrict__ x, int rows, 
         for (int v = 0; v < V; ++v) acc[a][v] = 0.f;
       if (active) {
         const int c0 = cg * V;
-        for (int p = pg; p < D; p += PG) {
-          const Vf<V> g = ldv<V>(Gr + (long long)p * C + c0);
-          if constexpr (TAPS == 9) {
-            const int yy = (int)fW.div(p), xx = p - yy * W;
+        for (int p = pg; p < D; p += U * PG) {
+          Vf<V> g[U], a[U];
+          float m[U];
 #pragma unroll
-            for (int t = 0; t < 9; ++t) {
-              const int sy = yy + t / 3 - 1, sx = xx + t % 3 - 1;
-              if ((unsigned)sy < (unsigned)H && (unsigned)sx < (unsigned)W) {
-                const Vf<V> a = ldv<V>(xi + (long long)(sy * W + sx) * C + c0);
+          for (int u = 0; u < U; ++u) {
+            const int pu = p + u * PG;
+            m[u] = pu < D ? 1.f : 0.f;
+            const long long o = (long long)min(pu, D - 1) * C + c0;
+            g[u] = ldv<V>(Gr + o);
+            if constexpr (TAPS == 1) a[u] = ldv<V>(xi + o);
+          }
 #pragma unroll
-                for (int v = 0; v < V; ++v) acc[t][v] += g.v[v] * a.v[v];
-              }
+          for (int u = 0; u < U; ++u)
+#pragma unroll
+            for (int v = 0; v < V; ++v) {
+              const float gv = g[u].v[v] * m[u];
+              if constexpr (TAPS == 1) acc[0][v] += gv * a[u].v[v];
+              if constexpr (BIAS) acc[TAPS][v] += gv;
             }
-          } else if constexpr (TAPS == 1) {
-            const Vf<V> a = ldv<V>(xi + (long long)p * C + c0);
-#pragma unroll
-            for (int v = 0; v < V; ++v) acc[0][v] += g.v[v] * a.v[v];
-          }
-          if constexpr (BIAS) {
-#pragma unroll
-            for (int v = 0; v < V; ++v) acc[TAPS][v] += g.v[v];
-          }
         }
       }
       __syncthreads();   // the previous pass's reduction has read `red`
@@ -346,25 +400,115 @@ k_pix_wgrad(const float* __restrict__ G, const float* __restrict__ x, int rows, 
   }
 }
 
+// Depthwise form (9 taps, optional bias): the nine shifted input pixels of a pixel are shared
+// by the O cotangent rows of its image, so a workgroup takes one image, one band of its pixels
+// and 64 channels (lane = channel, wave = pixel group), loads the nine taps once per pixel and
+// accumulates them against OB rows (n, o) at a time.  The four waves' sums are added in a
+// fixed order through LDS; with several bands, each band writes its sums to `part`
+// ([band][row][10 C], bias last) and k_band_reduce adds the bands in order.
+constexpr int kDwOB = 8;
+
+template <bool BIAS>
+__global__ void __launch_bounds__(256)
+k_dw_wgrad(const float* __restrict__ G, const float* __restrict__ x, int images, int O, int H, int W,
+           FastDiv fW, int C, int bands, int cgroups, float* __restrict__ out, long long ld_out,
+           long long off_w, long long off_b, long long band_stride) {
+  constexpr int NA = 9 + (BIAS ? 1 : 0);
+  __shared__ float red[4][NA][64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int D = H * W;
+  const int per_band = (D + bands - 1) / bands;
+  const long long img_elems = (long long)D * C;
+  const int work = images * bands * cgroups;
+  for (int wg = blockIdx.x; wg < work; wg += gridDim.x) {
+    const int cgi = wg % cgroups, rest = wg / cgroups;
+    const int band = rest % bands, n = rest / bands;
+    const int cc = min(cgi * 64 + lane, C - 1);   // lanes past C load a valid channel, unused
+    const int p0 = band * per_band, p1 = min(D, p0 + per_band);
+    const float* xi = x + (long long)n * img_elems;
+    for (int o0 = 0; o0 < O; o0 += kDwOB) {
+      float acc[kDwOB][NA];
+#pragma unroll
+      for (int i = 0; i < kDwOB; ++i)
+#pragma unroll
+        for (int a = 0; a < NA; ++a) acc[i][a] = 0.f;
+      for (int p = p0 + wave; p < p1; p += 4) {
+        const int yy = (int)fW.div(p), xx = p - yy * W;
+        // every load reads a valid address (clamped pixel, clamped row) and is issued without a
+        // branch, so the 17 loads of a pixel are in flight together; rows past O accumulate
+        // sums that are never stored
+        float xt[9], g[kDwOB];
+#pragma unroll
+        for (int t = 0; t < 9; ++t) {
+          const int sy = yy + t / 3 - 1, sx = xx + t % 3 - 1;
+          const bool ok = (unsigned)sy < (unsigned)H && (unsigned)sx < (unsigned)W;
+          const int syc = min(max(sy, 0), H - 1), sxc = min(max(sx, 0), W - 1);
+          const float v = xi[(long long)(syc * W + sxc) * C + cc];
+          xt[t] = ok ? v : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < kDwOB; ++i)
+          g[i] = G[((long long)n * O + min(o0 + i, O - 1)) * img_elems + (long long)p * C + cc];
+#pragma unroll
+        for (int i = 0; i < kDwOB; ++i) {
+#pragma unroll
+          for (int t = 0; t < 9; ++t) acc[i][t] += g[i] * xt[t];
+          if constexpr (BIAS) acc[i][9] += g[i];
+        }
+      }
+#pragma unroll
+      for (int i = 0; i < kDwOB; ++i) {
+        if (o0 + i >= O) break;   // uniform over the workgroup
+        __syncthreads();          // the previous row's sums have been read
+#pragma unroll
+        for (int a = 0; a < NA; ++a) red[wave][a][lane] = acc[i][a];
+        __syncthreads();
+        const long long r = (long long)n * O + o0 + i;
+        for (int j = threadIdx.x; j < NA * 64; j += 256) {
+          const int a = j >> 6, l = j & 63;
+          const int c = cgi * 64 + l;
+          if (c < C) {
+            const float sum = ((red[0][a][l] + red[1][a][l]) + red[2][a][l]) + red[3][a][l];
+            const long long col = a < 9 ? off_w + (long long)a * C + c : off_b + c;
+            out[band * band_stride + r * ld_out + col] = sum;
+          }
+        }
+      }
+    }
+  }
+}
+
+// J[r, off_w + j] (j < 9 C) and J[r, off_b + j - 9 C] (the bias, 9 C <= j < ncols) = sum over the
+// bands of part[band][r][j] (row stride 10 C), in band order.
+__global__ void __launch_bounds__(256)
+k_band_reduce(const float* __restrict__ part, int bands, long long rows, int ncols, int C,
+              float* __restrict__ J, long long ldJ, long long off_w, long long off_b) {
+  const long long total = rows * ncols, band_stride = rows * 10LL * C;
+  for (long long i = blockIdx.x * 256LL + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
+    const long long r = i / ncols;
+    const int j = (int)(i - r * ncols);
+    const long long src = r * 10LL * C + j;
+    float sum = 0.f;
+    for (int b = 0; b < bands; ++b) sum += part[b * band_stride + src];
+    J[r * ldJ + (j < 9 * C ? off_w + j : off_b + (j - 9 * C))] = sum;
+  }
+}
+
 template <int V, int TAPS, bool BIAS>
-hipError_t pix_wgrad_t(hipStream_t s, const float* G, const float* x, int rows, int O, int H, int W, int C,
-                       float* J, long long ldJ, long long off_w, long long off_b) {
+hipError_t pix_wgrad_t(hipStream_t s, const float* G, const float* x, int rows, int O, int D, int C, float* J,
+                       long long ldJ, long long off_w, long long off_b) {
   const int grid = std::max(1, std::min(rows, 1 << 20));
-  k_pix_wgrad<V, TAPS, BIAS><<<dim3(grid), dim3(256), 0, s>>>(G, x, rows, O, H, W, FastDiv((uint32_t)W), C, J,
-                                                              ldJ, off_w, off_b);
+  k_pix_wgrad<V, TAPS, BIAS><<<dim3(grid), dim3(256), 0, s>>>(G, x, rows, O, D, C, J, ldJ, off_w, off_b);
   return hipGetLastError();
 }
 
 template <int V>
-hipError_t pix_wgrad_v(hipStream_t s, const float* G, const float* x, int rows, int O, int H, int W, int C,
-                       int taps, int bias, float* J, long long ldJ, long long off_w, long long off_b) {
-  if (taps == 9)
-    return bias ? pix_wgrad_t<V, 9, true>(s, G, x, rows, O, H, W, C, J, ldJ, off_w, off_b)
-                : pix_wgrad_t<V, 9, false>(s, G, x, rows, O, H, W, C, J, ldJ, off_w, off_b);
+hipError_t pix_wgrad_v(hipStream_t s, const float* G, const float* x, int rows, int O, int D, int C, int taps,
+                       int bias, float* J, long long ldJ, long long off_w, long long off_b) {
   if (taps == 1)
-    return bias ? pix_wgrad_t<V, 1, true>(s, G, x, rows, O, H, W, C, J, ldJ, off_w, off_b)
-                : pix_wgrad_t<V, 1, false>(s, G, x, rows, O, H, W, C, J, ldJ, off_w, off_b);
-  if (taps == 0 && bias) return pix_wgrad_t<V, 0, true>(s, G, x, rows, O, H, W, C, J, ldJ, off_w, off_b);
+    return bias ? pix_wgrad_t<V, 1, true>(s, G, x, rows, O, D, C, J, ldJ, off_w, off_b)
+                : pix_wgrad_t<V, 1, false>(s, G, x, rows, O, D, C, J, ldJ, off_w, off_b);
+  if (taps == 0 && bias) return pix_wgrad_t<V, 0, true>(s, G, x, rows, O, D, C, J, ldJ, off_w, off_b);
   return hipErrorInvalidValue;
 }
 
@@ -382,15 +526,19 @@ bool plane_fits(long long images, long long plane) {
 }  // namespace
 
 // ------------------------------------------------------------------------------ launchers
+// pixels per lane of the depthwise forward (fp64 sums) and backward (fp32)
+constexpr int kDwFwdXS = 4, kDwBwdXS = 8;
+
 hipError_t launch_dw_fwd(hipStream_t s, const float* x, int images, int H, int W, int C, const float* w,
                          const float* bias, int act, float* hn, float* dphi) {
   if (!plane_fits(images, (long long)H * W * C)) return hipErrorInvalidValue;
+  const int XB = cdiv_i(W, kDwFwdXS);
   if (use_vec4(C, {x, w, hn, dphi})) {
-    k_dw_fwd<4><<<plane_grid(images, (long long)H * W * C / 4), dim3(256), 0, s>>>(
-        x, images, H, W, FastDiv((uint32_t)(C / 4)), FastDiv((uint32_t)W), w, bias, act, hn, dphi);
+    k_dw_fwd<4, kDwFwdXS><<<plane_grid(images, (long long)H * XB * C / 4), dim3(256), 0, s>>>(
+        x, images, H, W, FastDiv((uint32_t)(C / 4)), FastDiv((uint32_t)XB), w, bias, act, hn, dphi);
   } else {
-    k_dw_fwd<1><<<plane_grid(images, (long long)H * W * C), dim3(256), 0, s>>>(
-        x, images, H, W, FastDiv((uint32_t)C), FastDiv((uint32_t)W), w, bias, act, hn, dphi);
+    k_dw_fwd<1, kDwFwdXS><<<plane_grid(images, (long long)H * XB * C), dim3(256), 0, s>>>(
+        x, images, H, W, FastDiv((uint32_t)C), FastDiv((uint32_t)XB), w, bias, act, hn, dphi);
   }
   return hipGetLastError();
 }
@@ -425,12 +573,13 @@ hipError_t launch_dw_bwd(hipStream_t s, const float* G, int images, int O, int H
                          const float* w, const float* dphi, float* out) {
   const long long rows = (long long)images * O;
   if (rows >= (1LL << 31) || !plane_fits(rows, (long long)H * W * C)) return hipErrorInvalidValue;
+  const int XB = cdiv_i(W, kDwBwdXS);
   if (use_vec4(C, {G, w, dphi, out})) {
-    k_dw_bwd<4><<<plane_grid(rows, (long long)H * W * C / 4), dim3(256), 0, s>>>(
-        G, (int)rows, O, H, W, FastDiv((uint32_t)(C / 4)), FastDiv((uint32_t)W), w, dphi, out);
+    k_dw_bwd<4, kDwBwdXS><<<plane_grid(rows, (long long)H * XB * C / 4), dim3(256), 0, s>>>(
+        G, (int)rows, O, H, W, FastDiv((uint32_t)(C / 4)), FastDiv((uint32_t)XB), w, dphi, out);
   } else {
-    k_dw_bwd<1><<<plane_grid(rows, (long long)H * W * C), dim3(256), 0, s>>>(
-        G, (int)rows, O, H, W, FastDiv((uint32_t)C), FastDiv((uint32_t)W), w, dphi, out);
+    k_dw_bwd<1, kDwBwdXS><<<plane_grid(rows, (long long)H * XB * C), dim3(256), 0, s>>>(
+        G, (int)rows, O, H, W, FastDiv((uint32_t)C), FastDiv((uint32_t)XB), w, dphi, out);
   }
   return hipGetLastError();
 }
@@ -454,25 +603,57 @@ hipError_t launch_pool_bwd(hipStream_t s, const float* G, int images, int O, int
   const long long rows = (long long)images * O;
   if (H % 2 || W % 2 || rows >= (1LL << 31) || !plane_fits(rows, (long long)H * W * C))
     return hipErrorInvalidValue;
+  const long long pooled = (long long)(H / 2) * (W / 2) * C;
   if (use_vec4(C, {G, dphi, out})) {
-    k_pool_bwd<4><<<plane_grid(rows, (long long)H * W * C / 4), dim3(256), 0, s>>>(
-        G, (int)rows, O, H, W, FastDiv((uint32_t)(C / 4)), FastDiv((uint32_t)W), dphi, out);
+    k_pool_bwd<4><<<plane_grid(rows, pooled / 4), dim3(256), 0, s>>>(
+        G, (int)rows, O, H, W, FastDiv((uint32_t)(C / 4)), FastDiv((uint32_t)(W / 2)), dphi, out);
   } else {
-    k_pool_bwd<1><<<plane_grid(rows, (long long)H * W * C), dim3(256), 0, s>>>(
-        G, (int)rows, O, H, W, FastDiv((uint32_t)C), FastDiv((uint32_t)W), dphi, out);
+    k_pool_bwd<1><<<plane_grid(rows, pooled), dim3(256), 0, s>>>(
+        G, (int)rows, O, H, W, FastDiv((uint32_t)C), FastDiv((uint32_t)(W / 2)), dphi, out);
   }
   return hipGetLastError();
 }
 
 hipError_t launch_pix_wgrad(hipStream_t s, const float* G, const float* x, int images, int O, int H, int W,
                             int C, int taps, int bias, float* J, long long ldJ, long long off_w,
-                            long long off_b) {
+                            long long off_b, float* part, long long part_capacity) {
   const long long rows = (long long)images * O;
   if (rows >= (1LL << 31) || !plane_fits(rows, (long long)H * W * C)) return hipErrorInvalidValue;
   if (taps != 0 && taps != 1 && taps != 9) return hipErrorInvalidValue;
+  if (taps == 9) {
+    // bands of pixels: about four workgroups per compute unit of 256, at least 64 pixels a
+    // band, and as many bands' sums as `part` holds
+    const int D = H * W, cgroups = cdiv_i(C, 64);
+    const long long ncols = 10LL * C;
+    const long long per_band = rows * ncols;
+    long long bands = std::min<long long>(cdiv_i(1024, (long long)images * cgroups), std::max(1, D / 64));
+    if (part && per_band > 0) bands = std::min(bands, part_capacity / per_band);
+    else bands = 1;
+    bands = std::max(1LL, bands);
+    const long long work = (long long)images * bands * cgroups;
+    if (work >= (1LL << 31)) return hipErrorInvalidValue;
+    const int grid = (int)std::min<long long>(work, 1 << 20);
+    float* out = bands > 1 ? part : J;
+    const long long ld_out = bands > 1 ? ncols : ldJ;
+    const long long ow = bands > 1 ? 0 : off_w, ob = bands > 1 ? 9LL * C : off_b;
+    if (bias)
+      k_dw_wgrad<true><<<dim3(grid), dim3(256), 0, s>>>(G, x, images, O, H, W, FastDiv((uint32_t)W), C,
+                                                          (int)bands, cgroups, out, ld_out, ow, ob, per_band);
+    else
+      k_dw_wgrad<false><<<dim3(grid), dim3(256), 0, s>>>(G, x, images, O, H, W, FastDiv((uint32_t)W), C,
+                                                           (int)bands, cgroups, out, ld_out, ow, ob, per_band);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || bands == 1) return e;
+    // the band sums have a row stride of 10 C; without a bias only the first 9 C are written
+    const int nc = (int)(bias ? ncols : 9LL * C);
+    const long long total = rows * nc;
+    const int rg = (int)std::max(1LL, std::min<long long>((total + 255) / 256, 1 << 16));
+    k_band_reduce<<<dim3(rg), dim3(256), 0, s>>>(part, (int)bands, rows, nc, C, J, ldJ, off_w, off_b);
+    return hipGetLastError();
+  }
   if (use_vec4(C, {G, x}))
-    return pix_wgrad_v<4>(s, G, x, (int)rows, O, H, W, C, taps, bias, J, ldJ, off_w, off_b);
-  return pix_wgrad_v<1>(s, G, x, (int)rows, O, H, W, C, taps, bias, J, ldJ, off_w, off_b);
+    return pix_wgrad_v<4>(s, G, x, (int)rows, O, H * W, C, taps, bias, J, ldJ, off_w, off_b);
+  return pix_wgrad_v<1>(s, G, x, (int)rows, O, H * W, C, taps, bias, J, ldJ, off_w, off_b);
 }
 
 }  // namespace ntk

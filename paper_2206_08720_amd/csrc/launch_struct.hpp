@@ -36,8 +36,10 @@ hipError_t launch_pool_bwd(hipStream_t s, const float* G, int images, int O, int
 //   taps = 1: J[r, off_w + c]       = sum_p G[r, p, c] x[img, p, c]                 (scale)
 //   taps = 0: no weight columns
 //   bias:     J[r, off_b + c]       = sum_p G[r, p, c]                              (any bias)
+// With taps = 9 the pixels are split into bands whose sums go to `part` (capacity in floats;
+// may be null: one band) and are then added in band order.
 hipError_t launch_pix_wgrad(hipStream_t s, const float* G, const float* x, int images, int O, int H, int W,
                             int C, int taps, int bias, float* J, long long ldJ, long long off_w,
-                            long long off_b);
+                            long long off_b, float* part, long long part_capacity);
 
 }  // namespace ntk

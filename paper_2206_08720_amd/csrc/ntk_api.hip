@@ -967,14 +967,14 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
       }
       if (L.has_bias) {
         prof_begin(P, s, KC_STRUCT_WGRAD);
-        e = launch_pix_wgrad(s, Gcur, nullptr, M, Oe, Hl, Wl, cout, 0, 1, J, Kcall, 0, jb[l]);
+        e = launch_pix_wgrad(s, Gcur, nullptr, M, Oe, Hl, Wl, cout, 0, 1, J, Kcall, 0, jb[l], nullptr, 0);
         prof_end(P, s, KC_STRUCT_WGRAD);
         if (e != hipSuccess) return hip_fail(h, e, "conv bias cotangent");
       }
     } else if (L.kind != NTK_AVGPOOL2) {
       prof_begin(P, s, KC_STRUCT_WGRAD);
       e = launch_pix_wgrad(s, Gcur, hptr(l), M, Oe, Hl, Wl, cout, L.kind == NTK_DWCONV3X3_SAME ? 9 : 1,
-                           L.has_bias, J, Kcall, jw[l], jb[l]);
+                           L.has_bias, J, Kcall, jw[l], jb[l], F(h->off_part), h->part_capacity);
       prof_end(P, s, KC_STRUCT_WGRAD);
       if (e != hipSuccess) return hip_fail(h, e, "depthwise / scale weight-space cotangent");
     }
