@@ -88,21 +88,25 @@ def _weight_cols(kind, cin, cout):
 
 def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", batch="full"):
     """CNN counts per stage.  3x3 convolutions as in the module docstring; the further layer
-    kinds (memory-bound, counted for completeness): depthwise 3x3 forward, backward and
-    weight-space cotangent 2 M (Oe) D 9 C each; scale forward 2 M D C, backward M Oe D C,
-    cotangent 2 M Oe D C; a 2x2 pool M D C forward and M Oe D C backward (D: its input
-    pixels); a bias M D C forward and its cotangent (a pixel sum) M Oe D C.  The contraction
-    covers every weight-space column (9 Cin Cout, 9 C, C, and C per bias)."""
+    kinds (memory-bound, counted for completeness, in the struct_* stages): depthwise 3x3
+    forward, backward and weight-space cotangent 2 M (Oe) D 9 C each; scale forward M D C (2 M D C
+    with a bias), backward M Oe D C, cotangent 2 M Oe D C; a 2x2 pool M D C forward and
+    M Oe D C backward (D: its input pixels); a bias M D C forward and its cotangent (a pixel sum)
+    M Oe D C.  The contraction covers every weight-space column (9 Cin Cout, 9 C, C, and C per
+    bias)."""
     layers = spec["layers"]
     sp, C = _spatial_layers(spec)
     O = layers[-1]["out"]
     Oe, Oc, pairs = _variant(O, n1, n2, output, batch, symmetric)
     gpairs = n1 if batch == "diagonal" else n1 * n2
     M = n1 if symmetric else n1 + n2
-    fwd = bwd = wg = cols = io = 0.0
+    # the 3x3 convolutions' stages ("forward", "backward", "wgrad"), and those of the other kinds
+    # and of the biases (memory-bound kernels of their own: "struct_forward", "struct_backward",
+    # "struct_wgrad"); a conv bias is added in the conv forward kernel's epilogue
+    fwd = bwd = wg = sfwd = sbwd = swg = cols = io = 0.0
     for i, (k, cin, cout, D, bias) in enumerate(sp):
         if k == "conv3x3":
-            fwd += 2.0 * M * D * 9 * cin * cout
+            fwd += 2.0 * M * D * 9 * cin * cout + (1.0 * M * D * cout if bias else 0.0)
             if i >= 1:
                 bwd += 2.0 * M * Oe * D * 9 * cout * cin
             if order == "outside_in":
@@ -112,28 +116,30 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
                 # (every input pair, also on the symmetric schedule)
                 io += 2.0 * gpairs * (D * D * 9 * cin + Oe * D * D * cout + Oc * D * cout)
         elif k == "dwconv3x3":
-            fwd += 2.0 * M * D * 9 * cout
+            sfwd += 2.0 * M * D * 9 * cout + (1.0 * M * D * cout if bias else 0.0)
             if i >= 1:
-                bwd += 2.0 * M * Oe * D * 9 * cout
-            wg += 2.0 * M * Oe * D * 9 * cout
+                sbwd += 2.0 * M * Oe * D * 9 * cout
+            swg += 2.0 * M * Oe * D * 9 * cout
             cols += 9 * cout
         elif k == "scale":
-            fwd += 2.0 * M * D * cout
+            sfwd += 2.0 * M * D * cout if bias else 1.0 * M * D * cout
             if i >= 1:
-                bwd += 1.0 * M * Oe * D * cout
-            wg += 2.0 * M * Oe * D * cout
+                sbwd += 1.0 * M * Oe * D * cout
+            swg += 2.0 * M * Oe * D * cout
             cols += cout
         else:  # avgpool2
-            fwd += 1.0 * M * D * cout
+            sfwd += 1.0 * M * D * cout
             if i >= 1:
-                bwd += 1.0 * M * Oe * D * cout
+                sbwd += 1.0 * M * Oe * D * cout
         if bias:
-            fwd += 1.0 * M * D * cout
-            wg += 1.0 * M * Oe * D * cout
+            swg += 1.0 * M * Oe * D * cout
             cols += cout
     st = {"forward": fwd, "backward": bwd, "gram": 2.0 * gpairs * C}
     if wg:
         st["wgrad"] = wg
+    for key, v in (("struct_forward", sfwd), ("struct_backward", sbwd), ("struct_wgrad", swg)):
+        if v:
+            st[key] = v
     st["contraction"] = 2.0 * pairs * Oc * cols + io
     st["total"] = sum(st.values())
     return st

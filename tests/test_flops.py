@@ -89,9 +89,14 @@ def test_structured_layer_kinds_counts():
                                                ("dwconv3x3", "erf", True), ("scale", "none", False)], O)
     f = cnn_flops(spec, N, N)
     M, D0, D1 = 2 * N, 24, 6
-    assert f["forward"] == 2 * M * D0 * 9 * 2 * 8 + M * D0 * 8 + M * D0 * 8 \
-        + 2 * M * D1 * 9 * 8 + M * D1 * 8 + 2 * M * D1 * 8
-    assert f["backward"] == M * O * D0 * 8 + 2 * M * O * D1 * 9 * 8 + M * O * D1 * 8
+    # the conv (with its bias in the epilogue), then the pool, depthwise (+ bias) and scale
+    assert f["forward"] == 2 * M * D0 * 9 * 2 * 8 + M * D0 * 8
+    assert f["struct_forward"] == M * D0 * 8 + 2 * M * D1 * 9 * 8 + M * D1 * 8 + M * D1 * 8
+    assert f["backward"] == 0
+    assert f["struct_backward"] == M * O * D0 * 8 + 2 * M * O * D1 * 9 * 8 + M * O * D1 * 8
+    assert f["wgrad"] == 2 * M * O * 8 * 9 * 2 * D0
+    assert f["struct_wgrad"] == M * O * D0 * 8 + 2 * M * O * D1 * 9 * 8 + M * O * D1 * 8 \
+        + 2 * M * O * D1 * 8
     # J columns: 9 Cin Cout + Cout (conv and its bias), 9 C + C (depthwise and bias), C (scale)
     assert f["contraction"] == 2 * N * N * O * O * (9 * 2 * 8 + 8 + 9 * 8 + 8 + 8)
     assert param_total(spec) == oracle.param_count(spec) == 9 * 2 * 8 + 8 + 9 * 8 + 8 + 8 + 8 * O
