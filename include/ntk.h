@@ -203,8 +203,7 @@ int ntk_compute(ntk_handle* h, const float* const* params, const float* X1, int 
  *   v    device [n2, O] fp32: v[n2*O + o2].
  *   out  device [n1, O] fp32: out[n1*O + o1] = sum_{n2, o2} Theta(x1_{n1}, x2_{n2})[o1, o2] v[n2, o2].
  * Time about 3 forward passes of the batches (no N1 N2 O^2 term).  The output and batch
- * variants and NTK_OPT_METHOD do not apply.  Convolutional models must consist of bias-free
- * CONV3X3_SAME layers (NTK_E_UNSUPPORTED otherwise).  The first call on a handle allocates the
+ * variants and NTK_OPT_METHOD do not apply.  Every layer kind is supported.  The first call on a handle allocates the
  * weight-space vector (one float per parameter) and the tangent buffers.  Stream-ordered,
  * asynchronous, deterministic; NTK_E_ARG for null pointers or sizes out of range.
  */

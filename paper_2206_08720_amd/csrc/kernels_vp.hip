@@ -56,7 +56,7 @@ hipError_t launch_colsum(hipStream_t s, const float* x, int R, int C, float* out
 
 // Cotangent of the last conv pre-activation from the cotangent u [n, C] of the pooled
 // features: out[s, p, c] = u[s, c] / D * dphi[s, p, c] (global average pooling spreads u
-// evenly over the D pixels).
+// evenly over the D pixels; dphi null: the identity).
 __global__ void __launch_bounds__(256)
 k_gap_adjoint(const float* __restrict__ u, const float* __restrict__ dphi, int n, int D, int C,
               float* __restrict__ out) {
@@ -66,7 +66,7 @@ k_gap_adjoint(const float* __restrict__ u, const float* __restrict__ dphi, int n
     const int c = (int)(i % C);
     const long long sp = i / C;
     const int smp = (int)(sp / D);
-    out[i] = u[(long long)smp * C + c] * inv * dphi[i];
+    out[i] = dphi ? u[(long long)smp * C + c] * inv * dphi[i] : u[(long long)smp * C + c] * inv;
   }
 }
 

@@ -148,12 +148,11 @@ struct ntk_handle {
   std::vector<int> bh, bw;        // image height and width at each layer boundary 0..nc
   std::vector<int> wslot, bslot;  // parameter slots of layer l's weight and bias (-1: none)
   int rslot = 0;                  // parameter slot of the readout weight
-  bool vp_ok = false;             // only bias-free 3x3 convolutions: NTK-vector products supported
   std::vector<size_t> off_ch;     // layer inputs h_l, l = 0..nc (nc: the GAP input) [Mmax, bh_l, bw_l, c_l]
   std::vector<size_t> off_cdphi;  // act'(z_l) of parametrised layers [Mmax, bh_{l+1}, bw_{l+1}, c_{l+1}]
   std::vector<size_t> off_Kt;     // flipped kernels of the 3x3 convolutions l >= 1 [c_l, 9, c_{l+1}]
-  std::vector<long long> joff;    // column of the 3x3 convolution weights in J when every layer is
-                                  // outside-in (the NTK-vector product's layout)
+  std::vector<long long> joff;    // first column of layer l's weight block (then its bias) in J when
+                                  // every layer is outside-in (the NTK-vector product's layout)
   long long Ktot = 0;             // columns of J at most: every weight and bias column
   size_t off_g = 0, off_Gping = 0, off_Gpong = 0, off_J = 0, off_gram_r = 0, off_part = 0;
   long long part_capacity = 0;    // floats of the split-K partial buffer
@@ -326,7 +325,6 @@ static void plan_cnn(ntk_handle* h) {
   h->bw[0] = h->in_w;
   h->wslot.assign(nc, -1);
   h->bslot.assign(nc, -1);
-  h->vp_ok = true;
   int slot = 0;
   for (int l = 0; l < nc; ++l) {
     const ntk_layer_desc& L = h->layers[l];
@@ -338,7 +336,6 @@ static void plan_cnn(ntk_handle* h) {
       h->wslot[l] = slot++;
       if (L.has_bias) h->bslot[l] = slot++;
     }
-    if (L.kind != NTK_CONV3X3_SAME || L.has_bias) h->vp_ok = false;
   }
   h->rslot = slot;
   const size_t Mmax = (size_t)h->max_n1 + h->max_n2;
@@ -1196,21 +1193,21 @@ static int vector_product_fcn(ntk_handle* h, const float* const* params, const f
 
 static int ensure_vp_workspace_cnn(ntk_handle* h) {
   if (h->vp_ws) return NTK_OK;
-  const int nc = h->nc, O = h->out_dim, D = h->D, C = h->ch[nc];
-  int cmax = 1;
-  for (int c : h->ch) cmax = std::max(cmax, c);
+  const int nc = h->nc, O = h->out_dim, C = h->ch[nc];
+  size_t pmax = 1;   // largest image of any layer boundary (pixels x channels)
+  for (int b = 0; b <= nc; ++b) pmax = std::max(pmax, (size_t)h->bh[b] * h->bw[b] * h->ch[b]);
   size_t off = 0;
   auto take = [&](size_t floats) {
     size_t o = off;
     off = align_up(off + floats * 4);
     return o;
   };
-  h->vp_off_tc.assign(1, take((size_t)h->Ktot + (size_t)O * C));   // conv layers, then the readout
+  h->vp_off_tc.assign(1, take((size_t)h->Ktot + (size_t)O * C));   // spatial layers, then the readout
   h->vp_off_dT = take((size_t)O * h->max_n2);
   h->vp_off_hT = take((size_t)C * h->max_n2);
   h->vp_off_WLt = take((size_t)C * O);
   h->vp_off_u = take((size_t)h->max_n2 * C);
-  const size_t img = (size_t)h->max_n1 * D * cmax;
+  const size_t img = (size_t)h->max_n1 * pmax;
   h->vp_off_t0 = take(img);
   h->vp_off_t1 = take(img);
   h->vp_off_ca = take(img);
@@ -1229,12 +1226,16 @@ static int ensure_vp_workspace_cnn(ntk_handle* h) {
 }
 
 // CNN form of vector_product_fcn: the VJP of batch 2 runs back through the readout, the global
-// average pool and the conv layers (the conv weight cotangent sum_{n,p} delta (x) patch is the
-// per-sample weight-space cotangent summed over samples); the JVP of batch 1 pushes the
-// weight-space vector forward through the convolutions, the pool and the readout.
+// average pool and the spatial layers, one cotangent row per sample; each layer's weight-space
+// cotangent (the same columns the NTK's J holds: a 3x3 convolution's sum_p delta (x) patch, the
+// depthwise and scale pixel sums, the bias pixel sums) is formed per sample and summed over the
+// samples.  The JVP of batch 1 then pushes that weight-space vector forward: the tangent of a
+// parametrised layer's pre-activation is the layer applied to the input tangent plus the layer
+// with the tangent weights applied to the input, plus the tangent bias, times act'; a pool
+// averages the tangent.
 static int vector_product_cnn(ntk_handle* h, const float* const* params, const float* X1, int n1,
                               const float* X2, int n2, const float* v, float* out) {
-  const int nc = h->nc, O = h->out_dim, H = h->H, W = h->W, D = h->D, C = h->ch[nc];
+  const int nc = h->nc, O = h->out_dim, C = h->ch[nc];
   const bool sym = h->opt_symmetric && X1 == X2 && n1 == n2;
   hipStream_t s = h->stream;
   Profiler* P = &h->prof;
@@ -1246,12 +1247,14 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
   auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
   auto V = [&](size_t off) { return reinterpret_cast<float*>(h->vp_ws + off); };
   auto hptr = [&](int l) -> const float* { return l == 0 ? h0 : F(h->off_ch[l]); };
-  const size_t r2 = sym ? 0 : (size_t)n1;
+  auto plane = [&](int b) { return (size_t)h->bh[b] * h->bw[b] * h->ch[b]; };
+  const size_t r2 = sym ? 0 : (size_t)n1;   // first row of batch 2 in the stacked arrays
   float* tc = V(h->vp_off_tc[0]);
   float* tc_d = tc + h->Ktot;              // readout part [O, C]
-  const float* Wd = params[nc];
+  const float* Wd = params[h->rslot];
   const float* g1 = F(h->off_g);
   const float* g2 = F(h->off_g) + r2 * C;
+  const int Dn = h->bh[nc] * h->bw[nc];
   hipError_t e;
   // ---- VJP of batch 2 at v
   prof_begin(P, s, KC_TRANSPOSE);
@@ -1284,56 +1287,115 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
   if (e != hipSuccess) return hip_fail(h, e, "pooled-feature cotangent");
   float* Gcur = F(h->off_Gping);
   float* Gnext = F(h->off_Gpong);
+  const float* dlast = h->wslot[nc - 1] >= 0 ? F(h->off_cdphi[nc - 1]) + r2 * plane(nc) : nullptr;
   prof_begin(P, s, KC_VP_ELEMENTWISE);
-  e = launch_gap_adjoint(s, V(h->vp_off_u), F(h->off_cdphi[nc - 1]) + r2 * D * C, n2, D, C, Gcur);
+  e = launch_gap_adjoint(s, V(h->vp_off_u), dlast, n2, Dn, C, Gcur);
   prof_end(P, s, KC_VP_ELEMENTWISE);
   if (e != hipSuccess) return hip_fail(h, e, "pooling adjoint");
   float* J = F(h->off_J);
   for (int l = nc - 1; l >= 0; --l) {
-    prof_begin(P, s, KC_CONV_WGRAD);
-    e = launch_conv_wgrad(s, Gcur, hptr(l) + r2 * D * h->ch[l], n2, 1, H, W, h->ch[l + 1], h->ch[l], J,
-                          h->Ktot, h->joff[l]);
-    prof_end(P, s, KC_CONV_WGRAD);
-    if (e != hipSuccess) return hip_fail(h, e, "conv weight cotangent");
+    const ntk_layer_desc& L = h->layers[l];
+    const int Hl = h->bh[l], Wl = h->bw[l], cin = h->ch[l], cout = h->ch[l + 1];
+    const float* hl = hptr(l) + r2 * plane(l);
+    const float* w = h->wslot[l] >= 0 ? params[h->wslot[l]] : nullptr;
+    const long long jw = h->joff[l], jb = jw + weight_cols(L, cin);
+    if (L.kind == NTK_CONV3X3_SAME) {
+      prof_begin(P, s, KC_CONV_WGRAD);
+      e = launch_conv_wgrad(s, Gcur, hl, n2, 1, Hl, Wl, cout, cin, J, h->Ktot, jw);
+      prof_end(P, s, KC_CONV_WGRAD);
+      if (e == hipSuccess && L.has_bias) {
+        prof_begin(P, s, KC_STRUCT_WGRAD);
+        e = launch_pix_wgrad(s, Gcur, nullptr, n2, 1, Hl, Wl, cout, 0, 1, J, h->Ktot, 0, jb, nullptr, 0);
+        prof_end(P, s, KC_STRUCT_WGRAD);
+      }
+    } else if (L.kind != NTK_AVGPOOL2) {
+      prof_begin(P, s, KC_STRUCT_WGRAD);
+      e = launch_pix_wgrad(s, Gcur, hl, n2, 1, Hl, Wl, cout, L.kind == NTK_DWCONV3X3_SAME ? 9 : 1, L.has_bias,
+                           J, h->Ktot, jw, jb, F(h->off_part), h->part_capacity);
+      prof_end(P, s, KC_STRUCT_WGRAD);
+    }
+    if (e != hipSuccess) return hip_fail(h, e, "VJP weight cotangent");
     if (l >= 1) {
-      prof_begin(P, s, KC_TRANSPOSE);
-      e = launch_conv_flip(s, params[l], h->ch[l + 1], h->ch[l], F(h->off_Kt[l]));
-      prof_end(P, s, KC_TRANSPOSE);
-      if (e != hipSuccess) return hip_fail(h, e, "kernel flip");
-      prof_begin(P, s, KC_CONV_BWD);
-      e = launch_conv_bwd(s, Gcur, n2, 1, H, W, h->ch[l + 1], F(h->off_Kt[l]), h->ch[l],
-                          F(h->off_cdphi[l - 1]) + r2 * D * h->ch[l], Gnext);
-      prof_end(P, s, KC_CONV_BWD);
-      if (e != hipSuccess) return hip_fail(h, e, "VJP conv backward");
+      const float* dprev = h->wslot[l - 1] >= 0 ? F(h->off_cdphi[l - 1]) + r2 * plane(l) : nullptr;
+      if (L.kind == NTK_CONV3X3_SAME) {
+        prof_begin(P, s, KC_TRANSPOSE);
+        e = launch_conv_flip(s, w, cout, cin, F(h->off_Kt[l]));
+        prof_end(P, s, KC_TRANSPOSE);
+        if (e != hipSuccess) return hip_fail(h, e, "kernel flip");
+        prof_begin(P, s, KC_CONV_BWD);
+        e = launch_conv_bwd(s, Gcur, n2, 1, Hl, Wl, cout, F(h->off_Kt[l]), cin, dprev, Gnext);
+        prof_end(P, s, KC_CONV_BWD);
+      } else {
+        prof_begin(P, s, KC_STRUCT_BWD);
+        if (L.kind == NTK_DWCONV3X3_SAME)
+          e = launch_dw_bwd(s, Gcur, n2, 1, Hl, Wl, cout, w, dprev, Gnext);
+        else if (L.kind == NTK_SCALE)
+          e = launch_scale_bwd(s, Gcur, n2, 1, Hl * Wl, cout, w, dprev, Gnext);
+        else
+          e = launch_pool_bwd(s, Gcur, n2, 1, Hl, Wl, cin, dprev, Gnext);
+        prof_end(P, s, KC_STRUCT_BWD);
+      }
+      if (e != hipSuccess) return hip_fail(h, e, "VJP backward");
       std::swap(Gcur, Gnext);
     }
   }
   prof_begin(P, s, KC_VP_ELEMENTWISE);
   e = launch_colsum(s, J, n2, (int)h->Ktot, tc);   // sum of the per-sample cotangents
   prof_end(P, s, KC_VP_ELEMENTWISE);
-  if (e != hipSuccess) return hip_fail(h, e, "conv weight cotangent sum");
+  if (e != hipSuccess) return hip_fail(h, e, "weight cotangent sum");
   // ---- JVP of batch 1 along theta_c
   float* tcur = V(h->vp_off_t0);
   float* tnext = V(h->vp_off_t1);
+  float* ca = V(h->vp_off_ca);
+  float* cb = V(h->vp_off_cb);
+  float* cd = V(h->vp_off_cd);   // act' outputs of the activation-free evaluations, unused
+  bool tzero = true;             // the tangent of layer l's input is zero (no parameter before it)
   for (int l = 0; l < nc; ++l) {
-    const int co = h->ch[l + 1];
-    prof_begin(P, s, KC_CONV_FWD);
-    e = launch_conv_fwd(s, hptr(l), n1, H, W, h->ch[l], tc + h->joff[l], co, NTK_ACT_NONE, nullptr,
-                        V(h->vp_off_cb), V(h->vp_off_cd));
-    if (e == hipSuccess && l > 0)
-      e = launch_conv_fwd(s, tcur, n1, H, W, h->ch[l], params[l], co, NTK_ACT_NONE, nullptr,
-                          V(h->vp_off_ca), V(h->vp_off_cd));
-    prof_end(P, s, KC_CONV_FWD);
-    if (e != hipSuccess) return hip_fail(h, e, "JVP convolution");
+    const ntk_layer_desc& L = h->layers[l];
+    const int Hl = h->bh[l], Wl = h->bw[l], cin = h->ch[l], cout = h->ch[l + 1];
+    if (L.kind == NTK_AVGPOOL2) {
+      if (tzero) continue;
+      prof_begin(P, s, KC_STRUCT_FWD);
+      e = launch_pool_fwd(s, tcur, n1, Hl, Wl, cin, tnext);
+      prof_end(P, s, KC_STRUCT_FWD);
+      if (e != hipSuccess) return hip_fail(h, e, "JVP pool");
+      std::swap(tcur, tnext);
+      continue;
+    }
+    const float* w = params[h->wslot[l]];
+    const float* tw = tc + h->joff[l];
+    const float* tb = L.has_bias ? tc + h->joff[l] + weight_cols(L, cin) : nullptr;
+    const float* hl = hptr(l);
+    // cb = the layer with the tangent weights applied to the input; ca = the layer applied to
+    // the input tangent
+    if (L.kind == NTK_CONV3X3_SAME) {
+      prof_begin(P, s, KC_CONV_FWD);
+      e = launch_conv_fwd(s, hl, n1, Hl, Wl, cin, tw, cout, NTK_ACT_NONE, nullptr, cb, cd);
+      if (e == hipSuccess && !tzero)
+        e = launch_conv_fwd(s, tcur, n1, Hl, Wl, cin, w, cout, NTK_ACT_NONE, nullptr, ca, cd);
+      prof_end(P, s, KC_CONV_FWD);
+    } else {
+      prof_begin(P, s, KC_STRUCT_FWD);
+      if (L.kind == NTK_DWCONV3X3_SAME) {
+        e = launch_dw_fwd(s, hl, n1, Hl, Wl, cin, tw, nullptr, NTK_ACT_NONE, cb, cd);
+        if (e == hipSuccess && !tzero) e = launch_dw_fwd(s, tcur, n1, Hl, Wl, cin, w, nullptr, NTK_ACT_NONE, ca, cd);
+      } else {
+        e = launch_scale_fwd(s, hl, n1, Hl * Wl, cin, tw, nullptr, NTK_ACT_NONE, cb, cd);
+        if (e == hipSuccess && !tzero)
+          e = launch_scale_fwd(s, tcur, n1, Hl * Wl, cin, w, nullptr, NTK_ACT_NONE, ca, cd);
+      }
+      prof_end(P, s, KC_STRUCT_FWD);
+    }
+    if (e != hipSuccess) return hip_fail(h, e, "JVP layer");
     prof_begin(P, s, KC_VP_ELEMENTWISE);
-    e = launch_jvp_combine(s, l > 0 ? V(h->vp_off_ca) : nullptr, V(h->vp_off_cb), nullptr,
-                           F(h->off_cdphi[l]), n1 * D, co, tnext);
+    e = launch_jvp_combine(s, tzero ? nullptr : ca, cb, tb, F(h->off_cdphi[l]), n1 * Hl * Wl, cout, tnext);
     prof_end(P, s, KC_VP_ELEMENTWISE);
     if (e != hipSuccess) return hip_fail(h, e, "JVP step");
     std::swap(tcur, tnext);
+    tzero = false;
   }
   prof_begin(P, s, KC_GAP);
-  e = launch_gap(s, tcur, n1, D, C, V(h->vp_off_gdot));
+  e = launch_gap(s, tcur, n1, Dn, C, V(h->vp_off_gdot));
   prof_end(P, s, KC_GAP);
   if (e != hipSuccess) return hip_fail(h, e, "JVP pooling");
   GramBatch gr{};
@@ -1464,9 +1526,6 @@ extern "C" int ntk_vector_product(ntk_handle* h, const float* const* params, con
   if (n1 > h->max_n1 || n2 > h->max_n2)
     return fail(h, NTK_E_ARG, "n1/n2 exceed the max_n1/max_n2 given to ntk_init");
   h->err.clear();
-  if (h->cnn && !h->vp_ok)
-    return fail(h, NTK_E_UNSUPPORTED,
-                "NTK-vector products of convolutional models take bias-free 3x3 convolutions only");
   if (h->cnn) return vector_product_cnn(h, params, X1, n1, X2, n2, v, out);
   return vector_product_fcn(h, params, X1, n1, X2, n2, v, out);
 }

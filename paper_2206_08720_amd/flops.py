@@ -192,17 +192,18 @@ def vp_flops(spec, n1, n2, symmetric=False):
     Gram kernel).  CNN: `forward_and_jvp` is the forward pass plus the JVP convolutions."""
     M = n1 if symmetric else n1 + n2
     layers = spec["layers"]
-    if any(Lr["kind"] == "conv3x3" for Lr in layers):
-        H, W, _ = spec["input_shape"]
-        D = H * W
-        convs = [Lr for Lr in layers if Lr["kind"] == "conv3x3"]
-        O, C = layers[-1]["out"], convs[-1]["out"]
-        conv = [9 * c["in"] * c["out"] for c in convs]
+    if any(Lr["kind"] != "dense" for Lr in layers):
+        # the 3x3 convolutions' matrix-core work (D: each layer's own pixels); the memory-bound
+        # depthwise, scale, bias and pool steps are not counted
+        sp, C = _spatial_layers(spec)
+        O = layers[-1]["out"]
+        conv = [(i, D, 9 * cin * cout) for i, (k, cin, cout, D, _) in enumerate(sp) if k == "conv3x3"]
+        first = min([i for i, (k, *_r) in enumerate(sp) if k != "avgpool2"] or [0])
         st = {
-            "forward_and_jvp": sum(2.0 * M * D * k for k in conv) + sum(2.0 * n1 * D * k for k in conv)
-            + sum(2.0 * n1 * D * k for k in conv[1:]),
-            "vjp_backward": sum(2.0 * n2 * D * k for k in conv[1:]),
-            "weight_cotangent": sum(2.0 * n2 * D * k for k in conv),
+            "forward_and_jvp": sum(2.0 * M * D * k for _, D, k in conv) + sum(2.0 * n1 * D * k for _, D, k in conv)
+            + sum(2.0 * n1 * D * k for i, D, k in conv if i > first),
+            "vjp_backward": sum(2.0 * n2 * D * k for i, D, k in conv if i >= 1),
+            "weight_cotangent": sum(2.0 * n2 * D * k for _, D, k in conv),
             "gram": 2.0 * n2 * O * C * 2 + 2.0 * n1 * O * C * 2,
         }
     else:

@@ -153,20 +153,3 @@ def test_struct_graph_replays_and_determinism():
             assert torch.equal(out, eager)
     finally:
         h.close()
-
-
-def test_struct_vector_product_is_refused():
-    import torch
-    from paper_2206_08720_amd import _lib
-    from paper_2206_08720_amd.ntk import NTK
-    from tests.gpu_helpers import to_dev
-    params, X1, X2 = _data(ORDER_SPEC, 3, 2, 651)
-    ps, (x1, x2) = to_dev(params), to_dev([X1, X2])
-    h = NTK(ORDER_SPEC, 3, 2)
-    try:
-        v = torch.zeros((2, 6), dtype=torch.float32, device=x1.device)
-        with pytest.raises(_lib.NTKError) as exc:
-            h.vector_product(ps, x1, x2, v)
-        assert exc.value.code == _lib.NTK_E_UNSUPPORTED
-    finally:
-        h.close()

@@ -42,6 +42,13 @@ CASES = [
     ("cnn 5x6, 2 conv layers", wl.cnn_spec("p5", (5, 6), 3, [8, 12], 5), 6, 9),
     ("cnn erf 4x4, O=3", wl.cnn_spec("p6", (4, 4), 2, [10], 3, act="erf"), 7, 4),
     ("cnn 8x8, 3 layers of 32", wl.cnn_spec("p7", (8, 8), 3, [32, 32, 32], 10), 12, 11),
+    # the further layer kinds: conv biases, depthwise, scale, 2x2 pools
+    ("cnn conv+bias, depthwise, pool, scale", wl.cnn_layers_spec(
+        "p8", (8, 8), 3, [("conv3x3", 16, "relu", True), ("dwconv3x3", "erf", True), ("avgpool2",),
+                          ("scale", "relu", True), ("conv3x3", 8, "erf", False)], 6), 7, 5),
+    ("cnn pool first, 6 channels (scalar lanes), last layer a pool", wl.cnn_layers_spec(
+        "p9", (4, 8), 6, [("avgpool2",), ("scale", "erf", False), ("dwconv3x3", "relu", False),
+                          ("avgpool2",)], 3), 5, 6),
 ]
 
 
@@ -76,6 +83,16 @@ def test_vector_product_cnn4_c64_32x32_full_size():
     got = gpu_vp(spec, params, X1, X2, v)
     cs, nw = scaled_errors(got, ref, scale)
     report("vp cnn4_c64_32x32", cs, nw)
+    assert cs <= TOL and nw <= TOL
+
+
+def test_vector_product_cnn_struct_c64_32x32_full_size():
+    spec, params, X1, X2 = wl.make_workload("cnn_struct_c64_32x32")
+    v = np.random.default_rng(7).standard_normal((X2.shape[0], 10)).astype(np.float32)
+    ref, scale = oracle.ntk_vp(spec, params, X1, X2, v, layer_storage=S)
+    got = gpu_vp(spec, params, X1, X2, v)
+    cs, nw = scaled_errors(got, ref, scale)
+    report("vp cnn_struct_c64_32x32", cs, nw)
     assert cs <= TOL and nw <= TOL
 
 
