@@ -99,4 +99,17 @@ __host__ __device__ inline int sk_fixup_tile(const SkShare& s, int j, int P8, in
   return ts;
 }
 
+// Per-sample tile grids on 8 XCDs: workgroup ids are dispatched round robin over the XCDs, so
+// workgroup id runs on XCD id % 8.  Sample s is given to XCD s % 8, and the XCD's workgroups
+// take its samples one after another, all `tiles` tiles of a sample in order, so the tiles that
+// share a sample's operands share that XCD's L2.  The grid has 8 * ceil(samples / 8) * tiles
+// workgroups; returns false (no work) for the ids of samples past the end.
+__host__ __device__ inline bool xcd_sample_tile(int id, int tiles, int samples, int& s, int& t) {
+  const int xcd = id & 7, slot = id >> 3;
+  const int j = slot / tiles;
+  t = slot - j * tiles;
+  s = j * 8 + xcd;
+  return s < samples;
+}
+
 }  // namespace ntk

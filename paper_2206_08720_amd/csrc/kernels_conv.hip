@@ -750,12 +750,13 @@ template <class Cfg, bool VA, bool VB>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, int H, int W, int C,
              int Cin, FastDiv fC, FastDiv fW, FastDiv fCin, float* __restrict__ J, long long ldJ,
-             long long off, int tiles_n) {
+             long long off, int tiles_m, int tiles_n, int samples) {
   extern __shared__ float smem[];
-  const int s = blockIdx.y;
+  int s, t;
+  if (!xcd_sample_tile(blockIdx.x, tiles_m * tiles_n, samples, s, t)) return;
   const int D = H * W;
   const int KC = 9 * Cin;
-  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+  const int tm = t / tiles_n, tn = t - tm * tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   LoadCotangentKOuterT<VA> la;
   la.g = G + (long long)s * O * D * C;
@@ -789,12 +790,13 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
 template <class Cfg, int NS>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O, int H, int W, int C, int Cin, FastDiv fC, FastDiv fW, FastDiv fCin,
-                 float* __restrict__ J, long long ldJ, long long off, int tiles_n) {
+                 float* __restrict__ J, long long ldJ, long long off, int tiles_m, int tiles_n, int samples) {
   extern __shared__ float smem[];
-  const int s = blockIdx.y;
+  int s, t;
+  if (!xcd_sample_tile(blockIdx.x, tiles_m * tiles_n, samples, s, t)) return;
   const int D = H * W;
   const int KC = 9 * Cin;
-  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+  const int tm = t / tiles_n, tn = t - tm * tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   DmaCotangentKOuter<Cfg::BM, Cfg::WAVES> ia;
   ia.g = G + (long long)s * O * D * C;
@@ -823,6 +825,11 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
   });
 }
 
+// Grid of the per-sample weight-space products: the tiles of one sample on one XCD, so the
+// column tiles that share a block of cotangent rows (and the row tiles that share the patch
+// columns) read them through one L2 (xcd_sample_tile).
+static unsigned wgrad_grid(int tiles, int images) { return (unsigned)(8 * ((images + 7) / 8) * tiles); }
+
 template <bool VA, bool VB>
 static hipError_t conv_wgrad_vec(hipStream_t s, const float* G, const float* h, int images, int O,
                                  int H, int W, int C, int Cin, float* J, long long ldJ, long long off) {
@@ -832,14 +839,18 @@ static hipError_t conv_wgrad_vec(hipStream_t s, const float* G, const float* h, 
   const int tn = cdiv(9 * Cin, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
   hipError_t e = set_smem<Cfg, LA, LB>((const void*)k_conv_wgrad<Cfg, VA, VB>);
   if (e != hipSuccess) return e;
-  k_conv_wgrad<Cfg, VA, VB><<<dim3(tm * tn, images), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, LA, LB>(), s>>>(
+  k_conv_wgrad<Cfg, VA, VB><<<dim3(wgrad_grid(tm * tn, images)), dim3(Cfg::THREADS),
+                              gemm_smem_bytes<Cfg, LA, LB>(), s>>>(
       G, h, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
-      ldJ, off, tn);
+      ldJ, off, tm, tn, images);
   return hipGetLastError();
 }
 
 hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
                              int W, int C, int Cin, float* J, long long ldJ, long long off) {
+  if ((long long)8 * ((images + 7) / 8) * cdiv(9 * Cin, CfgConv::BN) * cdiv((long long)O * C, CfgConv::BM) >=
+      (1LL << 31))
+    return hipErrorInvalidValue;
   // direct-to-LDS: one sample's cotangents and layer input each within a buffer resource
   if (C % 4 == 0 && Cin % 4 == 0 && aligned16(G) && aligned16(h) && (long long)O * H * W * C * 4 < (1LL << 31) &&
       (long long)H * W * Cin * 4 < (1LL << 31)) {
@@ -850,9 +861,9 @@ hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int 
     hipError_t e = hipFuncSetAttribute((const void*)k_conv_wgrad_dma<Cfg, NS>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (e != hipSuccess) return e;
-    k_conv_wgrad_dma<Cfg, NS><<<dim3(tm * tn, images), dim3(Cfg::THREADS), bytes, s>>>(
+    k_conv_wgrad_dma<Cfg, NS><<<dim3(wgrad_grid(tm * tn, images)), dim3(Cfg::THREADS), bytes, s>>>(
         G, h, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
-        ldJ, off, tn);
+        ldJ, off, tm, tn, images);
     return hipGetLastError();
   }
   const bool va = C % 4 == 0 && aligned16(G), vb = Cin % 4 == 0 && aligned16(h);

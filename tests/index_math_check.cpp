@@ -168,9 +168,36 @@ static void check_schedule(int T, int P, int L) {
   }
 }
 
+// every (sample, tile) exactly once, every workgroup of sample s on XCD s % 8, and an XCD's
+// workgroups in sample order
+static void check_xcd_sample_tile() {
+  for (int samples = 1; samples <= 70; ++samples)
+    for (int tiles : {1, 2, 5, 9, 45, 64}) {
+      const int grid = 8 * ((samples + 7) / 8) * tiles;
+      std::vector<int> seen((size_t)samples * tiles, 0);
+      std::vector<int> last(8, -1);
+      for (int id = 0; id < grid; ++id) {
+        int s = -1, t = -1;
+        if (!ntk::xcd_sample_tile(id, tiles, samples, s, t)) {
+          CHECK(s >= samples, "xcd_sample_tile: id %d refused but s = %d", id, s);
+          continue;
+        }
+        CHECK(t >= 0 && t < tiles && s >= 0, "xcd_sample_tile: id %d -> (%d, %d)", id, s, t);
+        CHECK(s % 8 == id % 8, "xcd_sample_tile: sample %d on XCD %d", s, id % 8);
+        CHECK(s >= last[id % 8], "xcd_sample_tile: XCD %d goes back to sample %d", id % 8, s);
+        last[id % 8] = s;
+        ++seen[(size_t)s * tiles + t];
+      }
+      for (size_t i = 0; i < seen.size(); ++i)
+        CHECK(seen[i] == 1, "xcd_sample_tile: samples=%d tiles=%d unit %zu covered %d times", samples, tiles,
+              i, seen[i]);
+    }
+}
+
 int main() {
   check_fastdiv();
   check_tile_orders();
+  check_xcd_sample_tile();
   long long n = 0;
   const int Ps[] = {16, 24, 32, 64, 80, 128, 256, 304, 512};
   const int Ls[] = {1, 2, 3, 5, 8, 9, 17};
