@@ -19,6 +19,7 @@
 // activation's decision is then that of the exact pre-activation of the fp32-stored inputs, as
 // in the dense and convolution forward kernels); cotangents are fp32.
 #include <algorithm>
+#include <type_traits>
 
 #include "../../include/ntk.h"
 #include "gemm_core.hpp"
@@ -403,12 +404,11 @@ k_pix_wgrad(const float* __restrict__ G, const float* __restrict__ x, int rows, 
 // Depthwise form (9 taps, optional bias): the nine shifted input pixels of a pixel are shared
 // by the O cotangent rows of its image, so a workgroup takes one image, one band of its pixels
 // and 64 channels (lane = channel, wave = pixel group), loads the nine taps once per pixel and
-// accumulates them against OB rows (n, o) at a time.  The four waves' sums are added in a
-// fixed order through LDS; with several bands, each band writes its sums to `part`
-// ([band][row][10 C], bias last) and k_band_reduce adds the bands in order.
-constexpr int kDwOB = 8;
-
-template <bool BIAS>
+// accumulates them against OB rows (n, o) at a time (OB: the launcher's choice, close to a
+// divisor of O, so that passes carry few unused rows).  The four waves' sums are added in a fixed
+// order through LDS; with several bands, each band writes its sums to `part` ([band][row][10 C],
+// bias last) and k_band_reduce adds the bands in order.
+template <int kDwOB, bool BIAS>
 __global__ void __launch_bounds__(256)
 k_dw_wgrad(const float* __restrict__ G, const float* __restrict__ x, int images, int O, int H, int W,
            FastDiv fW, int C, int bands, int cgroups, float* __restrict__ out, long long ld_out,
@@ -456,21 +456,24 @@ k_dw_wgrad(const float* __restrict__ G, const float* __restrict__ x, int images,
           if constexpr (BIAS) acc[i][9] += g[i];
         }
       }
+      // rows o0 + i < O only (uniform over the workgroup); fully unrolled so that acc[i] stays in
+      // registers
 #pragma unroll
       for (int i = 0; i < kDwOB; ++i) {
-        if (o0 + i >= O) break;   // uniform over the workgroup
-        __syncthreads();          // the previous row's sums have been read
+        if (o0 + i < O) {
+          __syncthreads();   // the previous row's sums have been read
 #pragma unroll
-        for (int a = 0; a < NA; ++a) red[wave][a][lane] = acc[i][a];
-        __syncthreads();
-        const long long r = (long long)n * O + o0 + i;
-        for (int j = threadIdx.x; j < NA * 64; j += 256) {
-          const int a = j >> 6, l = j & 63;
-          const int c = cgi * 64 + l;
-          if (c < C) {
-            const float sum = ((red[0][a][l] + red[1][a][l]) + red[2][a][l]) + red[3][a][l];
-            const long long col = a < 9 ? off_w + (long long)a * C + c : off_b + c;
-            out[band * band_stride + r * ld_out + col] = sum;
+          for (int a = 0; a < NA; ++a) red[wave][a][lane] = acc[i][a];
+          __syncthreads();
+          const long long r = (long long)n * O + o0 + i;
+          for (int j = threadIdx.x; j < NA * 64; j += 256) {
+            const int a = j >> 6, l = j & 63;
+            const int c = cgi * 64 + l;
+            if (c < C) {
+              const float sum = ((red[0][a][l] + red[1][a][l]) + red[2][a][l]) + red[3][a][l];
+              const long long col = a < 9 ? off_w + (long long)a * C + c : off_b + c;
+              out[band * band_stride + r * ld_out + col] = sum;
+            }
           }
         }
       }
@@ -636,12 +639,22 @@ hipError_t launch_pix_wgrad(hipStream_t s, const float* G, const float* x, int i
     float* out = bands > 1 ? part : J;
     const long long ld_out = bands > 1 ? ncols : ldJ;
     const long long ow = bands > 1 ? 0 : off_w, ob = bands > 1 ? 9LL * C : off_b;
-    if (bias)
-      k_dw_wgrad<true><<<dim3(grid), dim3(256), 0, s>>>(G, x, images, O, H, W, FastDiv((uint32_t)W), C,
-                                                          (int)bands, cgroups, out, ld_out, ow, ob, per_band);
-    else
-      k_dw_wgrad<false><<<dim3(grid), dim3(256), 0, s>>>(G, x, images, O, H, W, FastDiv((uint32_t)W), C,
-                                                           (int)bands, cgroups, out, ld_out, ow, ob, per_band);
+    auto go = [&](auto ob_tag) {
+      constexpr int OB = decltype(ob_tag)::value;
+      if (bias)
+        k_dw_wgrad<OB, true><<<dim3(grid), dim3(256), 0, s>>>(G, x, images, O, H, W, FastDiv((uint32_t)W), C,
+                                                              (int)bands, cgroups, out, ld_out, ow, ob, per_band);
+      else
+        k_dw_wgrad<OB, false><<<dim3(grid), dim3(256), 0, s>>>(G, x, images, O, H, W, FastDiv((uint32_t)W), C,
+                                                               (int)bands, cgroups, out, ld_out, ow, ob, per_band);
+    };
+    // cotangent rows per pass: O rounded up to 1, 2, 4, 5 or 8; two passes of 5 for 9 or 10 rows
+    // (ten rows' sums in registers make the compiler wait after each load); 8 beyond
+    if (O <= 1) go(std::integral_constant<int, 1>{});
+    else if (O <= 2) go(std::integral_constant<int, 2>{});
+    else if (O <= 4) go(std::integral_constant<int, 4>{});
+    else if (O <= 5 || O == 9 || O == 10) go(std::integral_constant<int, 5>{});
+    else go(std::integral_constant<int, 8>{});
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || bands == 1) return e;
     // the band sums have a row stride of 10 C; without a bias only the first 9 C are written
