@@ -153,3 +153,14 @@ def test_struct_graph_replays_and_determinism():
             assert torch.equal(out, eager)
     finally:
         h.close()
+
+
+@pytest.mark.parametrize("symmetric", [True, False])
+def test_hand_worked_struct_golden_on_gpu(golden_dir, symmetric):
+    import json
+    import os
+    d = json.load(open(os.path.join(golden_dir, "cnn_hand_struct.json")))
+    params = [np.array(p, dtype=np.float32) for p in d["params"]]
+    X = np.array(d["X"], dtype=np.float32)
+    got = gpu_ntk(d["spec"], params, X, X, symmetric=symmetric)
+    np.testing.assert_allclose(got, np.array(d["theta"]), rtol=1e-6, atol=1e-5)

@@ -127,7 +127,7 @@ def test_closed_form_two_linear_layers():
 
 
 @pytest.mark.parametrize("fname", ["fcn_hand_relu.json", "fcn_hand_relu_bias.json",
-                                   "cnn_hand_1x2.json"])
+                                   "cnn_hand_1x2.json", "cnn_hand_struct.json"])
 def test_hand_worked_golden(golden_dir, fname):
     d = json.load(open(os.path.join(golden_dir, fname)))
     spec = d["spec"]
@@ -224,7 +224,7 @@ def test_block_chunking_does_not_change_the_result():
 
 # ---- float32 layer storage (the mode GPU parity uses) --------------------------------------
 @pytest.mark.parametrize("fname", ["fcn_hand_relu.json", "fcn_hand_relu_bias.json",
-                                   "cnn_hand_1x2.json"])
+                                   "cnn_hand_1x2.json", "cnn_hand_struct.json"])
 def test_fp32_storage_reproduces_the_hand_worked_values(golden_dir, fname):
     # every intermediate value of these examples is exactly representable in float32
     d = json.load(open(os.path.join(golden_dir, fname)))
