@@ -26,14 +26,14 @@ inputs, the values the GPU library decides on.
 Conventions (the paper leaves them to the framework): ReLU'(0) = 0;
 erf'(z) = 2/sqrt(pi) exp(-z^2); convolutions are SAME (zero pad 1), stride 1,
 cross-correlation, NHWC activations, OHWI weights ([3, 3, C] for a depthwise
-convolution); a scale layer multiplies channel c (or feature c) by w[c];
+convolution, [Cout, Cin] for a pointwise 1x1 convolution); a scale layer multiplies channel c (or feature c) by w[c];
 "avgpool2" is the mean over 2x2 windows with stride 2; "gap" is the mean over
 the H*W pixels.  Inputs arrive as float32 and are upcast exactly to float64.
 
 Layer kinds and the structure of their weight-space Jacobian dz/dtheta (the
 paper's appendix on structured derivatives; the oracle forms each block
 explicitly all the same):
-* dense, conv3x3: constant-block-diagonal (a matrix product along one axis);
+* dense, conv3x3, conv1x1: constant-block-diagonal (a matrix product along one axis);
 * dwconv3x3: block-diagonal over channels (channel c's filter only feeds
   output channel c);
 * scale: block-diagonal over channels, and for images also output block-tiled
@@ -99,7 +99,7 @@ def _patches_transpose(dp, H, W, C):
 
 # ----------------------------------------------------------------------------- parameters
 # layer kinds with a weight (then an optional bias) and an activation
-_PARAM_KINDS = ("dense", "conv3x3", "dwconv3x3", "scale")
+_PARAM_KINDS = ("dense", "conv3x3", "conv1x1", "dwconv3x3", "scale")
 
 
 def _split_params(spec, params):
@@ -125,7 +125,7 @@ def _split_params(spec, params):
 def param_count(spec):
     P = 0
     for L in spec["layers"]:
-        if L["kind"] == "dense":
+        if L["kind"] in ("dense", "conv1x1"):
             P += L["out"] * L["in"] + (L["out"] if L["bias"] else 0)
         elif L["kind"] == "conv3x3":
             P += L["out"] * 9 * L["in"] + (L["out"] if L["bias"] else 0)
@@ -168,6 +168,13 @@ def _forward_record(spec, params, X, layer_storage="fp64"):
                 z = z + b
             z = z.reshape(N, H, W, w.shape[0])
             rec.append({"h": h, "z": z, "patches": pt})
+            h = _store(_phi(L["act"], z), layer_storage)
+        elif L["kind"] == "conv1x1":
+            w, b = p                                          # [Cout, Cin], every pixel
+            z = h @ w.T
+            if b is not None:
+                z = z + b
+            rec.append({"h": h, "z": z})
             h = _store(_phi(L["act"], z), layer_storage)
         elif L["kind"] == "dwconv3x3":
             w, b = p                                          # [3, 3, C]
@@ -232,6 +239,10 @@ def _output_cotangents(spec, params, rec, outputs):
             Cin = w.shape[3]
             dp = g.reshape(N, g.shape[1], H * W, Cout) @ w.reshape(Cout, -1)   # [N,Os,D,9Cin]
             g = _patches_transpose(dp, H, W, Cin)        # df/dh_li: [N, Os, H, W, Cin]
+        elif L["kind"] == "conv1x1":
+            G[li] = g
+            w, _ = wb[li]
+            g = g @ w                                     # df/dh_li: [N, Os, H, W, Cin]
         elif L["kind"] == "dwconv3x3":
             G[li] = g
             w, _ = wb[li]
@@ -302,6 +313,19 @@ def jacobian_blocks(spec, params, X, outputs=None, max_block_bytes=256 << 20, ch
                 # weight sharing over pixels: J[n,o,c,k] = sum_p G[n,o,p,c] patch[n,p,k]
                 J = np.swapaxes(gf[:, :, :, c0:c1], 2, 3) @ pt[:, None]   # [N,Os,cc,9Cin]
                 yield J.reshape(R, (c1 - c0) * k9)
+            if L["bias"]:
+                yield gf.sum(axis=2).reshape(R, cout)
+        elif L["kind"] == "conv1x1":
+            h = rec[li]["h"]                               # [N, H, W, Cin]
+            cout, cin = L["out"], L["in"]
+            hf = h.reshape(N, -1, cin)                     # [N, D, Cin]
+            gf = G[li].reshape(N, len(outputs), -1, cout)  # [N, Os, D, Cout]
+            step = max(1, int(max_block_bytes // (8 * Rc * cin)))
+            for c0 in range(0, cout, step):
+                c1 = min(cout, c0 + step)
+                # weight sharing over pixels: J[n,o,c,j] = sum_p G[n,o,p,c] h[n,p,j]
+                J = np.swapaxes(gf[:, :, :, c0:c1], 2, 3) @ hf[:, None]    # [N,Os,cc,Cin]
+                yield J.reshape(R, (c1 - c0) * cin)
             if L["bias"]:
                 yield gf.sum(axis=2).reshape(R, cout)
         elif L["kind"] == "dwconv3x3":

@@ -83,7 +83,8 @@ def _spatial_layers(spec):
 
 
 def _weight_cols(kind, cin, cout):
-    return {"conv3x3": 9 * cin * cout, "dwconv3x3": 9 * cout, "scale": cout}.get(kind, 0)
+    return {"conv3x3": 9 * cin * cout, "conv1x1": cin * cout, "dwconv3x3": 9 * cout,
+            "scale": cout}.get(kind, 0)
 
 
 def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", batch="full"):
@@ -105,7 +106,13 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
     # "struct_wgrad"); a conv bias is added in the conv forward kernel's epilogue
     fwd = bwd = wg = sfwd = sbwd = swg = cols = io = 0.0
     for i, (k, cin, cout, D, bias) in enumerate(sp):
-        if k == "conv3x3":
+        if k == "conv1x1":   # pointwise: always outside-in
+            fwd += 2.0 * M * D * cin * cout + (1.0 * M * D * cout if bias else 0.0)
+            if i >= 1:
+                bwd += 2.0 * M * Oe * D * cout * cin
+            wg += 2.0 * M * (Oe * cout) * cin * D
+            cols += cin * cout
+        elif k == "conv3x3":
             fwd += 2.0 * M * D * 9 * cin * cout + (1.0 * M * D * cout if bias else 0.0)
             if i >= 1:
                 bwd += 2.0 * M * Oe * D * 9 * cout * cin
@@ -151,7 +158,7 @@ def param_total(spec):
         k = Lr["kind"]
         if k == "dense":
             P += Lr["out"] * Lr["in"]
-        elif k in ("conv3x3", "dwconv3x3", "scale"):
+        elif k in ("conv3x3", "conv1x1", "dwconv3x3", "scale"):
             P += _weight_cols(k, Lr["in"], Lr["out"])
         else:
             continue
@@ -193,11 +200,12 @@ def vp_flops(spec, n1, n2, symmetric=False):
     M = n1 if symmetric else n1 + n2
     layers = spec["layers"]
     if any(Lr["kind"] != "dense" for Lr in layers):
-        # the 3x3 convolutions' matrix-core work (D: each layer's own pixels); the memory-bound
+        # the 3x3 and 1x1 convolutions' matrix-core work (D: each layer's own pixels); the memory-bound
         # depthwise, scale, bias and pool steps are not counted
         sp, C = _spatial_layers(spec)
         O = layers[-1]["out"]
-        conv = [(i, D, 9 * cin * cout) for i, (k, cin, cout, D, _) in enumerate(sp) if k == "conv3x3"]
+        conv = [(i, D, _weight_cols(k, cin, cout)) for i, (k, cin, cout, D, _) in enumerate(sp)
+                if k in ("conv3x3", "conv1x1")]
         first = min([i for i, (k, *_r) in enumerate(sp) if k != "avgpool2"] or [0])
         st = {
             "forward_and_jvp": sum(2.0 * M * D * k for _, D, k in conv) + sum(2.0 * n1 * D * k for _, D, k in conv)

@@ -102,3 +102,18 @@ def test_structured_layer_kinds_counts():
     assert param_total(spec) == oracle.param_count(spec) == 9 * 2 * 8 + 8 + 9 * 8 + 8 + 8 + 8 * O
     jc = ntk_flops(spec, N, N, method="jacobian")
     assert jc["contraction"] == 2 * N * N * O * O * oracle.param_count(spec)
+
+
+def test_pointwise_counts():
+    import oracle
+    from paper_2206_08720_amd.flops import param_total
+    N, O = 2, 3
+    spec = wl.cnn_layers_spec("pw", (2, 4), 3, [("conv1x1", 6, "relu", True), ("dwconv3x3", "relu", False),
+                                               ("conv1x1", 5, "erf", False)], O)
+    f = cnn_flops(spec, N, N)
+    M, D = 2 * N, 8
+    assert f["forward"] == 2 * M * D * 3 * 6 + M * D * 6 + 2 * M * D * 6 * 5
+    assert f["backward"] == 2 * M * O * D * 5 * 6
+    assert f["wgrad"] == 2 * M * O * 6 * 3 * D + 2 * M * O * 5 * 6 * D
+    assert f["contraction"] == 2 * N * N * O * O * (3 * 6 + 6 + 9 * 6 + 6 * 5)
+    assert param_total(spec) == oracle.param_count(spec)

@@ -37,10 +37,15 @@ def _tiny_specs():
                             [("dwconv3x3", "relu", False), ("conv3x3", 4, "none", True),
                              ("scale", "relu", False), ("avgpool2",), ("dwconv3x3", "none", True)],
                             2), "2/fan_in"),
+        # depthwise-separable blocks: depthwise 3x3 then pointwise 1x1
+        (wl.cnn_layers_spec("cnn_separable_erf", (4, 6), 3,
+                            [("conv1x1", 4, "erf", True), ("dwconv3x3", "erf", False),
+                             ("conv1x1", 5, "erf", True), ("avgpool2",), ("conv1x1", 3, "none", False)],
+                            2), "2/fan_in"),
     ]
 
 
-@pytest.mark.parametrize("idx", range(7))
+@pytest.mark.parametrize("idx", range(8))
 def test_forward_matches_torch_layers(idx):
     spec, wv = _tiny_specs()[idx]
     params = wl.make_params(spec, 11 + idx, wv, bias_var=0.3)
@@ -51,7 +56,7 @@ def test_forward_matches_torch_layers(idx):
     np.testing.assert_allclose(got, ref, rtol=1e-13, atol=1e-13)
 
 
-@pytest.mark.parametrize("idx", range(7))
+@pytest.mark.parametrize("idx", range(8))
 def test_jacobian_matches_torch_autograd(idx):
     spec, wv = _tiny_specs()[idx]
     params = wl.make_params(spec, 31 + idx, wv, bias_var=0.3)
@@ -72,7 +77,7 @@ def _relu_margin_ok(spec, params, X, margin=1e-3):
     return True
 
 
-@pytest.mark.parametrize("idx", [0, 1, 3, 4, 5])
+@pytest.mark.parametrize("idx", [0, 1, 3, 4, 5, 7])
 def test_jacobian_central_finite_differences(idx):
     spec, wv = _tiny_specs()[idx]
     params = wl.make_params(spec, 51 + idx, wv, bias_var=0.3)
@@ -137,7 +142,7 @@ def test_hand_worked_golden(golden_dir, fname):
     np.testing.assert_allclose(th, np.array(d["theta"]), rtol=0, atol=1e-12)
 
 
-@pytest.mark.parametrize("idx", [0, 1, 3, 5, 6])
+@pytest.mark.parametrize("idx", [0, 1, 3, 5, 6, 7])
 def test_symmetry_and_psd(idx):
     spec, wv = _tiny_specs()[idx]
     params = wl.make_params(spec, 71 + idx, wv, bias_var=0.3)
@@ -368,3 +373,38 @@ def test_depthwise_with_one_channel_is_a_3x3_conv():
     X2 = wl.make_inputs(dw, 2, 263)
     np.testing.assert_allclose(oracle.ntk_jc(dw, params, X1, X2),
                                oracle.ntk_jc(cv, cparams, X1, X2), rtol=1e-13, atol=1e-14)
+
+
+def test_pointwise_layers_on_1x1_images_are_the_mlp():
+    # on 1x1 images a pointwise convolution is a dense layer and the pool over one pixel is the
+    # identity, so the CNN's NTK is the MLP's
+    spec = wl.cnn_layers_spec("pw1x1", (1, 1), 5, [("conv1x1", 7, "erf", True), ("conv1x1", 6, "relu", True)], 3)
+    params = wl.make_params(spec, 271, "2/fan_in", bias_var=0.3)
+    X1 = wl.make_inputs(spec, 3, 272)
+    X2 = wl.make_inputs(spec, 4, 273)
+    mlp = {"name": "mlp", "input_shape": (5,),
+           "layers": [{"kind": "dense", "in": 5, "out": 7, "act": "erf", "bias": True},
+                      {"kind": "dense", "in": 7, "out": 6, "act": "relu", "bias": True},
+                      {"kind": "dense", "in": 6, "out": 3, "act": "none", "bias": False}]}
+    a = oracle.ntk_jc(spec, params, X1, X2)
+    b = oracle.ntk_jc(mlp, params, X1.reshape(3, 5), X2.reshape(4, 5))
+    np.testing.assert_allclose(a, b, rtol=1e-13, atol=1e-14)
+
+
+def test_pointwise_is_the_centre_tap_of_a_3x3_conv():
+    # a 3x3 convolution whose only nonzero tap is the centre acts as a pointwise one
+    pw = wl.cnn_layers_spec("pw", (3, 4), 3, [("conv1x1", 5, "erf", True)], 2)
+    cv = wl.cnn_layers_spec("cv", (3, 4), 3, [("conv3x3", 5, "erf", True)], 2)
+    params = wl.make_params(pw, 281, "2/fan_in", bias_var=0.3)
+    K = np.zeros((5, 3, 3, 3), dtype=np.float32)
+    K[:, 1, 1, :] = params[0]
+    X = wl.make_inputs(pw, 3, 282)
+    np.testing.assert_allclose(oracle.forward(pw, params, X), oracle.forward(cv, [K] + params[1:], X),
+                               rtol=1e-13, atol=1e-14)
+    # the Jacobian blocks: the pointwise block is the 3x3 block's centre-tap columns
+    Jp = oracle.jacobian(pw, params, X)
+    Jc = oracle.jacobian(cv, [K] + params[1:], X)
+    centre = np.zeros((5, 3, 3, 3), dtype=bool)
+    centre[:, 1, 1, :] = True
+    np.testing.assert_allclose(Jp[:, :, :15], Jc[:, :, :135][:, :, centre.ravel()], rtol=1e-13, atol=1e-14)
+    np.testing.assert_allclose(Jp[:, :, 15:], Jc[:, :, 135:], rtol=1e-13, atol=1e-14)

@@ -1,7 +1,8 @@
 """A float64 PyTorch (CPU) implementation of the workload networks, used only to pin the oracle.
 
 It builds f(theta, x) from torch's own layer routines (linear, conv2d with
-padding 1 -- grouped per channel for the depthwise layer --, avg_pool2d, relu,
+padding 1 -- grouped per channel for the depthwise layer, 1x1 for the pointwise one --,
+avg_pool2d, relu,
 erf, mean) so that torch autograd provides an independent
 Jacobian against which the oracle's hand-written reverse-mode Jacobian is
 checked.
@@ -32,6 +33,16 @@ def torch_forward(spec, flat_params, X):
                 i += 1
             # NHWC activations, OHWI weights -> torch's NCHW / OIHW
             y = F.conv2d(h.permute(0, 3, 1, 2), w.permute(0, 3, 1, 2), b, stride=1, padding=1)
+            h = y.permute(0, 2, 3, 1)
+        elif L["kind"] == "conv1x1":
+            w = flat_params[i]
+            i += 1
+            b = None
+            if L["bias"]:
+                b = flat_params[i]
+                i += 1
+            # weights [Cout, Cin] -> torch's OIHW with a 1x1 kernel
+            y = F.conv2d(h.permute(0, 3, 1, 2), w[:, :, None, None], b)
             h = y.permute(0, 2, 3, 1)
         elif L["kind"] == "dwconv3x3":
             w = flat_params[i]

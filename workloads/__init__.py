@@ -12,17 +12,18 @@ Network specification (a plain dict)::
      "input_shape": (d0,)  for a fully-connected net, or (H, W, C) NHWC for a CNN,
      "layers": [ {"kind": "dense",     "in": int, "out": int, "act": "relu"|"erf"|"none", "bias": bool},
                  {"kind": "conv3x3",   "in": int, "out": int, "act": ..., "bias": bool},
+                 {"kind": "conv1x1",   "in": int, "out": int, "act": ..., "bias": bool},
                  {"kind": "dwconv3x3", "in": C,   "out": C,   "act": ..., "bias": bool},
                  {"kind": "scale",     "in": C,   "out": C,   "act": ..., "bias": bool},
                  {"kind": "avgpool2"},
                  {"kind": "gap"} ]}
 
 Parameter order: layer by layer, the weight first and then the bias if the
-layer has one.  Dense weights are [out, in] row-major; 3x3 convolution weights
-are [Cout, 3, 3, Cin] (OHWI); depthwise 3x3 weights are [3, 3, C] (one 3x3
+layer has one.  Dense and pointwise (1x1 convolution) weights are [out, in] row-major;
+3x3 convolution weights are [Cout, 3, 3, Cin] (OHWI); depthwise 3x3 weights are [3, 3, C] (one 3x3
 filter per channel, channel fastest); scale weights are [C].  The forward map
-is z = h W^T (+ b) for a dense layer, a SAME (zero pad 1), stride-1
-cross-correlation for a conv layer (per channel for the depthwise one),
+is z = h W^T (+ b) for a dense layer and, at every pixel, for a pointwise layer, a SAME
+(zero pad 1), stride-1 cross-correlation for a 3x3 conv layer (per channel for the depthwise one),
 z = h * w (+ b) broadcast over the pixels for a scale layer, and
 h_next = act(z).  "avgpool2" is the mean over non-overlapping 2x2 windows
 (stride 2; H and W even) and "gap" the mean over all pixels; neither has
@@ -82,15 +83,15 @@ def cnn_spec(name, hw, c_in, channels, d_out, act="relu", bias=False):
 def cnn_layers_spec(name, hw, c_in, blocks, d_out):
     """CNN from a list of blocks, then global average pooling and a dense readout.
 
-    Each block is one of ("conv3x3", c_out, act, bias), ("dwconv3x3", act, bias),
-    ("scale", act, bias) or ("avgpool2",).
+    Each block is one of ("conv3x3", c_out, act, bias), ("conv1x1", c_out, act, bias),
+    ("dwconv3x3", act, bias), ("scale", act, bias) or ("avgpool2",).
     """
     H, W = hw
     layers = []
     c = c_in
     for b in blocks:
         kind = b[0]
-        if kind == "conv3x3":
+        if kind in ("conv3x3", "conv1x1"):
             _, co, act, bias = b
             layers.append({"kind": kind, "in": c, "out": co, "act": act, "bias": bool(bias)})
             c = co
@@ -107,14 +108,14 @@ def cnn_layers_spec(name, hw, c_in, blocks, d_out):
 
 
 # layer kinds that carry parameters (a weight, then an optional bias) and an activation
-PARAM_KINDS = ("dense", "conv3x3", "dwconv3x3", "scale")
+PARAM_KINDS = ("dense", "conv3x3", "conv1x1", "dwconv3x3", "scale")
 
 
 def param_shapes(spec):
     """Shapes of the parameter tensors in order (weight, then bias if present)."""
     shapes = []
     for L in spec["layers"]:
-        if L["kind"] == "dense":
+        if L["kind"] in ("dense", "conv1x1"):
             shapes.append((L["out"], L["in"]))
             if L["bias"]:
                 shapes.append((L["out"],))
@@ -140,8 +141,8 @@ def output_dim(spec):
 def make_params(spec, seed, weight_var="1/fan_in", bias_var=0.01):
     """Draw float32 parameters.  weight_var is "1/fan_in" or "2/fan_in" (a variance).
 
-    fan_in is `in` for a dense layer, 9*Cin for a 3x3 convolution and 9 for a
-    depthwise one.  Scale weights are drawn around 1, as N(1, 0.01), like the
+    fan_in is `in` for a dense or pointwise layer, 9*Cin for a 3x3 convolution and 9
+    for a depthwise one.  Scale weights are drawn around 1, as N(1, 0.01), like the
     affine scale of a normalisation layer.  Biases are N(0, bias_var)
     (bias_var is a variance).
     """
@@ -149,7 +150,7 @@ def make_params(spec, seed, weight_var="1/fan_in", bias_var=0.01):
     scale = {"1/fan_in": 1.0, "2/fan_in": 2.0}[weight_var]
     params = []
     for L in spec["layers"]:
-        if L["kind"] == "dense":
+        if L["kind"] in ("dense", "conv1x1"):
             fan_in = L["in"]
             shape = (L["out"], L["in"])
         elif L["kind"] == "conv3x3":
