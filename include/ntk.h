@@ -29,6 +29,8 @@
  *     order, at least one of them with parameters:
  *       CONV3X3_SAME   z = 3x3 cross-correlation, stride 1, zero padding 1, weights
  *                      [Cout,3,3,Cin] (OHWI), optional bias [Cout];
+ *       CONV1X1        pointwise: a dense layer at every pixel, weights [Cout,Cin],
+ *                      optional bias [Cout];
  *       DWCONV3X3_SAME depthwise: channel c convolved with its own 3x3 filter, weights
  *                      [3,3,C], optional bias [C]; in == out;
  *       SCALE          z = h * w[c], weights [C], optional bias [C]; in == out;
@@ -37,7 +39,7 @@
  *     Activations are NHWC.  The three parametrised kinds take any activation.
  *     How each kind's weight-space Jacobian is structured, and how it is contracted:
  *     the 3x3 convolution is constant-block-diagonal (the outside-in or inside-out
- *     orders of NTK_OPT_CONV_ORDER); the depthwise convolution is block-diagonal over
+ *     orders of NTK_OPT_CONV_ORDER), the pointwise one too (outside-in: Cout*Cin columns); the depthwise convolution is block-diagonal over
  *     channels and the scale layer block-diagonal over channels and output
  *     block-tiled over pixels (appendix "Block Diagonal", "Output Block-tiled"): their
  *     weight-space cotangents are per-channel pixel sums, 9*C and C columns; every
@@ -81,14 +83,15 @@ extern "C" {
 #define NTK_DWCONV3X3_SAME 3
 #define NTK_SCALE          4
 #define NTK_AVGPOOL2       5
+#define NTK_CONV1X1        6
 
 #define NTK_ACT_NONE       0
 #define NTK_ACT_RELU       1
 #define NTK_ACT_ERF        2
 
 typedef struct ntk_layer_desc {
-    int kind;      /* NTK_DENSE, NTK_CONV3X3_SAME, NTK_DWCONV3X3_SAME, NTK_SCALE,
-                      NTK_AVGPOOL2 or NTK_GAP                                             */
+    int kind;      /* NTK_DENSE, NTK_CONV3X3_SAME, NTK_CONV1X1, NTK_DWCONV3X3_SAME,
+                      NTK_SCALE, NTK_AVGPOOL2 or NTK_GAP                                  */
     int in;        /* input features / input channels (ignored for AVGPOOL2 and GAP)      */
     int out;       /* output features / output channels (ignored for AVGPOOL2 and GAP)    */
     int act;       /* activation applied to this layer's output (NTK_ACT_*; AVGPOOL2 and
@@ -179,7 +182,8 @@ int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, void* hip_stre
  * ntk_compute -- enqueue Theta(X1, X2) on the handle's stream.
  *   params  host array of device pointers, one per parameter tensor in layer
  *           order, weight first then bias (if has_bias): dense weight [out, in]
- *           row-major, conv weight [Cout, 3, 3, Cin] (OHWI), depthwise weight
+ *           row-major, conv weight [Cout, 3, 3, Cin] (OHWI), pointwise weight
+ *           [Cout, Cin], depthwise weight
  *           [3, 3, C], scale weight [C], every bias [out]; AVGPOOL2 and GAP have none.
  *   X1      device [n1, in_c] (FCN) or [n1, in_h, in_w, in_c] NHWC (CNN), fp32.
  *   X2      device, same layout with n2 rows.  X2 == X1 with n2 == n1 selects the

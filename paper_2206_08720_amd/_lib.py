@@ -23,7 +23,7 @@ ERROR_NAMES = {NTK_E_ARG: "NTK_E_ARG", NTK_E_SHAPE: "NTK_E_SHAPE",
                NTK_E_HIP: "NTK_E_HIP"}
 
 NTK_DENSE, NTK_CONV3X3_SAME, NTK_GAP = 0, 1, 2
-NTK_DWCONV3X3_SAME, NTK_SCALE, NTK_AVGPOOL2 = 3, 4, 5
+NTK_DWCONV3X3_SAME, NTK_SCALE, NTK_AVGPOOL2, NTK_CONV1X1 = 3, 4, 5, 6
 NTK_ACT_NONE, NTK_ACT_RELU, NTK_ACT_ERF = 0, 1, 2
 NTK_OPT_SYMMETRIC, NTK_OPT_CONV_ORDER = 1, 2
 NTK_CONV_ORDER_AUTO, NTK_CONV_ORDER_OUTSIDE_IN, NTK_CONV_ORDER_INSIDE_OUT = 0, 1, 2
@@ -125,7 +125,8 @@ def check(rc, handle=None):
 
 
 _KIND = {"dense": NTK_DENSE, "conv3x3": NTK_CONV3X3_SAME, "gap": NTK_GAP,
-         "dwconv3x3": NTK_DWCONV3X3_SAME, "scale": NTK_SCALE, "avgpool2": NTK_AVGPOOL2}
+         "dwconv3x3": NTK_DWCONV3X3_SAME, "scale": NTK_SCALE, "avgpool2": NTK_AVGPOOL2,
+         "conv1x1": NTK_CONV1X1}
 _ACT = {"none": NTK_ACT_NONE, "relu": NTK_ACT_RELU, "erf": NTK_ACT_ERF}
 
 

@@ -16,6 +16,8 @@
 //     cotangent J[(n,o),(c,k)] = sum_p G[n,o,p,c] patch[n,p,k]
 //   * J1 J2^T with a deterministic split over K, then a reduction adding the readout
 //     summand (g1.g2) delta_{o1 o2} and writing theta[n1][n2][o1][o2].
+#include <type_traits>
+
 #include "gemm_core.hpp"
 #include "launch_conv.hpp"
 
@@ -746,7 +748,7 @@ hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int
 // ------------------------------------------------------------------------------ weight-space cotangent
 // For sample s = blockIdx.y:  J[s*O + o][off + c*KC + k] = sum_p G[s,o,p,c] patch[s,p,k]
 // (VA / VB: float4 loads of the cotangent / patch operand)
-template <class Cfg, bool VA, bool VB>
+template <class Cfg, bool VA, bool VB, bool PW>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, int H, int W, int C,
              int Cin, FastDiv fC, FastDiv fW, FastDiv fCin, float* __restrict__ J, long long ldJ,
@@ -755,7 +757,7 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
   int s, t;
   if (!xcd_sample_tile(blockIdx.x, tiles_m * tiles_n, samples, s, t)) return;
   const int D = H * W;
-  const int KC = 9 * Cin;
+  const int KC = PW ? Cin : 9 * Cin;
   const int tm = t / tiles_n, tn = t - tm * tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   LoadCotangentKOuterT<VA> la;
@@ -765,18 +767,30 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
   la.C = C;
   la.D = D;
   la.fC = fC;
-  LoadPatchesKOuterT<VB> lb;
-  lb.x = h + (long long)s * D * Cin;
-  lb.rows = KC;
-  lb.K = D;
-  lb.H = H;
-  lb.W = W;
-  lb.C = Cin;
-  lb.fW = fW;
-  lb.fC = fCin;
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
-  gemm_mainloop<Cfg>(la, lb, m0, n0, 0, D, smem, acc);
+  if constexpr (PW) {
+    // pointwise: the columns are the input channels themselves, [D, Cin] of the sample
+    LoadCotangentKOuterT<VB> lb;
+    lb.g = h + (long long)s * D * Cin;
+    lb.rows = Cin;
+    lb.K = D;
+    lb.C = Cin;
+    lb.D = D;
+    lb.fC = fCin;
+    gemm_mainloop<Cfg>(la, lb, m0, n0, 0, D, smem, acc);
+  } else {
+    LoadPatchesKOuterT<VB> lb;
+    lb.x = h + (long long)s * D * Cin;
+    lb.rows = KC;
+    lb.K = D;
+    lb.H = H;
+    lb.W = W;
+    lb.C = Cin;
+    lb.fW = fW;
+    lb.fC = fCin;
+    gemm_mainloop<Cfg>(la, lb, m0, n0, 0, D, smem, acc);
+  }
   const int R = O * C;
   for_each_acc<Cfg>(acc, m0, n0, [&](int r, int k, float v) {
     if (r < R && k < KC) {
@@ -786,8 +800,8 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
   });
 }
 
-// direct-to-LDS form (C % 4 == 0 and Cin % 4 == 0): both operands K-outer, three LDS stages
-template <class Cfg, int NS>
+// direct-to-LDS form (C % 4 == 0 and Cin % 4 == 0): both operands K-outer, NS LDS stages
+template <class Cfg, int NS, bool PW>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O, int H, int W, int C, int Cin, FastDiv fC, FastDiv fW, FastDiv fCin,
                  float* __restrict__ J, long long ldJ, long long off, int tiles_m, int tiles_n, int samples) {
@@ -795,7 +809,7 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
   int s, t;
   if (!xcd_sample_tile(blockIdx.x, tiles_m * tiles_n, samples, s, t)) return;
   const int D = H * W;
-  const int KC = 9 * Cin;
+  const int KC = PW ? Cin : 9 * Cin;
   const int tm = t / tiles_n, tn = t - tm * tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   DmaCotangentKOuter<Cfg::BM, Cfg::WAVES> ia;
@@ -804,18 +818,29 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
   ia.D = D;
   ia.C = C;
   ia.fC = fC;
-  DmaPatchesKOuter<Cfg::BN, Cfg::WAVES> ib;
-  ib.x = h + (long long)s * D * Cin;
-  ib.rows = KC;
-  ib.K = D;
-  ib.H = H;
-  ib.W = W;
-  ib.C = Cin;
-  ib.fW = fW;
-  ib.fC = fCin;
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
-  gemm_mainloop_dma_ops<Cfg, NS>(ia, ib, m0, n0, 0, D, smem, acc);
+  if constexpr (PW) {
+    // pointwise: the columns are the input channels themselves, [D, Cin] of the sample
+    DmaCotangentKOuter<Cfg::BN, Cfg::WAVES> ib;
+    ib.g = h + (long long)s * D * Cin;
+    ib.rows = Cin;
+    ib.D = D;
+    ib.C = Cin;
+    ib.fC = fCin;
+    gemm_mainloop_dma_ops<Cfg, NS>(ia, ib, m0, n0, 0, D, smem, acc);
+  } else {
+    DmaPatchesKOuter<Cfg::BN, Cfg::WAVES> ib;
+    ib.x = h + (long long)s * D * Cin;
+    ib.rows = KC;
+    ib.K = D;
+    ib.H = H;
+    ib.W = W;
+    ib.C = Cin;
+    ib.fW = fW;
+    ib.fC = fCin;
+    gemm_mainloop_dma_ops<Cfg, NS>(ia, ib, m0, n0, 0, D, smem, acc);
+  }
   const int R = O * C;
   for_each_acc<Cfg>(acc, m0, n0, [&](int r, int k, float v) {
     if (r < R && k < KC) {
@@ -830,25 +855,29 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
 // columns) read them through one L2 (xcd_sample_tile).
 static unsigned wgrad_grid(int tiles, int images) { return (unsigned)(8 * ((images + 7) / 8) * tiles); }
 
-template <bool VA, bool VB>
+template <bool VA, bool VB, bool PW>
 static hipError_t conv_wgrad_vec(hipStream_t s, const float* G, const float* h, int images, int O,
                                  int H, int W, int C, int Cin, float* J, long long ldJ, long long off) {
   using Cfg = CfgConv;
   using LA = LoadCotangentKOuterT<VA>;
-  using LB = LoadPatchesKOuterT<VB>;
-  const int tn = cdiv(9 * Cin, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
-  hipError_t e = set_smem<Cfg, LA, LB>((const void*)k_conv_wgrad<Cfg, VA, VB>);
+  using LB = std::conditional_t<PW, LoadCotangentKOuterT<VB>, LoadPatchesKOuterT<VB>>;
+  const int tn = cdiv((PW ? 1 : 9) * Cin, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
+  hipError_t e = set_smem<Cfg, LA, LB>((const void*)k_conv_wgrad<Cfg, VA, VB, PW>);
   if (e != hipSuccess) return e;
-  k_conv_wgrad<Cfg, VA, VB><<<dim3(wgrad_grid(tm * tn, images)), dim3(Cfg::THREADS),
-                              gemm_smem_bytes<Cfg, LA, LB>(), s>>>(
+  k_conv_wgrad<Cfg, VA, VB, PW><<<dim3(wgrad_grid(tm * tn, images)), dim3(Cfg::THREADS),
+                                  gemm_smem_bytes<Cfg, LA, LB>(), s>>>(
       G, h, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
       ldJ, off, tm, tn, images);
   return hipGetLastError();
 }
 
-hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
-                             int W, int C, int Cin, float* J, long long ldJ, long long off) {
-  if ((long long)8 * ((images + 7) / 8) * cdiv(9 * Cin, CfgConv::BN) * cdiv((long long)O * C, CfgConv::BM) >=
+// Per-sample weight-space product of a 3x3 (PW = false: columns (tap, ci) of the patches) or a
+// pointwise (PW = true: columns ci of the layer input) convolution.
+template <bool PW>
+static hipError_t conv_wgrad_any(hipStream_t s, const float* G, const float* h, int images, int O, int H,
+                                 int W, int C, int Cin, float* J, long long ldJ, long long off) {
+  const int KC = (PW ? 1 : 9) * Cin;
+  if ((long long)8 * ((images + 7) / 8) * cdiv(KC, CfgConv::BN) * cdiv((long long)O * C, CfgConv::BM) >=
       (1LL << 31))
     return hipErrorInvalidValue;
   // direct-to-LDS: one sample's cotangents and layer input each within a buffer resource
@@ -856,20 +885,30 @@ hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int 
       (long long)H * W * Cin * 4 < (1LL << 31)) {
     using Cfg = CfgConvWg;
     constexpr int NS = kConvWgStages;
-    const int tn = cdiv(9 * Cin, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
+    const int tn = cdiv(KC, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
     constexpr int bytes = gemm_dma_smem_bytes<Cfg, NS>();
-    hipError_t e = hipFuncSetAttribute((const void*)k_conv_wgrad_dma<Cfg, NS>,
+    hipError_t e = hipFuncSetAttribute((const void*)k_conv_wgrad_dma<Cfg, NS, PW>,
                                        hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
     if (e != hipSuccess) return e;
-    k_conv_wgrad_dma<Cfg, NS><<<dim3(wgrad_grid(tm * tn, images)), dim3(Cfg::THREADS), bytes, s>>>(
+    k_conv_wgrad_dma<Cfg, NS, PW><<<dim3(wgrad_grid(tm * tn, images)), dim3(Cfg::THREADS), bytes, s>>>(
         G, h, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
         ldJ, off, tm, tn, images);
     return hipGetLastError();
   }
   const bool va = C % 4 == 0 && aligned16(G), vb = Cin % 4 == 0 && aligned16(h);
-  if (va && vb) return conv_wgrad_vec<true, true>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
-  if (va) return conv_wgrad_vec<true, false>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
-  return conv_wgrad_vec<false, false>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
+  if (va && vb) return conv_wgrad_vec<true, true, PW>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
+  if (va) return conv_wgrad_vec<true, false, PW>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
+  return conv_wgrad_vec<false, false, PW>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
+}
+
+hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
+                             int W, int C, int Cin, float* J, long long ldJ, long long off) {
+  return conv_wgrad_any<false>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
+}
+
+hipError_t launch_pw_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H, int W,
+                           int C, int Cin, float* J, long long ldJ, long long off) {
+  return conv_wgrad_any<true>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
 }
 
 // ------------------------------------------------------------------------------ split-K J1 J2^T

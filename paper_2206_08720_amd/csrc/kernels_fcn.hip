@@ -27,6 +27,7 @@ constexpr int kSkPerCu = 2, kSkStages = 2;
 // the forward splits K (up to kFwdMaxSplits ways) below kFwdSplitTiles output tiles
 constexpr int kFwdSplitTiles = 256, kFwdMaxSplits = 8;
 using CfgSmall = TileCfg<64, 64, 32, 32, 32>;   // 4 waves, 32x32 per wave
+using CfgPw = TileCfg<256, 64, 32, 32, 64>;     // pointwise backward, <= 64 channels: 8 waves
 using CfgFwd64 = TileCfg<64, 64, 32, 32, 16>;   // fp64 forward: 8 waves, 32x16 per wave
 using TrueT = std::true_type;
 using FalseT = std::false_type;
@@ -194,9 +195,39 @@ struct EpiBwd {
   }
 };
 
-template <class Cfg, bool VEC, bool DMA>
+// Pointwise-convolution form: rows r = (img*O + o)*D + p of cotangent pixels; the act' of the
+// layer before is per image pixel, dphi[img*D + p, c] (null: the identity).
+struct EpiBwdPix {
+  const float* dphi;
+  float* out;
+  int R, N;
+  FastDiv fOD, fD;
+  __device__ __forceinline__ long long drow(int r) const {
+    const int img = (int)fOD.div(r), q = r - img * (int)fOD.d;
+    return (long long)img * fD.d + (q - (int)fD.div(q) * (int)fD.d);
+  }
+  template <class Cfg>
+  __device__ __forceinline__ void tile(f32x16 (&acc)[Cfg::FM][Cfg::FN], int m0, int n0) const {
+    if (!dphi) {
+      for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, float v) {
+        if (r < R && c < N) out[(long long)r * N + c] = v;
+      });
+      return;
+    }
+    float g[Cfg::FM][Cfg::FN][16];
+    gather_acc<Cfg>(g, m0, n0, [&](int r, int c) {
+      const int rc = min(r, R - 1), cc = min(c, N - 1);
+      return dphi[drow(rc) * N + cc];
+    });
+    for_each_acc_aux<Cfg>(acc, g, m0, n0, [&](int r, int c, float v, float d) {
+      if (r < R && c < N) out[(long long)r * N + c] = v * d;
+    });
+  }
+};
+
+template <class Cfg, bool VEC, bool DMA, class Epi = EpiBwd>
 __global__ void __launch_bounds__(Cfg::THREADS)
-k_dense_bwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, EpiBwd epi, int tiles_n) {
+k_dense_bwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, Epi epi, int tiles_n) {
   extern __shared__ float smem[];
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
@@ -223,6 +254,39 @@ static hipError_t dense_bwd_cfg(hipStream_t s, const float* G, const float* Wt, 
   if (e != hipSuccess) return e;
   k_dense_bwd<Cfg, VEC, DMA><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(la, lb, epi, tn);
   return hipGetLastError();
+}
+
+template <class Cfg, bool VEC, bool DMA = false>
+static hipError_t pw_bwd_cfg(hipStream_t s, const float* G, const float* Wt, const float* dphi, int R, int N,
+                             int K, int O, int D, float* out) {
+  using L = LoadKInnerT<VEC>;
+  L la{G, R, K, K};
+  L lb{Wt, N, K, K};
+  EpiBwdPix epi{dphi, out, R, N, FastDiv((uint32_t)(O * D)), FastDiv((uint32_t)D)};
+  const int tn = cdiv(N, Cfg::BN), tm = cdiv(R, Cfg::BM);
+  constexpr int bytes = DMA ? gemm_dma_smem_bytes<Cfg, 2>() : gemm_smem_bytes<Cfg, L, L>();
+  hipError_t e = hipFuncSetAttribute((const void*)k_dense_bwd<Cfg, VEC, DMA, EpiBwdPix>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e != hipSuccess) return e;
+  k_dense_bwd<Cfg, VEC, DMA, EpiBwdPix><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(la, lb, epi, tn);
+  return hipGetLastError();
+}
+
+hipError_t launch_pw_bwd(hipStream_t s, const float* G, const float* Wt, const float* dphi, int R, int N,
+                         int K, int O, int D, float* out) {
+  if ((long long)O * D >= (1LL << 31) || R <= 0) return R <= 0 ? hipSuccess : hipErrorInvalidValue;
+  const long long big_tiles = (long long)cdiv(R, 128) * cdiv(N, 128);
+  const bool v = vec_ok(G, K, K) && vec_ok(Wt, K, K);
+  // at most 64 output channels: 256x64 tiles (8 waves of 32x64), no half-empty 128-wide tile
+  if (N <= 64 && (long long)cdiv(R, 256) >= 512 && v && K % 32 == 0 && dma_span_ok(K, K, 256))
+    return pw_bwd_cfg<CfgPw, true, true>(s, G, Wt, dphi, R, N, K, O, D, out);
+  if (big_tiles >= 512) {
+    if (v && K % 32 == 0 && dma_span_ok(K, K, 256)) return pw_bwd_cfg<CfgBig8, true, true>(s, G, Wt, dphi, R, N, K, O, D, out);
+    return v ? pw_bwd_cfg<CfgBig8, true>(s, G, Wt, dphi, R, N, K, O, D, out)
+             : pw_bwd_cfg<CfgBig8, false>(s, G, Wt, dphi, R, N, K, O, D, out);
+  }
+  return v ? pw_bwd_cfg<CfgSmall, true>(s, G, Wt, dphi, R, N, K, O, D, out)
+           : pw_bwd_cfg<CfgSmall, false>(s, G, Wt, dphi, R, N, K, O, D, out);
 }
 
 // Two 8-wave workgroups share a compute unit (4 waves per SIMD).  At the depth-8 width-2048

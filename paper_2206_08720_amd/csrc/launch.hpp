@@ -49,6 +49,10 @@ hipError_t launch_dense_fwd(hipStream_t s, const float* h, const float* W, const
 // out[r, c] = (sum_k G[r, k] Wt[c, k]) * dphi[(r / O), c].  G [R, K], Wt [N, K], dphi [R/O, N].
 hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, const float* dphi,
                             int R, int N, int K, int O, float* out);
+// Pointwise (1x1) convolution backward: rows r = (img*O + o)*D + p of R cotangent pixels,
+// out[r, c] = (sum_k G[r, k] Wt[c, k]) * dphi[img*D + p, c]  (dphi null: the identity).
+hipError_t launch_pw_bwd(hipStream_t s, const float* G, const float* Wt, const float* dphi, int R, int N,
+                         int K, int O, int D, float* out);
 // G[m, o, c] = W[o, c] * dphi[m, c]   (cotangent of the last hidden pre-activation).
 hipError_t launch_bwd_seed(hipStream_t s, const float* W, const float* dphi, int M, int O, int C,
                            float* G);

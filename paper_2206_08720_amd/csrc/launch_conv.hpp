@@ -24,6 +24,9 @@ hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int
 // J[(s*O + o), off + c*9*Cin + k] = sum_p G[s, o, p, c] patch(h)[s, p, k] for every sample s.
 hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
                              int W, int C, int Cin, float* J, long long ldJ, long long off);
+// Pointwise (1x1) form: J[(s*O + o), off + c*Cin + ci] = sum_p G[s, o, p, c] h[s, p, ci].
+hipError_t launch_pw_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
+                           int W, int C, int Cin, float* J, long long ldJ, long long off);
 // Deterministic split-K product J1 J2^T: plan, partial products, reduction into theta.
 int splitk_tile();
 // splits * R1 * R2 <= part_capacity (floats) always holds for the returned plan.

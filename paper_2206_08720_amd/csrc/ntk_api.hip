@@ -150,7 +150,8 @@ struct ntk_handle {
   int rslot = 0;                  // parameter slot of the readout weight
   std::vector<size_t> off_ch;     // layer inputs h_l, l = 0..nc (nc: the GAP input) [Mmax, bh_l, bw_l, c_l]
   std::vector<size_t> off_cdphi;  // act'(z_l) of parametrised layers [Mmax, bh_{l+1}, bw_{l+1}, c_{l+1}]
-  std::vector<size_t> off_Kt;     // flipped kernels of the 3x3 convolutions l >= 1 [c_l, 9, c_{l+1}]
+  std::vector<size_t> off_Kt;     // flipped 3x3 kernels [c_l, 9, c_{l+1}] and transposed pointwise
+                                  // weights [c_l, c_{l+1}] of the layers l >= 1
   std::vector<long long> joff;    // first column of layer l's weight block (then its bias) in J when
                                   // every layer is outside-in (the NTK-vector product's layout)
   long long Ktot = 0;             // columns of J at most: every weight and bias column
@@ -174,7 +175,8 @@ static int hip_fail(ntk_handle* h, hipError_t e, const char* what) {
 
 // ------------------------------------------------------------------------------ validation
 static bool is_spatial_kind(int k) {
-  return k == NTK_CONV3X3_SAME || k == NTK_DWCONV3X3_SAME || k == NTK_SCALE || k == NTK_AVGPOOL2;
+  return k == NTK_CONV3X3_SAME || k == NTK_CONV1X1 || k == NTK_DWCONV3X3_SAME || k == NTK_SCALE ||
+         k == NTK_AVGPOOL2;
 }
 
 static int validate(const ntk_model_desc* m, ntk_handle* tmp) {
@@ -212,7 +214,7 @@ static int validate(const ntk_model_desc* m, ntk_handle* tmp) {
     tmp->cnn = false;
     return NTK_OK;
   }
-  // CNN: spatial layers (3x3 or depthwise 3x3 convolutions, scale layers, 2x2 average pools),
+  // CNN: spatial layers (3x3, pointwise or depthwise 3x3 convolutions, scale layers, 2x2 pools),
   // then gap, then a dense readout
   int i = 0;
   if (m->in_h <= 0 || m->in_w <= 0 || m->in_c <= 0) return fail(nullptr, NTK_E_SHAPE, "bad input shape");
@@ -229,7 +231,7 @@ static int validate(const ntk_model_desc* m, ntk_handle* tmp) {
       ww /= 2;
     } else {
       if (L.in != c) return fail(nullptr, NTK_E_SHAPE, at + "in != previous channels");
-      if (L.kind != NTK_CONV3X3_SAME && L.out != L.in)
+      if ((L.kind == NTK_DWCONV3X3_SAME || L.kind == NTK_SCALE) && L.out != L.in)
         return fail(nullptr, NTK_E_SHAPE, at + "depthwise and scale layers keep the channel count (out == in)");
       c = L.out;
       any_param = true;
@@ -300,10 +302,11 @@ static void plan_fcn(ntk_handle* h) {
 }
 
 // Columns of a spatial layer's weight block in J: 9 Cin Cout (3x3 convolution, outside-in),
-// 9 C (depthwise), C (scale), 0 (pool).
+// Cin Cout (pointwise), 9 C (depthwise), C (scale), 0 (pool).
 static long long weight_cols(const ntk_layer_desc& L, int cin) {
   switch (L.kind) {
     case NTK_CONV3X3_SAME: return 9LL * cin * L.out;
+    case NTK_CONV1X1: return (long long)cin * L.out;
     case NTK_DWCONV3X3_SAME: return 9LL * L.out;
     case NTK_SCALE: return L.out;
     default: return 0;
@@ -356,8 +359,9 @@ static void plan_cnn(ntk_handle* h) {
   for (int l = 0; l <= nc; ++l) h->off_ch[l] = take(Mmax * plane(l));
   for (int l = 0; l < nc; ++l)
     if (h->wslot[l] >= 0) h->off_cdphi[l] = take(Mmax * plane(l + 1));
-  for (int l = 1; l < nc; ++l)
-    if (h->layers[l].kind == NTK_CONV3X3_SAME) h->off_Kt[l] = take((size_t)9 * h->ch[l] * h->ch[l + 1]);
+  for (int l = 1; l < nc; ++l)   // flipped 3x3 kernels, transposed pointwise weights
+    if (h->layers[l].kind == NTK_CONV3X3_SAME || h->layers[l].kind == NTK_CONV1X1)
+      h->off_Kt[l] = take((size_t)(h->layers[l].kind == NTK_CONV1X1 ? 1 : 9) * h->ch[l] * h->ch[l + 1]);
   h->off_g = take(Mmax * h->ch[nc]);
   h->off_Gping = take(Mmax * O * gmax);
   h->off_Gpong = take(Mmax * O * gmax);
@@ -812,6 +816,10 @@ static int cnn_forward(ntk_handle* h, const float* const* params, const float* X
       prof_begin(P, s, KC_CONV_FWD);
       e = launch_conv_fwd(s, x, M, Hl, Wl, C, w, L.out, L.act, b, out, dphi);
       prof_end(P, s, KC_CONV_FWD);
+    } else if (L.kind == NTK_CONV1X1) {   // a dense layer at every pixel
+      prof_begin(P, s, KC_CONV_FWD);
+      e = launch_dense_fwd(s, x, w, b, M * Hl * Wl, L.out, C, L.act, out, dphi, nullptr, 0);
+      prof_end(P, s, KC_CONV_FWD);
     } else {
       prof_begin(P, s, KC_STRUCT_FWD);
       if (L.kind == NTK_DWCONV3X3_SAME)
@@ -920,11 +928,14 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   // 2. cotangents of every spatial layer's output for all O outputs, and per layer its
   //    weight-space cotangent columns of J (or its inside-out summand)
   for (int l = 1; l < nc; ++l) {
-    if (h->layers[l].kind != NTK_CONV3X3_SAME) continue;
+    const int kind = h->layers[l].kind;
+    if (kind != NTK_CONV3X3_SAME && kind != NTK_CONV1X1) continue;
     prof_begin(P, s, KC_TRANSPOSE);
-    e = launch_conv_flip(s, params[h->wslot[l]], h->ch[l + 1], h->ch[l], F(h->off_Kt[l]));
+    e = kind == NTK_CONV3X3_SAME
+            ? launch_conv_flip(s, params[h->wslot[l]], h->ch[l + 1], h->ch[l], F(h->off_Kt[l]))
+            : launch_transpose(s, params[h->wslot[l]], h->ch[l + 1], h->ch[l], F(h->off_Kt[l]));
     prof_end(P, s, KC_TRANSPOSE);
-    if (e != hipSuccess) return hip_fail(h, e, "kernel flip");
+    if (e != hipSuccess) return hip_fail(h, e, "kernel flip / transpose");
   }
   float* Gcur = F(h->off_Gping);
   float* Gnext = F(h->off_Gpong);
@@ -968,6 +979,16 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
         prof_end(P, s, KC_STRUCT_WGRAD);
         if (e != hipSuccess) return hip_fail(h, e, "conv bias cotangent");
       }
+    } else if (L.kind == NTK_CONV1X1) {
+      prof_begin(P, s, KC_CONV_WGRAD);
+      e = launch_pw_wgrad(s, Gcur, hptr(l), M, Oe, Hl, Wl, cout, cin, J, Kcall, jw[l]);
+      prof_end(P, s, KC_CONV_WGRAD);
+      if (e == hipSuccess && L.has_bias) {
+        prof_begin(P, s, KC_STRUCT_WGRAD);
+        e = launch_pix_wgrad(s, Gcur, nullptr, M, Oe, Hl, Wl, cout, 0, 1, J, Kcall, 0, jb[l], nullptr, 0);
+        prof_end(P, s, KC_STRUCT_WGRAD);
+      }
+      if (e != hipSuccess) return hip_fail(h, e, "pointwise weight-space cotangent");
     } else if (L.kind != NTK_AVGPOOL2) {
       prof_begin(P, s, KC_STRUCT_WGRAD);
       e = launch_pix_wgrad(s, Gcur, hptr(l), M, Oe, Hl, Wl, cout, L.kind == NTK_DWCONV3X3_SAME ? 9 : 1,
@@ -981,6 +1002,10 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
       if (L.kind == NTK_CONV3X3_SAME) {
         prof_begin(P, s, KC_CONV_BWD);
         e = launch_conv_bwd(s, Gcur, M, Oe, Hl, Wl, cout, F(h->off_Kt[l]), cin, dprev, Gnext);
+        prof_end(P, s, KC_CONV_BWD);
+      } else if (L.kind == NTK_CONV1X1) {
+        prof_begin(P, s, KC_CONV_BWD);
+        e = launch_pw_bwd(s, Gcur, F(h->off_Kt[l]), dprev, M * Oe * Hl * Wl, cin, cout, Oe, Hl * Wl, Gnext);
         prof_end(P, s, KC_CONV_BWD);
       } else {
         prof_begin(P, s, KC_STRUCT_BWD);
@@ -1299,9 +1324,10 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
     const float* hl = hptr(l) + r2 * plane(l);
     const float* w = h->wslot[l] >= 0 ? params[h->wslot[l]] : nullptr;
     const long long jw = h->joff[l], jb = jw + weight_cols(L, cin);
-    if (L.kind == NTK_CONV3X3_SAME) {
+    if (L.kind == NTK_CONV3X3_SAME || L.kind == NTK_CONV1X1) {
       prof_begin(P, s, KC_CONV_WGRAD);
-      e = launch_conv_wgrad(s, Gcur, hl, n2, 1, Hl, Wl, cout, cin, J, h->Ktot, jw);
+      e = L.kind == NTK_CONV3X3_SAME ? launch_conv_wgrad(s, Gcur, hl, n2, 1, Hl, Wl, cout, cin, J, h->Ktot, jw)
+                                     : launch_pw_wgrad(s, Gcur, hl, n2, 1, Hl, Wl, cout, cin, J, h->Ktot, jw);
       prof_end(P, s, KC_CONV_WGRAD);
       if (e == hipSuccess && L.has_bias) {
         prof_begin(P, s, KC_STRUCT_WGRAD);
@@ -1317,13 +1343,15 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
     if (e != hipSuccess) return hip_fail(h, e, "VJP weight cotangent");
     if (l >= 1) {
       const float* dprev = h->wslot[l - 1] >= 0 ? F(h->off_cdphi[l - 1]) + r2 * plane(l) : nullptr;
-      if (L.kind == NTK_CONV3X3_SAME) {
+      if (L.kind == NTK_CONV3X3_SAME || L.kind == NTK_CONV1X1) {
+        const bool c3 = L.kind == NTK_CONV3X3_SAME;
         prof_begin(P, s, KC_TRANSPOSE);
-        e = launch_conv_flip(s, w, cout, cin, F(h->off_Kt[l]));
+        e = c3 ? launch_conv_flip(s, w, cout, cin, F(h->off_Kt[l])) : launch_transpose(s, w, cout, cin, F(h->off_Kt[l]));
         prof_end(P, s, KC_TRANSPOSE);
-        if (e != hipSuccess) return hip_fail(h, e, "kernel flip");
+        if (e != hipSuccess) return hip_fail(h, e, "kernel flip / transpose");
         prof_begin(P, s, KC_CONV_BWD);
-        e = launch_conv_bwd(s, Gcur, n2, 1, Hl, Wl, cout, F(h->off_Kt[l]), cin, dprev, Gnext);
+        e = c3 ? launch_conv_bwd(s, Gcur, n2, 1, Hl, Wl, cout, F(h->off_Kt[l]), cin, dprev, Gnext)
+               : launch_pw_bwd(s, Gcur, F(h->off_Kt[l]), dprev, n2 * Hl * Wl, cin, cout, 1, Hl * Wl, Gnext);
         prof_end(P, s, KC_CONV_BWD);
       } else {
         prof_begin(P, s, KC_STRUCT_BWD);
@@ -1373,6 +1401,13 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
       e = launch_conv_fwd(s, hl, n1, Hl, Wl, cin, tw, cout, NTK_ACT_NONE, nullptr, cb, cd);
       if (e == hipSuccess && !tzero)
         e = launch_conv_fwd(s, tcur, n1, Hl, Wl, cin, w, cout, NTK_ACT_NONE, nullptr, ca, cd);
+      prof_end(P, s, KC_CONV_FWD);
+    } else if (L.kind == NTK_CONV1X1) {
+      const int rows = n1 * Hl * Wl;
+      prof_begin(P, s, KC_CONV_FWD);
+      e = launch_dense_fwd(s, hl, tw, nullptr, rows, cout, cin, NTK_ACT_NONE, cb, cd, nullptr, 0);
+      if (e == hipSuccess && !tzero)
+        e = launch_dense_fwd(s, tcur, w, nullptr, rows, cout, cin, NTK_ACT_NONE, ca, cd, nullptr, 0);
       prof_end(P, s, KC_CONV_FWD);
     } else {
       prof_begin(P, s, KC_STRUCT_FWD);

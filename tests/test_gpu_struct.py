@@ -73,6 +73,20 @@ CASES = [
     ("32 channels (direct-to-LDS conv loads) with biases, ragged rows",
      _spec("s11", (6, 6), 3, [("conv3x3", 32, "relu", True), ("dwconv3x3", "relu", True),
                               ("avgpool2",), ("conv3x3", 32, "relu", True)], 10), 23, 17),
+    # pointwise (1x1) convolutions: depthwise-separable blocks
+    ("separable block, 32 channels (direct-to-LDS pointwise product)",
+     _spec("s12", (8, 8), 3, [("conv3x3", 32, "relu", True), ("dwconv3x3", "relu", True),
+                              ("conv1x1", 64, "relu", True), ("avgpool2",), ("dwconv3x3", "erf", False),
+                              ("conv1x1", 32, "erf", True)], 10), 9, 7),
+    ("pointwise first, 3 and 6 channels (register-staged loaders)",
+     _spec("s13", (5, 7), 3, [("conv1x1", 6, "erf", True), ("dwconv3x3", "relu", False),
+                              ("conv1x1", 5, "relu", True)], 4), 5, 6),
+    ("pointwise on 1x1 images (an MLP with biases)",
+     _spec("s14", (1, 1), 12, [("conv1x1", 40, "erf", True), ("scale", "relu", True),
+                               ("conv1x1", 24, "relu", True)], 5), 13, 11),
+    ("pointwise after a pool, last layer without activation",
+     _spec("s15", (4, 4), 8, [("dwconv3x3", "relu", True), ("avgpool2",), ("conv1x1", 16, "none", True)], 3),
+     4, 3),
 ]
 
 
@@ -98,6 +112,36 @@ def test_struct_conv_orders_and_method(order):
             "inside_out": {_lib.NTK_OPT_CONV_ORDER: _lib.NTK_CONV_ORDER_INSIDE_OUT},
             "jacobian": {_lib.NTK_OPT_METHOD: _lib.NTK_METHOD_JACOBIAN}}[order]
     _vs_jc(f"struct model, {order}", ORDER_SPEC, params, X1, X2, options=opts)
+
+
+SEP_SPEC = _spec("sep", (8, 8), 4, [("conv1x1", 16, "relu", True), ("dwconv3x3", "relu", True),
+                                   ("avgpool2",), ("conv1x1", 12, "erf", True), ("conv3x3", 8, "relu", False)], 5)
+
+
+@pytest.mark.parametrize("mode", ["jacobian", "trace", "logit-diagonal", "aliased"])
+def test_pointwise_model_modes(mode):
+    from paper_2206_08720_amd import _lib
+    params, X1, X2 = _data(SEP_SPEC, 7, 6, 661)
+    if mode == "jacobian":
+        _vs_jc("separable, Jacobian contraction", SEP_SPEC, params, X1, X2,
+               options={_lib.NTK_OPT_METHOD: _lib.NTK_METHOD_JACOBIAN})
+        return
+    if mode == "aliased":
+        got = _vs_jc("separable, aliased", SEP_SPEC, params, X1, X1)
+        N, O = got.shape[0], got.shape[2]
+        M = got.transpose(0, 2, 1, 3).reshape(N * O, N * O)
+        np.testing.assert_allclose(M, M.T, rtol=0, atol=1e-5 * np.abs(M).max())
+        return
+    output, batch = ("trace", "full") if mode == "trace" else ("logit", "diagonal")
+    X2 = X2 if batch == "full" else wl.make_inputs(SEP_SPEC, 7, 662)
+    full, d1, d2 = oracle.ntk_jc_with_norms(SEP_SPEC, params, X1, X2, layer_storage=S)
+    got = gpu_ntk(SEP_SPEC, params, X1, X2, variant=(output, batch, 3))
+    ref = variant_of(full, output, batch, 3)
+    scale = variant_scale(d1, d2, output, batch, 3)
+    assert got.shape == ref.shape
+    cs, nw = scaled_errors(got, ref, scale)
+    report(f"separable {output}/{batch}", cs, nw)
+    assert cs <= TOL and nw <= TOL
 
 
 @pytest.mark.parametrize("symmetric", [True, False])

@@ -49,6 +49,9 @@ CASES = [
     ("cnn pool first, 6 channels (scalar lanes), last layer a pool", wl.cnn_layers_spec(
         "p9", (4, 8), 6, [("avgpool2",), ("scale", "erf", False), ("dwconv3x3", "relu", False),
                           ("avgpool2",)], 3), 5, 6),
+    ("cnn separable blocks with pointwise convolutions", wl.cnn_layers_spec(
+        "p10", (6, 6), 3, [("conv1x1", 32, "relu", True), ("dwconv3x3", "erf", True),
+                           ("conv1x1", 16, "erf", False), ("avgpool2",), ("conv1x1", 5, "relu", True)], 4), 6, 5),
 ]
 
 

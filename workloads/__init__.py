@@ -206,13 +206,15 @@ WORKLOADS = {
         n1=64, n2=64, weight_var="2/fan_in", x_dist="normal", x2_is_x1=False),
     # The further structure rules of the paper's appendix on structured derivatives, one
     # layer kind each: convolution biases (output block-tiled), a depthwise convolution
-    # (block-diagonal), a per-channel scale with bias (block-diagonal over channels and
-    # output block-tiled over pixels), and a 2x2 average pool between convolutions.
+    # (block-diagonal) followed by a pointwise one (a depthwise-separable block), a
+    # per-channel scale with bias (block-diagonal over channels and output block-tiled over
+    # pixels), and a 2x2 average pool between convolutions.
     "cnn_struct_c64_32x32": dict(
         index=6, spec=cnn_layers_spec(
             "cnn_struct_c64_32x32", (32, 32), 3,
-            [("conv3x3", 64, "relu", True), ("dwconv3x3", "relu", True), ("avgpool2",),
-             ("conv3x3", 64, "relu", True), ("scale", "relu", True), ("conv3x3", 64, "relu", True)],
+            [("conv3x3", 64, "relu", True), ("dwconv3x3", "relu", True), ("conv1x1", 64, "relu", True),
+             ("avgpool2",), ("conv3x3", 64, "relu", True), ("scale", "relu", True),
+             ("conv3x3", 64, "relu", True)],
             10),
         n1=64, n2=64, weight_var="2/fan_in", bias_var=0.01, x_dist="normal", x2_is_x1=False),
 }
