@@ -408,7 +408,7 @@ k_pix_wgrad(const float* __restrict__ G, const float* __restrict__ x, int rows, 
 // divisor of O, so that passes carry few unused rows).  The four waves' sums are added in a fixed
 // order through LDS; with several bands, each band writes its sums to `part` ([band][row][10 C],
 // bias last) and k_band_reduce adds the bands in order.
-template <int kDwOB, bool BIAS>
+template <int OB, bool BIAS>
 __global__ void __launch_bounds__(256)
 k_dw_wgrad(const float* __restrict__ G, const float* __restrict__ x, int images, int O, int H, int W,
            FastDiv fW, int C, int bands, int cgroups, float* __restrict__ out, long long ld_out,
@@ -426,10 +426,10 @@ k_dw_wgrad(const float* __restrict__ G, const float* __restrict__ x, int images,
     const int cc = min(cgi * 64 + lane, C - 1);   // lanes past C load a valid channel, unused
     const int p0 = band * per_band, p1 = min(D, p0 + per_band);
     const float* xi = x + (long long)n * img_elems;
-    for (int o0 = 0; o0 < O; o0 += kDwOB) {
-      float acc[kDwOB][NA];
+    for (int o0 = 0; o0 < O; o0 += OB) {
+      float acc[OB][NA];
 #pragma unroll
-      for (int i = 0; i < kDwOB; ++i)
+      for (int i = 0; i < OB; ++i)
 #pragma unroll
         for (int a = 0; a < NA; ++a) acc[i][a] = 0.f;
       for (int p = p0 + wave; p < p1; p += 4) {
@@ -437,7 +437,7 @@ k_dw_wgrad(const float* __restrict__ G, const float* __restrict__ x, int images,
         // every load reads a valid address (clamped pixel, clamped row) and is issued without a
         // branch, so the 17 loads of a pixel are in flight together; rows past O accumulate
         // sums that are never stored
-        float xt[9], g[kDwOB];
+        float xt[9], g[OB];
 #pragma unroll
         for (int t = 0; t < 9; ++t) {
           const int sy = yy + t / 3 - 1, sx = xx + t % 3 - 1;
@@ -447,10 +447,10 @@ k_dw_wgrad(const float* __restrict__ G, const float* __restrict__ x, int images,
           xt[t] = ok ? v : 0.f;
         }
 #pragma unroll
-        for (int i = 0; i < kDwOB; ++i)
+        for (int i = 0; i < OB; ++i)
           g[i] = G[((long long)n * O + min(o0 + i, O - 1)) * img_elems + (long long)p * C + cc];
 #pragma unroll
-        for (int i = 0; i < kDwOB; ++i) {
+        for (int i = 0; i < OB; ++i) {
 #pragma unroll
           for (int t = 0; t < 9; ++t) acc[i][t] += g[i] * xt[t];
           if constexpr (BIAS) acc[i][9] += g[i];
@@ -459,7 +459,7 @@ k_dw_wgrad(const float* __restrict__ G, const float* __restrict__ x, int images,
       // rows o0 + i < O only (uniform over the workgroup); fully unrolled so that acc[i] stays in
       // registers
 #pragma unroll
-      for (int i = 0; i < kDwOB; ++i) {
+      for (int i = 0; i < OB; ++i) {
         if (o0 + i < O) {
           __syncthreads();   // the previous row's sums have been read
 #pragma unroll
