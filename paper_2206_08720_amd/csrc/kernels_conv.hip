@@ -1092,7 +1092,8 @@ namespace ntk {
 // ------------------------------------------------------------------------------ inside-out order
 // For one input pair (n1, n2) = blockIdx.x and every conv layer marked inside-out:
 //   PK[p1, p2] = patch1[p1] . patch2[p2]   (the inner Jacobian product; built from the pixel
-//                Gram H[q1, q2] = h1[q1] . h2[q2] summed over the 9 taps shifted together)
+//                Gram H[q1, q2] = h1[q1] . h2[q2] summed over the 9 taps shifted together; for a
+//                pointwise layer the patch is the pixel itself and PK = H)
 //   T[c, p2]   = sum_p1 G1[o1, p1, c] PK[p1, p2]                      (one o1 at a time)
 //   theta[o1, o2] += sum_{p2, c} T[c, p2] G2[o2, p2, c]
 // which is the inside-out contraction order of the constant-block-diagonal MJJMP with
@@ -1105,6 +1106,7 @@ struct PairLayer {
   const float* h;    // layer input of the stacked batch, [M, D, Cin]
   const float* G;    // cotangent of the layer output, [M*O, D, C]
   int Cin, C;
+  int taps;          // 9 (3x3 convolution) or 1 (pointwise)
 };
 struct PairArgs {
   PairLayer layer[kMaxLayers];
@@ -1141,6 +1143,10 @@ k_conv_pairsum(PairArgs a, int n1, int n2, int n2_offset, int O, int H, int W,
     __syncthreads();
     // patch-pair Gram: both patches use the same tap, so the shifted pixel pairs are summed
     for (int q = t; q < D * D; q += 256) {
+      if (L.taps == 1) {
+        PK[q] = Hs[q];
+        continue;
+      }
       const int p1 = q / D, p2 = q - p1 * D;
       const int y1 = p1 / W, x1 = p1 - y1 * W, y2 = p2 / W, x2 = p2 - y2 * W;
       float acc = 0.f;
@@ -1226,6 +1232,7 @@ hipError_t launch_conv_pairsum(hipStream_t s, const PairLayerList& layers, int n
     a.layer[i].G = layers.G[i];
     a.layer[i].Cin = layers.Cin[i];
     a.layer[i].C = layers.C[i];
+    a.layer[i].taps = layers.taps[i];
   }
   const int bytes = (256 * kPairOB + 2 * kPairDMax * kPairDMax + kPairCC * kPairDMax +
                      kPairOMax * kPairOMax) * 4;

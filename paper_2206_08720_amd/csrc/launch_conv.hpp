@@ -40,13 +40,14 @@ hipError_t launch_ntk_reduce(hipStream_t s, const float* part, int splits, int N
                              int symmetric, const float* w, const float* gram, float rscale,
                              int accumulate, float* theta);
 
-// Inside-out order for the conv layers listed (see k_conv_pairsum).  The G pointers must stay
+// Inside-out order for the 3x3 or pointwise conv layers listed (see k_conv_pairsum).  The G pointers must stay
 // valid until the kernel runs, so every listed layer's cotangent must still be resident.
 struct PairLayerList {
   const float* h[kMaxLayers];
   const float* G[kMaxLayers];
   int Cin[kMaxLayers];
   int C[kMaxLayers];
+  int taps[kMaxLayers];   // 9: 3x3 convolution, 1: pointwise
   int count;
 };
 int pairsum_supported(int D, int O);

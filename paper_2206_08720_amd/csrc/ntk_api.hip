@@ -855,20 +855,22 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   const int Oe = logit ? 1 : O;
   const double pairs = diag ? (double)n1 : (double)n1 * n2;
   const double Oc = trace ? (double)O : (double)Oe * Oe;   // output pairs per input pair
-  // contraction order of each 3x3 convolution: the cost model of the appendix "CNN NTK
-  // Complexity" (outside-in N1 N2 O^2 F Cin Cout plus forming J, N O D F Cin Cout per sample,
-  // against inside-out N1 N2 (D^2 F Cin + O D^2 Cout + O^2 D Cout)), or the forced option.
-  // Depthwise and scale layers (block-diagonal weight-space Jacobians, 9 C and C columns) and
-  // every bias (output block-tiled, C columns) always contract outside-in: their O^2 P term is
-  // the smallest of the orders there.
+  // contraction order of each 3x3 (F = 9 taps) or pointwise (F = 1) convolution: the cost model
+  // of the appendix "CNN NTK Complexity" (outside-in N1 N2 O^2 F Cin Cout plus forming J,
+  // N O D F Cin Cout per sample, against inside-out N1 N2 (D^2 F Cin + O D^2 Cout + O^2 D Cout)),
+  // or the forced option.  Depthwise and scale layers (block-diagonal weight-space Jacobians,
+  // 9 C and C columns) and every bias (output block-tiled, C columns) always contract
+  // outside-in: their O^2 P term is the smallest of the orders there.
   std::vector<char> inside(nc, 0);
   for (int l = 0; l < nc; ++l) {
-    if (h->layers[l].kind != NTK_CONV3X3_SAME || h->opt_method == NTK_METHOD_JACOBIAN) continue;
+    const int kind = h->layers[l].kind;
+    if ((kind != NTK_CONV3X3_SAME && kind != NTK_CONV1X1) || h->opt_method == NTK_METHOD_JACOBIAN) continue;
+    const double F = kind == NTK_CONV1X1 ? 1 : 9;
     const double Dl = (double)h->bh[l] * h->bw[l];
     const bool io_ok = pairsum_supported(h->bh[l] * h->bw[l], Oe) != 0;
     const double Cin = h->ch[l], Co = h->ch[l + 1];
-    const double oi = pairs * Oc * 9 * Cin * Co + (double)M * Oe * Dl * 9 * Cin * Co;
-    const double io = pairs * (Dl * Dl * 9 * Cin + (double)Oe * Dl * Dl * Co + Oc * Dl * Co);
+    const double oi = pairs * Oc * F * Cin * Co + (double)M * Oe * Dl * F * Cin * Co;
+    const double io = pairs * (Dl * Dl * F * Cin + (double)Oe * Dl * Dl * Co + Oc * Dl * Co);
     if (h->opt_conv_order == NTK_CONV_ORDER_INSIDE_OUT) {
       if (!io_ok) return fail(h, NTK_E_UNSUPPORTED, "the inside-out order needs D <= 64 pixels and O <= 64");
       inside[l] = 1;
@@ -883,7 +885,7 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   for (int l = 0; l < nc; ++l) {
     const ntk_layer_desc& L = h->layers[l];
     if (L.kind == NTK_AVGPOOL2) continue;
-    if (!(L.kind == NTK_CONV3X3_SAME && inside[l])) {
+    if (!inside[l]) {
       jw[l] = Kcall;
       Kcall += weight_cols(L, h->ch[l]);
     }
@@ -961,6 +963,7 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
         pl.G[0] = Gcur;
         pl.Cin[0] = cin;
         pl.C[0] = cout;
+        pl.taps[0] = 9;
         prof_begin(P, s, KC_CONV_PAIRSUM);
         e = launch_conv_pairsum(s, pl, n1, n2, n2_off, Oe, Hl, Wl, F(h->off_gram_r), theta_written ? 1 : 0,
                                 trace ? 1 : 0, diag ? 1 : 0, theta);
@@ -980,9 +983,24 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
         if (e != hipSuccess) return hip_fail(h, e, "conv bias cotangent");
       }
     } else if (L.kind == NTK_CONV1X1) {
-      prof_begin(P, s, KC_CONV_WGRAD);
-      e = launch_pw_wgrad(s, Gcur, hptr(l), M, Oe, Hl, Wl, cout, cin, J, Kcall, jw[l]);
-      prof_end(P, s, KC_CONV_WGRAD);
+      if (inside[l]) {
+        PairLayerList pl{};
+        pl.count = 1;
+        pl.h[0] = hptr(l);
+        pl.G[0] = Gcur;
+        pl.Cin[0] = cin;
+        pl.C[0] = cout;
+        pl.taps[0] = 1;
+        prof_begin(P, s, KC_CONV_PAIRSUM);
+        e = launch_conv_pairsum(s, pl, n1, n2, n2_off, Oe, Hl, Wl, F(h->off_gram_r), theta_written ? 1 : 0,
+                                trace ? 1 : 0, diag ? 1 : 0, theta);
+        prof_end(P, s, KC_CONV_PAIRSUM);
+        theta_written = true;
+      } else {
+        prof_begin(P, s, KC_CONV_WGRAD);
+        e = launch_pw_wgrad(s, Gcur, hptr(l), M, Oe, Hl, Wl, cout, cin, J, Kcall, jw[l]);
+        prof_end(P, s, KC_CONV_WGRAD);
+      }
       if (e == hipSuccess && L.has_bias) {
         prof_begin(P, s, KC_STRUCT_WGRAD);
         e = launch_pix_wgrad(s, Gcur, nullptr, M, Oe, Hl, Wl, cout, 0, 1, J, Kcall, 0, jb[l], nullptr, 0);

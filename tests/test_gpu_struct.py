@@ -118,13 +118,15 @@ SEP_SPEC = _spec("sep", (8, 8), 4, [("conv1x1", 16, "relu", True), ("dwconv3x3",
                                    ("avgpool2",), ("conv1x1", 12, "erf", True), ("conv3x3", 8, "relu", False)], 5)
 
 
-@pytest.mark.parametrize("mode", ["jacobian", "trace", "logit-diagonal", "aliased"])
+@pytest.mark.parametrize("mode", ["jacobian", "inside_out", "outside_in", "trace", "logit-diagonal", "aliased"])
 def test_pointwise_model_modes(mode):
     from paper_2206_08720_amd import _lib
     params, X1, X2 = _data(SEP_SPEC, 7, 6, 661)
-    if mode == "jacobian":
-        _vs_jc("separable, Jacobian contraction", SEP_SPEC, params, X1, X2,
-               options={_lib.NTK_OPT_METHOD: _lib.NTK_METHOD_JACOBIAN})
+    if mode in ("jacobian", "inside_out", "outside_in"):
+        opts = {"jacobian": {_lib.NTK_OPT_METHOD: _lib.NTK_METHOD_JACOBIAN},
+                "inside_out": {_lib.NTK_OPT_CONV_ORDER: _lib.NTK_CONV_ORDER_INSIDE_OUT},
+                "outside_in": {_lib.NTK_OPT_CONV_ORDER: _lib.NTK_CONV_ORDER_OUTSIDE_IN}}[mode]
+        _vs_jc(f"separable, {mode}", SEP_SPEC, params, X1, X2, options=opts)
         return
     if mode == "aliased":
         got = _vs_jc("separable, aliased", SEP_SPEC, params, X1, X1)
