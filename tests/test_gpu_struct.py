@@ -210,3 +210,20 @@ def test_hand_worked_struct_golden_on_gpu(golden_dir, symmetric):
     X = np.array(d["X"], dtype=np.float32)
     got = gpu_ntk(d["spec"], params, X, X, symmetric=symmetric)
     np.testing.assert_allclose(got, np.array(d["theta"]), rtol=1e-6, atol=1e-5)
+
+
+LARGE_CASES = [
+    ("128x128 images, 16384-pixel planes",
+     _spec("l1", (128, 128), 4, [("conv3x3", 8, "relu", True), ("dwconv3x3", "erf", True), ("avgpool2",),
+                                 ("conv1x1", 4, "relu", True), ("scale", "erf", True)], 3), 2, 3),
+    ("2048 channels: 32 channel groups of 64 in the depthwise columns, wide pointwise columns",
+     _spec("l2", (2, 2), 2048, [("dwconv3x3", "relu", True), ("scale", "erf", True), ("conv1x1", 8, "relu", True)], 3),
+     3, 2),
+]
+
+
+@pytest.mark.parametrize("case", LARGE_CASES, ids=[c[0] for c in LARGE_CASES])
+def test_struct_large_sizes(case):
+    label, spec, n1, n2 = case
+    params, X1, X2 = _data(spec, n1, n2, 700 + n1 * 5 + n2)
+    _vs_jc(label, spec, params, X1, X2)
