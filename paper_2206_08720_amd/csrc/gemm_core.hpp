@@ -421,6 +421,15 @@ __host__ inline bool vec_ok(const void* p, long long ld, long long K) {
 }
 
 // ------------------------------------------------------------------------------ misc
+// Element at a 32-bit byte offset from a base pointer.  With a wave-uniform base this is the
+// scalar-base + 32-bit vector-offset addressing form, one instruction per access with no
+// 64-bit address arithmetic.  The caller keeps `bytes` below 4 GiB.
+__device__ __forceinline__ float& at_bytes(float* base, uint32_t bytes) {
+  return *reinterpret_cast<float*>(reinterpret_cast<char*>(base) + bytes);
+}
+__device__ __forceinline__ const float& at_bytes(const float* base, uint32_t bytes) {
+  return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(base) + bytes);
+}
 __device__ __forceinline__ float act_fwd(int act, float z) {
   if (act == 1) return z > 0.f ? z : 0.f;
   if (act == 2) return erff(z);

@@ -657,6 +657,105 @@ hipError_t launch_conv_flip(hipStream_t s, const float* K, int Cout, int Cin, fl
 }
 
 // ------------------------------------------------------------------------------ backward
+// Row arithmetic of the epilogues below, per 32-row MFMA fragment: lane l holds rows
+// r0 + 8*(v/4) + 4*(l/32) + v%4 (v = 0..15) of column l%32 of the fragment.
+__device__ __forceinline__ int frag_row(int v, int lane) { return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3); }
+
+// Epilogue of the transposed convolution: out[r, c] = acc[r, c] * dphi[img*D + p, c] for rows
+// r = (img*O + o)*D + p (null dphi: the identity).  A fragment that lies inside R and inside
+// one cotangent image (no multiple of D in (r0, r0 + 31]) maps to 32 consecutive rows of dphi,
+// so its row arithmetic is done once and an element costs an offset, a load, a multiply and a
+// store; other fragments take the per-element form.
+template <class Cfg>
+__device__ __forceinline__ void conv_bwd_store(f32x16 (&acc)[Cfg::FM][Cfg::FN], int m0, int n0,
+                                               const float* __restrict__ dphi, float* __restrict__ out, int R,
+                                               int N, FastDiv fOD, FastDiv fD) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
+  const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
+  const int D = (int)fD.d;
+#pragma unroll
+  for (int fm = 0; fm < Cfg::FM; ++fm) {
+    const int r0 = __builtin_amdgcn_readfirstlane(m0 + wm0 + fm * 32);
+    if (r0 >= R) continue;
+    const int t0 = (int)fD.div(r0);
+    if (r0 + 32 <= R && (int)fD.div(r0 + 31) == t0) {
+      const int img = (int)fOD.div(r0);
+      float* ob = out + (long long)r0 * N;
+      const float* db = dphi ? dphi + ((long long)img * D + (r0 - t0 * D)) * N : nullptr;
+#pragma unroll
+      for (int fn = 0; fn < Cfg::FN; ++fn) {
+        const int c = n0 + wn0 + fn * 32 + (lane & 31);
+        if (c >= N) continue;
+        if (db) {
+          float d[16];
+#pragma unroll
+          for (int v = 0; v < 16; ++v) d[v] = at_bytes(db, (uint32_t)(frag_row(v, lane) * N + c) * 4u);
+#pragma unroll
+          for (int v = 0; v < 16; ++v) at_bytes(ob, (uint32_t)(frag_row(v, lane) * N + c) * 4u) = acc[fm][fn][v] * d[v];
+        } else {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) at_bytes(ob, (uint32_t)(frag_row(v, lane) * N + c) * 4u) = acc[fm][fn][v];
+        }
+      }
+    } else {
+#pragma unroll
+      for (int fn = 0; fn < Cfg::FN; ++fn)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = r0 + frag_row(v, lane), c = n0 + wn0 + fn * 32 + (lane & 31);
+          if (r < R && c < N) {
+            const int img = (int)fOD.div(r);
+            const int p = r - (int)fD.div(r) * D;
+            const float d = dphi ? dphi[((long long)img * D + p) * N + c] : 1.f;
+            out[(long long)r * N + c] = acc[fm][fn][v] * d;
+          }
+        }
+    }
+  }
+}
+
+// Epilogue of the per-sample weight-space product of sample s: J[(s*O + o)*ldJ + off + c*KC + k]
+// = acc[r = o*C + c, k].  A fragment inside R = O*C and inside one o (no multiple of C in
+// (r0, r0 + 31]) writes 32 consecutive c of one row of J, addressed from one base.
+template <class Cfg>
+__device__ __forceinline__ void conv_wgrad_store(f32x16 (&acc)[Cfg::FM][Cfg::FN], int m0, int n0, int s,
+                                                 int O, FastDiv fC, int KC, float* __restrict__ J,
+                                                 long long ldJ, long long off) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
+  const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
+  const int C = (int)fC.d, R = O * C;
+#pragma unroll
+  for (int fm = 0; fm < Cfg::FM; ++fm) {
+    const int r0 = __builtin_amdgcn_readfirstlane(m0 + wm0 + fm * 32);
+    if (r0 >= R) continue;
+    const int o0 = (int)fC.div(r0);
+    if (r0 + 32 <= R && (int)fC.div(r0 + 31) == o0) {
+      float* base = J + ((long long)s * O + o0) * ldJ + off + (long long)(r0 - o0 * C) * KC;
+#pragma unroll
+      for (int fn = 0; fn < Cfg::FN; ++fn) {
+        const int k = n0 + wn0 + fn * 32 + (lane & 31);
+        if (k >= KC) continue;
+#pragma unroll
+        for (int v = 0; v < 16; ++v) at_bytes(base, (uint32_t)(frag_row(v, lane) * KC + k) * 4u) = acc[fm][fn][v];
+      }
+    } else {
+#pragma unroll
+      for (int fn = 0; fn < Cfg::FN; ++fn)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = r0 + frag_row(v, lane), k = n0 + wn0 + fn * 32 + (lane & 31);
+          if (r < R && k < KC) {
+            const int o = (int)fC.div(r), c = r - o * C;
+            J[((long long)s * O + o) * ldJ + off + (long long)c * KC + k] = acc[fm][fn][v];
+          }
+        }
+    }
+  }
+}
 // out[(img*O+o), p, ci] = (sum_k patch(G)[.., p, k] Kt[ci, k]) * dphi[img, p, ci]
 template <class Cfg, bool VEC>
 __global__ void __launch_bounds__(Cfg::THREADS)
@@ -668,16 +767,7 @@ k_conv_bwd(LoadPatchesKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restr
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
   gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
-  float g[Cfg::FM][Cfg::FN][16];
-  gather_acc<Cfg>(g, m0, n0, [&](int r, int c) {
-    const int rc = min(r, R - 1), cc = min(c, N - 1);
-    const int img = (int)fOD.div(rc);              // r = (img*O + o)*D + p
-    const int p = rc - (int)fD.div(rc) * (int)fD.d;
-    return dphi ? dphi[((long long)img * fD.d + p) * N + cc] : 1.f;
-  });
-  for_each_acc_aux<Cfg>(acc, g, m0, n0, [&](int r, int c, float v, float d) {
-    if (r < R && c < N) out[(long long)r * N + c] = v * d;
-  });
+  conv_bwd_store<Cfg>(acc, m0, n0, dphi, out, R, N, fOD, fD);
 }
 
 // direct-to-LDS form (Cg % 32 == 0): the cotangent patches gathered by the DMA, NS LDS stages
@@ -692,16 +782,7 @@ k_conv_bwd_dma(DmaPatches<Cfg::BM, Cfg::WAVES> pa, DmaRowMajor<Cfg::BN, Cfg::WAV
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
   gemm_mainloop_dma_ops<Cfg, NS>(pa, pb, m0, n0, 0, K, smem, acc);
-  float g[Cfg::FM][Cfg::FN][16];
-  gather_acc<Cfg>(g, m0, n0, [&](int r, int c) {
-    const int rc = min(r, R - 1), cc = min(c, N - 1);
-    const int img = (int)fOD.div(rc);
-    const int p = rc - (int)fD.div(rc) * (int)fD.d;
-    return dphi ? dphi[((long long)img * fD.d + p) * N + cc] : 1.f;
-  });
-  for_each_acc_aux<Cfg>(acc, g, m0, n0, [&](int r, int c, float v, float d) {
-    if (r < R && c < N) out[(long long)r * N + c] = v * d;
-  });
+  conv_bwd_store<Cfg>(acc, m0, n0, dphi, out, R, N, fOD, fD);
 }
 
 template <bool VEC>
@@ -791,13 +872,7 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
     lb.fC = fCin;
     gemm_mainloop<Cfg>(la, lb, m0, n0, 0, D, smem, acc);
   }
-  const int R = O * C;
-  for_each_acc<Cfg>(acc, m0, n0, [&](int r, int k, float v) {
-    if (r < R && k < KC) {
-      const int o = (int)fC.div(r), c = r - o * C;
-      J[((long long)s * O + o) * ldJ + off + (long long)c * KC + k] = v;
-    }
-  });
+  conv_wgrad_store<Cfg>(acc, m0, n0, s, O, fC, KC, J, ldJ, off);
 }
 
 // direct-to-LDS form (C % 4 == 0 and Cin % 4 == 0): both operands K-outer, NS LDS stages
@@ -841,13 +916,7 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
     ib.fC = fCin;
     gemm_mainloop_dma_ops<Cfg, NS>(ia, ib, m0, n0, 0, D, smem, acc);
   }
-  const int R = O * C;
-  for_each_acc<Cfg>(acc, m0, n0, [&](int r, int k, float v) {
-    if (r < R && k < KC) {
-      const int o = (int)fC.div(r), c = r - o * C;
-      J[((long long)s * O + o) * ldJ + off + (long long)c * KC + k] = v;
-    }
-  });
+  conv_wgrad_store<Cfg>(acc, m0, n0, s, O, fC, KC, J, ldJ, off);
 }
 
 // Grid of the per-sample weight-space products: the tiles of one sample on one XCD, so the

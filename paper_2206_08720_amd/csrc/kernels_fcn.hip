@@ -179,16 +179,53 @@ struct EpiBwd {
   float* out;
   int R, N;
   FastDiv fO;
+  // Per 32-row MFMA fragment inside R: the out rows and the dphi rows r / O are addressed from
+  // two wave-uniform bases (rows r0 and r0 / O) with 32-bit offsets, and the 16 row quotients
+  // of a lane are shared by its column fragments.
   template <class Cfg>
   __device__ __forceinline__ void tile(f32x16 (&acc)[Cfg::FM][Cfg::FN], int m0, int n0) const {
-    float g[Cfg::FM][Cfg::FN][16];
-    gather_acc<Cfg>(g, m0, n0, [&](int r, int c) {
-      const int rc = min(r, R - 1), cc = min(c, N - 1);
-      return dphi[(long long)fO.div(rc) * N + cc];
-    });
-    for_each_acc_aux<Cfg>(acc, g, m0, n0, [&](int r, int c, float v, float d) {
-      if (r < R && c < N) out[(long long)r * N + c] = v * d;
-    });
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
+    const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
+#pragma unroll
+    for (int fm = 0; fm < Cfg::FM; ++fm) {
+      const int r0 = __builtin_amdgcn_readfirstlane(m0 + wm0 + fm * 32);
+      if (r0 >= R) continue;
+      if (r0 + 32 <= R) {
+        const int q0 = (int)fO.div(r0);
+        float* ob = out + (long long)r0 * N;
+        const float* db = dphi + (long long)q0 * N;
+        int dq[16];
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int i = 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+          dq[v] = ((int)fO.div(r0 + i) - q0) * N;
+        }
+#pragma unroll
+        for (int fn = 0; fn < Cfg::FN; ++fn) {
+          const int c = n0 + wn0 + fn * 32 + (lane & 31);
+          if (c >= N) continue;
+          float d[16];
+#pragma unroll
+          for (int v = 0; v < 16; ++v) d[v] = at_bytes(db, (uint32_t)(dq[v] + c) * 4u);
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int i = 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+            at_bytes(ob, (uint32_t)(i * N + c) * 4u) = acc[fm][fn][v] * d[v];
+          }
+        }
+      } else {
+#pragma unroll
+        for (int fn = 0; fn < Cfg::FN; ++fn)
+#pragma unroll
+          for (int v = 0; v < 16; ++v) {
+            const int r = r0 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+            const int c = n0 + wn0 + fn * 32 + (lane & 31);
+            if (r < R && c < N) out[(long long)r * N + c] = acc[fm][fn][v] * dphi[(long long)fO.div(r) * N + c];
+          }
+      }
+    }
   }
   __device__ __forceinline__ void elem(int r, int c, float v) const {
     if (r < R && c < N) out[(long long)r * N + c] = v * dphi[(long long)fO.div(r) * N + c];
