@@ -380,6 +380,76 @@ __device__ __forceinline__ void for_each_acc_aux(f32x16 (&acc)[Cfg::FM][Cfg::FN]
       }
 }
 
+// Element at a 32-bit byte offset from a base pointer.  With a wave-uniform base this is the
+// scalar-base + 32-bit vector-offset addressing form, one instruction per access with no
+// 64-bit address arithmetic.  The caller keeps `bytes` below 4 GiB.
+__device__ __forceinline__ float& at_bytes(float* base, uint32_t bytes) {
+  return *reinterpret_cast<float*>(reinterpret_cast<char*>(base) + bytes);
+}
+__device__ __forceinline__ const float& at_bytes(const float* base, uint32_t bytes) {
+  return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(base) + bytes);
+}
+
+// Row arithmetic of the epilogues below, per 32-row MFMA fragment: lane l holds rows
+// r0 + 8*(v/4) + 4*(l/32) + v%4 (v = 0..15) of column l%32 of the fragment.
+__device__ __forceinline__ int frag_row(int v, int lane) { return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3); }
+
+// Epilogue of the cotangent backward through a convolution (3x3 or pointwise):
+// out[r, c] = acc[r, c] * dphi[img*D + p, c] for rows r = (img*O + o)*D + p of the O cotangent
+// images of each image (null dphi: the identity).  A fragment that lies inside R and inside
+// one cotangent image (no multiple of D in (r0, r0 + 31]) maps to 32 consecutive rows of dphi,
+// so its row arithmetic is done once and an element costs an offset, a load, a multiply and a
+// store (32-bit byte offsets: N < 2^25); other fragments take the per-element form.
+template <class Cfg>
+__device__ __forceinline__ void store_pixel_rows(f32x16 (&acc)[Cfg::FM][Cfg::FN], int m0, int n0,
+                                                 const float* __restrict__ dphi, float* __restrict__ out, int R,
+                                                 int N, FastDiv fOD, FastDiv fD) {
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
+  const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
+  const int D = (int)fD.d;
+#pragma unroll
+  for (int fm = 0; fm < Cfg::FM; ++fm) {
+    const int r0 = __builtin_amdgcn_readfirstlane(m0 + wm0 + fm * 32);
+    if (r0 >= R) continue;
+    const int t0 = (int)fD.div(r0);
+    if (r0 + 32 <= R && N < (1 << 25) && (int)fD.div(r0 + 31) == t0) {
+      const int img = (int)fOD.div(r0);
+      float* ob = out + (long long)r0 * N;
+      const float* db = dphi ? dphi + ((long long)img * D + (r0 - t0 * D)) * N : nullptr;
+#pragma unroll
+      for (int fn = 0; fn < Cfg::FN; ++fn) {
+        const int c = n0 + wn0 + fn * 32 + (lane & 31);
+        if (c >= N) continue;
+        if (db) {
+          float d[16];
+#pragma unroll
+          for (int v = 0; v < 16; ++v) d[v] = at_bytes(db, (uint32_t)(frag_row(v, lane) * N + c) * 4u);
+#pragma unroll
+          for (int v = 0; v < 16; ++v) at_bytes(ob, (uint32_t)(frag_row(v, lane) * N + c) * 4u) = acc[fm][fn][v] * d[v];
+        } else {
+#pragma unroll
+          for (int v = 0; v < 16; ++v) at_bytes(ob, (uint32_t)(frag_row(v, lane) * N + c) * 4u) = acc[fm][fn][v];
+        }
+      }
+    } else {
+#pragma unroll
+      for (int fn = 0; fn < Cfg::FN; ++fn)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int r = r0 + frag_row(v, lane), c = n0 + wn0 + fn * 32 + (lane & 31);
+          if (r < R && c < N) {
+            const int img = (int)fOD.div(r);
+            const int p = r - (int)fD.div(r) * D;
+            const float d = dphi ? dphi[((long long)img * D + p) * N + c] : 1.f;
+            out[(long long)r * N + c] = acc[fm][fn][v] * d;
+          }
+        }
+    }
+  }
+}
+
 // ------------------------------------------------------------------------------ loaders
 // Loaders never branch: an out-of-range element is read from a clamped (valid) address and
 // replaced by 0 with a select, so the main loop has no divergent control flow.
@@ -421,15 +491,6 @@ __host__ inline bool vec_ok(const void* p, long long ld, long long K) {
 }
 
 // ------------------------------------------------------------------------------ misc
-// Element at a 32-bit byte offset from a base pointer.  With a wave-uniform base this is the
-// scalar-base + 32-bit vector-offset addressing form, one instruction per access with no
-// 64-bit address arithmetic.  The caller keeps `bytes` below 4 GiB.
-__device__ __forceinline__ float& at_bytes(float* base, uint32_t bytes) {
-  return *reinterpret_cast<float*>(reinterpret_cast<char*>(base) + bytes);
-}
-__device__ __forceinline__ const float& at_bytes(const float* base, uint32_t bytes) {
-  return *reinterpret_cast<const float*>(reinterpret_cast<const char*>(base) + bytes);
-}
 __device__ __forceinline__ float act_fwd(int act, float z) {
   if (act == 1) return z > 0.f ? z : 0.f;
   if (act == 2) return erff(z);

@@ -657,68 +657,10 @@ hipError_t launch_conv_flip(hipStream_t s, const float* K, int Cout, int Cin, fl
 }
 
 // ------------------------------------------------------------------------------ backward
-// Row arithmetic of the epilogues below, per 32-row MFMA fragment: lane l holds rows
-// r0 + 8*(v/4) + 4*(l/32) + v%4 (v = 0..15) of column l%32 of the fragment.
-__device__ __forceinline__ int frag_row(int v, int lane) { return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3); }
-
-// Epilogue of the transposed convolution: out[r, c] = acc[r, c] * dphi[img*D + p, c] for rows
-// r = (img*O + o)*D + p (null dphi: the identity).  A fragment that lies inside R and inside
-// one cotangent image (no multiple of D in (r0, r0 + 31]) maps to 32 consecutive rows of dphi,
-// so its row arithmetic is done once and an element costs an offset, a load, a multiply and a
-// store; other fragments take the per-element form.
-template <class Cfg>
-__device__ __forceinline__ void conv_bwd_store(f32x16 (&acc)[Cfg::FM][Cfg::FN], int m0, int n0,
-                                               const float* __restrict__ dphi, float* __restrict__ out, int R,
-                                               int N, FastDiv fOD, FastDiv fD) {
-  const int lane = threadIdx.x & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
-  const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
-  const int D = (int)fD.d;
-#pragma unroll
-  for (int fm = 0; fm < Cfg::FM; ++fm) {
-    const int r0 = __builtin_amdgcn_readfirstlane(m0 + wm0 + fm * 32);
-    if (r0 >= R) continue;
-    const int t0 = (int)fD.div(r0);
-    if (r0 + 32 <= R && (int)fD.div(r0 + 31) == t0) {
-      const int img = (int)fOD.div(r0);
-      float* ob = out + (long long)r0 * N;
-      const float* db = dphi ? dphi + ((long long)img * D + (r0 - t0 * D)) * N : nullptr;
-#pragma unroll
-      for (int fn = 0; fn < Cfg::FN; ++fn) {
-        const int c = n0 + wn0 + fn * 32 + (lane & 31);
-        if (c >= N) continue;
-        if (db) {
-          float d[16];
-#pragma unroll
-          for (int v = 0; v < 16; ++v) d[v] = at_bytes(db, (uint32_t)(frag_row(v, lane) * N + c) * 4u);
-#pragma unroll
-          for (int v = 0; v < 16; ++v) at_bytes(ob, (uint32_t)(frag_row(v, lane) * N + c) * 4u) = acc[fm][fn][v] * d[v];
-        } else {
-#pragma unroll
-          for (int v = 0; v < 16; ++v) at_bytes(ob, (uint32_t)(frag_row(v, lane) * N + c) * 4u) = acc[fm][fn][v];
-        }
-      }
-    } else {
-#pragma unroll
-      for (int fn = 0; fn < Cfg::FN; ++fn)
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int r = r0 + frag_row(v, lane), c = n0 + wn0 + fn * 32 + (lane & 31);
-          if (r < R && c < N) {
-            const int img = (int)fOD.div(r);
-            const int p = r - (int)fD.div(r) * D;
-            const float d = dphi ? dphi[((long long)img * D + p) * N + c] : 1.f;
-            out[(long long)r * N + c] = acc[fm][fn][v] * d;
-          }
-        }
-    }
-  }
-}
-
 // Epilogue of the per-sample weight-space product of sample s: J[(s*O + o)*ldJ + off + c*KC + k]
 // = acc[r = o*C + c, k].  A fragment inside R = O*C and inside one o (no multiple of C in
-// (r0, r0 + 31]) writes 32 consecutive c of one row of J, addressed from one base.
+// (r0, r0 + 31]) writes 32 consecutive c of one row of J, addressed from one base (32-bit
+// byte offsets: KC < 2^25).
 template <class Cfg>
 __device__ __forceinline__ void conv_wgrad_store(f32x16 (&acc)[Cfg::FM][Cfg::FN], int m0, int n0, int s,
                                                  int O, FastDiv fC, int KC, float* __restrict__ J,
@@ -733,7 +675,7 @@ __device__ __forceinline__ void conv_wgrad_store(f32x16 (&acc)[Cfg::FM][Cfg::FN]
     const int r0 = __builtin_amdgcn_readfirstlane(m0 + wm0 + fm * 32);
     if (r0 >= R) continue;
     const int o0 = (int)fC.div(r0);
-    if (r0 + 32 <= R && (int)fC.div(r0 + 31) == o0) {
+    if (r0 + 32 <= R && KC < (1 << 25) && (int)fC.div(r0 + 31) == o0) {
       float* base = J + ((long long)s * O + o0) * ldJ + off + (long long)(r0 - o0 * C) * KC;
 #pragma unroll
       for (int fn = 0; fn < Cfg::FN; ++fn) {
@@ -767,7 +709,7 @@ k_conv_bwd(LoadPatchesKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restr
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
   gemm_mainloop<Cfg>(la, lb, m0, n0, 0, la.K, smem, acc);
-  conv_bwd_store<Cfg>(acc, m0, n0, dphi, out, R, N, fOD, fD);
+  store_pixel_rows<Cfg>(acc, m0, n0, dphi, out, R, N, fOD, fD);
 }
 
 // direct-to-LDS form (Cg % 32 == 0): the cotangent patches gathered by the DMA, NS LDS stages
@@ -782,7 +724,7 @@ k_conv_bwd_dma(DmaPatches<Cfg::BM, Cfg::WAVES> pa, DmaRowMajor<Cfg::BN, Cfg::WAV
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
   gemm_mainloop_dma_ops<Cfg, NS>(pa, pb, m0, n0, 0, K, smem, acc);
-  conv_bwd_store<Cfg>(acc, m0, n0, dphi, out, R, N, fOD, fD);
+  store_pixel_rows<Cfg>(acc, m0, n0, dphi, out, R, N, fOD, fD);
 }
 
 template <bool VEC>

@@ -180,8 +180,8 @@ struct EpiBwd {
   int R, N;
   FastDiv fO;
   // Per 32-row MFMA fragment inside R: the out rows and the dphi rows r / O are addressed from
-  // two wave-uniform bases (rows r0 and r0 / O) with 32-bit offsets, and the 16 row quotients
-  // of a lane are shared by its column fragments.
+  // two wave-uniform bases (rows r0 and r0 / O) with 32-bit byte offsets (N < 2^25), and the 16
+  // row quotients of a lane are shared by its column fragments.
   template <class Cfg>
   __device__ __forceinline__ void tile(f32x16 (&acc)[Cfg::FM][Cfg::FN], int m0, int n0) const {
     const int lane = threadIdx.x & 63;
@@ -192,7 +192,7 @@ struct EpiBwd {
     for (int fm = 0; fm < Cfg::FM; ++fm) {
       const int r0 = __builtin_amdgcn_readfirstlane(m0 + wm0 + fm * 32);
       if (r0 >= R) continue;
-      if (r0 + 32 <= R) {
+      if (r0 + 32 <= R && N < (1 << 25)) {
         const int q0 = (int)fO.div(r0);
         float* ob = out + (long long)r0 * N;
         const float* db = dphi + (long long)q0 * N;
@@ -239,26 +239,9 @@ struct EpiBwdPix {
   float* out;
   int R, N;
   FastDiv fOD, fD;
-  __device__ __forceinline__ long long drow(int r) const {
-    const int img = (int)fOD.div(r), q = r - img * (int)fOD.d;
-    return (long long)img * fD.d + (q - (int)fD.div(q) * (int)fD.d);
-  }
   template <class Cfg>
   __device__ __forceinline__ void tile(f32x16 (&acc)[Cfg::FM][Cfg::FN], int m0, int n0) const {
-    if (!dphi) {
-      for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, float v) {
-        if (r < R && c < N) out[(long long)r * N + c] = v;
-      });
-      return;
-    }
-    float g[Cfg::FM][Cfg::FN][16];
-    gather_acc<Cfg>(g, m0, n0, [&](int r, int c) {
-      const int rc = min(r, R - 1), cc = min(c, N - 1);
-      return dphi[drow(rc) * N + cc];
-    });
-    for_each_acc_aux<Cfg>(acc, g, m0, n0, [&](int r, int c, float v, float d) {
-      if (r < R && c < N) out[(long long)r * N + c] = v * d;
-    });
+    store_pixel_rows<Cfg>(acc, m0, n0, dphi, out, R, N, fOD, fD);
   }
 };
 
