@@ -595,6 +595,33 @@ struct MmaBlocks<Cfg, TA, TB, f32x16> {
   }
 };
 
+// Two accumulators per 32x32 fragment, taking alternate MFMA steps (k = 2j into v[0], 2j + 1
+// into v[1]), summed by the caller after the loop: a wave with one fragment then has two
+// independent MFMA chains instead of one.
+struct DualAcc {
+  f32x16 v[2];
+};
+
+template <class Cfg, class TA, class TB>
+struct MmaBlocks<Cfg, TA, TB, DualAcc> {
+  static constexpr int NB = 4;
+  using Frag = typename MmaBlocks<Cfg, TA, TB, f32x16>::Frag;
+  __device__ static __forceinline__ void load(const float* As, const float* Bs, int blk, int wm0, int wn0,
+                                              int lane, Frag& f) {
+    MmaBlocks<Cfg, TA, TB, f32x16>::load(As, Bs, blk, wm0, wn0, lane, f);
+  }
+  __device__ static __forceinline__ void mma(const Frag& f, DualAcc (&acc)[Cfg::FM][Cfg::FN]) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int fm = 0; fm < Cfg::FM; ++fm)
+#pragma unroll
+        for (int fn = 0; fn < Cfg::FN; ++fn)
+          acc[fm][fn].v[t & 1] =
+              __builtin_amdgcn_mfma_f32_32x32x2f32(f.a[fm][t], f.b[fn][t], acc[fm][fn].v[t & 1], 0, 0, 0);
+  }
+};
+
 // fp64 (pre-activations of the forward pass): two blocks of 16 k, each 4 MFMA steps of
 // 16x16x4 f64 on the fp32 tile values widened exactly.
 template <class Cfg, class TA, class TB>

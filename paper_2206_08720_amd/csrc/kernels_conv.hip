@@ -835,8 +835,14 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
   ia.D = D;
   ia.C = C;
   ia.fC = fC;
-  f32x16 acc[Cfg::FM][Cfg::FN];
-  zero_acc<Cfg>(acc);
+  // two MFMA chains per fragment (DualAcc), added after the K loop
+  DualAcc dacc[Cfg::FM][Cfg::FN];
+#pragma unroll
+  for (int fm = 0; fm < Cfg::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < Cfg::FN; ++fn)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) dacc[fm][fn].v[0][v] = dacc[fm][fn].v[1][v] = 0.f;
   if constexpr (PW) {
     // pointwise: the columns are the input channels themselves, [D, Cin] of the sample
     DmaCotangentKOuter<Cfg::BN, Cfg::WAVES> ib;
@@ -845,7 +851,7 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
     ib.D = D;
     ib.C = Cin;
     ib.fC = fCin;
-    gemm_mainloop_dma_ops<Cfg, NS>(ia, ib, m0, n0, 0, D, smem, acc);
+    gemm_mainloop_dma_ops<Cfg, NS>(ia, ib, m0, n0, 0, D, smem, dacc);
   } else {
     DmaPatchesKOuter<Cfg::BN, Cfg::WAVES> ib;
     ib.x = h + (long long)s * D * Cin;
@@ -856,8 +862,13 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
     ib.C = Cin;
     ib.fW = fW;
     ib.fC = fCin;
-    gemm_mainloop_dma_ops<Cfg, NS>(ia, ib, m0, n0, 0, D, smem, acc);
+    gemm_mainloop_dma_ops<Cfg, NS>(ia, ib, m0, n0, 0, D, smem, dacc);
   }
+  f32x16 acc[Cfg::FM][Cfg::FN];
+#pragma unroll
+  for (int fm = 0; fm < Cfg::FM; ++fm)
+#pragma unroll
+    for (int fn = 0; fn < Cfg::FN; ++fn) acc[fm][fn] = dacc[fm][fn].v[0] + dacc[fm][fn].v[1];
   conv_wgrad_store<Cfg>(acc, m0, n0, s, O, fC, KC, J, ldJ, off);
 }
 
