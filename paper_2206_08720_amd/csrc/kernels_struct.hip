@@ -81,6 +81,43 @@ dim3 plane_grid(long long rows, long long plane) {
   return dim3(bx, by);
 }
 
+// Work items q < plane of `rows` planes (images, or cotangent images r = img*per + o), visited
+// as f(r, q).  The XCD form (ids > 0) gives each workgroup step one 256-item chunk of one plane,
+// assigned by xcd_sample_tile with the `per` planes of one image as a sample: all chunks of an
+// image -- whose 3x3 windows overlap by a row at the chunk edges, and whose O cotangent images
+// share the image's act' -- run on one XCD and meet in its L2.  Its grid is a multiple of 8
+// workgroups, so a workgroup stays on its XCD across steps.  The plain form (ids == 0) strides the
+// planes over blockIdx.y.
+template <class F>
+__device__ __forceinline__ void for_plane_items(int rows, int per, int plane, int ids, F&& f) {
+  if (ids > 0) {
+    const int chunks = (plane + 255) / 256, tiles = per * chunks;
+    for (int id = blockIdx.x; id < ids; id += gridDim.x) {
+      int g, t;
+      if (!xcd_sample_tile(id, tiles, rows / per, g, t)) continue;
+      const int k = t / chunks;
+      const int q = (t - k * chunks) * 256 + (int)threadIdx.x;
+      if (q < plane) f(g * per + k, q);
+    }
+  } else {
+    for (int r = blockIdx.y; r < rows; r += gridDim.y)
+      for (int q = blockIdx.x * 256 + threadIdx.x; q < plane; q += gridDim.x * 256) f(r, q);
+  }
+}
+
+// Launch shape of for_plane_items: the XCD form when its ids fit an int, else the plain form.
+struct PlaneLaunch {
+  dim3 grid;
+  int ids;
+};
+PlaneLaunch plane_launch(long long rows, int per, long long plane) {
+  const long long chunks = (plane + 255) / 256, groups = rows / per;
+  const long long ids = 8 * ((groups + 7) / 8) * per * chunks;
+  if (rows % per == 0 && ids > 0 && ids < (1LL << 31))
+    return {dim3((unsigned)std::min<long long>(ids, 1LL << 20)), (int)ids};
+  return {plane_grid(rows, plane), 0};
+}
+
 // ------------------------------------------------------------------------------ 3x3 windows
 // A lane computes XS consecutive output pixels of one image row for V channels:
 //   acc[j] = sum_{kh, kw} src(y + kh - 1, x0 + j + kw - 1) * tap[kh*3 + kw]   (zero outside).
@@ -125,13 +162,13 @@ template <int V, int XS>
 __global__ void __launch_bounds__(256)
 k_dw_fwd(const float* __restrict__ x, int images, int H, int W, FastDiv fCG, FastDiv fXB,
          const float* __restrict__ w, const float* __restrict__ bias, int act, float* __restrict__ hn,
-         float* __restrict__ dphi) {
+         float* __restrict__ dphi, int ids) {
   const int CG = (int)fCG.d, C = CG * V, XB = (int)fXB.d;
   const int plane = H * XB * CG;
   const long long img_elems = (long long)H * W * C;
-  for (int n = blockIdx.y; n < images; n += gridDim.y) {
+  for_plane_items(images, 1, plane, ids, [&](int n, int q) {
     const float* xi = x + (long long)n * img_elems;
-    for (int q = blockIdx.x * 256 + threadIdx.x; q < plane; q += gridDim.x * 256) {
+    {
       const int rest = (int)fCG.div(q), cg = q - rest * CG;
       const int yy = (int)fXB.div(rest), xb = rest - yy * XB;
       const int c0 = cg * V, x0 = xb * XS;
@@ -159,7 +196,7 @@ k_dw_fwd(const float* __restrict__ x, int images, int H, int W, FastDiv fCG, Fas
         }
       }
     }
-  }
+  });
 }
 
 template <int V>
@@ -215,14 +252,14 @@ k_pool_fwd(const float* __restrict__ x, int images, int Ho, int Wo, FastDiv fCG,
 template <int V, int XS>
 __global__ void __launch_bounds__(256)
 k_dw_bwd(const float* __restrict__ G, int rows, int O, int H, int W, FastDiv fCG, FastDiv fXB,
-         const float* __restrict__ w, const float* __restrict__ dphi, float* __restrict__ out) {
+         const float* __restrict__ w, const float* __restrict__ dphi, float* __restrict__ out, int ids) {
   const int CG = (int)fCG.d, C = CG * V, XB = (int)fXB.d;
   const int plane = H * XB * CG;
   const long long img_elems = (long long)H * W * C;
-  for (int r = blockIdx.y; r < rows; r += gridDim.y) {
+  for_plane_items(rows, O, plane, ids, [&](int r, int q) {
     const float* Gr = G + (long long)r * img_elems;
     const long long dbase = (long long)(r / O) * img_elems;
-    for (int q = blockIdx.x * 256 + threadIdx.x; q < plane; q += gridDim.x * 256) {
+    {
       const int rest = (int)fCG.div(q), cg = q - rest * CG;
       const int yy = (int)fXB.div(rest), xb = rest - yy * XB;
       const int c0 = cg * V, x0 = xb * XS;
@@ -254,7 +291,7 @@ k_dw_bwd(const float* __restrict__ G, int rows, int O, int H, int W, FastDiv fCG
         }
       }
     }
-  }
+  });
 }
 
 template <int V>
@@ -537,11 +574,13 @@ hipError_t launch_dw_fwd(hipStream_t s, const float* x, int images, int H, int W
   if (!plane_fits(images, (long long)H * W * C)) return hipErrorInvalidValue;
   const int XB = cdiv_i(W, kDwFwdXS);
   if (use_vec4(C, {x, w, hn, dphi})) {
-    k_dw_fwd<4, kDwFwdXS><<<plane_grid(images, (long long)H * XB * C / 4), dim3(256), 0, s>>>(
-        x, images, H, W, FastDiv((uint32_t)(C / 4)), FastDiv((uint32_t)XB), w, bias, act, hn, dphi);
+    const PlaneLaunch L = plane_launch(images, 1, (long long)H * XB * C / 4);
+    k_dw_fwd<4, kDwFwdXS><<<L.grid, dim3(256), 0, s>>>(
+        x, images, H, W, FastDiv((uint32_t)(C / 4)), FastDiv((uint32_t)XB), w, bias, act, hn, dphi, L.ids);
   } else {
-    k_dw_fwd<1, kDwFwdXS><<<plane_grid(images, (long long)H * XB * C), dim3(256), 0, s>>>(
-        x, images, H, W, FastDiv((uint32_t)C), FastDiv((uint32_t)XB), w, bias, act, hn, dphi);
+    const PlaneLaunch L = plane_launch(images, 1, (long long)H * XB * C);
+    k_dw_fwd<1, kDwFwdXS><<<L.grid, dim3(256), 0, s>>>(
+        x, images, H, W, FastDiv((uint32_t)C), FastDiv((uint32_t)XB), w, bias, act, hn, dphi, L.ids);
   }
   return hipGetLastError();
 }
@@ -578,11 +617,13 @@ hipError_t launch_dw_bwd(hipStream_t s, const float* G, int images, int O, int H
   if (rows >= (1LL << 31) || !plane_fits(rows, (long long)H * W * C)) return hipErrorInvalidValue;
   const int XB = cdiv_i(W, kDwBwdXS);
   if (use_vec4(C, {G, w, dphi, out})) {
-    k_dw_bwd<4, kDwBwdXS><<<plane_grid(rows, (long long)H * XB * C / 4), dim3(256), 0, s>>>(
-        G, (int)rows, O, H, W, FastDiv((uint32_t)(C / 4)), FastDiv((uint32_t)XB), w, dphi, out);
+    const PlaneLaunch L = plane_launch(rows, O, (long long)H * XB * C / 4);
+    k_dw_bwd<4, kDwBwdXS><<<L.grid, dim3(256), 0, s>>>(
+        G, (int)rows, O, H, W, FastDiv((uint32_t)(C / 4)), FastDiv((uint32_t)XB), w, dphi, out, L.ids);
   } else {
-    k_dw_bwd<1, kDwBwdXS><<<plane_grid(rows, (long long)H * XB * C), dim3(256), 0, s>>>(
-        G, (int)rows, O, H, W, FastDiv((uint32_t)C), FastDiv((uint32_t)XB), w, dphi, out);
+    const PlaneLaunch L = plane_launch(rows, O, (long long)H * XB * C);
+    k_dw_bwd<1, kDwBwdXS><<<L.grid, dim3(256), 0, s>>>(
+        G, (int)rows, O, H, W, FastDiv((uint32_t)C), FastDiv((uint32_t)XB), w, dphi, out, L.ids);
   }
   return hipGetLastError();
 }
