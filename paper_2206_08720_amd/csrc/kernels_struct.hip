@@ -119,7 +119,8 @@ PlaneLaunch plane_launch(long long rows, int per, long long plane) {
 }
 
 // ------------------------------------------------------------------------------ 3x3 windows
-// A lane computes XS consecutive output pixels of one image row for V channels:
+// Forward (fp64 sums, whose widened window would not fit a taller block in registers): a lane
+// computes XS consecutive output pixels of one image row for V channels:
 //   acc[j] = sum_{kh, kw} src(y + kh - 1, x0 + j + kw - 1) * tap[kh*3 + kw]   (zero outside).
 // The 3 x (XS + 2) input pixels the outputs share are loaded first, all at once (each load
 // from a clamped, valid address, the value zeroed outside the image, so no load waits behind a
@@ -152,6 +153,58 @@ __device__ __forceinline__ void dw_segment(const float* __restrict__ img, int H,
 #pragma unroll
         for (int kw = 0; kw < 3; ++kw) sum += (A)win[kh][j + kw].v[v] * (A)tap[kh * 3 + kw].v[v];
       acc[j][v] = sum;
+    }
+  }
+}
+
+// Backward (fp32 sums): a lane computes an RS x XS block of output pixels (rows y0 .. y0 + RS - 1,
+// columns x0 .. x0 + XS - 1) for V channels, walking down the rows:
+//   acc[j] = sum_{kh, kw} src(y + kh - 1, x0 + j + kw - 1) * tap[kh*3 + kw]   (zero outside).
+// Three input rows of XS + 2 pixels stay in registers as a ring; each output row loads one new
+// input row (issued before the row before is formed), so the block costs (RS + 2)(XS + 2)
+// loads instead of 3 (XS + 2) per row.  Every load reads a clamped, valid address and the value
+// is zeroed outside the image, so no load waits behind a branch.  emit(y, acc) receives each
+// output row inside the image.
+template <int V, int XS>
+__device__ __forceinline__ void dw_load_row(const float* __restrict__ img, int H, int W, int C, int c0, int sy,
+                                            int x0, Vf<V> (&row)[XS + 2]) {
+  const int syc = min(max(sy, 0), H - 1);
+  const bool rok = (unsigned)sy < (unsigned)H;
+#pragma unroll
+  for (int j = 0; j < XS + 2; ++j) {
+    const int xc = x0 + j - 1;
+    const bool ok = rok && (unsigned)xc < (unsigned)W;
+    const Vf<V> t = ldv<V>(img + ((long long)syc * W + min(max(xc, 0), W - 1)) * C + c0);
+#pragma unroll
+    for (int v = 0; v < V; ++v) row[j].v[v] = ok ? t.v[v] : 0.f;
+  }
+}
+
+template <int V, int XS, int RS, typename A, class Emit>
+__device__ __forceinline__ void dw_rows(const float* __restrict__ img, int H, int W, int C, int c0, int y0,
+                                        int x0, const Vf<V> (&tap)[9], Emit&& emit) {
+  Vf<V> win[3][XS + 2];
+  dw_load_row<V, XS>(img, H, W, C, c0, y0 - 1, x0, win[0]);
+  dw_load_row<V, XS>(img, H, W, C, c0, y0, x0, win[1]);
+#pragma unroll
+  for (int i = 0; i < RS; ++i) {
+    // ring slots of input rows y - 1, y, y + 1 for output row y = y0 + i
+    const int y = y0 + i;
+    dw_load_row<V, XS>(img, H, W, C, c0, y + 1, x0, win[(i + 2) % 3]);
+    if (y < H) {
+      A acc[XS][V];
+#pragma unroll
+      for (int j = 0; j < XS; ++j)
+#pragma unroll
+        for (int v = 0; v < V; ++v) {
+          A sum = 0;
+#pragma unroll
+          for (int kh = 0; kh < 3; ++kh)
+#pragma unroll
+            for (int kw = 0; kw < 3; ++kw) sum += (A)win[(i + kh) % 3][j + kw].v[v] * (A)tap[kh * 3 + kw].v[v];
+          acc[j][v] = sum;
+        }
+      emit(y, acc);
     }
   }
 }
@@ -248,49 +301,41 @@ k_pool_fwd(const float* __restrict__ x, int images, int Ho, int Wo, FastDiv fCG,
 
 // ------------------------------------------------------------------------------ backward
 // Input pixel q receives G at output pixel q - offset(t) through tap t: the same 3x3 window
-// with the taps flipped, tap'[kh*3 + kw] = w[(2 - kh)*3 + (2 - kw)].
-template <int V, int XS>
+// with the taps flipped, tap'[kh*3 + kw] = w[(2 - kh)*3 + (2 - kw)].  Work item q of a cotangent
+// image as in the forward: an RS x XS block of pixels.
+template <int V, int XS, int RS>
 __global__ void __launch_bounds__(256)
 k_dw_bwd(const float* __restrict__ G, int rows, int O, int H, int W, FastDiv fCG, FastDiv fXB,
          const float* __restrict__ w, const float* __restrict__ dphi, float* __restrict__ out, int ids) {
   const int CG = (int)fCG.d, C = CG * V, XB = (int)fXB.d;
-  const int plane = H * XB * CG;
+  const int plane = ((H + RS - 1) / RS) * XB * CG;
   const long long img_elems = (long long)H * W * C;
   for_plane_items(rows, O, plane, ids, [&](int r, int q) {
     const float* Gr = G + (long long)r * img_elems;
-    const long long dbase = (long long)(r / O) * img_elems;
-    {
-      const int rest = (int)fCG.div(q), cg = q - rest * CG;
-      const int yy = (int)fXB.div(rest), xb = rest - yy * XB;
-      const int c0 = cg * V, x0 = xb * XS;
-      Vf<V> tap[9];
+    const float* dimg = dphi ? dphi + (long long)(r / O) * img_elems : nullptr;
+    const int rest = (int)fCG.div(q), cg = q - rest * CG;
+    const int yb = (int)fXB.div(rest), xb = rest - yb * XB;
+    const int c0 = cg * V, x0 = xb * XS;
+    Vf<V> tap[9];
 #pragma unroll
-      for (int t = 0; t < 9; ++t) tap[t] = ldv<V>(w + (8 - t) * C + c0);
-      // act' of the output pixels (clamped column, unused past W), issued with the window's loads
+    for (int t = 0; t < 9; ++t) tap[t] = ldv<V>(w + (8 - t) * C + c0);
+    dw_rows<V, XS, RS, float>(Gr, H, W, C, c0, yb * RS, x0, tap, [&](int y, const float (&acc)[XS][V]) {
+      // act' of the output pixels (clamped column, unused past W)
       Vf<V> d[XS];
-      if (dphi) {
+      if (dimg) {
 #pragma unroll
-        for (int j = 0; j < XS; ++j)
-          d[j] = ldv<V>(dphi + dbase + ((long long)yy * W + min(x0 + j, W - 1)) * C + c0);
-      }
-      float acc[XS][V];
-      dw_segment<V, XS, float>(Gr, H, W, C, c0, yy, x0, tap, acc);
-      if (dphi) {
-#pragma unroll
-        for (int j = 0; j < XS; ++j)
-#pragma unroll
-          for (int v = 0; v < V; ++v) acc[j][v] *= d[j].v[v];
+        for (int j = 0; j < XS; ++j) d[j] = ldv<V>(dimg + ((long long)y * W + min(x0 + j, W - 1)) * C + c0);
       }
 #pragma unroll
       for (int j = 0; j < XS; ++j) {
         if (x0 + j < W) {
           Vf<V> res;
 #pragma unroll
-          for (int v = 0; v < V; ++v) res.v[v] = acc[j][v];
-          stv<V>(out + (long long)r * img_elems + ((long long)yy * W + x0 + j) * C + c0, res);
+          for (int v = 0; v < V; ++v) res.v[v] = dimg ? acc[j][v] * d[j].v[v] : acc[j][v];
+          stv<V>(out + (long long)r * img_elems + ((long long)y * W + x0 + j) * C + c0, res);
         }
       }
-    }
+    });
   });
 }
 
@@ -566,8 +611,9 @@ bool plane_fits(long long images, long long plane) {
 }  // namespace
 
 // ------------------------------------------------------------------------------ launchers
-// pixels per lane of the depthwise forward (fp64 sums) and backward (fp32)
-constexpr int kDwFwdXS = 4, kDwBwdXS = 8;
+// output pixels per lane of the depthwise forward (fp64 sums, one row) and output block per
+// lane of the backward (fp32: XS pixels of RS rows)
+constexpr int kDwFwdXS = 4, kDwBwdXS = 4, kDwBwdRS = 8;
 
 hipError_t launch_dw_fwd(hipStream_t s, const float* x, int images, int H, int W, int C, const float* w,
                          const float* bias, int act, float* hn, float* dphi) {
@@ -615,14 +661,14 @@ hipError_t launch_dw_bwd(hipStream_t s, const float* G, int images, int O, int H
                          const float* w, const float* dphi, float* out) {
   const long long rows = (long long)images * O;
   if (rows >= (1LL << 31) || !plane_fits(rows, (long long)H * W * C)) return hipErrorInvalidValue;
-  const int XB = cdiv_i(W, kDwBwdXS);
+  const int XB = cdiv_i(W, kDwBwdXS), YB = cdiv_i(H, kDwBwdRS);
   if (use_vec4(C, {G, w, dphi, out})) {
-    const PlaneLaunch L = plane_launch(rows, O, (long long)H * XB * C / 4);
-    k_dw_bwd<4, kDwBwdXS><<<L.grid, dim3(256), 0, s>>>(
+    const PlaneLaunch L = plane_launch(rows, O, (long long)YB * XB * C / 4);
+    k_dw_bwd<4, kDwBwdXS, kDwBwdRS><<<L.grid, dim3(256), 0, s>>>(
         G, (int)rows, O, H, W, FastDiv((uint32_t)(C / 4)), FastDiv((uint32_t)XB), w, dphi, out, L.ids);
   } else {
-    const PlaneLaunch L = plane_launch(rows, O, (long long)H * XB * C);
-    k_dw_bwd<1, kDwBwdXS><<<L.grid, dim3(256), 0, s>>>(
+    const PlaneLaunch L = plane_launch(rows, O, (long long)YB * XB * C);
+    k_dw_bwd<1, kDwBwdXS, kDwBwdRS><<<L.grid, dim3(256), 0, s>>>(
         G, (int)rows, O, H, W, FastDiv((uint32_t)C), FastDiv((uint32_t)XB), w, dphi, out, L.ids);
   }
   return hipGetLastError();
