@@ -82,30 +82,25 @@ dim3 plane_grid(long long rows, long long plane) {
 }
 
 // Work items q < plane of `rows` planes (images, or cotangent images r = img*per + o), visited
-// as f(r, q).  The XCD form (ids > 0) gives each workgroup step one 256-item chunk of one plane,
-// assigned by xcd_sample_tile with the `per` planes of one image as a sample: all chunks of an
-// image -- whose 3x3 windows overlap by a row at the chunk edges, and whose O cotangent images
-// share the image's act' -- run on one XCD and meet in its L2.  Its grid is a multiple of 8
-// workgroups, so a workgroup stays on its XCD across steps.  The plain form (ids == 0) strides the
-// planes over blockIdx.y.
+// as f(r, q).  Each workgroup step takes one 256-item chunk of one plane, assigned by
+// xcd_sample_tile with the `per` planes of one image as a sample: all chunks of an image -- whose
+// 3x3 windows overlap by a row at the chunk edges, and whose O cotangent images share the
+// image's act' -- run on one XCD and meet in its L2.  The grid is a multiple of 8 workgroups, so
+// a workgroup stays on its XCD across steps.
 template <class F>
 __device__ __forceinline__ void for_plane_items(int rows, int per, int plane, int ids, F&& f) {
-  if (ids > 0) {
-    const int chunks = (plane + 255) / 256, tiles = per * chunks;
-    for (int id = blockIdx.x; id < ids; id += gridDim.x) {
-      int g, t;
-      if (!xcd_sample_tile(id, tiles, rows / per, g, t)) continue;
-      const int k = t / chunks;
-      const int q = (t - k * chunks) * 256 + (int)threadIdx.x;
-      if (q < plane) f(g * per + k, q);
-    }
-  } else {
-    for (int r = blockIdx.y; r < rows; r += gridDim.y)
-      for (int q = blockIdx.x * 256 + threadIdx.x; q < plane; q += gridDim.x * 256) f(r, q);
+  const int chunks = (plane + 255) / 256, tiles = per * chunks;
+  for (int id = blockIdx.x; id < ids; id += gridDim.x) {
+    int g, t;
+    if (!xcd_sample_tile(id, tiles, rows / per, g, t)) continue;
+    const int k = t / chunks;
+    const int q = (t - k * chunks) * 256 + (int)threadIdx.x;
+    if (q < plane) f(g * per + k, q);
   }
 }
 
-// Launch shape of for_plane_items: the XCD form when its ids fit an int, else the plain form.
+// Launch shape of for_plane_items; ids = 0 (nothing launched: an invalid-value error) when the
+// chunk ids would not fit an int, which takes more than 2^39 work items.
 struct PlaneLaunch {
   dim3 grid;
   int ids;
@@ -113,9 +108,8 @@ struct PlaneLaunch {
 PlaneLaunch plane_launch(long long rows, int per, long long plane) {
   const long long chunks = (plane + 255) / 256, groups = rows / per;
   const long long ids = 8 * ((groups + 7) / 8) * per * chunks;
-  if (rows % per == 0 && ids > 0 && ids < (1LL << 31))
-    return {dim3((unsigned)std::min<long long>(ids, 1LL << 20)), (int)ids};
-  return {plane_grid(rows, plane), 0};
+  if (per <= 0 || rows % per != 0 || ids <= 0 || ids >= (1LL << 31)) return {dim3(1), 0};
+  return {dim3((unsigned)std::min<long long>(ids, 1LL << 20)), (int)ids};
 }
 
 // ------------------------------------------------------------------------------ 3x3 windows
@@ -618,13 +612,16 @@ constexpr int kDwFwdXS = 4, kDwBwdXS = 4, kDwBwdRS = 8;
 hipError_t launch_dw_fwd(hipStream_t s, const float* x, int images, int H, int W, int C, const float* w,
                          const float* bias, int act, float* hn, float* dphi) {
   if (!plane_fits(images, (long long)H * W * C)) return hipErrorInvalidValue;
+  if (images == 0 || H * W * C == 0) return hipSuccess;
   const int XB = cdiv_i(W, kDwFwdXS);
   if (use_vec4(C, {x, w, hn, dphi})) {
     const PlaneLaunch L = plane_launch(images, 1, (long long)H * XB * C / 4);
+    if (L.ids == 0) return hipErrorInvalidValue;
     k_dw_fwd<4, kDwFwdXS><<<L.grid, dim3(256), 0, s>>>(
         x, images, H, W, FastDiv((uint32_t)(C / 4)), FastDiv((uint32_t)XB), w, bias, act, hn, dphi, L.ids);
   } else {
     const PlaneLaunch L = plane_launch(images, 1, (long long)H * XB * C);
+    if (L.ids == 0) return hipErrorInvalidValue;
     k_dw_fwd<1, kDwFwdXS><<<L.grid, dim3(256), 0, s>>>(
         x, images, H, W, FastDiv((uint32_t)C), FastDiv((uint32_t)XB), w, bias, act, hn, dphi, L.ids);
   }
@@ -661,13 +658,16 @@ hipError_t launch_dw_bwd(hipStream_t s, const float* G, int images, int O, int H
                          const float* w, const float* dphi, float* out) {
   const long long rows = (long long)images * O;
   if (rows >= (1LL << 31) || !plane_fits(rows, (long long)H * W * C)) return hipErrorInvalidValue;
+  if (rows == 0 || H * W * C == 0) return hipSuccess;
   const int XB = cdiv_i(W, kDwBwdXS), YB = cdiv_i(H, kDwBwdRS);
   if (use_vec4(C, {G, w, dphi, out})) {
     const PlaneLaunch L = plane_launch(rows, O, (long long)YB * XB * C / 4);
+    if (L.ids == 0) return hipErrorInvalidValue;
     k_dw_bwd<4, kDwBwdXS, kDwBwdRS><<<L.grid, dim3(256), 0, s>>>(
         G, (int)rows, O, H, W, FastDiv((uint32_t)(C / 4)), FastDiv((uint32_t)XB), w, dphi, out, L.ids);
   } else {
     const PlaneLaunch L = plane_launch(rows, O, (long long)YB * XB * C);
+    if (L.ids == 0) return hipErrorInvalidValue;
     k_dw_bwd<1, kDwBwdXS, kDwBwdRS><<<L.grid, dim3(256), 0, s>>>(
         G, (int)rows, O, H, W, FastDiv((uint32_t)C), FastDiv((uint32_t)XB), w, dphi, out, L.ids);
   }
