@@ -39,7 +39,7 @@ HBM_PEAK_GBS = 8000.0
 # kernel class -> stage of the FLOP counter
 STAGE_OF = {"dense_fwd": "forward", "dense_bwd": "backward", "gram": "gram",
             "ntk_fcn": "contraction", "conv_fwd": "forward", "conv_bwd": "backward",
-            "conv_wgrad": "wgrad", "ntk_splitk": "contraction", "conv_pairsum": "contraction",
+            "conv_wgrad": "wgrad", "ntk_splitk": "contraction", "conv_pairsum": "pairsum",
             "ntk_diag": "contraction", "struct_fwd": "struct_forward",
             "struct_bwd": "struct_backward", "struct_wgrad": "struct_wgrad"}
 # kernel class -> stage of the NTK-vector product's counter
@@ -62,6 +62,8 @@ def parse():
     ap.add_argument("--logit", type=int, default=0, help="o* of --output logit")
     ap.add_argument("--method", default="structured", choices=["structured", "jacobian"],
                     help="structured derivatives (default) or the Jacobian-contraction baseline")
+    ap.add_argument("--conv-order", default="auto", choices=["auto", "outside_in", "inside_out"],
+                    help="contraction order of the 3x3 and pointwise convolutions (auto: the cost model)")
     ap.add_argument("--op", default="ntk", choices=["ntk", "vp"],
                     help="ntk: Theta(X1, X2); vp: the NTK-vector product Theta(X1, X2) v")
     ap.add_argument("--graph", action="store_true",
@@ -184,6 +186,9 @@ def main():
     h = NTK(spec, n1, n2)
     h.set_variant(args.output, args.batch, args.logit)
     h.set_method(args.method)
+    h.set_option(_lib.NTK_OPT_CONV_ORDER, {"auto": _lib.NTK_CONV_ORDER_AUTO,
+                                           "outside_in": _lib.NTK_CONV_ORDER_OUTSIDE_IN,
+                                           "inside_out": _lib.NTK_CONV_ORDER_INSIDE_OUT}[args.conv_order])
     stream = torch.cuda.current_stream()
     if args.op == "vp":
         vvec = torch.from_numpy(np.random.default_rng(0).standard_normal((n2, O)).astype(np.float32)).cuda()
@@ -236,7 +241,7 @@ def main():
 
     entries = ntk_entries(spec, n1, n2, args.output, args.batch)
     fl = ntk_flops(spec, n1, n2, symmetric=sym, output=args.output, batch=args.batch,
-                   method=args.method)
+                   method=args.method, order=args.conv_order)
     stage_of = STAGE_OF
     if args.op == "vp":
         entries = n1 * O                    # outputs of one NTK-vector product
@@ -260,7 +265,9 @@ def main():
     avg_ms = tot / cnt
     flop_per_launch = fl[stage_of[dom]] / (cnt / args.steps)
     achieved = flop_per_launch / (avg_ms * 1e-3) / 1e12
-    roofline = {"kernel": dom, "bound": "mfma", "achieved": achieved,
+    # the inside-out pair sums (k_conv_pairsum) are fp32 vector FMAs: bound by the ALU, whose fp32
+    # vector peak on MI355X equals the fp32 matrix one (256 CUs x 4 SIMDs x 64 FLOP/clk x 2.4 GHz)
+    roofline = {"kernel": dom, "bound": "alu" if stage_of[dom] == "pairsum" else "mfma", "achieved": achieved,
                 "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
                 "frac": achieved / FP32_MFMA_PEAK_TFLOPS, "traffic": measured_traffic(name, dom),
                 "flop_per_launch": flop_per_launch, "avg_launch_ms": avg_ms}
@@ -284,6 +291,7 @@ def main():
                    "layers": [[L.get("in"), L.get("out"), L.get("act")] for L in spec["layers"]],
                    "symmetric_schedule": sym, "parallelism": "single GPU",
                    "method": args.method, "op": args.op, "hip_graph": use_graph,
+                   "conv_order": args.conv_order,
                    "variant": {"output": args.output, "batch": args.batch,
                                **({"logit": args.logit} if args.output == "logit" else {})}},
         "tflops": tflops, "frac_of_fp32_mfma_peak": tflops / FP32_MFMA_PEAK_TFLOPS,

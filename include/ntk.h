@@ -117,7 +117,9 @@ typedef struct ntk_handle ntk_handle;
 #define NTK_OPT_SYMMETRIC   1
 /* NTK_OPT_CONV_ORDER: contraction order of the convolutional summands (appendix
  * "No Structure": outside-in vs inside-out; appendix "CNN NTK Complexity").
- * 0 = auto (pick the cheaper order by the paper's CNN cost model, per layer),
+ * 0 = auto (per layer, the faster order by the paper's CNN cost model, the inside-out
+ *     FLOPs weighted by the measured time per FLOP of the pair-sum kernels on MI355X
+ *     relative to the matrix-core path: 9 for images of at most 16 pixels, 54 above),
  * 1 = outside-in (per-sample weight-space Jacobian, then J1 J2^T),
  * 2 = inside-out (patch-pair Gram times cotangent Gram, summed over pixel pairs).  */
 #define NTK_OPT_CONV_ORDER  2

@@ -839,6 +839,12 @@ static int cnn_forward(ntk_handle* h, const float* const* params, const float* X
   return NTK_OK;
 }
 
+// Time per FLOP of the inside-out pair sums (fp32 vector FMAs) relative to the outside-in path
+// (MFMA products), measured on MI355X at the 4-layer 64-channel CNN on 4x4 images: the kernel
+// for images of at most 16 pixels (k_conv_pairsum_small) 14 against 129 TFLOP/s, the general
+// one (k_conv_pairsum) 2.4.  The cost model compares times, not FLOP counts.
+constexpr double kInsideOutFlopCostSmall = 9.0, kInsideOutFlopCost = 54.0;
+
 static int compute_cnn(ntk_handle* h, const float* const* params, const float* X1, int n1,
                        const float* X2, int n2, float* theta) {
   const int nc = h->nc, O = h->out_dim;
@@ -858,9 +864,10 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   // contraction order of each 3x3 (F = 9 taps) or pointwise (F = 1) convolution: the cost model
   // of the appendix "CNN NTK Complexity" (outside-in N1 N2 O^2 F Cin Cout plus forming J,
   // N O D F Cin Cout per sample, against inside-out N1 N2 (D^2 F Cin + O D^2 Cout + O^2 D Cout)),
-  // or the forced option.  Depthwise and scale layers (block-diagonal weight-space Jacobians,
-  // 9 C and C columns) and every bias (output block-tiled, C columns) always contract
-  // outside-in: their O^2 P term is the smallest of the orders there.
+  // with the inside-out FLOPs weighted by their measured time per FLOP, or the forced option.  Depthwise
+  // and scale layers (block-diagonal weight-space Jacobians, 9 C and C columns) and every bias
+  // (output block-tiled, C columns) always contract outside-in: their O^2 P term is the
+  // smallest of the orders there.
   std::vector<char> inside(nc, 0);
   for (int l = 0; l < nc; ++l) {
     const int kind = h->layers[l].kind;
@@ -870,7 +877,8 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
     const bool io_ok = pairsum_supported(h->bh[l] * h->bw[l], Oe) != 0;
     const double Cin = h->ch[l], Co = h->ch[l + 1];
     const double oi = pairs * Oc * F * Cin * Co + (double)M * Oe * Dl * F * Cin * Co;
-    const double io = pairs * (Dl * Dl * F * Cin + (double)Oe * Dl * Dl * Co + Oc * Dl * Co);
+    const double io = (Dl <= 16 ? kInsideOutFlopCostSmall : kInsideOutFlopCost) * pairs *
+                      (Dl * Dl * F * Cin + (double)Oe * Dl * Dl * Co + Oc * Dl * Co);
     if (h->opt_conv_order == NTK_CONV_ORDER_INSIDE_OUT) {
       if (!io_ok) return fail(h, NTK_E_UNSUPPORTED, "the inside-out order needs D <= 64 pixels and O <= 64");
       inside[l] = 1;

@@ -87,6 +87,29 @@ def _weight_cols(kind, cin, cout):
             "scale": cout}.get(kind, 0)
 
 
+# Time per FLOP of the inside-out pair sums relative to the outside-in matrix-core path, as in
+# the library's cost model: images of at most 16 pixels, and larger ones.
+INSIDE_OUT_FLOP_COST_SMALL, INSIDE_OUT_FLOP_COST = 9.0, 54.0
+
+
+def _inside_out(kind, D, cin, cout, M, Oe, Oc, gpairs, order):
+    """Whether a 3x3 or pointwise convolution is contracted inside-out: forced by `order`, or
+    (order "auto") the library's per-layer choice by the cost model of the appendix "CNN NTK
+    Complexity": outside-in gpairs Oc F Cin Cout plus forming J, M Oe D F Cin Cout, against
+    inside-out gpairs (D^2 F Cin + Oe D^2 Cout + Oc D Cout) times its measured time per FLOP
+    (INSIDE_OUT_FLOP_COST_SMALL for D <= 16, else INSIDE_OUT_FLOP_COST), inside-out only for
+    D <= 64 and Oe <= 64 (the pair-sum kernels' limits)."""
+    if kind not in ("conv3x3", "conv1x1") or order == "outside_in":
+        return False
+    if order == "inside_out":
+        return True
+    F = 9 if kind == "conv3x3" else 1
+    oi = gpairs * Oc * F * cin * cout + M * Oe * D * F * cin * cout
+    w = INSIDE_OUT_FLOP_COST_SMALL if D <= 16 else INSIDE_OUT_FLOP_COST
+    io = w * gpairs * (D * D * F * cin + Oe * D * D * cout + Oc * D * cout)
+    return D <= 64 and Oe <= 64 and io < oi
+
+
 def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", batch="full"):
     """CNN counts per stage.  3x3 convolutions as in the module docstring; the further layer
     kinds (memory-bound, counted for completeness, in the struct_* stages): depthwise 3x3
@@ -94,7 +117,9 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
     with a bias), backward M Oe D C, cotangent 2 M Oe D C; a 2x2 pool M D C forward and
     M Oe D C backward (D: its input pixels); a bias M D C forward and its cotangent (a pixel sum)
     M Oe D C.  The contraction covers every weight-space column (9 Cin Cout, 9 C, C, and C per
-    bias)."""
+    bias).  `order` is "outside_in", "inside_out" or "auto" (the library's
+    per-layer choice, _inside_out) for the 3x3 and pointwise convolutions; a layer contracted
+    inside-out forms no J columns and counts its pair sums in the stage "pairsum"."""
     layers = spec["layers"]
     sp, C = _spatial_layers(spec)
     O = layers[-1]["out"]
@@ -106,22 +131,17 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
     # "struct_wgrad"); a conv bias is added in the conv forward kernel's epilogue
     fwd = bwd = wg = sfwd = sbwd = swg = cols = io = 0.0
     for i, (k, cin, cout, D, bias) in enumerate(sp):
-        if k == "conv1x1":   # pointwise: always outside-in
-            fwd += 2.0 * M * D * cin * cout + (1.0 * M * D * cout if bias else 0.0)
+        if k in ("conv1x1", "conv3x3"):
+            F = 9 if k == "conv3x3" else 1
+            fwd += 2.0 * M * D * F * cin * cout + (1.0 * M * D * cout if bias else 0.0)
             if i >= 1:
-                bwd += 2.0 * M * Oe * D * cout * cin
-            wg += 2.0 * M * (Oe * cout) * cin * D
-            cols += cin * cout
-        elif k == "conv3x3":
-            fwd += 2.0 * M * D * 9 * cin * cout + (1.0 * M * D * cout if bias else 0.0)
-            if i >= 1:
-                bwd += 2.0 * M * Oe * D * 9 * cout * cin
-            if order == "outside_in":
-                wg += 2.0 * M * (Oe * cout) * (9 * cin) * D
-                cols += 9 * cin * cout
+                bwd += 2.0 * M * Oe * D * F * cout * cin
+            if not _inside_out(k, D, cin, cout, M, Oe, Oc, gpairs, order):
+                wg += 2.0 * M * (Oe * cout) * (F * cin) * D
+                cols += F * cin * cout
             else:  # inside-out: patch Gram, one-sided cotangent contraction, then the O x O product
                 # (every input pair, also on the symmetric schedule)
-                io += 2.0 * gpairs * (D * D * 9 * cin + Oe * D * D * cout + Oc * D * cout)
+                io += 2.0 * gpairs * (D * D * F * cin + Oe * D * D * cout + Oc * D * cout)
         elif k == "dwconv3x3":
             sfwd += 2.0 * M * D * 9 * cout + (1.0 * M * D * cout if bias else 0.0)
             if i >= 1:
@@ -147,7 +167,9 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
     for key, v in (("struct_forward", sfwd), ("struct_backward", sbwd), ("struct_wgrad", swg)):
         if v:
             st[key] = v
-    st["contraction"] = 2.0 * pairs * Oc * cols + io
+    st["contraction"] = 2.0 * pairs * Oc * cols
+    if io:
+        st["pairsum"] = io
     st["total"] = sum(st.values())
     return st
 

@@ -43,6 +43,32 @@ def test_cnn4_c64_32x32_full():
     _vs_jc("cnn4_c64_32x32", spec, params, X1, X2)
 
 
+@pytest.fixture(scope="module")
+def c4x4_reference():
+    spec, params, X1, X2 = wl.make_workload("cnn4_c64_4x4")
+    ref, d1, d2 = oracle.ntk_jc_with_norms(spec, params, X1, X2, layer_storage=S)
+    return spec, params, X1, X2, ref, d1, d2
+
+
+@pytest.mark.parametrize("order", ["auto", "outside_in", "inside_out"])
+def test_cnn4_c64_4x4_full(c4x4_reference, order):
+    """The 4-layer CNN on 4x4 images in full, in the cost model's mixed orders (the three
+    64->64 convolutions inside-out, the 3-channel one outside-in: both the pair-sum and the
+    split-K kernels run) and forced all-outside-in and all-inside-out."""
+    from paper_2206_08720_amd import _lib
+    spec, params, X1, X2, ref, d1, d2 = c4x4_reference
+    opt = {"auto": _lib.NTK_CONV_ORDER_AUTO, "outside_in": _lib.NTK_CONV_ORDER_OUTSIDE_IN,
+           "inside_out": _lib.NTK_CONV_ORDER_INSIDE_OUT}[order]
+    print(f"[parity] cnn4_c64_4x4 order={order}", flush=True)
+    prof = {}
+    got = gpu_ntk(spec, params, X1, X2, options={_lib.NTK_OPT_CONV_ORDER: opt}, profile=prof)
+    cs, nw = errors(got, ref, d1, d2)
+    report(f"cnn4_c64_4x4 {order}", cs, nw)
+    assert got.shape == ref.shape and cs <= TOL and nw <= TOL
+    assert ("conv_pairsum" in prof) == (order != "outside_in")
+    assert ("ntk_splitk" in prof) == (order != "inside_out")
+
+
 CASES = [
     # label, spec, n1, n2
     ("one conv layer, 1x1 images", wl.cnn_spec("c1", (1, 1), 3, [8], 4), 5, 6),

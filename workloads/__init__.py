@@ -186,7 +186,7 @@ def make_inputs(spec, n, seed, dist="normal"):
     return x.astype(np.float32)
 
 
-# The five reference workloads.  "depth D" = D hidden layers of width W plus a
+# The reference workloads.  "depth D" = D hidden layers of width W plus a
 # dense readout (D + 1 weight matrices), the paper's FCN of Section 4.1.
 WORKLOADS = {
     "tiny_relu_mlp": dict(
@@ -217,6 +217,12 @@ WORKLOADS = {
              ("conv3x3", 64, "relu", True)],
             10),
         n1=64, n2=64, weight_var="2/fan_in", bias_var=0.01, x_dist="normal", x2_is_x1=False),
+    # The 4-layer CNN on 4x4 images (D = 16): the cost model of the appendix "CNN NTK
+    # Complexity" contracts the three 64->64 convolutions inside-out (about 9x cheaper than
+    # outside-in there) and the 3-channel one outside-in.
+    "cnn4_c64_4x4": dict(
+        index=7, spec=cnn_spec("cnn4_c64_4x4", (4, 4), 3, [64] * 4, 10, act="relu"),
+        n1=64, n2=64, weight_var="2/fan_in", x_dist="normal", x2_is_x1=False),
 }
 
 
