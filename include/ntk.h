@@ -119,7 +119,7 @@ typedef struct ntk_handle ntk_handle;
  * "No Structure": outside-in vs inside-out; appendix "CNN NTK Complexity").
  * 0 = auto (per layer, the faster order by the paper's CNN cost model, the inside-out
  *     FLOPs weighted by the measured time per FLOP of the pair-sum kernels on MI355X
- *     relative to the matrix-core path: 9 for images of at most 16 pixels, 54 above),
+ *     relative to the matrix-core path: 9 for images of at most 16 pixels, 40 above),
  * 1 = outside-in (per-sample weight-space Jacobian, then J1 J2^T),
  * 2 = inside-out (patch-pair Gram times cotangent Gram, summed over pixel pairs).  */
 #define NTK_OPT_CONV_ORDER  2

@@ -1135,6 +1135,20 @@ struct PairArgs {
   int count;
 };
 
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ float dpp_add(float v) {
+  return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xF, false));
+}
+__device__ __forceinline__ float wave_sum(float v) {
+  v = dpp_add<0xB1, 0xF>(v);    // quad_perm [1, 0, 3, 2]
+  v = dpp_add<0x4E, 0xF>(v);    // quad_perm [2, 3, 0, 1]
+  v = dpp_add<0x141, 0xF>(v);   // row_half_mirror
+  v = dpp_add<0x140, 0xF>(v);   // row_mirror
+  v = dpp_add<0x142, 0xA>(v);   // row_bcast15 into rows 1 and 3
+  v = dpp_add<0x143, 0xC>(v);   // row_bcast31 into rows 2 and 3
+  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
+}
+
 __global__ void __launch_bounds__(256)
 k_conv_pairsum(PairArgs a, int n1, int n2, int n2_offset, int O, int H, int W,
                const float* __restrict__ gram, int accumulate, int trace, int diag,
@@ -1210,14 +1224,16 @@ k_conv_pairsum(PairArgs a, int n1, int n2, int n2_offset, int O, int H, int W,
             for (int j = 0; j < kPairOB; ++j)
               if (j < nb) part[j] += tv * G2[((long long)(ob + j) * D + p2) * L.C + c0 + c];
           }
+          // each wave's lanes summed by the DPP butterfly, then the four waves in order
 #pragma unroll
-          for (int j = 0; j < kPairOB; ++j) Hs[j * 256 + t] = part[j];
-          __syncthreads();
-          if (t < nb) {
-            float v = 0.f;
-            for (int q = 0; q < 256; ++q) v += Hs[t * 256 + q];
-            Th[trace ? 0 : o1 * O + ob + t] += v;
+          for (int j = 0; j < kPairOB; ++j) {
+            if (j < nb) {
+              const float v = wave_sum(part[j]);
+              if ((t & 63) == 0) Hs[j * 4 + (t >> 6)] = v;
+            }
           }
+          __syncthreads();
+          if (t < nb) Th[trace ? 0 : o1 * O + ob + t] += ((Hs[t * 4] + Hs[t * 4 + 1]) + Hs[t * 4 + 2]) + Hs[t * 4 + 3];
           __syncthreads();
         }
       }
@@ -1259,20 +1275,6 @@ constexpr int kSmallD = 16, kSmallOB = 12, kSmallCC = 64;
 // lane pairs and quads (quad_perm), half rows (row_half_mirror) and rows (row_mirror) leave
 // every lane of a row with its row's sum; row_bcast15 / row_bcast31 then add rows 0 into 1, 2 into
 // 3, and rows 0-1 into 2-3, so lane 63 holds the total, which every lane reads.  Fixed order.
-template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ float dpp_add(float v) {
-  return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xF, false));
-}
-__device__ __forceinline__ float wave_sum(float v) {
-  v = dpp_add<0xB1, 0xF>(v);    // quad_perm [1, 0, 3, 2]
-  v = dpp_add<0x4E, 0xF>(v);    // quad_perm [2, 3, 0, 1]
-  v = dpp_add<0x141, 0xF>(v);   // row_half_mirror
-  v = dpp_add<0x140, 0xF>(v);   // row_mirror
-  v = dpp_add<0x142, 0xA>(v);   // row_bcast15 into rows 1 and 3
-  v = dpp_add<0x143, 0xC>(v);   // row_bcast31 into rows 2 and 3
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
-}
-
 // G1[o1, p1, c] for p1 < 16 (zero past D or past C; clamped, valid addresses)
 __device__ __forceinline__ void load_g1(const float* __restrict__ G1, int o1, int D, int C, int c, bool cok,
                                         float (&g1)[kSmallD]) {

@@ -840,10 +840,11 @@ static int cnn_forward(ntk_handle* h, const float* const* params, const float* X
 }
 
 // Time per FLOP of the inside-out pair sums (fp32 vector FMAs) relative to the outside-in path
-// (MFMA products), measured on MI355X at the 4-layer 64-channel CNN on 4x4 images: the kernel
-// for images of at most 16 pixels (k_conv_pairsum_small) 14 against 129 TFLOP/s, the general
-// one (k_conv_pairsum) 2.4.  The cost model compares times, not FLOP counts.
-constexpr double kInsideOutFlopCostSmall = 9.0, kInsideOutFlopCost = 54.0;
+// (MFMA products), measured on MI355X with 4-layer 64-channel CNNs: the kernel for images of at
+// most 16 pixels (k_conv_pairsum_small) 14 TFLOP/s on 4x4 images, the general one
+// (k_conv_pairsum) 3.0-3.3 on 5x5 to 8x8 images, against 129 for the matrix-core path.  The cost
+// model compares times, not FLOP counts.
+constexpr double kInsideOutFlopCostSmall = 9.0, kInsideOutFlopCost = 40.0;
 
 static int compute_cnn(ntk_handle* h, const float* const* params, const float* X1, int n1,
                        const float* X2, int n2, float* theta) {

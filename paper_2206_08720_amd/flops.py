@@ -89,7 +89,7 @@ def _weight_cols(kind, cin, cout):
 
 # Time per FLOP of the inside-out pair sums relative to the outside-in matrix-core path, as in
 # the library's cost model: images of at most 16 pixels, and larger ones.
-INSIDE_OUT_FLOP_COST_SMALL, INSIDE_OUT_FLOP_COST = 9.0, 54.0
+INSIDE_OUT_FLOP_COST_SMALL, INSIDE_OUT_FLOP_COST = 9.0, 40.0
 
 
 def _inside_out(kind, D, cin, cout, M, Oe, Oc, gpairs, order):
