@@ -34,6 +34,9 @@ sys.path.insert(0, ROOT)
 
 METRIC = "NTK entries/sec (N1·N2·O²) and fp32 MFMA TFLOP/s, FCN depth 8 width 2048"
 FP32_MFMA_PEAK_TFLOPS = 157.3      # MI355X dense fp32 matrix peak
+# fp32 vector FMAs without the packed forms (the library is compiled with them disabled):
+# 256 CUs x 4 SIMDs x 16 lanes x 2 FLOP x 2.4 GHz = 78.6 TFLOP/s (the packed forms double it)
+FP32_VALU_PEAK_TFLOPS = 78.6
 HBM_PEAK_GBS = 8000.0
 
 # kernel class -> stage of the FLOP counter
@@ -42,6 +45,8 @@ STAGE_OF = {"dense_fwd": "forward", "dense_bwd": "backward", "gram": "gram",
             "conv_wgrad": "wgrad", "ntk_splitk": "contraction", "conv_pairsum": "pairsum",
             "ntk_diag": "contraction", "struct_fwd": "struct_forward",
             "struct_bwd": "struct_backward", "struct_wgrad": "struct_wgrad"}
+# stages computed with fp32 vector FMAs rather than MFMA: the inside-out pair sums
+VALU_STAGES = {"pairsum"}
 # kernel class -> stage of the NTK-vector product's counter
 VP_STAGE_OF = {"dense_fwd": "forward", "dense_bwd": "vjp_backward", "gram": "gram_products",
                "conv_fwd": "forward_and_jvp", "conv_bwd": "vjp_backward",
@@ -265,11 +270,13 @@ def main():
     avg_ms = tot / cnt
     flop_per_launch = fl[stage_of[dom]] / (cnt / args.steps)
     achieved = flop_per_launch / (avg_ms * 1e-3) / 1e12
-    # the inside-out pair sums (k_conv_pairsum) are fp32 vector FMAs: bound by the ALU, whose fp32
-    # vector peak on MI355X equals the fp32 matrix one (256 CUs x 4 SIMDs x 64 FLOP/clk x 2.4 GHz)
-    roofline = {"kernel": dom, "bound": "alu" if stage_of[dom] == "pairsum" else "mfma", "achieved": achieved,
-                "peak": FP32_MFMA_PEAK_TFLOPS, "unit": "TFLOP/s",
-                "frac": achieved / FP32_MFMA_PEAK_TFLOPS, "traffic": measured_traffic(name, dom),
+    # a kernel class of fp32 vector FMAs is bound by the ALU (FP32_VALU_PEAK_TFLOPS), the others
+    # by the matrix cores
+    alu = stage_of[dom] in VALU_STAGES
+    peak = FP32_VALU_PEAK_TFLOPS if alu else FP32_MFMA_PEAK_TFLOPS
+    roofline = {"kernel": dom, "bound": "alu" if alu else "mfma", "achieved": achieved,
+                "peak": peak, "unit": "TFLOP/s",
+                "frac": achieved / peak, "traffic": measured_traffic(name, dom),
                 "flop_per_launch": flop_per_launch, "avg_launch_ms": avg_ms}
 
     h.close()

@@ -175,6 +175,13 @@ typedef struct ntk_handle ntk_handle;
  *   hip_stream  hipStream_t the work is enqueued on; NULL = the default stream.
  *   out         receives the new handle; set to NULL on any error.
  * Returns NTK_OK, NTK_E_ARG, NTK_E_SHAPE, NTK_E_UNSUPPORTED, NTK_E_OOM or NTK_E_HIP.
+ * Size limit: every array the kernels index -- theta [max_n1, max_n2, O, O], an input batch,
+ * each layer's inputs and cotangents for max_n1 + max_n2 samples and all O outputs, the
+ * weight-space cotangent columns of a CNN, the split-K partials -- must hold fewer than 2^31
+ * elements (the kernels form rows and offsets as 32-bit ints).  A descriptor and batch sizes
+ * that break this are refused with NTK_E_UNSUPPORTED, naming the array, before any HIP call
+ * and before anything is allocated; larger problems are computed in blocks of samples
+ * (Theta(X1[R1], X2[R2]) is the block [R1, R2] of Theta(X1, X2)).
  * The device is the one current on the calling thread; later calls must keep it current.
  */
 int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, void* hip_stream,

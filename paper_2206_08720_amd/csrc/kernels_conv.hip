@@ -736,7 +736,8 @@ static hipError_t conv_bwd_vec(hipStream_t s, const float* G, int images, int O,
   const int D = H * W;
   LA la = patches_kinner<VEC>(G, images * O, H, W, Cg);
   LB lb{Kt, Cin, 9 * Cg, 9 * Cg};
-  const int R = images * O * D;
+  int R;
+  if (!to_int((long long)images * O * D, R)) return hipErrorInvalidValue;
   const int tn = cdiv(Cin, Cfg::BN), tm = cdiv(R, Cfg::BM);
   hipError_t e = set_smem<Cfg, LA, LB>((const void*)k_conv_bwd<Cfg, VEC>);
   if (e != hipSuccess) return e;
@@ -751,7 +752,8 @@ hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int
     using Cfg = CfgConvBwd;
     constexpr int NS = kConvBwdStages;
     const int D = H * W, Kd = 9 * Cg;
-    const int R = images * O * D;
+    int R;
+    if (!to_int((long long)images * O * D, R)) return hipErrorInvalidValue;
     const int tn = cdiv(Cin, Cfg::BN), tm = cdiv(R, Cfg::BM);
     auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(G, images * O, H, W, Cg);
     DmaRowMajor<Cfg::BN, Cfg::WAVES> pb{Kt, Kd, Cin};
@@ -1014,7 +1016,7 @@ __global__ void k_ntk_reduce(const float* __restrict__ part, int splits, int N1,
                              int symmetric, int tile, const float* __restrict__ w,
                              const float* __restrict__ gram, float rscale, int accumulate,
                              float* __restrict__ theta) {
-  const int R1 = N1 * O, R2 = N2 * O;
+  const int R1 = N1 * O, R2 = N2 * O;   // below 2^31: the launcher checked them
   const long long total = (long long)R1 * R2;
   for (long long i = blockIdx.x * (long long)blockDim.x + threadIdx.x; i < total;
        i += (long long)gridDim.x * blockDim.x) {
@@ -1100,7 +1102,9 @@ hipError_t launch_ntk_splitk(hipStream_t s, const float* J1, const float* J2, in
 hipError_t launch_ntk_reduce(hipStream_t s, const float* part, int splits, int N1, int N2, int O,
                              int symmetric, const float* w, const float* gram, float rscale,
                              int accumulate, float* theta) {
-  const long long total = (long long)N1 * O * N2 * O;
+  int R1, R2;
+  if (!to_int((long long)N1 * O, R1) || !to_int((long long)N2 * O, R2)) return hipErrorInvalidValue;
+  const long long total = (long long)R1 * R2;
   const int blocks = (int)std::min<long long>((total + 255) / 256, 256 * 64);
   k_ntk_reduce<<<dim3(blocks), dim3(256), 0, s>>>(part, splits, N1, N2, O, symmetric, CfgSplitK::BM,
                                                   w, gram, rscale, accumulate, theta);

@@ -713,7 +713,8 @@ long long ntk_fcn_part_floats(int num_cu) {
 
 hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2, int O,
                           int symmetric, float* theta, int num_cu, float* part) {
-  const int R1 = N1 * O, R2 = N2 * O;
+  int R1, R2;
+  if (!to_int((long long)N1 * O, R1) || !to_int((long long)N2 * O, R2)) return hipErrorInvalidValue;
   bool v = true;
   for (int l = 0; l < c.L; ++l)
     v = v && vec_ok(c.G1[l], c.K[l], c.K[l]) && vec_ok(c.G2[l], c.K[l], c.K[l]);

@@ -8,6 +8,15 @@ namespace ntk {
 
 constexpr int kMaxLayers = 64;  // parametrised layers a model may have
 
+// Narrow a row or element count formed in 64 bits to the int the kernels take.  ntk_init keeps
+// every array the kernels index below 2^31 elements, so this holds for every call on a handle;
+// a count that would wrap is reported as a launch error instead of being truncated.
+inline bool to_int(long long v, int& out) {
+  if (v < 0 || v > 2147483647LL) return false;
+  out = (int)v;
+  return true;
+}
+
 // Timing hook: every launcher brackets its kernel(s) with prof_begin/prof_end.
 struct Profiler;
 void prof_begin(Profiler* p, hipStream_t s, int cls);

@@ -251,6 +251,94 @@ static int validate(const ntk_model_desc* m, ntk_handle* tmp) {
   return NTK_OK;
 }
 
+// ------------------------------------------------------------------------------ index range
+// The launchers and kernels form row counts (samples x outputs x pixels), element offsets
+// inside one array and tile counts as 32-bit ints.  All of them stay in range when every array a
+// kernel indexes -- each workspace array, the inputs, the parameters and theta -- holds fewer
+// than 2^31 elements, which ntk_init checks, before any HIP call, for the largest batches the
+// handle allows.  Products are saturated, so the check itself cannot overflow.
+constexpr long long kMaxElems = (1LL << 31) - 1;
+constexpr long long kSat = 1LL << 62;
+
+static long long smul(long long a, long long b) {
+  long long r;
+  if (a < 0 || b < 0 || __builtin_mul_overflow(a, b, &r) || r > kSat) return kSat;
+  return r;
+}
+static long long smul(std::initializer_list<long long> f) {
+  long long r = 1;
+  for (long long x : f) r = smul(r, x);
+  return r;
+}
+static long long sadd(long long a, long long b) { return std::min(kSat, a + b); }
+
+// Largest arrays of the plan for batches of at most n1 and n2 samples, as (elements, what).
+// Mirrors plan_fcn / plan_cnn (and the lazily allocated Jacobian-contraction and
+// NTK-vector-product buffers), but in saturating arithmetic on the raw descriptor.
+static int check_index_range(const ntk_handle& t, long long n1, long long n2) {
+  const long long O = t.out_dim, M = sadd(n1, n2), T = 128;   // T: the split-K tile (splitk_tile())
+  long long worst = 0;
+  std::string what;
+  auto need = [&](long long elems, const std::string& w) {
+    if (elems > worst) {
+      worst = elems;
+      what = w;
+    }
+  };
+  auto tiles = [&](long long r1, long long r2) { return smul((r1 + T - 1) / T, (r2 + T - 1) / T); };
+  need(smul({n1, n2, O, O}), "theta [n1, n2, O, O]");
+  const long long in_elems = smul({(long long)t.in_h, t.in_w, t.in_c});
+  need(smul(std::max(n1, n2), in_elems), "an input batch");
+  const int n = (int)t.layers.size();
+  if (!t.cnn) {
+    long long dmax = t.layers[0].in;
+    for (int l = 0; l < n; ++l) {
+      const ntk_layer_desc& L = t.layers[l];
+      dmax = std::max<long long>(dmax, L.out);
+      need(smul(M, L.in), "layer " + std::to_string(l) + " inputs [n1 + n2, in]");
+      need(smul((long long)L.in, L.out), "layer " + std::to_string(l) + " weights");
+      need(smul({M, O, (long long)L.out}), "layer " + std::to_string(l) + " cotangents [(n1 + n2) O, out]");
+    }
+    need(smul(sadd(1024, tiles(n1, n2)), T * T), "split-K partials of one-output variants");
+    need(smul({std::max(n1, n2), O, sadd(dmax, 1)}), "Jacobian-contraction rows");
+    need(smul(sadd(1024, tiles(smul(n1, O), smul(n2, O))), T * T), "Jacobian-contraction partials");
+    need(smul(dmax, std::max(n1, n2)), "NTK-vector-product tangents");
+  } else {
+    long long hh = t.in_h, ww = t.in_w, c = t.in_c, ktot = 0;
+    const int nc = n - 2;
+    for (int l = 0; l < nc; ++l) {
+      const ntk_layer_desc& L = t.layers[l];
+      const long long plane_in = smul({hh, ww, c});
+      need(smul(M, plane_in), "layer " + std::to_string(l) + " inputs [n1 + n2, H, W, C]");
+      if (L.kind == NTK_AVGPOOL2) {
+        hh /= 2;
+        ww /= 2;
+        continue;
+      }
+      const long long wcols = L.kind == NTK_CONV3X3_SAME ? smul({9, c, (long long)L.out})
+                              : L.kind == NTK_CONV1X1    ? smul(c, L.out)
+                              : L.kind == NTK_DWCONV3X3_SAME ? smul(9, L.out)
+                                                             : (long long)L.out;
+      need(wcols, "layer " + std::to_string(l) + " weights");
+      ktot = sadd(ktot, sadd(wcols, L.has_bias ? L.out : 0));
+      c = L.out;
+      const long long plane_out = smul({hh, ww, c});
+      need(smul(M, plane_out), "layer " + std::to_string(l) + " outputs [n1 + n2, H, W, C]");
+      need(smul({M, O, plane_out}), "layer " + std::to_string(l) + " cotangents [(n1 + n2) O, H, W, C]");
+    }
+    need(smul({M, O, ktot}), "weight-space cotangent columns J [(n1 + n2) O, K]");
+    need(smul(sadd(1024, tiles(smul(n1, O), smul(n2, O))), T * T), "split-K partials");
+    need(smul(c, O), "readout weights");
+    need(sadd(ktot, smul(O, c)), "NTK-vector-product weight-space vector");
+    need(smul({std::max(n1, n2), O, sadd(c, 1)}), "Jacobian-contraction rows");
+  }
+  if (worst <= kMaxElems) return NTK_OK;
+  return fail(nullptr, NTK_E_UNSUPPORTED,
+              what + " would hold " + std::to_string(worst) +
+                  " elements; every array the library indexes must stay below 2^31 (compute theta "
+                  "in sample blocks instead)");
+}
+
 static size_t align_up(size_t x) { return (x + 255) & ~size_t(255); }
 
 // ------------------------------------------------------------------------------ planning
@@ -400,6 +488,13 @@ extern "C" int ntk_init(const ntk_model_desc* model, int max_n1, int max_n2, voi
   ntk_handle tmp;
   int rc = validate(model, &tmp);
   if (rc != NTK_OK) return rc;
+  tmp.layers.assign(model->layers, model->layers + model->n_layers);
+  tmp.in_h = model->in_h;
+  tmp.in_w = model->in_w;
+  tmp.in_c = model->in_c;
+  tmp.out_dim = model->out_dim;
+  rc = check_index_range(tmp, max_n1, max_n2);
+  if (rc != NTK_OK) return rc;
   ntk_handle* h = new (std::nothrow) ntk_handle();
   if (!h) return fail(nullptr, NTK_E_OOM, "host allocation failed");
   h->layers.assign(model->layers, model->layers + model->n_layers);
@@ -474,10 +569,12 @@ static hipError_t contract_rows(ntk_handle* h, const float* A, const float* B, i
   }
   const int Or = trace ? 1 : Oe;
   const long long Kc = trace ? (long long)Oe * K : K;
+  int R1, R2;
+  if (!to_int((long long)n1 * Or, R1) || !to_int((long long)n2 * Or, R2)) return hipErrorInvalidValue;
   int chunk = 0;
-  const int splits = splitk_plan(n1 * Or, n2 * Or, Kc, sym ? 1 : 0, part_capacity, &chunk);
+  const int splits = splitk_plan(R1, R2, Kc, sym ? 1 : 0, part_capacity, &chunk);
   prof_begin(P, s, KC_NTK_SPLITK);
-  e = launch_ntk_splitk(s, A, B, n1 * Or, n2 * Or, Kc, Kc, sym ? 1 : 0, chunk, splits, part);
+  e = launch_ntk_splitk(s, A, B, R1, R2, Kc, Kc, sym ? 1 : 0, chunk, splits, part);
   prof_end(P, s, KC_NTK_SPLITK);
   if (e != hipSuccess) return e;
   prof_begin(P, s, KC_NTK_REDUCE);
@@ -1032,7 +1129,10 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
         prof_end(P, s, KC_CONV_BWD);
       } else if (L.kind == NTK_CONV1X1) {
         prof_begin(P, s, KC_CONV_BWD);
-        e = launch_pw_bwd(s, Gcur, F(h->off_Kt[l]), dprev, M * Oe * Hl * Wl, cin, cout, Oe, Hl * Wl, Gnext);
+        int rows;
+        e = to_int((long long)M * Oe * Hl * Wl, rows)
+                ? launch_pw_bwd(s, Gcur, F(h->off_Kt[l]), dprev, rows, cin, cout, Oe, Hl * Wl, Gnext)
+                : hipErrorInvalidValue;
         prof_end(P, s, KC_CONV_BWD);
       } else {
         prof_begin(P, s, KC_STRUCT_BWD);
@@ -1087,7 +1187,9 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
     }
     const int Or = trace ? 1 : Oe;                 // rows per sample of the contraction
     const long long Kc = trace ? (long long)O * Kcall : Kcall;
-    const int R1 = n1 * Or, R2 = n2 * Or;
+    int R1, R2;
+    if (!to_int((long long)n1 * Or, R1) || !to_int((long long)n2 * Or, R2))
+      return fail(h, NTK_E_UNSUPPORTED, "contraction rows exceed 2^31");
     int chunk = 0;
     const int splits = splitk_plan(R1, R2, Kc, sym ? 1 : 0, h->part_capacity, &chunk);
     prof_begin(P, s, KC_NTK_SPLITK);

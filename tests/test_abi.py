@@ -136,3 +136,47 @@ def test_init_accepts_the_structured_layer_kinds(lib):
     finally:
         if h.value:
             lib.ntk_free(h)
+
+
+def test_init_refuses_sizes_past_the_32_bit_index_range(lib):
+    """Every array the kernels index must hold fewer than 2^31 elements; a plan that breaks this
+    is refused with NTK_E_UNSUPPORTED before any HIP call (so here, without a GPU, the code is
+    not NTK_E_HIP), and the message names the array."""
+    from paper_2206_08720_amd import _lib
+    # theta [n1, n2, O, O] alone: 2^16 x 2^16 samples x 10 x 10 outputs
+    assert _init(lib, wl.fcn_spec("f", 8, [16], 10), 1 << 16, 1 << 16)[0] == _lib.NTK_E_UNSUPPORTED
+    assert "theta" in _lib.last_error() and "2^31" in _lib.last_error()
+    # a small theta (256 x 256 x 100 x 100), but the cotangents of a wide layer:
+    # (n1 + n2) * O * width = 512 * 100 * 65536
+    rc, _ = _init(lib, wl.fcn_spec("f", 64, [65536], 100), 256, 256)
+    assert rc == _lib.NTK_E_UNSUPPORTED and "cotangents" in _lib.last_error()
+    # 8192 images, O = 100, 64 x 64 pixels, 8 channels: 3.4e9 cotangent rows, 2.7e10 cotangent
+    # elements (and a theta of 1.7e11 elements)
+    rc, _ = _init(lib, wl.cnn_spec("c", (64, 64), 3, [8], 100), 4096, 4096)
+    assert rc == _lib.NTK_E_UNSUPPORTED and "would hold" in _lib.last_error()
+    # a small theta, but the conv cotangents [(n1 + n2) O, 256, 256, 64] = 2.1e10 elements
+    rc, _ = _init(lib, wl.cnn_spec("c", (256, 256), 3, [64], 10), 256, 256)
+    assert rc == _lib.NTK_E_UNSUPPORTED and "cotangents" in _lib.last_error()
+    # the outside-in weight-space columns J [(n1 + n2) O, 9 Cin Cout]: 512-channel layers
+    rc, _ = _init(lib, wl.cnn_spec("c", (4, 4), 3, [512, 512], 10), 512, 512)
+    assert rc == _lib.NTK_E_UNSUPPORTED and "J" in _lib.last_error()
+    # saturating arithmetic: dimensions near 2^31 each do not wrap into a small product
+    huge = wl.cnn_spec("c", (1 << 15, 1 << 15), 1 << 15, [1 << 15], 1 << 15)
+    assert _init(lib, huge, 1 << 30, 1 << 30)[0] == _lib.NTK_E_UNSUPPORTED
+    # n1 + n2 itself past 2^31
+    assert _init(lib, wl.fcn_spec("f", 1, [1], 1), (1 << 31) - 1, (1 << 31) - 1)[0] == \
+        _lib.NTK_E_UNSUPPORTED
+
+
+def test_init_accepts_the_largest_workloads(lib):
+    """The benchmarked shapes stay inside the range: validation passes, and without a GPU the
+    first device call then fails with NTK_E_HIP (or succeeds on a GPU host)."""
+    from paper_2206_08720_amd import _lib
+    for name in ("relu_mlp_d8_w2048", "erf_mlp_d3_w4096", "cnn4_c64_32x32", "cnn_struct_c64_32x32"):
+        w = wl.WORKLOADS[name]
+        rc, h = _init(lib, w["spec"], w["n1"], w["n2"])
+        try:
+            assert rc in (_lib.NTK_OK, _lib.NTK_E_HIP), (name, _lib.last_error())
+        finally:
+            if h.value:
+                lib.ntk_free(h)
