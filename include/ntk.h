@@ -223,6 +223,30 @@ int ntk_compute(ntk_handle* h, const float* const* params, const float* X1, int 
 int ntk_vector_product(ntk_handle* h, const float* const* params, const float* X1, int n1,
                        const float* X2, int n2, const float* v, float* out);
 
+/* ---- an entry point that allocates nothing ---------------------------------------
+ * ntk_compute_static -- for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc.  Enqueues the full theta
+ * [n1, n2, O, O] on `hip_stream` (NULL = the default stream), as ntk_compute does with the
+ * default options (structured method, full output, the symmetric schedule when X2 == X1 and
+ * n2 == n1, automatic conv contraction order), but without a handle: the descriptor is
+ * validated and planned on every call (host work only), and the workspace is one fixed device
+ * array of NTK_STATIC_SCRATCH_BYTES inside the library per GPU, which stays resident until the
+ * process ends.  The call allocates and frees no device memory, and creates no streams or
+ * events.
+ *   model, params, X1, n1, X2, n2, theta  as for ntk_init and ntk_compute.
+ * Returns NTK_OK, NTK_E_ARG, NTK_E_SHAPE, NTK_E_UNSUPPORTED or NTK_E_HIP; the message is read
+ * with ntk_last_error(NULL).  NTK_E_UNSUPPORTED, with nothing enqueued, also when the
+ * workspace of this model and these batch sizes exceeds NTK_STATIC_SCRATCH_BYTES (the message
+ * gives the bytes needed; use ntk_init then).
+ * Every call on a GPU uses that GPU's one array and leaves its contents there (nothing in it
+ * needs clearing between calls): calls that overlap on one GPU -- on different streams or
+ * from different host threads -- race, and the caller must order them.  The first call with a
+ * device current looks up the array's device address.
+ */
+#define NTK_STATIC_SCRATCH_BYTES (64 * 1024 * 1024)
+int ntk_compute_static(const ntk_model_desc* model, const float* const* params, const float* X1, int n1,
+                       const float* X2, int n2, float* theta, void* hip_stream);
+
 /* ntk_free -- release the workspace and the handle.  NULL is a no-op.  Synchronises
  * the handle's stream first. */
 int ntk_free(ntk_handle* h);

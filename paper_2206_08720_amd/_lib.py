@@ -36,7 +36,8 @@ NTK_OPT_GRAPH = 7
 EXPORTED_SYMBOLS = ("ntk_init", "ntk_compute", "ntk_free", "ntk_last_error", "ntk_set_option",
                     "ntk_set_stream", "ntk_workspace_bytes", "ntk_profile_enable",
                     "ntk_profile_read", "ntk_device_info", "ntk_mfma_peak",
-                    "ntk_vector_product")
+                    "ntk_vector_product", "ntk_compute_static")
+STATIC_SCRATCH_BYTES = 64 * 1024 * 1024   # NTK_STATIC_SCRATCH_BYTES
 
 
 class ntk_layer_desc(ctypes.Structure):
@@ -92,6 +93,9 @@ def load():
     lib.ntk_profile_read.restype = ctypes.c_int
     lib.ntk_vector_product.argtypes = [P, ctypes.POINTER(P), P, ctypes.c_int, P, ctypes.c_int, P, P]
     lib.ntk_vector_product.restype = ctypes.c_int
+    lib.ntk_compute_static.argtypes = [ctypes.POINTER(ntk_model_desc), ctypes.POINTER(P), P, ctypes.c_int, P,
+                                       ctypes.c_int, P, P]
+    lib.ntk_compute_static.restype = ctypes.c_int
     lib.ntk_device_info.argtypes = [ctypes.POINTER(ctypes.c_int), ctypes.POINTER(ctypes.c_int)]
     lib.ntk_device_info.restype = ctypes.c_int
     lib.ntk_mfma_peak.argtypes = [ctypes.c_int, ctypes.POINTER(ctypes.c_double)]

@@ -11,6 +11,7 @@
 #include <algorithm>
 #include <cstdio>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -86,6 +87,9 @@ struct ntk_handle {
   int in_h = 1, in_w = 1, in_c = 0, out_dim = 0;
   bool cnn = false;
   int max_n1 = 0, max_n2 = 0;
+  // lean plan (ntk_compute_static): no stream-K or split-forward partials, the smallest split-K
+  // buffer, so that the workspace is only the arrays one evaluation of the full theta needs
+  bool lean = false;
   hipStream_t stream = nullptr;
   // a second stream of the library's own for the independent steps (weight transposes during
   // the forward pass, layer-input Grams during the backward), joined back with events
@@ -367,14 +371,15 @@ static void plan_fcn(ntk_handle* h) {
   for (int l = 0; l < L; ++l) h->off_G[l] = take(Mmax * O * h->dims[l + 1]);
   for (int l = 1; l < L; ++l) h->off_Wt[l] = take((size_t)h->dims[l] * h->dims[l + 1]);
   for (int l = 0; l <= L; ++l) h->off_gram[l] = take((size_t)h->max_n1 * h->max_n2);
-  h->off_skpart = take((size_t)ntk_fcn_part_floats(h->num_cu));
-  {
+  if (h->lean) {   // the full theta only: no stream-K, no split forward, no one-output variants
+    h->off_skpart = h->off_fpart = h->off_vpart = 0;
+    h->fpart_capacity = h->vpart_capacity = 0;
+  } else {
+    h->off_skpart = take((size_t)ntk_fcn_part_floats(h->num_cu));
     long long dmax = 1;
     for (int d : h->dims) dmax = std::max<long long>(dmax, d);
     h->fpart_capacity = dense_fwd_part_doubles((long long)Mmax, dmax);
     h->off_fpart = take((size_t)h->fpart_capacity * 2);
-  }
-  {
     const int T = splitk_tile();
     const size_t tiles_max = (size_t)((h->max_n1 + T - 1) / T) * ((h->max_n2 + T - 1) / T);
     h->vpart_capacity = (long long)(1024 + tiles_max) * T * T;   // >= max_n1 * max_n2
@@ -464,7 +469,9 @@ static void plan_cnn(ntk_handle* h) {
   h->off_gram_r = take((size_t)h->max_n1 * h->max_n2);
   const int T = splitk_tile();
   const size_t tiles_max = (size_t)((h->max_n1 * O + T - 1) / T) * ((h->max_n2 * O + T - 1) / T);
-  h->part_capacity = (long long)(1024 + tiles_max) * T * T;   // >= R1max * R2max
+  // >= R1max * R2max: the split-K plan never holds fewer than one partial product; the lean plan
+  // keeps four (split-K up to 4 ways)
+  h->part_capacity = h->lean ? 4LL * h->max_n1 * O * h->max_n2 * O : (long long)(1024 + tiles_max) * T * T;
   h->off_part = take((size_t)h->part_capacity);
   h->ws_bytes = off;
 }
@@ -874,7 +881,7 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   c.gram_readout = F(h->off_gram[L]);
   c.readout_scale = 1.f;
   prof_begin(P, s, KC_NTK_FCN);
-  e = launch_ntk_fcn(s, c, n1, n2, O, sym ? 1 : 0, theta, h->num_cu, F(h->off_skpart));
+  e = launch_ntk_fcn(s, c, n1, n2, O, sym ? 1 : 0, theta, h->num_cu, h->lean ? nullptr : F(h->off_skpart));
   prof_end(P, s, KC_NTK_FCN);
   if (e != hipSuccess) return hip_fail(h, e, "ntk contraction");
   return NTK_OK;
@@ -1680,6 +1687,71 @@ extern "C" int ntk_compute(ntk_handle* h, const float* const* params, const floa
       return compute_graph(h, params, X1, n1, X2, n2, theta);
   }
   return compute_eager(h, params, X1, n1, X2, n2, theta);
+}
+
+// ------------------------------------------------------------------------------ no-allocation entry
+// The workspace of ntk_compute_static: one array per device, resident until the process ends.
+// In host code `scratch` names a host-side stand-in, not the device array, so it is never passed
+// to a kernel or a copy; the device address comes from hipGetSymbolAddress, once per device, on
+// the first call made with that device current.
+static __device__ __align__(256) char scratch[NTK_STATIC_SCRATCH_BYTES];
+constexpr int kMaxDevices = 64;
+static std::mutex g_scratch_mu;
+static char* g_scratch_ptr[kMaxDevices] = {};
+
+static int static_scratch(char** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_fail(nullptr, e, "hipGetDevice");
+  if (dev < 0 || dev >= kMaxDevices) return fail(nullptr, NTK_E_UNSUPPORTED, "device index beyond 63");
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess || !p) return hip_fail(nullptr, e, "hipGetSymbolAddress of the static scratch");
+    g_scratch_ptr[dev] = static_cast<char*>(p);
+  }
+  *out = g_scratch_ptr[dev];
+  return NTK_OK;
+}
+
+extern "C" int ntk_compute_static(const ntk_model_desc* model, const float* const* params, const float* X1,
+                                  int n1, const float* X2, int n2, float* theta, void* hip_stream) {
+  if (!params || !X1 || !X2 || !theta) return fail(nullptr, NTK_E_ARG, "null pointer argument");
+  if (n1 <= 0 || n2 <= 0) return fail(nullptr, NTK_E_ARG, "n1 and n2 must be positive");
+  // a handle on the stack: host bookkeeping only, no streams, events or device memory
+  ntk_handle h;
+  int rc = validate(model, &h);
+  if (rc != NTK_OK) return rc;
+  h.layers.assign(model->layers, model->layers + model->n_layers);
+  h.in_h = model->in_h;
+  h.in_w = model->in_w;
+  h.in_c = model->in_c;
+  h.out_dim = model->out_dim;
+  rc = check_index_range(h, n1, n2);
+  if (rc != NTK_OK) return rc;
+  h.max_n1 = n1;
+  h.max_n2 = n2;
+  h.lean = true;
+  if (h.cnn)
+    plan_cnn(&h);
+  else
+    plan_fcn(&h);
+  if (h.ws_bytes > (size_t)NTK_STATIC_SCRATCH_BYTES)
+    return fail(nullptr, NTK_E_UNSUPPORTED,
+                "this model and these batch sizes need " + std::to_string(h.ws_bytes) +
+                    " bytes of workspace; the static scratch holds " + std::to_string(NTK_STATIC_SCRATCH_BYTES) +
+                    " (use ntk_init and ntk_compute)");
+  const int np = param_tensor_count(&h);
+  for (int i = 0; i < np; ++i)
+    if (!params[i]) return fail(nullptr, NTK_E_ARG, "null parameter pointer");
+  rc = static_scratch(&h.ws);
+  if (rc != NTK_OK) return rc;
+  h.stream = (hipStream_t)hip_stream;
+  rc = compute_eager(&h, params, X1, n1, X2, n2, theta);
+  h.ws = nullptr;   // the scratch is never released
+  if (rc != NTK_OK) g_init_error = h.err;
+  return rc;
 }
 
 extern "C" int ntk_vector_product(ntk_handle* h, const float* const* params, const float* X1, int n1,

@@ -165,3 +165,30 @@ def compute(spec, params, X1, X2=None, output="full", batch="full", logit=0, met
         return out
     finally:
         h.close()
+
+
+def compute_static(spec, params, X1, X2=None, out=None, stream=None):
+    """Enqueue the full Theta(X1, X2) through ntk_compute_static: no handle, and no device
+    memory allocated by the library (its workspace is the library's fixed per-GPU scratch
+    array of _lib.STATIC_SCRATCH_BYTES).  `out` [n1, n2, O, O] may be given so that nothing at
+    all is allocated; otherwise it is allocated here, by torch.  Asynchronous on `stream`
+    (default: the current stream)."""
+    lib = _lib.load()
+    X2 = X1 if X2 is None else X2
+    O = spec["layers"][-1]["out"]
+    n1, n2 = X1.shape[0], X2.shape[0]
+    for i, t in enumerate(list(params) + [X1, X2]):
+        if not isinstance(t, torch.Tensor) or not t.is_cuda or t.dtype != torch.float32 \
+                or not t.is_contiguous():
+            raise TypeError(f"argument {i} must be a contiguous float32 tensor on the GPU")
+    if out is None:
+        out = torch.empty((n1, n2, O, O), dtype=torch.float32, device=X1.device)
+    elif tuple(out.shape) != (n1, n2, O, O) or out.dtype != torch.float32 or not out.is_contiguous():
+        raise ValueError(f"out must be a contiguous float32 tensor of shape {(n1, n2, O, O)}")
+    desc, keep = _lib.model_desc(spec)
+    ptrs = (ctypes.c_void_p * len(params))(*[p.data_ptr() for p in params])
+    s = torch.cuda.current_stream() if stream is None else stream
+    _lib.check(lib.ntk_compute_static(ctypes.byref(desc), ptrs, ctypes.c_void_p(X1.data_ptr()), n1,
+                                      ctypes.c_void_p(X2.data_ptr()), n2, ctypes.c_void_p(out.data_ptr()),
+                                      ctypes.c_void_p(s.cuda_stream)))
+    return out

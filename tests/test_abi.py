@@ -180,3 +180,34 @@ def test_init_accepts_the_largest_workloads(lib):
         finally:
             if h.value:
                 lib.ntk_free(h)
+
+
+def _static(lib, spec, n1, n2):
+    """ntk_compute_static with dummy non-null device pointers: every check it makes before the
+    first HIP call runs, and nothing is dereferenced on the host."""
+    from paper_2206_08720_amd import _lib
+    desc, keep = _lib.model_desc(spec)
+    nparams = len(wl.param_shapes(spec))
+    ptrs = (ctypes.c_void_p * nparams)(*([256] * nparams))
+    dummy = ctypes.c_void_p(256)
+    return lib.ntk_compute_static(ctypes.byref(desc), ptrs, dummy, n1, dummy, n2, dummy, None)
+
+
+def test_static_entry_checks_before_any_device_call(lib):
+    """The entry point that allocates nothing refuses, before any HIP call, null pointers,
+    malformed models and workspaces beyond its fixed scratch (naming the bytes needed); shapes
+    that fit get as far as the first device call (NTK_E_HIP without a GPU)."""
+    from paper_2206_08720_amd import _lib
+    desc, keep = _lib.model_desc(wl.fcn_spec("f", 8, [16], 3))
+    assert lib.ntk_compute_static(ctypes.byref(desc), None, None, 1, None, 1, None, None) == _lib.NTK_E_ARG
+    bad = wl.fcn_spec("b", 8, [16], 3)
+    bad["layers"][1]["in"] = 15
+    assert _static(lib, bad, 4, 4) == _lib.NTK_E_SHAPE
+    # the depth-8 width-2048 FCN at 512 + 512 samples needs ~0.9 GB: refused, with the size
+    big = wl.WORKLOADS["relu_mlp_d8_w2048"]["spec"]
+    assert _static(lib, big, 512, 512) == _lib.NTK_E_UNSUPPORTED
+    msg = _lib.last_error()
+    assert "static scratch" in msg and str(_lib.STATIC_SCRATCH_BYTES) in msg
+    for name in ("tiny_relu_mlp", "relu_mlp_d4_w512"):
+        w = wl.WORKLOADS[name]
+        assert _static(lib, w["spec"], w["n1"], w["n2"]) in (_lib.NTK_OK, _lib.NTK_E_HIP), _lib.last_error()

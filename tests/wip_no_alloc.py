@@ -1,0 +1,82 @@
+"""The entry point that allocates nothing (ntk_compute_static) against ntk_compute, through the
+C ABI: two calls in a row on the same GPU scratch, the second with smaller batches, each
+compared with the handle-based entry point on the same inputs to the parity bar (CS-normalised
+and normwise 1e-4).  The output is pre-filled with NaN, so every entry must be written."""
+import numpy as np
+import pytest
+
+import workloads as wl
+from gpu_helpers import TOL, errors, to_dev
+
+pytestmark = pytest.mark.gpu
+
+
+def _cnn16():
+    return wl.cnn_spec("cnn16_4x4", (4, 4), 3, [16, 16], 10, act="relu")
+
+
+def _struct():
+    return wl.cnn_layers_spec("struct_8x8", (8, 8), 3,
+                              [("conv3x3", 8, "relu", True), ("dwconv3x3", "relu", True),
+                               ("conv1x1", 8, "erf", True), ("avgpool2",), ("scale", "relu", True),
+                               ("conv3x3", 8, "relu", False)], 5)
+
+
+def _case(name):
+    """(spec, params, X1, X2, second call's (n1, n2))."""
+    if name in wl.WORKLOADS:
+        spec, params, X1, X2 = wl.make_workload(name)
+        small = {"tiny_relu_mlp": (5, 3), "relu_mlp_d4_w512": (64, 64)}[name]
+        return spec, params, X1, X2, small
+    spec = _cnn16() if name == "cnn16_4x4" else _struct()
+    params = wl.make_params(spec, 4242, "2/fan_in")
+    X1 = wl.make_inputs(spec, 12, 4343)
+    X2 = wl.make_inputs(spec, 10, 4444)
+    return spec, params, X1, X2, (7, 4)
+
+
+def _handle_theta(spec, params, X1, X2):
+    from gpu_helpers import gpu_ntk
+    return gpu_ntk(spec, params, X1, X2)
+
+
+@pytest.mark.parametrize("name", ["tiny_relu_mlp", "relu_mlp_d4_w512", "cnn16_4x4", "struct_8x8"])
+def test_static_entry_matches_ntk_compute(name):
+    import torch
+    from paper_2206_08720_amd.ntk import compute_static
+    spec, params, X1, X2, (m1, m2) = _case(name)
+    ps = to_dev(params)
+    aliased = X2 is X1
+    for k, (a, b) in enumerate([(X1.shape[0], X2.shape[0]), (m1, m1 if aliased else m2)]):
+        print(f"[no-alloc] {name} call {k}: n1={a} n2={b} aliased={aliased}", flush=True)
+        x1n = np.ascontiguousarray(X1[:a])
+        x2n = x1n if aliased else np.ascontiguousarray(X2[:b])
+        x1 = to_dev([x1n])[0]
+        x2 = x1 if aliased else to_dev([x2n])[0]
+        O = spec["layers"][-1]["out"]
+        out = torch.full((a, b, O, O), float("nan"), dtype=torch.float32, device="cuda")
+        compute_static(spec, ps, x1, x2, out=out)
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+        ref = _handle_theta(spec, params, x1n, x2n).astype(np.float64)
+        d1 = np.einsum("nnoo->no", _handle_theta(spec, params, x1n, x1n).astype(np.float64))
+        d2 = np.einsum("nnoo->no", _handle_theta(spec, params, x2n, x2n).astype(np.float64))
+        assert np.all(np.isfinite(got))
+        cs, nw = errors(got, ref, d1, d2)
+        print(f"[no-alloc] {name} call {k}: cs={cs:.3g} normwise={nw:.3g}", flush=True)
+        assert cs <= TOL and nw <= TOL
+
+
+def test_static_entry_refuses_a_workspace_beyond_its_scratch():
+    import torch
+    from paper_2206_08720_amd import _lib
+    from paper_2206_08720_amd.ntk import compute_static
+    spec, params, X1, X2 = wl.make_workload("relu_mlp_d8_w2048", 512, 512)
+    ps = to_dev(params)
+    x1, x2 = to_dev([X1, X2])
+    out = torch.zeros((512, 512, 10, 10), dtype=torch.float32, device="cuda")
+    with pytest.raises(_lib.NTKError) as ei:
+        compute_static(spec, ps, x1, x2, out=out)
+    assert ei.value.code == _lib.NTK_E_UNSUPPORTED and "static scratch" in str(ei.value)
+    torch.cuda.synchronize()
+    assert float(out.abs().max()) == 0.0     # nothing was enqueued
