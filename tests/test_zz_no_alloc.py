@@ -6,7 +6,7 @@ import numpy as np
 import pytest
 
 import workloads as wl
-from gpu_helpers import TOL, errors, to_dev
+from tests.gpu_helpers import TOL, errors, to_dev
 
 pytestmark = pytest.mark.gpu
 
@@ -36,7 +36,7 @@ def _case(name):
 
 
 def _handle_theta(spec, params, X1, X2):
-    from gpu_helpers import gpu_ntk
+    from tests.gpu_helpers import gpu_ntk
     return gpu_ntk(spec, params, X1, X2)
 
 
