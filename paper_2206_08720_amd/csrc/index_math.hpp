@@ -112,4 +112,17 @@ __host__ __device__ inline bool xcd_sample_tile(int id, int tiles, int samples, 
   return s < samples;
 }
 
+// Blocks in contiguous ranges per XCD: workgroup id runs on XCD id % 8, and XCD x takes the
+// blocks [x * nblocks / 8, (x + 1) * nblocks / 8) in order, so the blocks of one XCD are
+// neighbours in the caller's block order (and share that XCD's L2 for the operands they have in
+// common).  The grid has 8 * ceil(nblocks / 8) workgroups; returns false for the ids past the end
+// of their XCD's range.
+__host__ __device__ inline bool xcd_block(int id, int nblocks, int& blk) {
+  const int xcd = id & 7, slot = id >> 3;
+  const int base = (int)((long long)xcd * nblocks / 8);
+  const int end = (int)((long long)(xcd + 1) * nblocks / 8);
+  blk = base + slot;
+  return blk < end;
+}
+
 }  // namespace ntk

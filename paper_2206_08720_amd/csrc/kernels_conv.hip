@@ -1112,343 +1112,3 @@ hipError_t launch_ntk_reduce(hipStream_t s, const float* part, int splits, int N
 }
 
 }  // namespace ntk
-
-namespace ntk {
-
-// ------------------------------------------------------------------------------ inside-out order
-// For one input pair (n1, n2) = blockIdx.x and every conv layer marked inside-out:
-//   PK[p1, p2] = patch1[p1] . patch2[p2]   (the inner Jacobian product; built from the pixel
-//                Gram H[q1, q2] = h1[q1] . h2[q2] summed over the 9 taps shifted together; for a
-//                pointwise layer the patch is the pixel itself and PK = H)
-//   T[c, p2]   = sum_p1 G1[o1, p1, c] PK[p1, p2]                      (one o1 at a time)
-//   theta[o1, o2] += sum_{p2, c} T[c, p2] G2[o2, p2, c]
-// which is the inside-out contraction order of the constant-block-diagonal MJJMP with
-// cost N^2 (D^2 F W + O D^2 W + O^2 D W).  Then the readout summand (g1.g2) delta is added
-// (unless an outside-in pass already wrote theta, in which case theta is accumulated into).
-// Fixed summation order: deterministic.  Limits: D <= 64, O <= 64 (LDS), C chunked by 64.
-constexpr int kPairDMax = 64, kPairOMax = 64, kPairCC = 64, kPairOB = 16;
-
-struct PairLayer {
-  const float* h;    // layer input of the stacked batch, [M, D, Cin]
-  const float* G;    // cotangent of the layer output, [M*O, D, C]
-  int Cin, C;
-  int taps;          // 9 (3x3 convolution) or 1 (pointwise)
-};
-struct PairArgs {
-  PairLayer layer[kMaxLayers];
-  int count;
-};
-
-template <int CTRL, int ROW_MASK>
-__device__ __forceinline__ float dpp_add(float v) {
-  return v + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, ROW_MASK, 0xF, false));
-}
-__device__ __forceinline__ float wave_sum(float v) {
-  v = dpp_add<0xB1, 0xF>(v);    // quad_perm [1, 0, 3, 2]
-  v = dpp_add<0x4E, 0xF>(v);    // quad_perm [2, 3, 0, 1]
-  v = dpp_add<0x141, 0xF>(v);   // row_half_mirror
-  v = dpp_add<0x140, 0xF>(v);   // row_mirror
-  v = dpp_add<0x142, 0xA>(v);   // row_bcast15 into rows 1 and 3
-  v = dpp_add<0x143, 0xC>(v);   // row_bcast31 into rows 2 and 3
-  return __int_as_float(__builtin_amdgcn_readlane(__float_as_int(v), 63));
-}
-
-__global__ void __launch_bounds__(256)
-k_conv_pairsum(PairArgs a, int n1, int n2, int n2_offset, int O, int H, int W,
-               const float* __restrict__ gram, int accumulate, int trace, int diag,
-               float* __restrict__ theta) {
-  extern __shared__ float sm[];
-  const int D = H * W;
-  float* Hs = sm;                           // [D][D]; later the reduction scratch [256][OB]
-  float* PK = Hs + 256 * kPairOB;           // [D][D]
-  float* Ts = PK + kPairDMax * kPairDMax;   // [CC][D]
-  float* Th = Ts + kPairCC * kPairDMax;     // [O][O]
-  const int t = threadIdx.x;
-  // sample indices within batch 1 / 2 (batch diagonal: the pair (n, n))
-  const int i1 = diag ? blockIdx.x : blockIdx.x / n2, i2 = diag ? blockIdx.x : blockIdx.x % n2;
-  const int s1 = i1, s2 = n2_offset + i2;                  // rows of the stacked batch
-  const int n_out = trace ? 1 : O * O;                     // outputs per pair
-  for (int q = t; q < n_out; q += 256) Th[q] = 0.f;
-  for (int li = 0; li < a.count; ++li) {
-    const PairLayer L = a.layer[li];
-    const float* h1 = L.h + (long long)s1 * D * L.Cin;
-    const float* h2 = L.h + (long long)s2 * D * L.Cin;
-    // pixel Gram
-    for (int q = t; q < D * D; q += 256) {
-      const int q1 = q / D, q2 = q - q1 * D;
-      float acc = 0.f;
-      for (int ci = 0; ci < L.Cin; ++ci) acc += h1[q1 * L.Cin + ci] * h2[q2 * L.Cin + ci];
-      Hs[q] = acc;
-    }
-    __syncthreads();
-    // patch-pair Gram: both patches use the same tap, so the shifted pixel pairs are summed
-    for (int q = t; q < D * D; q += 256) {
-      if (L.taps == 1) {
-        PK[q] = Hs[q];
-        continue;
-      }
-      const int p1 = q / D, p2 = q - p1 * D;
-      const int y1 = p1 / W, x1 = p1 - y1 * W, y2 = p2 / W, x2 = p2 - y2 * W;
-      float acc = 0.f;
-      for (int kh = 0; kh < 3; ++kh)
-        for (int kw = 0; kw < 3; ++kw) {
-          const int a1 = y1 + kh - 1, b1 = x1 + kw - 1, a2 = y2 + kh - 1, b2 = x2 + kw - 1;
-          if (a1 >= 0 && a1 < H && b1 >= 0 && b1 < W && a2 >= 0 && a2 < H && b2 >= 0 && b2 < W)
-            acc += Hs[(a1 * W + b1) * D + (a2 * W + b2)];
-        }
-      PK[q] = acc;
-    }
-    __syncthreads();
-    const float* G1 = L.G + (long long)s1 * O * D * L.C;
-    const float* G2 = L.G + (long long)s2 * O * D * L.C;
-    for (int c0 = 0; c0 < L.C; c0 += kPairCC) {
-      const int cc = min(kPairCC, L.C - c0);
-      for (int o1 = 0; o1 < O; ++o1) {
-        // T[c, p2] = sum_p1 G1[o1, p1, c0 + c] PK[p1, p2]
-        for (int q = t; q < cc * D; q += 256) {
-          const int p2 = q / cc, c = q - p2 * cc;
-          float acc = 0.f;
-          for (int p1 = 0; p1 < D; ++p1)
-            acc += G1[((long long)o1 * D + p1) * L.C + c0 + c] * PK[p1 * D + p2];
-          Ts[c * D + p2] = acc;
-        }
-        __syncthreads();
-        // theta[o1, o2] += sum_{p2, c} T[c, p2] G2[o2, p2, c0 + c], OB outputs at a time
-        // (traced: only o2 = o1, summed into one value)
-        const int ob_begin = trace ? o1 : 0, ob_end = trace ? o1 + 1 : O;
-        for (int ob = ob_begin; ob < ob_end; ob += kPairOB) {
-          const int nb = min(kPairOB, ob_end - ob);
-          float part[kPairOB];
-#pragma unroll
-          for (int j = 0; j < kPairOB; ++j) part[j] = 0.f;
-          for (int q = t; q < cc * D; q += 256) {
-            const int p2 = q / cc, c = q - p2 * cc;
-            const float tv = Ts[c * D + p2];
-#pragma unroll
-            for (int j = 0; j < kPairOB; ++j)
-              if (j < nb) part[j] += tv * G2[((long long)(ob + j) * D + p2) * L.C + c0 + c];
-          }
-          // each wave's lanes summed by the DPP butterfly, then the four waves in order
-#pragma unroll
-          for (int j = 0; j < kPairOB; ++j) {
-            if (j < nb) {
-              const float v = wave_sum(part[j]);
-              if ((t & 63) == 0) Hs[j * 4 + (t >> 6)] = v;
-            }
-          }
-          __syncthreads();
-          if (t < nb) Th[trace ? 0 : o1 * O + ob + t] += ((Hs[t * 4] + Hs[t * 4 + 1]) + Hs[t * 4 + 2]) + Hs[t * 4 + 3];
-          __syncthreads();
-        }
-      }
-    }
-  }
-  __syncthreads();
-  // readout summand (g1 . g2) delta_{o1 o2}; traced: O (g1 . g2).  gram is [n1, n2], or the
-  // per-sample [n] vector on the batch diagonal.
-  const float gr = diag ? gram[i1] : gram[(long long)i1 * n2 + i2];
-  const long long pair = diag ? i1 : (long long)i1 * n2 + i2;
-  for (int q = t; q < n_out; q += 256) {
-    const int o1 = q / O, o2 = q - o1 * O;
-    float* dst = theta + pair * n_out + q;
-    float v = Th[q];
-    if (accumulate)
-      v += *dst;
-    else if (trace)
-      v += (float)O * gr;
-    else if (o1 == o2)
-      v += gr;
-    *dst = v;
-  }
-}
-
-// The same pair sums for images of at most 16 pixels (the shapes where inside-out is the cheaper
-// order), laid out for the vector units: one workgroup of four waves per input pair.  Per layer:
-//   * the two samples' layer inputs are staged in LDS (64 input channels at a time, rows padded to
-//     65 floats) and thread (q1, q2) forms the pixel Gram H[q1, q2]; then PK as above;
-//   * per chunk of 64 output channels c (lane = channel) and block of at most kSmallOB outputs o2
-//     (their G2 staged in LDS), wave w takes o1 = w, w + 4, ...:
-//       t[p2] = sum_p1 G1[o1, p1, c] PK[p1, p2]       (registers; PK rows read as broadcasts; the
-//                                                      next o1's G1 is loaded meanwhile)
-//       s[o2] = sum_p2 t[p2] G2[o2, p2, c]
-//     and theta[o1, o2] (LDS) += the sum of s[o2] over the 64 lanes, by a fixed butterfly.
-// Every sum runs in a fixed order: deterministic.
-constexpr int kSmallD = 16, kSmallOB = 12, kSmallCC = 64;
-
-// Sum over the 64 lanes of a wave with DPP moves (register to register, a few cycles each):
-// lane pairs and quads (quad_perm), half rows (row_half_mirror) and rows (row_mirror) leave
-// every lane of a row with its row's sum; row_bcast15 / row_bcast31 then add rows 0 into 1, 2 into
-// 3, and rows 0-1 into 2-3, so lane 63 holds the total, which every lane reads.  Fixed order.
-// G1[o1, p1, c] for p1 < 16 (zero past D or past C; clamped, valid addresses)
-__device__ __forceinline__ void load_g1(const float* __restrict__ G1, int o1, int D, int C, int c, bool cok,
-                                        float (&g1)[kSmallD]) {
-  const int cc = cok ? c : C - 1;
-#pragma unroll
-  for (int p1 = 0; p1 < kSmallD; ++p1) {
-    const float v = G1[((long long)o1 * D + min(p1, D - 1)) * C + cc];
-    g1[p1] = (p1 < D && cok) ? v : 0.f;
-  }
-}
-
-__global__ void __launch_bounds__(256)
-k_conv_pairsum_small(PairArgs a, int n1, int n2, int n2_offset, int O, int H, int W,
-                     const float* __restrict__ gram, int accumulate, int trace, int diag,
-                     float* __restrict__ theta) {
-  extern __shared__ float sm[];
-  constexpr int XL = kSmallCC + 1;               // padded row of a staged layer input
-  float* X1s = sm;                               // [16][65]
-  float* X2s = X1s + kSmallD * XL;               // [16][65]
-  float* Hs = X2s + kSmallD * XL;                // [16][16]
-  float* PK = Hs + kSmallD * kSmallD;            // [16][16]
-  float* G2s = PK + kSmallD * kSmallD;           // [kSmallOB][16][64]
-  float* Th = G2s + kSmallOB * kSmallD * kSmallCC; // [O][O] (traced: one sum per wave, [4])
-  const int D = H * W;
-  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
-  const int i1 = diag ? blockIdx.x : blockIdx.x / n2, i2 = diag ? blockIdx.x : blockIdx.x % n2;
-  const int s1 = i1, s2 = n2_offset + i2;
-  const int n_out = trace ? 1 : O * O;
-  for (int q = t; q < (trace ? 4 : n_out); q += 256) Th[q] = 0.f;
-  for (int li = 0; li < a.count; ++li) {
-    const PairLayer L = a.layer[li];
-    const float* h1 = L.h + (long long)s1 * D * L.Cin;
-    const float* h2 = L.h + (long long)s2 * D * L.Cin;
-    // pixel Gram, 64 input channels at a time
-    const int q1 = t >> 4, q2 = t & 15;
-    float hacc = 0.f;
-    for (int c0 = 0; c0 < L.Cin; c0 += kSmallCC) {
-      const int cc = min(kSmallCC, L.Cin - c0);
-      __syncthreads();                           // the previous chunk's reads are done
-      for (int q = t; q < D * kSmallCC; q += 256) {
-        const int p = q / kSmallCC, c = q - p * kSmallCC;
-        X1s[p * XL + c] = c < cc ? h1[(long long)p * L.Cin + c0 + c] : 0.f;
-        X2s[p * XL + c] = c < cc ? h2[(long long)p * L.Cin + c0 + c] : 0.f;
-      }
-      __syncthreads();
-      if (q1 < D && q2 < D)
-        for (int c = 0; c < cc; ++c) hacc += X1s[q1 * XL + c] * X2s[q2 * XL + c];
-    }
-    if (q1 < D && q2 < D) Hs[q1 * kSmallD + q2] = hacc;
-    __syncthreads();
-    // patch-pair Gram: both patches use the same tap, so the shifted pixel pairs are summed;
-    // rows and columns past D are zero
-    {
-      float acc = 0.f;
-      if (q1 < D && q2 < D) {
-        if (L.taps == 1) {
-          acc = Hs[q1 * kSmallD + q2];
-        } else {
-          const int y1 = q1 / W, x1 = q1 - y1 * W, y2 = q2 / W, x2 = q2 - y2 * W;
-          for (int kh = 0; kh < 3; ++kh)
-            for (int kw = 0; kw < 3; ++kw) {
-              const int a1 = y1 + kh - 1, b1 = x1 + kw - 1, a2 = y2 + kh - 1, b2 = x2 + kw - 1;
-              if (a1 >= 0 && a1 < H && b1 >= 0 && b1 < W && a2 >= 0 && a2 < H && b2 >= 0 && b2 < W)
-                acc += Hs[(a1 * W + b1) * kSmallD + (a2 * W + b2)];
-            }
-        }
-      }
-      PK[q1 * kSmallD + q2] = acc;
-    }
-    const float* G1 = L.G + (long long)s1 * O * D * L.C;
-    const float* G2 = L.G + (long long)s2 * O * D * L.C;
-    for (int c0 = 0; c0 < L.C; c0 += kSmallCC) {
-      const int c = c0 + lane;
-      const bool cok = c < L.C;
-      for (int ob = 0; ob < O; ob += kSmallOB) {
-        const int nb = min(kSmallOB, O - ob);
-        __syncthreads();                         // PK written; the previous block's G2 reads done
-        // all 16 pixel rows are written (zeros past D and past C), so that every term of the
-        // unrolled sums below reads a defined value
-        for (int q = t; q < nb * kSmallD * kSmallCC; q += 256) {
-          const int j = q / (kSmallD * kSmallCC), rem = q - j * kSmallD * kSmallCC;
-          const int p2 = rem / kSmallCC, l = rem - p2 * kSmallCC;
-          G2s[q] = (p2 < D && c0 + l < L.C) ? G2[((long long)(ob + j) * D + p2) * L.C + c0 + l] : 0.f;
-        }
-        __syncthreads();
-        float g1[kSmallD];
-        if (wave < O) load_g1(G1, wave, D, L.C, c, cok, g1);
-        for (int o1 = wave; o1 < O; o1 += 4) {
-          // the next o1's G1 is in flight while this one's sums are formed
-          float g1n[kSmallD];
-          load_g1(G1, min(o1 + 4, O - 1), D, L.C, c, cok, g1n);
-          if (!(trace && (o1 < ob || o1 >= ob + nb))) {   // traced: only o2 = o1
-            float tv[kSmallD];
-#pragma unroll
-            for (int p2 = 0; p2 < kSmallD; ++p2) tv[p2] = 0.f;
-#pragma unroll
-            for (int p1 = 0; p1 < kSmallD; ++p1)
-#pragma unroll
-              for (int p2 = 0; p2 < kSmallD; ++p2) tv[p2] += g1[p1] * PK[p1 * kSmallD + p2];
-            // unrolled over the block (guarded), so that the outputs' sums and lane reductions
-            // overlap instead of running one after another
-#pragma unroll
-            for (int j = 0; j < kSmallOB; ++j) {
-              if (j < nb && !(trace && ob + j != o1)) {
-                float sv = 0.f;
-#pragma unroll
-                for (int p2 = 0; p2 < kSmallD; ++p2) sv += tv[p2] * G2s[(j * kSmallD + p2) * kSmallCC + lane];
-                sv = wave_sum(sv);
-                if (lane == 0) Th[trace ? wave : o1 * O + ob + j] += sv;   // rows of o1 are this wave's
-              }
-            }
-          }
-#pragma unroll
-          for (int p1 = 0; p1 < kSmallD; ++p1) g1[p1] = g1n[p1];
-        }
-      }
-    }
-    __syncthreads();                             // Hs / PK are rewritten by the next layer
-  }
-  __syncthreads();
-  const float gr = diag ? gram[i1] : gram[(long long)i1 * n2 + i2];
-  const long long pair = diag ? i1 : (long long)i1 * n2 + i2;
-  for (int q = t; q < n_out; q += 256) {
-    const int o1 = q / O, o2 = q - o1 * O;
-    float* dst = theta + pair * n_out + q;
-    float v = trace ? ((Th[0] + Th[1]) + Th[2]) + Th[3] : Th[q];
-    if (accumulate)
-      v += *dst;
-    else if (trace)
-      v += (float)O * gr;
-    else if (o1 == o2)
-      v += gr;
-    *dst = v;
-  }
-}
-
-int pairsum_supported(int D, int O) { return D <= kPairDMax && O <= kPairOMax; }
-
-hipError_t launch_conv_pairsum(hipStream_t s, const PairLayerList& layers, int n1, int n2,
-                               int n2_offset, int O, int H, int W, const float* gram, int accumulate,
-                               int trace, int diag, float* theta) {
-  PairArgs a{};
-  a.count = layers.count;
-  for (int i = 0; i < layers.count; ++i) {
-    a.layer[i].h = layers.h[i];
-    a.layer[i].G = layers.G[i];
-    a.layer[i].Cin = layers.Cin[i];
-    a.layer[i].C = layers.C[i];
-    a.layer[i].taps = layers.taps[i];
-  }
-  if (H * W <= kSmallD) {
-    const int bytes = (2 * kSmallD * (kSmallCC + 1) + 2 * kSmallD * kSmallD + kSmallOB * kSmallD * kSmallCC +
-                       (trace ? 4 : O * O)) * 4;
-    hipError_t e = hipFuncSetAttribute((const void*)k_conv_pairsum_small,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-    if (e != hipSuccess) return e;
-    k_conv_pairsum_small<<<dim3(diag ? n1 : n1 * n2), dim3(256), bytes, s>>>(a, n1, n2, n2_offset, O, H, W,
-                                                                           gram, accumulate, trace, diag,
-                                                                           theta);
-    return hipGetLastError();
-  }
-  const int bytes = (256 * kPairOB + 2 * kPairDMax * kPairDMax + kPairCC * kPairDMax +
-                     kPairOMax * kPairOMax) * 4;
-  hipError_t e = hipFuncSetAttribute((const void*)k_conv_pairsum,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-  if (e != hipSuccess) return e;
-  k_conv_pairsum<<<dim3(diag ? n1 : n1 * n2), dim3(256), bytes, s>>>(a, n1, n2, n2_offset, O, H, W,
-                                                                     gram, accumulate, trace, diag,
-                                                                     theta);
-  return hipGetLastError();
-}
-
-}  // namespace ntk

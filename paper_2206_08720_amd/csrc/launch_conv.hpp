@@ -40,22 +40,17 @@ hipError_t launch_ntk_reduce(hipStream_t s, const float* part, int splits, int N
                              int symmetric, const float* w, const float* gram, float rscale,
                              int accumulate, float* theta);
 
-// Inside-out order for the 3x3 or pointwise conv layers listed (see k_conv_pairsum).  The G pointers must stay
-// valid until the kernel runs, so every listed layer's cotangent must still be resident.
-struct PairLayerList {
-  const float* h[kMaxLayers];
-  const float* G[kMaxLayers];
-  int Cin[kMaxLayers];
-  int C[kMaxLayers];
-  int taps[kMaxLayers];   // 9: 3x3 convolution, 1: pointwise
-  int count;
-};
-int pairsum_supported(int D, int O);
+// Inside-out order of one 3x3 (taps = 9) or pointwise (taps = 1) convolution on the matrix cores
+// (see kernels_pairsum.hip): theta (+)= the layer's summand for every input pair, from its input
+// h [M, D, Cin] and output cotangent G [M*O, D, C] of the stacked batch (batch 2 from row
+// n2_offset).  Gt is a workspace of pairsum_gt_floats(rows of the stacked batch, O, D, C) floats.
 // trace != 0: one value per pair, sum_o Theta[o, o] (readout summand O (g1 . g2)).
-// diag != 0: only the pairs (n, n), n < n1; gram is then the per-sample vector g1[n] . g2[n]
-// and theta is [n1, ...].
-hipError_t launch_conv_pairsum(hipStream_t s, const PairLayerList& layers, int n1, int n2,
-                               int n2_offset, int O, int H, int W, const float* gram, int accumulate,
-                               int trace, int diag, float* theta);
+// diag != 0: only the pairs (n, n), n < n1 = n2; gram is then the per-sample vector g1[n] . g2[n]
+// and theta is [n1, ...].  accumulate = 0 writes theta with the readout summand added.
+int pairsum_supported(int D);
+long long pairsum_gt_floats(long long images, int O, int D, int C);
+hipError_t launch_conv_pairsum(hipStream_t s, const float* h, const float* G, float* Gt, int n1, int n2,
+                               int n2_offset, int O, int H, int W, int Cin, int C, int taps,
+                               const float* gram, int accumulate, int trace, int diag, float* theta);
 
 }  // namespace ntk

@@ -160,6 +160,7 @@ struct ntk_handle {
                                   // every layer is outside-in (the NTK-vector product's layout)
   long long Ktot = 0;             // columns of J at most: every weight and bias column
   size_t off_g = 0, off_Gping = 0, off_Gpong = 0, off_J = 0, off_gram_r = 0, off_part = 0;
+  size_t off_gt = 0;              // the inside-out kernel's copy of a cotangent [M, C, O, Dp]
   long long part_capacity = 0;    // floats of the split-K partial buffer
 };
 
@@ -329,6 +330,9 @@ static int check_index_range(const ntk_handle& t, long long n1, long long n2) {
       const long long plane_out = smul({hh, ww, c});
       need(smul(M, plane_out), "layer " + std::to_string(l) + " outputs [n1 + n2, H, W, C]");
       need(smul({M, O, plane_out}), "layer " + std::to_string(l) + " cotangents [(n1 + n2) O, H, W, C]");
+      if (L.kind == NTK_CONV3X3_SAME || L.kind == NTK_CONV1X1)   // the inside-out copy [M, C, O, Dp]
+        need(smul({M, O, c, 16 * ((smul(hh, ww) + 15) / 16)}),
+             "layer " + std::to_string(l) + " cotangent copy of the inside-out order");
     }
     need(smul({M, O, ktot}), "weight-space cotangent columns J [(n1 + n2) O, K]");
     need(smul(sadd(1024, tiles(smul(n1, O), smul(n2, O))), T * T), "split-K partials");
@@ -467,6 +471,16 @@ static void plan_cnn(ntk_handle* h) {
   h->Ktot = kt;
   h->off_J = take(Mmax * O * (size_t)kt);
   h->off_gram_r = take((size_t)h->max_n1 * h->max_n2);
+  {   // the largest cotangent copy of a convolution the inside-out order can take
+    long long gt = 0;
+    for (int l = 0; l < nc; ++l) {
+      const int kind = h->layers[l].kind;
+      const int Dl = h->bh[l] * h->bw[l];
+      if ((kind == NTK_CONV3X3_SAME || kind == NTK_CONV1X1) && pairsum_supported(Dl))
+        gt = std::max(gt, pairsum_gt_floats((long long)Mmax, (int)O, Dl, h->ch[l + 1]));
+    }
+    h->off_gt = gt ? take((size_t)gt) : 0;
+  }
   const int T = splitk_tile();
   const size_t tiles_max = (size_t)((h->max_n1 * O + T - 1) / T) * ((h->max_n2 * O + T - 1) / T);
   // >= R1max * R2max: the split-K plan never holds fewer than one partial product; the lean plan
@@ -943,12 +957,19 @@ static int cnn_forward(ntk_handle* h, const float* const* params, const float* X
   return NTK_OK;
 }
 
-// Time per FLOP of the inside-out pair sums (fp32 vector FMAs) relative to the outside-in path
-// (MFMA products), measured on MI355X with 4-layer 64-channel CNNs: the kernel for images of at
-// most 16 pixels (k_conv_pairsum_small) 14 TFLOP/s on 4x4 images, the general one
-// (k_conv_pairsum) 3.0-3.3 on 5x5 to 8x8 images, against 129 for the matrix-core path.  The cost
-// model compares times, not FLOP counts.
-constexpr double kInsideOutFlopCostSmall = 9.0, kInsideOutFlopCost = 40.0;
+// The inside-out order's cost for the order choice: the matrix-core work its kernel executes
+// (pixels padded to Dp = 16 ceil(D / 16), outputs to 16 ceil(Oe / 16), input channels to 16 per
+// step; per block of 16 x 16 outputs the pixel Gram Dp^2 Cin, the product with the patch-pair Gram
+// 16 Dp^2 C and the output product 256 Dp C, multiply-adds per input pair), times its measured
+// time per multiply-add relative to the outside-in products.
+constexpr double kInsideOutTimeWeight = 1.0;
+
+static double inside_out_cost(double pairs, int D, int Cin, int C, int Oe, bool trace) {
+  const double Dp = 16.0 * ((D + 15) / 16), Ci = 16.0 * ((Cin + 15) / 16), nob = (Oe + 15) / 16;
+  const double gram_blocks = trace ? 1 : nob * nob, out_blocks = trace ? nob : nob * nob;
+  return kInsideOutTimeWeight * pairs *
+         (gram_blocks * Dp * Dp * Ci + out_blocks * (16.0 * Dp * Dp * C + 256.0 * Dp * C));
+}
 
 static int compute_cnn(ntk_handle* h, const float* const* params, const float* X1, int n1,
                        const float* X2, int n2, float* theta) {
@@ -978,14 +999,13 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
     const int kind = h->layers[l].kind;
     if ((kind != NTK_CONV3X3_SAME && kind != NTK_CONV1X1) || h->opt_method == NTK_METHOD_JACOBIAN) continue;
     const double F = kind == NTK_CONV1X1 ? 1 : 9;
-    const double Dl = (double)h->bh[l] * h->bw[l];
-    const bool io_ok = pairsum_supported(h->bh[l] * h->bw[l], Oe) != 0;
+    const int Dl = h->bh[l] * h->bw[l];
+    const bool io_ok = pairsum_supported(Dl) != 0;
     const double Cin = h->ch[l], Co = h->ch[l + 1];
     const double oi = pairs * Oc * F * Cin * Co + (double)M * Oe * Dl * F * Cin * Co;
-    const double io = (Dl <= 16 ? kInsideOutFlopCostSmall : kInsideOutFlopCost) * pairs *
-                      (Dl * Dl * F * Cin + (double)Oe * Dl * Dl * Co + Oc * Dl * Co);
+    const double io = inside_out_cost(pairs, Dl, h->ch[l], h->ch[l + 1], Oe, trace);
     if (h->opt_conv_order == NTK_CONV_ORDER_INSIDE_OUT) {
-      if (!io_ok) return fail(h, NTK_E_UNSUPPORTED, "the inside-out order needs D <= 64 pixels and O <= 64");
+      if (!io_ok) return fail(h, NTK_E_UNSUPPORTED, "the inside-out order needs images of at most 64 pixels");
       inside[l] = 1;
     } else if (h->opt_conv_order == NTK_CONV_ORDER_AUTO) {
       inside[l] = (io_ok && io < oi) ? 1 : 0;
@@ -1070,16 +1090,9 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
     // Gcur: the cotangent of layer l's pre-activation (of its output for a pool), [M*Oe, ., ., cout]
     if (L.kind == NTK_CONV3X3_SAME) {
       if (inside[l]) {
-        PairLayerList pl{};
-        pl.count = 1;
-        pl.h[0] = hptr(l);
-        pl.G[0] = Gcur;
-        pl.Cin[0] = cin;
-        pl.C[0] = cout;
-        pl.taps[0] = 9;
         prof_begin(P, s, KC_CONV_PAIRSUM);
-        e = launch_conv_pairsum(s, pl, n1, n2, n2_off, Oe, Hl, Wl, F(h->off_gram_r), theta_written ? 1 : 0,
-                                trace ? 1 : 0, diag ? 1 : 0, theta);
+        e = launch_conv_pairsum(s, hptr(l), Gcur, F(h->off_gt), n1, n2, n2_off, Oe, Hl, Wl, cin, cout, 9,
+                                F(h->off_gram_r), theta_written ? 1 : 0, trace ? 1 : 0, diag ? 1 : 0, theta);
         prof_end(P, s, KC_CONV_PAIRSUM);
         if (e != hipSuccess) return hip_fail(h, e, "conv inside-out pair sum");
         theta_written = true;
@@ -1097,16 +1110,9 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
       }
     } else if (L.kind == NTK_CONV1X1) {
       if (inside[l]) {
-        PairLayerList pl{};
-        pl.count = 1;
-        pl.h[0] = hptr(l);
-        pl.G[0] = Gcur;
-        pl.Cin[0] = cin;
-        pl.C[0] = cout;
-        pl.taps[0] = 1;
         prof_begin(P, s, KC_CONV_PAIRSUM);
-        e = launch_conv_pairsum(s, pl, n1, n2, n2_off, Oe, Hl, Wl, F(h->off_gram_r), theta_written ? 1 : 0,
-                                trace ? 1 : 0, diag ? 1 : 0, theta);
+        e = launch_conv_pairsum(s, hptr(l), Gcur, F(h->off_gt), n1, n2, n2_off, Oe, Hl, Wl, cin, cout, 1,
+                                F(h->off_gram_r), theta_written ? 1 : 0, trace ? 1 : 0, diag ? 1 : 0, theta);
         prof_end(P, s, KC_CONV_PAIRSUM);
         theta_written = true;
       } else {

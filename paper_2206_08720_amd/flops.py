@@ -87,27 +87,36 @@ def _weight_cols(kind, cin, cout):
             "scale": cout}.get(kind, 0)
 
 
-# Time per FLOP of the inside-out pair sums relative to the outside-in matrix-core path, as in
-# the library's cost model: images of at most 16 pixels, and larger ones.
-INSIDE_OUT_FLOP_COST_SMALL, INSIDE_OUT_FLOP_COST = 9.0, 40.0
+# Time per executed matrix-core multiply-add of the inside-out kernel relative to the outside-in
+# products, as in the library's cost model.
+INSIDE_OUT_TIME_WEIGHT = 1.0
 
 
-def _inside_out(kind, D, cin, cout, M, Oe, Oc, gpairs, order):
+def inside_out_cost(pairs, D, cin, cout, Oe, trace=False):
+    """The library's cost of the inside-out order of one convolution: the multiply-adds its
+    matrix-core kernel executes, with the pixels padded to Dp = 16 ceil(D / 16), the outputs to
+    blocks of 16 and the input channels to steps of 16 (per block of 16 x 16 outputs: the pixel
+    Gram Dp^2 Cin, the product with the patch-pair Gram 16 Dp^2 C, the output product 256 Dp C),
+    times INSIDE_OUT_TIME_WEIGHT."""
+    Dp, ci, nob = 16 * -(-D // 16), 16 * -(-cin // 16), -(-Oe // 16)
+    gram_blocks, out_blocks = (1, nob) if trace else (nob * nob, nob * nob)
+    return INSIDE_OUT_TIME_WEIGHT * pairs * (gram_blocks * Dp * Dp * ci
+                                             + out_blocks * (16 * Dp * Dp * cout + 256 * Dp * cout))
+
+
+def _inside_out(kind, D, cin, cout, M, Oe, Oc, gpairs, order, trace=False):
     """Whether a 3x3 or pointwise convolution is contracted inside-out: forced by `order`, or
     (order "auto") the library's per-layer choice by the cost model of the appendix "CNN NTK
-    Complexity": outside-in gpairs Oc F Cin Cout plus forming J, M Oe D F Cin Cout, against
-    inside-out gpairs (D^2 F Cin + Oe D^2 Cout + Oc D Cout) times its measured time per FLOP
-    (INSIDE_OUT_FLOP_COST_SMALL for D <= 16, else INSIDE_OUT_FLOP_COST), inside-out only for
-    D <= 64 and Oe <= 64 (the pair-sum kernels' limits)."""
+    Complexity": outside-in gpairs Oc F Cin Cout plus forming J, M Oe D F Cin Cout, against the
+    inside-out kernel's cost (inside_out_cost); inside-out only for images of at most 64 pixels
+    (the kernel's limit)."""
     if kind not in ("conv3x3", "conv1x1") or order == "outside_in":
         return False
     if order == "inside_out":
         return True
     F = 9 if kind == "conv3x3" else 1
     oi = gpairs * Oc * F * cin * cout + M * Oe * D * F * cin * cout
-    w = INSIDE_OUT_FLOP_COST_SMALL if D <= 16 else INSIDE_OUT_FLOP_COST
-    io = w * gpairs * (D * D * F * cin + Oe * D * D * cout + Oc * D * cout)
-    return D <= 64 and Oe <= 64 and io < oi
+    return D <= 64 and inside_out_cost(gpairs, D, cin, cout, Oe, trace) < oi
 
 
 def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", batch="full"):
@@ -119,7 +128,10 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
     M Oe D C.  The contraction covers every weight-space column (9 Cin Cout, 9 C, C, and C per
     bias).  `order` is "outside_in", "inside_out" or "auto" (the library's
     per-layer choice, _inside_out) for the 3x3 and pointwise convolutions; a layer contracted
-    inside-out forms no J columns and counts its pair sums in the stage "pairsum"."""
+    inside-out forms no J columns and counts its own operations in the stage "pairsum": the
+    pixel Gram D^2 Cin, the F D^2 tap sums of the patch-pair Gram (one FLOP each), and the
+    products Oe D^2 Cout and Oc D Cout (the form of the appendix "CNN NTK Complexity" with the
+    patch-pair Gram built from the pixel Gram instead of D^2 F Cin patch products)."""
     layers = spec["layers"]
     sp, C = _spatial_layers(spec)
     O = layers[-1]["out"]
@@ -136,12 +148,13 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
             fwd += 2.0 * M * D * F * cin * cout + (1.0 * M * D * cout if bias else 0.0)
             if i >= 1:
                 bwd += 2.0 * M * Oe * D * F * cout * cin
-            if not _inside_out(k, D, cin, cout, M, Oe, Oc, gpairs, order):
+            if not _inside_out(k, D, cin, cout, M, Oe, Oc, gpairs, order, output == "trace"):
                 wg += 2.0 * M * (Oe * cout) * (F * cin) * D
                 cols += F * cin * cout
-            else:  # inside-out: patch Gram, one-sided cotangent contraction, then the O x O product
-                # (every input pair, also on the symmetric schedule)
-                io += 2.0 * gpairs * (D * D * F * cin + Oe * D * D * cout + Oc * D * cout)
+            else:  # inside-out (every input pair, also on the symmetric schedule): the pixel Gram,
+                # the F-tap sums forming the patch-pair Gram, the one-sided cotangent product and
+                # the O x O product
+                io += gpairs * (2.0 * D * D * cin + F * D * D + 2.0 * Oe * D * D * cout + 2.0 * Oc * D * cout)
         elif k == "dwconv3x3":
             sfwd += 2.0 * M * D * 9 * cout + (1.0 * M * D * cout if bias else 0.0)
             if i >= 1:

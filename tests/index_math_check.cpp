@@ -8,6 +8,7 @@
 //     covers every (tile, layer) unit exactly once, writes each finished tile exactly once,
 //     never writes a partial-buffer slot twice, and its fixup reads exactly the slots that
 //     hold the split tile's partial sums, each layer once.
+#include <algorithm>
 #include <cstdint>
 #include <cstdio>
 #include <cstdlib>
@@ -194,10 +195,48 @@ static void check_xcd_sample_tile() {
     }
 }
 
+// The per-XCD block ranges: a grid of 8 * ceil(n / 8) workgroups visits every block exactly once,
+// and the blocks of one XCD form one contiguous range in block order.
+static void check_xcd_block() {
+  long long launches = 0;
+  std::vector<int> sizes;
+  for (int n = 1; n <= 4096; ++n) sizes.push_back(n);
+  for (int n : {8191, 8192, 8193, 65535, 65536, 1 << 20, (1 << 20) + 5}) sizes.push_back(n);
+  for (int n : sizes) {
+    const int grid = 8 * ((n + 7) / 8);
+    std::vector<char> seen(n, 0);
+    std::vector<int> lo(8, n), hi(8, -1);
+    int visited = 0;
+    for (int id = 0; id < grid; ++id) {
+      int blk = -1;
+      if (!xcd_block(id, n, blk)) continue;
+      CHECK(blk >= 0 && blk < n, "xcd_block n=%d id=%d -> %d", n, id, blk);
+      CHECK(!seen[blk]++, "xcd_block n=%d visits block %d twice", n, blk);
+      const int x = id & 7;
+      lo[x] = std::min(lo[x], blk);
+      hi[x] = std::max(hi[x], blk);
+      ++visited;
+    }
+    CHECK(visited == n, "xcd_block n=%d visits %d blocks", n, visited);
+    for (int x = 0; x < 8; ++x)
+      if (hi[x] >= 0) {
+        int cnt = 0;
+        for (int id = x; id < grid; id += 8) {
+          int blk;
+          cnt += xcd_block(id, n, blk) ? 1 : 0;
+        }
+        CHECK(hi[x] - lo[x] + 1 == cnt, "xcd_block n=%d: XCD %d range not contiguous", n, x);
+      }
+    ++launches;
+  }
+  std::printf("xcd_block: %lld grids\n", launches);
+}
+
 int main() {
   check_fastdiv();
   check_tile_orders();
   check_xcd_sample_tile();
+  check_xcd_block();
   long long n = 0;
   const int Ps[] = {16, 24, 32, 64, 80, 128, 256, 304, 512};
   const int Ls[] = {1, 2, 3, 5, 8, 9, 17};

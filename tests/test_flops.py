@@ -48,19 +48,20 @@ def test_cnn_terms_match_complexities_cnn():
     # outside-in: N^2 O^2 F W^2 per layer for J1 J2^T, plus N O D F W^2 to form J
     assert oi["contraction"] == 2 * (N * O) * (N * O) * 2 * Fs * W * W
     assert oi["wgrad"] == 2 * (2 * N) * O * W * Fs * W * D * 2
-    # inside-out: N^2 (D^2 F W + O D^2 W + O^2 D W) per layer, and no J columns
-    assert io["pairsum"] == 2 * 2 * N * N * (D * D * Fs * W + O * D * D * W + O * O * D * W)
+    # inside-out: N^2 (D^2 F W + O D^2 W + O^2 D W) multiply-adds per layer in the paper's table;
+    # here the patch-pair Gram comes from the pixel Gram (D^2 W) and F D^2 tap sums; no J columns
+    assert io["pairsum"] == 2 * N * N * (2 * D * D * W + Fs * D * D + 2 * O * D * D * W + 2 * O * O * D * W)
     assert io["contraction"] == 0 and "wgrad" not in io
 
 
 def test_auto_order_is_the_cost_model():
     """order="auto" mirrors the library's per-layer choice: on 4x4 images the three 64->64
-    convolutions go inside-out (the pair sums ~9x cheaper), the 3-channel one stays outside-in;
+    convolutions go inside-out (several times cheaper), the 3-channel one stays outside-in;
     on 32x32 images every layer stays outside-in."""
     spec, _, _, _ = wl.make_workload("cnn4_c64_4x4")
     N, O, D, W = 64, 10, 16, 64
     a = cnn_flops(spec, N, N, order="auto")
-    assert a["pairsum"] == 3 * 2 * N * N * (D * D * 9 * W + O * D * D * W + O * O * D * W)
+    assert a["pairsum"] == 3 * N * N * (2 * D * D * W + 9 * D * D + 2 * O * D * D * W + 2 * O * O * D * W)
     assert a["contraction"] == 2 * N * N * O * O * 9 * 3 * W
     assert a["wgrad"] == 2 * (2 * N) * O * W * 9 * 3 * D
     oi = cnn_flops(spec, N, N, order="outside_in")

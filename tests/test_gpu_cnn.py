@@ -128,6 +128,13 @@ ORDER_CASES = [
     ("D=4", wl.cnn_spec("o4", (2, 2), 3, [16, 16], 10), 6, 5),
     ("D=16", wl.cnn_spec("o16", (4, 4), 3, [64, 64, 64], 10), 8, 7),
     ("D=16 erf, C=20, O=7", wl.cnn_spec("o16e", (4, 4), 5, [20, 20], 7, act="erf"), 5, 9),
+    # the matrix-core pair kernel's other pixel blocks (Dp = 32, 48, 64), ragged images, odd
+    # channel counts and several blocks of 16 outputs (O = 20: 2 x 2 output blocks, O = 33: 3 x 3)
+    ("D=36 (6x6), C=24", wl.cnn_spec("o36", (6, 6), 3, [24, 24], 10), 7, 6),
+    ("D=64 (8x8), C=32, O=5", wl.cnn_spec("o64", (8, 8), 3, [32, 32], 5), 5, 6),
+    ("D=49 (7x7), O=20", wl.cnn_spec("o49", (7, 7), 3, [16, 16], 20), 5, 4),
+    ("D=9 (3x3), odd channels, O=33", wl.cnn_spec("o9", (3, 3), 5, [7, 9], 33, act="erf"), 4, 5),
+    ("D=30 (5x6), 3 layers, O=17", wl.cnn_spec("o30", (5, 6), 2, [12, 20, 16], 17), 3, 7),
 ]
 
 
@@ -173,7 +180,7 @@ def test_inside_out_rejects_large_images_without_enqueuing():
     from paper_2206_08720_amd import _lib
     from paper_2206_08720_amd.ntk import NTK
     from tests.gpu_helpers import to_dev
-    spec = wl.cnn_spec("big", (9, 9), 3, [8], 2)         # D = 81 > 64
+    spec = wl.cnn_spec("big", (9, 9), 3, [8], 2)         # D = 81 > 64 pixels
     params = to_dev(wl.make_params(spec, 1, "2/fan_in"))
     X = to_dev([wl.make_inputs(spec, 2, 2)])[0]
     h = NTK(spec, 2, 2)

@@ -87,6 +87,8 @@ CNN_CASES = [
     ("inside-out D=16", wl.cnn_spec("w2", (4, 4), 3, [16, 16], 6), "inside_out", 7, 7),
     ("auto, mixed orders D=16", wl.cnn_spec("w3", (4, 4), 3, [64, 64, 64], 10), "auto", 5, 5),
     ("erf inside-out D=9, O=3", wl.cnn_spec("w4", (3, 3), 2, [10], 3, act="erf"), "inside_out", 4, 4),
+    ("inside-out D=25, O=20 (two output blocks)", wl.cnn_spec("w5", (5, 5), 3, [12, 12], 20), "inside_out", 5, 5),
+    ("inside-out D=64, O=18", wl.cnn_spec("w6", (8, 8), 4, [16], 18), "inside_out", 6, 6),
 ]
 
 
