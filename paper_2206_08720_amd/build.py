@@ -25,9 +25,11 @@ ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
           "-Wno-unused-result", "-I", os.path.join(PKG, "..", "include")]
-# Per-file extras.  diag.hip: keep MFMA accumulators in the VGPR form, so that the fp64
+# Per-file extras.  Keep MFMA accumulators in the VGPR form: in diag.hip so that the fp64
 # chains are not copied between accumulation and architectural registers every iteration.
-PER_FILE = {"diag.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+PER_FILE = {"diag.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+            # the inside-out kernel feeds an MFMA's result to the next MFMA as an A operand
+            "kernels_pairsum.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _run(cmd):
