@@ -387,7 +387,39 @@ __global__ void k_transpose(const float* __restrict__ W, int R, int C, float* __
   }
 }
 
+// The same for R and C multiples of 4 with 16-byte aligned rows: 64 x 64 tiles, every global
+// access a float4 (a row quad of W read, a column quad of W written as a row quad of Wt).
+__global__ void __launch_bounds__(256) k_transpose4(const float* __restrict__ W, int R, int C, float* __restrict__ Wt) {
+  __shared__ float tile[64][65];
+  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
+  const int q = threadIdx.x & 15, rr = threadIdx.x >> 4;   // quad within a 64-wide row, row 0..15
+#pragma unroll
+  for (int j = 0; j < 64; j += 16) {
+    const int r = r0 + rr + j, c = c0 + 4 * q;
+    if (r < R && c < C) {
+      const float4 v = *reinterpret_cast<const float4*>(W + (long long)r * C + c);
+      tile[rr + j][4 * q] = v.x;
+      tile[rr + j][4 * q + 1] = v.y;
+      tile[rr + j][4 * q + 2] = v.z;
+      tile[rr + j][4 * q + 3] = v.w;
+    }
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 64; j += 16) {
+    const int c = c0 + rr + j, r = r0 + 4 * q;
+    if (r < R && c < C) {
+      const float4 v = {tile[4 * q][rr + j], tile[4 * q + 1][rr + j], tile[4 * q + 2][rr + j], tile[4 * q + 3][rr + j]};
+      *reinterpret_cast<float4*>(Wt + (long long)c * R + r) = v;
+    }
+  }
+}
+
 hipError_t launch_transpose(hipStream_t s, const float* W, int R, int C, float* Wt) {
+  if (R % 4 == 0 && C % 4 == 0 && vec_ok(W, C, C) && vec_ok(Wt, R, R)) {
+    k_transpose4<<<dim3(cdiv(C, 64), cdiv(R, 64)), dim3(256), 0, s>>>(W, R, C, Wt);
+    return hipGetLastError();
+  }
   k_transpose<<<dim3(cdiv(C, 32), cdiv(R, 32)), dim3(256), 0, s>>>(W, R, C, Wt);
   return hipGetLastError();
 }

@@ -89,6 +89,15 @@ def test_large_fcn_full_size(name, rows1, rows2, outs):
     cs, nw = errors(got[np.ix_(rows1, rows2, outs, outs)], sub, s1, s2)
     report(f"{name} sampled entries vs JC", cs, nw)
     assert cs <= TOL and nw <= TOL
+    # the stored block of the Jacobian contraction itself (tests/golden/make_jc_blocks.py): every
+    # output, samples spread over the batches (for the depth-8 network one in every 128-row
+    # tile of the contraction's rows (n, o))
+    blk = np.load(os.path.join(os.path.dirname(__file__), "golden", f"jc_block_{name}.npz"))
+    r1, r2 = blk["rows1"], blk["rows2"]
+    cs, nw = errors(got[np.ix_(r1, r2)], blk["theta"].astype(np.float64), blk["sq1"].astype(np.float64),
+                    blk["sq2"].astype(np.float64))
+    report(f"{name} {len(r1)} x {len(r2)} samples, all outputs, vs stored JC block", cs, nw)
+    assert cs <= TOL and nw <= TOL
 
 
 EDGE = [
