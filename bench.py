@@ -110,6 +110,21 @@ def measured_traffic(name, kernel):
             + rec["write_size_kib_per_launch"] * rec["write_scale"]) * 1024.0
 
 
+def measured_mfma_busy(name, kernel):
+    """Fraction of the class's kernel time the matrix cores were busy, from the committed
+    SQ_VALU_MFMA_BUSY_CYCLES / SQ_BUSY_CU_CYCLES record (a CU has 4 SIMDs: busy fraction =
+    MFMA-busy cycles / (4 x CU-busy cycles)), or None when the record is for another
+    kernel/workload or the kernel sources changed since it was taken."""
+    path = os.path.join(ROOT, "profiles", f"{name}_mfma_busy.json")
+    if not os.path.exists(path):
+        return None
+    rec = json.load(open(path))
+    cls = rec.get("classes", {}).get(kernel)
+    if cls is None or cls.get("sources_sha256_16") != sources_sha16(cls.get("kernel_source", "kernels_fcn.hip")):
+        return None
+    return cls["mfma_busy"]
+
+
 def cpu_baseline(name, n, n1_full, n2_full):
     """Time the fp64 Jacobian-contraction oracle on Theta(X1[:n], X2[:n]) (after an untimed
     one-sample call), and extrapolate to the full Theta: the per-sample part (forward, O
@@ -277,6 +292,7 @@ def main():
     roofline = {"kernel": dom, "bound": "alu" if alu else "mfma", "achieved": achieved,
                 "peak": peak, "unit": "TFLOP/s",
                 "frac": achieved / peak, "traffic": measured_traffic(name, dom),
+                "mfma_busy": measured_mfma_busy(name, dom),
                 "flop_per_launch": flop_per_launch, "avg_launch_ms": avg_ms}
 
     h.close()
