@@ -13,9 +13,10 @@ records of one ntk_compute instead (NTK_OPT_GRAPH: every kernel of the step runs
 every replay, on the same device buffers; the graph is recorded by one untimed call before the
 warm-up, like the handle's set-up).
 
-roofline: the dominant kernel class (largest time share) is timed live with HIP
-events recorded by the library around each launch on its own stream during the timed steps
-(with --graph: during as many further eager steps);
+The steps that give the throughput run without per-kernel events.  roofline: the dominant
+kernel class (largest time share) is then timed live with HIP events recorded by the library
+around each launch on its own stream, over as many further eager steps (ms_per_step_profiled
+is their mean step time);
 `achieved` = its algorithmic FLOPs per launch / average launch time.
 cpu_baseline: the fp64 Jacobian-contraction oracle on a bounded sample of the same
 workload (a few samples of X1 x X2, all outputs), timed on this host.
@@ -34,9 +35,7 @@ sys.path.insert(0, ROOT)
 
 METRIC = "NTK entries/sec (N1·N2·O²) and fp32 MFMA TFLOP/s, FCN depth 8 width 2048"
 FP32_MFMA_PEAK_TFLOPS = 157.3      # MI355X dense fp32 matrix peak
-# fp32 vector FMAs without the packed forms (the library is compiled with them disabled):
-# 256 CUs x 4 SIMDs x 16 lanes x 2 FLOP x 2.4 GHz = 78.6 TFLOP/s (the packed forms double it)
-FP32_VALU_PEAK_TFLOPS = 78.6
+FP64_MFMA_PEAK_TFLOPS = 78.6       # MI355X dense fp64 matrix peak (the forward passes)
 HBM_PEAK_GBS = 8000.0
 
 # kernel class -> stage of the FLOP counter
@@ -45,8 +44,6 @@ STAGE_OF = {"dense_fwd": "forward", "dense_bwd": "backward", "gram": "gram",
             "conv_wgrad": "wgrad", "ntk_splitk": "contraction", "conv_pairsum": "pairsum",
             "ntk_diag": "contraction", "struct_fwd": "struct_forward",
             "struct_bwd": "struct_backward", "struct_wgrad": "struct_wgrad"}
-# stages computed with fp32 vector FMAs rather than MFMA: the inside-out pair sums
-VALU_STAGES = {"pairsum"}
 # kernel class -> stage of the NTK-vector product's counter
 VP_STAGE_OF = {"dense_fwd": "forward", "dense_bwd": "vjp_backward", "gram": "gram_products",
                "conv_fwd": "forward_and_jvp", "conv_bwd": "vjp_backward",
@@ -251,11 +248,14 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    ms, step_ms, wall, prof = timed(args.steps, profiled=not use_graph)
-    if use_graph:                              # per-kernel timing from eager steps
+    # the throughput comes from steps without the per-kernel events (each event record costs a
+    # few microseconds of host and GPU time, a third of a step on the smallest workloads); the
+    # kernel classes are then timed over as many eager steps with the library's HIP events
+    ms, step_ms, wall, _ = timed(args.steps, profiled=False)
+    if use_graph:
         h.set_option(_lib.NTK_OPT_GRAPH, 0)
         step()
-        _, _, _, prof = timed(args.steps, profiled=True)
+    ms_profiled, _, _, prof = timed(args.steps, profiled=True)
     ms_median = step_ms[len(step_ms) // 2] if len(step_ms) % 2 else \
         0.5 * (step_ms[len(step_ms) // 2 - 1] + step_ms[len(step_ms) // 2])
 
@@ -285,11 +285,9 @@ def main():
     avg_ms = tot / cnt
     flop_per_launch = fl[stage_of[dom]] / (cnt / args.steps)
     achieved = flop_per_launch / (avg_ms * 1e-3) / 1e12
-    # a kernel class of fp32 vector FMAs is bound by the ALU (FP32_VALU_PEAK_TFLOPS), the others
-    # by the matrix cores
-    alu = stage_of[dom] in VALU_STAGES
-    peak = FP32_VALU_PEAK_TFLOPS if alu else FP32_MFMA_PEAK_TFLOPS
-    roofline = {"kernel": dom, "bound": "alu" if alu else "mfma", "achieved": achieved,
+    # every priced class runs on the matrix cores: the forward in fp64, the rest in fp32
+    peak = FP64_MFMA_PEAK_TFLOPS if stage_of[dom] == "forward" else FP32_MFMA_PEAK_TFLOPS
+    roofline = {"kernel": dom, "bound": "mfma", "achieved": achieved,
                 "peak": peak, "unit": "TFLOP/s",
                 "frac": achieved / peak, "traffic": measured_traffic(name, dom),
                 "mfma_busy": measured_mfma_busy(name, dom),
@@ -307,7 +305,7 @@ def main():
         "value": value, "unit": "NTK entries/s" if args.op == "ntk" else "(Theta v) entries/s",
         "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup, "ms_per_step": ms,
-        "ms_per_step_median": ms_median, "ms_per_step_min": step_ms[0],
+        "ms_per_step_median": ms_median, "ms_per_step_min": step_ms[0], "ms_per_step_profiled": ms_profiled,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic (seeded N(0,1) inputs, He-init weights)",
         "config": {"workload": name, "n1": n1, "n2": n2, "O": O,
