@@ -742,8 +742,8 @@ __host__ inline bool dma_span_ok(long long ld, long long K, int rows) {
 }
 
 // K loop over [k_begin, k_end) (k_begin a multiple of 32; a ragged last K tile is the issuers'
-// business) for the tile (m0, n0), with NSTAGE LDS stages (2: tile kt+1 in flight during tile
-// kt; 3: tiles kt+1 and kt+2).  One barrier per K tile, placed before the tile's last MFMA
+// business) for the tile (m0, n0), with NSTAGE LDS stages (tiles kt+1 .. kt+NSTAGE-1 in flight
+// during tile kt).  One barrier per K tile, placed before the tile's last MFMA
 // block: by then every wave holds that block's fragments in registers (so the stage may be
 // overwritten afterwards) and has seen its own loads of tile kt+1 land, and the fragments of
 // tile kt+1's first block are read while the last block's MFMAs run.  Ends with a barrier, so
@@ -764,7 +764,7 @@ __device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, in
   const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
   const int nk = (k_end - k_begin + 31) / 32;
   if (nk <= 0) return;
-  static_assert(NSTAGE == 2 || NSTAGE == 3, "two or three LDS stages");
+  static_assert(NSTAGE >= 2 && NSTAGE <= 4, "two to four LDS stages");
   ia.prepare(m0, wave, lane);
   ib.prepare(n0, wave, lane);
   auto stage = [&](int kt) { return smem + (kt % NSTAGE) * STAGE; };
@@ -773,11 +773,12 @@ __device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, in
     ia.template issue<Cfg::WAVES>(k_begin + kt * 32, st, wave, lane);
     ib.template issue<Cfg::WAVES>(k_begin + kt * 32, st + TA::FLOATS, wave, lane);
   };
-  issue(0);
-  if (NSTAGE == 3 && nk > 1) issue(1);
-  // tile 0 in LDS (with three stages tile 1's loads may stay in flight); a bare s_barrier (no
-  // fence, which would drain every outstanding load) makes it visible to every wave
-  wait_vmcnt_dyn(NSTAGE == 3 && nk > 1 ? PER_TILE : 0);
+  // tiles 0 .. NSTAGE - 2 in flight
+  const int pre = nk < NSTAGE - 1 ? nk : NSTAGE - 1;
+  for (int j = 0; j < pre; ++j) issue(j);
+  // tile 0 in LDS (the later tiles' loads may stay in flight: loads complete in order); a bare
+  // s_barrier (no fence, which would drain every outstanding load) makes it visible to every wave
+  wait_vmcnt_dyn((pre - 1) * PER_TILE);
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_sched_barrier(0);
   typename MB::Frag f[2];
@@ -793,9 +794,10 @@ __device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, in
       __builtin_amdgcn_sched_barrier(0);
     }
     if (kt + 1 < nk) {
-      // this wave's loads of tile kt+1 landed (with three stages tile kt+2's may stay in
+      // this wave's loads of tile kt+1 landed (those of tiles kt+2 .. kt+NSTAGE-1 may stay in
       // flight) and its reads of tile kt returned; after the barrier every wave's have
-      wait_vmcnt_lgkm0_dyn(NSTAGE == 3 && kt + 2 < nk ? PER_TILE : 0);
+      const int later = nk - kt - 2 < NSTAGE - 2 ? nk - kt - 2 : NSTAGE - 2;
+      wait_vmcnt_lgkm0_dyn((later > 0 ? later : 0) * PER_TILE);
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
       const float* sn = stage(kt + 1);

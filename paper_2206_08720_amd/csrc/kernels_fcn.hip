@@ -24,6 +24,9 @@ using CfgSK = CfgBig8;                          // stream-K contraction
 // The stream-K contraction keeps two workgroups per compute unit (two LDS stages each, so
 // both fit the 160 KB of LDS): one workgroup's barrier waits are covered by the other's MFMAs.
 constexpr int kSkPerCu = 2, kSkStages = 2;
+// LDS stages of the direct-to-LDS loop of the layer-split contraction (64 x 64 tiles): two
+// stages (32 KB) let four workgroups share a compute unit
+constexpr int kSplitStages = 2;
 // the forward splits K (up to kFwdMaxSplits ways) below kFwdSplitTiles output tiles
 constexpr int kFwdSplitTiles = 256, kFwdMaxSplits = 8;
 using CfgSmall = TileCfg<64, 64, 32, 32, 32>;   // 4 waves, 32x32 per wave
@@ -326,6 +329,7 @@ hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, cons
     return v ? dense_bwd_cfg<CfgBig8, true>(s, G, Wt, dphi, R, N, K, O, out)
              : dense_bwd_cfg<CfgBig8, false>(s, G, Wt, dphi, R, N, K, O, out);
   }
+  if (v && K % 32 == 0 && dma_span_ok(K, K, 256)) return dense_bwd_cfg<CfgSmall, true, true>(s, G, Wt, dphi, R, N, K, O, out);
   return v ? dense_bwd_cfg<CfgSmall, true>(s, G, Wt, dphi, R, N, K, O, out)
            : dense_bwd_cfg<CfgSmall, false>(s, G, Wt, dphi, R, N, K, O, out);
 }
@@ -372,9 +376,9 @@ hipError_t launch_bwd_seed(hipStream_t s, const float* W, const float* dphi, int
   return hipGetLastError();
 }
 
-__global__ void k_transpose(const float* __restrict__ W, int R, int C, float* __restrict__ Wt) {
-  __shared__ float tile[32][33];
-  const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+// One 32 x 32 tile of Wt = W^T (W is R x C, row-major), staged through LDS.
+__device__ __forceinline__ void transpose_tile(const float* __restrict__ W, int R, int C, float* __restrict__ Wt,
+                                               int c0, int r0, float (*tile)[33]) {
   const int tx = threadIdx.x & 31, ty = threadIdx.x >> 5;  // 256 threads: 32 x 8
   for (int j = ty; j < 32; j += 8) {
     const int r = r0 + j, c = c0 + tx;
@@ -387,11 +391,10 @@ __global__ void k_transpose(const float* __restrict__ W, int R, int C, float* __
   }
 }
 
-// The same for R and C multiples of 4 with 16-byte aligned rows: 64 x 64 tiles, every global
+// The same for R and C multiples of 4 with 16-byte aligned rows: a 64 x 64 tile, every global
 // access a float4 (a row quad of W read, a column quad of W written as a row quad of Wt).
-__global__ void __launch_bounds__(256) k_transpose4(const float* __restrict__ W, int R, int C, float* __restrict__ Wt) {
-  __shared__ float tile[64][65];
-  const int c0 = blockIdx.x * 64, r0 = blockIdx.y * 64;
+__device__ __forceinline__ void transpose_tile4(const float* __restrict__ W, int R, int C, float* __restrict__ Wt,
+                                                int c0, int r0, float (*tile)[65]) {
   const int q = threadIdx.x & 15, rr = threadIdx.x >> 4;   // quad within a 64-wide row, row 0..15
 #pragma unroll
   for (int j = 0; j < 64; j += 16) {
@@ -415,12 +418,54 @@ __global__ void __launch_bounds__(256) k_transpose4(const float* __restrict__ W,
   }
 }
 
+__global__ void __launch_bounds__(256) k_transpose(const float* __restrict__ W, int R, int C, float* __restrict__ Wt) {
+  __shared__ float tile[32][33];
+  transpose_tile(W, R, C, Wt, blockIdx.x * 32, blockIdx.y * 32, tile);
+}
+
+__global__ void __launch_bounds__(256) k_transpose4(const float* __restrict__ W, int R, int C, float* __restrict__ Wt) {
+  __shared__ float tile[64][65];
+  transpose_tile4(W, R, C, Wt, blockIdx.x * 64, blockIdx.y * 64, tile);
+}
+
+// Several transposes in one launch: matrix z = blockIdx.z; workgroups past its tile grid exit.
+template <bool VEC4>
+__global__ void __launch_bounds__(256) k_transpose_batch(TransposeBatch b) {
+  constexpr int T = VEC4 ? 64 : 32;
+  __shared__ float tile[T][T + 1];
+  const int z = blockIdx.z;
+  const int R = b.R[z], C = b.C[z];
+  const int c0 = blockIdx.x * T, r0 = blockIdx.y * T;
+  if (c0 >= C || r0 >= R) return;
+  if constexpr (VEC4)
+    transpose_tile4(b.W[z], R, C, b.Wt[z], c0, r0, tile);
+  else
+    transpose_tile(b.W[z], R, C, b.Wt[z], c0, r0, tile);
+}
+
 hipError_t launch_transpose(hipStream_t s, const float* W, int R, int C, float* Wt) {
   if (R % 4 == 0 && C % 4 == 0 && vec_ok(W, C, C) && vec_ok(Wt, R, R)) {
     k_transpose4<<<dim3(cdiv(C, 64), cdiv(R, 64)), dim3(256), 0, s>>>(W, R, C, Wt);
     return hipGetLastError();
   }
   k_transpose<<<dim3(cdiv(C, 32), cdiv(R, 32)), dim3(256), 0, s>>>(W, R, C, Wt);
+  return hipGetLastError();
+}
+
+hipError_t launch_transpose_batch(hipStream_t s, const TransposeBatch& b) {
+  if (b.count <= 0) return hipSuccess;
+  if (b.count > kMaxLayers) return hipErrorInvalidValue;
+  bool v4 = true;
+  int maxR = 0, maxC = 0;
+  for (int z = 0; z < b.count; ++z) {
+    v4 = v4 && b.R[z] % 4 == 0 && b.C[z] % 4 == 0 && vec_ok(b.W[z], b.C[z], b.C[z]) && vec_ok(b.Wt[z], b.R[z], b.R[z]);
+    maxR = std::max(maxR, b.R[z]);
+    maxC = std::max(maxC, b.C[z]);
+  }
+  if (v4)
+    k_transpose_batch<true><<<dim3(cdiv(maxC, 64), cdiv(maxR, 64), b.count), dim3(256), 0, s>>>(b);
+  else
+    k_transpose_batch<false><<<dim3(cdiv(maxC, 32), cdiv(maxR, 32), b.count), dim3(256), 0, s>>>(b);
   return hipGetLastError();
 }
 
@@ -457,10 +502,72 @@ static hipError_t gram_vec(hipStream_t s, const GramBatch& g, int N1, int N2) {
   return hipGetLastError();
 }
 
-hipError_t launch_gram(hipStream_t s, const GramBatch& g, int N1, int N2) {
+// Small batches: the 64 x 64 tiles of k_gram would leave most compute units idle, so workgroup
+// (block, z) computes one 16 x 16 block of layer z's Gram with the 16x16x4 fp32 MFMA, its four
+// waves taking every fourth 16-column slice of K; the waves' partial blocks are then added in
+// wave order through LDS.  The MFMA takes A[i][k] from lane i + 16 k and B[k][j] from lane
+// j + 16 k, and returns D[4 (l / 16) + v][l % 16] in register v of lane l.  Lane l loads the four
+// columns k0 + 4 (l / 16) + q (q = 0..3) of row l % 16 of both operands, and MFMA q contracts
+// element q of both, so the four MFMAs cover the 16 columns of the slice (in a permuted order,
+// the same for both operands).
+template <bool VEC>
+__global__ void __launch_bounds__(256) k_gram_small(GramBatch g, int N1, int N2, int tiles_n) {
+  __shared__ float red[4][256];
+  const int z = blockIdx.y;
+  const int m0 = (blockIdx.x / tiles_n) * 16, n0 = (blockIdx.x % tiles_n) * 16;
+  const int K = g.K[z];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = lane & 15, kq = 4 * (lane >> 4);
+  const bool va = m0 + i < N1, vb = n0 + i < N2;
+  const float* __restrict__ pa = g.h1[z] + (long long)min(m0 + i, N1 - 1) * K;
+  const float* __restrict__ pb = g.h2[z] + (long long)min(n0 + i, N2 - 1) * K;
+  f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll 4
+  for (int k0 = 16 * wave; k0 < K; k0 += 64) {
+    const int k = k0 + kq;
+    f32x4 a = {0.f, 0.f, 0.f, 0.f}, b = {0.f, 0.f, 0.f, 0.f};
+    if (VEC) {   // K % 4 == 0 and 16-byte aligned rows: the 4 columns are all in or all out
+      if (k < K) {
+        a = *reinterpret_cast<const f32x4*>(pa + k);
+        b = *reinterpret_cast<const f32x4*>(pb + k);
+      }
+    } else {
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        if (k + q < K) {
+          a[q] = pa[k + q];
+          b[q] = pb[k + q];
+        }
+    }
+    if (!va) a = f32x4{0.f, 0.f, 0.f, 0.f};
+    if (!vb) b = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[q], b[q], acc, 0, 0, 0);
+  }
+#pragma unroll
+  for (int v = 0; v < 4; ++v) red[wave][(4 * (lane >> 4) + v) * 16 + i] = acc[v];
+  __syncthreads();
+  const int r = threadIdx.x >> 4, c = threadIdx.x & 15;
+  if (m0 + r < N1 && n0 + c < N2) {
+    const float v = ((red[0][threadIdx.x] + red[1][threadIdx.x]) + red[2][threadIdx.x]) + red[3][threadIdx.x];
+    g.out[z][(long long)(m0 + r) * N2 + n0 + c] = v + g.beta[z];
+  }
+}
+
+hipError_t launch_gram(hipStream_t s, const GramBatch& g, int N1, int N2, int num_cu) {
+  if (g.count <= 0) return hipSuccess;
   bool v = true;
   for (int z = 0; z < g.count; ++z)
     v = v && vec_ok(g.h1[z], g.K[z], g.K[z]) && vec_ok(g.h2[z], g.K[z], g.K[z]);
+  if ((long long)cdiv(N1, CfgSmall::BM) * cdiv(N2, CfgSmall::BN) * g.count < num_cu) {
+    const int tn = cdiv(N2, 16);
+    const dim3 grid(cdiv(N1, 16) * tn, g.count);
+    if (v)
+      k_gram_small<true><<<grid, dim3(256), 0, s>>>(g, N1, N2, tn);
+    else
+      k_gram_small<false><<<grid, dim3(256), 0, s>>>(g, N1, N2, tn);
+    return hipGetLastError();
+  }
   return v ? gram_vec<true>(s, g, N1, N2) : gram_vec<false>(s, g, N1, N2);
 }
 
@@ -484,6 +591,44 @@ __device__ __forceinline__ void stage_gram(const float* __restrict__ gram, int N
   __syncthreads();
 }
 
+// tot += gram_l[n1, n2] * (G1_l G2_l^T) over the tile at (m0, n0) (the scalar x1.x2 of Eq.
+// mixed_product_example weights the cotangent product); the tile's Gram block is staged in the
+// LDS tile area, free after the main loop.  Ends with a barrier.
+template <class Cfg, bool VEC, bool DMA = false>
+__device__ __forceinline__ void fcn_layer_term(const FcnContraction& c, int l, int N2, int R1, int R2, FastDiv fO,
+                                               int m0, int n0, float* smem, f32x16 (&tot)[Cfg::FM][Cfg::FN]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM, wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
+  const int K = c.K[l];
+  LoadKInnerT<VEC> la{c.G1[l], R1, K, K};
+  LoadKInnerT<VEC> lb{c.G2[l], R2, K, K};
+  f32x16 acc[Cfg::FM][Cfg::FN];
+  zero_acc<Cfg>(acc);
+  if (DMA)
+    gemm_mainloop_dma<Cfg, kSplitStages>(c.G1[l], K, R1, c.G2[l], K, R2, m0, n0, 0, K, smem, acc);
+  else
+    gemm_mainloop<Cfg>(la, lb, m0, n0, 0, K, smem, acc);
+  int n1lo, n2lo, S2;
+  stage_gram<Cfg>(c.gram[l], N2, R1, R2, fO, m0, n0, smem, n1lo, n2lo, S2);
+#pragma unroll
+  for (int fn = 0; fn < Cfg::FN; ++fn) {
+    const int s = min(n0 + wn0 + fn * 32 + (lane & 31), R2 - 1);
+    const int b = (int)fO.div(s) - n2lo;
+#pragma unroll
+    for (int fm = 0; fm < Cfg::FM; ++fm) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int r = min(m0 + wm0 + fm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3), R1 - 1);
+        const int a = (int)fO.div(r) - n1lo;
+        tot[fm][fn][v] += smem[a * S2 + b] * acc[fm][fn][v];
+      }
+      // keep one fragment's Gram values live at a time (register pressure)
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+  __syncthreads();
+}
+
 template <class Cfg, bool VEC>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_ntk_fcn(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __restrict__ theta,
@@ -499,40 +644,9 @@ k_ntk_fcn(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __
   const int O = (int)fO.d;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   const int R1 = N1 * O, R2 = N2 * O;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM, wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
-
   f32x16 tot[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(tot);
-  for (int l = 0; l < c.L; ++l) {
-    const int K = c.K[l];
-    LoadKInnerT<VEC> la{c.G1[l], R1, K, K};
-    LoadKInnerT<VEC> lb{c.G2[l], R2, K, K};
-    f32x16 acc[Cfg::FM][Cfg::FN];
-    zero_acc<Cfg>(acc);
-    gemm_mainloop<Cfg>(la, lb, m0, n0, 0, K, smem, acc);
-    // tot += gram_l[n1, n2] * acc  (the scalar x1.x2 of Eq. mixed_product_example); the
-    // tile's Gram block is staged in the LDS tile area, free after the main loop
-    int n1lo, n2lo, S2;
-    stage_gram<Cfg>(c.gram[l], N2, R1, R2, fO, m0, n0, smem, n1lo, n2lo, S2);
-#pragma unroll
-    for (int fn = 0; fn < Cfg::FN; ++fn) {
-      const int s = min(n0 + wn0 + fn * 32 + (lane & 31), R2 - 1);
-      const int b = (int)fO.div(s) - n2lo;
-#pragma unroll
-      for (int fm = 0; fm < Cfg::FM; ++fm) {
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-          const int r = min(m0 + wm0 + fm * 32 + 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3), R1 - 1);
-          const int a = (int)fO.div(r) - n1lo;
-          tot[fm][fn][v] += smem[a * S2 + b] * acc[fm][fn][v];
-        }
-        // keep one fragment's Gram values live at a time (register pressure)
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
-    __syncthreads();
-  }
+  for (int l = 0; l < c.L; ++l) fcn_layer_term<Cfg, VEC>(c, l, N2, R1, R2, fO, m0, n0, smem, tot);
   int n1lo, n2lo, S2;
   stage_gram<Cfg>(c.gram_readout, N2, R1, R2, fO, m0, n0, smem, n1lo, n2lo, S2);
   const bool mirror = symmetric && tm != tn;
@@ -545,6 +659,128 @@ k_ntk_fcn(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __
       if (mirror) theta[(((long long)n2 * N1 + n1) * O + o2) * O + o1] = v;
     }
   });
+}
+
+// ------------------------------------------------------------------------------ layer-split contraction
+// Few output tiles (small batches): the layers are cut into NG contiguous groups, group g holding
+// layers [g L / NG, (g + 1) L / NG), and workgroup (g, t) sums group g's terms of tile t, so the
+// launch has T NG workgroups instead of T.  Each stores its partial tile (row-major 64 x 64) at
+// part[(g T + t) 4096]; k_ntk_fcn_lreduce then adds the NG partials of a tile in group order and
+// the readout summand and writes theta, so the result does not depend on the order in which the
+// workgroups ran.
+__device__ __forceinline__ void fcn_tile_coords(int t, int symmetric, int tiles_n, int& tm, int& tn) {
+  if (symmetric) {
+    tri_index(t, tiles_n, tm, tn);
+  } else {
+    tm = t / tiles_n;
+    tn = t - tm * tiles_n;
+  }
+}
+
+template <class Cfg, bool VEC, bool DMA>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_ntk_fcn_lpart(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, int tiles_n, int T, int NG,
+                float* __restrict__ part) {
+  extern __shared__ float smem[];
+  // the (group, tile) list in group-major order, in contiguous ranges per XCD: an XCD's
+  // workgroups read the cotangents of one or two layer groups through its L2
+  int blk;
+  if (!xcd_block(blockIdx.x, T * NG, blk)) return;
+  const int g = blk / T, t = blk - g * T;
+  int tm, tn;
+  fcn_tile_coords(t, symmetric, tiles_n, tm, tn);
+  const int O = (int)fO.d;
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  const int R1 = N1 * O, R2 = N2 * O;
+  const int l0 = (int)((long long)g * c.L / NG), l1 = (int)((long long)(g + 1) * c.L / NG);
+  f32x16 tot[Cfg::FM][Cfg::FN];
+  zero_acc<Cfg>(tot);
+  for (int l = l0; l < l1; ++l) fcn_layer_term<Cfg, VEC, DMA>(c, l, N2, R1, R2, fO, m0, n0, smem, tot);
+  float* P = part + ((long long)g * T + t) * (Cfg::BM * Cfg::BN);
+  for_each_acc<Cfg>(tot, 0, 0, [&](int r, int s, float v) { P[r * Cfg::BN + s] = v; });
+}
+
+// One workgroup per tile.  Each thread adds 16 elements (four float4s) of the tile's NG partials
+// in group order, the four loads of one partial in flight together, adds the readout summand and
+// stages the result in LDS; theta is then written in runs of O consecutive floats: the direct
+// block in row order, the mirrored one (symmetric schedule) in column order.
+__global__ void __launch_bounds__(256)
+k_ntk_fcn_lreduce(const float* __restrict__ gram_readout, float readout_scale, int N1, int N2, FastDiv fO,
+                  int symmetric, int tiles_n, int T, int NG, const float* __restrict__ part,
+                  float* __restrict__ theta) {
+  __shared__ float sg[64 * 64];
+  __shared__ float tile[64][65];
+  const int t = blockIdx.x;
+  int tm, tn;
+  fcn_tile_coords(t, symmetric, tiles_n, tm, tn);
+  const int O = (int)fO.d;
+  const int m0 = tm * 64, n0 = tn * 64;
+  const int R1 = N1 * O, R2 = N2 * O;
+  // the readout Gram block of the tile (rows r cover samples r / O)
+  const int n1lo = (int)fO.div(m0), n2lo = (int)fO.div(n0);
+  const int S1 = (int)fO.div(min(m0 + 64, R1) - 1) - n1lo + 1;
+  const int S2 = (int)fO.div(min(n0 + 64, R2) - 1) - n2lo + 1;
+  for (int q = threadIdx.x; q < S1 * S2; q += 256) {
+    const int a = q / S2, b = q - a * S2;
+    sg[q] = gram_readout[(long long)(n1lo + a) * N2 + n2lo + b];
+  }
+  // partial sums in group order: element e = 4 (threadIdx.x + 256 j) + i, j = 0..3, i = 0..3
+  const float4* P = reinterpret_cast<const float4*>(part + (long long)t * 4096);
+  const long long gstride = (long long)T * 1024;   // float4s between the partials of two groups
+  float4 v[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) v[j] = P[threadIdx.x + 256 * j];
+  for (int g = 1; g < NG; ++g) {
+    float4 w[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) w[j] = P[g * gstride + threadIdx.x + 256 * j];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      v[j].x += w[j].x;
+      v[j].y += w[j].y;
+      v[j].z += w[j].z;
+      v[j].w += w[j].w;
+    }
+  }
+  __syncthreads();   // sg complete
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = 4 * (threadIdx.x + 256 * j);
+    const int rl = e >> 6, sl = e & 63;
+    const float vv[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+    const int r = m0 + rl;
+    const int n1 = (int)fO.div(min(r, R1 - 1)), o1 = r - n1 * O;
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int s = n0 + sl + i;
+      const int n2 = (int)fO.div(min(s, R2 - 1)), o2 = s - n2 * O;
+      float x = vv[i];
+      if (o1 == o2 && r < R1 && s < R2) x += readout_scale * sg[(n1 - n1lo) * S2 + (n2 - n2lo)];
+      tile[rl][sl + i] = x;
+    }
+  }
+  __syncthreads();
+  // direct block: consecutive threads take consecutive columns s = (n2, o2)
+  for (int e = threadIdx.x; e < 4096; e += 256) {
+    const int rl = e >> 6, sl = e & 63;
+    const int r = m0 + rl, s = n0 + sl;
+    if (r < R1 && s < R2) {
+      const int n1 = (int)fO.div(r), o1 = r - n1 * O;
+      const int n2 = (int)fO.div(s), o2 = s - n2 * O;
+      theta[(((long long)n1 * N2 + n2) * O + o1) * O + o2] = tile[rl][sl];
+    }
+  }
+  if (!(symmetric && tm != tn)) return;
+  // mirrored block theta[n2][n1][o2][o1]: consecutive threads take consecutive rows r = (n1, o1)
+  for (int e = threadIdx.x; e < 4096; e += 256) {
+    const int sl = e >> 6, rl = e & 63;
+    const int r = m0 + rl, s = n0 + sl;
+    if (r < R1 && s < R2) {
+      const int n1 = (int)fO.div(r), o1 = r - n1 * O;
+      const int n2 = (int)fO.div(s), o2 = s - n2 * O;
+      theta[(((long long)n2 * N1 + n1) * O + o2) * O + o1] = tile[rl][sl];
+    }
+  }
 }
 
 // ------------------------------------------------------------------------------ stream-K contraction
@@ -743,6 +979,27 @@ long long ntk_fcn_part_floats(int num_cu) {
   return (long long)kSkPerCu * num_cu * 2 * CfgSK::BM * CfgSK::BN;
 }
 
+static bool fcn_uses_stream_k(int L, long long big_tiles, int num_cu, bool part) {
+  // stream-K when there are at least as many whole tiles as persistent workgroups (P must be
+  // a multiple of 8 for the XCD-aware range order)
+  return L >= 1 && part && num_cu >= 16 && num_cu % 8 == 0 && big_tiles >= kSkPerCu * num_cu;
+}
+
+// Few output tiles: the number of layer groups of the layer-split contraction (>= 2), or 0 when
+// that form does not apply.
+static int fcn_split_groups(long long R1, long long R2, int L, int symmetric, int num_cu, bool part) {
+  const long long big_tiles = (long long)cdiv(R1, 128) * cdiv(R2, 128);
+  if (!part || L < 2 || fcn_uses_stream_k(L, big_tiles, num_cu, part) || big_tiles >= 512) return 0;
+  // fewer 64 x 64 tiles than two per compute unit: about four workgroups per compute unit in
+  // all, as far as the partial tiles fit the buffer
+  const long long ts_m = cdiv(R1, 64), ts_n = cdiv(R2, 64);
+  const long long Ts = symmetric ? ts_n * (ts_n + 1) / 2 : ts_m * ts_n;
+  if (Ts >= 2LL * num_cu) return 0;
+  long long NG = std::min<long long>(L, (4LL * num_cu + Ts - 1) / Ts);
+  NG = std::min<long long>(NG, ntk_fcn_part_floats(num_cu) / (Ts * 4096));
+  return NG >= 2 ? (int)NG : 0;
+}
+
 hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2, int O,
                           int symmetric, float* theta, int num_cu, float* part) {
   int R1, R2;
@@ -791,11 +1048,32 @@ hipError_t launch_ntk_fcn(hipStream_t s, const FcnContraction& c, int N1, int N2
     return hipGetLastError();
   };
   const long long big_tiles = (long long)cdiv(R1, 128) * cdiv(R2, 128);
-  // stream-K when there are at least as many whole tiles as persistent workgroups (P must be
-  // a multiple of 8 for the XCD-aware range order)
-  if (c.L >= 1 && part && num_cu >= 16 && num_cu % 8 == 0 && big_tiles >= kSkPerCu * num_cu)
+  if (fcn_uses_stream_k(c.L, big_tiles, num_cu, part != nullptr))
     return dma ? go_sk(TrueT{}, TrueT{}) : (v ? go_sk(TrueT{}, FalseT{}) : go_sk(FalseT{}, FalseT{}));
   if (big_tiles >= 512) return v ? go(CfgBig8{}, TrueT{}) : go(CfgBig8{}, FalseT{});
+  const int NG = fcn_split_groups(R1, R2, c.L, symmetric, num_cu, part != nullptr);
+  auto go_split = [&](auto vec_tag, auto dma_tag) -> hipError_t {
+    using Cfg = CfgSmall;
+    constexpr bool VEC = decltype(vec_tag)::value;
+    constexpr bool DMA = decltype(dma_tag)::value;
+    using L = LoadKInnerT<VEC>;
+    constexpr int bytes = DMA ? gemm_dma_smem_bytes<Cfg, kSplitStages>() : gemm_smem_bytes<Cfg, L, L>();
+    static_assert(64 * 64 <= bytes / 4, "Gram block must fit the LDS tile area");
+    const int tm = cdiv(R1, 64), tn = cdiv(R2, 64);
+    const int T = symmetric ? tn * (tn + 1) / 2 : tm * tn;
+    const FastDiv fO((uint32_t)O);
+    hipError_t e = hipFuncSetAttribute((const void*)k_ntk_fcn_lpart<Cfg, VEC, DMA>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess) return e;
+    k_ntk_fcn_lpart<Cfg, VEC, DMA><<<dim3(8 * cdiv((long long)T * NG, 8)), dim3(Cfg::THREADS), bytes, s>>>(
+        c, N1, N2, fO, symmetric, tn, T, NG, part);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    k_ntk_fcn_lreduce<<<dim3(T), dim3(256), 0, s>>>(c.gram_readout, c.readout_scale, N1, N2, fO, symmetric, tn, T,
+                                                    NG, part, theta);
+    return hipGetLastError();
+  };
+  if (NG >= 2) return dma ? go_split(TrueT{}, TrueT{}) : (v ? go_split(TrueT{}, FalseT{}) : go_split(FalseT{}, FalseT{}));
   return v ? go(CfgSmall{}, TrueT{}) : go(CfgSmall{}, FalseT{});
 }
 

@@ -67,6 +67,14 @@ hipError_t launch_bwd_seed(hipStream_t s, const float* W, const float* dphi, int
                            float* G);
 // Wt [C, R] = W^T for W [R, C].
 hipError_t launch_transpose(hipStream_t s, const float* W, int R, int C, float* Wt);
+// Wt[z] = W[z]^T for z < count (each W[z] R[z] x C[z], row-major), in one launch.
+struct TransposeBatch {
+  const float* W[kMaxLayers];
+  float* Wt[kMaxLayers];
+  int R[kMaxLayers], C[kMaxLayers];
+  int count;
+};
+hipError_t launch_transpose_batch(hipStream_t s, const TransposeBatch& b);
 
 struct GramBatch {
   const float* h1[kMaxLayers + 1];
@@ -77,7 +85,8 @@ struct GramBatch {
   int count;
 };
 // out_l[n1, n2] = h1_l[n1] . h2_l[n2] + beta_l for every l (rows of h have stride K_l).
-hipError_t launch_gram(hipStream_t s, const GramBatch& g, int N1, int N2);
+// Batches whose matrix-core tiles would not fill num_cu compute units run on the vector units.
+hipError_t launch_gram(hipStream_t s, const GramBatch& g, int N1, int N2, int num_cu);
 
 struct FcnContraction {
   const float* G1[kMaxLayers];    // cotangents of batch 1, [N1*O, K_l]

@@ -696,6 +696,9 @@ static int fcn_forward(ntk_handle* h, const float* const* params, const float* X
   return NTK_OK;
 }
 
+// forward FLOPs from which the FCN path puts independent steps on the second stream
+constexpr double kAuxStreamMinFlops = 4e9;
+
 static int compute_fcn(ntk_handle* h, const float* const* params, const float* X1, int n1,
                        const float* X2, int n2, float* theta) {
   const int L = h->L;
@@ -704,10 +707,11 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   const int M = sym ? n1 : n1 + n2;
   hipStream_t s = h->stream;
   // independent steps go to the library's second stream when it exists and the problem is big
-  // enough for the overlap to outweigh the cross-stream synchronisation (a few microseconds)
+  // enough for the overlap to outweigh the cross-stream synchronisation (an event record and
+  // wait cost about 12 us of host time, so below a few GFLOP a single stream is faster)
   double fwd_flops = 0;
   for (int l = 0; l < L; ++l) fwd_flops += 2.0 * M * h->dims[l] * h->dims[l + 1];
-  hipStream_t aux = fwd_flops >= 1e7 ? h->aux : nullptr;
+  hipStream_t aux = fwd_flops >= kAuxStreamMinFlops ? h->aux : nullptr;
   hipStream_t sa = aux ? aux : s;
   Profiler* P = &h->prof;
   auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
@@ -724,11 +728,19 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     if ((e = hipEventRecord(h->ev_fork, s)) != hipSuccess || (e = hipStreamWaitEvent(sa, h->ev_fork, 0)) != hipSuccess)
       return hip_fail(h, e, "stream fork");
   }
-  for (int l = 1; l < L; ++l) {
+  if (L >= 2) {
+    TransposeBatch tb{};
+    tb.count = L - 1;
+    for (int l = 1; l < L; ++l) {
+      tb.W[l - 1] = params[h->param_index[l]];
+      tb.Wt[l - 1] = F(h->off_Wt[l]);
+      tb.R[l - 1] = h->dims[l + 1];
+      tb.C[l - 1] = h->dims[l];
+    }
     prof_begin(P, sa, KC_TRANSPOSE);
-    e = launch_transpose(sa, params[h->param_index[l]], h->dims[l + 1], h->dims[l], F(h->off_Wt[l]));
+    e = launch_transpose_batch(sa, tb);
     prof_end(P, sa, KC_TRANSPOSE);
-    if (e != hipSuccess) return hip_fail(h, e, "weight transpose");
+    if (e != hipSuccess) return hip_fail(h, e, "weight transposes");
   }
   if (aux && (e = hipEventRecord(h->ev_tr, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
   // 1. forward pass keeping the layer inputs
@@ -769,7 +781,7 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
         gb.beta[l] = h->layers[l].has_bias ? 1.0f : 0.0f;
       }
       prof_begin(P, sa, KC_GRAM);
-      e = launch_gram(sa, gb, n1, n2);
+      e = launch_gram(sa, gb, n1, n2, h->num_cu);
       prof_end(P, sa, KC_GRAM);
       if (e != hipSuccess) return hip_fail(h, e, "gram");
     }
@@ -1056,7 +1068,7 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
     gb.K[0] = C;
     gb.beta[0] = 0.f;
     prof_begin(P, s, KC_GRAM);
-    e = launch_gram(s, gb, n1, n2);
+    e = launch_gram(s, gb, n1, n2, h->num_cu);
     prof_end(P, s, KC_GRAM);
   }
   if (e != hipSuccess) return hip_fail(h, e, "gram");
@@ -1311,7 +1323,7 @@ static int vector_product_fcn(ntk_handle* h, const float* const* params, const f
     gb.K[0] = n2;
     gb.beta[0] = 0.f;
     prof_begin(P, s, KC_GRAM);
-    e = launch_gram(s, gb, dout, din);
+    e = launch_gram(s, gb, dout, din, h->num_cu);
     prof_end(P, s, KC_GRAM);
     if (e != hipSuccess) return hip_fail(h, e, "weight-space cotangent");
     if (h->layers[l].has_bias) {
@@ -1342,7 +1354,7 @@ static int vector_product_fcn(ntk_handle* h, const float* const* params, const f
       gb.beta[1] = 0.f;
     }
     prof_begin(P, s, KC_GRAM);
-    e = launch_gram(s, gb, n1, dout);
+    e = launch_gram(s, gb, n1, dout, h->num_cu);
     prof_end(P, s, KC_GRAM);
     if (e != hipSuccess) return hip_fail(h, e, "JVP products");
     const float* bias_t = h->layers[l].has_bias ? V(h->vp_off_tcb[l]) : nullptr;
@@ -1438,7 +1450,7 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
   gb.K[0] = n2;
   gb.beta[0] = 0.f;
   prof_begin(P, s, KC_GRAM);
-  e = launch_gram(s, gb, O, C);
+  e = launch_gram(s, gb, O, C, h->num_cu);
   prof_end(P, s, KC_GRAM);
   if (e != hipSuccess) return hip_fail(h, e, "readout weight cotangent");
   GramBatch gu{};
@@ -1449,7 +1461,7 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
   gu.K[0] = O;
   gu.beta[0] = 0.f;
   prof_begin(P, s, KC_GRAM);
-  e = launch_gram(s, gu, n2, C);
+  e = launch_gram(s, gu, n2, C, h->num_cu);
   prof_end(P, s, KC_GRAM);
   if (e != hipSuccess) return hip_fail(h, e, "pooled-feature cotangent");
   float* Gcur = F(h->off_Gping);
@@ -1588,7 +1600,7 @@ static int vector_product_cnn(ntk_handle* h, const float* const* params, const f
   gr.K[1] = C;
   gr.beta[1] = 0.f;
   prof_begin(P, s, KC_GRAM);
-  e = launch_gram(s, gr, n1, O);
+  e = launch_gram(s, gr, n1, O, h->num_cu);
   prof_end(P, s, KC_GRAM);
   if (e != hipSuccess) return hip_fail(h, e, "JVP readout");
   prof_begin(P, s, KC_VP_ELEMENTWISE);
