@@ -33,6 +33,11 @@ using CfgConv = TileCfg<128, 64, 32, 32, 32>;      // backward / wgrad, fp32 MFM
 using CfgConvBwd = TileCfg<256, 64, 32, 32, 64>;
 using CfgConvWg = CfgConv;
 constexpr int kConvBwdStages = 2, kConvWgStages = 2;
+// Small images (few output rows): below kConvFewTiles tiles of the shapes above, the backward
+// takes 128x64 tiles (8 waves of 32x32) and the fp64 forward 32x32 tiles (4 waves of 16x16), so
+// that the launch still spreads over the compute units.
+constexpr int kConvFewTiles = 512;
+using CfgConvF64Small = TileCfg<32, 32, 32, 16, 16>;
 using CfgSplitK = TileCfg<128, 128, 32, 64, 64>;   // J1 J2^T partial products
 using CfgSplitKDma = TileCfg<128, 128, 32, 32, 64>;  // the same, direct-to-LDS: 8 waves of 32x64
 
@@ -491,20 +496,28 @@ static hipError_t conv_fwd_vec(hipStream_t s, const float* x, int images, int H,
   return hipGetLastError();
 }
 
+template <class Cfg>
+static hipError_t conv_fwd_dma_cfg(hipStream_t s, const float* x, int images, int H, int W, int Cin,
+                                   const float* K, int Cout, int act, const float* bias, float* hn, float* dphi) {
+  const int M = images * H * W, Kd = 9 * Cin;
+  const int tn = cdiv(Cout, Cfg::BN), tm = cdiv(M, Cfg::BM);
+  auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(x, images, H, W, Cin);
+  DmaRowMajor<Cfg::BN, Cfg::WAVES> pb{K, Kd, Cout};
+  constexpr int bytes = gemm_dma_smem_bytes<Cfg, 3>();
+  hipError_t e = hipFuncSetAttribute((const void*)k_conv_fwd_dma<Cfg>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e != hipSuccess) return e;
+  k_conv_fwd_dma<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(pa, pb, Kd, M, Cout, act, bias, hn, dphi, tn);
+  return hipGetLastError();
+}
+
 hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int W, int Cin,
                            const float* K, int Cout, int act, const float* bias, float* hn, float* dphi) {
   if (conv_dma_ok(x, (long long)images * H * W * Cin, Cin, K)) {
-    using Cfg = CfgConvF64;
-    const int M = images * H * W, Kd = 9 * Cin;
-    const int tn = cdiv(Cout, Cfg::BN), tm = cdiv(M, Cfg::BM);
-    auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(x, images, H, W, Cin);
-    DmaRowMajor<Cfg::BN, Cfg::WAVES> pb{K, Kd, Cout};
-    constexpr int bytes = gemm_dma_smem_bytes<Cfg, 3>();
-    hipError_t e = hipFuncSetAttribute((const void*)k_conv_fwd_dma<Cfg>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-    if (e != hipSuccess) return e;
-    k_conv_fwd_dma<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(pa, pb, Kd, M, Cout, act, bias, hn, dphi, tn);
-    return hipGetLastError();
+    const long long tiles = (long long)cdiv((long long)images * H * W, CfgConvF64::BM) * cdiv(Cout, CfgConvF64::BN);
+    if (tiles < kConvFewTiles)
+      return conv_fwd_dma_cfg<CfgConvF64Small>(s, x, images, H, W, Cin, K, Cout, act, bias, hn, dphi);
+    return conv_fwd_dma_cfg<CfgConvF64>(s, x, images, H, W, Cin, K, Cout, act, bias, hn, dphi);
   }
   if (Cin % 4 == 0 && aligned16(x) && vec_ok(K, 9 * Cin, 9 * Cin))
     return conv_fwd_vec<true>(s, x, images, H, W, Cin, K, Cout, act, bias, hn, dphi);
@@ -746,24 +759,31 @@ static hipError_t conv_bwd_vec(hipStream_t s, const float* G, int images, int O,
   return hipGetLastError();
 }
 
+template <class Cfg>
+static hipError_t conv_bwd_dma_cfg(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
+                                   const float* Kt, int Cin, const float* dphi, float* out) {
+  constexpr int NS = kConvBwdStages;
+  const int D = H * W, Kd = 9 * Cg;
+  int R;
+  if (!to_int((long long)images * O * D, R)) return hipErrorInvalidValue;
+  const int tn = cdiv(Cin, Cfg::BN), tm = cdiv(R, Cfg::BM);
+  auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(G, images * O, H, W, Cg);
+  DmaRowMajor<Cfg::BN, Cfg::WAVES> pb{Kt, Kd, Cin};
+  constexpr int bytes = gemm_dma_smem_bytes<Cfg, NS>();
+  hipError_t e = hipFuncSetAttribute((const void*)k_conv_bwd_dma<Cfg, NS>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e != hipSuccess) return e;
+  k_conv_bwd_dma<Cfg, NS><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(
+      pa, pb, Kd, dphi, R, Cin, FastDiv((uint32_t)(O * D)), FastDiv((uint32_t)D), out, tn);
+  return hipGetLastError();
+}
+
 hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
                            const float* Kt, int Cin, const float* dphi, float* out) {
   if (conv_dma_ok(G, (long long)images * O * H * W * Cg, Cg, Kt)) {
-    using Cfg = CfgConvBwd;
-    constexpr int NS = kConvBwdStages;
-    const int D = H * W, Kd = 9 * Cg;
-    int R;
-    if (!to_int((long long)images * O * D, R)) return hipErrorInvalidValue;
-    const int tn = cdiv(Cin, Cfg::BN), tm = cdiv(R, Cfg::BM);
-    auto pa = dma_patches<Cfg::BM, Cfg::WAVES>(G, images * O, H, W, Cg);
-    DmaRowMajor<Cfg::BN, Cfg::WAVES> pb{Kt, Kd, Cin};
-    constexpr int bytes = gemm_dma_smem_bytes<Cfg, NS>();
-    hipError_t e = hipFuncSetAttribute((const void*)k_conv_bwd_dma<Cfg, NS>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-    if (e != hipSuccess) return e;
-    k_conv_bwd_dma<Cfg, NS><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(
-        pa, pb, Kd, dphi, R, Cin, FastDiv((uint32_t)(O * D)), FastDiv((uint32_t)D), out, tn);
-    return hipGetLastError();
+    const long long tiles = (long long)cdiv((long long)images * O * H * W, CfgConvBwd::BM) * cdiv(Cin, CfgConvBwd::BN);
+    if (tiles < kConvFewTiles) return conv_bwd_dma_cfg<CfgConv>(s, G, images, O, H, W, Cg, Kt, Cin, dphi, out);
+    return conv_bwd_dma_cfg<CfgConvBwd>(s, G, images, O, H, W, Cg, Kt, Cin, dphi, out);
   }
   if (Cg % 4 == 0 && aligned16(G) && vec_ok(Kt, 9 * Cg, 9 * Cg))
     return conv_bwd_vec<true>(s, G, images, O, H, W, Cg, Kt, Cin, dphi, out);
