@@ -74,20 +74,23 @@ struct PairMfmaArgs {
 };
 
 // Geometry of one instantiation, DT blocks of 16 pixels:
-//  * pairs per wave PPW: four for images of at most 16 pixels (one sample of batch 1 against four
-//    of batch 2: the G1 operand of a channel is read once for the four), one otherwise (the PK
-//    registers of four pairs would not fit);
-//  * a workgroup of 4 waves takes B1 x B2 input pairs (4 x 4, or 2 x 2), or with DIAG four pairs
+//  * pairs per wave PPW: two for images of at most 16 pixels (one sample of batch 1 against two
+//    of batch 2: the G1 operand of a channel is read once for the two; with four pairs per wave
+//    the 4x4-image CNN's 64 x 64 pairs leave one wave per SIMD, 196 vs 177 us for three layers,
+//    and one pair per wave took 203), one otherwise (the PK registers of more would not fit);
+//  * a workgroup of 4 waves takes B1 x B2 input pairs (4 x PPW, or 2 x 2), or with DIAG four pairs
 //    (n, n) of the batch diagonal; its NS = B1 + B2 sample slots (batch 1, then batch 2) are staged
 //    per chunk of CC channels, 16 cotangent rows x Dp pixels per slot and channel, each row padded
 //    by 4 floats so that the 16 rows one 16-byte read touches fall in 16 distinct bank groups.
+constexpr int kPairsPerWave16 = 2;   // pairs per wave for images of at most 16 pixels
+
 template <int DT, bool DIAG>
 struct PairGeom {
   static constexpr int Dp = 16 * DT;
   static constexpr int LD = Dp + 4;
-  static constexpr int PPW = (DT == 1 && !DIAG) ? 4 : 1;
-  static constexpr int B1 = DIAG ? 4 : (PPW == 4 ? 4 : 2);
-  static constexpr int B2 = DIAG ? 4 : (PPW == 4 ? 4 : 2);
+  static constexpr int PPW = (DT == 1 && !DIAG) ? kPairsPerWave16 : 1;
+  static constexpr int B1 = DIAG ? 4 : (PPW > 1 ? 4 : 2);
+  static constexpr int B2 = DIAG ? 4 : (PPW > 1 ? PPW : 2);
   static constexpr int NS = B1 + B2;
   static constexpr int CC0 = 512 / (NS * LD);             // two chunks in about 64 KB of LDS
   static constexpr int CC = CC0 > 0 ? CC0 : 1;
@@ -95,7 +98,9 @@ struct PairGeom {
   static constexpr int CHUNK = ROWS * LD;                 // floats of one chunk buffer
   static constexpr int NU = ROWS * Dp / 4 / 256;          // float4 loads per thread per chunk
   static_assert(ROWS * Dp / 4 % 256 == 0, "a chunk splits evenly into float4 loads");
-  static constexpr int HFLOATS = 4 * PPW * Dp * Dp;       // the pixel Grams of every wave's pairs
+  // the pixel Grams of every wave's pairs, rows LD = Dp + 4 floats apart: the four lane groups
+  // of a PK read (rows 4g + j) then fall 16 banks apart
+  static constexpr int HFLOATS = 4 * PPW * Dp * LD;
   static constexpr int SMEM = (2 * CHUNK > HFLOATS ? 2 * CHUNK : HFLOATS) * 4;
 };
 
@@ -151,7 +156,7 @@ k_pairsum_mfma(PairMfmaArgs a) {
       slot_ok[B1 + k] = B2 * bj + k < a.n2;
       slot_m[B1 + k] = a.n2_off + min(B2 * bj + k, a.n2 - 1);
     }
-    if constexpr (PPW == 4) {
+    if constexpr (PPW > 1) {
       s1 = wave;
       i1 = B1 * bi + wave;
 #pragma unroll
@@ -301,20 +306,20 @@ k_pairsum_mfma(PairMfmaArgs a) {
     }
 #pragma unroll
     for (int p = 0; p < PPW; ++p) {
-      float* Hs = sm + (wave * PPW + p) * Dp * Dp;
+      float* Hs = sm + (wave * PPW + p) * Dp * LD;
 #pragma unroll
       for (int r = 0; r < DT; ++r)
 #pragma unroll
         for (int s = 0; s < DT; ++s)
 #pragma unroll
-          for (int v = 0; v < 4; ++v) Hs[(16 * r + 4 * g + v) * Dp + 16 * s + li] = hc[p][r][s][v];
+          for (int v = 0; v < 4; ++v) Hs[(16 * r + 4 * g + v) * LD + 16 * s + li] = hc[p][r][s][v];
     }
   }
   __syncthreads();
   float pk[PPW][DT][DT][4];
   // ---- this lane's PK entries (the A operands of the X products).  Both patches of a PK entry
   // take the same tap, so tap (dy, dx) adds H[p1 + s, p2 + s] with s = dy W + dx, i.e. the entry
-  // (dy W + dx)(Dp + 1) further on, when both shifted pixels lie inside the image: a 9-bit mask
+  // (dy W + dx)(LD + 1) further on, when both shifted pixels lie inside the image: a 9-bit mask
   // per pixel (bit 3 (dy + 1) + dx + 1), formed once per pixel the lane touches.
   auto tapmask = [&](int p) -> unsigned {
     if (p >= D) return 0u;
@@ -337,7 +342,7 @@ k_pairsum_mfma(PairMfmaArgs a) {
   const int W = a.W;
 #pragma unroll
   for (int p = 0; p < PPW; ++p) {
-    const float* Hs = sm + (wave * PPW + p) * Dp * Dp;
+    const float* Hs = sm + (wave * PPW + p) * Dp * LD;
 #pragma unroll
     for (int rt = 0; rt < DT; ++rt)
 #pragma unroll
@@ -345,7 +350,7 @@ k_pairsum_mfma(PairMfmaArgs a) {
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const unsigned m = m1[t][j] & m2[rt];
-          const int e = (16 * t + 4 * g + j) * Dp + 16 * rt + li;   // H[p1][p2]
+          const int e = (16 * t + 4 * g + j) * LD + 16 * rt + li;   // H[p1][p2]
           float v;
           if (a.taps == 1) {
             v = (m >> 4) & 1u ? Hs[e] : 0.f;
@@ -357,7 +362,7 @@ k_pairsum_mfma(PairMfmaArgs a) {
               for (int dx = -1; dx <= 1; ++dx) {
                 const int k = 3 * (dy + 1) + dx + 1;
                 // a masked tap reads a clamped, valid address and adds nothing
-                const int ee = min(max(e + (dy * W + dx) * (Dp + 1), 0), Dp * Dp - 1);
+                const int ee = min(max(e + (dy * W + dx) * (LD + 1), 0), Dp * LD - 1);
                 const float hv = Hs[ee];
                 v += (m >> k) & 1u ? hv : 0.f;
               }
