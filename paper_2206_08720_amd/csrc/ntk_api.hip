@@ -661,39 +661,57 @@ static int jc_dense_layer(ntk_handle* h, const float* G1, const float* G2, long 
 
 // Forward pass of the stacked batch [X1; X2] (or X1 alone when sym) keeping every layer input
 // h_l and act'(z_l); *h0 receives the layer-0 input (X1 itself when sym).
-static int fcn_forward(ntk_handle* h, const float* const* params, const float* X1, int n1,
-                       const float* X2, int n2, bool sym, const float** h0) {
+// The layers of the forward pass for the rows [r0, r1) of the stacked batch (h0: its layer-0
+// input), on stream st; split-K partials (one buffer) only when use_part.
+static int fcn_forward_rows(ntk_handle* h, const float* const* params, const float* h0, int r0, int r1,
+                            hipStream_t st, bool use_part) {
   const int L = h->L;
-  const int M = sym ? n1 : n1 + n2;
-  hipStream_t s = h->stream;
   Profiler* P = &h->prof;
   auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
-  for (int l = 0; l <= L; ++l) {
-    if (!params[h->param_index[l]]) return fail(h, NTK_E_ARG, "null weight pointer");
-    if (h->layers[l].has_bias && !params[h->param_index[l] + 1]) return fail(h, NTK_E_ARG, "null bias pointer");
-  }
-  hipError_t e;
-  const int d0 = h->dims[0];
-  *h0 = X1;
-  if (!sym) {
-    prof_begin(P, s, KC_COPY);
-    e = launch_stack2(s, X1, (long long)n1 * d0, X2, (long long)n2 * d0, F(h->off_h[0]));
-    prof_end(P, s, KC_COPY);
-    if (e != hipSuccess) return hip_fail(h, e, "stacking X1/X2");
-    *h0 = F(h->off_h[0]);
-  }
   // the readout's own output f is not needed
   for (int l = 0; l < L; ++l) {
     const float* W = params[h->param_index[l]];
     const float* b = h->layers[l].has_bias ? params[h->param_index[l] + 1] : nullptr;
-    prof_begin(P, s, KC_DENSE_FWD);
-    e = launch_dense_fwd(s, l == 0 ? *h0 : F(h->off_h[l]), W, b, M, h->dims[l + 1], h->dims[l],
-                         h->layers[l].act, F(h->off_h[l + 1]), F(h->off_dphi[l]),
-                         reinterpret_cast<double*>(h->ws + h->off_fpart), h->fpart_capacity);
-    prof_end(P, s, KC_DENSE_FWD);
+    const float* in = (l == 0 ? h0 : F(h->off_h[l])) + (size_t)r0 * h->dims[l];
+    prof_begin(P, st, KC_DENSE_FWD);
+    hipError_t e = launch_dense_fwd(st, in, W, b, r1 - r0, h->dims[l + 1], h->dims[l], h->layers[l].act,
+                                    F(h->off_h[l + 1]) + (size_t)r0 * h->dims[l + 1],
+                                    F(h->off_dphi[l]) + (size_t)r0 * h->dims[l + 1],
+                                    use_part ? reinterpret_cast<double*>(h->ws + h->off_fpart) : nullptr,
+                                    use_part ? h->fpart_capacity : 0);
+    prof_end(P, st, KC_DENSE_FWD);
     if (e != hipSuccess) return hip_fail(h, e, "dense forward");
   }
   return NTK_OK;
+}
+
+// The stacked batch [X1; X2] (X1 alone when sym) into *h0, on the handle's stream.
+static int fcn_stack(ntk_handle* h, const float* const* params, const float* X1, int n1, const float* X2,
+                     int n2, bool sym, const float** h0) {
+  const int L = h->L;
+  for (int l = 0; l <= L; ++l) {
+    if (!params[h->param_index[l]]) return fail(h, NTK_E_ARG, "null weight pointer");
+    if (h->layers[l].has_bias && !params[h->param_index[l] + 1]) return fail(h, NTK_E_ARG, "null bias pointer");
+  }
+  *h0 = X1;
+  if (!sym) {
+    const int d0 = h->dims[0];
+    float* dst = reinterpret_cast<float*>(h->ws + h->off_h[0]);
+    prof_begin(&h->prof, h->stream, KC_COPY);
+    hipError_t e = launch_stack2(h->stream, X1, (long long)n1 * d0, X2, (long long)n2 * d0, dst);
+    prof_end(&h->prof, h->stream, KC_COPY);
+    if (e != hipSuccess) return hip_fail(h, e, "stacking X1/X2");
+    *h0 = dst;
+  }
+  return NTK_OK;
+}
+
+// Forward pass of the stacked batch keeping the layer inputs, on the handle's stream.
+static int fcn_forward(ntk_handle* h, const float* const* params, const float* X1, int n1,
+                       const float* X2, int n2, bool sym, const float** h0) {
+  int rc = fcn_stack(h, params, X1, n1, X2, n2, sym, h0);
+  if (rc != NTK_OK) return rc;
+  return fcn_forward_rows(h, params, *h0, 0, sym ? n1 : n1 + n2, h->stream, true);
 }
 
 // forward FLOPs from which the FCN path puts independent steps on the second stream
@@ -723,12 +741,8 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   const int Oe = logit ? 1 : O;
   for (int l = 0; l <= L; ++l)
     if (!params[h->param_index[l]]) return fail(h, NTK_E_ARG, "null weight pointer");
-  // 0. weight transposes for the backward, on the second stream while the forward runs
-  if (aux) {
-    if ((e = hipEventRecord(h->ev_fork, s)) != hipSuccess || (e = hipStreamWaitEvent(sa, h->ev_fork, 0)) != hipSuccess)
-      return hip_fail(h, e, "stream fork");
-  }
-  if (L >= 2) {
+  auto transposes = [&](hipStream_t st) -> int {
+    if (L < 2) return NTK_OK;
     TransposeBatch tb{};
     tb.count = L - 1;
     for (int l = 1; l < L; ++l) {
@@ -737,25 +751,17 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
       tb.R[l - 1] = h->dims[l + 1];
       tb.C[l - 1] = h->dims[l];
     }
-    prof_begin(P, sa, KC_TRANSPOSE);
-    e = launch_transpose_batch(sa, tb);
-    prof_end(P, sa, KC_TRANSPOSE);
-    if (e != hipSuccess) return hip_fail(h, e, "weight transposes");
-  }
-  if (aux && (e = hipEventRecord(h->ev_tr, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
-  // 1. forward pass keeping the layer inputs
+    prof_begin(P, st, KC_TRANSPOSE);
+    hipError_t err = launch_transpose_batch(st, tb);
+    prof_end(P, st, KC_TRANSPOSE);
+    return err == hipSuccess ? NTK_OK : hip_fail(h, err, "weight transposes");
+  };
   const float* h0 = nullptr;
-  int rc0 = fcn_forward(h, params, X1, n1, X2, n2, sym, &h0);
-  if (rc0 != NTK_OK) return rc0;
   auto hptr = [&](int l) -> const float* { return l == 0 ? h0 : F(h->off_h[l]); };
   auto H2 = [&](int l) -> const float* { return sym ? hptr(l) : hptr(l) + (size_t)n1 * h->dims[l]; };
-  // 2. layer-input Grams (the x1.x2 scalars; per-sample scalars on the batch diagonal), on the
-  //    second stream while the backward runs
-  if (!jc) {
-    if (aux) {
-      if ((e = hipEventRecord(h->ev_fwd, s)) != hipSuccess || (e = hipStreamWaitEvent(sa, h->ev_fwd, 0)) != hipSuccess)
-        return hip_fail(h, e, "stream fork");
-    }
+  // layer-input Grams (the x1.x2 scalars; per-sample scalars on the batch diagonal)
+  auto grams = [&](hipStream_t st) -> int {
+    hipError_t err;
     if (diag) {
       RowdotBatch rb{};
       rb.count = L + 1;
@@ -766,68 +772,127 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
         rb.K[l] = h->dims[l];
         rb.beta[l] = h->layers[l].has_bias ? 1.0f : 0.0f;
       }
-      prof_begin(P, sa, KC_GRAM);
-      e = launch_rowdot(sa, rb, n1);
-      prof_end(P, sa, KC_GRAM);
-      if (e != hipSuccess) return hip_fail(h, e, "diagonal layer-input scalars");
-    } else {
-      GramBatch gb{};
-      gb.count = L + 1;
-      for (int l = 0; l <= L; ++l) {
-        gb.h1[l] = hptr(l);
-        gb.h2[l] = H2(l);
-        gb.out[l] = F(h->off_gram[l]);
-        gb.K[l] = h->dims[l];
-        gb.beta[l] = h->layers[l].has_bias ? 1.0f : 0.0f;
-      }
-      prof_begin(P, sa, KC_GRAM);
-      e = launch_gram(sa, gb, n1, n2, h->num_cu);
-      prof_end(P, sa, KC_GRAM);
-      if (e != hipSuccess) return hip_fail(h, e, "gram");
+      prof_begin(P, st, KC_GRAM);
+      err = launch_rowdot(st, rb, n1);
+      prof_end(P, st, KC_GRAM);
+      return err == hipSuccess ? NTK_OK : hip_fail(h, err, "diagonal layer-input scalars");
     }
-    if (aux && (e = hipEventRecord(h->ev_gram, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
+    GramBatch gb{};
+    gb.count = L + 1;
+    for (int l = 0; l <= L; ++l) {
+      gb.h1[l] = hptr(l);
+      gb.h2[l] = H2(l);
+      gb.out[l] = F(h->off_gram[l]);
+      gb.K[l] = h->dims[l];
+      gb.beta[l] = h->layers[l].has_bias ? 1.0f : 0.0f;
+    }
+    prof_begin(P, st, KC_GRAM);
+    err = launch_gram(st, gb, n1, n2, h->num_cu);
+    prof_end(P, st, KC_GRAM);
+    return err == hipSuccess ? NTK_OK : hip_fail(h, err, "gram");
+  };
+  // cotangents of the last hidden pre-activation for all O outputs at once (for the one logit o*
+  // alone in NTK_OUTPUT_LOGIT: the cotangent rows are then (n) instead of (n, o)), rows [r0, r1)
+  const float* WL = params[h->param_index[L]] + (logit ? (size_t)h->opt_logit * h->dims[L] : 0);
+  auto seed = [&](hipStream_t st, int r0, int r1) -> int {
+    prof_begin(P, st, KC_BWD_SEED);
+    hipError_t err = launch_bwd_seed(st, WL, F(h->off_dphi[L - 1]) + (size_t)r0 * h->dims[L], r1 - r0, Oe,
+                                     h->dims[L], F(h->off_G[L - 1]) + (size_t)r0 * Oe * h->dims[L]);
+    prof_end(P, st, KC_BWD_SEED);
+    return err == hipSuccess ? NTK_OK : hip_fail(h, err, "backward seed");
+  };
+  // one layer of the cotangent backward for the samples [r0, r1)
+  auto bwd_layer = [&](hipStream_t st, int l, int r0, int r1) -> hipError_t {
+    const size_t K = h->dims[l + 1], N = h->dims[l];
+    return launch_dense_bwd(st, F(h->off_G[l]) + (size_t)r0 * Oe * K, F(h->off_Wt[l]),
+                            F(h->off_dphi[l - 1]) + (size_t)r0 * N, (r1 - r0) * Oe, N, K, Oe,
+                            F(h->off_G[l - 1]) + (size_t)r0 * Oe * N);
+  };
+  auto fork = [&](hipEvent_t ev, hipStream_t from, hipStream_t to) -> int {
+    hipError_t err = hipEventRecord(ev, from);
+    if (err == hipSuccess) err = hipStreamWaitEvent(to, ev, 0);
+    return err == hipSuccess ? NTK_OK : hip_fail(h, err, "stream event");
+  };
+  // The rows (n, o) are independent through the backward, so with a second stream the samples
+  // are split in two halves, each a chain of layer GEMMs on its own stream: one half's partial
+  // last round of tiles and its launch gaps are filled by the other half's work.  Split only when
+  // every layer of a half still fills the chip (at least 2 tiles of 128 x 128 per CU).  The rows
+  // are independent through the forward pass and the seed as well, so these are split with the
+  // backward when every forward layer of a half also runs without split-K partials (a single
+  // buffer); the per-kernel profiler (one bracket open at a time) keeps the forward on one stream.
+  long long min_tiles = -1;
+  for (int l = L - 1; l >= 1; --l) {
+    const long long t = ((long long)(M / 2) * Oe + 127) / 128 * ((h->dims[l] + 127) / 128);
+    min_tiles = min_tiles < 0 ? t : std::min(min_tiles, t);
   }
-  // 3. cotangents of every hidden pre-activation for all O outputs at once (for the one
-  //    logit o* alone in NTK_OUTPUT_LOGIT: the cotangent rows are then (n) instead of (n, o))
-  if (aux && (e = hipStreamWaitEvent(s, h->ev_tr, 0)) != hipSuccess) return hip_fail(h, e, "stream join");
-  if (L >= 1) {
-    const float* WL = params[h->param_index[L]] + (logit ? (size_t)h->opt_logit * h->dims[L] : 0);
-    prof_begin(P, s, KC_BWD_SEED);
-    e = launch_bwd_seed(s, WL, F(h->off_dphi[L - 1]), M, Oe, h->dims[L], F(h->off_G[L - 1]));
-    prof_end(P, s, KC_BWD_SEED);
-    if (e != hipSuccess) return hip_fail(h, e, "backward seed");
-    // The rows (n, o) are independent through the backward, so with a second stream the
-    // samples are split in two halves, each a chain of layer GEMMs on its own stream: the
-    // partial last round of one half's layer overlaps the other half's work.  Split only when
-    // every layer of a half still fills the chip (at least 2 tiles of 128 x 128 per CU).
-    long long min_tiles = -1;
-    for (int l = L - 1; l >= 1; --l) {
-      const long long t = ((long long)(M / 2) * Oe + 127) / 128 * ((h->dims[l] + 127) / 128);
-      min_tiles = min_tiles < 0 ? t : std::min(min_tiles, t);
+  const bool split = aux && L >= 2 && M >= 2 && min_tiles >= 2LL * h->num_cu;
+  const int MA = split ? M / 2 : M;   // samples on the main stream; the rest on the second
+  bool halves = split && !P->enabled;
+  for (int l = 0; l < L && halves; ++l) halves = !dense_fwd_uses_partials(MA, h->dims[l + 1]);
+  int rc;
+  if (halves) {
+    // stream s: the forward and backward of samples [0, MA), then the Grams;
+    // stream aux: the transposes, then the forward and backward of samples [MA, M)
+    if ((rc = fcn_stack(h, params, X1, n1, X2, n2, sym, &h0)) != NTK_OK) return rc;
+    if ((rc = fork(h->ev_fork, s, aux)) != NTK_OK || (rc = transposes(aux)) != NTK_OK) return rc;
+    if ((e = hipEventRecord(h->ev_tr, aux)) != hipSuccess) return hip_fail(h, e, "stream event");
+    for (int l = 0; l < L; ++l) {
+      // one layer at a time on each stream, so that both streams have work enqueued early
+      const float* W = params[h->param_index[l]];
+      const float* b = h->layers[l].has_bias ? params[h->param_index[l] + 1] : nullptr;
+      for (int half = 0; half < 2; ++half) {
+        const int r0 = half ? MA : 0, r1 = half ? M : MA;
+        const float* in = (l == 0 ? h0 : F(h->off_h[l])) + (size_t)r0 * h->dims[l];
+        e = launch_dense_fwd(half ? aux : s, in, W, b, r1 - r0, h->dims[l + 1], h->dims[l], h->layers[l].act,
+                             F(h->off_h[l + 1]) + (size_t)r0 * h->dims[l + 1],
+                             F(h->off_dphi[l]) + (size_t)r0 * h->dims[l + 1], nullptr, 0);
+        if (e != hipSuccess) return hip_fail(h, e, "dense forward");
+      }
     }
-    const bool split = aux && L >= 2 && M >= 2 && min_tiles >= 2LL * h->num_cu;
-    const int MA = split ? M / 2 : M;   // samples on the main stream; the rest on the second
-    if (split && ((e = hipEventRecord(h->ev_seed, s)) != hipSuccess ||
-                  (e = hipStreamWaitEvent(aux, h->ev_seed, 0)) != hipSuccess))
-      return hip_fail(h, e, "stream fork");
-    prof_begin(P, s, KC_DENSE_BWD);
+    if ((e = hipEventRecord(h->ev_fwd, aux)) != hipSuccess) return hip_fail(h, e, "stream event");
+    if ((rc = seed(s, 0, MA)) != NTK_OK || (rc = seed(aux, MA, M)) != NTK_OK) return rc;
+    if ((e = hipStreamWaitEvent(s, h->ev_tr, 0)) != hipSuccess) return hip_fail(h, e, "stream join");
     for (int l = L - 1; l >= 1; --l) {
-      const size_t K = h->dims[l + 1], N = h->dims[l];
-      e = launch_dense_bwd(s, F(h->off_G[l]), F(h->off_Wt[l]), F(h->off_dphi[l - 1]), MA * Oe, N, K, Oe,
-                           F(h->off_G[l - 1]));
-      if (e == hipSuccess && split)
-        e = launch_dense_bwd(aux, F(h->off_G[l]) + (size_t)MA * Oe * K, F(h->off_Wt[l]),
-                             F(h->off_dphi[l - 1]) + (size_t)MA * N, (M - MA) * Oe, N, K, Oe,
-                             F(h->off_G[l - 1]) + (size_t)MA * Oe * N);
+      e = bwd_layer(s, l, 0, MA);
+      if (e == hipSuccess) e = bwd_layer(aux, l, MA, M);
       if (e != hipSuccess) return hip_fail(h, e, "dense backward");
     }
-    if (split && ((e = hipEventRecord(h->ev_bwd, aux)) != hipSuccess ||
-                  (e = hipStreamWaitEvent(s, h->ev_bwd, 0)) != hipSuccess))
+    if ((e = hipEventRecord(h->ev_bwd, aux)) != hipSuccess) return hip_fail(h, e, "stream event");
+    if (!jc) {
+      if ((e = hipStreamWaitEvent(s, h->ev_fwd, 0)) != hipSuccess) return hip_fail(h, e, "stream join");
+      if ((rc = grams(s)) != NTK_OK) return rc;
+    }
+    if ((e = hipStreamWaitEvent(s, h->ev_bwd, 0)) != hipSuccess) return hip_fail(h, e, "stream join");
+  } else {
+    // 0. weight transposes for the backward, on the second stream while the forward runs
+    if (aux && (rc = fork(h->ev_fork, s, aux)) != NTK_OK) return rc;
+    if ((rc = transposes(sa)) != NTK_OK) return rc;
+    if (aux && (e = hipEventRecord(h->ev_tr, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
+    // 1. forward pass keeping the layer inputs
+    if ((rc = fcn_forward(h, params, X1, n1, X2, n2, sym, &h0)) != NTK_OK) return rc;
+    // 2. the Grams, on the second stream while the backward runs
+    if (!jc) {
+      if (aux && (rc = fork(h->ev_fwd, s, sa)) != NTK_OK) return rc;
+      if ((rc = grams(sa)) != NTK_OK) return rc;
+      if (aux && (e = hipEventRecord(h->ev_gram, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
+    }
+    // 3. the cotangents of every hidden pre-activation
+    if (aux && (e = hipStreamWaitEvent(s, h->ev_tr, 0)) != hipSuccess) return hip_fail(h, e, "stream join");
+    if (L >= 1) {
+      if ((rc = seed(s, 0, M)) != NTK_OK) return rc;
+      if (split && (rc = fork(h->ev_seed, s, aux)) != NTK_OK) return rc;
+      prof_begin(P, s, KC_DENSE_BWD);
+      for (int l = L - 1; l >= 1; --l) {
+        e = bwd_layer(s, l, 0, MA);
+        if (e == hipSuccess && split) e = bwd_layer(aux, l, MA, M);
+        if (e != hipSuccess) return hip_fail(h, e, "dense backward");
+      }
+      if (split && (rc = fork(h->ev_bwd, aux, s)) != NTK_OK) return rc;
+      prof_end(P, s, KC_DENSE_BWD);
+    }
+    if (!jc && aux && (e = hipStreamWaitEvent(s, h->ev_gram, 0)) != hipSuccess)
       return hip_fail(h, e, "stream join");
-    prof_end(P, s, KC_DENSE_BWD);
   }
-  if (!jc && aux && (e = hipStreamWaitEvent(s, h->ev_gram, 0)) != hipSuccess)
-    return hip_fail(h, e, "stream join");
   auto G1 = [&](int l) -> const float* { return F(h->off_G[l]); };
   auto G2 = [&](int l) -> const float* {
     return sym ? F(h->off_G[l]) : F(h->off_G[l]) + (size_t)n1 * Oe * h->dims[l + 1];
