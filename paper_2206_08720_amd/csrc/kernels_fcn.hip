@@ -121,10 +121,6 @@ k_dense_fwd_reduce(const double* __restrict__ part, int splits, int M, int N, co
   }
 }
 
-bool dense_fwd_uses_partials(int M, int N) {
-  return (long long)cdiv(M, CfgFwd64::BM) * cdiv(N, CfgFwd64::BN) < kFwdSplitTiles;
-}
-
 long long dense_fwd_part_doubles(long long max_rows, long long max_cols) {
   // the split form only runs below kFwdSplitTiles output tiles of 64 x 64
   return std::min<long long>(kFwdMaxSplits * max_rows * max_cols,

@@ -55,8 +55,6 @@ long long dense_fwd_part_doubles(long long max_rows, long long max_cols);
 hipError_t launch_dense_fwd(hipStream_t s, const float* h, const float* W, const float* b, int M,
                             int N, int K, int act, float* hn, float* dphi, double* part,
                             long long part_capacity);
-// Whether launch_dense_fwd with a partial buffer would split K (few output tiles) for M x N.
-bool dense_fwd_uses_partials(int M, int N);
 // out[r, c] = (sum_k G[r, k] Wt[c, k]) * dphi[(r / O), c].  G [R, K], Wt [N, K], dphi [R/O, N].
 hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, const float* dphi,
                             int R, int N, int K, int O, float* out);

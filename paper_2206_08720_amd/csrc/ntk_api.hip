@@ -818,8 +818,8 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   // last round of tiles and its launch gaps are filled by the other half's work.  Split only when
   // every layer of a half still fills the chip (at least 2 tiles of 128 x 128 per CU).  The rows
   // are independent through the forward pass and the seed as well, so these are split with the
-  // backward when every forward layer of a half also runs without split-K partials (a single
-  // buffer); the per-kernel profiler (one bracket open at a time) keeps the forward on one stream.
+  // backward (each half's split-K forward, if any, takes its own half of the partial buffer); the
+  // per-kernel profiler (one bracket open at a time) keeps the forward on one stream.
   long long min_tiles = -1;
   for (int l = L - 1; l >= 1; --l) {
     const long long t = ((long long)(M / 2) * Oe + 127) / 128 * ((h->dims[l] + 127) / 128);
@@ -827,8 +827,7 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   }
   const bool split = aux && L >= 2 && M >= 2 && min_tiles >= 2LL * h->num_cu;
   const int MA = split ? M / 2 : M;   // samples on the main stream; the rest on the second
-  bool halves = split && !P->enabled;
-  for (int l = 0; l < L && halves; ++l) halves = !dense_fwd_uses_partials(MA, h->dims[l + 1]);
+  const bool halves = split && !P->enabled;
   int rc;
   if (halves) {
     // stream s: the forward and backward of samples [0, MA), then the Grams;
@@ -843,9 +842,11 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
       for (int half = 0; half < 2; ++half) {
         const int r0 = half ? MA : 0, r1 = half ? M : MA;
         const float* in = (l == 0 ? h0 : F(h->off_h[l])) + (size_t)r0 * h->dims[l];
+        const long long cap = h->fpart_capacity / 2;
+        double* part = h->fpart_capacity ? reinterpret_cast<double*>(h->ws + h->off_fpart) + half * cap : nullptr;
         e = launch_dense_fwd(half ? aux : s, in, W, b, r1 - r0, h->dims[l + 1], h->dims[l], h->layers[l].act,
                              F(h->off_h[l + 1]) + (size_t)r0 * h->dims[l + 1],
-                             F(h->off_dphi[l]) + (size_t)r0 * h->dims[l + 1], nullptr, 0);
+                             F(h->off_dphi[l]) + (size_t)r0 * h->dims[l + 1], part, part ? cap : 0);
         if (e != hipSuccess) return hip_fail(h, e, "dense forward");
       }
     }
