@@ -1065,10 +1065,10 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   const int Oe = logit ? 1 : O;
   const double pairs = diag ? (double)n1 : (double)n1 * n2;
   const double Oc = trace ? (double)O : (double)Oe * Oe;   // output pairs per input pair
-  // contraction order of each 3x3 (F = 9 taps) or pointwise (F = 1) convolution: the cost model
-  // of the appendix "CNN NTK Complexity" (outside-in N1 N2 O^2 F Cin Cout plus forming J,
-  // N O D F Cin Cout per sample, against inside-out N1 N2 (D^2 F Cin + O D^2 Cout + O^2 D Cout)),
-  // with the inside-out FLOPs weighted by their measured time per FLOP, or the forced option.  Depthwise
+  // contraction order of each 3x3 (F = 9 taps) or pointwise (F = 1) convolution: the outside-in
+  // cost of the appendix "CNN NTK Complexity" (N1 N2 O^2 F Cin Cout plus forming J, N O D F Cin Cout
+  // per sample) against the matrix-core work the inside-out kernel executes (inside_out_cost), or
+  // the forced option; inside-out only for images of at most 64 pixels.  Depthwise
   // and scale layers (block-diagonal weight-space Jacobians, 9 C and C columns) and every bias
   // (output block-tiled, C columns) always contract outside-in: their O^2 P term is the
   // smallest of the orders there.
