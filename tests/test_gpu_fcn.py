@@ -249,3 +249,24 @@ def test_backward_split_over_two_streams_with_an_odd_batch():
     jc, e1, e2 = oracle.ntk_jc_with_norms(spec, params, X1[[0, 410]], X2[[0, 1, 411]], layer_storage=S)
     cs, nw = errors(got[np.ix_([0, 410], [0, 1, 411])], jc, e1, e2)
     assert cs <= TOL and nw <= TOL
+
+
+def test_sample_halves_schedule_matches_one_stream_bit_for_bit():
+    # 512 + 512 samples of a width-2048 FCN: the forward, seed and backward run as two sample
+    # halves on the two streams (each half still makes 8 x 32 forward tiles, no split-K, and
+    # 40 x 16 backward tiles); with per-kernel profiling on, the forward runs on one stream.  Every
+    # row's sums keep their order either way, so the two Theta are equal bit for bit.
+    spec = wl.fcn_spec("halves", 64, [2048, 2048], 10)
+    params = wl.make_params(spec, 81, "2/fan_in")
+    X1 = wl.make_inputs(spec, 512, 82)
+    X2 = wl.make_inputs(spec, 512, 83)
+    got = gpu_ntk(spec, params, X1, X2)
+    prof = {}
+    one_stream = gpu_ntk(spec, params, X1, X2, profile=prof)
+    assert "dense_fwd" in prof
+    assert np.array_equal(got, one_stream)
+    sub1, sub2 = [0, 255, 511], [0, 256, 511]
+    jc, e1, e2 = oracle.ntk_jc_with_norms(spec, params, X1[sub1], X2[sub2], layer_storage=S)
+    cs, nw = errors(got[np.ix_(sub1, sub2)], jc, e1, e2)
+    report("sample-halves schedule, sampled rows vs JC", cs, nw)
+    assert cs <= TOL and nw <= TOL
