@@ -669,6 +669,35 @@ hipError_t launch_conv_flip(hipStream_t s, const float* K, int Cout, int Cin, fl
   return hipGetLastError();
 }
 
+// Kernel z of the batch: blockIdx.y; tap t of T is read from tap T - 1 - t (the 3x3 flip:
+// (kh, kw) -> (2 - kh, 2 - kw); with T = 1 a transpose).
+__global__ void __launch_bounds__(256) k_conv_flip_batch(FlipBatch b) {
+  const int z = blockIdx.y;
+  const int Cout = b.Cout[z], Cin = b.Cin[z], T = b.taps[z];
+  const int total = Cout * T * Cin;
+  const float* __restrict__ K = b.K[z];
+  float* __restrict__ Kt = b.Kt[z];
+  for (int i = blockIdx.x * blockDim.x + threadIdx.x; i < total; i += gridDim.x * blockDim.x) {
+    const int co = i % Cout;
+    const int rest = i / Cout;
+    const int tap = rest % T, ci = rest / T;
+    Kt[i] = K[((long long)co * T + (T - 1 - tap)) * Cin + ci];
+  }
+}
+
+hipError_t launch_conv_flip_batch(hipStream_t s, const FlipBatch& b) {
+  if (b.count <= 0) return hipSuccess;
+  if (b.count > kMaxLayers) return hipErrorInvalidValue;
+  long long most = 0;
+  for (int z = 0; z < b.count; ++z) {
+    if (b.taps[z] != 1 && b.taps[z] != 9) return hipErrorInvalidValue;
+    most = std::max(most, (long long)b.Cout[z] * b.taps[z] * b.Cin[z]);
+  }
+  if (most >= (1LL << 31)) return hipErrorInvalidValue;
+  k_conv_flip_batch<<<dim3((unsigned)std::min<long long>(cdiv(most, 256), 1024), b.count), dim3(256), 0, s>>>(b);
+  return hipGetLastError();
+}
+
 // ------------------------------------------------------------------------------ backward
 // Epilogue of the per-sample weight-space product of sample s: J[(s*O + o)*ldJ + off + c*KC + k]
 // = acc[r = o*C + c, k].  A fragment inside R = O*C and inside one o (no multiple of C in

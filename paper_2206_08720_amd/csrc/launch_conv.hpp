@@ -17,6 +17,15 @@ hipError_t launch_conv_seed(hipStream_t s, const float* Wd, const float* dphi, i
                             int D, int C, float* G);
 // Kt [Cin, 3, 3, Cout] = K [Cout, 2-kh, 2-kw, Cin]  (the kernel of the transposed convolution).
 hipError_t launch_conv_flip(hipStream_t s, const float* K, int Cout, int Cin, float* Kt);
+// The same for several layers in one launch: Kt_z [Cin_z, T_z, Cout_z] = K_z [Cout_z, T_z - 1 - t, Cin_z]
+// for z < count, T_z = 9 (a 3x3 kernel flipped) or 1 (a pointwise kernel transposed).
+struct FlipBatch {
+  const float* K[kMaxLayers];
+  float* Kt[kMaxLayers];
+  int Cout[kMaxLayers], Cin[kMaxLayers], taps[kMaxLayers];
+  int count;
+};
+hipError_t launch_conv_flip_batch(hipStream_t s, const FlipBatch& b);
 // out [images*O, D, Cin] = conv3x3(G [images*O, H, W, Cg], Kt [Cin, 3, 3, Cg]) * dphi [images, D, Cin]
 // (dphi null: the identity).
 hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,

@@ -1140,15 +1140,23 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   if (e != hipSuccess) return hip_fail(h, e, "gram");
   // 2. cotangents of every spatial layer's output for all O outputs, and per layer its
   //    weight-space cotangent columns of J (or its inside-out summand)
-  for (int l = 1; l < nc; ++l) {
-    const int kind = h->layers[l].kind;
-    if (kind != NTK_CONV3X3_SAME && kind != NTK_CONV1X1) continue;
+  {
+    // the flipped 3x3 kernels and transposed pointwise ones of the backward, in one launch
+    FlipBatch fb{};
+    for (int l = 1; l < nc; ++l) {
+      const int kind = h->layers[l].kind;
+      if (kind != NTK_CONV3X3_SAME && kind != NTK_CONV1X1) continue;
+      fb.K[fb.count] = params[h->wslot[l]];
+      fb.Kt[fb.count] = F(h->off_Kt[l]);
+      fb.Cout[fb.count] = h->ch[l + 1];
+      fb.Cin[fb.count] = h->ch[l];
+      fb.taps[fb.count] = kind == NTK_CONV3X3_SAME ? 9 : 1;
+      ++fb.count;
+    }
     prof_begin(P, s, KC_TRANSPOSE);
-    e = kind == NTK_CONV3X3_SAME
-            ? launch_conv_flip(s, params[h->wslot[l]], h->ch[l + 1], h->ch[l], F(h->off_Kt[l]))
-            : launch_transpose(s, params[h->wslot[l]], h->ch[l + 1], h->ch[l], F(h->off_Kt[l]));
+    e = launch_conv_flip_batch(s, fb);
     prof_end(P, s, KC_TRANSPOSE);
-    if (e != hipSuccess) return hip_fail(h, e, "kernel flip / transpose");
+    if (e != hipSuccess) return hip_fail(h, e, "kernel flips / transposes");
   }
   float* Gcur = F(h->off_Gping);
   float* Gnext = F(h->off_Gpong);
