@@ -287,19 +287,33 @@ struct DmaPatches {
   template <int WV>
   static constexpr int OPS = ROWS / (8 * WV);
   __amdgpu_buffer_rsrc_t rsrc;
-  int base[NI], y[NI], xx[NI], ok[NI];
+  // per issued row: the byte offset of its pixel's 16-byte chunk (tap (1, 1), channel block 0)
+  // and a 9-bit mask, bit t set when tap t of the pixel lies inside the image (none for rows
+  // past the end), so that an issue is a bit test, an add of the K tile's uniform tap offset and a
+  // select
+  int base4[NI];
+  unsigned tmask[NI];
   __device__ __forceinline__ void prepare(int row0, int wave, int lane) {
     rsrc = buffer_rsrc(x, (uint32_t)((long long)rows * C * 4));
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const int row = row0 + (i * WAVES + wave) * 8 + (lane >> 3);
+      const int r = (i * WAVES + wave) * 8 + (lane >> 3);
+      const int row = row0 + r;
       const int rc = min(row, rows - 1);
       const int img = (int)fD.div(rc), p = rc - img * (int)fD.d;
       const int yy = (int)fW.div(p), xq = p - yy * W;
-      base[i] = ((img * H + yy) * W + xq) * C;
-      y[i] = yy;
-      xx[i] = xq;
-      ok[i] = row < rows ? 1 : 0;
+      const int c = DmaTile<ROWS>::swz(r, lane & 7);   // global chunk stored at lane & 7
+      base4[i] = (((img * H + yy) * W + xq) * C + 4 * c) * 4;
+      // opaque: the compiler would otherwise re-derive the offset from its factors at every
+      // issue (a 64-bit multiply-add and three more instructions per row)
+      asm volatile("" : "+v"(base4[i]));
+      unsigned m = 0;
+#pragma unroll
+      for (int t = 0; t < 9; ++t) {
+        const int ky = yy + t / 3 - 1, kx = xq + t % 3 - 1;
+        m |= ((unsigned)ky < (unsigned)H && (unsigned)kx < (unsigned)W) ? (1u << t) : 0u;
+      }
+      tmask[i] = row < rows ? m : 0u;
     }
   }
   template <int WV>
@@ -307,15 +321,11 @@ struct DmaPatches {
     static_assert(WV == WAVES, "issuer built for this workgroup shape");
     const int t = (int)fC.div(k0), cb = k0 - t * C;
     const int kh = (t * 11) >> 5, kw = t - 3 * kh;
-    const int tapoff = ((kh - 1) * W + (kw - 1)) * C + cb;
+    const int tapoff4 = (((kh - 1) * W + (kw - 1)) * C + cb) * 4;   // uniform
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int r0 = (i * WAVES + wave) * 8;
-      const int r = r0 + (lane >> 3);
-      const int c = DmaTile<ROWS>::swz(r, lane & 7);
-      const int yy = y[i] + kh - 1, xq = xx[i] + kw - 1;
-      const bool good = ok[i] & ((unsigned)yy < (unsigned)H) & ((unsigned)xq < (unsigned)W);
-      const uint32_t voff = good ? (uint32_t)(base[i] + tapoff + 4 * c) * 4u : kDmaPastEnd;
+      const uint32_t voff = (tmask[i] >> t) & 1u ? (uint32_t)(base4[i] + tapoff4) : kDmaPastEnd;
       buffer_dma16(rsrc, voff, 0, lds + __builtin_amdgcn_readfirstlane(r0 * DmaTile<ROWS>::BK));
     }
   }
