@@ -367,7 +367,10 @@ struct DmaCotangentKOuter {
   template <int WV>
   static constexpr int OPS = ROWS / (8 * WV);
   __amdgpu_buffer_rsrc_t rsrc;
-  int off[NI], kl[NI], ok[NI];
+  // per issued row: the byte offset of its 16-byte chunk at pixel kl (the K tile's first pixel
+  // k0 adds the uniform k0 C 4 through the scalar offset) and the bound k0 < klim of the pixels
+  // inside the sample (klim = D - kl; none for rows past the end)
+  int base4[NI], klim[NI];
   __device__ __forceinline__ void prepare(int row0, int wave, int lane) {
     rsrc = buffer_rsrc(g, (uint32_t)((long long)rows * D * 4));
 #pragma unroll
@@ -377,19 +380,19 @@ struct DmaCotangentKOuter {
       const int row = row0 + 4 * Tile::swz(k, pos);
       const int rc = min(row, rows - 4);
       const int oo = (int)fC.div(rc), cc = rc - oo * C;
-      off[i] = oo * D * C + cc;
-      kl[i] = k;
-      ok[i] = row < rows ? 1 : 0;
+      base4[i] = (oo * D * C + cc + k * C) * 4;
+      asm volatile("" : "+v"(base4[i]));   // kept whole, not re-derived at each issue
+      klim[i] = row < rows ? D - k : -1;
     }
   }
   template <int WV>
   __device__ __forceinline__ void issue(int k0, float* lds, int wave, int lane) const {
     static_assert(WV == WAVES, "issuer built for this workgroup shape");
+    const uint32_t soff = (uint32_t)k0 * C * 4u;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const int p = k0 + kl[i];
-      const uint32_t voff = (ok[i] & (p < D)) ? (uint32_t)(off[i] + p * C) * 4u : kDmaPastEnd;
-      buffer_dma16(rsrc, voff, 0, lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256));
+      const uint32_t voff = k0 < klim[i] ? (uint32_t)base4[i] : kDmaPastEnd;
+      buffer_dma16(rsrc, voff, soff, lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256));
     }
   }
 };
@@ -405,9 +408,13 @@ struct DmaPatchesKOuter {
   template <int WV>
   static constexpr int OPS = ROWS / (8 * WV);
   __amdgpu_buffer_rsrc_t rsrc;
-  int kl[NI], dy[NI], dx[NI], ci[NI], ok[NI];
+  // per issued row (tap (dy, dx), channel ci) at pixel kl of the K tile: the byte offset of its
+  // shifted pixel kl + dy W + dx through a resource that starts W + 1 pixels before the sample
+  // (so the offset is never negative; the K tile's first pixel k0 adds the uniform k0 C 4 through
+  // the scalar offset), and what the tap's bounds test needs
+  int base4[NI], kl[NI], dy[NI], dx[NI], ok[NI];
   __device__ __forceinline__ void prepare(int row0, int wave, int lane) {
-    rsrc = buffer_rsrc(x, (uint32_t)((long long)K * C * 4));
+    rsrc = buffer_rsrc(x - (long long)(W + 1) * C, (uint32_t)((long long)(K + W + 1) * C * 4));
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int o = (i * WAVES + wave) * 256 + 4 * lane;
@@ -416,25 +423,35 @@ struct DmaPatchesKOuter {
       const int rc = min(row, rows - 4);
       const int t = (int)fC.div(rc);
       const int kh = (t * 11) >> 5, kw = t - 3 * kh;
+      const int ci = rc - t * C;
       kl[i] = k;
       dy[i] = kh - 1;
       dx[i] = kw - 1;
-      ci[i] = rc - t * C;
+      base4[i] = ((k + (kh - 1) * W + (kw - 1) + W + 1) * C + ci) * 4;
+      asm volatile("" : "+v"(base4[i]));   // kept whole, not re-derived at each issue
       ok[i] = row < rows ? 1 : 0;
     }
   }
   template <int WV>
   __device__ __forceinline__ void issue(int k0, float* lds, int wave, int lane) const {
     static_assert(WV == WAVES, "issuer built for this workgroup shape");
+    const uint32_t soff = (uint32_t)k0 * C * 4u;
+    const bool row32 = W % 32 == 0;   // a K tile of 32 pixels (k0 % 32 == 0) lies in one image row
+    const int y0 = (int)fW.div(k0), x0 = k0 - y0 * W;   // uniform
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const int p = k0 + kl[i];
-      const int pc = min(p, K - 1);
-      const int y = (int)fW.div(pc), xx = pc - y * W;
-      const int yy = y + dy[i], xq = xx + dx[i];
-      const bool good = ok[i] & (p < K) & ((unsigned)yy < (unsigned)H) & ((unsigned)xq < (unsigned)W);
-      const uint32_t voff = good ? (uint32_t)((yy * W + xq) * C + ci[i]) * 4u : kDmaPastEnd;
-      buffer_dma16(rsrc, voff, 0, lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256));
+      bool good;
+      if (row32) {
+        good = ok[i] & (kl[i] < K - k0) & ((unsigned)(y0 + dy[i]) < (unsigned)H) &
+               ((unsigned)(x0 + kl[i] + dx[i]) < (unsigned)W);
+      } else {
+        const int p = k0 + kl[i];
+        const int pc = min(p, K - 1);
+        const int y = (int)fW.div(pc), xx = pc - y * W;
+        good = ok[i] & (p < K) & ((unsigned)(y + dy[i]) < (unsigned)H) & ((unsigned)(xx + dx[i]) < (unsigned)W);
+      }
+      const uint32_t voff = good ? (uint32_t)base4[i] : kDmaPastEnd;
+      buffer_dma16(rsrc, voff, soff, lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256));
     }
   }
 };
