@@ -767,25 +767,27 @@ __device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, in
   static_assert(NSTAGE >= 2 && NSTAGE <= 4, "two to four LDS stages");
   ia.prepare(m0, wave, lane);
   ib.prepare(n0, wave, lane);
-  auto stage = [&](int kt) { return smem + (kt % NSTAGE) * STAGE; };
-  auto issue = [&](int kt) {
-    float* st = stage(kt);
+  // tile kt lives in stage kt % NSTAGE; the K loop is unrolled NSTAGE times so that every stage
+  // offset is a compile-time constant (the fragment reads then take it as an immediate offset
+  // instead of recomputing their addresses at every K tile)
+  auto issue = [&](int kt, float* st) {
     ia.template issue<Cfg::WAVES>(k_begin + kt * 32, st, wave, lane);
     ib.template issue<Cfg::WAVES>(k_begin + kt * 32, st + TA::FLOATS, wave, lane);
   };
   // tiles 0 .. NSTAGE - 2 in flight
   const int pre = nk < NSTAGE - 1 ? nk : NSTAGE - 1;
-  for (int j = 0; j < pre; ++j) issue(j);
+  for (int j = 0; j < pre; ++j) issue(j, smem + j * STAGE);
   // tile 0 in LDS (the later tiles' loads may stay in flight: loads complete in order); a bare
   // s_barrier (no fence, which would drain every outstanding load) makes it visible to every wave
   wait_vmcnt_dyn((pre - 1) * PER_TILE);
   __builtin_amdgcn_s_barrier();
   __builtin_amdgcn_sched_barrier(0);
   typename MB::Frag f[2];
-  MB::load(stage(0), stage(0) + TA::FLOATS, 0, wm0, wn0, lane, f[0]);
-  for (int kt = 0; kt < nk; ++kt) {
-    const float* st = stage(kt);
-    if (kt + NSTAGE - 1 < nk) issue(kt + NSTAGE - 1);
+  MB::load(smem, smem + TA::FLOATS, 0, wm0, wn0, lane, f[0]);
+  auto tile = [&](int kt, auto stage_tag) {
+    constexpr int S = decltype(stage_tag)::value;
+    const float* st = smem + S * STAGE;
+    if (kt + NSTAGE - 1 < nk) issue(kt + NSTAGE - 1, smem + ((S + NSTAGE - 1) % NSTAGE) * STAGE);
 #pragma unroll
     for (int blk = 0; blk + 1 < MB::NB; ++blk) {
       MB::load(st, st + TA::FLOATS, blk + 1, wm0, wn0, lane, f[(blk + 1) & 1]);
@@ -800,13 +802,27 @@ __device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, in
       wait_vmcnt_lgkm0_dyn((later > 0 ? later : 0) * PER_TILE);
       __builtin_amdgcn_s_barrier();
       __builtin_amdgcn_sched_barrier(0);
-      const float* sn = stage(kt + 1);
+      const float* sn = smem + ((S + 1) % NSTAGE) * STAGE;
       MB::load(sn, sn + TA::FLOATS, 0, wm0, wn0, lane, f[0]);
       __builtin_amdgcn_sched_barrier(0);
     }
     MB::mma(f[(MB::NB - 1) & 1], acc);
     __builtin_amdgcn_sched_barrier(0);
+  };
+  // whole groups of NSTAGE tiles, then the remainder (no tile of the loop body is conditional,
+  // which would make the accumulators flow through two paths and be copied at every iteration)
+  int kb = 0;
+  for (; kb + NSTAGE <= nk; kb += NSTAGE) {
+    tile(kb, std::integral_constant<int, 0>{});
+    tile(kb + 1, std::integral_constant<int, 1>{});
+    if constexpr (NSTAGE > 2) tile(kb + 2, std::integral_constant<int, 2>{});
+    if constexpr (NSTAGE > 3) tile(kb + 3, std::integral_constant<int, 3>{});
   }
+  if (kb < nk) tile(kb, std::integral_constant<int, 0>{});
+  if constexpr (NSTAGE > 2)
+    if (kb + 1 < nk) tile(kb + 1, std::integral_constant<int, 1>{});
+  if constexpr (NSTAGE > 3)
+    if (kb + 2 < nk) tile(kb + 2, std::integral_constant<int, 2>{});
   __syncthreads();
 }
 

@@ -287,14 +287,16 @@ struct DmaPatches {
   template <int WV>
   static constexpr int OPS = ROWS / (8 * WV);
   __amdgpu_buffer_rsrc_t rsrc;
-  // per issued row: the byte offset of its pixel's 16-byte chunk (tap (1, 1), channel block 0)
-  // and a 9-bit mask, bit t set when tap t of the pixel lies inside the image (none for rows
-  // past the end), so that an issue is a bit test, an add of the K tile's uniform tap offset and a
-  // select
+  // per issued row: the byte offset of its pixel's 16-byte chunk (channel block 0) through a
+  // resource that starts W + 1 pixels before the batch, so that every tap's shift is a
+  // non-negative uniform offset (the scalar offset of the load), and a 9-bit mask, bit t set
+  // when tap t of the pixel lies OUTSIDE the image (all set for rows past the end).  An issue
+  // is then a bit extract and a shift-or: the offset with bit 31 set is past the resource's end
+  // (base4 + the largest tap offset stays below 2^31), which loads zeros.
   int base4[NI];
-  unsigned tmask[NI];
+  unsigned omask[NI];
   __device__ __forceinline__ void prepare(int row0, int wave, int lane) {
-    rsrc = buffer_rsrc(x, (uint32_t)((long long)rows * C * 4));
+    rsrc = buffer_rsrc(x - (long long)(W + 1) * C, (uint32_t)((long long)(rows + 2 * (W + 1)) * C * 4));
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int r = (i * WAVES + wave) * 8 + (lane >> 3);
@@ -311,9 +313,9 @@ struct DmaPatches {
 #pragma unroll
       for (int t = 0; t < 9; ++t) {
         const int ky = yy + t / 3 - 1, kx = xq + t % 3 - 1;
-        m |= ((unsigned)ky < (unsigned)H && (unsigned)kx < (unsigned)W) ? (1u << t) : 0u;
+        m |= ((unsigned)ky < (unsigned)H && (unsigned)kx < (unsigned)W) ? 0u : (1u << t);
       }
-      tmask[i] = row < rows ? m : 0u;
+      omask[i] = row < rows ? m : 0x1FFu;
     }
   }
   template <int WV>
@@ -321,12 +323,12 @@ struct DmaPatches {
     static_assert(WV == WAVES, "issuer built for this workgroup shape");
     const int t = (int)fC.div(k0), cb = k0 - t * C;
     const int kh = (t * 11) >> 5, kw = t - 3 * kh;
-    const int tapoff4 = (((kh - 1) * W + (kw - 1)) * C + cb) * 4;   // uniform
+    const uint32_t soff = (uint32_t)(((kh * W + kw) * C + cb) * 4);   // uniform, >= 0
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
       const int r0 = (i * WAVES + wave) * 8;
-      const uint32_t voff = (tmask[i] >> t) & 1u ? (uint32_t)(base4[i] + tapoff4) : kDmaPastEnd;
-      buffer_dma16(rsrc, voff, 0, lds + __builtin_amdgcn_readfirstlane(r0 * DmaTile<ROWS>::BK));
+      const uint32_t voff = (((omask[i] >> t) & 1u) << 31) | (uint32_t)base4[i];
+      buffer_dma16(rsrc, voff, soff, lds + __builtin_amdgcn_readfirstlane(r0 * DmaTile<ROWS>::BK));
     }
   }
 };
@@ -346,9 +348,10 @@ static DmaPatches<ROWS, WAVES> dma_patches(const float* x, int images, int H, in
 }
 
 // The direct-to-LDS path needs C % 32 == 0, 16-byte aligned operands, an activation batch of
-// `elems` floats and weight tiles within the buffer-resource span.
-static bool conv_dma_ok(const void* x, long long elems, int C, const void* K) {
-  return C % 32 == 0 && aligned16(x) && aligned16(K) && elems * 4 < (1LL << 31) &&
+// `elems` floats (images of width W) and weight tiles within the buffer-resource span; the
+// patch resource spans the batch and W + 1 pixels on either side.
+static bool conv_dma_ok(const void* x, long long elems, int W, int C, const void* K) {
+  return C % 32 == 0 && aligned16(x) && aligned16(K) && (elems + 2LL * (W + 1) * C) * 4 < (1LL << 31) &&
          dma_span_ok(9LL * C, 9LL * C, 256);
 }
 
@@ -540,7 +543,7 @@ static hipError_t conv_fwd_dma_cfg(hipStream_t s, const float* x, int images, in
 
 hipError_t launch_conv_fwd(hipStream_t s, const float* x, int images, int H, int W, int Cin,
                            const float* K, int Cout, int act, const float* bias, float* hn, float* dphi) {
-  if (conv_dma_ok(x, (long long)images * H * W * Cin, Cin, K)) {
+  if (conv_dma_ok(x, (long long)images * H * W * Cin, W, Cin, K)) {
     const long long tiles = (long long)cdiv((long long)images * H * W, CfgConvF64::BM) * cdiv(Cout, CfgConvF64::BN);
     if (tiles < kConvFewTiles)
       return conv_fwd_dma_cfg<CfgConvF64Small>(s, x, images, H, W, Cin, K, Cout, act, bias, hn, dphi);
@@ -836,7 +839,7 @@ static hipError_t conv_bwd_dma_cfg(hipStream_t s, const float* G, int images, in
 
 hipError_t launch_conv_bwd(hipStream_t s, const float* G, int images, int O, int H, int W, int Cg,
                            const float* Kt, int Cin, const float* dphi, float* out) {
-  if (conv_dma_ok(G, (long long)images * O * H * W * Cg, Cg, Kt)) {
+  if (conv_dma_ok(G, (long long)images * O * H * W * Cg, W, Cg, Kt)) {
     const long long tiles = (long long)cdiv((long long)images * O * H * W, CfgConvBwd::BM) * cdiv(Cin, CfgConvBwd::BN);
     if (tiles < kConvFewTiles) return conv_bwd_dma_cfg<CfgConv>(s, G, images, O, H, W, Cg, Kt, Cin, dphi, out);
     return conv_bwd_dma_cfg<CfgConvBwd>(s, G, images, O, H, W, Cg, Kt, Cin, dphi, out);

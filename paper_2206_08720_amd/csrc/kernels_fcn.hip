@@ -27,6 +27,8 @@ constexpr int kSkPerCu = 2, kSkStages = 2;
 // LDS stages of the direct-to-LDS loop of the layer-split contraction (64 x 64 tiles): two
 // stages (32 KB) let four workgroups share a compute unit
 constexpr int kSplitStages = 2;
+// LDS stages of the Grams' direct-to-LDS loop (64 x 64 tiles)
+constexpr int kGramStages = 3;
 // the forward splits K (up to kFwdMaxSplits ways) below kFwdSplitTiles output tiles
 constexpr int kFwdSplitTiles = 256, kFwdMaxSplits = 8;
 using CfgSmall = TileCfg<64, 64, 32, 32, 32>;   // 4 waves, 32x32 per wave
@@ -470,7 +472,7 @@ hipError_t launch_transpose_batch(hipStream_t s, const TransposeBatch& b) {
 }
 
 // ------------------------------------------------------------------------------ Grams
-template <class Cfg, bool VEC>
+template <class Cfg, bool VEC, bool DMA>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_gram(GramBatch g, int N1, int N2, int tiles_n) {
   extern __shared__ float smem[];
@@ -478,11 +480,15 @@ k_gram(GramBatch g, int N1, int N2, int tiles_n) {
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
   const int K = g.K[z];
-  LoadKInnerT<VEC> la{g.h1[z], N1, K, K};
-  LoadKInnerT<VEC> lb{g.h2[z], N2, K, K};
   f32x16 acc[Cfg::FM][Cfg::FN];
   zero_acc<Cfg>(acc);
-  gemm_mainloop<Cfg>(la, lb, m0, n0, 0, K, smem, acc);
+  if (DMA) {
+    gemm_mainloop_dma<Cfg, kGramStages>(g.h1[z], K, N1, g.h2[z], K, N2, m0, n0, 0, K, smem, acc);
+  } else {
+    LoadKInnerT<VEC> la{g.h1[z], N1, K, K};
+    LoadKInnerT<VEC> lb{g.h2[z], N2, K, K};
+    gemm_mainloop<Cfg>(la, lb, m0, n0, 0, K, smem, acc);
+  }
   float* out = g.out[z];
   const float beta = g.beta[z];
   for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, float v) {
@@ -490,15 +496,16 @@ k_gram(GramBatch g, int N1, int N2, int tiles_n) {
   });
 }
 
-template <bool VEC>
+template <bool VEC, bool DMA>
 static hipError_t gram_vec(hipStream_t s, const GramBatch& g, int N1, int N2) {
   using Cfg = CfgSmall;
   using L = LoadKInnerT<VEC>;
   const int tn = cdiv(N2, Cfg::BN), tm = cdiv(N1, Cfg::BM);
-  hipError_t e = set_smem<Cfg, L, L>((const void*)k_gram<Cfg, VEC>);
+  constexpr int bytes = DMA ? gemm_dma_smem_bytes<Cfg, kGramStages>() : gemm_smem_bytes<Cfg, L, L>();
+  hipError_t e = hipFuncSetAttribute((const void*)k_gram<Cfg, VEC, DMA>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
   if (e != hipSuccess) return e;
-  k_gram<Cfg, VEC><<<dim3(tm * tn, g.count), dim3(Cfg::THREADS), gemm_smem_bytes<Cfg, L, L>(), s>>>(
-      g, N1, N2, tn);
+  k_gram<Cfg, VEC, DMA><<<dim3(tm * tn, g.count), dim3(Cfg::THREADS), bytes, s>>>(g, N1, N2, tn);
   return hipGetLastError();
 }
 
@@ -568,7 +575,11 @@ hipError_t launch_gram(hipStream_t s, const GramBatch& g, int N1, int N2, int nu
       k_gram_small<false><<<grid, dim3(256), 0, s>>>(g, N1, N2, tn);
     return hipGetLastError();
   }
-  return v ? gram_vec<true>(s, g, N1, N2) : gram_vec<false>(s, g, N1, N2);
+  bool dma = v;
+  for (int z = 0; z < g.count; ++z)
+    dma = dma && g.K[z] % 32 == 0 && dma_span_ok(g.K[z], g.K[z], 256);
+  if (dma) return gram_vec<true, true>(s, g, N1, N2);
+  return v ? gram_vec<true, false>(s, g, N1, N2) : gram_vec<false, false>(s, g, N1, N2);
 }
 
 // ------------------------------------------------------------------------------ fused contraction
@@ -863,8 +874,10 @@ __device__ __forceinline__ void fcn_tile_layers(const FcnContraction& c, int l0,
   }
 }
 
+// kSkPerCu workgroups per compute unit must be resident together: the register budget is that
+// of kSkPerCu * THREADS / 256 waves per SIMD
 template <class Cfg, bool VEC, bool DMA>
-__global__ void __launch_bounds__(Cfg::THREADS)
+__global__ void __launch_bounds__(Cfg::THREADS, kSkPerCu * Cfg::THREADS / 256)
 k_ntk_fcn_sk(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, float* __restrict__ theta,
              int tiles_m, int tiles_n, int T, int P, float* __restrict__ part) {
   extern __shared__ float smem[];
