@@ -360,7 +360,7 @@ static bool conv_dma_ok(const void* x, long long elems, int W, int C, const void
 // over the sample's tensor.  Each lane's (k-row, row chunk) inside the tile is fixed, so its row
 // part is computed once per tile; pixels past D and padding taps read past the resource (zeros).
 // G of the sample: rows (o, c) of O*C (C % 4 == 0), element G[o, p, c].
-template <int ROWS, int WAVES>
+template <int ROWS, int WAVES, bool WHOLE = false>
 struct DmaCotangentKOuter {
   using Tile = DmaTileKOuter<ROWS>;
   const float* __restrict__ g;
@@ -371,9 +371,10 @@ struct DmaCotangentKOuter {
   static constexpr int OPS = ROWS / (8 * WV);
   __amdgpu_buffer_rsrc_t rsrc;
   // per issued row: the byte offset of its 16-byte chunk at pixel kl (the K tile's first pixel
-  // k0 adds the uniform k0 C 4 through the scalar offset) and the bound k0 < klim of the pixels
-  // inside the sample (klim = D - kl; none for rows past the end)
-  int base4[NI], klim[NI];
+  // k0 adds the uniform k0 C 4 through the scalar offset), with bit 31 set for rows past the end
+  // (past the resource's end: zeros), and the bound k0 < klim of the pixels inside the sample
+  // (klim = D - kl), tested unless WHOLE (D a multiple of the K tile)
+  int pre4[NI], klim[NI];
   __device__ __forceinline__ void prepare(int row0, int wave, int lane) {
     rsrc = buffer_rsrc(g, (uint32_t)((long long)rows * D * 4));
 #pragma unroll
@@ -383,9 +384,9 @@ struct DmaCotangentKOuter {
       const int row = row0 + 4 * Tile::swz(k, pos);
       const int rc = min(row, rows - 4);
       const int oo = (int)fC.div(rc), cc = rc - oo * C;
-      base4[i] = (oo * D * C + cc + k * C) * 4;
-      asm volatile("" : "+v"(base4[i]));   // kept whole, not re-derived at each issue
-      klim[i] = row < rows ? D - k : -1;
+      pre4[i] = (int)((uint32_t)((oo * D * C + cc + k * C) * 4) | (row < rows ? 0u : kDmaPastEnd));
+      asm volatile("" : "+v"(pre4[i]));   // kept whole, not re-derived at each issue
+      klim[i] = D - k;
     }
   }
   template <int WV>
@@ -394,14 +395,15 @@ struct DmaCotangentKOuter {
     const uint32_t soff = (uint32_t)k0 * C * 4u;
 #pragma unroll
     for (int i = 0; i < NI; ++i) {
-      const uint32_t voff = k0 < klim[i] ? (uint32_t)base4[i] : kDmaPastEnd;
+      // WHOLE (D % 32 == 0): every pixel of every K tile is inside the sample
+      const uint32_t voff = WHOLE ? (uint32_t)pre4[i] : ((uint32_t)pre4[i] | (k0 < klim[i] ? 0u : kDmaPastEnd));
       buffer_dma16(rsrc, voff, soff, lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256));
     }
   }
 };
 
 // Patches of the sample's layer input [H, W, C] (C % 4 == 0): rows (tap, ci) of 9*C.
-template <int ROWS, int WAVES>
+template <int ROWS, int WAVES, bool ROW32 = false>
 struct DmaPatchesKOuter {
   using Tile = DmaTileKOuter<ROWS>;
   const float* __restrict__ x;
@@ -414,8 +416,14 @@ struct DmaPatchesKOuter {
   // per issued row (tap (dy, dx), channel ci) at pixel kl of the K tile: the byte offset of its
   // shifted pixel kl + dy W + dx through a resource that starts W + 1 pixels before the sample
   // (so the offset is never negative; the K tile's first pixel k0 adds the uniform k0 C 4 through
-  // the scalar offset), and what the tap's bounds test needs
+  // the scalar offset), and what the tap's bounds test needs.  With ROW32 (W a multiple of the K
+  // tile of 32 pixels) a K tile is a run of 32 pixels of one image row, and a row's tap is outside the
+  // image exactly when one of the uniform conditions in its 5-bit mask `out` holds: bit 0 the
+  // tile is the image's first row (dy = -1), bit 1 its last row (dy = 1), bit 2 the tile starts
+  // an image row (kl = 0, dx = -1), bit 3 it ends one (kl = 31, dx = 1), bit 4 always (rows past
+  // the end).
   int base4[NI], kl[NI], dy[NI], dx[NI], ok[NI];
+  unsigned out[NI];
   __device__ __forceinline__ void prepare(int row0, int wave, int lane) {
     rsrc = buffer_rsrc(x - (long long)(W + 1) * C, (uint32_t)((long long)(K + W + 1) * C * 4));
 #pragma unroll
@@ -433,28 +441,33 @@ struct DmaPatchesKOuter {
       base4[i] = ((k + (kh - 1) * W + (kw - 1) + W + 1) * C + ci) * 4;
       asm volatile("" : "+v"(base4[i]));   // kept whole, not re-derived at each issue
       ok[i] = row < rows ? 1 : 0;
+      out[i] = (kh == 0 ? 1u : 0u) | (kh == 2 ? 2u : 0u) | (k == 0 && kw == 0 ? 4u : 0u) |
+               (k == 31 && kw == 2 ? 8u : 0u) | (row < rows ? 0u : 16u);
     }
   }
   template <int WV>
   __device__ __forceinline__ void issue(int k0, float* lds, int wave, int lane) const {
     static_assert(WV == WAVES, "issuer built for this workgroup shape");
     const uint32_t soff = (uint32_t)k0 * C * 4u;
-    const bool row32 = W % 32 == 0;   // a K tile of 32 pixels (k0 % 32 == 0) lies in one image row
-    const int y0 = (int)fW.div(k0), x0 = k0 - y0 * W;   // uniform
+    if constexpr (ROW32) {
+      const int y0 = (int)fW.div(k0), x0 = k0 - y0 * W;   // uniform
+      const unsigned bad = (y0 == 0 ? 1u : 0u) | (y0 == H - 1 ? 2u : 0u) | (x0 == 0 ? 4u : 0u) |
+                           (x0 + 32 == W ? 8u : 0u) | 16u;
 #pragma unroll
-    for (int i = 0; i < NI; ++i) {
-      bool good;
-      if (row32) {
-        good = ok[i] & (kl[i] < K - k0) & ((unsigned)(y0 + dy[i]) < (unsigned)H) &
-               ((unsigned)(x0 + kl[i] + dx[i]) < (unsigned)W);
-      } else {
-        const int p = k0 + kl[i];
-        const int pc = min(p, K - 1);
-        const int y = (int)fW.div(pc), xx = pc - y * W;
-        good = ok[i] & (p < K) & ((unsigned)(y + dy[i]) < (unsigned)H) & ((unsigned)(xx + dx[i]) < (unsigned)W);
+      for (int i = 0; i < NI; ++i) {
+        const uint32_t voff = (uint32_t)base4[i] | ((out[i] & bad) ? kDmaPastEnd : 0u);
+        buffer_dma16(rsrc, voff, soff, lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256));
       }
+    } else {
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+      const int p = k0 + kl[i];
+      const int pc = min(p, K - 1);
+      const int y = (int)fW.div(pc), xx = pc - y * W;
+      const bool good = ok[i] & (p < K) & ((unsigned)(y + dy[i]) < (unsigned)H) & ((unsigned)(xx + dx[i]) < (unsigned)W);
       const uint32_t voff = good ? (uint32_t)base4[i] : kDmaPastEnd;
       buffer_dma16(rsrc, voff, soff, lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256));
+      }
     }
   }
 };
@@ -899,7 +912,9 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
 }
 
 // direct-to-LDS form (C % 4 == 0 and Cin % 4 == 0): both operands K-outer, NS LDS stages
-template <class Cfg, int NS, bool PW>
+// AL: every K tile of 32 pixels is whole (D % 32 == 0) and, for the 3x3 patches, lies in one
+// image row (W % 32 == 0)
+template <class Cfg, int NS, bool PW, bool AL>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O, int H, int W, int C, int Cin, FastDiv fC, FastDiv fW, FastDiv fCin,
                  float* __restrict__ J, long long ldJ, long long off, int tiles_m, int tiles_n, int samples) {
@@ -910,7 +925,7 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
   const int KC = PW ? Cin : 9 * Cin;
   const int tm = t / tiles_n, tn = t - tm * tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
-  DmaCotangentKOuter<Cfg::BM, Cfg::WAVES> ia;
+  DmaCotangentKOuter<Cfg::BM, Cfg::WAVES, AL> ia;
   ia.g = G + (long long)s * O * D * C;
   ia.rows = O * C;
   ia.D = D;
@@ -926,7 +941,7 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
       for (int v = 0; v < 16; ++v) dacc[fm][fn].v[0][v] = dacc[fm][fn].v[1][v] = 0.f;
   if constexpr (PW) {
     // pointwise: the columns are the input channels themselves, [D, Cin] of the sample
-    DmaCotangentKOuter<Cfg::BN, Cfg::WAVES> ib;
+    DmaCotangentKOuter<Cfg::BN, Cfg::WAVES, AL> ib;
     ib.g = h + (long long)s * D * Cin;
     ib.rows = Cin;
     ib.D = D;
@@ -934,7 +949,7 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
     ib.fC = fCin;
     gemm_mainloop_dma_ops<Cfg, NS>(ia, ib, m0, n0, 0, D, smem, dacc);
   } else {
-    DmaPatchesKOuter<Cfg::BN, Cfg::WAVES> ib;
+    DmaPatchesKOuter<Cfg::BN, Cfg::WAVES, AL> ib;
     ib.x = h + (long long)s * D * Cin;
     ib.rows = KC;
     ib.K = D;
@@ -990,13 +1005,18 @@ static hipError_t conv_wgrad_any(hipStream_t s, const float* G, const float* h, 
     constexpr int NS = kConvWgStages;
     const int tn = cdiv(KC, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
     constexpr int bytes = gemm_dma_smem_bytes<Cfg, NS>();
-    hipError_t e = hipFuncSetAttribute((const void*)k_conv_wgrad_dma<Cfg, NS, PW>,
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-    if (e != hipSuccess) return e;
-    k_conv_wgrad_dma<Cfg, NS, PW><<<dim3(wgrad_grid(tm * tn, images)), dim3(Cfg::THREADS), bytes, s>>>(
-        G, h, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
-        ldJ, off, tm, tn, images);
-    return hipGetLastError();
+    auto go = [&](auto al_tag) -> hipError_t {
+      constexpr bool AL = decltype(al_tag)::value;
+      hipError_t e = hipFuncSetAttribute((const void*)k_conv_wgrad_dma<Cfg, NS, PW, AL>,
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+      if (e != hipSuccess) return e;
+      k_conv_wgrad_dma<Cfg, NS, PW, AL><<<dim3(wgrad_grid(tm * tn, images)), dim3(Cfg::THREADS), bytes, s>>>(
+          G, h, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
+          ldJ, off, tm, tn, images);
+      return hipGetLastError();
+    };
+    const bool al = PW ? (H * W) % 32 == 0 : W % 32 == 0;
+    return al ? go(std::true_type{}) : go(std::false_type{});
   }
   const bool va = C % 4 == 0 && aligned16(G), vb = Cin % 4 == 0 && aligned16(h);
   if (va && vb) return conv_wgrad_vec<true, true, PW>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);

@@ -80,6 +80,9 @@ CASES = [
     # tiles and padding taps on every border
     ("direct-to-LDS patches, ragged 5x7", wl.cnn_spec("c6", (5, 7), 3, [32, 32, 32], 3), 5, 4),
     ("direct-to-LDS patches, 1x1 images", wl.cnn_spec("c7", (1, 1), 4, [32, 64], 2), 3, 7),
+    # image width a multiple of 32: each 32-pixel K tile of the weight-space product is one run
+    # of an image row (tiles at x = 0 and x = 32 of each of the 3 rows)
+    ("aligned pixel rows, 3x64 images", wl.cnn_spec("c8", (3, 64), 3, [32, 32], 3), 4, 3),
 ]
 
 
