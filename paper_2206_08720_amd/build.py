@@ -29,7 +29,10 @@ COMMON = ["-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
 # chains are not copied between accumulation and architectural registers every iteration.
 PER_FILE = {"diag.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
             # the inside-out kernel feeds an MFMA's result to the next MFMA as an A operand
-            "kernels_pairsum.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
+            "kernels_pairsum.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+            # the fp64 convolution forward otherwise moves its accumulators between the two
+            # register files at every group of K tiles
+            "kernels_conv.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"]}
 
 
 def _run(cmd):
