@@ -32,6 +32,7 @@ using CfgConv = TileCfg<128, 64, 32, 32, 32>;      // backward / wgrad, fp32 MFM
 // tiles, 4/8 waves and 2/3 stages at the CNN workload.
 using CfgConvBwd = TileCfg<256, 64, 32, 32, 64>;
 using CfgConvWg = CfgConv;
+using CfgConvWgSmall = TileCfg<64, 64, 32, 32, 32>;   // one-output rows (O C <= 64): 4 waves
 constexpr int kConvBwdStages = 2, kConvWgStages = 2;
 // Small images (few output rows): below kConvFewTiles tiles of the shapes above, the backward
 // takes 128x64 tiles (8 waves of 32x32) and the fp64 forward 32x32 tiles (4 waves of 16x16), so
@@ -694,6 +695,88 @@ hipError_t launch_conv_seed(hipStream_t s, const float* Wd, const float* dphi, i
   return hipGetLastError();
 }
 
+// The last convolution's summand when its cotangent is the readout's (through the global pool):
+// theta[n1, n2, o1, o2] += scale sum_c Wr[o1, c] Wr[o2, c] Mc[c, n1, n2].  LDS form: a workgroup
+// stages Wr and w2[c][o1 O + o2] = Wr[o1, c] Wr[o2, c] once, then per block of kFoldPairs input pairs
+// their Mc columns, and each thread sums entries (pair, o1, o2) from LDS.  Otherwise one thread
+// per entry reads Wr and Mc directly.
+constexpr int kFoldPairs = 16, kFoldIlp = 8;
+constexpr int kFoldLdsFloats = 16384;
+template <bool LDS>
+__global__ void __launch_bounds__(256)
+k_readout_fold(const float* __restrict__ Wr, int C, int O, const float* __restrict__ Mc, int N1, int N2,
+               float scale, float* __restrict__ theta) {
+  extern __shared__ float sm[];
+  const int OO = O * O;
+  const long long plane = (long long)N1 * N2;
+  if (!LDS) {
+    for (long long idx = blockIdx.x * 256LL + threadIdx.x; idx < plane * OO; idx += (long long)gridDim.x * 256) {
+      const long long pr = idx / OO;
+      const int oo = (int)(idx - pr * OO);
+      const int o1 = oo / O, o2 = oo - o1 * O;
+      float acc = 0.f;
+      for (int c = 0; c < C; ++c) acc += (Wr[o1 * C + c] * Wr[o2 * C + c]) * Mc[c * plane + pr];
+      theta[idx] += scale * acc;
+    }
+    return;
+  }
+  float* w2 = sm;
+  float* mc = sm + C * OO;
+  float* wr = mc + C * kFoldPairs;
+  for (int i = threadIdx.x; i < O * C; i += 256) wr[i] = Wr[i];
+  __syncthreads();
+  for (int i = threadIdx.x; i < C * OO; i += 256) {
+    const int c = i / OO, oo = i - c * OO;
+    const int o1 = oo / O, o2 = oo - o1 * O;
+    w2[i] = wr[o1 * C + c] * wr[o2 * C + c];
+  }
+  for (long long p0 = (long long)blockIdx.x * kFoldPairs; p0 < plane; p0 += (long long)gridDim.x * kFoldPairs) {
+    const int np = (int)min<long long>(kFoldPairs, plane - p0);
+    __syncthreads();   // w2 staged; the previous block's reads of mc done
+    for (int i = threadIdx.x; i < C * kFoldPairs; i += 256) {
+      const int c = i / kFoldPairs, j = i - c * kFoldPairs;
+      mc[i] = j < np ? Mc[c * plane + p0 + j] : 0.f;
+    }
+    __syncthreads();
+    // kFoldIlp entries per thread at once (independent sums, their LDS reads in flight together)
+    const int ne = np * OO;
+    for (int e0 = threadIdx.x; e0 < ne; e0 += 256 * kFoldIlp) {
+      float acc[kFoldIlp];
+      int wo[kFoldIlp], mo[kFoldIlp];
+#pragma unroll
+      for (int q = 0; q < kFoldIlp; ++q) {
+        const int e = min(e0 + q * 256, ne - 1);
+        const int j = e / OO;
+        wo[q] = e - j * OO;
+        mo[q] = j;
+        acc[q] = 0.f;
+      }
+#pragma unroll 4
+      for (int c = 0; c < C; ++c)
+#pragma unroll
+        for (int q = 0; q < kFoldIlp; ++q) acc[q] += w2[c * OO + wo[q]] * mc[c * kFoldPairs + mo[q]];
+#pragma unroll
+      for (int q = 0; q < kFoldIlp; ++q)
+        if (e0 + q * 256 < ne) theta[(p0 + mo[q]) * OO + wo[q]] += scale * acc[q];
+    }
+  }
+}
+
+hipError_t launch_readout_fold(hipStream_t s, const float* Wr, int C, int O, const float* Mc, int N1, int N2,
+                               float scale, float* theta) {
+  const long long plane = (long long)N1 * N2;
+  if (plane <= 0 || O <= 0 || C <= 0) return hipSuccess;
+  const long long lds = (long long)C * ((long long)O * O + kFoldPairs + O);
+  if (lds <= kFoldLdsFloats) {
+    const unsigned grid = (unsigned)std::min<long long>((plane + kFoldPairs - 1) / kFoldPairs, 4096);
+    k_readout_fold<true><<<dim3(grid), dim3(256), (size_t)lds * 4, s>>>(Wr, C, O, Mc, N1, N2, scale, theta);
+  } else {
+    const unsigned grid = (unsigned)std::min<long long>((plane * O * O + 255) / 256, 65536);
+    k_readout_fold<false><<<dim3(grid), dim3(256), 0, s>>>(Wr, C, O, Mc, N1, N2, scale, theta);
+  }
+  return hipGetLastError();
+}
+
 // Kt[ci, kh, kw, co] = K[co, 2 - kh, 2 - kw, ci]
 __global__ void k_conv_flip(const float* __restrict__ K, int Cout, int Cin, float* __restrict__ Kt) {
   const int total = Cout * 9 * Cin;
@@ -1001,12 +1084,12 @@ static hipError_t conv_wgrad_any(hipStream_t s, const float* G, const float* h, 
   // direct-to-LDS: one sample's cotangents and layer input each within a buffer resource
   if (C % 4 == 0 && Cin % 4 == 0 && aligned16(G) && aligned16(h) && (long long)O * H * W * C * 4 < (1LL << 31) &&
       (long long)H * W * Cin * 4 < (1LL << 31)) {
-    using Cfg = CfgConvWg;
     constexpr int NS = kConvWgStages;
-    const int tn = cdiv(KC, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
-    constexpr int bytes = gemm_dma_smem_bytes<Cfg, NS>();
-    auto go = [&](auto al_tag) -> hipError_t {
+    auto go = [&](auto cfg_tag, auto al_tag) -> hipError_t {
+      using Cfg = decltype(cfg_tag);
       constexpr bool AL = decltype(al_tag)::value;
+      const int tn = cdiv(KC, Cfg::BN), tm = cdiv(O * C, Cfg::BM);
+      constexpr int bytes = gemm_dma_smem_bytes<Cfg, NS>();
       hipError_t e = hipFuncSetAttribute((const void*)k_conv_wgrad_dma<Cfg, NS, PW, AL>,
                                          hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
       if (e != hipSuccess) return e;
@@ -1016,7 +1099,10 @@ static hipError_t conv_wgrad_any(hipStream_t s, const float* G, const float* h, 
       return hipGetLastError();
     };
     const bool al = PW ? (H * W) % 32 == 0 : W % 32 == 0;
-    return al ? go(std::true_type{}) : go(std::false_type{});
+    // at most 64 rows (O C: one output, as for the folded last convolution): 64 x 64 tiles
+    if (O * C <= 64)
+      return al ? go(CfgConvWgSmall{}, std::true_type{}) : go(CfgConvWgSmall{}, std::false_type{});
+    return al ? go(CfgConvWg{}, std::true_type{}) : go(CfgConvWg{}, std::false_type{});
   }
   const bool va = C % 4 == 0 && aligned16(G), vb = Cin % 4 == 0 && aligned16(h);
   if (va && vb) return conv_wgrad_vec<true, true, PW>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);

@@ -509,6 +509,54 @@ static hipError_t gram_vec(hipStream_t s, const GramBatch& g, int N1, int N2) {
   return hipGetLastError();
 }
 
+// Strided batch of Grams: out[b][n1][n2] = a1[n1 ld + b bs : + K] . a2[n2 ld + b bs : + K] for
+// b < batches (one 64 x 64 tile of batch blockIdx.y per workgroup).
+template <class Cfg, bool VEC, bool DMA>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_gram_strided(const float* __restrict__ a1, const float* __restrict__ a2, int N1, int N2, int K, long long ld,
+               long long bs, float* __restrict__ out, int tiles_n) {
+  extern __shared__ float smem[];
+  const int b = blockIdx.y;
+  const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  f32x16 acc[Cfg::FM][Cfg::FN];
+  zero_acc<Cfg>(acc);
+  if (DMA) {
+    gemm_mainloop_dma<Cfg, kGramStages>(a1 + b * bs, ld, N1, a2 + b * bs, ld, N2, m0, n0, 0, K, smem, acc);
+  } else {
+    LoadKInnerT<VEC> la{a1 + b * bs, N1, K, ld};
+    LoadKInnerT<VEC> lb{a2 + b * bs, N2, K, ld};
+    gemm_mainloop<Cfg>(la, lb, m0, n0, 0, K, smem, acc);
+  }
+  float* o = out + (long long)b * N1 * N2;
+  for_each_acc<Cfg>(acc, m0, n0, [&](int r, int c, float v) {
+    if (r < N1 && c < N2) o[(long long)r * N2 + c] = v;
+  });
+}
+
+hipError_t launch_gram_strided(hipStream_t s, const float* a1, const float* a2, int N1, int N2, int K,
+                               long long ld, long long bs, int batches, float* out) {
+  if (batches <= 0 || N1 <= 0 || N2 <= 0) return hipSuccess;
+  if (batches > 65535) return hipErrorInvalidValue;
+  using Cfg = CfgSmall;
+  const int tn = cdiv(N2, Cfg::BN), tm = cdiv(N1, Cfg::BM);
+  const bool v = vec_ok(a1, ld, K) && vec_ok(a2, ld, K) && bs % 4 == 0;
+  const bool dma = v && K % 32 == 0 && dma_span_ok(ld, K, 256);
+  auto go = [&](auto vec_tag, auto dma_tag) -> hipError_t {
+    constexpr bool VEC = decltype(vec_tag)::value, DMA = decltype(dma_tag)::value;
+    using L = LoadKInnerT<VEC>;
+    constexpr int bytes = DMA ? gemm_dma_smem_bytes<Cfg, kGramStages>() : gemm_smem_bytes<Cfg, L, L>();
+    hipError_t e = hipFuncSetAttribute((const void*)k_gram_strided<Cfg, VEC, DMA>,
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess) return e;
+    k_gram_strided<Cfg, VEC, DMA><<<dim3(tm * tn, batches), dim3(Cfg::THREADS), bytes, s>>>(a1, a2, N1, N2, K, ld,
+                                                                                          bs, out, tn);
+    return hipGetLastError();
+  };
+  if (dma) return go(TrueT{}, TrueT{});
+  return v ? go(TrueT{}, FalseT{}) : go(FalseT{}, FalseT{});
+}
+
 // Small batches: the 64 x 64 tiles of k_gram would leave most compute units idle, so workgroup
 // (block, z) computes one 16 x 16 block of layer z's Gram with the 16x16x4 fp32 MFMA, its four
 // waves taking every fourth 16-column slice of K; the waves' partial blocks are then added in

@@ -87,6 +87,10 @@ struct GramBatch {
 // out_l[n1, n2] = h1_l[n1] . h2_l[n2] + beta_l for every l (rows of h have stride K_l).
 // Batches whose matrix-core tiles would not fill num_cu compute units run on the vector units.
 hipError_t launch_gram(hipStream_t s, const GramBatch& g, int N1, int N2, int num_cu);
+// out[b][n1][n2] = a1[n1 ld + b bs .. + K] . a2[n2 ld + b bs .. + K] for b < batches (rows of
+// stride ld floats, batch b at the float offset b bs of each row)
+hipError_t launch_gram_strided(hipStream_t s, const float* a1, const float* a2, int N1, int N2, int K,
+                               long long ld, long long bs, int batches, float* out);
 
 struct FcnContraction {
   const float* G1[kMaxLayers];    // cotangents of batch 1, [N1*O, K_l]

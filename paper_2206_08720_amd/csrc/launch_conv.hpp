@@ -36,6 +36,9 @@ hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int 
 // Pointwise (1x1) form: J[(s*O + o), off + c*Cin + ci] = sum_p G[s, o, p, c] h[s, p, ci].
 hipError_t launch_pw_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
                            int W, int C, int Cin, float* J, long long ldJ, long long off);
+// theta[n1, n2, o1, o2] += scale sum_c Wr[o1, c] Wr[o2, c] Mc[c, n1, n2] (Wr [O, C], Mc [C, N1, N2]).
+hipError_t launch_readout_fold(hipStream_t s, const float* Wr, int C, int O, const float* Mc, int N1, int N2,
+                               float scale, float* theta);
 // Deterministic split-K product J1 J2^T: plan, partial products, reduction into theta.
 int splitk_tile();
 // splits * R1 * R2 <= part_capacity (floats) always holds for the returned plan.

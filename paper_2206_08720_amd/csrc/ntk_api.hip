@@ -161,6 +161,7 @@ struct ntk_handle {
   long long Ktot = 0;             // columns of J at most: every weight and bias column
   size_t off_g = 0, off_Gping = 0, off_Gpong = 0, off_J = 0, off_gram_r = 0, off_part = 0;
   size_t off_gt = 0;              // the inside-out kernel's copy of a cotangent [M, C, O, Dp]
+  size_t off_mc = 0;              // per-channel Grams of the last convolution [C, N1, N2] (0: none)
   long long part_capacity = 0;    // floats of the split-K partial buffer
 };
 
@@ -469,8 +470,13 @@ static void plan_cnn(ntk_handle* h) {
     kt += weight_cols(L, h->ch[l]) + (L.has_bias ? L.out : 0);
   }
   h->Ktot = kt;
-  h->off_J = take(Mmax * O * (size_t)kt);
+  h->off_J = take(Mmax * O * (size_t)kt + 4);   // + the 16-byte boundary of a folded layer's rows
   h->off_gram_r = take((size_t)h->max_n1 * h->max_n2);
+  {   // a last 3x3 or pointwise convolution may contract through per-channel Grams (compute_cnn)
+    const int kind = nc >= 1 ? h->layers[nc - 1].kind : -1;
+    if ((kind == NTK_CONV3X3_SAME || kind == NTK_CONV1X1) && O >= 2)
+      h->off_mc = take((size_t)h->ch[nc] * h->max_n1 * h->max_n2);
+  }
   {   // the largest cotangent copy of a convolution the inside-out order can take
     long long gt = 0;
     for (int l = 0; l < nc; ++l) {
@@ -1089,21 +1095,39 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
       inside[l] = (io_ok && io < oi) ? 1 : 0;
     }
   }
-  // columns of J in this call: per layer its weight block (unless contracted inside-out), then
-  // its bias
+  // The last convolution's output cotangent is the readout's through the global pool,
+  // G[n, o, p, c] = Wr[o, c] act'(z[n, p, c]) / D, so its weight-space columns factor as
+  // Wr[o, c] A[n, c, k] / D with A[n, c, k] = sum_p act'(z[n, p, c]) patch[n, p, k], and its
+  // summand is sum_c Wr[o1, c] Wr[o2, c] (A1[., c, .] A2[., c, .]^T)[n1, n2] / D^2: the O outputs
+  // leave that layer's weight-space product and contraction ("fold").  Outside-in layers only, the
+  // full O x O output, with other columns in J (the split-K contraction then writes theta first).
+  const int ll = nc - 1;
+  bool fold = nc >= 1 && h->off_mc && !inside[ll] && h->wslot[ll] >= 0 && O >= 2 && !logit && !trace &&
+              !diag && h->opt_method != NTK_METHOD_JACOBIAN &&
+              (h->layers[ll].kind == NTK_CONV3X3_SAME || h->layers[ll].kind == NTK_CONV1X1);
+  // columns of J in this call: per layer its weight block (unless contracted inside-out or
+  // folded), then its bias
   std::vector<long long> jw(nc, 0), jb(nc, 0);
   long long Kcall = 0;
-  for (int l = 0; l < nc; ++l) {
-    const ntk_layer_desc& L = h->layers[l];
-    if (L.kind == NTK_AVGPOOL2) continue;
-    if (!inside[l]) {
-      jw[l] = Kcall;
-      Kcall += weight_cols(L, h->ch[l]);
+  auto plan_columns = [&]() {
+    Kcall = 0;
+    for (int l = 0; l < nc; ++l) {
+      const ntk_layer_desc& L = h->layers[l];
+      if (L.kind == NTK_AVGPOOL2) continue;
+      if (!inside[l] && !(fold && l == ll)) {
+        jw[l] = Kcall;
+        Kcall += weight_cols(L, h->ch[l]);
+      }
+      if (L.has_bias) {
+        jb[l] = Kcall;
+        Kcall += L.out;
+      }
     }
-    if (L.has_bias) {
-      jb[l] = Kcall;
-      Kcall += L.out;
-    }
+  };
+  plan_columns();
+  if (fold && Kcall == 0) {
+    fold = false;
+    plan_columns();
   }
   hipError_t e;
   // 1. forward pass keeping every spatial layer's input, then global average pooling
@@ -1167,6 +1191,9 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   prof_end(P, s, KC_CONV_SEED);
   if (e != hipSuccess) return hip_fail(h, e, "conv seed");
   float* J = F(h->off_J);
+  // the folded layer's A: in J past this call's columns (J holds that layer's O C F Cin columns
+  // per row), at a 16-byte boundary
+  float* fold_A = J + (((size_t)M * Oe * Kcall + 3) & ~(size_t)3);
   bool theta_written = false;
   const int n2_off = sym ? 0 : n1;
   for (int l = nc - 1; l >= 0; --l) {
@@ -1174,7 +1201,23 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
     const int Hl = h->bh[l], Wl = h->bw[l], cin = h->ch[l], cout = h->ch[l + 1];
     const float* w = h->wslot[l] >= 0 ? params[h->wslot[l]] : nullptr;
     // Gcur: the cotangent of layer l's pre-activation (of its output for a pool), [M*Oe, ., ., cout]
-    if (L.kind == NTK_CONV3X3_SAME) {
+    if (fold && l == ll) {
+      // A [M, C, F Cin] from act'(z) in place of the O cotangents (the "fold" above), in J past
+      // the columns of this call
+      const float* dz = F(h->off_cdphi[ll]);
+      prof_begin(P, s, KC_CONV_WGRAD);
+      e = L.kind == NTK_CONV3X3_SAME
+              ? launch_conv_wgrad(s, dz, hptr(l), M, 1, Hl, Wl, cout, cin, fold_A, 9LL * cin * cout, 0)
+              : launch_pw_wgrad(s, dz, hptr(l), M, 1, Hl, Wl, cout, cin, fold_A, (long long)cin * cout, 0);
+      prof_end(P, s, KC_CONV_WGRAD);
+      if (e != hipSuccess) return hip_fail(h, e, "last convolution's channel cotangents");
+      if (L.has_bias) {
+        prof_begin(P, s, KC_STRUCT_WGRAD);
+        e = launch_pix_wgrad(s, Gcur, nullptr, M, Oe, Hl, Wl, cout, 0, 1, J, Kcall, 0, jb[l], nullptr, 0);
+        prof_end(P, s, KC_STRUCT_WGRAD);
+        if (e != hipSuccess) return hip_fail(h, e, "conv bias cotangent");
+      }
+    } else if (L.kind == NTK_CONV3X3_SAME) {
       if (inside[l]) {
         prof_begin(P, s, KC_CONV_PAIRSUM);
         e = launch_conv_pairsum(s, hptr(l), Gcur, F(h->off_gt), n1, n2, n2_off, Oe, Hl, Wl, cin, cout, 9,
@@ -1300,6 +1343,19 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
                           rscale, theta_written ? 1 : 0, theta);
     prof_end(P, s, KC_NTK_REDUCE);
     if (e != hipSuccess) return hip_fail(h, e, "split-K reduction");
+  }
+  if (fold) {
+    // theta += sum_c Wr[o1, c] Wr[o2, c] Mc[c] / D^2, Mc[c] = A1[., c, .] A2[., c, .]^T
+    const ntk_layer_desc& L = h->layers[ll];
+    const int cin = h->ch[ll], KC = (L.kind == NTK_CONV3X3_SAME ? 9 : 1) * cin;
+    const int D = h->bh[nc] * h->bw[nc];
+    const float* A2 = sym ? fold_A : fold_A + (size_t)n1 * C * KC;
+    prof_begin(P, s, KC_GRAM);
+    e = launch_gram_strided(s, fold_A, A2, n1, n2, KC, (long long)C * KC, KC, C, F(h->off_mc));
+    if (e == hipSuccess)
+      e = launch_readout_fold(s, params[h->rslot], C, O, F(h->off_mc), n1, n2, 1.f / ((float)D * (float)D), theta);
+    prof_end(P, s, KC_GRAM);
+    if (e != hipSuccess) return hip_fail(h, e, "last convolution's summand");
   }
   return NTK_OK;
 }

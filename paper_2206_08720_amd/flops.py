@@ -119,7 +119,27 @@ def _inside_out(kind, D, cin, cout, M, Oe, Oc, gpairs, order, trace=False):
     return D <= 64 and inside_out_cost(gpairs, D, cin, cout, Oe, trace) < oi
 
 
-def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", batch="full"):
+def _folds_last_conv(sp, O, output, batch, M, Oe, Oc, gpairs, order):
+    """Whether the library folds the last convolution (its cotangent is the readout's through the
+    global pool, so its weight-space columns factor into Wr[o, c] times O-free per-channel rows and
+    its summand into per-channel Grams): a last 3x3 or pointwise convolution contracted
+    outside-in, the full O x O output (O >= 2) on the full batch, and other weight-space columns
+    (a bias or another layer's) in the contraction."""
+    if not sp or O < 2 or output != "full" or batch != "full":
+        return False
+    k, cin, cout, D, bias = sp[-1]
+    if k not in ("conv3x3", "conv1x1") or _inside_out(k, D, cin, cout, M, Oe, Oc, gpairs, order):
+        return False
+    others = bool(bias)
+    for i, (k2, ci, co, D2, b2) in enumerate(sp[:-1]):
+        if b2 or k2 in ("dwconv3x3", "scale"):
+            others = True
+        elif k2 in ("conv3x3", "conv1x1") and not _inside_out(k2, D2, ci, co, M, Oe, Oc, gpairs, order):
+            others = True
+    return others
+
+
+def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", batch="full", fold=True):
     """CNN counts per stage.  3x3 convolutions as in the module docstring; the further layer
     kinds (memory-bound, counted for completeness, in the struct_* stages): depthwise 3x3
     forward, backward and weight-space cotangent 2 M (Oe) D 9 C each; scale forward M D C (2 M D C
@@ -131,7 +151,10 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
     inside-out forms no J columns and counts its own operations in the stage "pairsum": the
     pixel Gram D^2 Cin, the F D^2 tap sums of the patch-pair Gram (one FLOP each), and the
     products Oe D^2 Cout and Oc D Cout (the form of the appendix "CNN NTK Complexity" with the
-    patch-pair Gram built from the pixel Gram instead of D^2 F Cin patch products)."""
+    patch-pair Gram built from the pixel Gram instead of D^2 F Cin patch products).  With `fold`
+    (the library's schedule, _folds_last_conv) the last convolution forms O-free rows A [M, C, F Cin]
+    ("wgrad"), no J columns, and per-channel Grams plus their O x O sums ("gram"); fold=False counts
+    every outside-in layer alike, as the paper's table does."""
     layers = spec["layers"]
     sp, C = _spatial_layers(spec)
     O = layers[-1]["out"]
@@ -141,14 +164,20 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
     # the 3x3 convolutions' stages ("forward", "backward", "wgrad"), and those of the other kinds
     # and of the biases (memory-bound kernels of their own: "struct_forward", "struct_backward",
     # "struct_wgrad"); a conv bias is added in the conv forward kernel's epilogue
-    fwd = bwd = wg = sfwd = sbwd = swg = cols = io = 0.0
+    fwd = bwd = wg = sfwd = sbwd = swg = cols = io = fold_gram = 0.0
+    fold = fold and _folds_last_conv(sp, O, output, batch, M, Oe, Oc, gpairs, order)
     for i, (k, cin, cout, D, bias) in enumerate(sp):
         if k in ("conv1x1", "conv3x3"):
             F = 9 if k == "conv3x3" else 1
             fwd += 2.0 * M * D * F * cin * cout + (1.0 * M * D * cout if bias else 0.0)
             if i >= 1:
                 bwd += 2.0 * M * Oe * D * F * cout * cin
-            if not _inside_out(k, D, cin, cout, M, Oe, Oc, gpairs, order, output == "trace"):
+            if fold and i == len(sp) - 1:
+                # the folded last convolution: A [M, C, F Cin] (one row block per sample instead
+                # of O), the per-channel Grams of every input pair, and the O x O sums over C
+                wg += 2.0 * M * cout * (F * cin) * D
+                fold_gram = 2.0 * n1 * n2 * cout * F * cin + 3.0 * n1 * n2 * O * O * cout
+            elif not _inside_out(k, D, cin, cout, M, Oe, Oc, gpairs, order, output == "trace"):
                 wg += 2.0 * M * (Oe * cout) * (F * cin) * D
                 cols += F * cin * cout
             else:  # inside-out (every input pair, also on the symmetric schedule): the pixel Gram,
@@ -174,7 +203,7 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
         if bias:
             swg += 1.0 * M * Oe * D * cout
             cols += cout
-    st = {"forward": fwd, "backward": bwd, "gram": 2.0 * gpairs * C}
+    st = {"forward": fwd, "backward": bwd, "gram": 2.0 * gpairs * C + fold_gram}
     if wg:
         st["wgrad"] = wg
     for key, v in (("struct_forward", sfwd), ("struct_backward", sbwd), ("struct_wgrad", swg)):

@@ -37,17 +37,25 @@ def test_workload_totals():
     assert ntk_entries(spec, 512, 512) == 512 * 512 * 100
     spec, _, _, _ = wl.make_workload("cnn4_c64_32x32")
     c = cnn_flops(spec, 64, 64)
-    assert c["total"] == pytest.approx(7.06e11, rel=1e-3)
+    assert c["total"] == pytest.approx(5.89e11, rel=1e-3)
 
 
 def test_cnn_terms_match_complexities_cnn():
     N, O, D, W, Fs = 4, 5, 36, 8, 9
     spec = wl.cnn_spec("c", (6, 6), W, [W, W], O)
-    oi = cnn_flops(spec, N, N, order="outside_in")
+    oi = cnn_flops(spec, N, N, order="outside_in", fold=False)
     io = cnn_flops(spec, N, N, order="inside_out")
     # outside-in: N^2 O^2 F W^2 per layer for J1 J2^T, plus N O D F W^2 to form J
     assert oi["contraction"] == 2 * (N * O) * (N * O) * 2 * Fs * W * W
     assert oi["wgrad"] == 2 * (2 * N) * O * W * Fs * W * D * 2
+    # the library's schedule folds the last convolution (its cotangent is the readout's through
+    # the global pool): O-free rows A [2N, W, F W], per-channel Grams of the N^2 pairs and their
+    # O x O sums over the W channels, and no J columns of that layer
+    fo = cnn_flops(spec, N, N, order="outside_in")
+    assert fo["wgrad"] == 2 * (2 * N) * O * W * Fs * W * D + 2 * (2 * N) * W * Fs * W * D
+    assert fo["contraction"] == 2 * (N * O) * (N * O) * Fs * W * W
+    assert fo["gram"] == 2 * N * N * W + 2 * N * N * W * Fs * W + 3 * N * N * O * O * W
+    assert fo["forward"] == oi["forward"] and fo["backward"] == oi["backward"]
     # inside-out: N^2 (D^2 F W + O D^2 W + O^2 D W) multiply-adds per layer in the paper's table;
     # here the patch-pair Gram comes from the pixel Gram (D^2 W) and F D^2 tap sums; no J columns
     assert io["pairsum"] == 2 * N * N * (2 * D * D * W + Fs * D * D + 2 * O * D * D * W + 2 * O * O * D * W)
@@ -64,7 +72,7 @@ def test_auto_order_is_the_cost_model():
     assert a["pairsum"] == 3 * N * N * (2 * D * D * W + 9 * D * D + 2 * O * D * D * W + 2 * O * O * D * W)
     assert a["contraction"] == 2 * N * N * O * O * 9 * 3 * W
     assert a["wgrad"] == 2 * (2 * N) * O * W * 9 * 3 * D
-    oi = cnn_flops(spec, N, N, order="outside_in")
+    oi = cnn_flops(spec, N, N, order="outside_in", fold=False)
     assert oi["contraction"] + oi["wgrad"] > 8 * (a["pairsum"] + a["contraction"] + a["wgrad"])
     spec, _, _, _ = wl.make_workload("cnn4_c64_32x32")
     assert cnn_flops(spec, 64, 64, order="auto") == cnn_flops(spec, 64, 64, order="outside_in")
@@ -82,8 +90,10 @@ def test_variant_counts():
     assert dg["contraction"] == full["contraction"] / N and dg["gram"] == full["gram"] / N
     assert ntk_entries(spec, N, N, "trace") == N * N and ntk_entries(spec, N, N, "full", "diagonal") == N * O * O
     cs = wl.cnn_spec("c", (4, 4), 3, [8, 8], O)
-    cf, cl = cnn_flops(cs, N, N), cnn_flops(cs, N, N, output="logit")
+    cf, cl = cnn_flops(cs, N, N, fold=False), cnn_flops(cs, N, N, output="logit")
     assert cl["wgrad"] == cf["wgrad"] / O and cl["contraction"] == cf["contraction"] / O ** 2
+    # one logit: nothing to fold (the library folds the full O x O output only)
+    assert cnn_flops(cs, N, N, output="logit", fold=False) == cl
 
 
 def test_jacobian_contraction_count_is_the_papers_n2_o2_p():
@@ -128,10 +138,15 @@ def test_pointwise_counts():
     N, O = 2, 3
     spec = wl.cnn_layers_spec("pw", (2, 4), 3, [("conv1x1", 6, "relu", True), ("dwconv3x3", "relu", False),
                                                ("conv1x1", 5, "erf", False)], O)
-    f = cnn_flops(spec, N, N)
+    f = cnn_flops(spec, N, N, fold=False)
     M, D = 2 * N, 8
     assert f["forward"] == 2 * M * D * 3 * 6 + M * D * 6 + 2 * M * D * 6 * 5
     assert f["backward"] == 2 * M * O * D * 5 * 6
     assert f["wgrad"] == 2 * M * O * 6 * 3 * D + 2 * M * O * 5 * 6 * D
     assert f["contraction"] == 2 * N * N * O * O * (3 * 6 + 6 + 9 * 6 + 6 * 5)
+    # folded last pointwise convolution (5 channels of 6 inputs): O-free rows, no J columns
+    g = cnn_flops(spec, N, N)
+    assert g["wgrad"] == 2 * M * O * 6 * 3 * D + 2 * M * 5 * 6 * D
+    assert g["contraction"] == 2 * N * N * O * O * (3 * 6 + 6 + 9 * 6)
+    assert g["gram"] == 2 * N * N * 5 + 2 * N * N * 5 * 6 + 3 * N * N * O * O * 5
     assert param_total(spec) == oracle.param_count(spec)

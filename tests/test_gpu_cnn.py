@@ -95,6 +95,40 @@ def test_cnn_edge_shapes(case):
     _vs_jc(label, spec, params, X1, X2)
 
 
+FOLD_CASES = [
+    # label, spec, n1, n2, folded: the last convolution's summand through per-channel Grams of
+    # its O-free rows (its cotangent is the readout's through the global pool)
+    ("3x3 last, ragged 6x7", wl.cnn_layers_spec("f1", (6, 7), 3, [("conv3x3", 16, "relu", True),
+                                                                 ("conv3x3", 24, "erf", False)], 5), 7, 5, True),
+    ("pointwise last, 32 channels", wl.cnn_layers_spec("f2", (4, 8), 4, [("conv3x3", 32, "relu", False),
+                                                                        ("conv1x1", 32, "relu", True)], 3), 6, 9, True),
+    # a single convolution without bias: no other weight-space column, so no fold
+    ("single convolution", wl.cnn_layers_spec("f3", (5, 5), 3, [("conv3x3", 8, "relu", False)], 4), 4, 3, False),
+]
+
+
+@pytest.mark.parametrize("symmetric", [True, False])
+@pytest.mark.parametrize("case", FOLD_CASES, ids=[c[0] for c in FOLD_CASES])
+def test_folded_last_convolution(case, symmetric):
+    """The last convolution's O outputs factor out of its weight-space product: A[n, c, k] from
+    act'(z) alone, Theta += sum_c Wr[o1, c] Wr[o2, c] (A1 A2^T)_c / D^2.  Parity against the
+    oracle, forced outside-in, with X2 = X1 on the symmetric schedule and distinct batches
+    otherwise; the fold's Grams are a second launch of the Gram class."""
+    from paper_2206_08720_amd import _lib
+    label, spec, n1, n2, folded = case
+    params = wl.make_params(spec, 600 + n1, "2/fan_in")
+    X1 = wl.make_inputs(spec, n1, 610 + n1)
+    X2 = X1 if symmetric else wl.make_inputs(spec, n2, 620 + n2)
+    prof = {}
+    got = gpu_ntk(spec, params, X1, X2, symmetric=symmetric,
+                  options={_lib.NTK_OPT_CONV_ORDER: _lib.NTK_CONV_ORDER_OUTSIDE_IN}, profile=prof)
+    ref, d1, d2 = oracle.ntk_jc_with_norms(spec, params, X1, X2, layer_storage=S)
+    cs, nw = errors(got, ref, d1, d2)
+    report(f"fold {label} sym={symmetric}", cs, nw)
+    assert got.shape == ref.shape and cs <= TOL and nw <= TOL
+    assert prof["gram"][1] == (2 if folded else 1)
+
+
 @pytest.mark.parametrize("symmetric", [True, False])
 def test_cnn_aliased_inputs(symmetric):
     spec = wl.cnn_spec("alias", (6, 5), 3, [16, 16], 10)
