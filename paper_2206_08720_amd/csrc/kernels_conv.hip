@@ -725,10 +725,9 @@ k_readout_fold(const float* __restrict__ Wr, int C, int O, const float* __restri
   float* wr = mc + C * kFoldPairs;
   for (int i = threadIdx.x; i < O * C; i += 256) wr[i] = Wr[i];
   __syncthreads();
-  for (int i = threadIdx.x; i < C * OO; i += 256) {
-    const int c = i / OO, oo = i - c * OO;
+  for (int oo = threadIdx.x; oo < OO; oo += 256) {
     const int o1 = oo / O, o2 = oo - o1 * O;
-    w2[i] = wr[o1 * C + c] * wr[o2 * C + c];
+    for (int c = 0; c < C; ++c) w2[c * OO + oo] = wr[o1 * C + c] * wr[o2 * C + c];
   }
   for (long long p0 = (long long)blockIdx.x * kFoldPairs; p0 < plane; p0 += (long long)gridDim.x * kFoldPairs) {
     const int np = (int)min<long long>(kFoldPairs, plane - p0);

@@ -1102,9 +1102,29 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   // leave that layer's weight-space product and contraction ("fold").  Outside-in layers only, the
   // full O x O output, with other columns in J (the split-K contraction then writes theta first).
   const int ll = nc - 1;
-  bool fold = nc >= 1 && h->off_mc && !inside[ll] && h->wslot[ll] >= 0 && O >= 2 && !logit && !trace &&
-              !diag && h->opt_method != NTK_METHOD_JACOBIAN &&
+  bool fold = nc >= 1 && h->off_mc && h->wslot[ll] >= 0 && O >= 2 && !logit && !trace && !diag &&
+              h->opt_method != NTK_METHOD_JACOBIAN &&
               (h->layers[ll].kind == NTK_CONV3X3_SAME || h->layers[ll].kind == NTK_CONV1X1);
+  if (fold) {   // other weight-space columns: a bias, a depthwise or scale layer, an outside-in conv
+    bool others = h->layers[ll].has_bias != 0;
+    for (int l = 0; l < ll; ++l) {
+      const int kind = h->layers[l].kind;
+      others = others || h->layers[l].has_bias || kind == NTK_DWCONV3X3_SAME || kind == NTK_SCALE ||
+               ((kind == NTK_CONV3X3_SAME || kind == NTK_CONV1X1) && !inside[l]);
+    }
+    fold = others;
+  }
+  // With the fold available, the cost model's outside-in cost of the last convolution is that of
+  // the fold: the O-free rows M D F Cin Cout, the per-channel Grams N1 N2 F Cin Cout and their
+  // O x O sums N1 N2 O^2 Cout.
+  if (fold && inside[ll] && h->opt_conv_order == NTK_CONV_ORDER_AUTO) {
+    const ntk_layer_desc& L = h->layers[ll];
+    const double F = L.kind == NTK_CONV1X1 ? 1 : 9;
+    const double Dl = (double)h->bh[ll] * h->bw[ll], Cin = h->ch[ll], Co = h->ch[ll + 1];
+    const double folded = (double)M * Dl * F * Cin * Co + (double)n1 * n2 * (F * Cin * Co + (double)O * O * Co);
+    if (folded < inside_out_cost(pairs, (int)Dl, h->ch[ll], h->ch[ll + 1], Oe, trace)) inside[ll] = 0;
+  }
+  fold = fold && !inside[ll];
   // columns of J in this call: per layer its weight block (unless contracted inside-out or
   // folded), then its bias
   std::vector<long long> jw(nc, 0), jb(nc, 0);

@@ -119,24 +119,30 @@ def _inside_out(kind, D, cin, cout, M, Oe, Oc, gpairs, order, trace=False):
     return D <= 64 and inside_out_cost(gpairs, D, cin, cout, Oe, trace) < oi
 
 
-def _folds_last_conv(sp, O, output, batch, M, Oe, Oc, gpairs, order):
-    """Whether the library folds the last convolution (its cotangent is the readout's through the
-    global pool, so its weight-space columns factor into Wr[o, c] times O-free per-channel rows and
-    its summand into per-channel Grams): a last 3x3 or pointwise convolution contracted
-    outside-in, the full O x O output (O >= 2) on the full batch, and other weight-space columns
-    (a bias or another layer's) in the contraction."""
-    if not sp or O < 2 or output != "full" or batch != "full":
-        return False
+def _conv_orders(sp, O, n1, n2, output, batch, M, Oe, Oc, gpairs, order):
+    """Per spatial layer whether it is contracted inside-out, and whether the last convolution is
+    folded, as the library decides: _inside_out per layer; the fold (the last convolution's
+    cotangent is the readout's through the global pool, so its weight-space columns factor into
+    Wr[o, c] times O-free per-channel rows and its summand into per-channel Grams) for a last 3x3
+    or pointwise convolution, the full O x O output (O >= 2) on the full batch, with other
+    weight-space columns in the contraction (a bias, a depthwise or scale layer, an outside-in
+    convolution); with order "auto" the last convolution then goes outside-in when the fold's
+    M D F Cin Cout + N1 N2 (F Cin Cout + O^2 Cout) is below its inside-out cost."""
+    trace = output == "trace"
+    io = [_inside_out(k, D, cin, cout, M, Oe, Oc, gpairs, order, trace) for (k, cin, cout, D, bias) in sp]
+    if not sp or O < 2 or output != "full" or batch != "full" or sp[-1][0] not in ("conv3x3", "conv1x1"):
+        return io, False
+    others = bool(sp[-1][4]) or any(b or k in ("dwconv3x3", "scale") or (k in ("conv3x3", "conv1x1") and not io[i])
+                                    for i, (k, ci, co, D, b) in enumerate(sp[:-1]))
+    if not others:
+        return io, False
     k, cin, cout, D, bias = sp[-1]
-    if k not in ("conv3x3", "conv1x1") or _inside_out(k, D, cin, cout, M, Oe, Oc, gpairs, order):
-        return False
-    others = bool(bias)
-    for i, (k2, ci, co, D2, b2) in enumerate(sp[:-1]):
-        if b2 or k2 in ("dwconv3x3", "scale"):
-            others = True
-        elif k2 in ("conv3x3", "conv1x1") and not _inside_out(k2, D2, ci, co, M, Oe, Oc, gpairs, order):
-            others = True
-    return others
+    if io[-1] and order == "auto":
+        F = 9 if k == "conv3x3" else 1
+        folded = M * D * F * cin * cout + n1 * n2 * (F * cin * cout + O * O * cout)
+        if folded < inside_out_cost(gpairs, D, cin, cout, Oe, trace):
+            io[-1] = False
+    return io, not io[-1]
 
 
 def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", batch="full", fold=True):
@@ -152,9 +158,10 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
     pixel Gram D^2 Cin, the F D^2 tap sums of the patch-pair Gram (one FLOP each), and the
     products Oe D^2 Cout and Oc D Cout (the form of the appendix "CNN NTK Complexity" with the
     patch-pair Gram built from the pixel Gram instead of D^2 F Cin patch products).  With `fold`
-    (the library's schedule, _folds_last_conv) the last convolution forms O-free rows A [M, C, F Cin]
+    (the library's schedule, _conv_orders) the last convolution forms O-free rows A [M, C, F Cin]
     ("wgrad"), no J columns, and per-channel Grams plus their O x O sums ("gram"); fold=False counts
-    every outside-in layer alike, as the paper's table does."""
+    every outside-in layer alike, as the paper's table does (and the orders of the plain cost
+    model)."""
     layers = spec["layers"]
     sp, C = _spatial_layers(spec)
     O = layers[-1]["out"]
@@ -165,7 +172,11 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
     # and of the biases (memory-bound kernels of their own: "struct_forward", "struct_backward",
     # "struct_wgrad"); a conv bias is added in the conv forward kernel's epilogue
     fwd = bwd = wg = sfwd = sbwd = swg = cols = io = fold_gram = 0.0
-    fold = fold and _folds_last_conv(sp, O, output, batch, M, Oe, Oc, gpairs, order)
+    inside, can_fold = _conv_orders(sp, O, n1, n2, output, batch, M, Oe, Oc, gpairs, order)
+    if not fold and can_fold and order == "auto":   # the unfolded count keeps the plain cost model
+        inside = [_inside_out(k, D, cin, cout, M, Oe, Oc, gpairs, order, output == "trace")
+                  for (k, cin, cout, D, bias) in sp]
+    fold = fold and can_fold
     for i, (k, cin, cout, D, bias) in enumerate(sp):
         if k in ("conv1x1", "conv3x3"):
             F = 9 if k == "conv3x3" else 1
@@ -177,7 +188,7 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
                 # of O), the per-channel Grams of every input pair, and the O x O sums over C
                 wg += 2.0 * M * cout * (F * cin) * D
                 fold_gram = 2.0 * n1 * n2 * cout * F * cin + 3.0 * n1 * n2 * O * O * cout
-            elif not _inside_out(k, D, cin, cout, M, Oe, Oc, gpairs, order, output == "trace"):
+            elif not inside[i]:
                 wg += 2.0 * M * (Oe * cout) * (F * cin) * D
                 cols += F * cin * cout
             else:  # inside-out (every input pair, also on the symmetric schedule): the pixel Gram,

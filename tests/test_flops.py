@@ -63,17 +63,26 @@ def test_cnn_terms_match_complexities_cnn():
 
 
 def test_auto_order_is_the_cost_model():
-    """order="auto" mirrors the library's per-layer choice: on 4x4 images the three 64->64
-    convolutions go inside-out (several times cheaper), the 3-channel one stays outside-in;
-    on 32x32 images every layer stays outside-in."""
+    """order="auto" mirrors the library's per-layer choice: on 4x4 images the 64->64
+    convolutions go inside-out (several times cheaper than outside-in), except the last one,
+    whose fold (its O outputs out of its weight-space product) is cheaper still; the 3-channel
+    one stays outside-in; on 32x32 images every layer stays outside-in."""
     spec, _, _, _ = wl.make_workload("cnn4_c64_4x4")
     N, O, D, W = 64, 10, 16, 64
-    a = cnn_flops(spec, N, N, order="auto")
-    assert a["pairsum"] == 3 * N * N * (2 * D * D * W + 9 * D * D + 2 * O * D * D * W + 2 * O * O * D * W)
-    assert a["contraction"] == 2 * N * N * O * O * 9 * 3 * W
-    assert a["wgrad"] == 2 * (2 * N) * O * W * 9 * 3 * D
+    io1 = N * N * (2 * D * D * W + 9 * D * D + 2 * O * D * D * W + 2 * O * O * D * W)
+    plain = cnn_flops(spec, N, N, order="auto", fold=False)
+    assert plain["pairsum"] == 3 * io1
+    assert plain["contraction"] == 2 * N * N * O * O * 9 * 3 * W
+    assert plain["wgrad"] == 2 * (2 * N) * O * W * 9 * 3 * D
     oi = cnn_flops(spec, N, N, order="outside_in", fold=False)
-    assert oi["contraction"] + oi["wgrad"] > 8 * (a["pairsum"] + a["contraction"] + a["wgrad"])
+    assert oi["contraction"] + oi["wgrad"] > 8 * (plain["pairsum"] + plain["contraction"] + plain["wgrad"])
+    a = cnn_flops(spec, N, N, order="auto")
+    assert a["pairsum"] == 2 * io1
+    assert a["contraction"] == 2 * N * N * O * O * 9 * 3 * W
+    assert a["wgrad"] == 2 * (2 * N) * O * W * 9 * 3 * D + 2 * (2 * N) * W * 9 * W * D
+    assert a["gram"] == 2 * N * N * W + 2 * N * N * W * 9 * W + 3 * N * N * O * O * W
+    # the fold's cost (multiply-adds) against the last layer's inside-out cost
+    assert 2 * N * D * 9 * W * W + N * N * (9 * W * W + O * O * W) < io1 / 2
     spec, _, _, _ = wl.make_workload("cnn4_c64_32x32")
     assert cnn_flops(spec, 64, 64, order="auto") == cnn_flops(spec, 64, 64, order="outside_in")
 
