@@ -823,45 +823,56 @@ hipError_t launch_conv_flip_batch(hipStream_t s, const FlipBatch& b) {
   return hipGetLastError();
 }
 
-// ------------------------------------------------------------------------------ backward
-// Epilogue of the per-sample weight-space product of sample s: J[(s*O + o)*ldJ + off + c*KC + k]
-// = acc[r = o*C + c, k].  A fragment inside R = O*C and inside one o (no multiple of C in
-// (r0, r0 + 31]) writes 32 consecutive c of one row of J, addressed from one base (32-bit
-// byte offsets: KC < 2^25).
+// J[(s*O + o), off + c*KCs + js] = acc[r = o*C + c, k] for the GEMM columns k of KC = F Cin
+// (F taps of Cin computed input channels), stored as the columns js of KCs = F Cst (the first Cst
+// channels of each tap: a layer input padded from Cst to Cin channels has zero columns that are
+// not stored; Cst = Cin: js = k).  A fragment inside R = O*C and inside one o (no multiple of C
+// in (r0, r0 + 31]) writes 32 consecutive c of one row of J, addressed from one base (32-bit byte
+// offsets: KCs < 2^25).
 template <class Cfg>
 __device__ __forceinline__ void conv_wgrad_store(f32x16 (&acc)[Cfg::FM][Cfg::FN], int m0, int n0, int s,
-                                                 int O, FastDiv fC, int KC, float* __restrict__ J,
-                                                 long long ldJ, long long off) {
+                                                 int O, FastDiv fC, int KC, FastDiv fCin, int Cst,
+                                                 float* __restrict__ J, long long ldJ, long long off) {
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
   const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
   const int C = (int)fC.d, R = O * C;
+  const int Cin = (int)fCin.d, KCs = Cst == Cin ? KC : (KC / Cin) * Cst;
+  // the stored column of GEMM column k, or -1 (a padded channel or past KC)
+  auto col = [&](int k) {
+    if (k >= KC) return -1;
+    if (Cst == Cin) return k;
+    const int tap = (int)fCin.div(k), ci = k - tap * Cin;
+    return ci < Cst ? tap * Cst + ci : -1;
+  };
 #pragma unroll
   for (int fm = 0; fm < Cfg::FM; ++fm) {
     const int r0 = __builtin_amdgcn_readfirstlane(m0 + wm0 + fm * 32);
     if (r0 >= R) continue;
     const int o0 = (int)fC.div(r0);
-    if (r0 + 32 <= R && KC < (1 << 25) && (int)fC.div(r0 + 31) == o0) {
-      float* base = J + ((long long)s * O + o0) * ldJ + off + (long long)(r0 - o0 * C) * KC;
+    if (r0 + 32 <= R && KCs < (1 << 25) && (int)fC.div(r0 + 31) == o0) {
+      float* base = J + ((long long)s * O + o0) * ldJ + off + (long long)(r0 - o0 * C) * KCs;
 #pragma unroll
       for (int fn = 0; fn < Cfg::FN; ++fn) {
-        const int k = n0 + wn0 + fn * 32 + (lane & 31);
-        if (k >= KC) continue;
+        const int js = col(n0 + wn0 + fn * 32 + (lane & 31));
+        if (js < 0) continue;
 #pragma unroll
-        for (int v = 0; v < 16; ++v) at_bytes(base, (uint32_t)(frag_row(v, lane) * KC + k) * 4u) = acc[fm][fn][v];
+        for (int v = 0; v < 16; ++v) at_bytes(base, (uint32_t)(frag_row(v, lane) * KCs + js) * 4u) = acc[fm][fn][v];
       }
     } else {
 #pragma unroll
-      for (int fn = 0; fn < Cfg::FN; ++fn)
+      for (int fn = 0; fn < Cfg::FN; ++fn) {
+        const int js = col(n0 + wn0 + fn * 32 + (lane & 31));
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
-          const int r = r0 + frag_row(v, lane), k = n0 + wn0 + fn * 32 + (lane & 31);
-          if (r < R && k < KC) {
+          const int r = r0 + frag_row(v, lane);
+          if (r < R && js >= 0) {
             const int o = (int)fC.div(r), c = r - o * C;
-            J[((long long)s * O + o) * ldJ + off + (long long)c * KC + k] = acc[fm][fn][v];
+            J[((long long)s * O + o) * ldJ + off + (long long)c * KCs + js] = acc[fm][fn][v];
           }
         }
+      }
     }
   }
 }
@@ -990,7 +1001,7 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
     lb.fC = fCin;
     gemm_mainloop<Cfg>(la, lb, m0, n0, 0, D, smem, acc);
   }
-  conv_wgrad_store<Cfg>(acc, m0, n0, s, O, fC, KC, J, ldJ, off);
+  conv_wgrad_store<Cfg>(acc, m0, n0, s, O, fC, KC, fCin, Cin, J, ldJ, off);
 }
 
 // direct-to-LDS form (C % 4 == 0 and Cin % 4 == 0): both operands K-outer, NS LDS stages
@@ -999,7 +1010,7 @@ k_conv_wgrad(const float* __restrict__ G, const float* __restrict__ h, int O, in
 template <class Cfg, int NS, bool PW, bool AL>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O, int H, int W, int C, int Cin, FastDiv fC, FastDiv fW, FastDiv fCin,
-                 float* __restrict__ J, long long ldJ, long long off, int tiles_m, int tiles_n, int samples) {
+                 int Cst, float* __restrict__ J, long long ldJ, long long off, int tiles_m, int tiles_n, int samples) {
   extern __shared__ float smem[];
   int s, t;
   if (!xcd_sample_tile(blockIdx.x, tiles_m * tiles_n, samples, s, t)) return;
@@ -1047,7 +1058,7 @@ k_conv_wgrad_dma(const float* __restrict__ G, const float* __restrict__ h, int O
   for (int fm = 0; fm < Cfg::FM; ++fm)
 #pragma unroll
     for (int fn = 0; fn < Cfg::FN; ++fn) acc[fm][fn] = dacc[fm][fn].v[0] + dacc[fm][fn].v[1];
-  conv_wgrad_store<Cfg>(acc, m0, n0, s, O, fC, KC, J, ldJ, off);
+  conv_wgrad_store<Cfg>(acc, m0, n0, s, O, fC, KC, fCin, Cst, J, ldJ, off);
 }
 
 // Grid of the per-sample weight-space products: the tiles of one sample on one XCD, so the
@@ -1075,7 +1086,7 @@ static hipError_t conv_wgrad_vec(hipStream_t s, const float* G, const float* h, 
 // pointwise (PW = true: columns ci of the layer input) convolution.
 template <bool PW>
 static hipError_t conv_wgrad_any(hipStream_t s, const float* G, const float* h, int images, int O, int H,
-                                 int W, int C, int Cin, float* J, long long ldJ, long long off) {
+                                 int W, int C, int Cin, float* J, long long ldJ, long long off, int Cst) {
   const int KC = (PW ? 1 : 9) * Cin;
   if ((long long)8 * ((images + 7) / 8) * cdiv(KC, CfgConv::BN) * cdiv((long long)O * C, CfgConv::BM) >=
       (1LL << 31))
@@ -1093,7 +1104,7 @@ static hipError_t conv_wgrad_any(hipStream_t s, const float* G, const float* h, 
                                          hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
       if (e != hipSuccess) return e;
       k_conv_wgrad_dma<Cfg, NS, PW, AL><<<dim3(wgrad_grid(tm * tn, images)), dim3(Cfg::THREADS), bytes, s>>>(
-          G, h, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), J,
+          G, h, O, H, W, C, Cin, FastDiv((uint32_t)C), FastDiv((uint32_t)W), FastDiv((uint32_t)Cin), Cst, J,
           ldJ, off, tm, tn, images);
       return hipGetLastError();
     };
@@ -1103,6 +1114,7 @@ static hipError_t conv_wgrad_any(hipStream_t s, const float* G, const float* h, 
       return al ? go(CfgConvWgSmall{}, std::true_type{}) : go(CfgConvWgSmall{}, std::false_type{});
     return al ? go(CfgConvWg{}, std::true_type{}) : go(CfgConvWg{}, std::false_type{});
   }
+  if (Cst != Cin) return hipErrorInvalidValue;   // padded inputs take the direct-to-LDS form only
   const bool va = C % 4 == 0 && aligned16(G), vb = Cin % 4 == 0 && aligned16(h);
   if (va && vb) return conv_wgrad_vec<true, true, PW>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
   if (va) return conv_wgrad_vec<true, false, PW>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
@@ -1111,12 +1123,46 @@ static hipError_t conv_wgrad_any(hipStream_t s, const float* G, const float* h, 
 
 hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
                              int W, int C, int Cin, float* J, long long ldJ, long long off) {
-  return conv_wgrad_any<false>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
+  return conv_wgrad_any<false>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off, Cin);
 }
 
 hipError_t launch_pw_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H, int W,
                            int C, int Cin, float* J, long long ldJ, long long off) {
-  return conv_wgrad_any<true>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off);
+  return conv_wgrad_any<true>(s, G, h, images, O, H, W, C, Cin, J, ldJ, off, Cin);
+}
+
+// xp [rows, Cp] = x [rows, Cin] with zero channels Cin .. Cp - 1.
+__global__ void __launch_bounds__(256)
+k_pad_channels(const float* __restrict__ x, long long rows, int Cin, int Cp, float* __restrict__ xp) {
+  const long long total = rows * Cp;
+  for (long long i = blockIdx.x * 256LL + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
+    const long long r = i / Cp;
+    const int c = (int)(i - r * Cp);
+    xp[i] = c < Cin ? x[r * Cin + c] : 0.f;
+  }
+}
+
+// (images of fewer than kPadMinPixels pixels keep the register-staged form: a few K tiles per
+// sample do not repay the copy; 4x4 images measured slower padded)
+constexpr int kPadMinPixels = 256;
+bool conv_wgrad_pad_ok(int images, int O, int H, int W, int C, int Cin, const float* G, const float* xp) {
+  const int Cp = (Cin + 3) & ~3;
+  return Cin % 4 != 0 && C % 4 == 0 && H * W >= kPadMinPixels && aligned16(G) && aligned16(xp) &&
+         (long long)O * H * W * C * 4 < (1LL << 31) && (long long)H * W * Cp * 4 < (1LL << 31) &&
+         (long long)images * H * W * Cp < (1LL << 40);
+}
+
+hipError_t launch_conv_wgrad_padded(hipStream_t s, const float* G, const float* h, float* xp, int images, int O,
+                                    int H, int W, int C, int Cin, float* J, long long ldJ, long long off, bool pw) {
+  const int Cp = (Cin + 3) & ~3;
+  if (!conv_wgrad_pad_ok(images, O, H, W, C, Cin, G, xp)) return hipErrorInvalidValue;
+  const long long rows = (long long)images * H * W;
+  k_pad_channels<<<dim3((unsigned)std::min<long long>((rows * Cp + 255) / 256, 16384)), dim3(256), 0, s>>>(
+      h, rows, Cin, Cp, xp);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  return pw ? conv_wgrad_any<true>(s, G, xp, images, O, H, W, C, Cp, J, ldJ, off, Cin)
+            : conv_wgrad_any<false>(s, G, xp, images, O, H, W, C, Cp, J, ldJ, off, Cin);
 }
 
 // ------------------------------------------------------------------------------ split-K J1 J2^T

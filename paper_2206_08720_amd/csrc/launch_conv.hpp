@@ -36,6 +36,13 @@ hipError_t launch_conv_wgrad(hipStream_t s, const float* G, const float* h, int 
 // Pointwise (1x1) form: J[(s*O + o), off + c*Cin + ci] = sum_p G[s, o, p, c] h[s, p, ci].
 hipError_t launch_pw_wgrad(hipStream_t s, const float* G, const float* h, int images, int O, int H,
                            int W, int C, int Cin, float* J, long long ldJ, long long off);
+// The same products for Cin % 4 != 0 on the direct-to-LDS path: h [images, H, W, Cin] is first
+// copied into xp [images, H, W, Cp] (Cp = Cin rounded up to 4, zero channels past Cin; caller's
+// buffer), and the zero columns are not stored.  conv_wgrad_pad_ok: whether the shapes and
+// pointers allow it (else the register-staged form of launch_conv_wgrad / launch_pw_wgrad).
+bool conv_wgrad_pad_ok(int images, int O, int H, int W, int C, int Cin, const float* G, const float* xp);
+hipError_t launch_conv_wgrad_padded(hipStream_t s, const float* G, const float* h, float* xp, int images, int O,
+                                    int H, int W, int C, int Cin, float* J, long long ldJ, long long off, bool pw);
 // theta[n1, n2, o1, o2] += scale sum_c Wr[o1, c] Wr[o2, c] Mc[c, n1, n2] (Wr [O, C], Mc [C, N1, N2]).
 hipError_t launch_readout_fold(hipStream_t s, const float* Wr, int C, int O, const float* Mc, int N1, int N2,
                                float scale, float* theta);

@@ -162,6 +162,7 @@ struct ntk_handle {
   size_t off_g = 0, off_Gping = 0, off_Gpong = 0, off_J = 0, off_gram_r = 0, off_part = 0;
   size_t off_gt = 0;              // the inside-out kernel's copy of a cotangent [M, C, O, Dp]
   size_t off_mc = 0;              // per-channel Grams of the last convolution [C, N1, N2] (0: none)
+  size_t off_xpad = 0;            // a convolution input padded to a multiple of 4 channels (0: none)
   long long part_capacity = 0;    // floats of the split-K partial buffer
 };
 
@@ -472,6 +473,16 @@ static void plan_cnn(ntk_handle* h) {
   h->Ktot = kt;
   h->off_J = take(Mmax * O * (size_t)kt + 4);   // + the 16-byte boundary of a folded layer's rows
   h->off_gram_r = take((size_t)h->max_n1 * h->max_n2);
+  {   // the inputs of 3x3 and pointwise convolutions with Cin % 4 != 0, padded for the
+      // direct-to-LDS weight-space product
+    size_t pad = 0;
+    for (int l = 0; l < nc; ++l) {
+      const int kind = h->layers[l].kind;
+      if ((kind == NTK_CONV3X3_SAME || kind == NTK_CONV1X1) && h->ch[l] % 4 != 0)
+        pad = std::max(pad, (size_t)h->bh[l] * h->bw[l] * ((h->ch[l] + 3) & ~3));
+    }
+    if (pad) h->off_xpad = take(Mmax * pad);
+  }
   {   // a last 3x3 or pointwise convolution may contract through per-channel Grams (compute_cnn)
     const int kind = nc >= 1 ? h->layers[nc - 1].kind : -1;
     if ((kind == NTK_CONV3X3_SAME || kind == NTK_CONV1X1) && O >= 2)
@@ -1210,6 +1221,16 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   e = launch_conv_seed(s, Wd, dlast, M, Oe, h->bh[nc] * h->bw[nc], C, Gcur);
   prof_end(P, s, KC_CONV_SEED);
   if (e != hipSuccess) return hip_fail(h, e, "conv seed");
+  // weight-space product of layer l's 3x3 (pw: pointwise) convolution: inputs with Cin % 4 != 0
+  // padded to the direct-to-LDS form when possible
+  auto wgrad = [&](int l, const float* G, int Orows, float* Jout, long long ldJ, long long off, bool pw) {
+    const int Hl = h->bh[l], Wl = h->bw[l], cin = h->ch[l], cout = h->ch[l + 1];
+    float* xp = h->off_xpad ? F(h->off_xpad) : nullptr;
+    if (xp && conv_wgrad_pad_ok(M, Orows, Hl, Wl, cout, cin, G, xp))
+      return launch_conv_wgrad_padded(s, G, hptr(l), xp, M, Orows, Hl, Wl, cout, cin, Jout, ldJ, off, pw);
+    return pw ? launch_pw_wgrad(s, G, hptr(l), M, Orows, Hl, Wl, cout, cin, Jout, ldJ, off)
+              : launch_conv_wgrad(s, G, hptr(l), M, Orows, Hl, Wl, cout, cin, Jout, ldJ, off);
+  };
   float* J = F(h->off_J);
   // the folded layer's A: in J past this call's columns (J holds that layer's O C F Cin columns
   // per row), at a 16-byte boundary
@@ -1226,9 +1247,8 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
       // the columns of this call
       const float* dz = F(h->off_cdphi[ll]);
       prof_begin(P, s, KC_CONV_WGRAD);
-      e = L.kind == NTK_CONV3X3_SAME
-              ? launch_conv_wgrad(s, dz, hptr(l), M, 1, Hl, Wl, cout, cin, fold_A, 9LL * cin * cout, 0)
-              : launch_pw_wgrad(s, dz, hptr(l), M, 1, Hl, Wl, cout, cin, fold_A, (long long)cin * cout, 0);
+      e = L.kind == NTK_CONV3X3_SAME ? wgrad(l, dz, 1, fold_A, 9LL * cin * cout, 0, false)
+                                     : wgrad(l, dz, 1, fold_A, (long long)cin * cout, 0, true);
       prof_end(P, s, KC_CONV_WGRAD);
       if (e != hipSuccess) return hip_fail(h, e, "last convolution's channel cotangents");
       if (L.has_bias) {
@@ -1247,7 +1267,7 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
         theta_written = true;
       } else {
         prof_begin(P, s, KC_CONV_WGRAD);
-        e = launch_conv_wgrad(s, Gcur, hptr(l), M, Oe, Hl, Wl, cout, cin, J, Kcall, jw[l]);
+        e = wgrad(l, Gcur, Oe, J, Kcall, jw[l], false);
         prof_end(P, s, KC_CONV_WGRAD);
         if (e != hipSuccess) return hip_fail(h, e, "conv weight-space cotangent");
       }
@@ -1266,7 +1286,7 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
         theta_written = true;
       } else {
         prof_begin(P, s, KC_CONV_WGRAD);
-        e = launch_pw_wgrad(s, Gcur, hptr(l), M, Oe, Hl, Wl, cout, cin, J, Kcall, jw[l]);
+        e = wgrad(l, Gcur, Oe, J, Kcall, jw[l], true);
         prof_end(P, s, KC_CONV_WGRAD);
       }
       if (e == hipSuccess && L.has_bias) {

@@ -83,6 +83,9 @@ CASES = [
     # image width a multiple of 32: each 32-pixel K tile of the weight-space product is one run
     # of an image row (tiles at x = 0 and x = 32 of each of the 3 rows)
     ("aligned pixel rows, 3x64 images", wl.cnn_spec("c8", (3, 64), 3, [32, 32], 3), 4, 3),
+    # 3 input channels on 16x20 images: the weight-space product of the first layer on the
+    # direct-to-LDS path through a copy padded to 4 channels (the pad columns not stored)
+    ("3 input channels padded to 4, 16x20", wl.cnn_spec("c9", (16, 20), 3, [16, 12], 4), 3, 4),
 ]
 
 

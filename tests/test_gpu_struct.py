@@ -84,6 +84,8 @@ CASES = [
     ("pointwise on 1x1 images (an MLP with biases)",
      _spec("s14", (1, 1), 12, [("conv1x1", 40, "erf", True), ("scale", "relu", True),
                                ("conv1x1", 24, "relu", True)], 5), 13, 11),
+    ("pointwise first on 3 channels padded to 4, 16x16 images",
+     _spec("s16", (16, 16), 3, [("conv1x1", 8, "relu", True), ("conv3x3", 8, "erf", False)], 3), 3, 2),
     ("pointwise after a pool, last layer without activation",
      _spec("s15", (4, 4), 8, [("dwconv3x3", "relu", True), ("avgpool2",), ("conv1x1", 16, "none", True)], 3),
      4, 3),
