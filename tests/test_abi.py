@@ -184,7 +184,9 @@ def test_init_accepts_the_largest_workloads(lib):
 
 def _static(lib, spec, n1, n2):
     """ntk_compute_static with dummy non-null device pointers: every check it makes before the
-    first HIP call runs, and nothing is dereferenced on the host."""
+    first HIP call runs, and nothing is dereferenced on the host.  Only for calls that fail
+    before any kernel launch, or on hosts without a GPU: on a GPU the dummy addresses would be
+    read by the kernels."""
     from paper_2206_08720_amd import _lib
     desc, keep = _lib.model_desc(spec)
     nparams = len(wl.param_shapes(spec))
@@ -208,6 +210,12 @@ def test_static_entry_checks_before_any_device_call(lib):
     assert _static(lib, big, 512, 512) == _lib.NTK_E_UNSUPPORTED
     msg = _lib.last_error()
     assert "static scratch" in msg and str(_lib.STATIC_SCRATCH_BYTES) in msg
+    # Shapes that fit pass every check and reach the first device call, which fails without a
+    # GPU.  Where a GPU is visible the dummy addresses would reach the kernels, so this part runs
+    # only on hosts without one (counting devices does not initialise the runtime).
+    import torch
+    if torch.cuda.device_count() > 0:
+        return
     for name in ("tiny_relu_mlp", "relu_mlp_d4_w512"):
         w = wl.WORKLOADS[name]
-        assert _static(lib, w["spec"], w["n1"], w["n2"]) in (_lib.NTK_OK, _lib.NTK_E_HIP), _lib.last_error()
+        assert _static(lib, w["spec"], w["n1"], w["n2"]) == _lib.NTK_E_HIP, _lib.last_error()
