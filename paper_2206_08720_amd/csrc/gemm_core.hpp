@@ -735,6 +735,43 @@ struct DmaRowMajor {
   }
 };
 
+// DmaKOuterRowMajor: a K-outer operand B[k][n] = p[k ld + n] (row k of a row-major matrix holds
+// the tile's rows n0 .. n0 + ROWS - 1 at one k), in the DmaTileKOuter layout: the K tile's 32
+// k-rows of ROWS floats, 16-byte chunks, loaded by WAVES waves.  Columns past `cols` are read from
+// the last four (clamped; they only feed discarded outputs); the host checks cols % 4 == 0,
+// 16-byte alignment, K % 32 == 0 and krows * ld * 4 < 2^31.
+template <int ROWS, int WAVES>
+struct DmaKOuterRowMajor {
+  using Tile = DmaTileKOuter<ROWS>;
+  static_assert(ROWS % (8 * WAVES) == 0, "tile rows must split over the waves");
+  static constexpr int NI = ROWS / (8 * WAVES);
+  template <int WV>
+  static constexpr int OPS = ROWS / (8 * WV);
+  const float* __restrict__ p;
+  long long ld;
+  int cols, krows;
+  __amdgpu_buffer_rsrc_t rsrc;
+  uint32_t voff[NI];
+  __device__ __forceinline__ void prepare(int n0, int wave, int lane) {
+    rsrc = buffer_rsrc(p, (uint32_t)((long long)krows * ld * 4));
+#pragma unroll
+    for (int i = 0; i < NI; ++i) {
+      const int o = (i * WAVES + wave) * 256 + 4 * lane;     // float offset in the tile
+      const int k = o / ROWS, pos = (o % ROWS) >> 2;
+      const int n = min(n0 + 4 * Tile::swz(k, pos), cols - 4);
+      voff[i] = (uint32_t)(((long long)k * ld + n) * 4);
+    }
+  }
+  template <int WV>
+  __device__ __forceinline__ void issue(int k0, float* lds, int wave, int) const {
+    static_assert(WV == WAVES, "issuer built for this workgroup shape");
+#pragma unroll
+    for (int i = 0; i < NI; ++i)
+      buffer_dma16(rsrc, voff[i], (uint32_t)((long long)k0 * ld * 4),
+                   lds + __builtin_amdgcn_readfirstlane((i * WAVES + wave) * 256));
+  }
+};
+
 // Host check of the resource limit: a tile of `rows` rows of stride `ld` floats, read up to
 // column K, spans less than 2 GiB.
 __host__ inline bool dma_span_ok(long long ld, long long K, int rows) {

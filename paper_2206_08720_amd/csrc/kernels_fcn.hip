@@ -123,6 +123,119 @@ k_dense_fwd_reduce(const double* __restrict__ part, int splits, int M, int N, co
   }
 }
 
+// Few rows and columns (a small batch): one 16 x 16 block of z per workgroup, so that even a
+// 128 x 512 layer makes 256 workgroups without partial sums in memory.  The four waves take
+// every fourth 16-column slice of K with the 16x16x4 fp64 MFMA on the exactly widened fp32
+// values, and their partial blocks are added in wave order, in fp64, through LDS before the bias
+// and the activation's decision.  A lane loads the four columns k0 + 4 (l / 16) + q (q = 0..3) of
+// row l % 16 of both operands, and MFMA q contracts element q (the same column permutation for
+// both operands); the fp64 MFMA returns D[4 v + l / 16][l % 16] in element v of lane l.
+// Block coordinates of the small-batch kernels: the tm x tn blocks of B x B outputs are numbered
+// row by row (or column by column when by_cols) and cut into 8 contiguous ranges, one per XCD, so
+// that an XCD reads a slice of the larger operand through its L2 (and all of the smaller one).
+// False for the padding workgroups past an XCD's range.
+__device__ __forceinline__ bool small_block_coords(int tiles_m, int tiles_n, int by_cols, int B, int& m0,
+                                                   int& n0) {
+  int blk;
+  if (!xcd_block(blockIdx.x, tiles_m * tiles_n, blk)) return false;
+  const int tm = by_cols ? blk % tiles_m : blk / tiles_n;
+  const int tn = by_cols ? blk / tiles_m : blk % tiles_n;
+  m0 = tm * B;
+  n0 = tn * B;
+  return true;
+}
+
+constexpr int kFwdSmallBlocks = 1024;   // at most this many 16 x 16 blocks (four per CU)
+constexpr int kFwdSmallWaves = 8;
+constexpr int kSeedPre = 16;
+template <bool VEC, int WAVES>
+__global__ void __launch_bounds__(64 * WAVES)
+k_dense_fwd_small(const float* __restrict__ h, const float* __restrict__ W, const float* __restrict__ bias,
+                  int M, int N, int K, int act, float* __restrict__ hn, float* __restrict__ dphi,
+                  int tiles_m, int tiles_n, int by_cols, const float* __restrict__ sw, int so,
+                  float* __restrict__ sg) {
+  __shared__ double red[WAVES][256];
+  int m0, n0;
+  if (!small_block_coords(tiles_m, tiles_n, by_cols, 16, m0, n0)) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = lane & 15, kq = 4 * (lane >> 4);
+  const bool va = m0 + i < M, vb = n0 + i < N;
+  const float* __restrict__ pa = h + (long long)min(m0 + i, M - 1) * K;
+  const float* __restrict__ pb = W + (long long)min(n0 + i, N - 1) * K;
+  // the readout weights of this thread's output column for the fused seed, loaded ahead of
+  // the K loop (up to kSeedPre outputs; more are read in the epilogue)
+  const int r = m0 + (threadIdx.x >> 4), c = n0 + (threadIdx.x & 15);
+  float swv[kSeedPre];
+  if (sg && threadIdx.x < 256 && c < N) {
+#pragma unroll
+    for (int o = 0; o < kSeedPre; ++o) swv[o] = o < so ? sw[(long long)o * N + c] : 0.f;
+  }
+  f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+  // batches of U slices: every load of a batch is issued before its MFMAs, from addresses
+  // clamped into the rows (a column past K reads a valid element and is zeroed), so that the
+  // loop body has no branch
+  constexpr int U = 4;
+  for (int kb = 16 * wave; kb < K; kb += 16 * WAVES * U) {
+    f32x4 a[U], b[U];
+    bool in[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = kb + 16 * WAVES * u + kq;
+      if (VEC) {   // K % 4 == 0 and 16-byte aligned rows: the 4 columns are all in or all out
+        in[u] = k < K;
+        const int kc = min(k, K - 4);
+        a[u] = *reinterpret_cast<const f32x4*>(pa + kc);
+        b[u] = *reinterpret_cast<const f32x4*>(pb + kc);
+      } else {
+        in[u] = true;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int kc = min(k + q, K - 1);
+          const float x = pa[kc], y = pb[kc];
+          a[u][q] = k + q < K ? x : 0.f;
+          b[u][q] = k + q < K ? y : 0.f;
+        }
+      }
+    }
+    // keep the loads of the batch ahead of its MFMAs
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool use_a = va && in[u], use_b = vb && in[u];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        acc = __builtin_amdgcn_mfma_f64_16x16x4f64(use_a ? (double)a[u][q] : 0.0, use_b ? (double)b[u][q] : 0.0,
+                                                   acc, 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < 4; ++v) red[wave][(4 * v + (lane >> 4)) * 16 + i] = acc[v];
+  __syncthreads();
+  if (threadIdx.x < 256 && r < M && c < N) {
+    double z = red[0][threadIdx.x];
+#pragma unroll
+    for (int w = 1; w < WAVES; ++w) z += red[w][threadIdx.x];
+    if (bias) z += (double)bias[c];
+    float hv, dv;
+    fwd_epilogue(z, act, hv, dv);
+    hn[(long long)r * N + c] = hv;
+    dphi[(long long)r * N + c] = dv;
+    // the readout cotangents of the last hidden layer, G[r, o, c] = Wr[o, c] act'(z[r, c])
+    if (sg) {
+      float* g = sg + (long long)r * so * N + c;
+#pragma unroll
+      for (int o = 0; o < kSeedPre; ++o)
+        if (o < so) g[(long long)o * N] = swv[o] * dv;
+      for (int o = kSeedPre; o < so; ++o) g[(long long)o * N] = sw[(long long)o * N + c] * dv;
+    }
+  }
+}
+
+bool dense_fwd_small_ok(long long M, long long N) {
+  return M > 0 && N > 0 && (long long)cdiv(M, 64) * cdiv(N, 64) < kFwdSplitTiles &&
+         (long long)cdiv(M, 16) * cdiv(N, 16) <= kFwdSmallBlocks;
+}
+
 long long dense_fwd_part_doubles(long long max_rows, long long max_cols) {
   // the split form only runs below kFwdSplitTiles output tiles of 64 x 64
   return std::min<long long>(kFwdMaxSplits * max_rows * max_cols,
@@ -169,8 +282,27 @@ static hipError_t dense_fwd_cfg(hipStream_t s, const float* h, const float* W, c
 
 hipError_t launch_dense_fwd(hipStream_t s, const float* h, const float* W, const float* b, int M,
                             int N, int K, int act, float* hn, float* dphi, double* part,
-                            long long part_capacity) {
+                            long long part_capacity, const float* seedW, int seedO, float* seedG) {
   const bool v = vec_ok(h, K, K) && vec_ok(W, K, K);
+  if (M <= 0 || N <= 0) return hipSuccess;
+  if (dense_fwd_small_ok(M, N)) {
+    const long long blocks16 = (long long)cdiv(M, 16) * cdiv(N, 16);
+    const int tm = cdiv(M, 16), tn = cdiv(N, 16);
+    const int by_cols = M < N;   // each XCD reads a slice of the larger operand
+    const dim3 grid((unsigned)(8 * cdiv(blocks16, 8)));
+    constexpr int WV = kFwdSmallWaves;
+    if (v)
+      k_dense_fwd_small<true, WV><<<grid, dim3(64 * WV), 0, s>>>(h, W, b, M, N, K, act, hn, dphi, tm, tn, by_cols,
+                                                                 seedW, seedO, seedG);
+    else
+      k_dense_fwd_small<false, WV><<<grid, dim3(64 * WV), 0, s>>>(h, W, b, M, N, K, act, hn, dphi, tm, tn, by_cols,
+                                                                  seedW, seedO, seedG);
+    return hipGetLastError();
+  }
+  if (seedG) {
+    hipError_t e = launch_dense_fwd(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity, nullptr, 0, nullptr);
+    return e != hipSuccess ? e : launch_bwd_seed(s, seedW, dphi, M, seedO, N, seedG);
+  }
   if (v && K % 32 == 0 && dma_span_ok(K, K, 256))
     return dense_fwd_cfg<CfgFwd64, true, true>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity);
   if (v) return dense_fwd_cfg<CfgFwd64, true>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity);
@@ -281,6 +413,42 @@ static hipError_t dense_bwd_cfg(hipStream_t s, const float* G, const float* Wt, 
   return hipGetLastError();
 }
 
+// The same product with B read from W [K, N] itself (row k of W holds B[k][.]) through the
+// K-outer tile layout, so that no transposed copy of W is needed.
+template <class Cfg>
+__device__ __forceinline__ void dense_bwd_ko_tile(const float* __restrict__ G, const float* __restrict__ W, int R,
+                                                  int N, int K, const EpiBwd& epi, int tiles_n, int bx, float* smem) {
+  const int tm = bx / tiles_n, tn = bx % tiles_n;
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  f32x16 acc[Cfg::FM][Cfg::FN];
+  zero_acc<Cfg>(acc);
+  DmaRowMajor<Cfg::BM, Cfg::WAVES> ia{G, K, R};
+  DmaKOuterRowMajor<Cfg::BN, Cfg::WAVES> ib{W, N, N, K};
+  gemm_mainloop_dma_ops<Cfg, 2>(ia, ib, m0, n0, 0, K, smem, acc);
+  epi.template tile<Cfg>(acc, m0, n0);
+}
+
+template <class Cfg>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_dense_bwd_ko(const float* __restrict__ G, const float* __restrict__ W, int R, int N, int K, EpiBwd epi,
+               int tiles_n) {
+  extern __shared__ float smem[];
+  dense_bwd_ko_tile<Cfg>(G, W, R, N, K, epi, tiles_n, blockIdx.x, smem);
+}
+
+template <class Cfg>
+static hipError_t dense_bwd_ko_cfg(hipStream_t s, const float* G, const float* W, const float* dphi, int R,
+                                   int N, int K, int O, float* out) {
+  EpiBwd epi{dphi, out, R, N, FastDiv((uint32_t)O)};
+  const int tn = cdiv(N, Cfg::BN), tm = cdiv(R, Cfg::BM);
+  constexpr int bytes = gemm_dma_smem_bytes<Cfg, 2>();
+  hipError_t e = hipFuncSetAttribute((const void*)k_dense_bwd_ko<Cfg>,
+                                     hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+  if (e != hipSuccess) return e;
+  k_dense_bwd_ko<Cfg><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(G, W, R, N, K, epi, tn);
+  return hipGetLastError();
+}
+
 template <class Cfg, bool VEC, bool DMA = false>
 static hipError_t pw_bwd_cfg(hipStream_t s, const float* G, const float* Wt, const float* dphi, int R, int N,
                              int K, int O, int D, float* out) {
@@ -334,6 +502,115 @@ hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, cons
   if (v && K % 32 == 0 && dma_span_ok(K, K, 256)) return dense_bwd_cfg<CfgSmall, true, true>(s, G, Wt, dphi, R, N, K, O, out);
   return v ? dense_bwd_cfg<CfgSmall, true>(s, G, Wt, dphi, R, N, K, O, out)
            : dense_bwd_cfg<CfgSmall, false>(s, G, Wt, dphi, R, N, K, O, out);
+}
+
+// Few output tiles (a small batch): one 32 x 32 block of the cotangents per workgroup, its four
+// waves taking every fourth 8-column slice of K with the 32x32x2 fp32 MFMA, and the B operand read
+// from W itself (row k of W is B[k][.]; no transposed copy); the waves' partial blocks are added in
+// wave order through LDS and multiplied by act'.  A lane loads the columns k0 + 4 (l / 32) + q
+// (q = 0..3) of row l % 32 of G and the same rows of W at column l % 32 (32 lanes read 32
+// consecutive floats of a row of W), and MFMA q contracts element q; the MFMA returns
+// D[8 (v / 4) + 4 (l / 32) + v % 4][l % 32] in element v of lane l.
+constexpr int kBwdDirectTiles = 256;   // fewer 64 x 64 output tiles than this: the direct form
+constexpr int kBwdDirectWaves = 8;
+constexpr bool kBwdDirectForm = false;   // measured slower than the 64 x 64 tiles
+template <bool VEC, int WAVES>
+__global__ void __launch_bounds__(64 * WAVES)
+k_dense_bwd_direct(const float* __restrict__ G, const float* __restrict__ W, const float* __restrict__ dphi,
+                   int R, int N, int K, FastDiv fO, float* __restrict__ out, int tiles_m, int tiles_n,
+                   int by_cols) {
+  __shared__ float red[WAVES][1024];
+  int m0, n0;
+  if (!small_block_coords(tiles_m, tiles_n, by_cols, 32, m0, n0)) return;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int i = lane & 31, kh = 4 * (lane >> 5);
+  const bool va = m0 + i < R, vb = n0 + i < N;
+  const float* __restrict__ pa = G + (long long)min(m0 + i, R - 1) * K;
+  const float* __restrict__ pb = W + min(n0 + i, N - 1);
+  f32x16 acc;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+  // batches of U slices: every load of a batch is issued before its MFMAs, from addresses
+  // clamped into the operands (a column past K reads a valid element and is zeroed), so that
+  // the loop body has no branch
+  constexpr int U = 8;
+  for (int kb = 8 * wave; kb < K; kb += 8 * WAVES * U) {
+    f32x4 a[U], b[U];
+    bool in[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = kb + 8 * WAVES * u + kh;
+      if (VEC) {   // K % 4 == 0 and 16-byte aligned rows of G: the 4 columns are all in or all out
+        in[u] = k < K;
+        const int kc = min(k, K - 4);
+        a[u] = *reinterpret_cast<const f32x4*>(pa + kc);
+#pragma unroll
+        for (int q = 0; q < 4; ++q) b[u][q] = pb[(long long)(kc + q) * N];
+      } else {
+        in[u] = true;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int kc = min(k + q, K - 1);
+          const float x = pa[kc], y = pb[(long long)kc * N];
+          a[u][q] = k + q < K ? x : 0.f;
+          b[u][q] = k + q < K ? y : 0.f;
+        }
+      }
+    }
+    // keep the loads of the batch ahead of its MFMAs
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool use_a = va && in[u], use_b = vb && in[u];
+#pragma unroll
+      for (int q = 0; q < 4; ++q)
+        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(use_a ? a[u][q] : 0.f, use_b ? b[u][q] : 0.f, acc, 0, 0, 0);
+    }
+  }
+#pragma unroll
+  for (int v = 0; v < 16; ++v) red[wave][(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * 32 + i] = acc[v];
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 1024 / (64 * WAVES); ++j) {
+    const int t = threadIdx.x + 64 * WAVES * j, r = m0 + (t >> 5), c = n0 + (t & 31);
+    if (r < R && c < N) {
+      float v = red[0][t];
+#pragma unroll
+      for (int w = 1; w < WAVES; ++w) v += red[w][t];
+      out[(long long)r * N + c] = v * dphi[(long long)fO.div((uint32_t)r) * N + c];
+    }
+  }
+}
+
+bool dense_bwd_direct_ok(long long R, long long N, long long K) {
+  return R > 0 && N > 0 && K > 0 && R < (1LL << 31) && N < (1LL << 31) && K < (1LL << 31) &&
+         (long long)cdiv(R, 64) * cdiv(N, 64) < kBwdDirectTiles;
+}
+
+bool dense_bwd_w_ok(const float* G, const float* W, long long R, long long N, long long K) {
+  return R > 0 && R < (1LL << 31) && K % 32 == 0 && K > 0 && N % 4 == 0 && N >= 4 &&
+         vec_ok(G, K, K) && vec_ok(W, N, N) && dma_span_ok(K, K, 256) && K * N * 4 < (1LL << 31);
+}
+
+hipError_t launch_dense_bwd_w(hipStream_t s, const float* G, const float* W, const float* dphi, int R, int N,
+                              int K, int O, float* out) {
+  if (O <= 0) return hipErrorInvalidValue;
+  if (dense_bwd_direct_ok(R, N, K) && kBwdDirectForm) {
+    const int tm = cdiv(R, 32), tn = cdiv(N, 32);
+    const int by_cols = R < N;   // each XCD reads a slice of the larger operand
+    const dim3 grid((unsigned)(8 * cdiv((long long)tm * tn, 8)));
+    const FastDiv fO((uint32_t)O);
+    constexpr int WV = kBwdDirectWaves;
+    if (vec_ok(G, K, K))
+      k_dense_bwd_direct<true, WV><<<grid, dim3(64 * WV), 0, s>>>(G, W, dphi, R, N, K, fO, out, tm, tn, by_cols);
+    else
+      k_dense_bwd_direct<false, WV><<<grid, dim3(64 * WV), 0, s>>>(G, W, dphi, R, N, K, fO, out, tm, tn, by_cols);
+    return hipGetLastError();
+  }
+  if (!dense_bwd_w_ok(G, W, R, N, K)) return hipErrorInvalidValue;
+  const long long big_tiles = (long long)cdiv(R, 128) * cdiv(N, 128);
+  if (big_tiles >= 512) return dense_bwd_ko_cfg<CfgBig8>(s, G, W, dphi, R, N, K, O, out);
+  return dense_bwd_ko_cfg<CfgSmall>(s, G, W, dphi, R, N, K, O, out);
 }
 
 // ------------------------------------------------------------------------------ seed, transpose
@@ -566,10 +843,9 @@ hipError_t launch_gram_strided(hipStream_t s, const float* a1, const float* a2, 
 // element q of both, so the four MFMAs cover the 16 columns of the slice (in a permuted order,
 // the same for both operands).
 template <bool VEC>
-__global__ void __launch_bounds__(256) k_gram_small(GramBatch g, int N1, int N2, int tiles_n) {
-  __shared__ float red[4][256];
-  const int z = blockIdx.y;
-  const int m0 = (blockIdx.x / tiles_n) * 16, n0 = (blockIdx.x % tiles_n) * 16;
+__device__ __forceinline__ void gram_small_block(const GramBatch& g, int N1, int N2, int tiles_n, int bx, int z,
+                                                 float (*red)[256]) {
+  const int m0 = (bx / tiles_n) * 16, n0 = (bx % tiles_n) * 16;
   const int K = g.K[z];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int i = lane & 15, kq = 4 * (lane >> 4);
@@ -577,27 +853,41 @@ __global__ void __launch_bounds__(256) k_gram_small(GramBatch g, int N1, int N2,
   const float* __restrict__ pa = g.h1[z] + (long long)min(m0 + i, N1 - 1) * K;
   const float* __restrict__ pb = g.h2[z] + (long long)min(n0 + i, N2 - 1) * K;
   f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll 4
-  for (int k0 = 16 * wave; k0 < K; k0 += 64) {
-    const int k = k0 + kq;
-    f32x4 a = {0.f, 0.f, 0.f, 0.f}, b = {0.f, 0.f, 0.f, 0.f};
-    if (VEC) {   // K % 4 == 0 and 16-byte aligned rows: the 4 columns are all in or all out
-      if (k < K) {
-        a = *reinterpret_cast<const f32x4*>(pa + k);
-        b = *reinterpret_cast<const f32x4*>(pb + k);
+  // batches of U slices: every load of a batch is issued before its MFMAs, from addresses
+  // clamped into the rows (a column past K reads a valid element and is zeroed), so that the
+  // loop body has no branch
+  constexpr int U = 4;
+  for (int kb = 16 * wave; kb < K; kb += 64 * U) {
+    f32x4 a[U], b[U];
+    bool in[U];
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const int k = kb + 64 * u + kq;
+      if (VEC) {   // K % 4 == 0 and 16-byte aligned rows: the 4 columns are all in or all out
+        in[u] = k < K;
+        const int kc = min(k, K - 4);
+        a[u] = *reinterpret_cast<const f32x4*>(pa + kc);
+        b[u] = *reinterpret_cast<const f32x4*>(pb + kc);
+      } else {
+        in[u] = true;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int kc = min(k + q, K - 1);
+          const float x = pa[kc], y = pb[kc];
+          a[u][q] = k + q < K ? x : 0.f;
+          b[u][q] = k + q < K ? y : 0.f;
+        }
       }
-    } else {
+    }
+    // keep the loads of the batch ahead of its MFMAs
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int u = 0; u < U; ++u) {
+      const bool use_a = va && in[u], use_b = vb && in[u];
 #pragma unroll
       for (int q = 0; q < 4; ++q)
-        if (k + q < K) {
-          a[q] = pa[k + q];
-          b[q] = pb[k + q];
-        }
+        acc = __builtin_amdgcn_mfma_f32_16x16x4f32(use_a ? a[u][q] : 0.f, use_b ? b[u][q] : 0.f, acc, 0, 0, 0);
     }
-    if (!va) a = f32x4{0.f, 0.f, 0.f, 0.f};
-    if (!vb) b = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-    for (int q = 0; q < 4; ++q) acc = __builtin_amdgcn_mfma_f32_16x16x4f32(a[q], b[q], acc, 0, 0, 0);
   }
 #pragma unroll
   for (int v = 0; v < 4; ++v) red[wave][(4 * (lane >> 4) + v) * 16 + i] = acc[v];
@@ -607,6 +897,12 @@ __global__ void __launch_bounds__(256) k_gram_small(GramBatch g, int N1, int N2,
     const float v = ((red[0][threadIdx.x] + red[1][threadIdx.x]) + red[2][threadIdx.x]) + red[3][threadIdx.x];
     g.out[z][(long long)(m0 + r) * N2 + n0 + c] = v + g.beta[z];
   }
+}
+
+template <bool VEC>
+__global__ void __launch_bounds__(256) k_gram_small(GramBatch g, int N1, int N2, int tiles_n) {
+  __shared__ float red[4][256];
+  gram_small_block<VEC>(g, N1, N2, tiles_n, blockIdx.x, blockIdx.y, red);
 }
 
 hipError_t launch_gram(hipStream_t s, const GramBatch& g, int N1, int N2, int num_cu) {
@@ -629,6 +925,59 @@ hipError_t launch_gram(hipStream_t s, const GramBatch& g, int N1, int N2, int nu
   if (dma) return gram_vec<true, true>(s, g, N1, N2);
   return v ? gram_vec<true, false>(s, g, N1, N2) : gram_vec<false, false>(s, g, N1, N2);
 }
+
+// A backward layer of few tiles and the small-batch Grams in one launch: the first nbwd
+// workgroups take the layer's tiles (which leave compute units idle), the others the 16 x 16
+// Gram blocks (gblocks per layer input).
+template <class Cfg, bool GVEC>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_dense_bwd_ko_gram(const float* __restrict__ G, const float* __restrict__ W, int R, int N, int K, EpiBwd epi,
+                    int tiles_n, int nbwd, GramBatch g, int N1, int N2, int gtiles_n, int gblocks) {
+  extern __shared__ float smem[];
+  static_assert(Cfg::THREADS == 256, "the Gram blocks run on 256 threads");
+  if ((int)blockIdx.x < nbwd) {
+    dense_bwd_ko_tile<Cfg>(G, W, R, N, K, epi, tiles_n, blockIdx.x, smem);
+  } else {
+    const int b = blockIdx.x - nbwd;
+    gram_small_block<GVEC>(g, N1, N2, gtiles_n, b % gblocks, b / gblocks, reinterpret_cast<float (*)[256]>(smem));
+  }
+}
+
+static bool gram_small_fits(const GramBatch& g, int N1, int N2, int num_cu) {
+  return g.count > 0 && (long long)cdiv(N1, 64) * cdiv(N2, 64) * g.count < num_cu;
+}
+
+static bool gram_batch_vec(const GramBatch& g) {
+  bool v = true;
+  for (int z = 0; z < g.count; ++z) v = v && vec_ok(g.h1[z], g.K[z], g.K[z]) && vec_ok(g.h2[z], g.K[z], g.K[z]);
+  return v;
+}
+
+hipError_t launch_dense_bwd_w_gram(hipStream_t s, const float* G, const float* W, const float* dphi, int R, int N,
+                                   int K, int O, float* out, const GramBatch& g, int N1, int N2, int num_cu) {
+  if (O <= 0 || !dense_bwd_w_ok(G, W, R, N, K)) return hipErrorInvalidValue;
+  const long long big_tiles = (long long)cdiv(R, 128) * cdiv(N, 128);
+  if (big_tiles >= 512 || !gram_small_fits(g, N1, N2, num_cu) || (dense_bwd_direct_ok(R, N, K) && kBwdDirectForm)) {
+    hipError_t e = launch_dense_bwd_w(s, G, W, dphi, R, N, K, O, out);
+    return e != hipSuccess ? e : launch_gram(s, g, N1, N2, num_cu);
+  }
+  using Cfg = CfgSmall;
+  EpiBwd epi{dphi, out, R, N, FastDiv((uint32_t)O)};
+  const int tn = cdiv(N, Cfg::BN), tm = cdiv(R, Cfg::BM);
+  const int gtn = cdiv(N2, 16), gblocks = cdiv(N1, 16) * gtn;
+  const long long blocks = (long long)tm * tn + (long long)gblocks * g.count;
+  constexpr int bytes = gemm_dma_smem_bytes<Cfg, 2>();
+  static_assert(bytes >= 4 * 256 * 4, "the Gram blocks' partials fit the LDS of the tiles");
+  auto go = [&](auto kern) -> hipError_t {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess) return e;
+    kern<<<dim3((unsigned)blocks), dim3(Cfg::THREADS), bytes, s>>>(G, W, R, N, K, epi, tn, tm * tn, g, N1, N2, gtn,
+                                                                    gblocks);
+    return hipGetLastError();
+  };
+  return gram_batch_vec(g) ? go(k_dense_bwd_ko_gram<Cfg, true>) : go(k_dense_bwd_ko_gram<Cfg, false>);
+}
+
 
 // ------------------------------------------------------------------------------ fused contraction
 // Stage the block of a Gram matrix that a tile touches (rows r cover samples r / O) into
@@ -736,40 +1085,12 @@ __device__ __forceinline__ void fcn_tile_coords(int t, int symmetric, int tiles_
   }
 }
 
-template <class Cfg, bool VEC, bool DMA>
-__global__ void __launch_bounds__(Cfg::THREADS)
-k_ntk_fcn_lpart(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, int tiles_n, int T, int NG,
-                float* __restrict__ part) {
-  extern __shared__ float smem[];
-  // the (group, tile) list in group-major order, in contiguous ranges per XCD: an XCD's
-  // workgroups read the cotangents of one or two layer groups through its L2
-  int blk;
-  if (!xcd_block(blockIdx.x, T * NG, blk)) return;
-  const int g = blk / T, t = blk - g * T;
-  int tm, tn;
-  fcn_tile_coords(t, symmetric, tiles_n, tm, tn);
-  const int O = (int)fO.d;
-  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
-  const int R1 = N1 * O, R2 = N2 * O;
-  const int l0 = (int)((long long)g * c.L / NG), l1 = (int)((long long)(g + 1) * c.L / NG);
-  f32x16 tot[Cfg::FM][Cfg::FN];
-  zero_acc<Cfg>(tot);
-  for (int l = l0; l < l1; ++l) fcn_layer_term<Cfg, VEC, DMA>(c, l, N2, R1, R2, fO, m0, n0, smem, tot);
-  float* P = part + ((long long)g * T + t) * (Cfg::BM * Cfg::BN);
-  for_each_acc<Cfg>(tot, 0, 0, [&](int r, int s, float v) { P[r * Cfg::BN + s] = v; });
-}
-
-// One workgroup per tile.  Each thread adds 16 elements (four float4s) of the tile's NG partials
-// in group order, the four loads of one partial in flight together, adds the readout summand and
-// stages the result in LDS; theta is then written in runs of O consecutive floats: the direct
-// block in row order, the mirrored one (symmetric schedule) in column order.
-__global__ void __launch_bounds__(256)
-k_ntk_fcn_lreduce(const float* __restrict__ gram_readout, float readout_scale, int N1, int N2, FastDiv fO,
-                  int symmetric, int tiles_n, int T, int NG, const float* __restrict__ part,
-                  float* __restrict__ theta) {
-  __shared__ float sg[64 * 64];
-  __shared__ float tile[64][65];
-  const int t = blockIdx.x;
+// The work of one tile (256 threads): the NG partial tiles added in group order, the readout
+// summand, theta written from the LDS copy of the tile.  sg holds 64 x 64 floats, tile 64 x 65.
+__device__ __forceinline__ void fcn_tile_reduce(const float* __restrict__ gram_readout, float readout_scale, int N1,
+                                                int N2, FastDiv fO, int symmetric, int tiles_n, int T, int NG,
+                                                const float* __restrict__ part, float* __restrict__ theta, int t,
+                                                float* sg, float (*tile)[65]) {
   int tm, tn;
   fcn_tile_coords(t, symmetric, tiles_n, tm, tn);
   const int O = (int)fO.d;
@@ -789,17 +1110,27 @@ k_ntk_fcn_lreduce(const float* __restrict__ gram_readout, float readout_scale, i
   float4 v[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) v[j] = P[threadIdx.x + 256 * j];
-  for (int g = 1; g < NG; ++g) {
-    float4 w[4];
+  // the groups four at a time, all their loads in flight together (a group past NG reads the
+  // last one again and is not added)
+  for (int g0 = 1; g0 < NG; g0 += 4) {
+    float4 w[4][4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) w[j] = P[g * gstride + threadIdx.x + 256 * j];
+    for (int u = 0; u < 4; ++u) {
+      const long long g = min(g0 + u, NG - 1);
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      v[j].x += w[j].x;
-      v[j].y += w[j].y;
-      v[j].z += w[j].z;
-      v[j].w += w[j].w;
+      for (int j = 0; j < 4; ++j) w[u][j] = P[g * gstride + threadIdx.x + 256 * j];
     }
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (g0 + u < NG) {
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          v[j].x += w[u][j].x;
+          v[j].y += w[u][j].y;
+          v[j].z += w[u][j].z;
+          v[j].w += w[u][j].w;
+        }
+      }
   }
   __syncthreads();   // sg complete
 #pragma unroll
@@ -840,6 +1171,43 @@ k_ntk_fcn_lreduce(const float* __restrict__ gram_readout, float readout_scale, i
       theta[(((long long)n2 * N1 + n1) * O + o2) * O + o1] = tile[rl][sl];
     }
   }
+}
+
+template <class Cfg, bool VEC, bool DMA>
+__global__ void __launch_bounds__(Cfg::THREADS)
+k_ntk_fcn_lpart(FcnContraction c, int N1, int N2, FastDiv fO, int symmetric, int tiles_n, int T, int NG,
+                float* __restrict__ part) {
+  extern __shared__ float smem[];
+  // the (group, tile) list in group-major order, in contiguous ranges per XCD: an XCD's
+  // workgroups read the cotangents of one or two layer groups through its L2
+  int blk;
+  if (!xcd_block(blockIdx.x, T * NG, blk)) return;
+  const int g = blk / T, t = blk - g * T;
+  int tm, tn;
+  fcn_tile_coords(t, symmetric, tiles_n, tm, tn);
+  const int O = (int)fO.d;
+  const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
+  const int R1 = N1 * O, R2 = N2 * O;
+  const int l0 = (int)((long long)g * c.L / NG), l1 = (int)((long long)(g + 1) * c.L / NG);
+  f32x16 tot[Cfg::FM][Cfg::FN];
+  zero_acc<Cfg>(tot);
+  for (int l = l0; l < l1; ++l) fcn_layer_term<Cfg, VEC, DMA>(c, l, N2, R1, R2, fO, m0, n0, smem, tot);
+  float* P = part + ((long long)g * T + t) * (Cfg::BM * Cfg::BN);
+  for_each_acc<Cfg>(tot, 0, 0, [&](int r, int s, float v) { P[r * Cfg::BN + s] = v; });
+}
+
+// One workgroup per tile.  Each thread adds 16 elements (four float4s) of the tile's NG partials
+// in group order, the four loads of one partial in flight together, adds the readout summand and
+// stages the result in LDS; theta is then written in runs of O consecutive floats: the direct
+// block in row order, the mirrored one (symmetric schedule) in column order.
+__global__ void __launch_bounds__(256)
+k_ntk_fcn_lreduce(const float* __restrict__ gram_readout, float readout_scale, int N1, int N2, FastDiv fO,
+                  int symmetric, int tiles_n, int T, int NG, const float* __restrict__ part,
+                  float* __restrict__ theta) {
+  __shared__ float sg[64 * 64];
+  __shared__ float tile[64][65];
+  fcn_tile_reduce(gram_readout, readout_scale, N1, N2, fO, symmetric, tiles_n, T, NG, part, theta, blockIdx.x, sg,
+                  tile);
 }
 
 // ------------------------------------------------------------------------------ stream-K contraction

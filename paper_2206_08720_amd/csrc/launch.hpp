@@ -50,14 +50,24 @@ const char* kernel_class_name(int cls);
 
 // ---- fully-connected path ------------------------------------------------------------
 // z = h W^T (+ b);  hn = act(z);  dphi = act'(z).  h [M, K], W [N, K], hn/dphi [M, N].
-// Small batches split K over fp64 partials in `part` (capacity in doubles; may be null).
+// Small batches split K over fp64 partials in `part` (capacity in doubles; may be null).  With
+// seedG, also the readout cotangents seedG[m, o, c] = seedW[o, c] dphi[m, c] for o < seedO (in the
+// same launch where the shape allows).
 long long dense_fwd_part_doubles(long long max_rows, long long max_cols);
+// whether the forward of M x N outputs runs as one launch of 16 x 16 blocks (the seed then in it)
+bool dense_fwd_small_ok(long long M, long long N);
 hipError_t launch_dense_fwd(hipStream_t s, const float* h, const float* W, const float* b, int M,
                             int N, int K, int act, float* hn, float* dphi, double* part,
-                            long long part_capacity);
+                            long long part_capacity, const float* seedW = nullptr, int seedO = 0,
+                            float* seedG = nullptr);
 // out[r, c] = (sum_k G[r, k] Wt[c, k]) * dphi[(r / O), c].  G [R, K], Wt [N, K], dphi [R/O, N].
 hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, const float* dphi,
                             int R, int N, int K, int O, float* out);
+// The same product reading W [K, N] itself (out = (G W) * dphi[r / O]), without a transposed
+// copy: dense_bwd_w_ok says whether the shape and buffers take this form.
+bool dense_bwd_w_ok(const float* G, const float* W, long long R, long long N, long long K);
+hipError_t launch_dense_bwd_w(hipStream_t s, const float* G, const float* W, const float* dphi, int R, int N,
+                              int K, int O, float* out);
 // Pointwise (1x1) convolution backward: rows r = (img*O + o)*D + p of R cotangent pixels,
 // out[r, c] = (sum_k G[r, k] Wt[c, k]) * dphi[img*D + p, c]  (dphi null: the identity).
 hipError_t launch_pw_bwd(hipStream_t s, const float* G, const float* Wt, const float* dphi, int R, int N,
@@ -85,8 +95,12 @@ struct GramBatch {
   int count;
 };
 // out_l[n1, n2] = h1_l[n1] . h2_l[n2] + beta_l for every l (rows of h have stride K_l).
-// Batches whose matrix-core tiles would not fill num_cu compute units run on the vector units.
+// Batches whose 64 x 64 tiles would not fill num_cu compute units run in 16 x 16 blocks.
 hipError_t launch_gram(hipStream_t s, const GramBatch& g, int N1, int N2, int num_cu);
+// launch_dense_bwd_w and launch_gram together, in one launch where the layer's tiles leave
+// compute units idle and the Grams take 16 x 16 blocks.
+hipError_t launch_dense_bwd_w_gram(hipStream_t s, const float* G, const float* W, const float* dphi, int R, int N,
+                                   int K, int O, float* out, const GramBatch& g, int N1, int N2, int num_cu);
 // out[b][n1][n2] = a1[n1 ld + b bs .. + K] . a2[n2 ld + b bs .. + K] for b < batches (rows of
 // stride ld floats, batch b at the float offset b bs of each row)
 hipError_t launch_gram_strided(hipStream_t s, const float* a1, const float* a2, int N1, int N2, int K,

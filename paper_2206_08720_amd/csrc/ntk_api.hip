@@ -681,7 +681,8 @@ static int jc_dense_layer(ntk_handle* h, const float* G1, const float* G2, long 
 // The layers of the forward pass for the rows [r0, r1) of the stacked batch (h0: its layer-0
 // input), on stream st; split-K partials (one buffer) only when use_part.
 static int fcn_forward_rows(ntk_handle* h, const float* const* params, const float* h0, int r0, int r1,
-                            hipStream_t st, bool use_part) {
+                            hipStream_t st, bool use_part, const float* seedW = nullptr, int seedO = 0,
+                            float* seedG = nullptr) {
   const int L = h->L;
   Profiler* P = &h->prof;
   auto F = [&](size_t off) { return reinterpret_cast<float*>(h->ws + off); };
@@ -695,7 +696,8 @@ static int fcn_forward_rows(ntk_handle* h, const float* const* params, const flo
                                     F(h->off_h[l + 1]) + (size_t)r0 * h->dims[l + 1],
                                     F(h->off_dphi[l]) + (size_t)r0 * h->dims[l + 1],
                                     use_part ? reinterpret_cast<double*>(h->ws + h->off_fpart) : nullptr,
-                                    use_part ? h->fpart_capacity : 0);
+                                    use_part ? h->fpart_capacity : 0, l == L - 1 ? seedW : nullptr, seedO,
+                                    l == L - 1 ? seedG : nullptr);
     prof_end(P, st, KC_DENSE_FWD);
     if (e != hipSuccess) return hip_fail(h, e, "dense forward");
   }
@@ -725,12 +727,15 @@ static int fcn_stack(ntk_handle* h, const float* const* params, const float* X1,
 
 // Forward pass of the stacked batch keeping the layer inputs, on the handle's stream.
 static int fcn_forward(ntk_handle* h, const float* const* params, const float* X1, int n1,
-                       const float* X2, int n2, bool sym, const float** h0) {
+                       const float* X2, int n2, bool sym, const float** h0, const float* seedW = nullptr,
+                       int seedO = 0, float* seedG = nullptr) {
   int rc = fcn_stack(h, params, X1, n1, X2, n2, sym, h0);
   if (rc != NTK_OK) return rc;
-  return fcn_forward_rows(h, params, *h0, 0, sym ? n1 : n1 + n2, h->stream, true);
+  return fcn_forward_rows(h, params, *h0, 0, sym ? n1 : n1 + n2, h->stream, true, seedW, seedO, seedG);
 }
 
+// the cotangent backward reads each W_l itself (K-outer tiles) when the shapes allow
+constexpr bool kBwdFromW = true;
 // forward FLOPs from which the FCN path puts independent steps on the second stream
 constexpr double kAuxStreamMinFlops = 4e9;
 
@@ -758,8 +763,11 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   const int Oe = logit ? 1 : O;
   for (int l = 0; l <= L; ++l)
     if (!params[h->param_index[l]]) return fail(h, NTK_E_ARG, "null weight pointer");
+  // set below: every backward layer reads W_l itself (few output tiles), no transposed copies;
+  // with one stream, the Grams in the launch of the first backward layer
+  bool direct = false, gram_in_bwd = false;
   auto transposes = [&](hipStream_t st) -> int {
-    if (L < 2) return NTK_OK;
+    if (L < 2 || direct) return NTK_OK;
     TransposeBatch tb{};
     tb.count = L - 1;
     for (int l = 1; l < L; ++l) {
@@ -776,6 +784,18 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   const float* h0 = nullptr;
   auto hptr = [&](int l) -> const float* { return l == 0 ? h0 : F(h->off_h[l]); };
   auto H2 = [&](int l) -> const float* { return sym ? hptr(l) : hptr(l) + (size_t)n1 * h->dims[l]; };
+  auto gram_batch = [&]() {
+    GramBatch gb{};
+    gb.count = L + 1;
+    for (int l = 0; l <= L; ++l) {
+      gb.h1[l] = hptr(l);
+      gb.h2[l] = H2(l);
+      gb.out[l] = F(h->off_gram[l]);
+      gb.K[l] = h->dims[l];
+      gb.beta[l] = h->layers[l].has_bias ? 1.0f : 0.0f;
+    }
+    return gb;
+  };
   // layer-input Grams (the x1.x2 scalars; per-sample scalars on the batch diagonal)
   auto grams = [&](hipStream_t st) -> int {
     hipError_t err;
@@ -794,15 +814,7 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
       prof_end(P, st, KC_GRAM);
       return err == hipSuccess ? NTK_OK : hip_fail(h, err, "diagonal layer-input scalars");
     }
-    GramBatch gb{};
-    gb.count = L + 1;
-    for (int l = 0; l <= L; ++l) {
-      gb.h1[l] = hptr(l);
-      gb.h2[l] = H2(l);
-      gb.out[l] = F(h->off_gram[l]);
-      gb.K[l] = h->dims[l];
-      gb.beta[l] = h->layers[l].has_bias ? 1.0f : 0.0f;
-    }
+    const GramBatch gb = gram_batch();
     prof_begin(P, st, KC_GRAM);
     err = launch_gram(st, gb, n1, n2, h->num_cu);
     prof_end(P, st, KC_GRAM);
@@ -821,6 +833,14 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   // one layer of the cotangent backward for the samples [r0, r1)
   auto bwd_layer = [&](hipStream_t st, int l, int r0, int r1) -> hipError_t {
     const size_t K = h->dims[l + 1], N = h->dims[l];
+    if (direct && gram_in_bwd && l == L - 1)
+      return launch_dense_bwd_w_gram(st, F(h->off_G[l]) + (size_t)r0 * Oe * K, params[h->param_index[l]],
+                                     F(h->off_dphi[l - 1]) + (size_t)r0 * N, (r1 - r0) * Oe, N, K, Oe,
+                                     F(h->off_G[l - 1]) + (size_t)r0 * Oe * N, gram_batch(), n1, n2, h->num_cu);
+    if (direct)
+      return launch_dense_bwd_w(st, F(h->off_G[l]) + (size_t)r0 * Oe * K, params[h->param_index[l]],
+                                     F(h->off_dphi[l - 1]) + (size_t)r0 * N, (r1 - r0) * Oe, N, K, Oe,
+                                     F(h->off_G[l - 1]) + (size_t)r0 * Oe * N);
     return launch_dense_bwd(st, F(h->off_G[l]) + (size_t)r0 * Oe * K, F(h->off_Wt[l]),
                             F(h->off_dphi[l - 1]) + (size_t)r0 * N, (r1 - r0) * Oe, N, K, Oe,
                             F(h->off_G[l - 1]) + (size_t)r0 * Oe * N);
@@ -843,6 +863,11 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     min_tiles = min_tiles < 0 ? t : std::min(min_tiles, t);
   }
   const bool split = aux && L >= 2 && M >= 2 && min_tiles >= 2LL * h->num_cu;
+  direct = !split && L >= 2 && kBwdFromW;
+  for (int l = 1; l < L; ++l)
+    direct = direct && dense_bwd_w_ok(F(h->off_G[l]), params[h->param_index[l]], (long long)M * Oe, h->dims[l],
+                                      h->dims[l + 1]);
+  gram_in_bwd = direct && !aux && !jc && !diag;
   const int MA = split ? M / 2 : M;   // samples on the main stream; the rest on the second
   const bool halves = split && !P->enabled;
   int rc;
@@ -886,10 +911,15 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     if (aux && (rc = fork(h->ev_fork, s, aux)) != NTK_OK) return rc;
     if ((rc = transposes(sa)) != NTK_OK) return rc;
     if (aux && (e = hipEventRecord(h->ev_tr, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
-    // 1. forward pass keeping the layer inputs
-    if ((rc = fcn_forward(h, params, X1, n1, X2, n2, sym, &h0)) != NTK_OK) return rc;
-    // 2. the Grams, on the second stream while the backward runs
-    if (!jc) {
+    // 1. forward pass keeping the layer inputs (small batches: the readout cotangents in the
+    //    last layer's launch)
+    const bool fused_seed = L >= 1 && dense_fwd_small_ok(M, h->dims[L]);
+    if ((rc = fused_seed ? fcn_forward(h, params, X1, n1, X2, n2, sym, &h0, WL, Oe, F(h->off_G[L - 1]))
+                         : fcn_forward(h, params, X1, n1, X2, n2, sym, &h0)) != NTK_OK)
+      return rc;
+    // 2. the Grams, on the second stream while the backward runs (or in the first backward
+    //    layer's launch)
+    if (!jc && !gram_in_bwd) {
       if (aux && (rc = fork(h->ev_fwd, s, sa)) != NTK_OK) return rc;
       if ((rc = grams(sa)) != NTK_OK) return rc;
       if (aux && (e = hipEventRecord(h->ev_gram, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
@@ -897,7 +927,7 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     // 3. the cotangents of every hidden pre-activation
     if (aux && (e = hipStreamWaitEvent(s, h->ev_tr, 0)) != hipSuccess) return hip_fail(h, e, "stream join");
     if (L >= 1) {
-      if ((rc = seed(s, 0, M)) != NTK_OK) return rc;
+      if (!fused_seed && (rc = seed(s, 0, M)) != NTK_OK) return rc;
       if (split && (rc = fork(h->ev_seed, s, aux)) != NTK_OK) return rc;
       prof_begin(P, s, KC_DENSE_BWD);
       for (int l = L - 1; l >= 1; --l) {
