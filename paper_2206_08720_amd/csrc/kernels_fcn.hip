@@ -504,89 +504,6 @@ hipError_t launch_dense_bwd(hipStream_t s, const float* G, const float* Wt, cons
            : dense_bwd_cfg<CfgSmall, false>(s, G, Wt, dphi, R, N, K, O, out);
 }
 
-// Few output tiles (a small batch): one 32 x 32 block of the cotangents per workgroup, its four
-// waves taking every fourth 8-column slice of K with the 32x32x2 fp32 MFMA, and the B operand read
-// from W itself (row k of W is B[k][.]; no transposed copy); the waves' partial blocks are added in
-// wave order through LDS and multiplied by act'.  A lane loads the columns k0 + 4 (l / 32) + q
-// (q = 0..3) of row l % 32 of G and the same rows of W at column l % 32 (32 lanes read 32
-// consecutive floats of a row of W), and MFMA q contracts element q; the MFMA returns
-// D[8 (v / 4) + 4 (l / 32) + v % 4][l % 32] in element v of lane l.
-constexpr int kBwdDirectTiles = 256;   // fewer 64 x 64 output tiles than this: the direct form
-constexpr int kBwdDirectWaves = 8;
-constexpr bool kBwdDirectForm = false;   // measured slower than the 64 x 64 tiles
-template <bool VEC, int WAVES>
-__global__ void __launch_bounds__(64 * WAVES)
-k_dense_bwd_direct(const float* __restrict__ G, const float* __restrict__ W, const float* __restrict__ dphi,
-                   int R, int N, int K, FastDiv fO, float* __restrict__ out, int tiles_m, int tiles_n,
-                   int by_cols) {
-  __shared__ float red[WAVES][1024];
-  int m0, n0;
-  if (!small_block_coords(tiles_m, tiles_n, by_cols, 32, m0, n0)) return;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int i = lane & 31, kh = 4 * (lane >> 5);
-  const bool va = m0 + i < R, vb = n0 + i < N;
-  const float* __restrict__ pa = G + (long long)min(m0 + i, R - 1) * K;
-  const float* __restrict__ pb = W + min(n0 + i, N - 1);
-  f32x16 acc;
-#pragma unroll
-  for (int v = 0; v < 16; ++v) acc[v] = 0.f;
-  // batches of U slices: every load of a batch is issued before its MFMAs, from addresses
-  // clamped into the operands (a column past K reads a valid element and is zeroed), so that
-  // the loop body has no branch
-  constexpr int U = 8;
-  for (int kb = 8 * wave; kb < K; kb += 8 * WAVES * U) {
-    f32x4 a[U], b[U];
-    bool in[U];
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const int k = kb + 8 * WAVES * u + kh;
-      if (VEC) {   // K % 4 == 0 and 16-byte aligned rows of G: the 4 columns are all in or all out
-        in[u] = k < K;
-        const int kc = min(k, K - 4);
-        a[u] = *reinterpret_cast<const f32x4*>(pa + kc);
-#pragma unroll
-        for (int q = 0; q < 4; ++q) b[u][q] = pb[(long long)(kc + q) * N];
-      } else {
-        in[u] = true;
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const int kc = min(k + q, K - 1);
-          const float x = pa[kc], y = pb[(long long)kc * N];
-          a[u][q] = k + q < K ? x : 0.f;
-          b[u][q] = k + q < K ? y : 0.f;
-        }
-      }
-    }
-    // keep the loads of the batch ahead of its MFMAs
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int u = 0; u < U; ++u) {
-      const bool use_a = va && in[u], use_b = vb && in[u];
-#pragma unroll
-      for (int q = 0; q < 4; ++q)
-        acc = __builtin_amdgcn_mfma_f32_32x32x2f32(use_a ? a[u][q] : 0.f, use_b ? b[u][q] : 0.f, acc, 0, 0, 0);
-    }
-  }
-#pragma unroll
-  for (int v = 0; v < 16; ++v) red[wave][(8 * (v >> 2) + 4 * (lane >> 5) + (v & 3)) * 32 + i] = acc[v];
-  __syncthreads();
-#pragma unroll
-  for (int j = 0; j < 1024 / (64 * WAVES); ++j) {
-    const int t = threadIdx.x + 64 * WAVES * j, r = m0 + (t >> 5), c = n0 + (t & 31);
-    if (r < R && c < N) {
-      float v = red[0][t];
-#pragma unroll
-      for (int w = 1; w < WAVES; ++w) v += red[w][t];
-      out[(long long)r * N + c] = v * dphi[(long long)fO.div((uint32_t)r) * N + c];
-    }
-  }
-}
-
-bool dense_bwd_direct_ok(long long R, long long N, long long K) {
-  return R > 0 && N > 0 && K > 0 && R < (1LL << 31) && N < (1LL << 31) && K < (1LL << 31) &&
-         (long long)cdiv(R, 64) * cdiv(N, 64) < kBwdDirectTiles;
-}
-
 bool dense_bwd_w_ok(const float* G, const float* W, long long R, long long N, long long K) {
   return R > 0 && R < (1LL << 31) && K % 32 == 0 && K > 0 && N % 4 == 0 && N >= 4 &&
          vec_ok(G, K, K) && vec_ok(W, N, N) && dma_span_ok(K, K, 256) && K * N * 4 < (1LL << 31);
@@ -595,18 +512,6 @@ bool dense_bwd_w_ok(const float* G, const float* W, long long R, long long N, lo
 hipError_t launch_dense_bwd_w(hipStream_t s, const float* G, const float* W, const float* dphi, int R, int N,
                               int K, int O, float* out) {
   if (O <= 0) return hipErrorInvalidValue;
-  if (dense_bwd_direct_ok(R, N, K) && kBwdDirectForm) {
-    const int tm = cdiv(R, 32), tn = cdiv(N, 32);
-    const int by_cols = R < N;   // each XCD reads a slice of the larger operand
-    const dim3 grid((unsigned)(8 * cdiv((long long)tm * tn, 8)));
-    const FastDiv fO((uint32_t)O);
-    constexpr int WV = kBwdDirectWaves;
-    if (vec_ok(G, K, K))
-      k_dense_bwd_direct<true, WV><<<grid, dim3(64 * WV), 0, s>>>(G, W, dphi, R, N, K, fO, out, tm, tn, by_cols);
-    else
-      k_dense_bwd_direct<false, WV><<<grid, dim3(64 * WV), 0, s>>>(G, W, dphi, R, N, K, fO, out, tm, tn, by_cols);
-    return hipGetLastError();
-  }
   if (!dense_bwd_w_ok(G, W, R, N, K)) return hipErrorInvalidValue;
   const long long big_tiles = (long long)cdiv(R, 128) * cdiv(N, 128);
   if (big_tiles >= 512) return dense_bwd_ko_cfg<CfgBig8>(s, G, W, dphi, R, N, K, O, out);
@@ -957,7 +862,7 @@ hipError_t launch_dense_bwd_w_gram(hipStream_t s, const float* G, const float* W
                                    int K, int O, float* out, const GramBatch& g, int N1, int N2, int num_cu) {
   if (O <= 0 || !dense_bwd_w_ok(G, W, R, N, K)) return hipErrorInvalidValue;
   const long long big_tiles = (long long)cdiv(R, 128) * cdiv(N, 128);
-  if (big_tiles >= 512 || !gram_small_fits(g, N1, N2, num_cu) || (dense_bwd_direct_ok(R, N, K) && kBwdDirectForm)) {
+  if (big_tiles >= 512 || !gram_small_fits(g, N1, N2, num_cu)) {
     hipError_t e = launch_dense_bwd_w(s, G, W, dphi, R, N, K, O, out);
     return e != hipSuccess ? e : launch_gram(s, g, N1, N2, num_cu);
   }

@@ -734,8 +734,6 @@ static int fcn_forward(ntk_handle* h, const float* const* params, const float* X
   return fcn_forward_rows(h, params, *h0, 0, sym ? n1 : n1 + n2, h->stream, true, seedW, seedO, seedG);
 }
 
-// the cotangent backward reads each W_l itself (K-outer tiles) when the shapes allow
-constexpr bool kBwdFromW = true;
 // forward FLOPs from which the FCN path puts independent steps on the second stream
 constexpr double kAuxStreamMinFlops = 4e9;
 
@@ -763,11 +761,12 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   const int Oe = logit ? 1 : O;
   for (int l = 0; l <= L; ++l)
     if (!params[h->param_index[l]]) return fail(h, NTK_E_ARG, "null weight pointer");
-  // set below: every backward layer reads W_l itself (few output tiles), no transposed copies;
-  // with one stream, the Grams in the launch of the first backward layer
-  bool direct = false, gram_in_bwd = false;
+  // set below: every backward layer reads W_l itself (K-outer tiles) where the shapes allow, so
+  // that no transposed copies are made; with one stream, the Grams in the launch of the first
+  // backward layer
+  bool bwd_w = false, gram_in_bwd = false;
   auto transposes = [&](hipStream_t st) -> int {
-    if (L < 2 || direct) return NTK_OK;
+    if (L < 2 || bwd_w) return NTK_OK;
     TransposeBatch tb{};
     tb.count = L - 1;
     for (int l = 1; l < L; ++l) {
@@ -833,11 +832,11 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
   // one layer of the cotangent backward for the samples [r0, r1)
   auto bwd_layer = [&](hipStream_t st, int l, int r0, int r1) -> hipError_t {
     const size_t K = h->dims[l + 1], N = h->dims[l];
-    if (direct && gram_in_bwd && l == L - 1)
+    if (bwd_w && gram_in_bwd && l == L - 1)
       return launch_dense_bwd_w_gram(st, F(h->off_G[l]) + (size_t)r0 * Oe * K, params[h->param_index[l]],
                                      F(h->off_dphi[l - 1]) + (size_t)r0 * N, (r1 - r0) * Oe, N, K, Oe,
                                      F(h->off_G[l - 1]) + (size_t)r0 * Oe * N, gram_batch(), n1, n2, h->num_cu);
-    if (direct)
+    if (bwd_w)
       return launch_dense_bwd_w(st, F(h->off_G[l]) + (size_t)r0 * Oe * K, params[h->param_index[l]],
                                      F(h->off_dphi[l - 1]) + (size_t)r0 * N, (r1 - r0) * Oe, N, K, Oe,
                                      F(h->off_G[l - 1]) + (size_t)r0 * Oe * N);
@@ -863,17 +862,18 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     min_tiles = min_tiles < 0 ? t : std::min(min_tiles, t);
   }
   const bool split = aux && L >= 2 && M >= 2 && min_tiles >= 2LL * h->num_cu;
-  direct = !split && L >= 2 && kBwdFromW;
+  bwd_w = L >= 2;
   for (int l = 1; l < L; ++l)
-    direct = direct && dense_bwd_w_ok(F(h->off_G[l]), params[h->param_index[l]], (long long)M * Oe, h->dims[l],
+    bwd_w = bwd_w && dense_bwd_w_ok(F(h->off_G[l]), params[h->param_index[l]], (long long)M * Oe, h->dims[l],
                                       h->dims[l + 1]);
-  gram_in_bwd = direct && !aux && !jc && !diag;
+  gram_in_bwd = bwd_w && !aux && !jc && !diag;
   const int MA = split ? M / 2 : M;   // samples on the main stream; the rest on the second
   const bool halves = split && !P->enabled;
   int rc;
   if (halves) {
     // stream s: the forward and backward of samples [0, MA), then the Grams;
-    // stream aux: the transposes, then the forward and backward of samples [MA, M)
+    // stream aux: the weight transposes (when the backward cannot read W itself), then the
+    // forward and backward of samples [MA, M)
     if ((rc = fcn_stack(h, params, X1, n1, X2, n2, sym, &h0)) != NTK_OK) return rc;
     if ((rc = fork(h->ev_fork, s, aux)) != NTK_OK || (rc = transposes(aux)) != NTK_OK) return rc;
     if ((e = hipEventRecord(h->ev_tr, aux)) != hipSuccess) return hip_fail(h, e, "stream event");
@@ -907,7 +907,8 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     }
     if ((e = hipStreamWaitEvent(s, h->ev_bwd, 0)) != hipSuccess) return hip_fail(h, e, "stream join");
   } else {
-    // 0. weight transposes for the backward, on the second stream while the forward runs
+    // 0. weight transposes for a backward that cannot read W itself, on the second stream
+    //    while the forward runs
     if (aux && (rc = fork(h->ev_fork, s, aux)) != NTK_OK) return rc;
     if ((rc = transposes(sa)) != NTK_OK) return rc;
     if (aux && (e = hipEventRecord(h->ev_tr, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
