@@ -113,6 +113,8 @@ EDGE = [
     ("64 hidden layers (the maximum)", wl.fcn_spec("e9", 8, [16] * 64, 3, bias=True), 6, 5),
     ("one hidden layer of width 8192", wl.fcn_spec("e10", 16, [8192], 10), 8, 7),
     ("O=128 outputs", wl.fcn_spec("e11", 12, [40], 128, act="erf"), 6, 4),
+    # more 64 x 64 Gram tiles than CUs: the first backward layer and the Grams in two launches
+    ("Grams past the 16x16-block form, 700 x 700", wl.fcn_spec("e12", 24, [64, 64], 2, bias=True), 700, 700),
 ]
 
 
@@ -123,6 +125,37 @@ def test_edge_shapes(case):
     X1 = wl.make_inputs(spec, n1, 600 + n1)
     X2 = wl.make_inputs(spec, n2, 700 + n2)
     _vs_jc(label, spec, params, X1, X2)
+
+
+def test_unaligned_parameters_and_inputs():
+    """Weights, biases and inputs at 4-byte (not 16-byte) aligned addresses: the backward then
+    reads per-call transposed weights instead of W itself, and the forward and the Grams take
+    their scalar-load forms; Theta still matches the Jacobian contraction."""
+    import torch
+    from paper_2206_08720_amd.ntk import NTK
+    spec = wl.fcn_spec("unal", 32, [64, 64, 64], 5, act="relu", bias=True)
+    params = wl.make_params(spec, 41, bias_var=0.2)
+    X1 = wl.make_inputs(spec, 40, 42)
+    X2 = wl.make_inputs(spec, 33, 43)
+
+    def shifted(a):   # a contiguous view one float past a 256-byte aligned allocation
+        buf = torch.empty(a.size + 1, dtype=torch.float32, device="cuda")
+        v = buf[1:].view(a.shape)
+        v.copy_(torch.from_numpy(np.ascontiguousarray(a, dtype=np.float32)))
+        assert v.data_ptr() % 16 == 4
+        return v
+
+    h = NTK(spec, 40, 40)
+    try:
+        out = h.compute([shifted(p) for p in params], shifted(X1), shifted(X2))
+        torch.cuda.synchronize()
+        got = out.cpu().numpy()
+    finally:
+        h.close()
+    ref, d1, d2 = oracle.ntk_jc_with_norms(spec, params, X1, X2, layer_storage=S)
+    cs, nw = errors(got, ref, d1, d2)
+    report("unaligned parameters and inputs", cs, nw)
+    assert cs <= TOL and nw <= TOL
 
 
 @pytest.mark.parametrize("symmetric", [True, False])
