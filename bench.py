@@ -172,9 +172,9 @@ def copy_calibration():
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the NTK output "
-              "blocks are independent and would shard over a 2-D grid of GPUs, which this "
-              "build does not run.", file=sys.stderr)
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the NTK's output blocks "
+              "are independent and would shard over a 2-D grid of GPUs, but the library runs on one GPU "
+              "per process.", file=sys.stderr)
         sys.exit(2)
     import numpy as np
     import torch
