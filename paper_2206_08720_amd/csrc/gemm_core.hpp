@@ -784,10 +784,13 @@ __host__ inline bool dma_span_ok(long long ld, long long K, int rows) {
 // block: by then every wave holds that block's fragments in registers (so the stage may be
 // overwritten afterwards) and has seen its own loads of tile kt+1 land, and the fragments of
 // tile kt+1's first block are read while the last block's MFMAs run.  Ends with a barrier, so
-// the caller may reuse `smem` afterwards.
+// the caller may reuse `smem` afterwards.  `wave` is the wave's index among the Cfg::WAVES waves
+// that share this loop and its LDS stages (the _w form lets a workgroup run several such groups,
+// each on its own K range and LDS, as long as every group makes the same number of K tiles: the
+// barriers are the workgroup's).
 template <class Cfg, int NSTAGE, class IA, class IB, class AccT>
-__device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, int n0, int k_begin, int k_end,
-                                                      float* smem, AccT& acc) {
+__device__ __forceinline__ void gemm_mainloop_dma_ops_w(IA& ia, IB& ib, int m0, int n0, int k_begin, int k_end,
+                                                        float* smem, AccT& acc, int wave, int lane) {
   static_assert(Cfg::BK == 32, "direct-to-LDS main loop uses BK = 32");
   using TA = typename IA::Tile;
   using TB = typename IB::Tile;
@@ -795,8 +798,6 @@ __device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, in
   static_assert(MB::NB % 2 == 0, "fragment buffers alternate within a K tile");
   constexpr int STAGE = TA::FLOATS + TB::FLOATS;
   constexpr int PER_TILE = IA::template OPS<Cfg::WAVES> + IB::template OPS<Cfg::WAVES>;  // DMA ops per wave
-  const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
   const int wm0 = (wave / Cfg::WAVES_N) * Cfg::WM;
   const int wn0 = (wave % Cfg::WAVES_N) * Cfg::WN;
   const int nk = (k_end - k_begin + 31) / 32;
@@ -861,6 +862,13 @@ __device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, in
   if constexpr (NSTAGE > 3)
     if (kb + 2 < nk) tile(kb + 2, std::integral_constant<int, 2>{});
   __syncthreads();
+}
+
+template <class Cfg, int NSTAGE, class IA, class IB, class AccT>
+__device__ __forceinline__ void gemm_mainloop_dma_ops(IA& ia, IB& ib, int m0, int n0, int k_begin, int k_end,
+                                                      float* smem, AccT& acc) {
+  gemm_mainloop_dma_ops_w<Cfg, NSTAGE>(ia, ib, m0, n0, k_begin, k_end, smem, acc, (int)(threadIdx.x >> 6),
+                                       (int)(threadIdx.x & 63));
 }
 
 // Both operands K-contiguous row-major (LoadKInnerT<true> conditions, K % 32 == 0).
