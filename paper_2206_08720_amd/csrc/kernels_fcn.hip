@@ -123,13 +123,6 @@ k_dense_fwd_reduce(const double* __restrict__ part, int splits, int M, int N, co
   }
 }
 
-// Few rows and columns (a small batch): one 16 x 16 block of z per workgroup, so that even a
-// 128 x 512 layer makes 256 workgroups without partial sums in memory.  The four waves take
-// every fourth 16-column slice of K with the 16x16x4 fp64 MFMA on the exactly widened fp32
-// values, and their partial blocks are added in wave order, in fp64, through LDS before the bias
-// and the activation's decision.  A lane loads the four columns k0 + 4 (l / 16) + q (q = 0..3) of
-// row l % 16 of both operands, and MFMA q contracts element q (the same column permutation for
-// both operands); the fp64 MFMA returns D[4 v + l / 16][l % 16] in element v of lane l.
 // Block coordinates of the small-batch kernels: the tm x tn blocks of B x B outputs are numbered
 // row by row (or column by column when by_cols) and cut into 8 contiguous ranges, one per XCD, so
 // that an XCD reads a slice of the larger operand through its L2 (and all of the smaller one).
@@ -145,6 +138,14 @@ __device__ __forceinline__ bool small_block_coords(int tiles_m, int tiles_n, int
   return true;
 }
 
+// Few rows and columns (a small batch): one 16 x 16 block of z per workgroup, so that even a
+// 128 x 512 layer makes 256 workgroups without partial sums in memory.  The WAVES waves take
+// every WAVES-th 16-column slice of K with the 16x16x4 fp64 MFMA on the exactly widened fp32
+// values, and their partial blocks are added in wave order, in fp64, through LDS before the bias
+// and the activation's decision (with sg, the last hidden layer also writes the readout
+// cotangents).  A lane loads the four columns k0 + 4 (l / 16) + q (q = 0..3) of row l % 16 of
+// both operands, and MFMA q contracts element q (the same column permutation for both
+// operands); the fp64 MFMA returns D[4 v + l / 16][l % 16] in element v of lane l.
 constexpr int kFwdSmallBlocks = 1024;   // at most this many 16 x 16 blocks (four per CU)
 constexpr int kFwdSmallWaves = 8;
 constexpr int kSeedPre = 16;
