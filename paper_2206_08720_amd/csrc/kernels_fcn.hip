@@ -61,10 +61,13 @@ __device__ __forceinline__ void fwd_epilogue(double z, int act, float& h, float&
   }
 }
 
-template <class Cfg, bool VEC, bool DMA>
+// With SEED (the last hidden layer), the epilogue also writes the readout cotangents
+// sg[r, o, c] = sw[o, c] act'(z[r, c]) for o < so.
+template <class Cfg, bool VEC, bool DMA, bool SEED = false>
 __global__ void __launch_bounds__(Cfg::THREADS)
 k_dense_fwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restrict__ bias, int M, int N,
-            int act, float* __restrict__ hn, float* __restrict__ dphi, int tiles_n) {
+            int act, float* __restrict__ hn, float* __restrict__ dphi, int tiles_n,
+            const float* __restrict__ sw = nullptr, int so = 0, float* __restrict__ sg = nullptr) {
   extern __shared__ float smem[];
   const int tm = blockIdx.x / tiles_n, tn = blockIdx.x % tiles_n;
   const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
@@ -81,6 +84,10 @@ k_dense_fwd(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, const float* __restrict__ 
     if (r < M && c < N) {
       hn[(long long)r * N + c] = h;
       dphi[(long long)r * N + c] = d;
+      if (SEED) {
+        float* g = sg + (long long)r * so * N + c;
+        for (int o = 0; o < so; ++o) g[(long long)o * N] = sw[(long long)o * N + c] * d;
+      }
     }
   });
 }
@@ -110,7 +117,8 @@ k_dense_fwd_part(LoadKInnerT<VEC> la, LoadKInnerT<VEC> lb, int M, int N, int chu
 
 __global__ void __launch_bounds__(256)
 k_dense_fwd_reduce(const double* __restrict__ part, int splits, int M, int N, const float* __restrict__ bias,
-                   int act, float* __restrict__ hn, float* __restrict__ dphi) {
+                   int act, float* __restrict__ hn, float* __restrict__ dphi, const float* __restrict__ sw,
+                   int so, float* __restrict__ sg) {
   const long long total = (long long)M * N;
   for (long long i = blockIdx.x * 256LL + threadIdx.x; i < total; i += (long long)gridDim.x * 256) {
     double z = 0.0;
@@ -120,6 +128,10 @@ k_dense_fwd_reduce(const double* __restrict__ part, int splits, int M, int N, co
     fwd_epilogue(z, act, h, d);
     hn[i] = h;
     dphi[i] = d;
+    if (sg) {   // the readout cotangents of the last hidden layer
+      const long long r = i / N, c = i - r * N;
+      for (int o = 0; o < so; ++o) sg[(r * so + o) * N + c] = sw[(long long)o * N + c] * d;
+    }
   }
 }
 
@@ -246,7 +258,7 @@ long long dense_fwd_part_doubles(long long max_rows, long long max_cols) {
 template <class Cfg, bool VEC, bool DMA = false>
 static hipError_t dense_fwd_cfg(hipStream_t s, const float* h, const float* W, const float* b, int M,
                                 int N, int K, int act, float* hn, float* dphi, double* part,
-                                long long part_capacity) {
+                                long long part_capacity, const float* sw, int so, float* sg) {
   using L = LoadKInnerT<VEC>;
   L la{h, M, K, K};
   L lb{W, N, K, K};
@@ -270,15 +282,16 @@ static hipError_t dense_fwd_cfg(hipStream_t s, const float* h, const float* W, c
     if (e != hipSuccess) return e;
     const long long total = (long long)M * N;
     k_dense_fwd_reduce<<<dim3((unsigned)std::min<long long>((total + 255) / 256, 4096)), dim3(256), 0, s>>>(
-        part, splits, M, N, b, act, hn, dphi);
+        part, splits, M, N, b, act, hn, dphi, sw, so, sg);
     return hipGetLastError();
   }
-  hipError_t e = hipFuncSetAttribute((const void*)k_dense_fwd<Cfg, VEC, DMA>,
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
-  if (e != hipSuccess) return e;
-  k_dense_fwd<Cfg, VEC, DMA><<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(la, lb, b, M, N, act, hn,
-                                                                               dphi, tn);
-  return hipGetLastError();
+  auto go = [&](auto kern) -> hipError_t {
+    hipError_t e = hipFuncSetAttribute((const void*)kern, hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+    if (e != hipSuccess) return e;
+    kern<<<dim3(tm * tn), dim3(Cfg::THREADS), bytes, s>>>(la, lb, b, M, N, act, hn, dphi, tn, sw, so, sg);
+    return hipGetLastError();
+  };
+  return sg ? go(k_dense_fwd<Cfg, VEC, DMA, true>) : go(k_dense_fwd<Cfg, VEC, DMA, false>);
 }
 
 hipError_t launch_dense_fwd(hipStream_t s, const float* h, const float* W, const float* b, int M,
@@ -300,14 +313,14 @@ hipError_t launch_dense_fwd(hipStream_t s, const float* h, const float* W, const
                                                                   seedW, seedO, seedG);
     return hipGetLastError();
   }
-  if (seedG) {
-    hipError_t e = launch_dense_fwd(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity, nullptr, 0, nullptr);
-    return e != hipSuccess ? e : launch_bwd_seed(s, seedW, dphi, M, seedO, N, seedG);
-  }
   if (v && K % 32 == 0 && dma_span_ok(K, K, 256))
-    return dense_fwd_cfg<CfgFwd64, true, true>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity);
-  if (v) return dense_fwd_cfg<CfgFwd64, true>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity);
-  return dense_fwd_cfg<CfgFwd64, false>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity);
+    return dense_fwd_cfg<CfgFwd64, true, true>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity, seedW,
+                                               seedO, seedG);
+  if (v)
+    return dense_fwd_cfg<CfgFwd64, true>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity, seedW, seedO,
+                                         seedG);
+  return dense_fwd_cfg<CfgFwd64, false>(s, h, W, b, M, N, K, act, hn, dphi, part, part_capacity, seedW, seedO,
+                                        seedG);
 }
 
 // ------------------------------------------------------------------------------ backward
@@ -575,48 +588,7 @@ hipError_t launch_dense_bwd_w(hipStream_t s, const float* G, const float* W, con
   return dense_bwd_ko_cfg<CfgSmall>(s, G, W, dphi, R, N, K, O, out);
 }
 
-// ------------------------------------------------------------------------------ seed, transpose
-// G[(m, o), c] = W[o, c] * dphi[m, c]: workgroup w takes sample row m = w / ob and the outputs
-// o = (w % ob) * kSeedO ... (at most kSeedO of them), float4 columns when `vec` (C % 4 == 0,
-// 16-byte aligned buffers).
-constexpr int kSeedO = 4;
-__global__ void __launch_bounds__(256)
-k_bwd_seed(const float* __restrict__ W, const float* __restrict__ dphi, int M, int O, int C, int vec,
-           float* __restrict__ G) {
-  const int ob = (O + kSeedO - 1) / kSeedO;
-  for (long long w = blockIdx.x; w < (long long)M * ob; w += gridDim.x) {
-    const int m = (int)(w / ob);
-    const int o0 = (int)(w - (long long)m * ob) * kSeedO, o1 = min(O, o0 + kSeedO);
-    const float* dm = dphi + (long long)m * C;
-    float* gm = G + (long long)m * O * C;
-    if (vec) {
-      const int C4 = C >> 2;
-      for (int c4 = threadIdx.x; c4 < C4; c4 += blockDim.x) {
-        const float4 d = reinterpret_cast<const float4*>(dm)[c4];
-        for (int o = o0; o < o1; ++o) {
-          const float4 wv = reinterpret_cast<const float4*>(W + (long long)o * C)[c4];
-          reinterpret_cast<float4*>(gm + (long long)o * C)[c4] =
-              make_float4(wv.x * d.x, wv.y * d.y, wv.z * d.z, wv.w * d.w);
-        }
-      }
-    } else {
-      for (int c = threadIdx.x; c < C; c += blockDim.x) {
-        const float d = dm[c];
-        for (int o = o0; o < o1; ++o) gm[(long long)o * C + c] = W[(long long)o * C + c] * d;
-      }
-    }
-  }
-}
-
-hipError_t launch_bwd_seed(hipStream_t s, const float* W, const float* dphi, int M, int O, int C,
-                           float* G) {
-  if (M <= 0 || O <= 0 || C <= 0) return hipSuccess;
-  const int vec = vec_ok(W, C, C) && vec_ok(dphi, C, C) && vec_ok(G, C, C);
-  const long long work = (long long)M * ((O + kSeedO - 1) / kSeedO);
-  k_bwd_seed<<<dim3((unsigned)std::min<long long>(work, 65535)), dim3(256), 0, s>>>(W, dphi, M, O, C, vec, G);
-  return hipGetLastError();
-}
-
+// ------------------------------------------------------------------------------ transpose
 // One 32 x 32 tile of Wt = W^T (W is R x C, row-major), staged through LDS.
 __device__ __forceinline__ void transpose_tile(const float* __restrict__ W, int R, int C, float* __restrict__ Wt,
                                                int c0, int r0, float (*tile)[33]) {

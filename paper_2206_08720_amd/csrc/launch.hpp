@@ -51,8 +51,8 @@ const char* kernel_class_name(int cls);
 // ---- fully-connected path ------------------------------------------------------------
 // z = h W^T (+ b);  hn = act(z);  dphi = act'(z).  h [M, K], W [N, K], hn/dphi [M, N].
 // Small batches split K over fp64 partials in `part` (capacity in doubles; may be null).  With
-// seedG, also the readout cotangents seedG[m, o, c] = seedW[o, c] dphi[m, c] for o < seedO (in the
-// same launch where the shape allows).
+// seedG, the epilogue also writes the readout cotangents seedG[m, o, c] = seedW[o, c] dphi[m, c]
+// for o < seedO.
 long long dense_fwd_part_doubles(long long max_rows, long long max_cols);
 // whether the forward of M x N outputs runs as one launch of 16 x 16 blocks (the seed then in it)
 bool dense_fwd_small_ok(long long M, long long N);
@@ -72,9 +72,6 @@ hipError_t launch_dense_bwd_w(hipStream_t s, const float* G, const float* W, con
 // out[r, c] = (sum_k G[r, k] Wt[c, k]) * dphi[img*D + p, c]  (dphi null: the identity).
 hipError_t launch_pw_bwd(hipStream_t s, const float* G, const float* Wt, const float* dphi, int R, int N,
                          int K, int O, int D, float* out);
-// G[m, o, c] = W[o, c] * dphi[m, c]   (cotangent of the last hidden pre-activation).
-hipError_t launch_bwd_seed(hipStream_t s, const float* W, const float* dphi, int M, int O, int C,
-                           float* G);
 // Wt [C, R] = W^T for W [R, C].
 hipError_t launch_transpose(hipStream_t s, const float* W, int R, int C, float* Wt);
 // Wt[z] = W[z]^T for z < count (each W[z] R[z] x C[z], row-major), in one launch.

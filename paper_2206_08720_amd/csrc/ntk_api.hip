@@ -820,15 +820,9 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     return err == hipSuccess ? NTK_OK : hip_fail(h, err, "gram");
   };
   // cotangents of the last hidden pre-activation for all O outputs at once (for the one logit o*
-  // alone in NTK_OUTPUT_LOGIT: the cotangent rows are then (n) instead of (n, o)), rows [r0, r1)
+  // alone in NTK_OUTPUT_LOGIT: the cotangent rows are then (n) instead of (n, o)): written by the
+  // epilogue of the last forward layer, G[n, o, c] = WL[o, c] act'(z[n, c])
   const float* WL = params[h->param_index[L]] + (logit ? (size_t)h->opt_logit * h->dims[L] : 0);
-  auto seed = [&](hipStream_t st, int r0, int r1) -> int {
-    prof_begin(P, st, KC_BWD_SEED);
-    hipError_t err = launch_bwd_seed(st, WL, F(h->off_dphi[L - 1]) + (size_t)r0 * h->dims[L], r1 - r0, Oe,
-                                     h->dims[L], F(h->off_G[L - 1]) + (size_t)r0 * Oe * h->dims[L]);
-    prof_end(P, st, KC_BWD_SEED);
-    return err == hipSuccess ? NTK_OK : hip_fail(h, err, "backward seed");
-  };
   // one layer of the cotangent backward for the samples [r0, r1)
   auto bwd_layer = [&](hipStream_t st, int l, int r0, int r1) -> hipError_t {
     const size_t K = h->dims[l + 1], N = h->dims[l];
@@ -886,14 +880,15 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
         const float* in = (l == 0 ? h0 : F(h->off_h[l])) + (size_t)r0 * h->dims[l];
         const long long cap = h->fpart_capacity / 2;
         double* part = h->fpart_capacity ? reinterpret_cast<double*>(h->ws + h->off_fpart) + half * cap : nullptr;
+        const bool last = l == L - 1;
         e = launch_dense_fwd(half ? aux : s, in, W, b, r1 - r0, h->dims[l + 1], h->dims[l], h->layers[l].act,
                              F(h->off_h[l + 1]) + (size_t)r0 * h->dims[l + 1],
-                             F(h->off_dphi[l]) + (size_t)r0 * h->dims[l + 1], part, part ? cap : 0);
+                             F(h->off_dphi[l]) + (size_t)r0 * h->dims[l + 1], part, part ? cap : 0,
+                             last ? WL : nullptr, Oe, last ? F(h->off_G[l]) + (size_t)r0 * Oe * h->dims[l + 1] : nullptr);
         if (e != hipSuccess) return hip_fail(h, e, "dense forward");
       }
     }
     if ((e = hipEventRecord(h->ev_fwd, aux)) != hipSuccess) return hip_fail(h, e, "stream event");
-    if ((rc = seed(s, 0, MA)) != NTK_OK || (rc = seed(aux, MA, M)) != NTK_OK) return rc;
     if ((e = hipStreamWaitEvent(s, h->ev_tr, 0)) != hipSuccess) return hip_fail(h, e, "stream join");
     for (int l = L - 1; l >= 1; --l) {
       e = bwd_layer(s, l, 0, MA);
@@ -912,11 +907,10 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     if (aux && (rc = fork(h->ev_fork, s, aux)) != NTK_OK) return rc;
     if ((rc = transposes(sa)) != NTK_OK) return rc;
     if (aux && (e = hipEventRecord(h->ev_tr, sa)) != hipSuccess) return hip_fail(h, e, "stream event");
-    // 1. forward pass keeping the layer inputs (small batches: the readout cotangents in the
-    //    last layer's launch)
-    const bool fused_seed = L >= 1 && dense_fwd_small_ok(M, h->dims[L]);
-    if ((rc = fused_seed ? fcn_forward(h, params, X1, n1, X2, n2, sym, &h0, WL, Oe, F(h->off_G[L - 1]))
-                         : fcn_forward(h, params, X1, n1, X2, n2, sym, &h0)) != NTK_OK)
+    // 1. forward pass keeping the layer inputs, and the readout cotangents in the last layer's
+    //    epilogue
+    if ((rc = L >= 1 ? fcn_forward(h, params, X1, n1, X2, n2, sym, &h0, WL, Oe, F(h->off_G[L - 1]))
+                     : fcn_forward(h, params, X1, n1, X2, n2, sym, &h0)) != NTK_OK)
       return rc;
     // 2. the Grams, on the second stream while the backward runs (or in the first backward
     //    layer's launch)
@@ -928,7 +922,6 @@ static int compute_fcn(ntk_handle* h, const float* const* params, const float* X
     // 3. the cotangents of every hidden pre-activation
     if (aux && (e = hipStreamWaitEvent(s, h->ev_tr, 0)) != hipSuccess) return hip_fail(h, e, "stream join");
     if (L >= 1) {
-      if (!fused_seed && (rc = seed(s, 0, M)) != NTK_OK) return rc;
       if (split && (rc = fork(h->ev_seed, s, aux)) != NTK_OK) return rc;
       prof_begin(P, s, KC_DENSE_BWD);
       for (int l = L - 1; l >= 1; --l) {
