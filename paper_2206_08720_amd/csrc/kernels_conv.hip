@@ -776,6 +776,45 @@ hipError_t launch_readout_fold(hipStream_t s, const float* Wr, int C, int O, con
   return hipGetLastError();
 }
 
+// The traced output of the folded last convolution: theta[n1, n2] += scale sum_c w_c Mc[c][n1, n2]
+// with w_c = sum_o Wr[o, c]^2 (the trace of Wr[o1, c] Wr[o2, c] over o), staged in LDS when the C
+// weights fit (LDS), else formed per channel from Wr; one pair per thread, channels in order.
+template <bool LDS>
+__global__ void __launch_bounds__(256)
+k_readout_fold_trace(const float* __restrict__ Wr, int C, int O, const float* __restrict__ Mc, long long plane,
+                     float scale, float* __restrict__ theta) {
+  extern __shared__ float wsum[];
+  auto weight = [&](int c) -> float {
+    float v = 0.f;
+    for (int o = 0; o < O; ++o) {
+      const float x = Wr[(long long)o * C + c];
+      v += x * x;
+    }
+    return v;
+  };
+  if (LDS) {
+    for (int c = threadIdx.x; c < C; c += 256) wsum[c] = weight(c);
+    __syncthreads();
+  }
+  for (long long p = blockIdx.x * 256LL + threadIdx.x; p < plane; p += (long long)gridDim.x * 256) {
+    float acc = 0.f;
+    for (int c = 0; c < C; ++c) acc += (LDS ? wsum[c] : weight(c)) * Mc[(long long)c * plane + p];
+    theta[p] += scale * acc;
+  }
+}
+
+hipError_t launch_readout_fold_trace(hipStream_t s, const float* Wr, int C, int O, const float* Mc, int N1, int N2,
+                                     float scale, float* theta) {
+  const long long plane = (long long)N1 * N2;
+  if (plane <= 0 || O <= 0 || C <= 0) return hipSuccess;
+  const unsigned grid = (unsigned)std::min<long long>((plane + 255) / 256, 4096);
+  if (C <= kFoldLdsFloats)
+    k_readout_fold_trace<true><<<dim3(grid), dim3(256), (size_t)C * 4, s>>>(Wr, C, O, Mc, plane, scale, theta);
+  else
+    k_readout_fold_trace<false><<<dim3(grid), dim3(256), 0, s>>>(Wr, C, O, Mc, plane, scale, theta);
+  return hipGetLastError();
+}
+
 // Kt[ci, kh, kw, co] = K[co, 2 - kh, 2 - kw, ci]
 __global__ void k_conv_flip(const float* __restrict__ K, int Cout, int Cin, float* __restrict__ Kt) {
   const int total = Cout * 9 * Cin;

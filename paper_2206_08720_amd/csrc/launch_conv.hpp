@@ -46,6 +46,9 @@ hipError_t launch_conv_wgrad_padded(hipStream_t s, const float* G, const float* 
 // theta[n1, n2, o1, o2] += scale sum_c Wr[o1, c] Wr[o2, c] Mc[c, n1, n2] (Wr [O, C], Mc [C, N1, N2]).
 hipError_t launch_readout_fold(hipStream_t s, const float* Wr, int C, int O, const float* Mc, int N1, int N2,
                                float scale, float* theta);
+// The same for the traced output theta [N1, N2]: theta += scale sum_c (sum_o Wr[o, c]^2) Mc[c].
+hipError_t launch_readout_fold_trace(hipStream_t s, const float* Wr, int C, int O, const float* Mc, int N1, int N2,
+                                     float scale, float* theta);
 // Deterministic split-K product J1 J2^T: plan, partial products, reduction into theta.
 int splitk_tile();
 // splits * R1 * R2 <= part_capacity (floats) always holds for the returned plan.

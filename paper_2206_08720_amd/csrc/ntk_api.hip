@@ -1135,9 +1135,10 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   // Wr[o, c] A[n, c, k] / D with A[n, c, k] = sum_p act'(z[n, p, c]) patch[n, p, k], and its
   // summand is sum_c Wr[o1, c] Wr[o2, c] (A1[., c, .] A2[., c, .]^T)[n1, n2] / D^2: the O outputs
   // leave that layer's weight-space product and contraction ("fold").  Outside-in layers only, the
-  // full O x O output, with other columns in J (the split-K contraction then writes theta first).
+  // full O x O output or its trace (then sum_c (sum_o Wr[o, c]^2) Gram_c / D^2) on the full batch,
+  // with other columns in J (the split-K contraction then writes theta first).
   const int ll = nc - 1;
-  bool fold = nc >= 1 && h->off_mc && h->wslot[ll] >= 0 && O >= 2 && !logit && !trace && !diag &&
+  bool fold = nc >= 1 && h->off_mc && h->wslot[ll] >= 0 && O >= 2 && !logit && !diag &&
               h->opt_method != NTK_METHOD_JACOBIAN &&
               (h->layers[ll].kind == NTK_CONV3X3_SAME || h->layers[ll].kind == NTK_CONV1X1);
   if (fold) {   // other weight-space columns: a bias, a depthwise or scale layer, an outside-in conv
@@ -1417,7 +1418,10 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
     prof_begin(P, s, KC_GRAM);
     e = launch_gram_strided(s, fold_A, A2, n1, n2, KC, (long long)C * KC, KC, C, F(h->off_mc));
     if (e == hipSuccess)
-      e = launch_readout_fold(s, params[h->rslot], C, O, F(h->off_mc), n1, n2, 1.f / ((float)D * (float)D), theta);
+      e = trace ? launch_readout_fold_trace(s, params[h->rslot], C, O, F(h->off_mc), n1, n2,
+                                            1.f / ((float)D * (float)D), theta)
+                : launch_readout_fold(s, params[h->rslot], C, O, F(h->off_mc), n1, n2, 1.f / ((float)D * (float)D),
+                                      theta);
     prof_end(P, s, KC_GRAM);
     if (e != hipSuccess) return hip_fail(h, e, "last convolution's summand");
   }

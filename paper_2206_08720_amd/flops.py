@@ -124,13 +124,14 @@ def _conv_orders(sp, O, n1, n2, output, batch, M, Oe, Oc, gpairs, order):
     folded, as the library decides: _inside_out per layer; the fold (the last convolution's
     cotangent is the readout's through the global pool, so its weight-space columns factor into
     Wr[o, c] times O-free per-channel rows and its summand into per-channel Grams) for a last 3x3
-    or pointwise convolution, the full O x O output (O >= 2) on the full batch, with other
+    or pointwise convolution, the full O x O output or its trace (O >= 2) on the full batch, with other
     weight-space columns in the contraction (a bias, a depthwise or scale layer, an outside-in
     convolution); with order "auto" the last convolution then goes outside-in when the fold's
     M D F Cin Cout + N1 N2 (F Cin Cout + O^2 Cout) is below its inside-out cost."""
     trace = output == "trace"
     io = [_inside_out(k, D, cin, cout, M, Oe, Oc, gpairs, order, trace) for (k, cin, cout, D, bias) in sp]
-    if not sp or O < 2 or output != "full" or batch != "full" or sp[-1][0] not in ("conv3x3", "conv1x1"):
+    if not sp or O < 2 or output not in ("full", "trace") or batch != "full" or \
+            sp[-1][0] not in ("conv3x3", "conv1x1"):
         return io, False
     others = bool(sp[-1][4]) or any(b or k in ("dwconv3x3", "scale") or (k in ("conv3x3", "conv1x1") and not io[i])
                                     for i, (k, ci, co, D, b) in enumerate(sp[:-1]))
@@ -159,7 +160,8 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
     products Oe D^2 Cout and Oc D Cout (the form of the appendix "CNN NTK Complexity" with the
     patch-pair Gram built from the pixel Gram instead of D^2 F Cin patch products).  With `fold`
     (the library's schedule, _conv_orders) the last convolution forms O-free rows A [M, C, F Cin]
-    ("wgrad"), no J columns, and per-channel Grams plus their O x O sums ("gram"); fold=False counts
+    ("wgrad"), no J columns, and per-channel Grams plus their O x O sums, or for the trace their
+    sum weighted by sum_o Wr[o, c]^2 ("gram"); fold=False counts
     every outside-in layer alike, as the paper's table does (and the orders of the plain cost
     model)."""
     layers = spec["layers"]
@@ -187,7 +189,10 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
                 # the folded last convolution: A [M, C, F Cin] (one row block per sample instead
                 # of O), the per-channel Grams of every input pair, and the O x O sums over C
                 wg += 2.0 * M * cout * (F * cin) * D
-                fold_gram = 2.0 * n1 * n2 * cout * F * cin + 3.0 * n1 * n2 * O * O * cout
+                if output == "trace":   # weights sum_o Wr[o, c]^2, then one weighted sum per pair
+                    fold_gram = 2.0 * n1 * n2 * cout * F * cin + 2.0 * O * cout + 2.0 * n1 * n2 * cout
+                else:
+                    fold_gram = 2.0 * n1 * n2 * cout * F * cin + 3.0 * n1 * n2 * O * O * cout
             elif not inside[i]:
                 wg += 2.0 * M * (Oe * cout) * (F * cin) * D
                 cols += F * cin * cout

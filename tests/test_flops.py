@@ -101,8 +101,15 @@ def test_variant_counts():
     cs = wl.cnn_spec("c", (4, 4), 3, [8, 8], O)
     cf, cl = cnn_flops(cs, N, N, fold=False), cnn_flops(cs, N, N, output="logit")
     assert cl["wgrad"] == cf["wgrad"] / O and cl["contraction"] == cf["contraction"] / O ** 2
-    # one logit: nothing to fold (the library folds the full O x O output only)
+    # one logit: nothing to fold (its backward has one output already)
     assert cnn_flops(cs, N, N, output="logit", fold=False) == cl
+    # the trace folds the last convolution like the full output, with one weighted sum per pair
+    ct = cnn_flops(cs, N, N, output="trace")
+    ctu = cnn_flops(cs, N, N, output="trace", fold=False)
+    M, D, F, cin, cout = 2 * N, 16, 9, 8, 8
+    assert ctu["wgrad"] - ct["wgrad"] == 2 * M * (O - 1) * cout * F * cin * D
+    assert ct["gram"] - ctu["gram"] == 2 * N * N * cout * F * cin + 2 * O * cout + 2 * N * N * cout
+    assert ctu["contraction"] - ct["contraction"] == 2 * N * N * O * F * cin * cout
 
 
 def test_jacobian_contraction_count_is_the_papers_n2_o2_p():
