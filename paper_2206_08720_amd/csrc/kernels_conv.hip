@@ -776,6 +776,33 @@ hipError_t launch_readout_fold(hipStream_t s, const float* Wr, int C, int O, con
   return hipGetLastError();
 }
 
+// The batch diagonal of the folded last convolution's per-channel Grams: Mc[c][n] =
+// A1[n, c, :] . A2[n, c, :] (rows of KC floats, sample n's channel c at (n C + c) KC), one wave
+// per (c, n), the lanes' partial sums added in a fixed butterfly order.
+__global__ void __launch_bounds__(256)
+k_fold_rowdot(const float* __restrict__ A1, const float* __restrict__ A2, int n, int C, int KC,
+              float* __restrict__ Mc) {
+  const long long item = blockIdx.x * 4LL + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (item >= (long long)n * C) return;   // the whole wave
+  const int c = (int)(item / n), i = (int)(item - (long long)c * n);
+  const float* a = A1 + ((long long)i * C + c) * KC;
+  const float* b = A2 + ((long long)i * C + c) * KC;
+  float v = 0.f;
+  for (int k = lane; k < KC; k += 64) v += a[k] * b[k];
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  if (lane == 0) Mc[item] = v;
+}
+
+hipError_t launch_fold_rowdot(hipStream_t s, const float* A1, const float* A2, int n, int C, int KC, float* Mc) {
+  const long long items = (long long)n * C;
+  if (items <= 0) return hipSuccess;
+  if ((items + 3) / 4 > 0x7fffffffLL) return hipErrorInvalidValue;
+  k_fold_rowdot<<<dim3((unsigned)((items + 3) / 4)), dim3(256), 0, s>>>(A1, A2, n, C, KC, Mc);
+  return hipGetLastError();
+}
+
 // The traced output of the folded last convolution: theta[n1, n2] += scale sum_c w_c Mc[c][n1, n2]
 // with w_c = sum_o Wr[o, c]^2 (the trace of Wr[o1, c] Wr[o2, c] over o), staged in LDS when the C
 // weights fit (LDS), else formed per channel from Wr; one pair per thread, channels in order.

@@ -49,6 +49,10 @@ hipError_t launch_readout_fold(hipStream_t s, const float* Wr, int C, int O, con
 // The same for the traced output theta [N1, N2]: theta += scale sum_c (sum_o Wr[o, c]^2) Mc[c].
 hipError_t launch_readout_fold_trace(hipStream_t s, const float* Wr, int C, int O, const float* Mc, int N1, int N2,
                                      float scale, float* theta);
+// Mc[c][i] = A1[i, c, :] . A2[i, c, :] for i < n (rows of KC floats at (i C + c) KC): the per-channel
+// Grams of the folded last convolution on the batch diagonal (then launch_readout_fold with N1 = n,
+// N2 = 1 adds them into theta [n, O, O], launch_readout_fold_trace into theta [n]).
+hipError_t launch_fold_rowdot(hipStream_t s, const float* A1, const float* A2, int n, int C, int KC, float* Mc);
 // Deterministic split-K product J1 J2^T: plan, partial products, reduction into theta.
 int splitk_tile();
 // splits * R1 * R2 <= part_capacity (floats) always holds for the returned plan.

@@ -1135,10 +1135,11 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
   // Wr[o, c] A[n, c, k] / D with A[n, c, k] = sum_p act'(z[n, p, c]) patch[n, p, k], and its
   // summand is sum_c Wr[o1, c] Wr[o2, c] (A1[., c, .] A2[., c, .]^T)[n1, n2] / D^2: the O outputs
   // leave that layer's weight-space product and contraction ("fold").  Outside-in layers only, the
-  // full O x O output or its trace (then sum_c (sum_o Wr[o, c]^2) Gram_c / D^2) on the full batch,
-  // with other columns in J (the split-K contraction then writes theta first).
+  // full O x O output or its trace (then sum_c (sum_o Wr[o, c]^2) Gram_c / D^2), on the full batch
+  // or its diagonal (the per-channel Grams' diagonals), with other columns in J (their contraction
+  // then writes theta first).
   const int ll = nc - 1;
-  bool fold = nc >= 1 && h->off_mc && h->wslot[ll] >= 0 && O >= 2 && !logit && !diag &&
+  bool fold = nc >= 1 && h->off_mc && h->wslot[ll] >= 0 && O >= 2 && !logit &&
               h->opt_method != NTK_METHOD_JACOBIAN &&
               (h->layers[ll].kind == NTK_CONV3X3_SAME || h->layers[ll].kind == NTK_CONV1X1);
   if (fold) {   // other weight-space columns: a bias, a depthwise or scale layer, an outside-in conv
@@ -1157,7 +1158,7 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
     const ntk_layer_desc& L = h->layers[ll];
     const double F = L.kind == NTK_CONV1X1 ? 1 : 9;
     const double Dl = (double)h->bh[ll] * h->bw[ll], Cin = h->ch[ll], Co = h->ch[ll + 1];
-    const double folded = (double)M * Dl * F * Cin * Co + (double)n1 * n2 * (F * Cin * Co + (double)O * O * Co);
+    const double folded = (double)M * Dl * F * Cin * Co + pairs * (F * Cin * Co + (double)O * O * Co);
     if (folded < inside_out_cost(pairs, (int)Dl, h->ch[ll], h->ch[ll + 1], Oe, trace)) inside[ll] = 0;
   }
   fold = fold && !inside[ll];
@@ -1390,24 +1391,24 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
                           h->part_capacity);
       prof_end(P, s, KC_NTK_DIAG);
       if (e != hipSuccess) return hip_fail(h, e, "diagonal contraction");
-      return NTK_OK;
+    } else {
+      const int Or = trace ? 1 : Oe;                 // rows per sample of the contraction
+      const long long Kc = trace ? (long long)O * Kcall : Kcall;
+      int R1, R2;
+      if (!to_int((long long)n1 * Or, R1) || !to_int((long long)n2 * Or, R2))
+        return fail(h, NTK_E_UNSUPPORTED, "contraction rows exceed 2^31");
+      int chunk = 0;
+      const int splits = splitk_plan(R1, R2, Kc, sym ? 1 : 0, h->part_capacity, &chunk);
+      prof_begin(P, s, KC_NTK_SPLITK);
+      e = launch_ntk_splitk(s, J, J2, R1, R2, Kc, Kc, sym ? 1 : 0, chunk, splits, F(h->off_part));
+      prof_end(P, s, KC_NTK_SPLITK);
+      if (e != hipSuccess) return hip_fail(h, e, "split-K contraction");
+      prof_begin(P, s, KC_NTK_REDUCE);
+      e = launch_ntk_reduce(s, F(h->off_part), splits, n1, n2, Or, sym ? 1 : 0, nullptr, F(h->off_gram_r),
+                            rscale, theta_written ? 1 : 0, theta);
+      prof_end(P, s, KC_NTK_REDUCE);
+      if (e != hipSuccess) return hip_fail(h, e, "split-K reduction");
     }
-    const int Or = trace ? 1 : Oe;                 // rows per sample of the contraction
-    const long long Kc = trace ? (long long)O * Kcall : Kcall;
-    int R1, R2;
-    if (!to_int((long long)n1 * Or, R1) || !to_int((long long)n2 * Or, R2))
-      return fail(h, NTK_E_UNSUPPORTED, "contraction rows exceed 2^31");
-    int chunk = 0;
-    const int splits = splitk_plan(R1, R2, Kc, sym ? 1 : 0, h->part_capacity, &chunk);
-    prof_begin(P, s, KC_NTK_SPLITK);
-    e = launch_ntk_splitk(s, J, J2, R1, R2, Kc, Kc, sym ? 1 : 0, chunk, splits, F(h->off_part));
-    prof_end(P, s, KC_NTK_SPLITK);
-    if (e != hipSuccess) return hip_fail(h, e, "split-K contraction");
-    prof_begin(P, s, KC_NTK_REDUCE);
-    e = launch_ntk_reduce(s, F(h->off_part), splits, n1, n2, Or, sym ? 1 : 0, nullptr, F(h->off_gram_r),
-                          rscale, theta_written ? 1 : 0, theta);
-    prof_end(P, s, KC_NTK_REDUCE);
-    if (e != hipSuccess) return hip_fail(h, e, "split-K reduction");
   }
   if (fold) {
     // theta += sum_c Wr[o1, c] Wr[o2, c] Mc[c] / D^2, Mc[c] = A1[., c, .] A2[., c, .]^T
@@ -1415,12 +1416,15 @@ static int compute_cnn(ntk_handle* h, const float* const* params, const float* X
     const int cin = h->ch[ll], KC = (L.kind == NTK_CONV3X3_SAME ? 9 : 1) * cin;
     const int D = h->bh[nc] * h->bw[nc];
     const float* A2 = sym ? fold_A : fold_A + (size_t)n1 * C * KC;
+    // the Grams of every pair [C][n1][n2], or on the batch diagonal [C][n] (n2 = 1 below)
+    const int m2 = diag ? 1 : n2;
     prof_begin(P, s, KC_GRAM);
-    e = launch_gram_strided(s, fold_A, A2, n1, n2, KC, (long long)C * KC, KC, C, F(h->off_mc));
+    e = diag ? launch_fold_rowdot(s, fold_A, A2, n1, C, KC, F(h->off_mc))
+             : launch_gram_strided(s, fold_A, A2, n1, n2, KC, (long long)C * KC, KC, C, F(h->off_mc));
     if (e == hipSuccess)
-      e = trace ? launch_readout_fold_trace(s, params[h->rslot], C, O, F(h->off_mc), n1, n2,
+      e = trace ? launch_readout_fold_trace(s, params[h->rslot], C, O, F(h->off_mc), n1, m2,
                                             1.f / ((float)D * (float)D), theta)
-                : launch_readout_fold(s, params[h->rslot], C, O, F(h->off_mc), n1, n2, 1.f / ((float)D * (float)D),
+                : launch_readout_fold(s, params[h->rslot], C, O, F(h->off_mc), n1, m2, 1.f / ((float)D * (float)D),
                                       theta);
     prof_end(P, s, KC_GRAM);
     if (e != hipSuccess) return hip_fail(h, e, "last convolution's summand");

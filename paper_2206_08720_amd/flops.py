@@ -124,14 +124,14 @@ def _conv_orders(sp, O, n1, n2, output, batch, M, Oe, Oc, gpairs, order):
     folded, as the library decides: _inside_out per layer; the fold (the last convolution's
     cotangent is the readout's through the global pool, so its weight-space columns factor into
     Wr[o, c] times O-free per-channel rows and its summand into per-channel Grams) for a last 3x3
-    or pointwise convolution, the full O x O output or its trace (O >= 2) on the full batch, with other
+    or pointwise convolution, the full O x O output or its trace (O >= 2), on the full batch or its
+    diagonal, with other
     weight-space columns in the contraction (a bias, a depthwise or scale layer, an outside-in
     convolution); with order "auto" the last convolution then goes outside-in when the fold's
     M D F Cin Cout + N1 N2 (F Cin Cout + O^2 Cout) is below its inside-out cost."""
     trace = output == "trace"
     io = [_inside_out(k, D, cin, cout, M, Oe, Oc, gpairs, order, trace) for (k, cin, cout, D, bias) in sp]
-    if not sp or O < 2 or output not in ("full", "trace") or batch != "full" or \
-            sp[-1][0] not in ("conv3x3", "conv1x1"):
+    if not sp or O < 2 or output not in ("full", "trace") or sp[-1][0] not in ("conv3x3", "conv1x1"):
         return io, False
     others = bool(sp[-1][4]) or any(b or k in ("dwconv3x3", "scale") or (k in ("conv3x3", "conv1x1") and not io[i])
                                     for i, (k, ci, co, D, b) in enumerate(sp[:-1]))
@@ -140,7 +140,7 @@ def _conv_orders(sp, O, n1, n2, output, batch, M, Oe, Oc, gpairs, order):
     k, cin, cout, D, bias = sp[-1]
     if io[-1] and order == "auto":
         F = 9 if k == "conv3x3" else 1
-        folded = M * D * F * cin * cout + n1 * n2 * (F * cin * cout + O * O * cout)
+        folded = M * D * F * cin * cout + gpairs * (F * cin * cout + O * O * cout)
         if folded < inside_out_cost(gpairs, D, cin, cout, Oe, trace):
             io[-1] = False
     return io, not io[-1]
@@ -190,9 +190,9 @@ def cnn_flops(spec, n1, n2, symmetric=False, order="outside_in", output="full", 
                 # of O), the per-channel Grams of every input pair, and the O x O sums over C
                 wg += 2.0 * M * cout * (F * cin) * D
                 if output == "trace":   # weights sum_o Wr[o, c]^2, then one weighted sum per pair
-                    fold_gram = 2.0 * n1 * n2 * cout * F * cin + 2.0 * O * cout + 2.0 * n1 * n2 * cout
+                    fold_gram = 2.0 * gpairs * cout * F * cin + 2.0 * O * cout + 2.0 * gpairs * cout
                 else:
-                    fold_gram = 2.0 * n1 * n2 * cout * F * cin + 3.0 * n1 * n2 * O * O * cout
+                    fold_gram = 2.0 * gpairs * cout * F * cin + 3.0 * gpairs * O * O * cout
             elif not inside[i]:
                 wg += 2.0 * M * (Oe * cout) * (F * cin) * D
                 cols += F * cin * cout

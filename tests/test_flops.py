@@ -110,6 +110,11 @@ def test_variant_counts():
     assert ctu["wgrad"] - ct["wgrad"] == 2 * M * (O - 1) * cout * F * cin * D
     assert ct["gram"] - ctu["gram"] == 2 * N * N * cout * F * cin + 2 * O * cout + 2 * N * N * cout
     assert ctu["contraction"] - ct["contraction"] == 2 * N * N * O * F * cin * cout
+    # and on the batch diagonal: the per-channel Grams of the N pairs (n, n) only
+    cd = cnn_flops(cs, N, N, batch="diagonal")
+    cdu = cnn_flops(cs, N, N, batch="diagonal", fold=False)
+    assert cdu["wgrad"] - cd["wgrad"] == 2 * M * (O - 1) * cout * F * cin * D
+    assert cd["gram"] - cdu["gram"] == 2 * N * cout * F * cin + 3 * N * O * O * cout
 
 
 def test_jacobian_contraction_count_is_the_papers_n2_o2_p():

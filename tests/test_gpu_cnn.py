@@ -110,32 +110,36 @@ FOLD_CASES = [
 ]
 
 
-@pytest.mark.parametrize("output", ["full", "trace"])
+@pytest.mark.parametrize("variant", [("full", "full"), ("trace", "full"), ("full", "diagonal"),
+                                     ("trace", "diagonal")], ids=lambda v: f"{v[0]}-{v[1]}")
 @pytest.mark.parametrize("symmetric", [True, False])
 @pytest.mark.parametrize("case", FOLD_CASES, ids=[c[0] for c in FOLD_CASES])
-def test_folded_last_convolution(case, symmetric, output):
+def test_folded_last_convolution(case, symmetric, variant):
     """The last convolution's O outputs factor out of its weight-space product: A[n, c, k] from
     act'(z) alone, Theta += sum_c Wr[o1, c] Wr[o2, c] (A1 A2^T)_c / D^2 (the trace: weights
-    sum_o Wr[o, c]^2).  Parity against the oracle, forced outside-in, with X2 = X1 on the
-    symmetric schedule and distinct batches otherwise; the fold's Grams are a second launch of
-    the Gram class."""
+    sum_o Wr[o, c]^2; the batch diagonal: the Grams' diagonals).  Parity against the oracle,
+    forced outside-in, with X2 = X1 on the symmetric schedule and distinct batches otherwise; the
+    fold's Grams are a second launch of the Gram class."""
     from paper_2206_08720_amd import _lib
     from tests.gpu_helpers import scaled_errors, variant_of, variant_scale
     label, spec, n1, n2, folded = case
+    output, batch = variant
+    if batch == "diagonal":
+        n2 = n1
     params = wl.make_params(spec, 600 + n1, "2/fan_in")
     X1 = wl.make_inputs(spec, n1, 610 + n1)
     X2 = X1 if symmetric else wl.make_inputs(spec, n2, 620 + n2)
     prof = {}
     got = gpu_ntk(spec, params, X1, X2, symmetric=symmetric,
                   options={_lib.NTK_OPT_CONV_ORDER: _lib.NTK_CONV_ORDER_OUTSIDE_IN}, profile=prof,
-                  variant=(output, "full", 0))
+                  variant=(output, batch, 0))
     ref, d1, d2 = oracle.ntk_jc_with_norms(spec, params, X1, X2, layer_storage=S)
-    if output == "full":
+    if variant == ("full", "full"):
         cs, nw = errors(got, ref, d1, d2)
     else:
-        ref = variant_of(ref, output, "full", 0)
-        cs, nw = scaled_errors(got, ref, variant_scale(d1, d2, output, "full", 0))
-    report(f"fold {label} {output} sym={symmetric}", cs, nw)
+        ref = variant_of(ref, output, batch, 0)
+        cs, nw = scaled_errors(got, ref, variant_scale(d1, d2, output, batch, 0))
+    report(f"fold {label} {output}/{batch} sym={symmetric}", cs, nw)
     assert got.shape == ref.shape and cs <= TOL and nw <= TOL
     assert prof["gram"][1] == (2 if folded else 1)
 
